@@ -1,0 +1,209 @@
+"""Throughput of the LPP-SGD per-node step on one MI355X.
+
+Workload (the headline configuration): ResNet-20 (CIFAR shapes, 10 classes),
+fp32, batch 128 of synthetic N(0, 1) 3x32x32 images with uniform labels;
+P = 4 layer-block partitions, one worker per block on its own HIP stream,
+K = 1 replica, momentum 0.9, lr 0.1, asynchronous (Hogwild) mode.  A step is
+one worker iteration of Alg. 1: counter read&inc, snapshot, full forward,
+backward truncated at the worker's block, lock-free block update.  Workers
+are issued round-robin.  samples/s = 128 * steps / wall time of the timed
+region (inputs resident in HBM before it starts).
+
+Also reported, on the same JSON line:
+  roofline      the dominant kernel family's algorithmic flops per launch
+                over its average launch time, timed with HIP events on its
+                own streams during the timed region, against the fp32
+                matrix peak;
+  cpu_baseline  the fp64 oracle's step timed on the host cores on a bounded
+                sample (a baseline, not a target);
+  hbm_kernels   the block-update and replica-averaging kernels on 1 GiB-
+                scale buffers, as achieved HBM GB/s.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "train samples/sec (fwd+partial bwd+update), ResNet-20 b128; MFMA util, HBM GB/s"
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+FAMILIES = ["conv_fwd", "conv_dgrad", "conv_wgrad", "wgrad_reduce", "bn_stats", "bn_apply", "bn_bwd", "relu",
+            "add", "gap", "linear", "softmax_ce", "snapshot", "image", "sgd_update"]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--batch", type=int, default=128)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-hbm", action="store_true")
+    ap.add_argument("--cpu-steps", type=int, default=2)
+    return ap.parse_args()
+
+
+def hbm_kernels(torch, lpp):
+    """Block update (20 B/param with momentum) and 2-replica averaging
+    (16 B/param) on 64M-float (256 MiB) arrays: far beyond the 256 MB
+    last-level cache per pass."""
+    n = 64 << 20
+    out = {}
+    x, m, g = (torch.randn(n, device="cuda") for _ in range(3))
+    for _ in range(3):
+        lpp.kernel_sgd_update(x, m, g, 1e-3, 0.9, 0.0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    e0.record()
+    for _ in range(reps):
+        lpp.kernel_sgd_update(x, m, g, 1e-3, 0.9, 0.0)
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / reps / 1e3
+    gbs = 20.0 * n / t / 1e9
+    out["sgd_update"] = {"GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 3), "bytes_per_param": 20,
+                         "params": n}
+    del m
+    y = torch.randn(n, device="cuda")
+    for _ in range(3):
+        lpp.kernel_average([x, y])
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        lpp.kernel_average([x, y])
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / reps / 1e3
+    gbs = 16.0 * n / t / 1e9
+    out["average_k2"] = {"GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 3), "bytes_per_param": 16,
+                         "params": n}
+    del x, y, g
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline(steps, batch):
+    """The oracle (fp64 C, OpenMP) on `steps` ResNet-20 worker steps at the
+    same batch, partitions cycling over the four blocks."""
+    import synth
+    from oracle import lppref as R
+    from oracle import models as OM
+    o = OM.resnet20_p4()
+    x = synth.init_params(o.specs, 1).astype(np.float64)
+    m = np.zeros(o.d)
+    img = synth.images(7, batch, 3, 32, 32)
+    lab = synth.labels(7, batch, 10)
+    R.step(o, x, m, img[:2], lab[:2], 4, 0.0, 0.9)   # load and warm the library
+    t0 = time.perf_counter()
+    for s in range(steps):
+        R.step(o, x, m, img, lab, s % 4 + 1, 0.1, 0.9)
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": round(batch * steps / dt, 2), "unit": "samples/s", "cores": threads, "kind": "oracle",
+            "sample": "%d ResNet-20 worker steps (fwd + full bwd restricted to the block + update), batch %d, "
+                      "fp64, %.1f s" % (steps, batch, dt)}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print("bench.py measures one GPU only: this build runs the per-node step on a single MI355X "
+              "(--gpus %d is not supported)" % a.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import synth
+    from paper_2203_06638_amd import lpp
+    from paper_2203_06638_amd import models as PM
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.init()
+    B, P, K = a.batch, 4, 1
+    model = PM.resnet20(10)
+    info = lpp.describe(model, B)
+    x0 = synth.init_params(model.specs, 1)
+    pool = []
+    for b in range(8):
+        img = torch.from_numpy(synth.images(100 + b, B, 3, 32, 32)).cuda()
+        lab = torch.from_numpy(synth.labels(100 + b, B, 10)).cuda()
+        pool.append((img, lab))
+    streams = [torch.cuda.Stream() for _ in range(K * P)]
+    ctx = lpp.Context(model, K=K, batch=B, mode=lpp.ASYNC, momentum=0.9, streams=streams)
+    ctx.set_params(x0)
+
+    def run(n, start):
+        for s in range(start, start + n):
+            w = s % (K * P)
+            img, lab = pool[(s // (K * P)) % len(pool)]
+            ctx.step(w, img, lab, w % P + 1, 0.1)
+
+    run(a.warmup, 0)
+    ctx.sync()
+    # find the dominant kernel family on a short untimed pass
+    fam_time = {}
+    probe = 4 * P
+    for f in FAMILIES:
+        ctx.timer_enable(f)
+        run(probe, a.warmup)
+        ms, n, work = ctx.timer_read()
+        fam_time[f] = ms
+    ctx.timer_enable(None)
+    dom = max(fam_time, key=fam_time.get)
+    # timed region, with the dominant family bracketed by HIP events
+    ctx.timer_enable(dom)
+    ctx.sync()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(a.steps, a.warmup + probe * len(FAMILIES))
+    ctx.sync()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms, launches, work = ctx.timer_read()
+    ctx.timer_enable(None)
+    losses = [ctx.get_loss(w) for w in range(K * P)]
+    ctx.close()
+
+    value = B * a.steps / dt
+    achieved = (work / launches) / (ms / launches / 1e3) / 1e12 if launches else 0.0
+    mean_flops = info.fwd_flops + sum(info.bwd_flops[i] for i in range(1, P + 1)) / P
+    res = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(dt / a.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "ResNet-20 (10 classes), batch %d, fp32, P=4 partial-backprop workers on 4 HIP "
+                               "streams, K=1, momentum 0.9, async" % B,
+                   "global_batch": B, "partitions": P, "replicas": K,
+                   "mean_step_gflop": round(mean_flops / 1e9, 3),
+                   "model_tflops": round(mean_flops * a.steps / dt / 1e12, 2)},
+        "roofline": {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4),
+                     "traffic": None, "launches": launches, "avg_launch_us": round(ms / launches * 1e3, 2),
+                     "family_ms_probe": {k: round(v, 3) for k, v in sorted(fam_time.items(), key=lambda t: -t[1])}},
+        "final_losses": [round(l, 4) for l in losses],
+    }
+    if not a.no_hbm:
+        res["hbm_kernels"] = hbm_kernels(torch, lpp)
+    if not a.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(a.cpu_steps, B)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

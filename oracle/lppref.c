@@ -276,6 +276,57 @@ static void maxpool_bwd(const double* X, shp a, int N, int R, int st, int pad,
 
 /* ------------------------------ the model ------------------------------- */
 
+/* ---------------- condition scales of the parameter gradients ----------------
+ * For every parameter gradient, which is a sum of products, the sum of the
+ * magnitudes of those products.  A sum of terms each known to relative
+ * accuracy delta can only be computed to about delta times this scale, so
+ * it is the right yardstick for a gradient entry whose terms cancel. */
+static void conv_wscale(const double* X, shp a, int N, int K, int R, int st, int pad,
+                        const double* dY, shp o, double* sW, double* sb) {
+    #pragma omp parallel for collapse(2) schedule(static)
+    for (int k = 0; k < K; ++k)
+        for (int c = 0; c < a.c; ++c)
+            for (int r = 0; r < R; ++r)
+                for (int s = 0; s < R; ++s) {
+                    double acc = 0.0;
+                    for (int n = 0; n < N; ++n)
+                        for (int p = 0; p < o.h; ++p) {
+                            int hi = p * st - pad + r;
+                            if (hi < 0 || hi >= a.h) continue;
+                            for (int q = 0; q < o.w; ++q) {
+                                int wi = q * st - pad + s;
+                                if (wi < 0 || wi >= a.w) continue;
+                                acc += fabs(dY[(((long)n * K + k) * o.h + p) * o.w + q] *
+                                            X[(((long)n * a.c + c) * a.h + hi) * a.w + wi]);
+                            }
+                        }
+                    sW[((long)(k * a.c + c) * R + r) * R + s] = acc;
+                }
+    if (sb)
+        for (int k = 0; k < K; ++k) {
+            double acc = 0.0;
+            for (int n = 0; n < N; ++n)
+                for (long e = 0; e < (long)o.h * o.w; ++e) acc += fabs(dY[((long)n * K + k) * o.h * o.w + e]);
+            sb[k] = acc;
+        }
+}
+
+static void bn_scale(const double* X, shp a, int N, const double* mean, const double* rstd,
+                     const double* dY, double* sg, double* sb) {
+    long hw = (long)a.h * a.w;
+    for (int c = 0; c < a.c; ++c) {
+        double s1 = 0.0, s2 = 0.0;
+        for (int n = 0; n < N; ++n)
+            for (long e = 0; e < hw; ++e) {
+                long i = ((long)n * a.c + c) * hw + e;
+                s1 += fabs(dY[i]);
+                s2 += fabs(dY[i] * (X[i] - mean[c]) * rstd[c]);
+            }
+        sg[c] = s2;
+        sb[c] = s1;
+    }
+}
+
 /* Runs the forward pass, filling act[l] (and BN statistics) for every layer. */
 static void run_forward(const ref_layer* L, int nl, int N, shp img, const shp* S, const double* x,
                         const double* images, double bn_eps, double** act, double** bmean, double** brstd) {
@@ -340,9 +391,10 @@ static void run_forward(const ref_layer* L, int nl, int N, shp img, const shp* S
  *   grad    : d doubles out (may be NULL: forward only)
  * The last layer's output is the logits.  Returns 0, or -1 on a bad model.
  */
-int ref_forward_backward(const ref_layer* L, int nl, int N, int C, int H, int W,
-                         const double* x, const double* images, const int* labels,
-                         double bn_eps, double* logits, double* loss, double* grad) {
+static int forward_backward_impl(const ref_layer* L, int nl, int N, int C, int H, int W,
+                                 const double* x, const double* images, const int* labels,
+                                 double bn_eps, double* logits, double* loss, double* grad,
+                                 int gl, double* gout, double* gscale) {
     shp img = { C, H, W };
     shp* S = (shp*)calloc((size_t)nl, sizeof(shp));
     if (!S || infer_shapes(L, nl, img, S)) { free(S); return -1; }
@@ -395,11 +447,15 @@ int ref_forward_backward(const ref_layer* L, int nl, int N, int C, int H, int W,
                 double* dW = grad + y->poff;
                 double* db = y->bias ? dW + (long)y->cout * y->cin * y->k * y->k : NULL;
                 conv_bwd(X0, a, N, Wt, y->cout, y->k, y->stride, y->pad, dY, S[l], dX0, dW, db);
+                if (gscale)
+                    conv_wscale(X0, a, N, y->cout, y->k, y->stride, y->pad, dY, S[l], gscale + y->poff,
+                                y->bias ? gscale + y->poff + (long)y->cout * y->cin * y->k * y->k : NULL);
                 break;
             }
             case R_BN:
                 bn_bwd(X0, a, N, x + y->poff, bmean[l], brstd[l], dY, dX0,
                        grad + y->poff, grad + y->poff + y->cout);
+                if (gscale) bn_scale(X0, a, N, bmean[l], brstd[l], dY, gscale + y->poff, gscale + y->poff + y->cout);
                 break;
             case R_RELU:
                 if (dX0) for (long i = 0; i < n0; ++i) dX0[i] += X0[i] > 0.0 ? dY[i] : 0.0;
@@ -442,15 +498,57 @@ int ref_forward_backward(const ref_layer* L, int nl, int N, int C, int H, int W,
                             for (int o = 0; o < y->cout; ++o) acc += dY[(long)n * y->cout + o] * Wt[(long)o * y->cin + i];
                             dX0[(long)n * y->cin + i] += acc;
                         }
+                if (gscale)
+                    for (int o = 0; o < y->cout; ++o) {
+                        for (int i = 0; i < y->cin; ++i) {
+                            double acc = 0.0;
+                            for (int n = 0; n < N; ++n) acc += fabs(dY[(long)n * y->cout + o] * X0[(long)n * y->cin + i]);
+                            gscale[y->poff + (long)o * y->cin + i] = acc;
+                        }
+                        if (y->bias) {
+                            double acc = 0.0;
+                            for (int n = 0; n < N; ++n) acc += fabs(dY[(long)n * y->cout + o]);
+                            gscale[y->poff + (long)y->cout * y->cin + o] = acc;
+                        }
+                    }
                 break;
             }
             }
         }
+        if (gout && gl >= 0 && gl < nl) memcpy(gout, dact[gl], sizeof(double) * (size_t)numel(S[gl], N));
         for (int l = 0; l < nl; ++l) free(dact[l]);
     }
     for (int l = 0; l < nl; ++l) { free(act[l]); free(bmean[l]); free(brstd[l]); }
     free(act); free(dact); free(bmean); free(brstd); free(S); free(dZ);
     return 0;
+}
+
+int ref_forward_backward(const ref_layer* L, int nl, int N, int C, int H, int W,
+                         const double* x, const double* images, const int* labels,
+                         double bn_eps, double* logits, double* loss, double* grad) {
+    return forward_backward_impl(L, nl, N, C, H, W, x, images, labels, bn_eps, logits, loss, grad, -1, NULL, NULL);
+}
+
+/* Condition scale of every parameter gradient (see conv_wscale), d doubles;
+ * the gradient itself goes to grad. */
+int ref_grad_scale(const ref_layer* L, int nl, int N, int C, int H, int W,
+                   const double* x, const double* images, const int* labels,
+                   double bn_eps, double* grad, double* scale) {
+    double loss;
+    return forward_backward_impl(L, nl, N, C, H, W, x, images, labels, bn_eps, NULL, &loss, grad, -1, NULL, scale);
+}
+
+/* Gradient of the loss with respect to the output of layer `layer` (NCHW),
+ * from the full backward pass. */
+int ref_activation_grad(const ref_layer* L, int nl, int N, int C, int H, int W,
+                        const double* x, const double* images, const int* labels,
+                        double bn_eps, int layer, double* out) {
+    long d = ref_num_params(L, nl);
+    double* g = (double*)malloc(sizeof(double) * (size_t)(d > 0 ? d : 1));
+    double loss;
+    int rc = forward_backward_impl(L, nl, N, C, H, W, x, images, labels, bn_eps, NULL, &loss, g, layer, out, NULL);
+    free(g);
+    return rc;
 }
 
 /* Shapes of every layer output (c,h,w triples), for the tests. */
@@ -541,6 +639,66 @@ int ref_activation(const ref_layer* L, int nl, int N, int C, int H, int W, const
     }
     run_forward(L, nl, N, img, S, x, images, bn_eps, act, bmean, brstd);
     memcpy(out, act[layer], sizeof(double) * (size_t)numel(S[layer], N));
+    for (int l = 0; l < nl; ++l) { free(act[l]); free(bmean[l]); free(brstd[l]); }
+    free(act); free(bmean); free(brstd); free(S);
+    return 0;
+}
+
+/*
+ * How far the forward pass at x stays from the method's non-smooth points:
+ * the smallest |input| / max|input| over the inputs of every ReLU (per
+ * layer), and the smallest (largest - second largest) / max|input| over the
+ * windows of every max pool.  A gradient comparison between two precisions
+ * is well posed only when this exceeds the precisions' disagreement on
+ * those inputs; otherwise both mask / argmax decisions are valid.
+ */
+int ref_kink_margin(const ref_layer* L, int nl, int N, int C, int H, int W, const double* x,
+                    const double* images, double bn_eps, double* margin) {
+    shp img = { C, H, W };
+    shp* S = (shp*)calloc((size_t)nl, sizeof(shp));
+    if (!S || infer_shapes(L, nl, img, S)) { free(S); return -1; }
+    double** act = (double**)calloc((size_t)nl, sizeof(double*));
+    double** bmean = (double**)calloc((size_t)nl, sizeof(double*));
+    double** brstd = (double**)calloc((size_t)nl, sizeof(double*));
+    for (int l = 0; l < nl; ++l) {
+        act[l] = (double*)calloc((size_t)numel(S[l], N), sizeof(double));
+        if (L[l].op == R_BN) {
+            bmean[l] = (double*)calloc((size_t)S[l].c, sizeof(double));
+            brstd[l] = (double*)calloc((size_t)S[l].c, sizeof(double));
+        }
+    }
+    run_forward(L, nl, N, img, S, x, images, bn_eps, act, bmean, brstd);
+    double best = INFINITY;
+    for (int l = 0; l < nl; ++l) {
+        if (L[l].op != R_RELU && L[l].op != R_MAXPOOL) continue;
+        shp a = in_shape(S, L[l].in0, img);
+        const double* X = L[l].in0 < 0 ? images : act[L[l].in0];
+        long n = numel(a, N);
+        double mx = 0.0;
+        for (long i = 0; i < n; ++i) if (fabs(X[i]) > mx) mx = fabs(X[i]);
+        if (mx == 0.0) continue;
+        if (L[l].op == R_RELU) {
+            for (long i = 0; i < n; ++i) if (fabs(X[i]) / mx < best) best = fabs(X[i]) / mx;
+        } else {
+            shp o = S[l];
+            int R = L[l].k, st = L[l].stride, pad = L[l].pad;
+            for (int b = 0; b < N; ++b)
+                for (int c = 0; c < a.c; ++c)
+                    for (int p = 0; p < o.h; ++p)
+                        for (int q = 0; q < o.w; ++q) {
+                            double t1 = -INFINITY, t2 = -INFINITY;
+                            for (int r = 0; r < R; ++r)
+                                for (int s2 = 0; s2 < R; ++s2) {
+                                    int hi = p * st - pad + r, wi = q * st - pad + s2;
+                                    if (hi < 0 || hi >= a.h || wi < 0 || wi >= a.w) continue;
+                                    double v = X[(((long)b * a.c + c) * a.h + hi) * a.w + wi];
+                                    if (v > t1) { t2 = t1; t1 = v; } else if (v > t2) t2 = v;
+                                }
+                            if (t2 > -INFINITY && (t1 - t2) / mx < best) best = (t1 - t2) / mx;
+                        }
+        }
+    }
+    *margin = best;
     for (int l = 0; l < nl; ++l) { free(act[l]); free(bmean[l]); free(brstd[l]); }
     free(act); free(bmean); free(brstd); free(S);
     return 0;

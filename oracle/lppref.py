@@ -52,6 +52,12 @@ def lib():
         L.ref_step.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
                                dp, dp, dp, C.POINTER(C.c_int), C.c_long, C.c_long, C.c_double, C.c_double,
                                C.c_double, C.c_double, dp, dp, dp]
+        L.ref_activation_grad.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                          dp, dp, C.POINTER(C.c_int), C.c_double, C.c_int, dp]
+        L.ref_grad_scale.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                     dp, dp, C.POINTER(C.c_int), C.c_double, dp, dp]
+        L.ref_kink_margin.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                      dp, dp, C.c_double, dp]
         L.ref_activation.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
                                      dp, dp, C.c_double, C.c_int, dp]
         _LIB = L
@@ -112,6 +118,51 @@ def activation(net, x, images, layer):
     if rc:
         raise ValueError("inconsistent model")
     return out
+
+
+def activation_grad(net, x, images, labels, layer):
+    """Gradient of the loss w.r.t. the output of layer `layer` (fp64 NCHW)."""
+    x = np.ascontiguousarray(x, np.float64)
+    img = np.ascontiguousarray(images, np.float64)
+    lab = np.ascontiguousarray(labels, np.int32)
+    n = img.shape[0]
+    c, h, w = shapes(net)[layer]
+    out = np.zeros((n, c, h, w), np.float64)
+    rc = lib().ref_activation_grad(_layers(net), len(net.layers), n, *net.in_shape, _dp(x), _dp(img),
+                                   lab.ctypes.data_as(C.POINTER(C.c_int)), BN_EPS, layer, _dp(out))
+    if rc:
+        raise ValueError("inconsistent model")
+    return out
+
+
+def grad_scale(net, x, images, labels):
+    """(gradient, condition scale): for every parameter, the full gradient
+    and the sum of the magnitudes of the products it sums (fp64)."""
+    x = np.ascontiguousarray(x, np.float64)
+    img = np.ascontiguousarray(images, np.float64)
+    lab = np.ascontiguousarray(labels, np.int32)
+    g = np.zeros(net.d, np.float64)
+    sc = np.zeros(net.d, np.float64)
+    rc = lib().ref_grad_scale(_layers(net), len(net.layers), img.shape[0], *net.in_shape, _dp(x), _dp(img),
+                              lab.ctypes.data_as(C.POINTER(C.c_int)), BN_EPS, _dp(g), _dp(sc))
+    if rc:
+        raise ValueError("inconsistent model")
+    return g, sc
+
+
+def kink_margin(net, x, images):
+    """Smallest distance (relative to the layer's largest input) of any ReLU
+    input from 0, or of any max-pool window's runner-up from its maximum.
+    Gradients of two evaluations in different precisions agree only when
+    this exceeds their disagreement on those inputs."""
+    x = np.ascontiguousarray(x, np.float64)
+    img = np.ascontiguousarray(images, np.float64)
+    out = np.zeros(1, np.float64)
+    rc = lib().ref_kink_margin(_layers(net), len(net.layers), img.shape[0], *net.in_shape, _dp(x), _dp(img),
+                               BN_EPS, _dp(out))
+    if rc:
+        raise ValueError("inconsistent model")
+    return float(out[0])
 
 
 def block_update(x, m, g, lo, hi, lr, mu=0.0, wd=0.0):

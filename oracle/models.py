@@ -150,11 +150,12 @@ def tiny(n_classes=10, hw=32):
     return net.set_blocks([1, 2])
 
 
-def _basic_unit(net, x, cin, cout, stride):
+def _basic_unit(net, x, cin, cout, stride, relu=True):
     net.next_unit()
     h = net.conv(x, cin, cout, 3, stride, 1)
     h = net.bn(h, cout)
-    h = net.relu(h)
+    if relu:
+        h = net.relu(h)
     h = net.conv(h, cout, cout, 3, 1, 1)
     h = net.bn(h, cout)
     if stride != 1 or cin != cout:
@@ -163,22 +164,25 @@ def _basic_unit(net, x, cin, cout, stride):
     else:
         s = x
     h = net.add(h, s)
-    return net.relu(h)
+    return net.relu(h) if relu else h
 
 
-def resnet_cifar(n_per_stage=3, widths=(16, 32, 64), n_classes=10, hw=32):
+def resnet_cifar(n_per_stage=3, widths=(16, 32, 64), n_classes=10, hw=32, relu=True):
     """CIFAR ResNet with post-activation basic units and projection (1x1
     conv + BN) shortcuts.  Units: 0 = stem, 1..3n = residual units,
-    3n+1 = head."""
+    3n+1 = head.  relu=False drops every ReLU (a piecewise-smooth-free twin
+    with the same convolutions, used to compare gradients across
+    precisions)."""
     net = Net("resnet%d" % (6 * n_per_stage + 2), 3, hw, hw, n_classes)
     x = net.conv(-1, 3, widths[0], 3, 1, 1)
     x = net.bn(x, widths[0])
-    x = net.relu(x)
+    if relu:
+        x = net.relu(x)
     cin = widths[0]
     for si, w in enumerate(widths):
         for b in range(n_per_stage):
             stride = 2 if (si > 0 and b == 0) else 1
-            x = _basic_unit(net, x, cin, w, stride)
+            x = _basic_unit(net, x, cin, w, stride, relu)
             cin = w
     net.next_unit()
     x = net.gap(x)
@@ -246,10 +250,10 @@ def tiny_p2():
     return tiny()
 
 
-def resnet20_p4(n_classes=10):
+def resnet20_p4(n_classes=10, relu=True):
     # units: stem, s1u1..s1u3, s2u1..s2u3, s3u1..s3u3, head
     # blocks: {stem,s1u1,s1u2} {s1u3,s2u1} {s2u2,s2u3,s3u1} {s3u2,s3u3,head}
-    return resnet_cifar(3, (16, 32, 64), n_classes).set_blocks([1, 1, 1, 2, 2, 3, 3, 3, 4, 4, 4])
+    return resnet_cifar(3, (16, 32, 64), n_classes, relu=relu).set_blocks([1, 1, 1, 2, 2, 3, 3, 3, 4, 4, 4])
 
 
 def wrn16_8_p4(n_classes=100):

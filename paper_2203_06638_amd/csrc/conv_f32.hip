@@ -1,0 +1,373 @@
+// conv_f32.hip -- fp32 convolution passes on gfx950 matrix cores.
+//
+// Forward and data-gradient passes are one implicit GEMM
+//     Y[m][n] = sum_k A[m][k] * B[n][k]
+// with m an output pixel (NHWC), n an output channel, and k = (r, s, c) a
+// filter tap and source channel.  A is gathered on the fly from the NHWC
+// source activation; B is a weight matrix whose rows are contiguous in k
+// (the snapshot writes both the forward layout W_f[cout][r][s][cin] and the
+// data-gradient layout W_d[cin][r][s][cout]).
+//
+// Matrix-core mapping (v_mfma_f32_16x16x4_f32, 64 lanes): lane l supplies
+// A[row = l%16][k = l/16] and B[k = l/16][col = l%16] and holds
+// D[4*(l/16) + i][l%16], i = 0..3.  Each lane loads a float4 of four
+// consecutive channels for its row (pixel) and its column (filter row); the
+// four components feed four successive MFMAs, so the 16 k-values a lane
+// group covers per float4 are permuted identically in A and B (the sum is
+// over all of them either way).
+//
+// Weight gradient: dW[cout][(r,s,c)] = sum over output pixels p of
+// dY[p][cout] * X_im2col[p][(r,s,c)] -- a GEMM whose reduction runs over
+// N*Ho*Wo pixels.  Pixel chunks of 64 are staged through LDS (dY rows and
+// im2col rows as loaded, float4 along channels); each wave reduces 16 of the
+// chunk's pixels; waves are summed in a fixed order and every split of the
+// pixel range writes its own partial, summed in order by a second kernel.
+// No atomics anywhere: results are bitwise reproducible.
+#include "kernels.h"
+
+namespace lpp {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 mfma16x16x4(float a, float b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Offset of source pixel (n, hs, ws) feeding output pixel (n, p, q) through
+// tap (r, s), or -1 when the tap falls in the zero padding / between strides.
+template <int MODE>
+__device__ __forceinline__ int src_pixel(int n, int p, int q, int r, int s, const ConvGeom& g) {
+    int hs, ws;
+    if (MODE == CONV_FWD) {
+        hs = p * g.stride - g.pad + r;
+        ws = q * g.stride - g.pad + s;
+    } else {
+        // dX[p][q] gathers dY[(p + pad - r)/stride][(q + pad - s)/stride]
+        int hn = p + g.pad - r, wn = q + g.pad - s;
+        if (hn < 0 || wn < 0) return -1;
+        if (g.stride != 1) {
+            if ((hn % g.stride) | (wn % g.stride)) return -1;
+            hn /= g.stride;
+            wn /= g.stride;
+        }
+        hs = hn;
+        ws = wn;
+    }
+    if (hs < 0 || hs >= g.Hs || ws < 0 || ws >= g.Ws) return -1;
+    return ((n * g.Hs + hs) * g.Ws + ws) * g.Cs;
+}
+
+// WM waves along m (4/WM along n); each wave owns TM x TN tiles of 16x16.
+// FAST: Cs % 16 == 0, so a group of four float4 chunks never straddles a tap.
+template <int MODE, int WM, int TM, int TN, bool FAST>
+__global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ src, const float* __restrict__ B,
+                                                      const float* __restrict__ bias, float* __restrict__ Y,
+                                                      ConvGeom g, int accumulate) {
+    constexpr int WN = 4 / WM;
+    constexpr int BM = WM * TM * 16, BN = WN * TN * 16;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave % WM, wn = wave / WM;
+    const int gi = lane >> 4, li = lane & 15;
+    const int HoWo = g.Ho * g.Wo;
+    const int M = g.Nb * HoWo;
+    const int Ktot = g.R * g.S * g.Cs;
+    const int m_base = blockIdx.x * BM + wm * TM * 16;
+    const int n_base = blockIdx.y * BN + wn * TN * 16;
+
+    int an[TM], ap[TM], aq[TM];
+    bool av[TM];
+#pragma unroll
+    for (int t = 0; t < TM; ++t) {
+        int m = m_base + t * 16 + li;
+        av[t] = m < M;
+        int mm = av[t] ? m : 0;
+        an[t] = mm / HoWo;
+        int rem = mm - an[t] * HoWo;
+        ap[t] = rem / g.Wo;
+        aq[t] = rem - ap[t] * g.Wo;
+    }
+    const float* bp[TN];
+    bool bv[TN];
+#pragma unroll
+    for (int t = 0; t < TN; ++t) {
+        int n = n_base + t * 16 + li;
+        bv[t] = n < g.Ncols;
+        bp[t] = B + (long)(bv[t] ? n : 0) * Ktot;
+    }
+    f4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    if (FAST) {
+        for (int r = 0; r < g.R; ++r)
+            for (int s = 0; s < g.S; ++s) {
+                int so[TM];
+#pragma unroll
+                for (int t = 0; t < TM; ++t) so[t] = av[t] ? src_pixel<MODE>(an[t], ap[t], aq[t], r, s, g) : -1;
+                const int kt = (r * g.S + s) * g.Cs;
+                for (int c0 = 4 * gi; c0 < g.Cs; c0 += 16) {
+                    f4 a[TM], b[TN];
+#pragma unroll
+                    for (int t = 0; t < TM; ++t)
+                        a[t] = so[t] >= 0 ? *(const f4*)(src + so[t] + c0) : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int t = 0; t < TN; ++t)
+                        b[t] = bv[t] ? *(const f4*)(bp[t] + kt + c0) : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+#pragma unroll
+                        for (int x = 0; x < TM; ++x)
+#pragma unroll
+                            for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(a[x][j], b[y][j], acc[x][y]);
+                }
+            }
+    } else {
+        const int Cq = g.Cs >> 2;   // float4 chunks per tap
+        const int KC = Ktot >> 2;   // float4 chunks in all of k
+        for (int kc0 = 0; kc0 < KC; kc0 += 4) {
+            const int kc = kc0 + gi;
+            f4 a[TM], b[TN];
+#pragma unroll
+            for (int t = 0; t < TM; ++t) a[t] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int t = 0; t < TN; ++t) b[t] = f4{0.f, 0.f, 0.f, 0.f};
+            if (kc < KC) {
+                int tap = kc / Cq;
+                int c = (kc - tap * Cq) * 4;
+                int r = tap / g.S, s = tap - r * g.S;
+#pragma unroll
+                for (int t = 0; t < TM; ++t) {
+                    int so = av[t] ? src_pixel<MODE>(an[t], ap[t], aq[t], r, s, g) : -1;
+                    if (so >= 0) a[t] = *(const f4*)(src + so + c);
+                }
+#pragma unroll
+                for (int t = 0; t < TN; ++t)
+                    if (bv[t]) b[t] = *(const f4*)(bp[t] + kc * 4);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int x = 0; x < TM; ++x)
+#pragma unroll
+                    for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(a[x][j], b[y][j], acc[x][y]);
+        }
+    }
+
+#pragma unroll
+    for (int x = 0; x < TM; ++x)
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            const int n = n_base + y * 16 + li;
+            if (n >= g.Ncols) continue;
+            const float bb = bias ? bias[n] : 0.f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int m = m_base + x * 16 + gi * 4 + i;
+                if (m >= M) continue;
+                const long o = (long)m * g.Ncols + n;
+                float v = acc[x][y][i] + bb;
+                Y[o] = accumulate ? Y[o] + v : v;
+            }
+        }
+}
+
+template <int MODE, int WM, int TM, int TN>
+static hipError_t launch_cfg(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
+                             bool acc, hipStream_t st) {
+    constexpr int BM = WM * TM * 16, BN = (4 / WM) * TN * 16;
+    const long M = (long)g.Nb * g.Ho * g.Wo;
+    dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
+    if (g.Cs % 16 == 0)
+        hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true>), grid, dim3(256), 0, st, src, B, bias, Y, g,
+                           (int)acc);
+    else
+        hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false>), grid, dim3(256), 0, st, src, B, bias, Y, g,
+                           (int)acc);
+    return hipGetLastError();
+}
+
+template <int MODE>
+static hipError_t launch_mode(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
+                              bool acc, hipStream_t st) {
+    const long M = (long)g.Nb * g.Ho * g.Wo;
+    if (g.Ncols <= 16) return launch_cfg<MODE, 4, 2, 1>(src, B, bias, Y, g, acc, st);
+    if (g.Ncols <= 32) return launch_cfg<MODE, 4, 2, 2>(src, B, bias, Y, g, acc, st);
+    if (g.Ncols <= 64 || M < 64L * 512) {
+        if (M >= 64L * 512) return launch_cfg<MODE, 2, 2, 2>(src, B, bias, Y, g, acc, st);
+        return launch_cfg<MODE, 2, 1, 2>(src, B, bias, Y, g, acc, st);
+    }
+    return launch_cfg<MODE, 2, 2, 4>(src, B, bias, Y, g, acc, st);
+}
+
+hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
+                             const ConvGeom& g, bool accumulate, hipStream_t st) {
+    if (mode == CONV_FWD) return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, st);
+    return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, st);
+}
+
+// ------------------------------------------------------------------------
+// weight gradient
+// ------------------------------------------------------------------------
+
+struct WgArgs {
+    int Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, R, S, stride, pad, pix_per_split;
+};
+
+template <int TM, int TN>
+__global__ __launch_bounds__(256) void conv_wgrad_f32(const float* __restrict__ dY, const float* __restrict__ X,
+                                                      float* __restrict__ part, WgArgs a) {
+    constexpr int BMw = TM * 16, BNw = TN * 16;
+    __shared__ float As[64][BMw + 4];
+    __shared__ float Bs[64][BNw + 4];
+    __shared__ float red[TM * TN * 4][64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int gi = lane >> 4, li = lane & 15;
+    const int HoWo = a.Ho * a.Wo;
+    const int M = a.Nb * HoWo;
+    const int Ktot = a.R * a.S * a.Cin_p;
+    const int Cq = a.Cin_p >> 2;
+    const int m0 = blockIdx.x * BMw, n0 = blockIdx.y * BNw;
+    const int p_begin = blockIdx.z * a.pix_per_split;
+    const int p_end = min(M, p_begin + a.pix_per_split);
+
+    f4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    for (int pc = p_begin; pc < p_end; pc += 64) {
+        for (int idx = tid; idx < 64 * (BMw / 4); idx += 256) {
+            const int px = idx / (BMw / 4), cq = idx - px * (BMw / 4);
+            const int p = pc + px, co = m0 + cq * 4;
+            f4 v = f4{0.f, 0.f, 0.f, 0.f};
+            if (p < p_end && co < a.Cout) v = *(const f4*)(dY + (long)p * a.Cout + co);
+            *(f4*)&As[px][cq * 4] = v;
+        }
+        for (int idx = tid; idx < 64 * (BNw / 4); idx += 256) {
+            const int px = idx / (BNw / 4), cq = idx - px * (BNw / 4);
+            const int p = pc + px, col = n0 + cq * 4;
+            f4 v = f4{0.f, 0.f, 0.f, 0.f};
+            if (p < p_end && col < Ktot) {
+                const int quad = col >> 2;
+                const int tap = quad / Cq;
+                const int c = (quad - tap * Cq) * 4;
+                const int r = tap / a.S, s = tap - r * a.S;
+                const int n = p / HoWo;
+                const int rem = p - n * HoWo;
+                const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
+                const int hi = ho * a.stride - a.pad + r, wi = wo * a.stride - a.pad + s;
+                if (hi >= 0 && hi < a.Hi && wi >= 0 && wi < a.Wi)
+                    v = *(const f4*)(X + ((long)(n * a.Hi + hi) * a.Wi + wi) * a.Cin_p + c);
+            }
+            *(f4*)&Bs[px][cq * 4] = v;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int row = 16 * wave + 4 * j + gi;
+            float av[TM], bv[TN];
+#pragma unroll
+            for (int t = 0; t < TM; ++t) av[t] = As[row][t * 16 + li];
+#pragma unroll
+            for (int t = 0; t < TN; ++t) bv[t] = Bs[row][t * 16 + li];
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(av[x], bv[y], acc[x][y]);
+        }
+        __syncthreads();
+    }
+
+    // waves 0..3 summed in order through LDS
+    for (int w = 0; w < 4; ++w) {
+        if (wave == w) {
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int y = 0; y < TN; ++y)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        float* slot = &red[(x * TN + y) * 4 + i][lane];
+                        *slot = (w == 0) ? acc[x][y][i] : *slot + acc[x][y][i];
+                    }
+        }
+        __syncthreads();
+    }
+    if (wave == 3) {
+        float* out = part + (long)blockIdx.z * a.Cout * Ktot;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int y = 0; y < TN; ++y) {
+                const int col = n0 + y * 16 + li;
+                if (col >= Ktot) continue;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int co = m0 + x * 16 + gi * 4 + i;
+                    if (co < a.Cout) out[(long)co * Ktot + col] = red[(x * TN + y) * 4 + i][lane];
+                }
+            }
+    }
+}
+
+WgradPlan wgrad_plan(int Cout, int Ktot, long M) {
+    WgradPlan p;
+    p.tm = Cout <= 16 ? 1 : (Cout <= 32 ? 2 : 4);
+    p.tn = 4;
+    const long tiles = (long)((Cout + 16 * p.tm - 1) / (16 * p.tm)) * ((Ktot + 16 * p.tn - 1) / (16 * p.tn));
+    long splits = (1024 + tiles - 1) / tiles;
+    const long max_splits = (M + 255) / 256;
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    long pps = (M + splits - 1) / splits;
+    pps = (pps + 63) / 64 * 64;
+    p.pix_per_split = (int)pps;
+    p.splits = (int)((M + pps - 1) / pps);
+    p.part_floats = (long)p.splits * Cout * Ktot;
+    return p;
+}
+
+template <int TM, int TN>
+static hipError_t launch_wg(const float* dY, const float* X, float* part, const WgArgs& a, const WgradPlan& p,
+                            hipStream_t st) {
+    const int Ktot = a.R * a.S * a.Cin_p;
+    dim3 grid((unsigned)((a.Cout + TM * 16 - 1) / (TM * 16)), (unsigned)((Ktot + TN * 16 - 1) / (TN * 16)),
+              (unsigned)p.splits);
+    hipLaunchKernelGGL((conv_wgrad_f32<TM, TN>), grid, dim3(256), 0, st, dY, X, part, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int Nb, int Hi, int Wi, int Cin_p,
+                             int Ho, int Wo, int Cout, int R, int S, int stride, int pad, const WgradPlan& p,
+                             hipStream_t st) {
+    WgArgs a{Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, R, S, stride, pad, p.pix_per_split};
+    if (p.tm == 1) return launch_wg<1, 4>(dY, X, part, a, p, st);
+    if (p.tm == 2) return launch_wg<2, 4>(dY, X, part, a, p, st);
+    return launch_wg<4, 4>(dY, X, part, a, p, st);
+}
+
+__global__ void wgrad_reduce_kernel(const float* __restrict__ part, int splits, int Cout, int Ktot, int Cin,
+                                    int Cin_p, int R, int S, float* __restrict__ g) {
+    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (long)Cout * Ktot) return;
+    const int co = (int)(idx / Ktot), col = (int)(idx - (long)co * Ktot);
+    const int tap = col / Cin_p, c = col - tap * Cin_p;
+    if (c >= Cin) return;
+    float s = 0.f;
+    for (int k = 0; k < splits; ++k) s += part[(long)k * Cout * Ktot + idx];
+    const int r = tap / S, q = tap - r * S;
+    g[(((long)co * Cin + c) * R + r) * S + q] = s;
+}
+
+hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
+                               float* g, hipStream_t st) {
+    const long n = (long)Cout * Ktot;
+    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, splits, Cout,
+                       Ktot, Cin, Cin_p, R, S, g);
+    return hipGetLastError();
+}
+
+}  // namespace lpp

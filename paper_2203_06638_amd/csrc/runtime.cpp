@@ -1,0 +1,922 @@
+// runtime.cpp -- the host side of liblpp.so: model validation and layout,
+// truncated-backward plans, per-worker workspaces and streams, the step and
+// averaging executors, and the C ABI declared in include/lpp.h.
+//
+// Paper: arXiv 2203.06638 (LPP-SGD).  Alg. 1 gives the updater and averager
+// loops; Sec. 3 "Block partitions" defines the blocks; Sec. 3 "Discussion on
+// the Rule" gives the reason for the truncated backward pass (a partial
+// gradient only needs backpropagation from the output down to its block).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/lpp.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+#define HIPCHK(expr)                                                                         \
+    do {                                                                                     \
+        hipError_t _e = (expr);                                                              \
+        if (_e != hipSuccess) return fail(LPP_EHIP, std::string(#expr) + ": " + hipGetErrorString(_e)); \
+    } while (0)
+
+struct Shape {
+    int c = 0, h = 0, w = 0;
+    long numel() const { return (long)c * h * w; }
+};
+
+struct Layer {
+    lpp_layer L{};
+    Shape in0, in1, out;
+    long poff = -1, np = 0;       // canonical parameter range
+    long wcount = 0;              // conv/linear weight count (before the bias)
+    int cin_p = 0;                // conv: stored channels of the input
+    long wf_off = -1, wd_off = -1;// conv: W_f / W_d in the worker's weight buffer (floats)
+    double macs = 0;              // forward multiply-adds (conv, linear)
+    lpp::WgradPlan wg{};
+    // workspace offsets (bytes) of this layer's output, its gradient and aux data
+    size_t act = 0, dact = 0, aux = 0;
+};
+
+struct Plan {
+    std::vector<char> run;        // backward of this layer runs (its output grad exists)
+    std::vector<char> wgrad;      // parameter gradients of this layer are written
+    std::vector<char> din0, din1; // gradient into input 0 / 1 is computed
+    std::vector<char> acc0, acc1; // ... and accumulated onto an earlier contribution
+    double flops = 0;             // backward flops (dgrad + wgrad of conv/linear)
+};
+
+struct Model {
+    lpp_model_desc desc{};
+    std::vector<Layer> layers;
+    int P = 0;
+    long d = 0;
+    std::vector<long> blo, bhi;   // block ranges 0..P
+    int img_cp = 0;               // stored channels of the image
+    double fwd_flops = 0;
+    std::vector<Plan> plans;      // per partition 0..P
+};
+
+int ceil4(int c) { return (c + 3) / 4 * 4; }
+
+// Validates the description and fills shapes, parameter layout, blocks and
+// plans.  Returns LPP_OK or an error code with g_err set.
+int build_model(const lpp_model_desc* desc, int P, Model& M) {
+    if (!desc) return fail(LPP_EINVAL, "desc is NULL");
+    if (P < 1 || P > 64) return fail(LPP_EINVAL, "P must be in [1, 64]");
+    const lpp_model_desc& D = *desc;
+    if (D.n_layers < 1 || !D.layers) return fail(LPP_EINVAL, "model has no layers");
+    if (D.batch < 1 || D.in_c < 1 || D.in_h < 1 || D.in_w < 1 || D.n_classes < 1)
+        return fail(LPP_EINVAL, "batch, image shape and n_classes must be positive");
+    if (D.dtype != LPP_FP32 && D.dtype != LPP_BF16) return fail(LPP_EINVAL, "unknown dtype");
+    if (D.dtype == LPP_BF16) return fail(LPP_EUNSUPPORTED, "bf16 activations are not built yet");
+    if (!(D.bn_eps > 0.f) || !std::isfinite(D.bn_eps)) return fail(LPP_EINVAL, "bn_eps must be positive");
+    if (!(D.momentum >= 0.f) || !std::isfinite(D.momentum) || !std::isfinite(D.weight_decay))
+        return fail(LPP_EINVAL, "momentum must be >= 0 and finite; weight_decay finite");
+    M.desc = D;
+    M.desc.layers = nullptr;
+    M.P = P;
+    M.img_cp = ceil4(D.in_c);
+    const int n = D.n_layers;
+    M.layers.assign(n, Layer{});
+    const Shape img{D.in_c, D.in_h, D.in_w};
+    long d = 0;
+    int last_block = 0;
+    std::vector<char> block_seen(P + 1, 0);
+    std::vector<int> consumers(n, 0);
+    for (int l = 0; l < n; ++l) {
+        Layer& Y = M.layers[l];
+        Y.L = D.layers[l];
+        const lpp_layer& L = Y.L;
+        char where[64];
+        snprintf(where, sizeof where, "layer %d: ", l);
+        if (L.in0 < -1 || L.in0 >= l) return fail(LPP_EINVAL, std::string(where) + "in0 must be -1 or an earlier layer");
+        Y.in0 = L.in0 < 0 ? img : M.layers[L.in0].out;
+        if (L.in0 >= 0) consumers[L.in0]++;
+        if (L.in0 < 0 && L.op != LPP_CONV)
+            return fail(LPP_EUNSUPPORTED, std::string(where) + "only a conv may read the image");
+        Shape o = Y.in0;
+        switch (L.op) {
+        case LPP_CONV: {
+            if (L.cin != Y.in0.c) return fail(LPP_EINVAL, std::string(where) + "cin does not match the input");
+            if (L.cout < 1 || L.k < 1 || L.stride < 1 || L.pad < 0)
+                return fail(LPP_EINVAL, std::string(where) + "bad conv geometry");
+            o.c = L.cout;
+            o.h = (Y.in0.h + 2 * L.pad - L.k) / L.stride + 1;
+            o.w = (Y.in0.w + 2 * L.pad - L.k) / L.stride + 1;
+            if (Y.in0.h + 2 * L.pad < L.k || Y.in0.w + 2 * L.pad < L.k || o.h < 1 || o.w < 1)
+                return fail(LPP_EINVAL, std::string(where) + "conv output is empty");
+            if (L.cout % 4) return fail(LPP_EUNSUPPORTED, std::string(where) + "cout must be a multiple of 4");
+            Y.cin_p = L.in0 < 0 ? M.img_cp : L.cin;
+            if (Y.cin_p % 4) return fail(LPP_EUNSUPPORTED, std::string(where) + "cin must be a multiple of 4");
+            Y.wcount = (long)L.cout * L.cin * L.k * L.k;
+            Y.np = Y.wcount + (L.bias ? L.cout : 0);
+            Y.macs = (double)D.batch * o.h * o.w * L.cout * (double)L.cin * L.k * L.k;
+            break;
+        }
+        case LPP_BN:
+            if (L.cout != Y.in0.c) return fail(LPP_EINVAL, std::string(where) + "bn channels do not match the input");
+            Y.np = 2L * L.cout;
+            break;
+        case LPP_RELU:
+            break;
+        case LPP_ADD:
+            if (L.in1 < -1 || L.in1 >= l) return fail(LPP_EINVAL, std::string(where) + "in1 must be an earlier layer");
+            if (L.in1 < 0) return fail(LPP_EUNSUPPORTED, std::string(where) + "add cannot read the image");
+            Y.in1 = M.layers[L.in1].out;
+            consumers[L.in1]++;
+            if (Y.in1.c != Y.in0.c || Y.in1.h != Y.in0.h || Y.in1.w != Y.in0.w)
+                return fail(LPP_EINVAL, std::string(where) + "add inputs differ in shape");
+            break;
+        case LPP_MAXPOOL:
+            if (L.k < 1 || L.stride < 1 || L.pad < 0 || L.pad >= L.k || L.k * L.k > 255)
+                return fail(LPP_EINVAL, std::string(where) + "bad pool geometry");
+            o.h = (Y.in0.h + 2 * L.pad - L.k) / L.stride + 1;
+            o.w = (Y.in0.w + 2 * L.pad - L.k) / L.stride + 1;
+            if (o.h < 1 || o.w < 1) return fail(LPP_EINVAL, std::string(where) + "pool output is empty");
+            break;
+        case LPP_GAP:
+            o.h = 1;
+            o.w = 1;
+            break;
+        case LPP_LINEAR:
+            if (Y.in0.h != 1 || Y.in0.w != 1)
+                return fail(LPP_EUNSUPPORTED, std::string(where) + "linear input must be 1x1 (pool first)");
+            if (L.cin != Y.in0.c || L.cout < 1) return fail(LPP_EINVAL, std::string(where) + "bad linear shape");
+            o.c = L.cout;
+            Y.wcount = (long)L.cout * L.cin;
+            Y.np = Y.wcount + (L.bias ? L.cout : 0);
+            Y.macs = (double)D.batch * L.cout * L.cin;
+            break;
+        default:
+            return fail(LPP_EINVAL, std::string(where) + "unknown op");
+        }
+        Y.out = o;
+        if (L.op != LPP_LINEAR && o.c % 4)
+            return fail(LPP_EUNSUPPORTED, std::string(where) + "channel counts must be multiples of 4");
+        if ((double)D.batch * o.numel() >= 2147483647.0 || (double)D.batch * Y.in0.h * Y.in0.w * ceil4(Y.in0.c) >= 2147483647.0)
+            return fail(LPP_EUNSUPPORTED, std::string(where) + "activation exceeds 2^31 elements");
+        if (Y.np > 0) {
+            if (L.block < 1 || L.block > P) return fail(LPP_EINVAL, std::string(where) + "block must be in [1, P]");
+            if (L.block < last_block)
+                return fail(LPP_EINVAL, std::string(where) + "blocks must be contiguous runs in parameter order");
+            last_block = L.block;
+            block_seen[L.block] = 1;
+            Y.poff = d;
+            d += Y.np;
+        }
+    }
+    for (int i = 1; i <= P; ++i)
+        if (!block_seen[i]) return fail(LPP_EINVAL, "every block 1..P must own parameters");
+    const Layer& last = M.layers[n - 1];
+    if (last.L.op != LPP_LINEAR || last.out.c != D.n_classes)
+        return fail(LPP_EINVAL, "the last layer must be a linear layer with n_classes outputs");
+    for (int l = 0; l < n - 1; ++l)
+        if (consumers[l] == 0) return fail(LPP_EINVAL, "every layer but the last must feed another layer");
+    if (consumers[n - 1] != 0) return fail(LPP_EINVAL, "the logits layer cannot feed another layer");
+    M.d = d;
+    M.blo.assign(P + 1, 0);
+    M.bhi.assign(P + 1, 0);
+    M.blo[0] = 0;
+    M.bhi[0] = d;
+    for (int i = 1; i <= P; ++i) {
+        long lo = -1, hi = -1;
+        for (auto& Y : M.layers)
+            if (Y.np > 0 && Y.L.block == i) {
+                if (lo < 0) lo = Y.poff;
+                hi = Y.poff + Y.np;
+            }
+        M.blo[i] = lo;
+        M.bhi[i] = hi;
+    }
+    M.fwd_flops = 0;
+    for (auto& Y : M.layers) M.fwd_flops += 2.0 * Y.macs;
+
+    // truncated-backward plans
+    M.plans.assign(P + 1, Plan{});
+    for (int i = 0; i <= P; ++i) {
+        Plan& pl = M.plans[i];
+        pl.run.assign(n, 0);
+        pl.wgrad.assign(n, 0);
+        pl.din0.assign(n, 0);
+        pl.din1.assign(n, 0);
+        pl.acc0.assign(n, 0);
+        pl.acc1.assign(n, 0);
+        for (int l = 0; l < n; ++l) {
+            const Layer& Y = M.layers[l];
+            const bool inblk = Y.np > 0 && (i == 0 || Y.L.block == i);
+            pl.wgrad[l] = inblk;
+            pl.run[l] = inblk || (Y.L.in0 >= 0 && pl.run[Y.L.in0]) ||
+                        (Y.L.op == LPP_ADD && Y.L.in1 >= 0 && pl.run[Y.L.in1]);
+        }
+        std::vector<char> written(n, 0);
+        for (int l = n - 1; l >= 0; --l) {
+            if (!pl.run[l]) continue;
+            const Layer& Y = M.layers[l];
+            const int a = Y.L.in0;
+            if (a >= 0 && pl.run[a]) {
+                pl.din0[l] = 1;
+                pl.acc0[l] = written[a];
+                written[a] = 1;
+            }
+            if (Y.L.op == LPP_ADD) {
+                const int b = Y.L.in1;
+                if (b >= 0 && pl.run[b]) {
+                    pl.din1[l] = 1;
+                    pl.acc1[l] = written[b];
+                    written[b] = 1;
+                }
+            }
+            if (Y.L.op == LPP_CONV || Y.L.op == LPP_LINEAR) {
+                if (pl.wgrad[l]) pl.flops += 2.0 * Y.macs;
+                if (pl.din0[l]) pl.flops += 2.0 * Y.macs;
+            }
+        }
+    }
+    return LPP_OK;
+}
+
+// ------------------------------------------------------------------------
+
+struct Timer {
+    std::mutex mu;
+    std::string family;           // empty = off
+    struct Rec { hipEvent_t a, b; double work; };
+    std::vector<Rec> recs;
+    std::vector<hipEvent_t> pool;
+    double ms = 0, work = 0;
+    long launches = 0;
+};
+
+struct Worker {
+    hipStream_t stream = nullptr;
+    bool own_stream = false;
+    char* ws = nullptr;
+    float* v = nullptr;
+    float* wbuf = nullptr;
+    float* g = nullptr;
+    float* m = nullptr;
+    float* loss = nullptr;
+    float* img = nullptr;
+    double* red0 = nullptr;
+    double* red1 = nullptr;
+    float* wpart = nullptr;
+    int last_partition = -1;
+};
+
+}  // namespace
+
+struct lpp_ctx {
+    Model M;
+    int K = 0, P = 0, mode = 0;
+    long dpad = 0;
+    float* replicas = nullptr;               // K * dpad
+    std::vector<Worker> workers;
+    hipStream_t avg_stream = nullptr;
+    bool own_avg = false;
+    lpp::SnapConv* snap_dev = nullptr;
+    int n_snap = 0;
+    long wbuf_floats = 0;
+    size_t ws_bytes = 0;
+    size_t off_v = 0, off_wbuf = 0, off_g = 0, off_m = 0, off_loss = 0, off_img = 0, off_red0 = 0, off_red1 = 0,
+           off_wpart = 0;
+    std::unique_ptr<std::atomic<long>[]> counters;
+    Timer timer;
+    int device = 0;
+
+    float* act(Worker& w, int l) { return (float*)(w.ws + M.layers[l].act); }
+    float* dact(Worker& w, int l) { return (float*)(w.ws + M.layers[l].dact); }
+    float* aux(Worker& w, int l) { return (float*)(w.ws + M.layers[l].aux); }
+};
+
+namespace {
+
+template <class F>
+hipError_t timed_launch(lpp_ctx* c, const char* family, double work, hipStream_t st, F&& f) {
+    Timer& T = c->timer;
+    bool on = false;
+    hipEvent_t a = nullptr, b = nullptr;
+    {
+        std::lock_guard<std::mutex> g(T.mu);
+        if (!T.family.empty() && T.family == family) {
+            on = true;
+            for (hipEvent_t* e : {&a, &b}) {
+                if (!T.pool.empty()) {
+                    *e = T.pool.back();
+                    T.pool.pop_back();
+                } else if (hipEventCreate(e) != hipSuccess) {
+                    on = false;
+                }
+            }
+        }
+    }
+    if (on) hipEventRecord(a, st);
+    hipError_t e = f();
+    if (on) {
+        hipEventRecord(b, st);
+        std::lock_guard<std::mutex> g(T.mu);
+        T.recs.push_back({a, b, work});
+    }
+    return e;
+}
+
+#define LAUNCH(fam, work, st, call)                                                              \
+    do {                                                                                         \
+        hipError_t _e = timed_launch(c, fam, (work), (st), [&]() { return (call); });            \
+        if (_e != hipSuccess) return fail(LPP_EHIP, std::string(fam) + ": " + hipGetErrorString(_e)); \
+    } while (0)
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int check_worker(const lpp_ctx* c, int w) {
+    if (!c) return fail(LPP_EINVAL, "ctx is NULL");
+    if (w < 0 || w >= c->K * c->P) return fail(LPP_EINVAL, "worker out of range");
+    return LPP_OK;
+}
+
+int sync_all(lpp_ctx* c) {
+    for (auto& w : c->workers) HIPCHK(hipStreamSynchronize(w.stream));
+    HIPCHK(hipStreamSynchronize(c->avg_stream));
+    return LPP_OK;
+}
+
+void destroy_ctx(lpp_ctx* c) {
+    if (!c) return;
+    hipSetDevice(c->device);
+    for (auto& w : c->workers) {
+        if (w.stream) hipStreamSynchronize(w.stream);
+        if (w.ws) hipFree(w.ws);
+        if (w.own_stream && w.stream) hipStreamDestroy(w.stream);
+    }
+    if (c->avg_stream) hipStreamSynchronize(c->avg_stream);
+    if (c->own_avg && c->avg_stream) hipStreamDestroy(c->avg_stream);
+    if (c->replicas) hipFree(c->replicas);
+    if (c->snap_dev) hipFree(c->snap_dev);
+    for (auto& r : c->timer.recs) {
+        hipEventDestroy(r.a);
+        hipEventDestroy(r.b);
+    }
+    for (auto e : c->timer.pool) hipEventDestroy(e);
+    delete c;
+}
+
+// Forward pass of worker w at its snapshot; loss and dlogits at the end.
+int run_forward(lpp_ctx* c, Worker& w, const lpp_batch* b) {
+    Model& M = c->M;
+    const int N = M.desc.batch;
+    hipStream_t st = w.stream;
+    LAUNCH("image", 8.0 * N * M.desc.in_c * M.desc.in_h * M.desc.in_w, st,
+           lpp::launch_nchw_to_nhwc(b->images, w.img, N, M.desc.in_c, M.desc.in_h, M.desc.in_w, M.img_cp, st));
+    for (int l = 0; l < (int)M.layers.size(); ++l) {
+        Layer& Y = M.layers[l];
+        const float* x0 = Y.L.in0 < 0 ? w.img : c->act(w, Y.L.in0);
+        float* y = c->act(w, l);
+        const long Mrows = (long)N * Y.in0.h * Y.in0.w;
+        switch (Y.L.op) {
+        case LPP_CONV: {
+            lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride, Y.L.pad};
+            const float* bias = Y.L.bias ? w.v + Y.poff + Y.wcount : nullptr;
+            LAUNCH("conv_fwd", 2.0 * Y.macs, st,
+                   lpp::launch_conv_igemm(lpp::CONV_FWD, x0, w.wbuf + Y.wf_off, bias, y, g, false, st));
+            break;
+        }
+        case LPP_BN: {
+            const int C = Y.out.c;
+            float* ax = c->aux(w, l);   // mean, rstd, scale, shift, a, mdy, mdyx
+            const int nb = lpp::chan_reduce_blocks(Mrows, C);
+            LAUNCH("bn_stats", 4.0 * Mrows * C, st, lpp::launch_bn_stats_partial(x0, Mrows, C, w.red0, w.red1, st));
+            LAUNCH("bn_stats", 0.0, st,
+                   lpp::launch_bn_stats_finalize(w.red0, w.red1, nb, Mrows, C, w.v + Y.poff, w.v + Y.poff + C,
+                                                 M.desc.bn_eps, ax, ax + C, ax + 2 * C, ax + 3 * C, st));
+            LAUNCH("bn_apply", 8.0 * Mrows * C, st, lpp::launch_chan_affine(x0, ax + 2 * C, ax + 3 * C, y, Mrows, C, st));
+            break;
+        }
+        case LPP_RELU:
+            LAUNCH("relu", 8.0 * Mrows * Y.out.c, st, lpp::launch_relu_fwd(x0, y, Mrows * Y.out.c, st));
+            break;
+        case LPP_ADD:
+            LAUNCH("add", 12.0 * Mrows * Y.out.c, st,
+                   lpp::launch_add_fwd(x0, c->act(w, Y.L.in1), y, Mrows * Y.out.c, st));
+            break;
+        case LPP_MAXPOOL:
+            LAUNCH("maxpool", 4.0 * Mrows * Y.out.c, st,
+                   lpp::launch_maxpool_fwd(x0, y, (uint8_t*)c->aux(w, l), N, Y.in0.h, Y.in0.w, Y.in0.c, Y.out.h,
+                                           Y.out.w, Y.L.k, Y.L.stride, Y.L.pad, st));
+            break;
+        case LPP_GAP:
+            LAUNCH("gap", 4.0 * Mrows * Y.out.c, st,
+                   lpp::launch_gap_fwd(x0, y, N, Y.in0.h * Y.in0.w, Y.in0.c, st));
+            break;
+        case LPP_LINEAR: {
+            const float* W = w.v + Y.poff;
+            const float* bias = Y.L.bias ? W + Y.wcount : nullptr;
+            LAUNCH("linear", 2.0 * Y.macs, st, lpp::launch_linear_fwd(x0, W, bias, y, N, Y.L.cin, Y.L.cout, st));
+            break;
+        }
+        }
+    }
+    const int last = (int)M.layers.size() - 1;
+    LAUNCH("softmax_ce", 0.0, st,
+           lpp::launch_softmax_ce(c->act(w, last), b->labels, c->dact(w, last), w.loss, N, M.desc.n_classes, st));
+    return LPP_OK;
+}
+
+// Backward pass truncated at `partition`; parameter gradients go to w.g at
+// their canonical offsets.
+int run_backward(lpp_ctx* c, Worker& w, int partition) {
+    Model& M = c->M;
+    const Plan& pl = M.plans[partition];
+    const int N = M.desc.batch;
+    hipStream_t st = w.stream;
+    for (int l = (int)M.layers.size() - 1; l >= 0; --l) {
+        if (!pl.run[l]) continue;
+        Layer& Y = M.layers[l];
+        const float* x0 = Y.L.in0 < 0 ? w.img : c->act(w, Y.L.in0);
+        float* dy = c->dact(w, l);
+        float* dx0 = pl.din0[l] ? c->dact(w, Y.L.in0) : nullptr;
+        const long Min = (long)N * Y.in0.h * Y.in0.w;
+        switch (Y.L.op) {
+        case LPP_CONV: {
+            if (pl.wgrad[l]) {
+                const int Ktot = Y.L.k * Y.L.k * Y.cin_p;
+                LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
+                       lpp::launch_conv_wgrad(dy, x0, w.wpart, N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w,
+                                              Y.L.cout, Y.L.k, Y.L.k, Y.L.stride, Y.L.pad, Y.wg, st));
+                LAUNCH("wgrad_reduce", 4.0 * Y.wg.part_floats, st,
+                       lpp::launch_wgrad_reduce(w.wpart, Y.wg.splits, Y.L.cout, Ktot, Y.L.cin, Y.cin_p, Y.L.k,
+                                                Y.L.k, w.g + Y.poff, st));
+                if (Y.L.bias) {
+                    const long Mo = (long)N * Y.out.h * Y.out.w;
+                    const int nb = lpp::chan_reduce_blocks(Mo, Y.L.cout);
+                    LAUNCH("bias_grad", 4.0 * Mo * Y.L.cout, st,
+                           lpp::launch_col_sum_partial(dy, Mo, Y.L.cout, w.red0, st));
+                    LAUNCH("bias_grad", 0.0, st,
+                           lpp::launch_col_sum_finalize(w.red0, nb, Y.L.cout, w.g + Y.poff + Y.wcount, st));
+                }
+            }
+            if (dx0) {
+                lpp::ConvGeom g{N, Y.out.h, Y.out.w, Y.L.cout, Y.in0.h, Y.in0.w, Y.L.cin, Y.L.k, Y.L.k, Y.L.stride,
+                                Y.L.pad};
+                LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
+                       lpp::launch_conv_igemm(lpp::CONV_DGRAD, dy, w.wbuf + Y.wd_off, nullptr, dx0, g,
+                                              pl.acc0[l] != 0, st));
+            }
+            break;
+        }
+        case LPP_BN: {
+            const int C = Y.out.c;
+            float* ax = c->aux(w, l);
+            const int nb = lpp::chan_reduce_blocks(Min, C);
+            LAUNCH("bn_bwd", 8.0 * Min * C, st,
+                   lpp::launch_bn_bwd_partial(dy, x0, ax, ax + C, Min, C, w.red0, w.red1, st));
+            float* gg = pl.wgrad[l] ? w.g + Y.poff : nullptr;
+            float* gb = pl.wgrad[l] ? w.g + Y.poff + C : nullptr;
+            LAUNCH("bn_bwd", 0.0, st,
+                   lpp::launch_bn_bwd_finalize(w.red0, w.red1, nb, Min, C, w.v + Y.poff, ax + C, gg, gb, ax + 4 * C,
+                                               ax + 5 * C, ax + 6 * C, st));
+            if (dx0)
+                LAUNCH("bn_bwd", 12.0 * Min * C, st,
+                       lpp::launch_bn_bwd_data(dy, x0, ax, ax + C, ax + 4 * C, ax + 5 * C, ax + 6 * C, dx0, Min, C,
+                                               pl.acc0[l] != 0, st));
+            break;
+        }
+        case LPP_RELU:
+            if (dx0)
+                LAUNCH("relu", 12.0 * Min * Y.out.c, st,
+                       lpp::launch_relu_bwd(dy, x0, dx0, Min * Y.out.c, pl.acc0[l] != 0, st));
+            break;
+        case LPP_ADD:
+            if (dx0)
+                LAUNCH("add", 8.0 * Min * Y.out.c, st,
+                       lpp::launch_copy_acc(dy, dx0, Min * Y.out.c, pl.acc0[l] != 0, st));
+            if (pl.din1[l])
+                LAUNCH("add", 8.0 * Min * Y.out.c, st,
+                       lpp::launch_copy_acc(dy, c->dact(w, Y.L.in1), Min * Y.out.c, pl.acc1[l] != 0, st));
+            break;
+        case LPP_MAXPOOL:
+            if (dx0)
+                LAUNCH("maxpool", 8.0 * Min * Y.out.c, st,
+                       lpp::launch_maxpool_bwd(dy, (const uint8_t*)c->aux(w, l), dx0, N, Y.in0.h, Y.in0.w, Y.in0.c,
+                                               Y.out.h, Y.out.w, Y.L.k, Y.L.stride, Y.L.pad, pl.acc0[l] != 0, st));
+            break;
+        case LPP_GAP:
+            if (dx0)
+                LAUNCH("gap", 4.0 * Min * Y.in0.c, st,
+                       lpp::launch_gap_bwd(dy, dx0, N, Y.in0.h * Y.in0.w, Y.in0.c, pl.acc0[l] != 0, st));
+            break;
+        case LPP_LINEAR: {
+            const float* W = w.v + Y.poff;
+            if (pl.wgrad[l])
+                LAUNCH("linear", 2.0 * Y.macs, st,
+                       lpp::launch_linear_bwd_w(dy, x0, w.g + Y.poff, Y.L.bias ? w.g + Y.poff + Y.wcount : nullptr,
+                                                N, Y.L.cin, Y.L.cout, st));
+            if (dx0)
+                LAUNCH("linear", 2.0 * Y.macs, st,
+                       lpp::launch_linear_bwd_x(dy, W, dx0, N, Y.L.cin, Y.L.cout, pl.acc0[l] != 0, st));
+            break;
+        }
+        }
+    }
+    return LPP_OK;
+}
+
+}  // namespace
+
+// ========================================================================
+// C ABI
+// ========================================================================
+
+extern "C" {
+
+const char* lpp_last_error(void) { return g_err.c_str(); }
+
+int lpp_describe(const lpp_model_desc* desc, int P, lpp_model_info* out) {
+    if (!out) return fail(LPP_EINVAL, "out is NULL");
+    Model M;
+    int rc = build_model(desc, P, M);
+    if (rc) return rc;
+    memset(out, 0, sizeof *out);
+    out->d = M.d;
+    out->P = P;
+    for (int i = 0; i <= P; ++i) {
+        out->block_lo[i] = M.blo[i];
+        out->block_hi[i] = M.bhi[i];
+        out->bwd_flops[i] = M.plans[i].flops;
+    }
+    out->fwd_flops = M.fwd_flops;
+    return LPP_OK;
+}
+
+int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, lpp_ctx** out) {
+    if (!out) return fail(LPP_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (K < 1 || K > lpp::kMaxReplicas) return fail(LPP_EINVAL, "K must be in [1, 16]");
+    std::unique_ptr<lpp_ctx, void (*)(lpp_ctx*)> c(new lpp_ctx, destroy_ctx);
+    int rc = build_model(desc, P, c->M);
+    if (rc) return rc;
+    c->K = K;
+    c->P = P;
+    c->mode = opt ? opt->mode : LPP_SEQUENTIAL;
+    if (c->mode != LPP_SEQUENTIAL && c->mode != LPP_ASYNC) return fail(LPP_EINVAL, "unknown mode");
+    HIPCHK(hipGetDevice(&c->device));
+    Model& M = c->M;
+    const int N = M.desc.batch;
+    const long d = M.d;
+    c->dpad = (d + 63) / 64 * 64;
+
+    // conv weight layouts and the snapshot table
+    std::vector<lpp::SnapConv> snaps;
+    long wf = 0;
+    for (auto& Y : M.layers) {
+        if (Y.L.op != LPP_CONV) continue;
+        const long nf = (long)Y.L.cout * Y.L.k * Y.L.k * Y.cin_p;
+        const long nd = (long)Y.L.cin * Y.L.k * Y.L.k * Y.L.cout;
+        Y.wf_off = wf;
+        wf += (nf + 63) / 64 * 64;
+        Y.wd_off = wf;
+        wf += (nd + 63) / 64 * 64;
+        snaps.push_back({Y.poff, Y.np, Y.L.cout, Y.L.cin, Y.cin_p, Y.L.k, Y.L.k, Y.wf_off, Y.wd_off});
+        Y.wg = lpp::wgrad_plan(Y.L.cout, Y.L.k * Y.L.k * Y.cin_p, (long)N * Y.out.h * Y.out.w);
+    }
+    c->wbuf_floats = wf;
+    c->n_snap = (int)snaps.size();
+
+    // workspace layout (bytes)
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off = align256(off + bytes);
+        return o;
+    };
+    c->off_v = take(sizeof(float) * c->dpad);
+    c->off_wbuf = take(sizeof(float) * std::max<long>(wf, 1));
+    c->off_g = take(sizeof(float) * c->dpad);
+    c->off_m = take(sizeof(float) * c->dpad);
+    c->off_loss = take(sizeof(float) * (1 + N));
+    c->off_img = take(sizeof(float) * (size_t)N * M.desc.in_h * M.desc.in_w * M.img_cp);
+    long red_rows = 1, wpart = 1;
+    for (auto& Y : M.layers) {
+        const long rows_out = (long)N * Y.out.h * Y.out.w;
+        Y.act = take(sizeof(float) * (size_t)rows_out * Y.out.c);
+        Y.dact = take(sizeof(float) * (size_t)rows_out * Y.out.c);
+        if (Y.L.op == LPP_BN) Y.aux = take(sizeof(float) * 7 * Y.out.c);
+        if (Y.L.op == LPP_MAXPOOL) Y.aux = take((size_t)rows_out * Y.out.c);
+        const long rin = (long)N * Y.in0.h * Y.in0.w;
+        if (Y.L.op == LPP_BN) red_rows = std::max<long>(red_rows, (long)lpp::chan_reduce_blocks(rin, Y.out.c) * Y.out.c);
+        if (Y.L.op == LPP_CONV) {
+            red_rows = std::max<long>(red_rows, (long)lpp::chan_reduce_blocks(rows_out, Y.out.c) * Y.out.c);
+            wpart = std::max<long>(wpart, Y.wg.part_floats);
+        }
+    }
+    c->off_red0 = take(sizeof(double) * red_rows);
+    c->off_red1 = take(sizeof(double) * red_rows);
+    c->off_wpart = take(sizeof(float) * wpart);
+    c->ws_bytes = off;
+
+    // device allocations
+    if (hipMalloc((void**)&c->replicas, sizeof(float) * c->dpad * K) != hipSuccess)
+        return fail(LPP_ENOMEM, "replica allocation failed");
+    HIPCHK(hipMemset(c->replicas, 0, sizeof(float) * c->dpad * K));
+    if (!snaps.empty()) {
+        if (hipMalloc((void**)&c->snap_dev, sizeof(lpp::SnapConv) * snaps.size()) != hipSuccess)
+            return fail(LPP_ENOMEM, "snapshot table allocation failed");
+        HIPCHK(hipMemcpy(c->snap_dev, snaps.data(), sizeof(lpp::SnapConv) * snaps.size(), hipMemcpyHostToDevice));
+    }
+    c->counters.reset(new std::atomic<long>[K]);
+    for (int q = 0; q < K; ++q) c->counters[q].store(0);
+    c->workers.resize((size_t)K * P);
+    for (int i = 0; i < K * P; ++i) {
+        Worker& w = c->workers[i];
+        if (opt && opt->worker_streams && opt->worker_streams[i]) {
+            w.stream = (hipStream_t)opt->worker_streams[i];
+        } else {
+            HIPCHK(hipStreamCreateWithFlags(&w.stream, hipStreamNonBlocking));
+            w.own_stream = true;
+        }
+        if (hipMalloc((void**)&w.ws, c->ws_bytes) != hipSuccess)
+            return fail(LPP_ENOMEM, "worker workspace allocation failed");
+        HIPCHK(hipMemset(w.ws, 0, c->ws_bytes));
+        w.v = (float*)(w.ws + c->off_v);
+        w.wbuf = (float*)(w.ws + c->off_wbuf);
+        w.g = (float*)(w.ws + c->off_g);
+        w.m = (float*)(w.ws + c->off_m);
+        w.loss = (float*)(w.ws + c->off_loss);
+        w.img = (float*)(w.ws + c->off_img);
+        w.red0 = (double*)(w.ws + c->off_red0);
+        w.red1 = (double*)(w.ws + c->off_red1);
+        w.wpart = (float*)(w.ws + c->off_wpart);
+    }
+    if (opt && opt->avg_stream) {
+        c->avg_stream = (hipStream_t)opt->avg_stream;
+    } else {
+        HIPCHK(hipStreamCreateWithFlags(&c->avg_stream, hipStreamNonBlocking));
+        c->own_avg = true;
+    }
+    HIPCHK(hipDeviceSynchronize());
+    *out = c.release();
+    return LPP_OK;
+}
+
+int lpp_destroy(lpp_ctx* c) {
+    if (!c) return fail(LPP_EINVAL, "ctx is NULL");
+    destroy_ctx(c);
+    return LPP_OK;
+}
+
+int lpp_step(lpp_ctx* c, int worker, const lpp_batch* batch, int partition, float lr) {
+    int rc = check_worker(c, worker);
+    if (rc) return rc;
+    if (!batch || !batch->images || !batch->labels) return fail(LPP_EINVAL, "batch or its buffers are NULL");
+    if (batch->n != c->M.desc.batch) return fail(LPP_EINVAL, "batch->n must equal the model's batch");
+    if (partition < 0 || partition > c->P) return fail(LPP_EINVAL, "partition must be in [0, P]");
+    if (!std::isfinite(lr)) return fail(LPP_EINVAL, "lr must be finite");
+    Worker& w = c->workers[worker];
+    const int q = worker / c->P;
+    c->counters[q].fetch_add(1);                 // s := read&inc(C^q)
+    float* xq = c->replicas + (long)q * c->dpad;
+    const long d = c->M.d;
+    hipStream_t st = w.stream;
+    LAUNCH("snapshot", 8.0 * d, st, lpp::launch_snapshot(xq, w.v, d, c->snap_dev, c->n_snap, w.wbuf, st));
+    rc = run_forward(c, w, batch);
+    if (rc) return rc;
+    rc = run_backward(c, w, partition);
+    if (rc) return rc;
+    const long lo = c->M.blo[partition], hi = c->M.bhi[partition];
+    const bool mom = c->M.desc.momentum != 0.f;
+    LAUNCH("sgd_update", (mom ? 20.0 : 12.0) * (hi - lo), st,
+           lpp::launch_sgd_update(xq, mom ? w.m : nullptr, w.g, lo, hi, lr, c->M.desc.momentum,
+                                  c->M.desc.weight_decay, st));
+    w.last_partition = partition;
+    if (c->mode == LPP_SEQUENTIAL) HIPCHK(hipStreamSynchronize(st));
+    return LPP_OK;
+}
+
+int lpp_average(lpp_ctx* c, const int* replicas, int n_replicas) {
+    if (!c) return fail(LPP_EINVAL, "ctx is NULL");
+    lpp::RepPtrs rp{};
+    int n = 0;
+    if (!replicas) {
+        if (n_replicas != 0) return fail(LPP_EINVAL, "replicas NULL requires n_replicas == 0");
+        for (int q = 0; q < c->K; ++q) rp.p[n++] = c->replicas + (long)q * c->dpad;
+    } else {
+        if (n_replicas < 1 || n_replicas > c->K) return fail(LPP_EINVAL, "n_replicas out of range");
+        std::vector<char> seen(c->K, 0);
+        for (int i = 0; i < n_replicas; ++i) {
+            const int q = replicas[i];
+            if (q < 0 || q >= c->K || seen[q]) return fail(LPP_EINVAL, "replica ids must be distinct and in range");
+            seen[q] = 1;
+            rp.p[n++] = c->replicas + (long)q * c->dpad;
+        }
+    }
+    if (c->mode == LPP_SEQUENTIAL)
+        for (auto& w : c->workers) HIPCHK(hipStreamSynchronize(w.stream));
+    hipStream_t st = c->avg_stream;
+    LAUNCH("average", 8.0 * n * c->M.d, st, lpp::launch_average(rp, n, c->M.d, st));
+    if (c->mode == LPP_SEQUENTIAL) HIPCHK(hipStreamSynchronize(st));
+    return LPP_OK;
+}
+
+int lpp_sync(lpp_ctx* c) {
+    if (!c) return fail(LPP_EINVAL, "ctx is NULL");
+    return sync_all(c);
+}
+
+int lpp_set_params(lpp_ctx* c, int replica, const float* host, long d) {
+    if (!c || !host) return fail(LPP_EINVAL, "NULL argument");
+    if (d != c->M.d) return fail(LPP_EINVAL, "d does not match the model");
+    if (replica < -1 || replica >= c->K) return fail(LPP_EINVAL, "replica out of range");
+    int rc = sync_all(c);
+    if (rc) return rc;
+    for (int q = 0; q < c->K; ++q)
+        if (replica == -1 || replica == q)
+            HIPCHK(hipMemcpy(c->replicas + (long)q * c->dpad, host, sizeof(float) * d, hipMemcpyHostToDevice));
+    return LPP_OK;
+}
+
+int lpp_get_params(lpp_ctx* c, int replica, float* host, long d) {
+    if (!c || !host) return fail(LPP_EINVAL, "NULL argument");
+    if (d != c->M.d) return fail(LPP_EINVAL, "d does not match the model");
+    if (replica < 0 || replica >= c->K) return fail(LPP_EINVAL, "replica out of range");
+    int rc = sync_all(c);
+    if (rc) return rc;
+    HIPCHK(hipMemcpy(host, c->replicas + (long)replica * c->dpad, sizeof(float) * d, hipMemcpyDeviceToHost));
+    return LPP_OK;
+}
+
+int lpp_get_grad(lpp_ctx* c, int worker, float* host, long d) {
+    int rc = check_worker(c, worker);
+    if (rc) return rc;
+    if (!host || d != c->M.d) return fail(LPP_EINVAL, "bad host buffer or d");
+    rc = sync_all(c);
+    if (rc) return rc;
+    Worker& w = c->workers[worker];
+    std::fill(host, host + d, 0.f);
+    if (w.last_partition < 0) return LPP_OK;
+    const long lo = c->M.blo[w.last_partition], hi = c->M.bhi[w.last_partition];
+    HIPCHK(hipMemcpy(host + lo, w.g + lo, sizeof(float) * (hi - lo), hipMemcpyDeviceToHost));
+    return LPP_OK;
+}
+
+int lpp_get_momentum(lpp_ctx* c, int worker, float* host, long d) {
+    int rc = check_worker(c, worker);
+    if (rc) return rc;
+    if (!host || d != c->M.d) return fail(LPP_EINVAL, "bad host buffer or d");
+    rc = sync_all(c);
+    if (rc) return rc;
+    HIPCHK(hipMemcpy(host, c->workers[worker].m, sizeof(float) * d, hipMemcpyDeviceToHost));
+    return LPP_OK;
+}
+
+int lpp_set_momentum(lpp_ctx* c, int worker, const float* host, long d) {
+    int rc = check_worker(c, worker);
+    if (rc) return rc;
+    if (!host || d != c->M.d) return fail(LPP_EINVAL, "bad host buffer or d");
+    rc = sync_all(c);
+    if (rc) return rc;
+    HIPCHK(hipMemcpy(c->workers[worker].m, host, sizeof(float) * d, hipMemcpyHostToDevice));
+    return LPP_OK;
+}
+
+int lpp_get_loss(lpp_ctx* c, int worker, float* loss) {
+    int rc = check_worker(c, worker);
+    if (rc) return rc;
+    if (!loss) return fail(LPP_EINVAL, "loss is NULL");
+    rc = sync_all(c);
+    if (rc) return rc;
+    HIPCHK(hipMemcpy(loss, c->workers[worker].loss, sizeof(float), hipMemcpyDeviceToHost));
+    return LPP_OK;
+}
+
+int lpp_get_logits(lpp_ctx* c, int worker, float* host, long n) {
+    int rc = check_worker(c, worker);
+    if (rc) return rc;
+    const long want = (long)c->M.desc.batch * c->M.desc.n_classes;
+    if (!host || n != want) return fail(LPP_EINVAL, "n must be batch * n_classes");
+    rc = sync_all(c);
+    if (rc) return rc;
+    Worker& w = c->workers[worker];
+    HIPCHK(hipMemcpy(host, c->act(w, (int)c->M.layers.size() - 1), sizeof(float) * n, hipMemcpyDeviceToHost));
+    return LPP_OK;
+}
+
+static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* host, long n) {
+    int rc = check_worker(c, worker);
+    if (rc) return rc;
+    if (layer < 0 || layer >= (int)c->M.layers.size()) return fail(LPP_EINVAL, "layer out of range");
+    const Layer& Y = c->M.layers[layer];
+    const int N = c->M.desc.batch;
+    const long want = (long)N * Y.out.numel();
+    if (!host || n != want) return fail(LPP_EINVAL, "n must be batch * c * h * w of the layer");
+    Worker& w = c->workers[worker];
+    if (grad && (w.last_partition < 0 || !c->M.plans[w.last_partition].run[layer]))
+        return fail(LPP_ESTATE, "the last step's backward pass did not reach this layer");
+    rc = sync_all(c);
+    if (rc) return rc;
+    float* tmp = nullptr;
+    if (hipMalloc((void**)&tmp, sizeof(float) * n) != hipSuccess) return fail(LPP_ENOMEM, "temporary allocation");
+    const float* src = grad ? c->dact(w, layer) : c->act(w, layer);
+    hipError_t e = lpp::launch_nhwc_to_nchw(src, tmp, N, Y.out.c, Y.out.h, Y.out.w, Y.out.c, w.stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(w.stream);
+    if (e == hipSuccess) e = hipMemcpy(host, tmp, sizeof(float) * n, hipMemcpyDeviceToHost);
+    hipFree(tmp);
+    if (e != hipSuccess) return fail(LPP_EHIP, std::string("layer copy: ") + hipGetErrorString(e));
+    return LPP_OK;
+}
+
+int lpp_get_activation(lpp_ctx* c, int worker, int layer, float* host, long n) {
+    return copy_layer_nchw(c, worker, layer, false, host, n);
+}
+
+int lpp_get_activation_grad(lpp_ctx* c, int worker, int layer, float* host, long n) {
+    return copy_layer_nchw(c, worker, layer, true, host, n);
+}
+
+long lpp_num_params(const lpp_ctx* c) { return c ? c->M.d : -1; }
+
+int lpp_block_range(const lpp_ctx* c, int i, long* lo, long* hi) {
+    if (!c || !lo || !hi) return fail(LPP_EINVAL, "NULL argument");
+    if (i < 0 || i > c->P) return fail(LPP_EINVAL, "block out of range");
+    *lo = c->M.blo[i];
+    *hi = c->M.bhi[i];
+    return LPP_OK;
+}
+
+long lpp_counter(const lpp_ctx* c, int replica) {
+    if (!c || replica < 0 || replica >= c->K) return -1;
+    return c->counters[replica].load();
+}
+
+int lpp_timer_enable(lpp_ctx* c, const char* name) {
+    if (!c) return fail(LPP_EINVAL, "ctx is NULL");
+    int rc = sync_all(c);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> g(c->timer.mu);
+    for (auto& r : c->timer.recs) {
+        c->timer.pool.push_back(r.a);
+        c->timer.pool.push_back(r.b);
+    }
+    c->timer.recs.clear();
+    c->timer.family = name ? name : "";
+    c->timer.ms = c->timer.work = 0;
+    c->timer.launches = 0;
+    return LPP_OK;
+}
+
+int lpp_timer_read(lpp_ctx* c, double* ms, long* launches, double* work) {
+    if (!c || !ms || !launches || !work) return fail(LPP_EINVAL, "NULL argument");
+    int rc = sync_all(c);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> g(c->timer.mu);
+    for (auto& r : c->timer.recs) {
+        float t = 0.f;
+        HIPCHK(hipEventElapsedTime(&t, r.a, r.b));
+        c->timer.ms += t;
+        c->timer.work += r.work;
+        c->timer.launches += 1;
+        c->timer.pool.push_back(r.a);
+        c->timer.pool.push_back(r.b);
+    }
+    c->timer.recs.clear();
+    *ms = c->timer.ms;
+    *launches = c->timer.launches;
+    *work = c->timer.work;
+    return LPP_OK;
+}
+
+int lpp_kernel_sgd_update(float* x, float* m, const float* g, long n, float lr, float mu, float wd, void* stream) {
+    if (!x || !g || n < 0) return fail(LPP_EINVAL, "bad arguments");
+    if (((uintptr_t)x | (uintptr_t)g | (uintptr_t)m) & 15) return fail(LPP_EINVAL, "buffers must be 16-byte aligned");
+    hipError_t e = lpp::launch_sgd_update(x, m, g, 0, n, lr, mu, wd, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(LPP_EHIP, std::string("sgd_update: ") + hipGetErrorString(e));
+    return LPP_OK;
+}
+
+int lpp_kernel_average(float* const* replicas, int n_rep, long n, void* stream) {
+    if (!replicas || n_rep < 1 || n_rep > lpp::kMaxReplicas || n < 0) return fail(LPP_EINVAL, "bad arguments");
+    lpp::RepPtrs rp{};
+    for (int k = 0; k < n_rep; ++k) {
+        if (!replicas[k] || ((uintptr_t)replicas[k] & 15)) return fail(LPP_EINVAL, "replicas must be 16-byte aligned");
+        rp.p[k] = replicas[k];
+    }
+    hipError_t e = lpp::launch_average(rp, n_rep, n, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(LPP_EHIP, std::string("average: ") + hipGetErrorString(e));
+    return LPP_OK;
+}
+
+}  // extern "C"

@@ -69,3 +69,12 @@ def perturb(x: np.ndarray, seed: int, scale: float) -> np.ndarray:
     """x plus i.i.d. N(0, scale^2) noise (float32); used to move BN affine
     parameters and biases off their trivial initial values in tests."""
     return (x + _rng(seed + 31).standard_normal(x.shape, dtype=np.float32) * np.float32(scale)).astype(np.float32)
+
+
+def grid_values(seed: int, shape, step: float, bound: float) -> np.ndarray:
+    """float32 values drawn uniformly from the grid {k * step : |k*step| <=
+    bound} (step a power of two).  Sums of products of a few such values are
+    exact in float32, so two evaluations of a small convolution in any order
+    and precision produce identical values."""
+    k = int(round(bound / step))
+    return (_rng(seed + 4242).integers(-k, k + 1, size=shape).astype(np.float32) * np.float32(step))

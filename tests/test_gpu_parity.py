@@ -1,0 +1,512 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 CPU oracle, in
+the deterministic sequential mode, on seeded synthetic inputs.
+
+Bar (fp32): max relative error per tensor 1e-4 on logits and activations,
+1e-3 on gradients and updated parameters (tests/parity.py defines the
+measure).  Integer results (counters, block ranges) must match exactly;
+results the method fixes bit for bit (a partial gradient is the full
+gradient restricted to the block; untouched blocks) are compared bitwise.
+
+ReLU masks and max-pool argmaxes are decisions taken on floating-point
+values.  A gradient comparison is made only where both sides must take the
+same decisions: (a) inputs on an exact grid, so the values that decide are
+identical in both precisions; (b) inputs whose oracle-side kink margin
+clears the measured fp32/fp64 disagreement (tests/parity.py, KINK_BAND),
+chosen by the oracle alone; or (c) the ReLU-free twin of ResNet-20 (same
+convolutions, BN and residual adds, no decisions at all), which carries the
+full-size and multi-step gradient checks.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import lppref as R
+from oracle import models as OM
+from paper_2203_06638_amd import lpp
+from paper_2203_06638_amd import models as PM
+from tests import parity as T
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    torch.cuda.init()
+
+
+def dev(img, lab):
+    return (torch.from_numpy(np.ascontiguousarray(img)).cuda(),
+            torch.from_numpy(np.ascontiguousarray(lab, np.int32)).cuda())
+
+
+def check_grads(o, got, ref, lo=0, hi=None, what="grad", scale=None):
+    errs = T.tensor_errors(o, got, ref, lo, hi, scale=scale)
+    worst = T.worst(errs)
+    say("  worst %s error %s %.3e" % (what, worst[0], worst[1]))
+    assert worst[1] < T.TOL_GRAD, (what, worst)
+
+
+# ---------------------------------------------------------------------------
+# single convolutions on exact-grid inputs: forward, data and weight gradient
+# ---------------------------------------------------------------------------
+
+CONV_CASES = [
+    # cin, c1, k, stride, pad, c2, hw, batch
+    (3, 16, 3, 1, 1, 16, 8, 3),       # padded 3-channel image, generic k path, ragged M
+    (16, 32, 3, 2, 1, 32, 9, 2),      # stride 2, odd size
+    (32, 64, 1, 2, 0, 64, 8, 5),      # 1x1 stride-2 projection
+    (3, 64, 7, 2, 3, 64, 20, 2),      # 7x7 stride-2 stem
+    (8, 8, 3, 1, 1, 8, 6, 4),         # cin % 16 != 0
+    (64, 128, 3, 1, 1, 128, 5, 3),    # wide channels
+    (16, 256, 3, 1, 1, 256, 16, 8),   # widest output tile
+    (16, 16, 3, 1, 1, 16, 32, 16),    # ResNet-20 stage-1 shape, many wgrad splits
+]
+
+
+def grid_conv_inputs(o, seed, n):
+    """Images and first-conv weights on exact grids (so the first conv's
+    output, the ReLU's input, is exact in any precision); the rest seeded
+    normally."""
+    x = T.init_x(o.specs, seed)
+    rec = o.layers[0]
+    nw = rec["cout"] * rec["cin"] * rec["k"] ** 2
+    x[:nw] = synth.grid_values(seed, nw, 2.0 ** -5, 0.5)
+    img = synth.grid_values(seed + 1, (n,) + o.in_shape, 2.0 ** -6, 4.0)
+    lab = synth.labels(seed, n, o.n_classes)
+    return x, img, lab
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_conv_passes(case):
+    cin, c1, k, st, pad, c2, hw, n = case
+    say("conv case", case)
+    o, p = T.twin_conv_net(cin, c1, k, st, pad, c2, hw)
+    x, img, lab = grid_conv_inputs(o, 11, n)
+    loss, logits, _ = R.forward_backward(o, x, img, lab)
+    g, sc = R.grad_scale(o, x, img, lab)
+    with lpp.Context(p, K=1, batch=n) as ctx:
+        ctx.set_params(x)
+        ctx.step(0, *dev(img, lab), 0, 0.0)
+        ref0 = R.activation(o, x, img, 0)
+        assert np.array_equal(ctx.get_activation(0, 0, ref0.shape[1:]), ref0)   # exact by construction
+        ref2 = R.activation(o, x, img, 2)
+        assert T.relerr(ctx.get_activation(0, 2, ref2.shape[1:]), ref2, T.TAU_LOGITS) < T.TOL_LOGITS
+        assert T.relerr(ctx.get_logits(0), logits, T.TAU_LOGITS) < T.TOL_LOGITS
+        assert abs(ctx.get_loss(0) - loss) < 1e-5 * max(1.0, abs(loss))
+        check_grads(o, ctx.get_grad(0), g, scale=sc)
+        assert np.array_equal(ctx.get_params(0), x)   # lr = 0 leaves the replica bitwise unchanged
+
+
+def test_maxpool_routing_exact_grid():
+    """Exact-grid conv -> max pool 3x3/2 -> conv -> pool -> linear: the
+    argmax decisions are taken on identical values on both sides (no ties,
+    checked by the oracle), so the routed gradients must agree."""
+    o = OM.Net("poolnet", 3, 15, 15, 7)
+    a = o.maxpool(o.conv(-1, 3, 8, 3, 1, 1), 3, 2, 1)
+    a = o.gap(o.conv(a, 8, 16, 3, 1, 1))
+    o.next_unit()
+    o.linear(a, 16, 7)
+    o.set_blocks([1, 2])
+    p = PM.Model("poolnet", (3, 15, 15), 7)
+    y = p.maxpool(p.conv(-1, 8, 3), 3, 2, 1)
+    y = p.gap(p.conv(y, 16, 3))
+    p.new_unit()
+    p.linear(y, 7)
+    p.assign_blocks([1, 2])
+    seed, margin = T.well_posed_seed(o, lambda s: grid_conv_inputs(o, s, 4)[:2], band=0.0)
+    x, img, lab = grid_conv_inputs(o, seed, 4)
+    loss, logits, _ = R.forward_backward(o, x, img, lab)
+    g, sc = R.grad_scale(o, x, img, lab)
+    with lpp.Context(p, K=1, batch=4) as ctx:
+        ctx.set_params(x)
+        ctx.step(0, *dev(img, lab), 0, 0.0)
+        ref1 = R.activation(o, x, img, 1)
+        assert np.array_equal(ctx.get_activation(0, 1, ref1.shape[1:]), ref1)
+        assert T.relerr(ctx.get_logits(0), logits, T.TAU_LOGITS) < T.TOL_LOGITS
+        check_grads(o, ctx.get_grad(0), g, scale=sc)
+
+
+def test_bn_residual_passes():
+    o, p = T.twin_bn_net(16, 16, 8)
+    make = lambda s: (T.init_x(o.specs, s, perturb=0.2), T.inputs(s + 1, 6, o.in_shape, o.n_classes)[0])
+    seed, margin = T.well_posed_seed(o, make)
+    x, img = make(seed)
+    lab = T.inputs(seed + 1, 6, o.in_shape, o.n_classes)[1]
+    g, sc = R.grad_scale(o, x, img, lab)
+    with lpp.Context(p, K=1, batch=6) as ctx:
+        ctx.set_params(x)
+        ctx.step(0, *dev(img, lab), 0, 0.0)
+        T.assert_decisions_match(o, ctx, 0, x, img)
+        for layer in range(len(o.layers)):
+            ref = R.activation(o, x, img, layer)
+            got = ctx.get_activation(0, layer, ref.shape[1:])
+            assert T.relerr(got, ref, T.TAU_LOGITS) < T.TOL_LOGITS, ("activation", layer)
+        check_grads(o, ctx.get_grad(0), g, scale=sc)
+
+
+# ---------------------------------------------------------------------------
+# the workloads' models
+# ---------------------------------------------------------------------------
+
+def test_tiny_cnn_ten_steps():
+    """Tiny CNN, batch 8, P = 2, K = 1, lr 0.1, plain SGD: step s runs worker
+    s mod 2 on partition s mod 2 + 1.  Every step is checked teacher-forced
+    (both sides start from the oracle's parameters) and the free-running
+    run at the end; the seed is one whose whole oracle trajectory stays
+    clear of ReLU kinks."""
+    o, p = OM.tiny_p2(), PM.tiny_cnn()
+
+    band = 8e-7   # ~2.7x the deviation measured at its ReLU inputs (3e-7; two shallow convs)
+
+    def trajectory(seed):
+        x = T.init_x(o.specs, seed).astype(np.float64)
+        margins, xs, bs = [], [], []
+        for s in range(10):
+            img, lab = T.inputs(seed * 100 + s, 8, o.in_shape, 10)
+            margins.append(R.kink_margin(o, x, img))
+            if margins[-1] <= band:
+                break
+            xs.append(x.copy())
+            bs.append((img, lab))
+            R.step(o, x, None, img, lab, s % 2 + 1, 0.1)
+        return min(margins), xs, bs, x
+
+    # margins this wide over all ten steps are rare (about 1 seed in 3000)
+    seed = next(s for s in range(300, 3000) if trajectory(s)[0] > band)
+    margin, xs, batches, _ = trajectory(seed)
+    say("tiny seed", seed, "margin %.2e" % margin)
+    with lpp.Context(p, K=1, batch=8) as ctx, lpp.Context(p, K=1, batch=8) as free:
+        x0 = xs[0].astype(np.float32)
+        free.set_params(x0)
+        xfree = x0.astype(np.float64)
+        for s in range(10):
+            w, part = s % 2, s % 2 + 1
+            img, lab = batches[s]
+            xin = xs[s].astype(np.float32)
+            ctx.set_params(xin)
+            xr = xin.astype(np.float64)
+            _, sc = R.grad_scale(o, xr, img, lab)
+            g, loss, logits = R.step(o, xr, None, img, lab, part, 0.1)
+            ti, tl = dev(img, lab)
+            ctx.step(w, ti, tl, part, 0.1)
+            T.assert_decisions_match(o, ctx, w, xin, img, band)
+            free.step(w, ti, tl, part, 0.1)
+            R.step(o, xfree, None, img, lab, part, 0.1)
+            assert T.relerr(ctx.get_logits(w), logits, T.TAU_LOGITS) < T.TOL_LOGITS
+            lo, hi = o.block_range(part)
+            check_grads(o, ctx.get_grad(w), g, lo, hi, scale=sc)
+            errs = T.tensor_errors(o, ctx.get_params(0), xr)
+            assert max(errs.values()) < T.TOL_PARAM, (s, T.worst(errs))
+        assert free.counter(0) == 10
+        errs = T.tensor_errors(o, free.get_params(0), xfree)
+        assert max(errs.values()) < T.TOL_PARAM, T.worst(errs)
+
+
+def _partition_step(o, p, x, m0, img, lab, partition, lr=0.1, mu=0.9, band=None):
+    xr = x.astype(np.float64)
+    mr = m0.astype(np.float64)
+    _, sc = R.grad_scale(o, xr, img, lab)
+    g, loss, logits = R.step(o, xr, mr, img, lab, partition, lr, mu)
+    n = img.shape[0]
+    with lpp.Context(p, K=1, batch=n, momentum=mu) as ctx:
+        ctx.set_params(x)
+        w = max(partition - 1, 0)
+        ctx.set_momentum(w, m0)
+        ctx.step(w, *dev(img, lab), partition, lr)
+        if band is not None:
+            T.assert_decisions_match(o, ctx, w, x, img, band)
+        assert T.relerr(ctx.get_logits(w), logits, T.TAU_LOGITS) < T.TOL_LOGITS
+        lo, hi = o.block_range(partition)
+        check_grads(o, ctx.get_grad(w), g, lo, hi, scale=sc)
+        check_grads(o, ctx.get_momentum(w), mr, lo, hi, "momentum", scale=sc)
+        got = ctx.get_params(0)
+        errs = T.tensor_errors(o, got, xr)
+        assert max(errs.values()) < T.TOL_PARAM, T.worst(errs)
+        # outside the block nothing moved, bit for bit
+        assert np.array_equal(got[:lo], x[:lo]) and np.array_equal(got[hi:], x[hi:])
+        gm = ctx.get_momentum(w)
+        assert np.array_equal(gm[:lo], m0[:lo]) and np.array_equal(gm[hi:], m0[hi:])
+
+
+def test_resnet20_forward_small_batches():
+    """ResNet-20 with ReLUs: logits and every activation at batch 2 and 16
+    (the forward pass is continuous, so it is compared at any size).  Its
+    gradients are compared on the ReLU-free twin: with ~1e5 ReLU inputs per
+    image no input keeps a margin above the ~3e-6 fp32/fp64 pre-activation
+    disagreement, so both mask decisions are valid somewhere."""
+    o, p = OM.resnet20_p4(), PM.resnet20()
+    shapes = R.shapes(o)
+    for n in (2, 16):
+        x = T.init_x(o.specs, 47 + n)
+        img, lab = T.inputs(48 + n, n, o.in_shape, 10)
+        _, logits, _ = R.forward_backward(o, x, img, lab, grad=False)
+        with lpp.Context(p, K=1, batch=n) as ctx:
+            ctx.set_params(x)
+            ctx.step(0, *dev(img, lab), 0, 0.0)
+            assert T.relerr(ctx.get_logits(0), logits, T.TAU_LOGITS) < T.TOL_LOGITS
+            # intermediate activations (no bar is set for them; batch-norm over
+            # as few as 128 values per channel amplifies fp32 noise): 1e-3
+            for layer in range(0, len(o.layers), 3):
+                ref = R.activation(o, x, img, layer)
+                got = ctx.get_activation(0, layer, shapes[layer])
+                assert T.relerr(got, ref, T.TAU_LOGITS) < 1e-3, (n, layer)
+
+
+@pytest.mark.parametrize("partition", [0, 1, 2, 3, 4])
+def test_resnet20_relu_free_partition_step_batch16(partition):
+    o, p = OM.resnet20_p4(relu=False), PM.resnet20(act=False)
+    x = T.init_x(o.specs, 41)
+    img, lab = T.inputs(42, 16, o.in_shape, 10)
+    m0 = (np.random.default_rng(1).standard_normal(o.d) * 1e-2).astype(np.float32)
+    _partition_step(o, p, x, m0, img, lab, partition)
+
+
+def test_resnet20_activation_grads_layer_by_layer():
+    """Gradient w.r.t. every layer output of the ReLU-free ResNet-20 at
+    batch 16 (full backward), walked from the logits towards the image."""
+    o, p = OM.resnet20_p4(relu=False), PM.resnet20(act=False)
+    x = T.init_x(o.specs, 45)
+    img, lab = T.inputs(46, 16, o.in_shape, 10)
+    shapes = R.shapes(o)
+    bad = []
+    with lpp.Context(p, K=1, batch=16) as ctx:
+        ctx.set_params(x)
+        ctx.step(0, *dev(img, lab), 0, 0.0)
+        for layer in range(len(o.layers) - 1, 0, -1):
+            ref = R.activation_grad(o, x, img, lab, layer)
+            got = ctx.get_activation_grad(0, layer, shapes[layer])
+            e = T.relerr(got, ref, T.TAU_LOGITS)
+            if e > 1e-4:
+                bad.append((layer, e))
+    assert not bad, bad[:5]
+
+
+def test_partial_gradient_is_restricted_full_gradient_bitwise():
+    """Sec. 2/3: the block gradient is the restriction of the full gradient;
+    the truncated backward must reproduce it bit for bit."""
+    p = PM.resnet20()
+    o = OM.resnet20_p4()
+    x = T.init_x(o.specs, 51)
+    img, lab = T.inputs(52, 16, o.in_shape, 10)
+    with lpp.Context(p, K=1, batch=16) as ctx:
+        ctx.set_params(x)
+        ti, tl = dev(img, lab)
+        ctx.step(0, ti, tl, 0, 0.0)
+        full = ctx.get_grad(0)
+        for part in range(1, 5):
+            ctx.step(part - 1, ti, tl, part, 0.0)
+            g = ctx.get_grad(part - 1)
+            lo, hi = o.block_range(part)
+            assert np.array_equal(g[lo:hi], full[lo:hi]), part
+            assert not np.any(g[:lo]) and not np.any(g[hi:])
+
+
+def test_sequential_runs_are_bitwise_reproducible():
+    p = PM.resnet20()
+    x = T.init_x(p.specs, 61)
+    batches = [dev(*T.inputs(62 + s, 8, p.in_shape, 10)) for s in range(6)]
+    outs = []
+    for _ in range(2):
+        with lpp.Context(p, K=1, batch=8, momentum=0.9) as ctx:
+            ctx.set_params(x)
+            for s in range(6):
+                ctx.step(s % 4, *batches[s], s % 4 + 1, 0.1)
+            outs.append(ctx.get_params(0))
+    assert np.array_equal(outs[0], outs[1])
+
+
+def test_averaging_matches_oracle_and_invariants():
+    p = PM.resnet20(100)
+    o = OM.resnet20_p4(100)
+    rng = np.random.default_rng(7)
+    reps = [(rng.standard_normal(o.d)).astype(np.float32) for _ in range(4)]
+    with lpp.Context(p, K=4, batch=2) as ctx:
+        for q in range(4):
+            ctx.set_params(reps[q], q)
+        ctx.average()
+        ref = [r.astype(np.float64) for r in reps]
+        R.average(ref)
+        mean0 = np.mean([r.astype(np.float64) for r in reps], axis=0)
+        eps = 2.0 ** -24
+        mag = np.sum([np.abs(r.astype(np.float64)) for r in reps], axis=0)
+        for q in range(4):
+            got = ctx.get_params(q)
+            bound = 4 * eps * (mag + 2 * np.abs(reps[q].astype(np.float64)))
+            assert np.all(np.abs(got - ref[q]) <= bound)
+            assert np.all(np.abs(got - mean0) <= bound)
+        # subset averaging leaves the others untouched
+        before = [ctx.get_params(q) for q in range(4)]
+        ctx.set_params(reps[0], 0)
+        ctx.average([0, 2])
+        assert np.array_equal(ctx.get_params(1), before[1])
+        assert np.array_equal(ctx.get_params(3), before[3])
+    with lpp.Context(p, K=1, batch=2) as one:
+        one.set_params(reps[0])
+        one.average()
+        assert np.array_equal(one.get_params(0), reps[0])   # K = 1 is a no-op
+
+
+def test_resnet20_100_replicas_sequential_schedule():
+    """ResNet-20 (100 classes) shapes, K = 4 replicas x P = 4 workers,
+    momentum 0.9, averaging when every replica's counter has advanced by
+    H = 2; batch 4, 16 updates, compared with the oracle's sequential
+    schedule.  ReLU-free twin, so the 16-step trajectory is well posed."""
+    o, p = OM.resnet20_p4(100, relu=False), PM.resnet20(100, act=False)
+    K, P, H = 4, 4, 2
+    x0 = T.init_x(o.specs, 71)
+    sched = []
+    batches = {}
+    for rnd in range(4):
+        for q in range(K):
+            w = q * P + rnd % P
+            key = len(sched)
+            batches[key] = T.inputs(200 + key, 4, o.in_shape, 100)
+            sched.append((w, w % P + 1, key))
+    reps, moms, _ = R.run_sequential(o, x0.astype(np.float64), sched, batches, K, P, H, 0.05, 0.9)
+    with lpp.Context(p, K=K, batch=4, momentum=0.9) as ctx:
+        ctx.set_params(x0)
+        s_pre = 0
+        for (w, part, key) in sched:
+            ctx.step(w, *dev(*batches[key]), part, 0.05)
+            c = min(ctx.counter(q) for q in range(K))
+            if c - s_pre >= H:
+                s_pre = c
+                ctx.average()
+        assert [ctx.counter(q) for q in range(K)] == [4] * K
+        for q in range(K):
+            errs = T.tensor_errors(o, ctx.get_params(q), reps[q])
+            assert max(errs.values()) < T.TOL_PARAM, (q, T.worst(errs))
+
+
+# ---------------------------------------------------------------------------
+# the headline workload's full size (batch 128, momentum 0.9)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("partition", [1, 4])
+def test_full_size_relu_free_resnet20_gradients(partition):
+    o, p = OM.resnet20_p4(relu=False), PM.resnet20(act=False)
+    x = T.init_x(o.specs, 81)
+    img, lab = T.inputs(82, 128, o.in_shape, 10)
+    m0 = np.zeros(o.d, np.float32)
+    _partition_step(o, p, x, m0, img, lab, partition)
+
+
+def test_full_size_resnet20_forward_and_gradient_invariants():
+    """ResNet-20 with ReLUs at batch 128: logits and loss against the oracle
+    (the forward pass is continuous), and properties of the GPU's own
+    gradient that hold at any size: training-mode BN makes the loss
+    invariant to scaling the filters of the conv that feeds it, so
+    sum(W * dL/dW) over each such filter is 0; the partial gradient is the
+    full one restricted, bit for bit."""
+    o, p = OM.resnet20_p4(), PM.resnet20()
+    x = T.init_x(o.specs, 83)
+    img, lab = T.inputs(84, 128, o.in_shape, 10)
+    loss, logits, _ = R.forward_backward(o, x, img, lab, grad=False)
+    with lpp.Context(p, K=1, batch=128, momentum=0.9) as ctx:
+        ctx.set_params(x)
+        ti, tl = dev(img, lab)
+        ctx.step(0, ti, tl, 0, 0.0)
+        assert T.relerr(ctx.get_logits(0), logits, T.TAU_LOGITS) < T.TOL_LOGITS
+        assert abs(ctx.get_loss(0) - loss) < 1e-5 * abs(loss)
+        g = ctx.get_grad(0)
+        gd = g.astype(np.float64)
+        for li, rec in enumerate(o.layers):
+            if rec["op"] != OM.CONV:
+                continue
+            consumers = [r for r in o.layers if r["in0"] == li or r["in1"] == li]
+            if not (len(consumers) == 1 and consumers[0]["op"] == OM.BN):
+                continue
+            n = rec["cout"] * rec["cin"] * rec["k"] ** 2
+            w = x[rec["poff"]:rec["poff"] + n].reshape(rec["cout"], -1).astype(np.float64)
+            gw = gd[rec["poff"]:rec["poff"] + n].reshape(rec["cout"], -1)
+            dd = np.abs((w * gw).sum(axis=1))
+            scale = (np.abs(w) * np.abs(gw)).sum(axis=1)
+            assert np.all(dd <= 1e-3 * scale + 1e-12), (li, float((dd / np.maximum(scale, 1e-30)).max()))
+        for part in range(1, 5):
+            w = part - 1
+            ctx.step(w, ti, tl, part, 0.0)
+            gp = ctx.get_grad(w)
+            lo, hi = o.block_range(part)
+            assert np.array_equal(gp[lo:hi], g[lo:hi]), part
+
+
+# ---------------------------------------------------------------------------
+# the streaming kernels on their own, at ragged sizes
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n", [1, 7, 4096, 1_000_003])
+def test_kernel_sgd_update(n):
+    rng = np.random.default_rng(n)
+    x, m, g = (rng.standard_normal(n).astype(np.float32) for _ in range(3))
+    tx, tm, tg = (torch.from_numpy(a).cuda() for a in (x, m, g))
+    lpp.kernel_sgd_update(tx, tm, tg, 0.05, 0.9, 1e-4)
+    torch.cuda.synchronize()
+    xd, md, gd = (a.astype(np.float64) for a in (x, m, g))
+    mr = 0.9 * md + gd + 1e-4 * xd
+    xr = xd - 0.05 * mr
+    # fp32 evaluation of the same expressions: a few ulps of the operands
+    eps = 2.0 ** -24
+    mb = 4 * eps * (np.abs(0.9 * md) + np.abs(gd) + np.abs(1e-4 * xd))
+    assert np.all(np.abs(tm.cpu().numpy() - mr) <= mb)
+    xb = 4 * eps * (np.abs(xd) + np.abs(0.05 * mr)) + 0.05 * mb
+    assert np.all(np.abs(tx.cpu().numpy() - xr) <= xb)
+
+
+@pytest.mark.parametrize("k,n", [(2, 5), (3, 1001), (4, 1 << 20)])
+def test_kernel_average(k, n):
+    rng = np.random.default_rng(k * n)
+    reps = [rng.standard_normal(n).astype(np.float32) for _ in range(k)]
+    ts = [torch.from_numpy(r).cuda() for r in reps]
+    lpp.kernel_average(ts)
+    torch.cuda.synchronize()
+    ref = [r.astype(np.float64) for r in reps]
+    R.average(ref)
+    eps = 2.0 ** -24
+    mag = np.sum([np.abs(r.astype(np.float64)) for r in reps], axis=0) / k
+    for t, r0, r in zip(ts, reps, ref):
+        bound = 4 * eps * (k * mag + 2 * np.abs(r0.astype(np.float64)))
+        assert np.all(np.abs(t.cpu().numpy() - r) <= bound)
+
+
+# ---------------------------------------------------------------------------
+# asynchronous mode: no unique answer; check it trains and stays finite
+# ---------------------------------------------------------------------------
+
+def test_async_hogwild_training_smoke():
+    """P = 4 workers on their own streams update one ResNet-20 replica
+    without locks (Alg. 1).  On a fixed pool of 4 batches the loss must fall
+    and every block must move."""
+    p = PM.resnet20()
+    x = T.init_x(p.specs, 91)
+    pool = [dev(*T.inputs(92 + b, 32, p.in_shape, 10)) for b in range(4)]
+    with lpp.Context(p, K=1, batch=32, mode=lpp.ASYNC, momentum=0.9) as ctx:
+        ctx.set_params(x)
+        for w in range(4):
+            ctx.step(w, *pool[w], 0, 0.0)
+        ctx.sync()
+        first = np.mean([ctx.get_loss(w) for w in range(4)])
+        for s in range(120):
+            w = s % 4
+            ctx.step(w, *pool[(s // 4) % 4], w + 1, 0.05)
+        ctx.sync()
+        for w in range(4):
+            ctx.step(w, *pool[w], 0, 0.0)
+        ctx.sync()
+        last = np.mean([ctx.get_loss(w) for w in range(4)])
+        xn = ctx.get_params(0)
+        assert np.all(np.isfinite(xn))
+        say("async loss", first, "->", last)
+        assert last < first
+        for i in range(1, 5):
+            lo, hi = ctx.block_range(i)
+            assert not np.array_equal(xn[lo:hi], x[lo:hi])
+        assert ctx.counter(0) == 128

@@ -1,0 +1,105 @@
+"""Host-side checks of liblpp.so that need no GPU: it loads, exports every
+symbol include/lpp.h declares, validates model descriptions, and its block
+layout / flop accounting agree with the oracle's model lists and the paper's
+bound on partial backpropagation."""
+import os
+import re
+
+import pytest
+
+from oracle import models as OM
+from paper_2203_06638_amd import lpp
+from paper_2203_06638_amd import models as PM
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+PAIRS = [
+    ("tiny", PM.tiny_cnn, OM.tiny_p2),
+    ("resnet20", PM.resnet20, OM.resnet20_p4),
+    ("resnet20_100", lambda: PM.resnet20(100), lambda: OM.resnet20_p4(100)),
+    ("wrn16_8", PM.wrn16_8, OM.wrn16_8_p4),
+    ("resnet18", PM.resnet18, OM.resnet18_p4),
+]
+
+
+def test_library_exports_every_declared_function():
+    hdr = open(os.path.join(ROOT, "include", "lpp.h")).read()
+    names = sorted(set(re.findall(r"^\s*(?:int|long|const char\*)\s+(lpp_\w+)\s*\(", hdr, re.M)))
+    assert len(names) >= 20
+    L = lpp.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+@pytest.mark.parametrize("name,prod,ref", PAIRS)
+def test_layout_matches_oracle_models(name, prod, ref):
+    p, o = prod(), ref()
+    info = lpp.describe(p, 4)
+    assert info.d == o.d == p.d
+    assert p.specs == o.specs
+    assert p.P == o.P
+    for i in range(o.P + 1):
+        assert (info.block_lo[i], info.block_hi[i]) == o.block_range(i)
+    # layer lists agree field by field (op, inputs, geometry, bias)
+    assert len(p.layers) == len(o.layers)
+    for a, b in zip(p.layers, o.layers):
+        assert tuple(a[:9]) == (b["op"], b["in0"], b["in1"], b["cin"], b["cout"], b["k"], b["stride"], b["pad"],
+                                b["bias"]) or (a[0] in (lpp.RELU, lpp.ADD, lpp.GAP, lpp.MAXPOOL) and
+                                               a[0] == b["op"] and a[1] == b["in0"] and a[2] == b["in1"])
+
+
+def test_flops_and_partial_backprop_bound():
+    """ResNet-20 at batch 128: 10.45 GFLOP forward; the mean truncated
+    backward over the P own-block partitions costs at most (P+1)/(2P) of the
+    full backward (the paper's saving of F(c-1)/2 flops over c concurrent
+    partial steps, Sec. 3 'Discussion on the Rule')."""
+    for prod in (PM.resnet20, PM.wrn16_8, PM.resnet18):
+        m = prod()
+        info = lpp.describe(m, 128)
+        full = info.bwd_flops[0]
+        mean_partial = sum(info.bwd_flops[i] for i in range(1, m.P + 1)) / m.P
+        assert mean_partial <= (m.P + 1) / (2 * m.P) * full
+        # the deepest block needs the least backward work
+        assert info.bwd_flops[m.P] == min(info.bwd_flops[i] for i in range(1, m.P + 1))
+    info = lpp.describe(PM.resnet20(), 128)
+    assert abs(info.fwd_flops / 1e9 - 10.45) < 0.01
+    # full backward = dgrad + wgrad of every conv/linear but the stem's dgrad
+    m = PM.resnet20()
+    stem_macs = 128 * 32 * 32 * 16 * 3 * 9
+    assert abs(info.bwd_flops[0] - (2 * info.fwd_flops - 2 * stem_macs)) < 1.0
+
+
+def _desc_err(model, P=None, **kw):
+    with pytest.raises(lpp.LppError) as e:
+        info = lpp.ModelInfo()
+        desc = lpp.make_desc(model, 4, **kw)
+        lpp._check(lpp.lib().lpp_describe(lpp.C.byref(desc), P or model.P, lpp.C.byref(info)))
+    return e.value.code
+
+
+def test_describe_rejects_bad_models():
+    m = PM.resnet20()
+    m.layers[3][9] = 4   # block ids must not decrease along parameter order
+    assert _desc_err(m) == -1
+    m = PM.resnet20()
+    assert _desc_err(m, P=5) == -1          # block 5 owns nothing
+    m = PM.tiny_cnn()
+    m.layers[2][3] = 4   # cin mismatch
+    assert _desc_err(m) == -1
+    m = PM.tiny_cnn()
+    m.layers[0][1] = 3   # forward reference
+    assert _desc_err(m) == -1
+    m = PM.tiny_cnn()
+    assert _desc_err(m, bn_eps=0.0) == -1
+    m = PM.tiny_cnn()
+    m.layers[-1][4] = 11  # logits != n_classes
+    assert _desc_err(m) == -1
+    m = PM.tiny_cnn()
+    assert _desc_err(m, dtype=7) == -1
+
+
+def test_describe_accepts_ragged_shapes():
+    """Odd spatial sizes, a 7x7/2 stem and stride-2 units are valid."""
+    m = PM.resnet_imagenet((1, 1), (8, 16), n_classes=5, hw=23, blocks=[1, 1, 2, 2])
+    info = lpp.describe(m, 3)
+    assert info.d == m.d and info.P == 2
