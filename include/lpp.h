@@ -96,6 +96,14 @@ typedef struct {
                                      library creates its own streams (default
                                      priority)                                  */
     void* avg_stream;             /* hipStream_t or NULL (library-created)      */
+    int unfused;                  /* 0: fused kernels (default); 1: one kernel
+                                     sequence per layer, every layer output kept
+                                     (for lpp_get_activation on any layer)     */
+    int no_graphs;                /* 0: each (worker, partition) step is captured
+                                     once into a HIP graph and replayed
+                                     (default); 1: kernels launched one by one.
+                                     Steps run with a kernel timer enabled are
+                                     always launched one by one.               */
 } lpp_options;
 
 typedef struct {
@@ -180,7 +188,9 @@ int lpp_get_loss(lpp_ctx* ctx, int worker, float* loss);
 int lpp_get_logits(lpp_ctx* ctx, int worker, float* host, long n);
 
 /* Forward activation of `layer` from the worker's last step, as float32 NCHW
- * [batch][c][h][w] (n floats).  For checking a run layer by layer. */
+ * [batch][c][h][w] (n floats).  For checking a run layer by layer; with
+ * fused kernels only the outputs of convolutions and of each fused group are
+ * kept (LPP_ESTATE otherwise). */
 int lpp_get_activation(lpp_ctx* ctx, int worker, int layer, float* host, long n);
 
 /* Gradient of the loss with respect to the output of `layer` from the

@@ -59,10 +59,14 @@ __device__ __forceinline__ int src_pixel(int n, int p, int q, int r, int s, cons
 
 // WM waves along m (4/WM along n); each wave owns TM x TN tiles of 16x16.
 // FAST: Cs % 16 == 0, so a group of four float4 chunks never straddles a tap.
-template <int MODE, int WM, int TM, int TN, bool FAST>
+// STATS: also write, per output channel, the mean and the sum of squared
+// deviations from it over this workgroup's BM output rows (the batch-norm
+// statistics of the output, one partial per row tile).
+template <int MODE, int WM, int TM, int TN, bool FAST, bool STATS>
 __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                       const float* __restrict__ bias, float* __restrict__ Y,
-                                                      ConvGeom g, int accumulate) {
+                                                      ConvGeom g, int accumulate, float* __restrict__ pmean,
+                                                      float* __restrict__ pm2) {
     constexpr int WN = 4 / WM;
     constexpr int BM = WM * TM * 16, BN = WN * TN * 16;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -156,55 +160,139 @@ __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ 
     }
 
 #pragma unroll
-    for (int x = 0; x < TM; ++x)
+    for (int y = 0; y < TN; ++y) {
+        const int n = n_base + y * 16 + li;
+        const float bb = (bias && n < g.Ncols) ? bias[n] : 0.f;
 #pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            const int n = n_base + y * 16 + li;
-            if (n >= g.Ncols) continue;
-            const float bb = bias ? bias[n] : 0.f;
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[x][y][i] += bb;
+        if (n >= g.Ncols) continue;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int m = m_base + x * 16 + gi * 4 + i;
                 if (m >= M) continue;
                 const long o = (long)m * g.Ncols + n;
-                float v = acc[x][y][i] + bb;
+                const float v = acc[x][y][i];
                 Y[o] = accumulate ? Y[o] + v : v;
             }
+    }
+    if (STATS) {
+        // two passes over the tile held in registers: the mean, then the sum
+        // of squared deviations from it; lanes of a wave are combined with
+        // xor shuffles over the row-group bits, waves through LDS, all in a
+        // fixed order
+        __shared__ float red[WM][BN];
+        __shared__ float tile_mean[BN];
+        const int rows = min(BM, M - (int)blockIdx.x * BM);
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            float sacc = 0.f;
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (m_base + x * 16 + gi * 4 + i < M) sacc += acc[x][y][i];
+            sacc += __shfl_xor(sacc, 16);
+            sacc += __shfl_xor(sacc, 32);
+            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = sacc;
         }
+        __syncthreads();
+        if (threadIdx.x < BN) {
+            float t = 0.f;
+            for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
+            tile_mean[threadIdx.x] = t / (float)rows;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            const float mu = tile_mean[wn * TN * 16 + y * 16 + li];
+            float q = 0.f;
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (m_base + x * 16 + gi * 4 + i < M) {
+                        const float dv = acc[x][y][i] - mu;
+                        q += dv * dv;
+                    }
+            q += __shfl_xor(q, 16);
+            q += __shfl_xor(q, 32);
+            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = q;
+        }
+        __syncthreads();
+        if (threadIdx.x < BN) {
+            const int n = blockIdx.y * BN + threadIdx.x;
+            if (n < g.Ncols) {
+                float t = 0.f;
+                for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
+                pmean[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
+                pm2[(long)blockIdx.x * g.Ncols + n] = t;
+            }
+        }
+    }
 }
 
 template <int MODE, int WM, int TM, int TN>
 static hipError_t launch_cfg(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                             bool acc, hipStream_t st) {
+                             bool acc, float* pmean, float* pm2, hipStream_t st) {
     constexpr int BM = WM * TM * 16, BN = (4 / WM) * TN * 16;
     const long M = (long)g.Nb * g.Ho * g.Wo;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
-    if (g.Cs % 16 == 0)
-        hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true>), grid, dim3(256), 0, st, src, B, bias, Y, g,
-                           (int)acc);
-    else
-        hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false>), grid, dim3(256), 0, st, src, B, bias, Y, g,
-                           (int)acc);
+    const bool fast = g.Cs % 16 == 0;
+    if (pmean) {
+        if (fast)
+            hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true, true>), grid, dim3(256), 0, st, src, B, bias,
+                               Y, g, (int)acc, pmean, pm2);
+        else
+            hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false, true>), grid, dim3(256), 0, st, src, B, bias,
+                               Y, g, (int)acc, pmean, pm2);
+    } else {
+        if (fast)
+            hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true, false>), grid, dim3(256), 0, st, src, B, bias,
+                               Y, g, (int)acc, pmean, pm2);
+        else
+            hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false, false>), grid, dim3(256), 0, st, src, B, bias,
+                               Y, g, (int)acc, pmean, pm2);
+    }
     return hipGetLastError();
+}
+
+// Tile configuration for a pass: (WM, TM, TN) by output width and rows.
+struct ConvCfg { int wm, tm, tn; };
+static ConvCfg pick_cfg(const ConvGeom& g) {
+    const long M = (long)g.Nb * g.Ho * g.Wo;
+    if (g.Ncols <= 16) return {4, 2, 1};
+    if (g.Ncols <= 32) return {4, 2, 2};
+    if (g.Ncols <= 64 || M < 64L * 512) {
+        if (M >= 64L * 512) return {2, 2, 2};
+        return {2, 1, 2};
+    }
+    return {2, 2, 4};
+}
+
+int conv_tile_rows(const ConvGeom& g) {
+    ConvCfg c = pick_cfg(g);
+    return c.wm * c.tm * 16;
 }
 
 template <int MODE>
 static hipError_t launch_mode(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              bool acc, hipStream_t st) {
-    const long M = (long)g.Nb * g.Ho * g.Wo;
-    if (g.Ncols <= 16) return launch_cfg<MODE, 4, 2, 1>(src, B, bias, Y, g, acc, st);
-    if (g.Ncols <= 32) return launch_cfg<MODE, 4, 2, 2>(src, B, bias, Y, g, acc, st);
-    if (g.Ncols <= 64 || M < 64L * 512) {
-        if (M >= 64L * 512) return launch_cfg<MODE, 2, 2, 2>(src, B, bias, Y, g, acc, st);
-        return launch_cfg<MODE, 2, 1, 2>(src, B, bias, Y, g, acc, st);
-    }
-    return launch_cfg<MODE, 2, 2, 4>(src, B, bias, Y, g, acc, st);
+                              bool acc, float* pmean, float* pm2, hipStream_t st) {
+    ConvCfg c = pick_cfg(g);
+    if (c.wm == 4 && c.tn == 1) return launch_cfg<MODE, 4, 2, 1>(src, B, bias, Y, g, acc, pmean, pm2, st);
+    if (c.wm == 4) return launch_cfg<MODE, 4, 2, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
+    if (c.tn == 4) return launch_cfg<MODE, 2, 2, 4>(src, B, bias, Y, g, acc, pmean, pm2, st);
+    if (c.tm == 2) return launch_cfg<MODE, 2, 2, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
+    return launch_cfg<MODE, 2, 1, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
 }
 
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, hipStream_t st) {
-    if (mode == CONV_FWD) return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, st);
-    return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, st);
+                             const ConvGeom& g, bool accumulate, float* pmean, float* pm2, hipStream_t st) {
+    if (mode == CONV_FWD) return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, pmean, pm2, st);
+    return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, nullptr, nullptr, st);
 }
 
 // ------------------------------------------------------------------------
@@ -219,6 +307,8 @@ template <int TM, int TN>
 __global__ __launch_bounds__(256) void conv_wgrad_f32(const float* __restrict__ dY, const float* __restrict__ X,
                                                       float* __restrict__ part, WgArgs a) {
     constexpr int BMw = TM * 16, BNw = TN * 16;
+    constexpr int NA = 64 * (BMw / 4) / 256;   // dY quads per thread per chunk
+    constexpr int NB = 64 * (BNw / 4) / 256;   // im2col quads per thread per chunk
     __shared__ float As[64][BMw + 4];
     __shared__ float Bs[64][BNw + 4];
     __shared__ float red[TM * TN * 4][64];
@@ -232,39 +322,60 @@ __global__ __launch_bounds__(256) void conv_wgrad_f32(const float* __restrict__ 
     const int p_begin = blockIdx.z * a.pix_per_split;
     const int p_end = min(M, p_begin + a.pix_per_split);
 
+    // each thread's column quad is the same in every chunk: decode it once
+    const int bcq = tid % (BNw / 4);
+    const int col = n0 + bcq * 4;
+    const bool col_ok = col < Ktot;
+    int br = 0, bs = 0, bc = 0;
+    if (col_ok) {
+        const int quad = col >> 2;
+        const int tap = quad / Cq;
+        bc = (quad - tap * Cq) * 4;
+        br = tap / a.S;
+        bs = tap - br * a.S;
+    }
+    const int acq = tid % (BMw / 4);
+    const int aco = m0 + acq * 4;
+
+    f4 ra[NA], rb[NB];
+    auto load = [&](int pc) {
+#pragma unroll
+        for (int k = 0; k < NA; ++k) {
+            const int px = (tid + 256 * k) / (BMw / 4);
+            const int p = pc + px;
+            ra[k] = (p < p_end && aco < a.Cout) ? *(const f4*)(dY + (long)p * a.Cout + aco) : f4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int k = 0; k < NB; ++k) {
+            const int px = (tid + 256 * k) / (BNw / 4);
+            const int p = pc + px;
+            f4 v = f4{0.f, 0.f, 0.f, 0.f};
+            if (p < p_end && col_ok) {
+                const int n = p / HoWo;
+                const int rem = p - n * HoWo;
+                const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
+                const int hi = ho * a.stride - a.pad + br, wi = wo * a.stride - a.pad + bs;
+                if (hi >= 0 && hi < a.Hi && wi >= 0 && wi < a.Wi)
+                    v = *(const f4*)(X + ((long)(n * a.Hi + hi) * a.Wi + wi) * a.Cin_p + bc);
+            }
+            rb[k] = v;
+        }
+    };
+
     f4 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
+    if (p_begin < p_end) load(p_begin);
     for (int pc = p_begin; pc < p_end; pc += 64) {
-        for (int idx = tid; idx < 64 * (BMw / 4); idx += 256) {
-            const int px = idx / (BMw / 4), cq = idx - px * (BMw / 4);
-            const int p = pc + px, co = m0 + cq * 4;
-            f4 v = f4{0.f, 0.f, 0.f, 0.f};
-            if (p < p_end && co < a.Cout) v = *(const f4*)(dY + (long)p * a.Cout + co);
-            *(f4*)&As[px][cq * 4] = v;
-        }
-        for (int idx = tid; idx < 64 * (BNw / 4); idx += 256) {
-            const int px = idx / (BNw / 4), cq = idx - px * (BNw / 4);
-            const int p = pc + px, col = n0 + cq * 4;
-            f4 v = f4{0.f, 0.f, 0.f, 0.f};
-            if (p < p_end && col < Ktot) {
-                const int quad = col >> 2;
-                const int tap = quad / Cq;
-                const int c = (quad - tap * Cq) * 4;
-                const int r = tap / a.S, s = tap - r * a.S;
-                const int n = p / HoWo;
-                const int rem = p - n * HoWo;
-                const int ho = rem / a.Wo, wo = rem - ho * a.Wo;
-                const int hi = ho * a.stride - a.pad + r, wi = wo * a.stride - a.pad + s;
-                if (hi >= 0 && hi < a.Hi && wi >= 0 && wi < a.Wi)
-                    v = *(const f4*)(X + ((long)(n * a.Hi + hi) * a.Wi + wi) * a.Cin_p + c);
-            }
-            *(f4*)&Bs[px][cq * 4] = v;
-        }
+#pragma unroll
+        for (int k = 0; k < NA; ++k) *(f4*)&As[(tid + 256 * k) / (BMw / 4)][acq * 4] = ra[k];
+#pragma unroll
+        for (int k = 0; k < NB; ++k) *(f4*)&Bs[(tid + 256 * k) / (BNw / 4)][bcq * 4] = rb[k];
         __syncthreads();
+        if (pc + 64 < p_end) load(pc + 64);   // next chunk in flight during this one's MFMAs
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int row = 16 * wave + 4 * j + gi;
@@ -302,12 +413,12 @@ __global__ __launch_bounds__(256) void conv_wgrad_f32(const float* __restrict__ 
         for (int x = 0; x < TM; ++x)
 #pragma unroll
             for (int y = 0; y < TN; ++y) {
-                const int col = n0 + y * 16 + li;
-                if (col >= Ktot) continue;
+                const int cc = n0 + y * 16 + li;
+                if (cc >= Ktot) continue;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int co = m0 + x * 16 + gi * 4 + i;
-                    if (co < a.Cout) out[(long)co * Ktot + col] = red[(x * TN + y) * 4 + i][lane];
+                    if (co < a.Cout) out[(long)co * Ktot + cc] = red[(x * TN + y) * 4 + i][lane];
                 }
             }
     }
@@ -318,8 +429,9 @@ WgradPlan wgrad_plan(int Cout, int Ktot, long M) {
     p.tm = Cout <= 16 ? 1 : (Cout <= 32 ? 2 : 4);
     p.tn = 4;
     const long tiles = (long)((Cout + 16 * p.tm - 1) / (16 * p.tm)) * ((Ktot + 16 * p.tn - 1) / (16 * p.tn));
-    long splits = (1024 + tiles - 1) / tiles;
-    const long max_splits = (M + 255) / 256;
+    // about 512 workgroups per pass, each over at least 512 output pixels
+    long splits = (512 + tiles - 1) / tiles;
+    const long max_splits = (M + 511) / 512;
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
     long pps = (M + splits - 1) / splits;
@@ -349,15 +461,25 @@ hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int N
     return launch_wg<4, 4>(dY, X, part, a, p, st);
 }
 
-__global__ void wgrad_reduce_kernel(const float* __restrict__ part, int splits, int Cout, int Ktot, int Cin,
-                                    int Cin_p, int R, int S, float* __restrict__ g) {
-    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (long)Cout * Ktot) return;
+// 64 outputs per workgroup; four lanes per output each sum a fixed,
+// interleaved subset of the splits, then the four are added in order.
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ part, int splits, int Cout,
+                                                           int Ktot, int Cin, int Cin_p, int R, int S,
+                                                           float* __restrict__ g) {
+    __shared__ float red[4][64];
+    const int j = threadIdx.x & 63, sl = threadIdx.x >> 6;
+    const long idx = (long)blockIdx.x * 64 + j;
+    const long total = (long)Cout * Ktot;
+    float s = 0.f;
+    if (idx < total)
+        for (int k = sl; k < splits; k += 4) s += part[(long)k * total + idx];
+    red[sl][j] = s;
+    __syncthreads();
+    if (sl != 0 || idx >= total) return;
+    s = ((red[0][j] + red[1][j]) + red[2][j]) + red[3][j];
     const int co = (int)(idx / Ktot), col = (int)(idx - (long)co * Ktot);
     const int tap = col / Cin_p, c = col - tap * Cin_p;
     if (c >= Cin) return;
-    float s = 0.f;
-    for (int k = 0; k < splits; ++k) s += part[(long)k * Cout * Ktot + idx];
     const int r = tap / S, q = tap - r * S;
     g[(((long)co * Cin + c) * R + r) * S + q] = s;
 }
@@ -365,7 +487,7 @@ __global__ void wgrad_reduce_kernel(const float* __restrict__ part, int splits, 
 hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
                                float* g, hipStream_t st) {
     const long n = (long)Cout * Ktot;
-    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, splits, Cout,
+    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, part, splits, Cout,
                        Ktot, Cin, Cin_p, R, S, g);
     return hipGetLastError();
 }

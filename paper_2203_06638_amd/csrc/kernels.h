@@ -19,51 +19,83 @@ struct ConvGeom {
 
 enum ConvMode { CONV_FWD = 0, CONV_DGRAD = 1 };
 
-// Y[m][n] (+)= sum_k A[m][k] B[n][k] (+ bias[n]); see ConvGeom.
+// Per-step arguments, read by the step's kernels from device memory so that
+// one captured graph serves every step of a worker on a partition.
+struct StepArgs {
+    const float* images;
+    const int* labels;
+    float lr;
+};
+hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* labels, float lr, hipStream_t st);
+
+// Y[m][n] (+)= sum_k A[m][k] B[n][k] (+ bias[n]); see ConvGeom.  Forward
+// passes with pmean/pm2 non-null also write per-row-tile batch-norm
+// statistics of Y (tile mean and sum of squared deviations, [T][Ncols],
+// T = ceil(M / conv_tile_rows(g))).
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, hipStream_t st);
+                             const ConvGeom& g, bool accumulate, float* pmean, float* pm2, hipStream_t st);
+int conv_tile_rows(const ConvGeom& g);
 
 // Weight gradient: part[split][Cout][Ktot] = partial sums over pixel ranges
-// of dY[p][cout] * im2col(X)[p][(r,s,c)].  Returns the number of splits used
-// via *splits (computed by wgrad_plan).
+// of dY[p][cout] * im2col(X)[p][(r,s,c)] (wgrad_plan chooses the splits).
 struct WgradPlan { int tm, tn, splits, pix_per_split; long part_floats; };
 WgradPlan wgrad_plan(int Cout, int Ktot, long M);
 hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int Nb, int Hi, int Wi, int Cin_p,
                              int Ho, int Wo, int Cout, int R, int S, int stride, int pad, const WgradPlan& p,
                              hipStream_t st);
-// Sums the split partials in order and writes the canonical gradient
+// Sums the split partials in a fixed order and writes the canonical gradient
 // g[((cout*Cin + c)*R + r)*S + s] for c < Cin.
 hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
                                float* g, hipStream_t st);
 
-// Per-channel reductions over an [M][C] NHWC matrix, in two fixed-order
-// stages (partials per workgroup in fp64, then a finalize).
-int chan_reduce_blocks(long M, int C);
-// stats: psum[b][c] = sum x, psq[b][c] = sum x^2 over the block's rows
-hipError_t launch_bn_stats_partial(const float* x, long M, int C, double* psum, double* psq, hipStream_t st);
-// mean, rstd, and the affine apply coefficients scale = gamma*rstd,
-// shift = beta - mean*scale
-hipError_t launch_bn_stats_finalize(const double* psum, const double* psq, int nblk, long M, int C,
-                                    const float* gamma, const float* beta, float eps, float* mean, float* rstd,
-                                    float* scale, float* shift, hipStream_t st);
-hipError_t launch_chan_affine(const float* x, const float* scale, const float* shift, float* y, long M, int C,
-                              hipStream_t st);
-// backward sums: psum[b][c] = sum dy, psq[b][c] = sum dy * (x - mean) * rstd
-hipError_t launch_bn_bwd_partial(const float* dy, const float* x, const float* mean, const float* rstd, long M,
-                                 int C, double* psum, double* psq, hipStream_t st);
-// dbeta = sum dy, dgamma = sum dy*xhat (written to g_gamma/g_beta if not
-// null), and the data-gradient coefficients a = gamma*rstd, mdy = sum dy / M,
-// mdyx = sum dy*xhat / M
-hipError_t launch_bn_bwd_finalize(const double* psum, const double* psq, int nblk, long M, int C,
-                                  const float* gamma, const float* rstd, float* g_gamma, float* g_beta,
-                                  float* coef_a, float* coef_mdy, float* coef_mdyx, hipStream_t st);
-// dx (+)= a*(dy - mdy - (x - mean)*rstd*mdyx)
-hipError_t launch_bn_bwd_data(const float* dy, const float* x, const float* mean, const float* rstd,
-                              const float* a, const float* mdy, const float* mdyx, float* dx, long M, int C,
-                              bool accumulate, hipStream_t st);
-// column sums of dy (conv bias gradient): out[c] = sum_m dy[m][c]
-hipError_t launch_col_sum_partial(const float* dy, long M, int C, double* psum, hipStream_t st);
-hipError_t launch_col_sum_finalize(const double* psum, int nblk, int C, float* out, hipStream_t st);
+// ---- batch-norm statistics over [M][C] NHWC rows ----
+constexpr int kStatRows = 256;   // rows per tile of the stand-alone kernels
+int stats_tiles(long M);
+// per tile of kStatRows rows: mean and sum of squared deviations per channel
+hipError_t launch_stats_partial(const float* x, long M, int C, float* pmean, float* pm2, hipStream_t st);
+// merges T tiles of R rows (fp64, fixed order): mean, rstd = 1/sqrt(var+eps)
+// with the biased variance, scale = gamma*rstd, shift = beta - mean*scale
+hipError_t launch_stats_finalize(const float* pmean, const float* pm2, int T, int R, long M, int C,
+                                 const float* gamma, const float* beta, float eps, float* mean, float* rstd,
+                                 float* scale, float* shift, hipStream_t st);
+// out[c] = sum_t rows_t * pmean[t][c]: column sums from tile means
+hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C, float* out, hipStream_t st);
+// y = relu?(x1*s1 + t1 [+ r | + x2*s2 + t2])  (r: residual tensor; x2: a second
+// normalised input, used when both branches of a residual add end in BN)
+hipError_t launch_bn_act(const float* x1, const float* s1, const float* t1, const float* r, const float* x2,
+                         const float* s2, const float* t2, bool relu, float* y, long M, int C, hipStream_t st);
+
+// ---- batch-norm backward (with the group's ReLU mask and residual fan-out) ----
+struct BnBwdArgs {
+    const float* dy;                                   // gradient at the group output
+    const float* mask;                                 // ReLU output (g = dy where > 0) or null
+    const float* x1; const float* mean1; const float* rstd1;   // BN input and statistics
+    const float* x2; const float* mean2; const float* rstd2;   // second BN of a dual group, or null
+    long M;
+    int C;
+};
+// per tile of kStatRows rows: sum g, sum g*xhat1, sum g*xhat2
+hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, float* p0, float* p1, float* p2, hipStream_t st);
+// gg/gb (dgamma, dbeta; null = not wanted) and coef = [gamma*rstd | mean g |
+// mean g*xhat] per channel; the second set for a dual group (coef2 null if not)
+hipError_t launch_bn_bwd_finalize(const float* p0, const float* p1, const float* p2, int T, long M, int C,
+                                  const float* gamma1, const float* rstd1, float* gg1, float* gb1, float* coef1,
+                                  const float* gamma2, const float* rstd2, float* gg2, float* gb2, float* coef2,
+                                  hipStream_t st);
+// dx = a*(g - mean g - xhat*mean g*xhat) into dx1 / dx2 (null = skip), and g
+// into dres (the residual branch) -- each written or accumulated
+hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const float* coef1, const float* coef2, float* dx1, bool acc1,
+                               float* dx2, bool acc2, float* dres, bool accres, hipStream_t st);
+
+// ---- fused classifier head: global average pool, linear, softmax CE ----
+hipError_t launch_head_fwd(const float* x, int Nb, int HW, int C, const float* W, const float* b, int O,
+                           const StepArgs* args, float* feat, float* logits, float* dz, float* loss_per,
+                           hipStream_t st);
+// gW/gb (null: only the loss) and the batch-mean loss
+hipError_t launch_head_bwd_w(const float* dz, const float* feat, int Nb, int C, int O, float* gW, float* gb,
+                             const float* loss_per, float* loss, hipStream_t st);
+hipError_t launch_head_bwd_x(const float* dz, const float* W, int Nb, int HW, int C, int O, float* dx, bool acc,
+                             hipStream_t st);
 
 // elementwise (n multiple of 4)
 hipError_t launch_relu_fwd(const float* x, float* y, long n, hipStream_t st);
@@ -83,12 +115,14 @@ hipError_t launch_linear_bwd_w(const float* dz, const float* x, float* gW, float
                                hipStream_t st);
 hipError_t launch_linear_bwd_x(const float* dz, const float* W, float* dx, int Nb, int I, int O, bool accumulate,
                                hipStream_t st);
-// mean softmax cross-entropy: loss[0], dz = (softmax - onehot)/N
-hipError_t launch_softmax_ce(const float* z, const int* labels, float* dz, float* loss, int Nb, int Cls,
+// mean softmax cross-entropy: loss[0], per-sample losses at loss[1..N],
+// dz = (softmax - onehot)/N
+hipError_t launch_softmax_ce(const float* z, const StepArgs* args, float* dz, float* loss, int Nb, int Cls,
                              hipStream_t st);
 
-// NCHW (C channels) -> NHWC (Cp >= C channels, zero-padded)
-hipError_t launch_nchw_to_nhwc(const float* src, float* dst, int Nb, int C, int H, int W, int Cp, hipStream_t st);
+// the step's NCHW images (C channels) -> NHWC (Cp >= C channels, zero-padded)
+hipError_t launch_nchw_to_nhwc(const StepArgs* args, float* dst, int Nb, int C, int H, int W, int Cp,
+                               hipStream_t st);
 // NHWC (Cp) -> NCHW (C), for inspection
 hipError_t launch_nhwc_to_nchw(const float* src, float* dst, int Nb, int C, int H, int W, int Cp, hipStream_t st);
 
@@ -101,8 +135,9 @@ hipError_t launch_snapshot(const float* x, float* v, long d, const SnapConv* con
 
 // Block update (Alg. 1 updater's last step), e in [lo, hi):
 //   m = mu*m + g + wd*x; x -= lr*m   (m == null: x -= lr*(g + wd*x))
-hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long hi, float lr, float mu, float wd,
-                             hipStream_t st);
+// (lr taken from args when args is not null)
+hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long hi, const StepArgs* args, float lr,
+                             float mu, float wd, hipStream_t st);
 // Averaging round (Alg. 1 averager) over n_rep replicas of n floats.
 constexpr int kMaxReplicas = 16;
 struct RepPtrs { float* p[kMaxReplicas]; };

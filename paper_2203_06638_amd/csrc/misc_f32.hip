@@ -15,181 +15,365 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 static inline unsigned nblocks(long n, int per) { return (unsigned)((n + per - 1) / per); }
 
 // ------------------------------------------------------------------------
-// per-channel reductions over [M][C]
+// batch-norm statistics: per row tile, per channel, the tile mean and the
+// sum of squared deviations from it (two passes over the tile); merged over
+// tiles in fp64 by a fixed-order finalize
 // ------------------------------------------------------------------------
 
-constexpr int kRedRows = 1024;   // rows of the matrix per reduction workgroup
+int stats_tiles(long M) { return (int)((M + kStatRows - 1) / kStatRows); }
 
-int chan_reduce_blocks(long M, int C) {
-    (void)C;
-    return (int)((M + kRedRows - 1) / kRedRows);
+// Threads tile the rows x channel-quads of one row tile; quads beyond 256
+// are handled in chunks.  Returns nq (quads in this chunk) and rl (row lanes).
+__device__ __forceinline__ void quad_layout(int C4, int qbase, int& nq, int& rl) {
+    nq = min(256, C4 - qbase);
+    rl = 256 / nq;
 }
 
-// KIND 0: (sum x, sum x^2)   KIND 1: (sum dy, sum dy*xhat)   KIND 2: sum dy
-template <int KIND>
-__global__ __launch_bounds__(256) void chan_partial(const float* __restrict__ a, const float* __restrict__ b,
-                                                    const float* __restrict__ mean, const float* __restrict__ rstd,
-                                                    long M, int C, double* __restrict__ p0, double* __restrict__ p1) {
-    __shared__ double s0[256], s1[256];
-    const int C4 = C >> 2;
+__global__ __launch_bounds__(256) void stats_partial_k(const float* __restrict__ x, long M, int C,
+                                                       float* __restrict__ pmean, float* __restrict__ pm2) {
+    __shared__ f4 red[256];
+    __shared__ float mean_s[1024];
     const int tid = threadIdx.x;
-    const long r0 = (long)blockIdx.x * kRedRows;
-    const long r1 = min(M, r0 + kRedRows);
-    // threads tile (row lanes) x (channel quads); quads beyond 256 loop
+    const int C4 = C >> 2;
+    const long r0 = (long)blockIdx.x * kStatRows;
+    const long r1 = min(M, r0 + kStatRows);
+    const float rows = (float)(r1 - r0);
     for (int qbase = 0; qbase < C4; qbase += 256) {
-        const int nq = min(256, C4 - qbase);
-        const int rl = 256 / nq;             // rows processed in parallel
-        const int q = qbase + tid % nq;
-        const int lr = tid / nq;
-        double x0[4] = {0, 0, 0, 0}, x1[4] = {0, 0, 0, 0};
-        float mu[4] = {0, 0, 0, 0}, rs[4] = {0, 0, 0, 0};
-        if (KIND == 1 && lr < rl) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) { mu[i] = mean[q * 4 + i]; rs[i] = rstd[q * 4 + i]; }
+        int nq, rl;
+        quad_layout(C4, qbase, nq, rl);
+        const int q = qbase + tid % nq, lr = tid / nq;
+        const bool act = lr < rl;
+        f4 s = f4{0.f, 0.f, 0.f, 0.f};
+        if (act)
+            for (long r = r0 + lr; r < r1; r += rl) s += *(const f4*)(x + r * C + q * 4);
+        red[tid] = s;
+        __syncthreads();
+        if (tid < nq) {
+            f4 t = f4{0.f, 0.f, 0.f, 0.f};
+            for (int l = 0; l < rl; ++l) t += red[l * nq + tid];
+            for (int k = 0; k < 4; ++k) mean_s[(tid * 4 + k) & 1023] = t[k] / rows;
         }
-        if (lr < rl) {
+        __syncthreads();
+        f4 mu = f4{0.f, 0.f, 0.f, 0.f};
+        if (act)
+            for (int k = 0; k < 4; ++k) mu[k] = mean_s[((q - qbase) * 4 + k) & 1023];
+        f4 v = f4{0.f, 0.f, 0.f, 0.f};
+        if (act)
             for (long r = r0 + lr; r < r1; r += rl) {
-                const f4 va = *(const f4*)(a + r * C + q * 4);
-                if (KIND == 0) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) { x0[i] += (double)va[i]; x1[i] += (double)va[i] * (double)va[i]; }
-                } else if (KIND == 1) {
-                    const f4 vb = *(const f4*)(b + r * C + q * 4);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        x0[i] += (double)va[i];
-                        x1[i] += (double)va[i] * (double)((vb[i] - mu[i]) * rs[i]);
-                    }
-                } else {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) x0[i] += (double)va[i];
-                }
+                const f4 d = *(const f4*)(x + r * C + q * 4) - mu;
+                v += d * d;
+            }
+        __syncthreads();
+        red[tid] = v;
+        __syncthreads();
+        if (tid < nq) {
+            f4 t = f4{0.f, 0.f, 0.f, 0.f};
+            for (int l = 0; l < rl; ++l) t += red[l * nq + tid];
+            for (int k = 0; k < 4; ++k) {
+                const long o = (long)blockIdx.x * C + (qbase + tid) * 4 + k;
+                pmean[o] = mean_s[(tid * 4 + k) & 1023];
+                pm2[o] = t[k];
             }
         }
-        // reduce over the row lanes, one channel component at a time, fixed order
-        for (int i = 0; i < 4; ++i) {
-            s0[tid] = x0[i];
-            s1[tid] = x1[i];
-            __syncthreads();
-            if (tid < nq) {
-                double t0 = 0.0, t1 = 0.0;
-                for (int l = 0; l < rl; ++l) { t0 += s0[l * nq + tid]; t1 += s1[l * nq + tid]; }
-                const long o = (long)blockIdx.x * C + (qbase + tid) * 4 + i;
-                p0[o] = t0;
-                if (KIND != 2) p1[o] = t1;
-            }
-            __syncthreads();
-        }
+        __syncthreads();
     }
 }
 
-__global__ void bn_stats_finalize_k(const double* __restrict__ psum, const double* __restrict__ psq, int nblk, long M,
-                                    int C, const float* __restrict__ gamma, const float* __restrict__ beta, float eps,
-                                    float* mean, float* rstd, float* scale, float* shift) {
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
-    double s = 0.0, q = 0.0;
-    for (int b = 0; b < nblk; ++b) { s += psum[(long)b * C + c]; q += psq[(long)b * C + c]; }
-    const double mu = s / (double)M;
-    double var = q / (double)M - mu * mu;
-    if (var < 0.0) var = 0.0;
-    const double r = 1.0 / sqrt(var + (double)eps);
-    mean[c] = (float)mu;
-    rstd[c] = (float)r;
-    const double sc = (double)gamma[c] * r;
-    scale[c] = (float)sc;
-    shift[c] = (float)((double)beta[c] - mu * sc);
+// One workgroup per channel: thread j takes tiles j, j+256, ... and the 256
+// partial sums meet in a fixed-shape LDS tree.  mean = sum n_t m_t / M,
+// M2 = sum (M2_t + n_t (m_t - mean)^2).
+__device__ __forceinline__ double tree_sum256(double v, double* red) {
+    const int t = threadIdx.x;
+    red[t] = v;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) red[t] += red[t + w];
+        __syncthreads();
+    }
+    const double r = red[0];
+    __syncthreads();
+    return r;
 }
 
-__global__ void bn_bwd_finalize_k(const double* __restrict__ psum, const double* __restrict__ psq, int nblk, long M,
-                                  int C, const float* __restrict__ gamma, const float* __restrict__ rstd,
-                                  float* g_gamma, float* g_beta, float* ca, float* cmdy, float* cmdyx) {
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
-    double s = 0.0, q = 0.0;
-    for (int b = 0; b < nblk; ++b) { s += psum[(long)b * C + c]; q += psq[(long)b * C + c]; }
-    if (g_gamma) g_gamma[c] = (float)q;
-    if (g_beta) g_beta[c] = (float)s;
-    ca[c] = gamma[c] * rstd[c];
-    cmdy[c] = (float)(s / (double)M);
-    cmdyx[c] = (float)(q / (double)M);
-}
-
-__global__ void col_sum_finalize_k(const double* __restrict__ psum, int nblk, int C, float* out) {
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
+__global__ __launch_bounds__(256) void stats_finalize_k(const float* __restrict__ pmean, const float* __restrict__ pm2,
+                                                        int T, int R, long M, int C, const float* __restrict__ gamma,
+                                                        const float* __restrict__ beta, float eps, float* mean,
+                                                        float* rstd, float* scale, float* shift) {
+    __shared__ double red[256];
+    const int c = blockIdx.x;
     double s = 0.0;
-    for (int b = 0; b < nblk; ++b) s += psum[(long)b * C + c];
-    out[c] = (float)s;
+#pragma unroll 4
+    for (int t = threadIdx.x; t < T; t += 256)
+        s += (double)min((long)R, M - (long)t * R) * (double)pmean[(long)t * C + c];
+    const double mu = tree_sum256(s, red) / (double)M;
+    double q = 0.0;
+#pragma unroll 4
+    for (int t = threadIdx.x; t < T; t += 256) {
+        const double d = (double)pmean[(long)t * C + c] - mu;
+        q += (double)pm2[(long)t * C + c] + (double)min((long)R, M - (long)t * R) * d * d;
+    }
+    q = tree_sum256(q, red);
+    if (threadIdx.x == 0) {
+        const double r = 1.0 / sqrt(q / (double)M + (double)eps);
+        const double sc = (double)gamma[c] * r;
+        mean[c] = (float)mu;
+        rstd[c] = (float)r;
+        scale[c] = (float)sc;
+        shift[c] = (float)((double)beta[c] - mu * sc);
+    }
 }
 
-hipError_t launch_bn_stats_partial(const float* x, long M, int C, double* psum, double* psq, hipStream_t st) {
-    hipLaunchKernelGGL(chan_partial<0>, dim3(chan_reduce_blocks(M, C)), dim3(256), 0, st, x, nullptr, nullptr,
-                       nullptr, M, C, psum, psq);
+// out[c] = sum over tiles of n_t * mean_t (the column sum), fixed order
+__global__ __launch_bounds__(256) void sum_from_tiles_k(const float* __restrict__ pmean, int T, int R, long M, int C,
+                                                        float* __restrict__ out) {
+    __shared__ double red[256];
+    const int c = blockIdx.x;
+    double s = 0.0;
+    for (int t = threadIdx.x; t < T; t += 256)
+        s += (double)min((long)R, M - (long)t * R) * (double)pmean[(long)t * C + c];
+    s = tree_sum256(s, red);
+    if (threadIdx.x == 0) out[c] = (float)s;
+}
+
+hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C, float* out, hipStream_t st) {
+    hipLaunchKernelGGL(sum_from_tiles_k, dim3(C), dim3(256), 0, st, pmean, T, R, M, C, out);
     return hipGetLastError();
 }
-hipError_t launch_bn_stats_finalize(const double* psum, const double* psq, int nblk, long M, int C,
-                                    const float* gamma, const float* beta, float eps, float* mean, float* rstd,
-                                    float* scale, float* shift, hipStream_t st) {
-    hipLaunchKernelGGL(bn_stats_finalize_k, dim3(nblocks(C, 64)), dim3(64), 0, st, psum, psq, nblk, M, C, gamma,
-                       beta, eps, mean, rstd, scale, shift);
+
+hipError_t launch_stats_partial(const float* x, long M, int C, float* pmean, float* pm2, hipStream_t st) {
+    hipLaunchKernelGGL(stats_partial_k, dim3(stats_tiles(M)), dim3(256), 0, st, x, M, C, pmean, pm2);
     return hipGetLastError();
 }
-hipError_t launch_bn_bwd_partial(const float* dy, const float* x, const float* mean, const float* rstd, long M,
-                                 int C, double* psum, double* psq, hipStream_t st) {
-    hipLaunchKernelGGL(chan_partial<1>, dim3(chan_reduce_blocks(M, C)), dim3(256), 0, st, dy, x, mean, rstd, M, C,
-                       psum, psq);
-    return hipGetLastError();
-}
-hipError_t launch_bn_bwd_finalize(const double* psum, const double* psq, int nblk, long M, int C,
-                                  const float* gamma, const float* rstd, float* g_gamma, float* g_beta,
-                                  float* coef_a, float* coef_mdy, float* coef_mdyx, hipStream_t st) {
-    hipLaunchKernelGGL(bn_bwd_finalize_k, dim3(nblocks(C, 64)), dim3(64), 0, st, psum, psq, nblk, M, C, gamma, rstd,
-                       g_gamma, g_beta, coef_a, coef_mdy, coef_mdyx);
-    return hipGetLastError();
-}
-hipError_t launch_col_sum_partial(const float* dy, long M, int C, double* psum, hipStream_t st) {
-    hipLaunchKernelGGL(chan_partial<2>, dim3(chan_reduce_blocks(M, C)), dim3(256), 0, st, dy, nullptr, nullptr,
-                       nullptr, M, C, psum, nullptr);
-    return hipGetLastError();
-}
-hipError_t launch_col_sum_finalize(const double* psum, int nblk, int C, float* out, hipStream_t st) {
-    hipLaunchKernelGGL(col_sum_finalize_k, dim3(nblocks(C, 64)), dim3(64), 0, st, psum, nblk, C, out);
+
+hipError_t launch_stats_finalize(const float* pmean, const float* pm2, int T, int R, long M, int C,
+                                 const float* gamma, const float* beta, float eps, float* mean, float* rstd,
+                                 float* scale, float* shift, hipStream_t st) {
+    hipLaunchKernelGGL(stats_finalize_k, dim3(C), dim3(256), 0, st, pmean, pm2, T, R, M, C, gamma, beta, eps, mean,
+                       rstd, scale, shift);
     return hipGetLastError();
 }
 
 // ------------------------------------------------------------------------
-// elementwise
+// batch-norm apply, fused with the residual add and the ReLU that follow it
+//   y = act(x1*s1 + t1 [+ r | + x2*s2 + t2])
 // ------------------------------------------------------------------------
 
-__global__ void chan_affine_k(const f4* __restrict__ x, const float* __restrict__ scale,
-                              const float* __restrict__ shift, f4* __restrict__ y, long n4, int C) {
+template <int RES, bool RELU>
+__global__ void bn_act_k(const f4* __restrict__ x1, const float* __restrict__ s1, const float* __restrict__ t1,
+                         const f4* __restrict__ r, const f4* __restrict__ x2, const float* __restrict__ s2,
+                         const float* __restrict__ t2, f4* __restrict__ y, long n4, int C) {
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
         const int c = (int)((i * 4) % C);
-        f4 v = x[i];
+        const f4 a = x1[i];
         f4 o;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) o[k] = v[k] * scale[c + k] + shift[c + k];
+        for (int k = 0; k < 4; ++k) o[k] = a[k] * s1[c + k] + t1[c + k];
+        if (RES == 1) o += r[i];
+        if (RES == 2) {
+            const f4 b = x2[i];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) o[k] += b[k] * s2[c + k] + t2[c + k];
+        }
+        if (RELU) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) o[k] = o[k] > 0.f ? o[k] : 0.f;
+        }
         y[i] = o;
     }
 }
 
-__global__ void bn_bwd_data_k(const f4* __restrict__ dy, const f4* __restrict__ x, const float* __restrict__ mean,
-                              const float* __restrict__ rstd, const float* __restrict__ ca,
-                              const float* __restrict__ cmdy, const float* __restrict__ cmdyx, f4* __restrict__ dx,
-                              long n4, int C, int acc) {
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
-        const int c = (int)((i * 4) % C);
-        f4 g = dy[i], v = x[i];
-        f4 o = acc ? dx[i] : f4{0.f, 0.f, 0.f, 0.f};
+static unsigned ew_grid(long n4) {
+    long b = (n4 + 255) / 256;
+    return (unsigned)(b < 8192 ? (b < 1 ? 1 : b) : 8192);
+}
+
+hipError_t launch_bn_act(const float* x1, const float* s1, const float* t1, const float* r, const float* x2,
+                         const float* s2, const float* t2, bool relu, float* y, long M, int C, hipStream_t st) {
+    const long n4 = M * C / 4;
+    const int res = r ? 1 : (x2 ? 2 : 0);
+#define BNACT(RS, RL)                                                                                       \
+    hipLaunchKernelGGL((bn_act_k<RS, RL>), dim3(ew_grid(n4)), dim3(256), 0, st, (const f4*)x1, s1, t1,      \
+                       (const f4*)r, (const f4*)x2, s2, t2, (f4*)y, n4, C)
+    if (res == 0) { if (relu) BNACT(0, true); else BNACT(0, false); }
+    else if (res == 1) { if (relu) BNACT(1, true); else BNACT(1, false); }
+    else { if (relu) BNACT(2, true); else BNACT(2, false); }
+#undef BNACT
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------
+// batch-norm backward, with the ReLU mask and the residual fan-out of the
+// forward group folded in.  g = dy (masked by the group output > 0);
+// dgamma = sum g*xhat, dbeta = sum g;
+// dx = gamma*rstd*(g - mean(g) - xhat*mean(g*xhat)).
+// ------------------------------------------------------------------------
+
+template <bool MASK, bool DUAL>
+__global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, float* __restrict__ p0, float* __restrict__ p1,
+                                                       float* __restrict__ p2) {
+    __shared__ f4 red[3][256];
+    const int tid = threadIdx.x;
+    const int C = a.C, C4 = C >> 2;
+    const long r0 = (long)blockIdx.x * kStatRows;
+    const long r1 = min(a.M, r0 + kStatRows);
+    for (int qbase = 0; qbase < C4; qbase += 256) {
+        int nq, rl;
+        quad_layout(C4, qbase, nq, rl);
+        const int q = qbase + tid % nq, lr = tid / nq;
+        f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0, s2 = s0;
+        if (lr < rl) {
+            f4 m1, r1v, m2 = s0, r2v = s0;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const float xh = (v[k] - mean[c + k]) * rstd[c + k];
-            o[k] += ca[c + k] * (g[k] - cmdy[c + k] - xh * cmdyx[c + k]);
+            for (int k = 0; k < 4; ++k) {
+                m1[k] = a.mean1[q * 4 + k];
+                r1v[k] = a.rstd1[q * 4 + k];
+                if (DUAL) { m2[k] = a.mean2[q * 4 + k]; r2v[k] = a.rstd2[q * 4 + k]; }
+            }
+            for (long r = r0 + lr; r < r1; r += rl) {
+                const long o = r * C + q * 4;
+                f4 g = *(const f4*)(a.dy + o);
+                if (MASK) {
+                    const f4 y = *(const f4*)(a.mask + o);
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) g[k] = y[k] > 0.f ? g[k] : 0.f;
+                }
+                const f4 xh = (*(const f4*)(a.x1 + o) - m1) * r1v;
+                s0 += g;
+                s1 += g * xh;
+                if (DUAL) s2 += g * ((*(const f4*)(a.x2 + o) - m2) * r2v);
+            }
         }
-        dx[i] = o;
+        red[0][tid] = s0;
+        red[1][tid] = s1;
+        red[2][tid] = s2;
+        __syncthreads();
+        if (tid < nq) {
+            f4 t0 = f4{0.f, 0.f, 0.f, 0.f}, t1 = t0, t2 = t0;
+            for (int l = 0; l < rl; ++l) {
+                t0 += red[0][l * nq + tid];
+                t1 += red[1][l * nq + tid];
+                t2 += red[2][l * nq + tid];
+            }
+            for (int k = 0; k < 4; ++k) {
+                const long o = (long)blockIdx.x * C + (qbase + tid) * 4 + k;
+                p0[o] = t0[k];
+                p1[o] = t1[k];
+                if (DUAL) p2[o] = t2[k];
+            }
+        }
+        __syncthreads();
     }
 }
+
+__global__ __launch_bounds__(256) void bn_bwd_finalize_k(const float* __restrict__ p0, const float* __restrict__ p1,
+                                                         const float* __restrict__ p2, int T, long M, int C,
+                                                         const float* __restrict__ gamma1,
+                                                         const float* __restrict__ rstd1, float* gg1, float* gb1,
+                                                         float* coef1, const float* __restrict__ gamma2,
+                                                         const float* __restrict__ rstd2, float* gg2, float* gb2,
+                                                         float* coef2) {
+    __shared__ double red[256];
+    const int c = blockIdx.x;
+    const bool dual = coef2 != nullptr;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0;
+#pragma unroll 4
+    for (int t = threadIdx.x; t < T; t += 256) {
+        s0 += (double)p0[(long)t * C + c];
+        s1 += (double)p1[(long)t * C + c];
+        if (dual) s2 += (double)p2[(long)t * C + c];
+    }
+    const double t0 = tree_sum256(s0, red);
+    const double t1 = tree_sum256(s1, red);
+    const double t2 = dual ? tree_sum256(s2, red) : 0.0;
+    if (threadIdx.x != 0) return;
+    if (gg1) gg1[c] = (float)t1;
+    if (gb1) gb1[c] = (float)t0;
+    coef1[c] = gamma1[c] * rstd1[c];
+    coef1[C + c] = (float)(t0 / (double)M);
+    coef1[2 * C + c] = (float)(t1 / (double)M);
+    if (dual) {
+        if (gg2) gg2[c] = (float)t2;
+        if (gb2) gb2[c] = (float)t0;
+        coef2[c] = gamma2[c] * rstd2[c];
+        coef2[C + c] = (float)(t0 / (double)M);
+        coef2[2 * C + c] = (float)(t2 / (double)M);
+    }
+}
+
+template <bool MASK>
+__global__ void bn_bwd_apply_k(BnBwdArgs a, const float* __restrict__ coef1, const float* __restrict__ coef2,
+                               float* __restrict__ dx1, int acc1, float* __restrict__ dx2, int acc2,
+                               float* __restrict__ dres, int accres) {
+    const long n4 = a.M * a.C / 4;
+    const int C = a.C;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
+        const int c = (int)((i * 4) % C);
+        f4 g = ((const f4*)a.dy)[i];
+        if (MASK) {
+            const f4 y = ((const f4*)a.mask)[i];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) g[k] = y[k] > 0.f ? g[k] : 0.f;
+        }
+        if (dx1) {
+            const f4 x = ((const f4*)a.x1)[i];
+            f4 o = acc1 ? ((f4*)dx1)[i] : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float xh = (x[k] - a.mean1[c + k]) * a.rstd1[c + k];
+                o[k] += coef1[c + k] * (g[k] - coef1[C + c + k] - xh * coef1[2 * C + c + k]);
+            }
+            ((f4*)dx1)[i] = o;
+        }
+        if (dx2) {
+            const f4 x = ((const f4*)a.x2)[i];
+            f4 o = acc2 ? ((f4*)dx2)[i] : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float xh = (x[k] - a.mean2[c + k]) * a.rstd2[c + k];
+                o[k] += coef2[c + k] * (g[k] - coef2[C + c + k] - xh * coef2[2 * C + c + k]);
+            }
+            ((f4*)dx2)[i] = o;
+        }
+        if (dres) ((f4*)dres)[i] = accres ? ((f4*)dres)[i] + g : g;
+    }
+}
+
+hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, float* p0, float* p1, float* p2, hipStream_t st) {
+    const dim3 grid(stats_tiles(a.M));
+    if (a.mask) {
+        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<true, true>), grid, dim3(256), 0, st, a, p0, p1, p2);
+        else hipLaunchKernelGGL((bn_bwd_reduce_k<true, false>), grid, dim3(256), 0, st, a, p0, p1, p2);
+    } else {
+        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<false, true>), grid, dim3(256), 0, st, a, p0, p1, p2);
+        else hipLaunchKernelGGL((bn_bwd_reduce_k<false, false>), grid, dim3(256), 0, st, a, p0, p1, p2);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_bn_bwd_finalize(const float* p0, const float* p1, const float* p2, int T, long M, int C,
+                                  const float* gamma1, const float* rstd1, float* gg1, float* gb1, float* coef1,
+                                  const float* gamma2, const float* rstd2, float* gg2, float* gb2, float* coef2,
+                                  hipStream_t st) {
+    hipLaunchKernelGGL(bn_bwd_finalize_k, dim3(C), dim3(256), 0, st, p0, p1, p2, T, M, C, gamma1, rstd1, gg1, gb1,
+                       coef1, gamma2, rstd2, gg2, gb2, coef2);
+    return hipGetLastError();
+}
+
+hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const float* coef1, const float* coef2, float* dx1, bool acc1,
+                               float* dx2, bool acc2, float* dres, bool accres, hipStream_t st) {
+    const long n4 = a.M * a.C / 4;
+    if (a.mask)
+        hipLaunchKernelGGL((bn_bwd_apply_k<true>), dim3(ew_grid(n4)), dim3(256), 0, st, a, coef1, coef2, dx1,
+                           (int)acc1, dx2, (int)acc2, dres, (int)accres);
+    else
+        hipLaunchKernelGGL((bn_bwd_apply_k<false>), dim3(ew_grid(n4)), dim3(256), 0, st, a, coef1, coef2, dx1,
+                           (int)acc1, dx2, (int)acc2, dres, (int)accres);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------
+// elementwise (unfused per-layer mode)
+// ------------------------------------------------------------------------
 
 __global__ void relu_fwd_k(const f4* __restrict__ x, f4* __restrict__ y, long n4) {
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
@@ -221,26 +405,6 @@ __global__ void copy_acc_k(const f4* __restrict__ s, f4* __restrict__ d, long n4
         d[i] = acc ? d[i] + s[i] : s[i];
 }
 
-static unsigned ew_grid(long n4) {
-    long b = (n4 + 255) / 256;
-    return (unsigned)(b < 8192 ? (b < 1 ? 1 : b) : 8192);
-}
-
-hipError_t launch_chan_affine(const float* x, const float* scale, const float* shift, float* y, long M, int C,
-                              hipStream_t st) {
-    const long n4 = M * C / 4;
-    hipLaunchKernelGGL(chan_affine_k, dim3(ew_grid(n4)), dim3(256), 0, st, (const f4*)x, scale, shift, (f4*)y, n4,
-                       C);
-    return hipGetLastError();
-}
-hipError_t launch_bn_bwd_data(const float* dy, const float* x, const float* mean, const float* rstd,
-                              const float* a, const float* mdy, const float* mdyx, float* dx, long M, int C,
-                              bool accumulate, hipStream_t st) {
-    const long n4 = M * C / 4;
-    hipLaunchKernelGGL(bn_bwd_data_k, dim3(ew_grid(n4)), dim3(256), 0, st, (const f4*)dy, (const f4*)x, mean, rstd,
-                       a, mdy, mdyx, (f4*)dx, n4, C, (int)accumulate);
-    return hipGetLastError();
-}
 hipError_t launch_relu_fwd(const float* x, float* y, long n, hipStream_t st) {
     hipLaunchKernelGGL(relu_fwd_k, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const f4*)x, (f4*)y, n / 4);
     return hipGetLastError();
@@ -401,32 +565,150 @@ __global__ void linear_bwd_x_k(const float* __restrict__ dz, const float* __rest
     dx[idx] = acc ? dx[idx] + s : s;
 }
 
-// One workgroup; wave w handles samples w, w+4, ...; the batch mean is
-// summed by one thread in sample order.
-__global__ __launch_bounds__(256) void softmax_ce_k(const float* __restrict__ z, const int* __restrict__ labels,
-                                                    float* __restrict__ dz, float* __restrict__ loss,
-                                                    float* __restrict__ per_sample, int Nb, int Cls) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int n = wave; n < Nb; n += 4) {
-        const float* zr = z + (long)n * Cls;
-        float mx = -INFINITY;
-        for (int j = lane; j < Cls; j += 64) mx = fmaxf(mx, zr[j]);
-        for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-        float se = 0.f;
-        for (int j = lane; j < Cls; j += 64) se += expf(zr[j] - mx);
-        for (int off = 32; off > 0; off >>= 1) se += __shfl_xor(se, off);
-        const float lse = mx + logf(se);
-        const int y = labels[n];
-        for (int j = lane; j < Cls; j += 64)
-            dz[(long)n * Cls + j] = (expf(zr[j] - lse) - (j == y ? 1.f : 0.f)) / (float)Nb;
-        if (lane == 0) per_sample[n] = lse - zr[y];
+// One thread per sample (classes looped); per-sample losses go to
+// loss_per; loss_mean_k sums them in sample order.
+__global__ void softmax_ce_k(const float* __restrict__ z, const StepArgs* __restrict__ args,
+                             float* __restrict__ dz, float* __restrict__ loss_per, int Nb, int Cls) {
+    const int n = blockIdx.x * blockDim.x + threadIdx.x;
+    if (n >= Nb) return;
+    const float* zr = z + (long)n * Cls;
+    float mx = -INFINITY;
+    for (int j = 0; j < Cls; ++j) mx = fmaxf(mx, zr[j]);
+    float se = 0.f;
+    for (int j = 0; j < Cls; ++j) se += expf(zr[j] - mx);
+    const float lse = mx + logf(se);
+    const int y = args->labels[n];
+    for (int j = 0; j < Cls; ++j) dz[(long)n * Cls + j] = (expf(zr[j] - lse) - (j == y ? 1.f : 0.f)) / (float)Nb;
+    loss_per[n] = lse - zr[y];
+}
+
+__global__ void loss_mean_k(const float* __restrict__ loss_per, int Nb, float* __restrict__ loss) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    float s = 0.f;
+    for (int n = 0; n < Nb; ++n) s += loss_per[n];
+    loss[0] = s / (float)Nb;
+}
+
+// Fused head, one workgroup per sample: global average pool of the sample's
+// HW x C activation, logits = W f + b, softmax cross-entropy against its
+// label.  Writes the pooled features (for the weight gradient), the logits,
+// dz = (softmax - onehot)/N and the sample's loss.  Reductions over classes
+// run as fixed-shape trees in LDS.
+constexpr int kHeadMaxC = 2048, kHeadMaxO = 4096;
+__global__ __launch_bounds__(256) void head_fwd_k(const float* __restrict__ x, int Nb, int HW, int C,
+                                                  const float* __restrict__ W, const float* __restrict__ b, int O,
+                                                  const StepArgs* __restrict__ args, float* __restrict__ feat,
+                                                  float* __restrict__ logits, float* __restrict__ dz,
+                                                  float* __restrict__ loss_per) {
+    __shared__ float f_s[kHeadMaxC];
+    __shared__ float z_s[kHeadMaxO];
+    __shared__ float red[256];
+    const int n = blockIdx.x, t = threadIdx.x;
+    for (int c = t; c < C; c += 256) {
+        float s = 0.f;
+        for (int e = 0; e < HW; ++e) s += x[((long)n * HW + e) * C + c];
+        const float f = s / (float)HW;
+        f_s[c] = f;
+        feat[(long)n * C + c] = f;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    float mx = -INFINITY;
+    for (int o = t; o < O; o += 256) {
+        float z = b ? b[o] : 0.f;
+        const float* w = W + (long)o * C;
+        for (int c = 0; c < C; ++c) z += w[c] * f_s[c];
+        z_s[o] = z;
+        logits[(long)n * O + o] = z;
+        mx = fmaxf(mx, z);
+    }
+    red[t] = mx;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) red[t] = fmaxf(red[t], red[t + w]);
+        __syncthreads();
+    }
+    const float zmax = red[0];
+    __syncthreads();
+    float se = 0.f;
+    for (int o = t; o < O; o += 256) se += expf(z_s[o] - zmax);
+    red[t] = se;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (t < w) red[t] += red[t + w];
+        __syncthreads();
+    }
+    const float lse = zmax + logf(red[0]);
+    const int y = args->labels[n];
+    for (int o = t; o < O; o += 256)
+        dz[(long)n * O + o] = (expf(z_s[o] - lse) - (o == y ? 1.f : 0.f)) / (float)Nb;
+    if (t == 0) loss_per[n] = lse - z_s[y];
+}
+
+// dW[o][c] = sum_n dz[n][o] f[n][c]; db[o] = sum_n dz[n][o]; block 0 thread 0
+// also forms the batch-mean loss.
+__global__ void head_bwd_w_k(const float* __restrict__ dz, const float* __restrict__ feat, int Nb, int C, int O,
+                             float* __restrict__ gW, float* __restrict__ gb, const float* __restrict__ loss_per,
+                             float* __restrict__ loss) {
+    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx == 0) {
         float s = 0.f;
-        for (int n = 0; n < Nb; ++n) s += per_sample[n];
+        for (int n = 0; n < Nb; ++n) s += loss_per[n];
         loss[0] = s / (float)Nb;
     }
+    if (!gW) return;
+    if (idx < (long)O * C) {
+        const int o = (int)(idx / C), c = (int)(idx - (long)o * C);
+        float s = 0.f;
+        for (int n = 0; n < Nb; ++n) s += dz[(long)n * O + o] * feat[(long)n * C + c];
+        gW[idx] = s;
+    } else if (gb && idx < (long)O * C + O) {
+        const int o = (int)(idx - (long)O * C);
+        float s = 0.f;
+        for (int n = 0; n < Nb; ++n) s += dz[(long)n * O + o];
+        gb[o] = s;
+    }
+}
+
+// one workgroup per sample: df = (dz W) / HW, broadcast over the HW pixels
+__global__ __launch_bounds__(256) void head_bwd_x_k(const float* __restrict__ dz, const float* __restrict__ W,
+                                                    int Nb, int HW, int C, int O, float* __restrict__ dx, int acc) {
+    __shared__ float df[kHeadMaxC];
+    const int n = blockIdx.x, t = threadIdx.x;
+    for (int c = t; c < C; c += 256) {
+        float s = 0.f;
+        for (int o = 0; o < O; ++o) s += dz[(long)n * O + o] * W[(long)o * C + c];
+        df[c] = s / (float)HW;
+    }
+    __syncthreads();
+    const int C4 = C >> 2;
+    f4* out = (f4*)(dx + (long)n * HW * C);
+    for (int i = t; i < HW * C4; i += 256) {
+        const int c = (i % C4) * 4;
+        const f4 v = f4{df[c], df[c + 1], df[c + 2], df[c + 3]};
+        out[i] = acc ? out[i] + v : v;
+    }
+}
+
+hipError_t launch_head_fwd(const float* x, int Nb, int HW, int C, const float* W, const float* b, int O,
+                           const StepArgs* args, float* feat, float* logits, float* dz, float* loss_per,
+                           hipStream_t st) {
+    if (C > kHeadMaxC || O > kHeadMaxO) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(head_fwd_k, dim3(Nb), dim3(256), 0, st, x, Nb, HW, C, W, b, O, args, feat, logits, dz,
+                       loss_per);
+    return hipGetLastError();
+}
+hipError_t launch_head_bwd_w(const float* dz, const float* feat, int Nb, int C, int O, float* gW, float* gb,
+                             const float* loss_per, float* loss, hipStream_t st) {
+    const long n = gW ? (long)O * C + O : 1;
+    hipLaunchKernelGGL(head_bwd_w_k, dim3(nblocks(n, 256)), dim3(256), 0, st, dz, feat, Nb, C, O, gW, gb, loss_per,
+                       loss);
+    return hipGetLastError();
+}
+hipError_t launch_head_bwd_x(const float* dz, const float* W, int Nb, int HW, int C, int O, float* dx, bool acc,
+                             hipStream_t st) {
+    if (C > kHeadMaxC) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(head_bwd_x_k, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, dx, (int)acc);
+    return hipGetLastError();
 }
 
 hipError_t launch_linear_fwd(const float* x, const float* W, const float* b, float* y, int Nb, int I, int O,
@@ -446,10 +728,11 @@ hipError_t launch_linear_bwd_x(const float* dz, const float* W, float* dx, int N
                        (int)accumulate);
     return hipGetLastError();
 }
-hipError_t launch_softmax_ce(const float* z, const int* labels, float* dz, float* loss, int Nb, int Cls,
+hipError_t launch_softmax_ce(const float* z, const StepArgs* args, float* dz, float* loss, int Nb, int Cls,
                              hipStream_t st) {
     // per-sample losses live just after the loss scalar (caller sizes loss to 1 + Nb floats)
-    hipLaunchKernelGGL(softmax_ce_k, dim3(1), dim3(256), 0, st, z, labels, dz, loss, loss + 1, Nb, Cls);
+    hipLaunchKernelGGL(softmax_ce_k, dim3(nblocks(Nb, 64)), dim3(64), 0, st, z, args, dz, loss + 1, Nb, Cls);
+    hipLaunchKernelGGL(loss_mean_k, dim3(1), dim3(64), 0, st, loss + 1, Nb, loss);
     return hipGetLastError();
 }
 
@@ -457,8 +740,9 @@ hipError_t launch_softmax_ce(const float* z, const int* labels, float* dz, float
 // layouts
 // ------------------------------------------------------------------------
 
-__global__ void nchw_to_nhwc_k(const float* __restrict__ s, float* __restrict__ d, int Nb, int C, int H, int W,
-                               int Cp) {
+__global__ void nchw_to_nhwc_k(const StepArgs* __restrict__ args, float* __restrict__ d, int Nb, int C, int H,
+                               int W, int Cp) {
+    const float* __restrict__ s = args->images;
     const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
     const long total = (long)Nb * H * W * Cp;
     if (idx >= total) return;
@@ -485,14 +769,28 @@ __global__ void nhwc_to_nchw_k(const float* __restrict__ s, float* __restrict__ 
     d[idx] = s[(((long)n * H + h) * W + w) * Cp + c];
 }
 
-hipError_t launch_nchw_to_nhwc(const float* src, float* dst, int Nb, int C, int H, int W, int Cp, hipStream_t st) {
+hipError_t launch_nchw_to_nhwc(const StepArgs* args, float* dst, int Nb, int C, int H, int W, int Cp,
+                               hipStream_t st) {
     const long total = (long)Nb * H * W * Cp;
-    hipLaunchKernelGGL(nchw_to_nhwc_k, dim3(nblocks(total, 256)), dim3(256), 0, st, src, dst, Nb, C, H, W, Cp);
+    hipLaunchKernelGGL(nchw_to_nhwc_k, dim3(nblocks(total, 256)), dim3(256), 0, st, args, dst, Nb, C, H, W, Cp);
     return hipGetLastError();
 }
 hipError_t launch_nhwc_to_nchw(const float* src, float* dst, int Nb, int C, int H, int W, int Cp, hipStream_t st) {
     const long total = (long)Nb * H * W * C;
     hipLaunchKernelGGL(nhwc_to_nchw_k, dim3(nblocks(total, 256)), dim3(256), 0, st, src, dst, Nb, C, H, W, Cp);
+    return hipGetLastError();
+}
+
+__global__ void set_step_args_k(StepArgs* dst, const float* images, const int* labels, float lr) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) {
+        dst->images = images;
+        dst->labels = labels;
+        dst->lr = lr;
+    }
+}
+
+hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* labels, float lr, hipStream_t st) {
+    hipLaunchKernelGGL(set_step_args_k, dim3(1), dim3(64), 0, st, dst, images, labels, lr);
     return hipGetLastError();
 }
 
@@ -537,7 +835,8 @@ hipError_t launch_snapshot(const float* x, float* v, long d, const SnapConv* con
 // Each thread owns an aligned quad [4t, 4t+4) of the index space shifted to
 // the aligned start below lo; whole quads use 16-byte accesses.
 __global__ void sgd_update_k(float* __restrict__ x, float* __restrict__ m, const float* __restrict__ g, long lo,
-                             long hi, float lr, float mu, float wd) {
+                             long hi, const StepArgs* __restrict__ args, float lr_value, float mu, float wd) {
+    const float lr = args ? args->lr : lr_value;
     const long base = lo & ~3L;
     const long nq = (hi - base + 3) / 4;
     for (long q = (long)blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += (long)gridDim.x * blockDim.x) {
@@ -569,13 +868,13 @@ __global__ void sgd_update_k(float* __restrict__ x, float* __restrict__ m, const
     }
 }
 
-hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long hi, float lr, float mu, float wd,
-                             hipStream_t st) {
+hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long hi, const StepArgs* args, float lr,
+                             float mu, float wd, hipStream_t st) {
     if (hi <= lo) return hipSuccess;
     const long nq = (hi - (lo & ~3L) + 3) / 4;
     long b = (nq + 255) / 256;
     if (b > 8192) b = 8192;
-    hipLaunchKernelGGL(sgd_update_k, dim3((unsigned)b), dim3(256), 0, st, x, m, g, lo, hi, lr, mu, wd);
+    hipLaunchKernelGGL(sgd_update_k, dim3((unsigned)b), dim3(256), 0, st, x, m, g, lo, hi, args, lr, mu, wd);
     return hipGetLastError();
 }
 

@@ -62,6 +62,22 @@ struct Plan {
     double flops = 0;             // backward flops (dgrad + wgrad of conv/linear)
 };
 
+// Execution groups.  A group runs one fused kernel sequence and
+// materialises exactly one layer output (`out`); layers inside a group whose
+// outputs feed nothing else are never stored.
+enum GKind { G_CONV, G_BNACT, G_RELU, G_ADD, G_MAXPOOL, G_GAP, G_LINEAR, G_HEAD };
+struct Group {
+    GKind kind = G_CONV;
+    int out = -1;       // the layer whose output this group stores
+    int a = -1;         // G_CONV: conv; G_BNACT: first BN; G_HEAD: pool; else: the layer
+    int stats_bn = -1;  // G_CONV: BN whose batch statistics the conv epilogue computes
+    int bn2 = -1;       // G_BNACT: BN of the other branch of the residual add (both normalised)
+    int add = -1;       // G_BNACT: the residual add, if any
+    int res = -1;       // G_BNACT: the residual tensor added unnormalised, if any
+    int relu = -1;      // G_BNACT: the closing ReLU, if any
+    int lin = -1;       // G_HEAD: the linear layer
+};
+
 struct Model {
     lpp_model_desc desc{};
     std::vector<Layer> layers;
@@ -71,6 +87,10 @@ struct Model {
     int img_cp = 0;               // stored channels of the image
     double fwd_flops = 0;
     std::vector<Plan> plans;      // per partition 0..P
+    std::vector<std::vector<int>> consumers;
+    std::vector<Group> groups;    // in execution order
+    std::vector<char> stored;     // layer output materialised
+    std::vector<int> stats_from;  // BN: conv whose epilogue computes its statistics, or -1
 };
 
 int ceil4(int c) { return (c + 3) / 4 * 4; }
@@ -249,7 +269,88 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
             }
         }
     }
+    M.consumers.assign(n, {});
+    for (int l = 0; l < n; ++l) {
+        const lpp_layer& L = M.layers[l].L;
+        if (L.in0 >= 0) M.consumers[L.in0].push_back(l);
+        if (L.op == LPP_ADD && L.in1 >= 0 && L.in1 != L.in0) M.consumers[L.in1].push_back(l);
+    }
     return LPP_OK;
+}
+
+// Groups the layers for execution.  fused = false gives one group per layer
+// (every activation stored).  Fused patterns:
+//   conv whose only consumer is a BN: the conv epilogue computes the BN's
+//     batch statistics;
+//   BN [-> residual add (+ tensor | + another BN's output)] [-> ReLU], each
+//     link the only consumer of the previous: one elementwise pass forward,
+//     one masked reduce + apply pair backward;
+//   global average pool -> linear (the logits): one head kernel with the
+//     softmax cross-entropy.
+void build_groups(Model& M, bool fused) {
+    const int n = (int)M.layers.size();
+    auto op = [&](int l) { return M.layers[l].L.op; };
+    auto sole = [&](int l) { return M.consumers[l].size() == 1 ? M.consumers[l][0] : -1; };
+    M.groups.clear();
+    M.stored.assign(n, 0);
+    M.stats_from.assign(n, -1);
+    std::vector<char> taken(n, 0);
+    std::vector<Group> gs;
+    for (int l = 0; l < n; ++l) {
+        if (taken[l]) continue;
+        Group g;
+        const int op_l = op(l);
+        if (op_l == LPP_CONV) {
+            g.kind = G_CONV;
+            g.a = g.out = l;
+            const int c = sole(l);
+            if (fused && c >= 0 && op(c) == LPP_BN) {
+                g.stats_bn = c;
+                M.stats_from[c] = l;
+            }
+        } else if (op_l == LPP_BN) {
+            g.kind = G_BNACT;
+            g.a = g.out = l;
+            const int c = fused ? sole(l) : -1;
+            if (c >= 0 && op(c) == LPP_RELU && !taken[c]) {
+                g.relu = g.out = c;
+            } else if (c >= 0 && op(c) == LPP_ADD && !taken[c] && M.layers[c].L.in0 != M.layers[c].L.in1) {
+                const lpp_layer& A = M.layers[c].L;
+                const int other = A.in0 == l ? A.in1 : A.in0;
+                g.add = g.out = c;
+                if (other >= 0 && op(other) == LPP_BN && sole(other) == c && !taken[other])
+                    g.bn2 = other;
+                else
+                    g.res = other;
+                const int r = sole(c);
+                if (r >= 0 && op(r) == LPP_RELU && !taken[r]) g.relu = g.out = r;
+            }
+        } else if (op_l == LPP_GAP) {
+            const int c = fused ? sole(l) : -1;
+            if (c == n - 1 && op(c) == LPP_LINEAR) {
+                g.kind = G_HEAD;
+                g.a = l;
+                g.lin = g.out = c;
+            } else {
+                g.kind = G_GAP;
+                g.a = g.out = l;
+            }
+        } else {
+            g.kind = op_l == LPP_RELU ? G_RELU : op_l == LPP_ADD ? G_ADD : op_l == LPP_MAXPOOL ? G_MAXPOOL
+                                                                                              : G_LINEAR;
+            g.a = g.out = l;
+        }
+        for (int x : {g.a, g.bn2, g.add, g.relu, g.lin})
+            if (x >= 0) taken[x] = 1;
+        gs.push_back(g);
+    }
+    // a group runs when its last layer's inputs exist: order by output layer
+    std::stable_sort(gs.begin(), gs.end(), [](const Group& x, const Group& y) { return x.out < y.out; });
+    M.groups = gs;
+    for (auto& g : M.groups) {
+        M.stored[g.out] = 1;
+        if (g.kind == G_HEAD) M.stored[g.a] = 1;   // the pooled features, kept for the weight gradient
+    }
 }
 
 // ------------------------------------------------------------------------
@@ -274,9 +375,12 @@ struct Worker {
     float* m = nullptr;
     float* loss = nullptr;
     float* img = nullptr;
-    double* red0 = nullptr;
-    double* red1 = nullptr;
+    float* ps0 = nullptr;   // per-tile partial statistics (3 arrays)
+    float* ps1 = nullptr;
+    float* ps2 = nullptr;
     float* wpart = nullptr;
+    lpp::StepArgs* args = nullptr;          // device: this step's images, labels, lr
+    std::vector<hipGraphExec_t> graphs;     // one per partition, captured on first use
     int last_partition = -1;
 };
 
@@ -294,8 +398,10 @@ struct lpp_ctx {
     int n_snap = 0;
     long wbuf_floats = 0;
     size_t ws_bytes = 0;
-    size_t off_v = 0, off_wbuf = 0, off_g = 0, off_m = 0, off_loss = 0, off_img = 0, off_red0 = 0, off_red1 = 0,
-           off_wpart = 0;
+    size_t off_v = 0, off_wbuf = 0, off_g = 0, off_m = 0, off_loss = 0, off_img = 0, off_ps = 0, off_wpart = 0,
+           off_args = 0;
+    bool graphs = true;
+    long ps_floats = 0;
     std::unique_ptr<std::atomic<long>[]> counters;
     Timer timer;
     int device = 0;
@@ -361,6 +467,8 @@ void destroy_ctx(lpp_ctx* c) {
     hipSetDevice(c->device);
     for (auto& w : c->workers) {
         if (w.stream) hipStreamSynchronize(w.stream);
+        for (auto g : w.graphs)
+            if (g) hipGraphExecDestroy(g);
         if (w.ws) hipFree(w.ws);
         if (w.own_stream && w.stream) hipStreamDestroy(w.stream);
     }
@@ -376,64 +484,117 @@ void destroy_ctx(lpp_ctx* c) {
     delete c;
 }
 
+// Batch-norm statistics of BN layer b into its aux (mean, rstd, scale,
+// shift), from the input tensor (when no conv epilogue computed them).
+int bn_stats_standalone(lpp_ctx* c, Worker& w, int b) {
+    Model& M = c->M;
+    Layer& B = M.layers[b];
+    const int N = M.desc.batch, C = B.out.c;
+    const long rows = (long)N * B.in0.h * B.in0.w;
+    const float* x = c->act(w, B.L.in0);
+    float* ax = c->aux(w, b);
+    hipStream_t st = w.stream;
+    LAUNCH("bn_stats", 4.0 * rows * C, st, lpp::launch_stats_partial(x, rows, C, w.ps0, w.ps1, st));
+    LAUNCH("bn_stats", 0.0, st,
+           lpp::launch_stats_finalize(w.ps0, w.ps1, lpp::stats_tiles(rows), lpp::kStatRows, rows, C, w.v + B.poff,
+                                      w.v + B.poff + C, M.desc.bn_eps, ax, ax + C, ax + 2 * C, ax + 3 * C, st));
+    return LPP_OK;
+}
+
 // Forward pass of worker w at its snapshot; loss and dlogits at the end.
-int run_forward(lpp_ctx* c, Worker& w, const lpp_batch* b) {
+int run_forward(lpp_ctx* c, Worker& w) {
     Model& M = c->M;
     const int N = M.desc.batch;
     hipStream_t st = w.stream;
     LAUNCH("image", 8.0 * N * M.desc.in_c * M.desc.in_h * M.desc.in_w, st,
-           lpp::launch_nchw_to_nhwc(b->images, w.img, N, M.desc.in_c, M.desc.in_h, M.desc.in_w, M.img_cp, st));
-    for (int l = 0; l < (int)M.layers.size(); ++l) {
-        Layer& Y = M.layers[l];
+           lpp::launch_nchw_to_nhwc(w.args, w.img, N, M.desc.in_c, M.desc.in_h, M.desc.in_w, M.img_cp, st));
+    bool loss_done = false;
+    for (const Group& G : M.groups) {
+        Layer& Y = M.layers[G.a];
         const float* x0 = Y.L.in0 < 0 ? w.img : c->act(w, Y.L.in0);
-        float* y = c->act(w, l);
         const long Mrows = (long)N * Y.in0.h * Y.in0.w;
-        switch (Y.L.op) {
-        case LPP_CONV: {
+        switch (G.kind) {
+        case G_CONV: {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride, Y.L.pad};
             const float* bias = Y.L.bias ? w.v + Y.poff + Y.wcount : nullptr;
+            const bool st_on = G.stats_bn >= 0;
             LAUNCH("conv_fwd", 2.0 * Y.macs, st,
-                   lpp::launch_conv_igemm(lpp::CONV_FWD, x0, w.wbuf + Y.wf_off, bias, y, g, false, st));
+                   lpp::launch_conv_igemm(lpp::CONV_FWD, x0, w.wbuf + Y.wf_off, bias, c->act(w, G.a), g, false,
+                                          st_on ? w.ps0 : nullptr, st_on ? w.ps1 : nullptr, st));
+            if (st_on) {
+                const Layer& B = M.layers[G.stats_bn];
+                const long rows = (long)N * Y.out.h * Y.out.w;
+                const int R = lpp::conv_tile_rows(g);
+                const int T = (int)((rows + R - 1) / R);
+                float* ax = c->aux(w, G.stats_bn);
+                LAUNCH("bn_stats", 0.0, st,
+                       lpp::launch_stats_finalize(w.ps0, w.ps1, T, R, rows, Y.L.cout, w.v + B.poff,
+                                                  w.v + B.poff + Y.L.cout, M.desc.bn_eps, ax, ax + Y.L.cout,
+                                                  ax + 2 * Y.L.cout, ax + 3 * Y.L.cout, st));
+            }
             break;
         }
-        case LPP_BN: {
+        case G_BNACT: {
             const int C = Y.out.c;
-            float* ax = c->aux(w, l);   // mean, rstd, scale, shift, a, mdy, mdyx
-            const int nb = lpp::chan_reduce_blocks(Mrows, C);
-            LAUNCH("bn_stats", 4.0 * Mrows * C, st, lpp::launch_bn_stats_partial(x0, Mrows, C, w.red0, w.red1, st));
-            LAUNCH("bn_stats", 0.0, st,
-                   lpp::launch_bn_stats_finalize(w.red0, w.red1, nb, Mrows, C, w.v + Y.poff, w.v + Y.poff + C,
-                                                 M.desc.bn_eps, ax, ax + C, ax + 2 * C, ax + 3 * C, st));
-            LAUNCH("bn_apply", 8.0 * Mrows * C, st, lpp::launch_chan_affine(x0, ax + 2 * C, ax + 3 * C, y, Mrows, C, st));
+            if (M.stats_from[G.a] < 0) {
+                int rc = bn_stats_standalone(c, w, G.a);
+                if (rc) return rc;
+            }
+            if (G.bn2 >= 0 && M.stats_from[G.bn2] < 0) {
+                int rc = bn_stats_standalone(c, w, G.bn2);
+                if (rc) return rc;
+            }
+            const float* ax = c->aux(w, G.a);
+            const float* ax2 = G.bn2 >= 0 ? c->aux(w, G.bn2) : nullptr;
+            const float* x2 = G.bn2 >= 0 ? c->act(w, M.layers[G.bn2].L.in0) : nullptr;
+            const float* r = G.res >= 0 ? c->act(w, G.res) : nullptr;
+            const double bytes = 8.0 * Mrows * C + (r || x2 ? 4.0 * Mrows * C : 0.0);
+            LAUNCH("bn_act", bytes, st,
+                   lpp::launch_bn_act(x0, ax + 2 * C, ax + 3 * C, r, x2, ax2 ? ax2 + 2 * C : nullptr,
+                                      ax2 ? ax2 + 3 * C : nullptr, G.relu >= 0, c->act(w, G.out), Mrows, C, st));
             break;
         }
-        case LPP_RELU:
-            LAUNCH("relu", 8.0 * Mrows * Y.out.c, st, lpp::launch_relu_fwd(x0, y, Mrows * Y.out.c, st));
+        case G_RELU:
+            LAUNCH("relu", 8.0 * Mrows * Y.out.c, st, lpp::launch_relu_fwd(x0, c->act(w, G.a), Mrows * Y.out.c, st));
             break;
-        case LPP_ADD:
+        case G_ADD:
             LAUNCH("add", 12.0 * Mrows * Y.out.c, st,
-                   lpp::launch_add_fwd(x0, c->act(w, Y.L.in1), y, Mrows * Y.out.c, st));
+                   lpp::launch_add_fwd(x0, c->act(w, Y.L.in1), c->act(w, G.a), Mrows * Y.out.c, st));
             break;
-        case LPP_MAXPOOL:
+        case G_MAXPOOL:
             LAUNCH("maxpool", 4.0 * Mrows * Y.out.c, st,
-                   lpp::launch_maxpool_fwd(x0, y, (uint8_t*)c->aux(w, l), N, Y.in0.h, Y.in0.w, Y.in0.c, Y.out.h,
-                                           Y.out.w, Y.L.k, Y.L.stride, Y.L.pad, st));
+                   lpp::launch_maxpool_fwd(x0, c->act(w, G.a), (uint8_t*)c->aux(w, G.a), N, Y.in0.h, Y.in0.w,
+                                           Y.in0.c, Y.out.h, Y.out.w, Y.L.k, Y.L.stride, Y.L.pad, st));
             break;
-        case LPP_GAP:
+        case G_GAP:
             LAUNCH("gap", 4.0 * Mrows * Y.out.c, st,
-                   lpp::launch_gap_fwd(x0, y, N, Y.in0.h * Y.in0.w, Y.in0.c, st));
+                   lpp::launch_gap_fwd(x0, c->act(w, G.a), N, Y.in0.h * Y.in0.w, Y.in0.c, st));
             break;
-        case LPP_LINEAR: {
+        case G_LINEAR: {
             const float* W = w.v + Y.poff;
             const float* bias = Y.L.bias ? W + Y.wcount : nullptr;
-            LAUNCH("linear", 2.0 * Y.macs, st, lpp::launch_linear_fwd(x0, W, bias, y, N, Y.L.cin, Y.L.cout, st));
+            LAUNCH("linear", 2.0 * Y.macs, st,
+                   lpp::launch_linear_fwd(x0, W, bias, c->act(w, G.a), N, Y.L.cin, Y.L.cout, st));
+            break;
+        }
+        case G_HEAD: {
+            const Layer& L = M.layers[G.lin];
+            const float* W = w.v + L.poff;
+            LAUNCH("head", 4.0 * Mrows * Y.in0.c + 2.0 * L.macs, st,
+                   lpp::launch_head_fwd(x0, N, Y.in0.h * Y.in0.w, Y.in0.c, W, L.L.bias ? W + L.wcount : nullptr,
+                                        L.L.cout, w.args, c->act(w, G.a), c->act(w, G.lin), c->dact(w, G.lin),
+                                        w.loss + 1, st));
+            loss_done = true;
             break;
         }
         }
     }
-    const int last = (int)M.layers.size() - 1;
-    LAUNCH("softmax_ce", 0.0, st,
-           lpp::launch_softmax_ce(c->act(w, last), b->labels, c->dact(w, last), w.loss, N, M.desc.n_classes, st));
+    if (!loss_done) {
+        const int last = (int)M.layers.size() - 1;
+        LAUNCH("softmax_ce", 0.0, st,
+               lpp::launch_softmax_ce(c->act(w, last), w.args, c->dact(w, last), w.loss, N, M.desc.n_classes,
+                                      st));
+    }
     return LPP_OK;
 }
 
@@ -444,16 +605,18 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
     const Plan& pl = M.plans[partition];
     const int N = M.desc.batch;
     hipStream_t st = w.stream;
-    for (int l = (int)M.layers.size() - 1; l >= 0; --l) {
-        if (!pl.run[l]) continue;
-        Layer& Y = M.layers[l];
+    bool loss_done = false;
+    for (int gi = (int)M.groups.size() - 1; gi >= 0; --gi) {
+        const Group& G = M.groups[gi];
+        if (!pl.run[G.out]) continue;
+        Layer& Y = M.layers[G.a];
         const float* x0 = Y.L.in0 < 0 ? w.img : c->act(w, Y.L.in0);
-        float* dy = c->dact(w, l);
-        float* dx0 = pl.din0[l] ? c->dact(w, Y.L.in0) : nullptr;
+        float* dy = c->dact(w, G.out);
+        float* dx0 = pl.din0[G.a] ? c->dact(w, Y.L.in0) : nullptr;
         const long Min = (long)N * Y.in0.h * Y.in0.w;
-        switch (Y.L.op) {
-        case LPP_CONV: {
-            if (pl.wgrad[l]) {
+        switch (G.kind) {
+        case G_CONV: {
+            if (pl.wgrad[G.a]) {
                 const int Ktot = Y.L.k * Y.L.k * Y.cin_p;
                 LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
                        lpp::launch_conv_wgrad(dy, x0, w.wpart, N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w,
@@ -462,12 +625,13 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                        lpp::launch_wgrad_reduce(w.wpart, Y.wg.splits, Y.L.cout, Ktot, Y.L.cin, Y.cin_p, Y.L.k,
                                                 Y.L.k, w.g + Y.poff, st));
                 if (Y.L.bias) {
+                    // column sums of dY, from per-tile means
                     const long Mo = (long)N * Y.out.h * Y.out.w;
-                    const int nb = lpp::chan_reduce_blocks(Mo, Y.L.cout);
                     LAUNCH("bias_grad", 4.0 * Mo * Y.L.cout, st,
-                           lpp::launch_col_sum_partial(dy, Mo, Y.L.cout, w.red0, st));
+                           lpp::launch_stats_partial(dy, Mo, Y.L.cout, w.ps0, w.ps1, st));
                     LAUNCH("bias_grad", 0.0, st,
-                           lpp::launch_col_sum_finalize(w.red0, nb, Y.L.cout, w.g + Y.poff + Y.wcount, st));
+                           lpp::launch_sum_from_tiles(w.ps0, lpp::stats_tiles(Mo), lpp::kStatRows, Mo, Y.L.cout,
+                                                      w.g + Y.poff + Y.wcount, st));
                 }
             }
             if (dx0) {
@@ -475,64 +639,132 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                                 Y.L.pad};
                 LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
                        lpp::launch_conv_igemm(lpp::CONV_DGRAD, dy, w.wbuf + Y.wd_off, nullptr, dx0, g,
-                                              pl.acc0[l] != 0, st));
+                                              pl.acc0[G.a] != 0, nullptr, nullptr, st));
             }
             break;
         }
-        case LPP_BN: {
+        case G_BNACT: {
             const int C = Y.out.c;
-            float* ax = c->aux(w, l);
-            const int nb = lpp::chan_reduce_blocks(Min, C);
-            LAUNCH("bn_bwd", 8.0 * Min * C, st,
-                   lpp::launch_bn_bwd_partial(dy, x0, ax, ax + C, Min, C, w.red0, w.red1, st));
-            float* gg = pl.wgrad[l] ? w.g + Y.poff : nullptr;
-            float* gb = pl.wgrad[l] ? w.g + Y.poff + C : nullptr;
-            LAUNCH("bn_bwd", 0.0, st,
-                   lpp::launch_bn_bwd_finalize(w.red0, w.red1, nb, Min, C, w.v + Y.poff, ax + C, gg, gb, ax + 4 * C,
-                                               ax + 5 * C, ax + 6 * C, st));
-            if (dx0)
-                LAUNCH("bn_bwd", 12.0 * Min * C, st,
-                       lpp::launch_bn_bwd_data(dy, x0, ax, ax + C, ax + 4 * C, ax + 5 * C, ax + 6 * C, dx0, Min, C,
-                                               pl.acc0[l] != 0, st));
+            const int b2 = G.bn2;
+            const bool want1 = pl.run[G.a] && (pl.wgrad[G.a] || pl.din0[G.a]);
+            const bool want2 = b2 >= 0 && pl.run[b2] && (pl.wgrad[b2] || pl.din0[b2]);
+            bool want_res = false, acc_res = false;
+            if (G.res >= 0) {
+                const lpp_layer& A = M.layers[G.add].L;
+                want_res = A.in0 == G.res ? pl.din0[G.add] : pl.din1[G.add];
+                acc_res = A.in0 == G.res ? pl.acc0[G.add] : pl.acc1[G.add];
+            }
+            float* ax = c->aux(w, G.a);
+            float* ax2 = b2 >= 0 ? c->aux(w, b2) : nullptr;
+            const Layer* Y2 = b2 >= 0 ? &M.layers[b2] : nullptr;
+            lpp::BnBwdArgs a{dy, G.relu >= 0 ? c->act(w, G.out) : nullptr, x0, ax, ax + C,
+                             want2 ? c->act(w, Y2->L.in0) : nullptr, want2 ? ax2 : nullptr,
+                             want2 ? ax2 + C : nullptr, Min, C};
+            if (want1 || want2) {
+                const int T = lpp::stats_tiles(Min);
+                LAUNCH("bn_bwd", (a.mask ? 12.0 : 8.0) * Min * C + (want2 ? 4.0 * Min * C : 0.0), st,
+                       lpp::launch_bn_bwd_reduce(a, w.ps0, w.ps1, w.ps2, st));
+                float* gg1 = pl.wgrad[G.a] ? w.g + Y.poff : nullptr;
+                float* gb1 = pl.wgrad[G.a] ? w.g + Y.poff + C : nullptr;
+                float* gg2 = want2 && pl.wgrad[b2] ? w.g + Y2->poff : nullptr;
+                float* gb2 = want2 && pl.wgrad[b2] ? w.g + Y2->poff + C : nullptr;
+                LAUNCH("bn_bwd", 0.0, st,
+                       lpp::launch_bn_bwd_finalize(w.ps0, w.ps1, w.ps2, T, Min, C, w.v + Y.poff, ax + C, gg1, gb1,
+                                                   ax + 4 * C, want2 ? w.v + Y2->poff : nullptr,
+                                                   want2 ? ax2 + C : nullptr, gg2, gb2,
+                                                   want2 ? ax2 + 4 * C : nullptr, st));
+            }
+            float* d1 = want1 && pl.din0[G.a] ? dx0 : nullptr;
+            float* d2 = want2 && pl.din0[b2] ? c->dact(w, Y2->L.in0) : nullptr;
+            float* dr = want_res ? c->dact(w, G.res) : nullptr;
+            if (d1 || d2 || dr) {
+                const double bytes = ((a.mask ? 8.0 : 4.0) + (d1 ? 12.0 : 0.0) + (d2 ? 12.0 : 0.0) +
+                                      (dr ? (acc_res ? 8.0 : 4.0) : 0.0)) * Min * C;
+                LAUNCH("bn_bwd", bytes, st,
+                       lpp::launch_bn_bwd_apply(a, ax + 4 * C, want2 ? ax2 + 4 * C : nullptr, d1, pl.acc0[G.a] != 0,
+                                                d2, want2 && pl.acc0[b2] != 0, dr, acc_res, st));
+            }
             break;
         }
-        case LPP_RELU:
+        case G_RELU:
             if (dx0)
                 LAUNCH("relu", 12.0 * Min * Y.out.c, st,
-                       lpp::launch_relu_bwd(dy, x0, dx0, Min * Y.out.c, pl.acc0[l] != 0, st));
+                       lpp::launch_relu_bwd(dy, x0, dx0, Min * Y.out.c, pl.acc0[G.a] != 0, st));
             break;
-        case LPP_ADD:
+        case G_ADD:
             if (dx0)
                 LAUNCH("add", 8.0 * Min * Y.out.c, st,
-                       lpp::launch_copy_acc(dy, dx0, Min * Y.out.c, pl.acc0[l] != 0, st));
-            if (pl.din1[l])
+                       lpp::launch_copy_acc(dy, dx0, Min * Y.out.c, pl.acc0[G.a] != 0, st));
+            if (pl.din1[G.a])
                 LAUNCH("add", 8.0 * Min * Y.out.c, st,
-                       lpp::launch_copy_acc(dy, c->dact(w, Y.L.in1), Min * Y.out.c, pl.acc1[l] != 0, st));
+                       lpp::launch_copy_acc(dy, c->dact(w, Y.L.in1), Min * Y.out.c, pl.acc1[G.a] != 0, st));
             break;
-        case LPP_MAXPOOL:
+        case G_MAXPOOL:
             if (dx0)
                 LAUNCH("maxpool", 8.0 * Min * Y.out.c, st,
-                       lpp::launch_maxpool_bwd(dy, (const uint8_t*)c->aux(w, l), dx0, N, Y.in0.h, Y.in0.w, Y.in0.c,
-                                               Y.out.h, Y.out.w, Y.L.k, Y.L.stride, Y.L.pad, pl.acc0[l] != 0, st));
+                       lpp::launch_maxpool_bwd(dy, (const uint8_t*)c->aux(w, G.a), dx0, N, Y.in0.h, Y.in0.w,
+                                               Y.in0.c, Y.out.h, Y.out.w, Y.L.k, Y.L.stride, Y.L.pad,
+                                               pl.acc0[G.a] != 0, st));
             break;
-        case LPP_GAP:
+        case G_GAP:
             if (dx0)
                 LAUNCH("gap", 4.0 * Min * Y.in0.c, st,
-                       lpp::launch_gap_bwd(dy, dx0, N, Y.in0.h * Y.in0.w, Y.in0.c, pl.acc0[l] != 0, st));
+                       lpp::launch_gap_bwd(dy, dx0, N, Y.in0.h * Y.in0.w, Y.in0.c, pl.acc0[G.a] != 0, st));
             break;
-        case LPP_LINEAR: {
+        case G_LINEAR: {
             const float* W = w.v + Y.poff;
-            if (pl.wgrad[l])
+            if (pl.wgrad[G.a])
                 LAUNCH("linear", 2.0 * Y.macs, st,
                        lpp::launch_linear_bwd_w(dy, x0, w.g + Y.poff, Y.L.bias ? w.g + Y.poff + Y.wcount : nullptr,
                                                 N, Y.L.cin, Y.L.cout, st));
             if (dx0)
                 LAUNCH("linear", 2.0 * Y.macs, st,
-                       lpp::launch_linear_bwd_x(dy, W, dx0, N, Y.L.cin, Y.L.cout, pl.acc0[l] != 0, st));
+                       lpp::launch_linear_bwd_x(dy, W, dx0, N, Y.L.cin, Y.L.cout, pl.acc0[G.a] != 0, st));
+            break;
+        }
+        case G_HEAD: {
+            const Layer& L = M.layers[G.lin];
+            const bool wg = pl.wgrad[G.lin];
+            LAUNCH("head", wg ? 2.0 * L.macs : 0.0, st,
+                   lpp::launch_head_bwd_w(dy, c->act(w, G.a), N, L.L.cin, L.L.cout, wg ? w.g + L.poff : nullptr,
+                                          wg && L.L.bias ? w.g + L.poff + L.wcount : nullptr, w.loss + 1, w.loss,
+                                          st));
+            loss_done = true;
+            if (dx0)
+                LAUNCH("head", 2.0 * L.macs + 4.0 * Min * Y.in0.c, st,
+                       lpp::launch_head_bwd_x(dy, w.v + L.poff, N, Y.in0.h * Y.in0.w, Y.in0.c, L.L.cout, dx0,
+                                              pl.acc0[G.a] != 0, st));
             break;
         }
         }
     }
+    // the batch-mean loss, where the fused head's backward did not produce it
+    bool head = false;
+    for (const Group& G : M.groups) head |= G.kind == G_HEAD;
+    if (head && !loss_done)
+        LAUNCH("head", 0.0, st,
+               lpp::launch_head_bwd_w(nullptr, nullptr, N, 1, 1, nullptr, nullptr, w.loss + 1, w.loss, st));
+    return LPP_OK;
+}
+
+// The device work of one updater iteration on the worker's stream: snapshot
+// of the replica, forward, truncated backward, block update.  Per-step
+// arguments are read from w.args.
+int enqueue_step(lpp_ctx* c, Worker& w, int worker, int partition) {
+    const int q = worker / c->P;
+    float* xq = c->replicas + (long)q * c->dpad;
+    const long d = c->M.d;
+    hipStream_t st = w.stream;
+    LAUNCH("snapshot", 8.0 * d, st, lpp::launch_snapshot(xq, w.v, d, c->snap_dev, c->n_snap, w.wbuf, st));
+    int rc = run_forward(c, w);
+    if (rc) return rc;
+    rc = run_backward(c, w, partition);
+    if (rc) return rc;
+    const long lo = c->M.blo[partition], hi = c->M.bhi[partition];
+    const bool mom = c->M.desc.momentum != 0.f;
+    LAUNCH("sgd_update", (mom ? 20.0 : 12.0) * (hi - lo), st,
+           lpp::launch_sgd_update(xq, mom ? w.m : nullptr, w.g, lo, hi, w.args, 0.f, c->M.desc.momentum,
+                                  c->M.desc.weight_decay, st));
     return LPP_OK;
 }
 
@@ -574,6 +806,8 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
     c->P = P;
     c->mode = opt ? opt->mode : LPP_SEQUENTIAL;
     if (c->mode != LPP_SEQUENTIAL && c->mode != LPP_ASYNC) return fail(LPP_EINVAL, "unknown mode");
+    build_groups(c->M, !(opt && opt->unfused));
+    c->graphs = !(opt && opt->no_graphs);
     HIPCHK(hipGetDevice(&c->device));
     Model& M = c->M;
     const int N = M.desc.batch;
@@ -609,23 +843,31 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
     c->off_g = take(sizeof(float) * c->dpad);
     c->off_m = take(sizeof(float) * c->dpad);
     c->off_loss = take(sizeof(float) * (1 + N));
+    c->off_args = take(sizeof(lpp::StepArgs));
     c->off_img = take(sizeof(float) * (size_t)N * M.desc.in_h * M.desc.in_w * M.img_cp);
-    long red_rows = 1, wpart = 1;
-    for (auto& Y : M.layers) {
+    long ps = 1, wpart = 1;
+    for (int l = 0; l < (int)M.layers.size(); ++l) {
+        Layer& Y = M.layers[l];
         const long rows_out = (long)N * Y.out.h * Y.out.w;
-        Y.act = take(sizeof(float) * (size_t)rows_out * Y.out.c);
-        Y.dact = take(sizeof(float) * (size_t)rows_out * Y.out.c);
+        if (M.stored[l]) {
+            Y.act = take(sizeof(float) * (size_t)rows_out * Y.out.c);
+            Y.dact = take(sizeof(float) * (size_t)rows_out * Y.out.c);
+        }
         if (Y.L.op == LPP_BN) Y.aux = take(sizeof(float) * 7 * Y.out.c);
         if (Y.L.op == LPP_MAXPOOL) Y.aux = take((size_t)rows_out * Y.out.c);
         const long rin = (long)N * Y.in0.h * Y.in0.w;
-        if (Y.L.op == LPP_BN) red_rows = std::max<long>(red_rows, (long)lpp::chan_reduce_blocks(rin, Y.out.c) * Y.out.c);
+        if (Y.L.op == LPP_BN) ps = std::max<long>(ps, (long)lpp::stats_tiles(rin) * Y.out.c);
         if (Y.L.op == LPP_CONV) {
-            red_rows = std::max<long>(red_rows, (long)lpp::chan_reduce_blocks(rows_out, Y.out.c) * Y.out.c);
+            lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
+                            Y.L.pad};
+            const long tiles = (rows_out + lpp::conv_tile_rows(g) - 1) / lpp::conv_tile_rows(g);
+            ps = std::max<long>(ps, tiles * Y.L.cout);
+            ps = std::max<long>(ps, (long)lpp::stats_tiles(rows_out) * Y.L.cout);
             wpart = std::max<long>(wpart, Y.wg.part_floats);
         }
     }
-    c->off_red0 = take(sizeof(double) * red_rows);
-    c->off_red1 = take(sizeof(double) * red_rows);
+    c->ps_floats = ps;
+    c->off_ps = take(sizeof(float) * 3 * ps);
     c->off_wpart = take(sizeof(float) * wpart);
     c->ws_bytes = off;
 
@@ -658,9 +900,12 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         w.m = (float*)(w.ws + c->off_m);
         w.loss = (float*)(w.ws + c->off_loss);
         w.img = (float*)(w.ws + c->off_img);
-        w.red0 = (double*)(w.ws + c->off_red0);
-        w.red1 = (double*)(w.ws + c->off_red1);
+        w.ps0 = (float*)(w.ws + c->off_ps);
+        w.ps1 = w.ps0 + c->ps_floats;
+        w.ps2 = w.ps1 + c->ps_floats;
         w.wpart = (float*)(w.ws + c->off_wpart);
+        w.args = (lpp::StepArgs*)(w.ws + c->off_args);
+        w.graphs.assign(P + 1, nullptr);
     }
     if (opt && opt->avg_stream) {
         c->avg_stream = (hipStream_t)opt->avg_stream;
@@ -689,19 +934,39 @@ int lpp_step(lpp_ctx* c, int worker, const lpp_batch* batch, int partition, floa
     Worker& w = c->workers[worker];
     const int q = worker / c->P;
     c->counters[q].fetch_add(1);                 // s := read&inc(C^q)
-    float* xq = c->replicas + (long)q * c->dpad;
-    const long d = c->M.d;
     hipStream_t st = w.stream;
-    LAUNCH("snapshot", 8.0 * d, st, lpp::launch_snapshot(xq, w.v, d, c->snap_dev, c->n_snap, w.wbuf, st));
-    rc = run_forward(c, w, batch);
-    if (rc) return rc;
-    rc = run_backward(c, w, partition);
-    if (rc) return rc;
-    const long lo = c->M.blo[partition], hi = c->M.bhi[partition];
-    const bool mom = c->M.desc.momentum != 0.f;
-    LAUNCH("sgd_update", (mom ? 20.0 : 12.0) * (hi - lo), st,
-           lpp::launch_sgd_update(xq, mom ? w.m : nullptr, w.g, lo, hi, lr, c->M.desc.momentum,
-                                  c->M.desc.weight_decay, st));
+    LAUNCH("args", 0.0, st, lpp::launch_set_step_args(w.args, batch->images, batch->labels, lr, st));
+    bool timing;
+    {
+        std::lock_guard<std::mutex> g(c->timer.mu);
+        timing = !c->timer.family.empty();
+    }
+    if (c->graphs && !timing) {
+        // one graph per (worker, partition): snapshot, forward, truncated
+        // backward and update, captured once and replayed
+        hipGraphExec_t& ge = w.graphs[partition];
+        if (!ge) {
+            HIPCHK(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+            rc = enqueue_step(c, w, worker, partition);
+            hipGraph_t graph = nullptr;
+            hipError_t e = hipStreamEndCapture(st, &graph);
+            if (rc) {
+                if (graph) hipGraphDestroy(graph);
+                return rc;
+            }
+            if (e != hipSuccess) return fail(LPP_EHIP, std::string("stream capture: ") + hipGetErrorString(e));
+            e = hipGraphInstantiate(&ge, graph, nullptr, nullptr, 0);
+            hipGraphDestroy(graph);
+            if (e != hipSuccess) {
+                ge = nullptr;
+                return fail(LPP_EHIP, std::string("graph instantiate: ") + hipGetErrorString(e));
+            }
+        }
+        HIPCHK(hipGraphLaunch(ge, st));
+    } else {
+        rc = enqueue_step(c, w, worker, partition);
+        if (rc) return rc;
+    }
     w.last_partition = partition;
     if (c->mode == LPP_SEQUENTIAL) HIPCHK(hipStreamSynchronize(st));
     return LPP_OK;
@@ -819,19 +1084,52 @@ static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* 
     int rc = check_worker(c, worker);
     if (rc) return rc;
     if (layer < 0 || layer >= (int)c->M.layers.size()) return fail(LPP_EINVAL, "layer out of range");
-    const Layer& Y = c->M.layers[layer];
-    const int N = c->M.desc.batch;
+    const Model& M = c->M;
+    const Layer& Y = M.layers[layer];
+    const int N = M.desc.batch;
     const long want = (long)N * Y.out.numel();
     if (!host || n != want) return fail(LPP_EINVAL, "n must be batch * c * h * w of the layer");
     Worker& w = c->workers[worker];
-    if (grad && (w.last_partition < 0 || !c->M.plans[w.last_partition].run[layer]))
+    // a fused-away output of a batch-norm group is rebuilt from the group's
+    // stored inputs and batch-norm coefficients (the group's own expression
+    // without its ReLU)
+    const Group* G = nullptr;
+    if (!M.stored[layer]) {
+        for (const Group& g : M.groups)
+            if (g.kind == G_BNACT && (layer == g.a || layer == g.add || layer == g.bn2)) G = &g;
+        if (grad || !G) return fail(LPP_ESTATE, "this layer's output is fused away (create the context with unfused = 1)");
+    }
+    if (grad && (w.last_partition < 0 || !M.plans[w.last_partition].run[layer]))
         return fail(LPP_ESTATE, "the last step's backward pass did not reach this layer");
     rc = sync_all(c);
     if (rc) return rc;
     float* tmp = nullptr;
-    if (hipMalloc((void**)&tmp, sizeof(float) * n) != hipSuccess) return fail(LPP_ENOMEM, "temporary allocation");
-    const float* src = grad ? c->dact(w, layer) : c->act(w, layer);
-    hipError_t e = lpp::launch_nhwc_to_nchw(src, tmp, N, Y.out.c, Y.out.h, Y.out.w, Y.out.c, w.stream);
+    if (hipMalloc((void**)&tmp, sizeof(float) * n * (G ? 2 : 1)) != hipSuccess)
+        return fail(LPP_ENOMEM, "temporary allocation");
+    const float* src = grad ? c->dact(w, layer) : nullptr;
+    hipError_t e = hipSuccess;
+    if (G) {
+        const int C = Y.out.c;
+        const long rows = (long)N * Y.out.h * Y.out.w;
+        const int b = layer == G->bn2 ? G->bn2 : G->a;
+        const float* ax = c->aux(w, b);
+        const float* x = c->act(w, M.layers[b].L.in0);
+        const float *r = nullptr, *x2 = nullptr, *s2 = nullptr, *t2 = nullptr;
+        if (layer == G->add) {
+            r = G->res >= 0 ? c->act(w, G->res) : nullptr;
+            if (G->bn2 >= 0) {
+                const float* ax2 = c->aux(w, G->bn2);
+                x2 = c->act(w, M.layers[G->bn2].L.in0);
+                s2 = ax2 + 2 * C;
+                t2 = ax2 + 3 * C;
+            }
+        }
+        e = lpp::launch_bn_act(x, ax + 2 * C, ax + 3 * C, r, x2, s2, t2, false, tmp + n, rows, C, w.stream);
+        src = tmp + n;
+    } else if (!grad) {
+        src = c->act(w, layer);
+    }
+    if (e == hipSuccess) e = lpp::launch_nhwc_to_nchw(src, tmp, N, Y.out.c, Y.out.h, Y.out.w, Y.out.c, w.stream);
     if (e == hipSuccess) e = hipStreamSynchronize(w.stream);
     if (e == hipSuccess) e = hipMemcpy(host, tmp, sizeof(float) * n, hipMemcpyDeviceToHost);
     hipFree(tmp);
@@ -902,7 +1200,7 @@ int lpp_timer_read(lpp_ctx* c, double* ms, long* launches, double* work) {
 int lpp_kernel_sgd_update(float* x, float* m, const float* g, long n, float lr, float mu, float wd, void* stream) {
     if (!x || !g || n < 0) return fail(LPP_EINVAL, "bad arguments");
     if (((uintptr_t)x | (uintptr_t)g | (uintptr_t)m) & 15) return fail(LPP_EINVAL, "buffers must be 16-byte aligned");
-    hipError_t e = lpp::launch_sgd_update(x, m, g, 0, n, lr, mu, wd, (hipStream_t)stream);
+    hipError_t e = lpp::launch_sgd_update(x, m, g, 0, n, nullptr, lr, mu, wd, (hipStream_t)stream);
     if (e != hipSuccess) return fail(LPP_EHIP, std::string("sgd_update: ") + hipGetErrorString(e));
     return LPP_OK;
 }

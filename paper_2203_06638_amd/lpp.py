@@ -41,7 +41,8 @@ class ModelDesc(C.Structure):
 
 
 class Options(C.Structure):
-    _fields_ = [("mode", C.c_int), ("worker_streams", C.POINTER(C.c_void_p)), ("avg_stream", C.c_void_p)]
+    _fields_ = [("mode", C.c_int), ("worker_streams", C.POINTER(C.c_void_p)), ("avg_stream", C.c_void_p),
+                ("unfused", C.c_int), ("no_graphs", C.c_int)]
 
 
 class Batch(C.Structure):
@@ -131,11 +132,11 @@ class Context:
     """One lpp_ctx: K replicas x P workers of `model` on the current device."""
 
     def __init__(self, model, K, batch, mode=SEQUENTIAL, dtype=FP32, momentum=0.0, weight_decay=0.0,
-                 bn_eps=1e-5, streams=None, avg_stream=None):
+                 bn_eps=1e-5, streams=None, avg_stream=None, unfused=False, graphs=True):
         self.model = model
         self.K, self.P, self.batch = K, model.P, batch
         self._desc = make_desc(model, batch, dtype, momentum, weight_decay, bn_eps)
-        opt = Options(mode, None, None)
+        opt = Options(mode, None, None, int(unfused), int(not graphs))
         if streams is not None:
             assert len(streams) == K * model.P
             self._streams = (C.c_void_p * len(streams))(*[_stream_handle(s).value for s in streams])

@@ -135,14 +135,15 @@ def test_maxpool_routing_exact_grid():
         check_grads(o, ctx.get_grad(0), g, scale=sc)
 
 
-def test_bn_residual_passes():
+@pytest.mark.parametrize("unfused", [False, True], ids=["fused", "unfused"])
+def test_bn_residual_passes(unfused):
     o, p = T.twin_bn_net(16, 16, 8)
     make = lambda s: (T.init_x(o.specs, s, perturb=0.2), T.inputs(s + 1, 6, o.in_shape, o.n_classes)[0])
     seed, margin = T.well_posed_seed(o, make)
     x, img = make(seed)
     lab = T.inputs(seed + 1, 6, o.in_shape, o.n_classes)[1]
     g, sc = R.grad_scale(o, x, img, lab)
-    with lpp.Context(p, K=1, batch=6) as ctx:
+    with lpp.Context(p, K=1, batch=6, unfused=unfused) as ctx:
         ctx.set_params(x)
         ctx.step(0, *dev(img, lab), 0, 0.0)
         T.assert_decisions_match(o, ctx, 0, x, img)
@@ -211,13 +212,13 @@ def test_tiny_cnn_ten_steps():
         assert max(errs.values()) < T.TOL_PARAM, T.worst(errs)
 
 
-def _partition_step(o, p, x, m0, img, lab, partition, lr=0.1, mu=0.9, band=None):
+def _partition_step(o, p, x, m0, img, lab, partition, lr=0.1, mu=0.9, band=None, unfused=False):
     xr = x.astype(np.float64)
     mr = m0.astype(np.float64)
     _, sc = R.grad_scale(o, xr, img, lab)
     g, loss, logits = R.step(o, xr, mr, img, lab, partition, lr, mu)
     n = img.shape[0]
-    with lpp.Context(p, K=1, batch=n, momentum=mu) as ctx:
+    with lpp.Context(p, K=1, batch=n, momentum=mu, unfused=unfused) as ctx:
         ctx.set_params(x)
         w = max(partition - 1, 0)
         ctx.set_momentum(w, m0)
@@ -261,24 +262,26 @@ def test_resnet20_forward_small_batches():
                 assert T.relerr(got, ref, T.TAU_LOGITS) < 1e-3, (n, layer)
 
 
+@pytest.mark.parametrize("unfused", [False, True], ids=["fused", "unfused"])
 @pytest.mark.parametrize("partition", [0, 1, 2, 3, 4])
-def test_resnet20_relu_free_partition_step_batch16(partition):
+def test_resnet20_relu_free_partition_step_batch16(partition, unfused):
     o, p = OM.resnet20_p4(relu=False), PM.resnet20(act=False)
     x = T.init_x(o.specs, 41)
     img, lab = T.inputs(42, 16, o.in_shape, 10)
     m0 = (np.random.default_rng(1).standard_normal(o.d) * 1e-2).astype(np.float32)
-    _partition_step(o, p, x, m0, img, lab, partition)
+    _partition_step(o, p, x, m0, img, lab, partition, unfused=unfused)
 
 
 def test_resnet20_activation_grads_layer_by_layer():
     """Gradient w.r.t. every layer output of the ReLU-free ResNet-20 at
-    batch 16 (full backward), walked from the logits towards the image."""
+    batch 16 (full backward), walked from the logits towards the image, on
+    the per-layer (unfused) kernels, which keep every layer's gradient."""
     o, p = OM.resnet20_p4(relu=False), PM.resnet20(act=False)
     x = T.init_x(o.specs, 45)
     img, lab = T.inputs(46, 16, o.in_shape, 10)
     shapes = R.shapes(o)
     bad = []
-    with lpp.Context(p, K=1, batch=16) as ctx:
+    with lpp.Context(p, K=1, batch=16, unfused=True) as ctx:
         ctx.set_params(x)
         ctx.step(0, *dev(img, lab), 0, 0.0)
         for layer in range(len(o.layers) - 1, 0, -1):
@@ -510,3 +513,24 @@ def test_async_hogwild_training_smoke():
             lo, hi = ctx.block_range(i)
             assert not np.array_equal(xn[lo:hi], x[lo:hi])
         assert ctx.counter(0) == 128
+
+
+def test_graph_replays_match_direct_launches():
+    """Each (worker, partition) step is captured once into a HIP graph and
+    replayed with new images, labels and lr read from device memory.  Every
+    replay, with eager host<->device traffic and syncs between replays, must
+    equal the step launched kernel by kernel, bit for bit."""
+    p = PM.resnet20()
+    x = T.init_x(p.specs, 95)
+    batches = [dev(*T.inputs(96 + s, 8, p.in_shape, 10)) for s in range(8)]
+    with lpp.Context(p, K=1, batch=8, momentum=0.9, graphs=True) as gctx, \
+            lpp.Context(p, K=1, batch=8, momentum=0.9, graphs=False) as dctx:
+        gctx.set_params(x)
+        dctx.set_params(x)
+        for s in range(8):
+            w, part, lr = s % 2, (s % 2) * 3 + 1, 0.1 / (s + 1)
+            gctx.step(w, *batches[s], part, lr)
+            dctx.step(w, *batches[s], part, lr)
+            assert np.array_equal(gctx.get_params(0), dctx.get_params(0)), s
+            assert np.array_equal(gctx.get_momentum(w), dctx.get_momentum(w)), s
+            assert gctx.get_loss(w) == dctx.get_loss(w)
