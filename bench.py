@@ -49,7 +49,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-hbm", action="store_true")
     ap.add_argument("--cpu-steps", type=int, default=2)
-    ap.add_argument("--issue-threads", type=int, default=4,
+    ap.add_argument("--replicas", type=int, default=1, help="K (the headline workload has K = 1)")
+    ap.add_argument("--workers-used", type=int, default=0,
+                    help="issue steps to only the first n workers (0 = all); for latency studies")
+    ap.add_argument("--issue-threads", type=int, default=1,
                     help="host threads issuing steps; each owns a fixed set of workers")
     return ap.parse_args()
 
@@ -129,7 +132,7 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.init()
-    B, P, K = a.batch, 4, 1
+    B, P, K = a.batch, 4, a.replicas
     model = PM.resnet20(10)
     info = lpp.describe(model, B)
     x0 = synth.init_params(model.specs, 1)
@@ -143,14 +146,15 @@ def main():
     ctx.set_params(x0)
 
     issue = [0.0]
-    nthr = max(1, min(a.issue_threads, K * P))
+    nw = a.workers_used or K * P
+    nthr = max(1, min(a.issue_threads, nw))
 
     def run_range(start, n, thr):
         for s in range(start, start + n):
-            w = s % (K * P)
+            w = s % nw
             if w % nthr != thr:
                 continue
-            img, lab = pool[(s // (K * P)) % len(pool)]
+            img, lab = pool[(s // nw) % len(pool)]
             ctx.step(w, img, lab, w % P + 1, 0.1)
 
     def run(n, start):

@@ -235,6 +235,422 @@ __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ 
     }
 }
 
+// LDS-staged variant for Cs % 16 == 0.  A k-step is one filter tap and 16
+// source channels.  The workgroup's A tile (BM rows x 16) and B tile (BN rows
+// x 16) are loaded cooperatively as float4 (each thread keeps the same rows in
+// every k-step, so row decoding happens once), double-buffered in LDS with the
+// next k-step's global loads in flight during this k-step's MFMAs; one
+// barrier per k-step.  Waves form a WM x WN grid over the tile; a wave owns
+// TM x TN 16x16 output tiles and reads its operands as float4 from LDS.
+template <int MODE, int BM, int BN, int WM, bool STATS>
+__global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ src, const float* __restrict__ B,
+                                                    const float* __restrict__ bias, float* __restrict__ Y,
+                                                    ConvGeom g, int accumulate, float* __restrict__ pmean,
+                                                      float* __restrict__ pm2) {
+    constexpr int WN = 4 / WM;
+    constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
+    constexpr int LDW = 20;                                  // 16 floats + 4 pad per LDS row
+    constexpr int NA = (BM * 4 + 255) / 256, NB = (BN * 4 + 255) / 256;
+    __shared__ float As[2][BM][LDW];
+    __shared__ float Bs[2][BN][LDW];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % WM, wn = wave / WM;
+    const int gi = lane >> 4, li = lane & 15;
+    const int HoWo = g.Ho * g.Wo;
+    const int M = g.Nb * HoWo;
+    const int Ktot = g.R * g.S * g.Cs;
+    const int CG = g.Cs >> 4;                                // 16-channel groups per tap
+    const int KS = g.R * g.S * CG;                           // k-steps
+    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+    const int quad = tid & 3;                                // each thread's float4 within a 16-wide row
+
+    // rows of A this thread loads: (tid + 256 i) / 4
+    int an[NA], ap[NA], aq[NA];
+    bool av[NA];
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+        const int row = (tid + 256 * i) >> 2;
+        const int m = m0 + row;
+        av[i] = (tid + 256 * i) < BM * 4 && m < M;
+        const int mm = av[i] ? m : 0;
+        an[i] = mm / HoWo;
+        const int rem = mm - an[i] * HoWo;
+        ap[i] = rem / g.Wo;
+        aq[i] = rem - ap[i] * g.Wo;
+    }
+    const float* brow[NB];
+    bool bvld[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+        const int row = (tid + 256 * i) >> 2;
+        const int n = n0 + row;
+        bvld[i] = (tid + 256 * i) < BN * 4 && n < g.Ncols;
+        brow[i] = B + (long)(bvld[i] ? n : 0) * Ktot + quad * 4;
+    }
+
+    f4 ra[NA], rb[NB];
+    auto gload = [&](int ks) {
+        const int tap = ks / CG;
+        const int cg = ks - tap * CG;
+        const int r = tap / g.S, sx = tap - r * g.S;
+        const int c = cg * 16 + quad * 4;
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+            const int so = av[i] ? src_pixel<MODE>(an[i], ap[i], aq[i], r, sx, g) : -1;
+            ra[i] = so >= 0 ? *(const f4*)(src + so + c) : f4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) rb[i] = bvld[i] ? *(const f4*)(brow[i] + ks * 16) : f4{0.f, 0.f, 0.f, 0.f};
+    };
+    auto lstore = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < NA; ++i)
+            if ((tid + 256 * i) < BM * 4) *(f4*)&As[buf][(tid + 256 * i) >> 2][quad * 4] = ra[i];
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+            if ((tid + 256 * i) < BN * 4) *(f4*)&Bs[buf][(tid + 256 * i) >> 2][quad * 4] = rb[i];
+    };
+
+    f4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    for (int ks = 0; ks < KS; ++ks) {
+        const int buf = ks & 1;
+        if (ks + 1 < KS) gload(ks + 1);
+        f4 a[TM], b[TN];
+#pragma unroll
+        for (int x = 0; x < TM; ++x) a[x] = *(const f4*)&As[buf][(wm * TM + x) * 16 + li][gi * 4];
+#pragma unroll
+        for (int y = 0; y < TN; ++y) b[y] = *(const f4*)&Bs[buf][(wn * TN + y) * 16 + li][gi * 4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(a[x][j], b[y][j], acc[x][y]);
+        if (ks + 1 < KS) lstore(buf ^ 1);
+        __syncthreads();
+    }
+
+    const int m_base = m0 + wm * TM * 16;
+    const int n_base = n0 + wn * TN * 16;
+#pragma unroll
+    for (int y = 0; y < TN; ++y) {
+        const int n = n_base + y * 16 + li;
+        const float bb = (bias && n < g.Ncols) ? bias[n] : 0.f;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[x][y][i] += bb;
+        if (n >= g.Ncols) continue;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int m = m_base + x * 16 + gi * 4 + i;
+                if (m >= M) continue;
+                const long o = (long)m * g.Ncols + n;
+                const float v = acc[x][y][i];
+                Y[o] = accumulate ? Y[o] + v : v;
+            }
+    }
+    if (STATS) {
+        __shared__ float red[WM][BN];
+        __shared__ float tile_mean[BN];
+        const int rows = min(BM, M - m0);
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            float sacc = 0.f;
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (m_base + x * 16 + gi * 4 + i < M) sacc += acc[x][y][i];
+            sacc += __shfl_xor(sacc, 16);
+            sacc += __shfl_xor(sacc, 32);
+            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = sacc;
+        }
+        __syncthreads();
+        if (threadIdx.x < BN) {
+            float t = 0.f;
+            for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
+            tile_mean[threadIdx.x] = t / (float)rows;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            const float mu = tile_mean[wn * TN * 16 + y * 16 + li];
+            float q = 0.f;
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (m_base + x * 16 + gi * 4 + i < M) {
+                        const float dv = acc[x][y][i] - mu;
+                        q += dv * dv;
+                    }
+            q += __shfl_xor(q, 16);
+            q += __shfl_xor(q, 32);
+            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = q;
+        }
+        __syncthreads();
+        if (threadIdx.x < BN) {
+            const int n = n0 + threadIdx.x;
+            if (n < g.Ncols) {
+                float t = 0.f;
+                for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
+                pmean[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
+                pm2[(long)blockIdx.x * g.Ncols + n] = t;
+            }
+        }
+    }
+}
+
+template <int MODE, int BM, int BN, int WM>
+static hipError_t launch_lds(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
+                             bool acc, float* pmean, float* pm2, hipStream_t st) {
+    const long M = (long)g.Nb * g.Ho * g.Wo;
+    dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
+    if (pmean)
+        hipLaunchKernelGGL((conv_lds_f32<MODE, BM, BN, WM, true>), grid, dim3(256), 0, st, src, B, bias, Y, g,
+                           (int)acc, pmean, pm2);
+    else
+        hipLaunchKernelGGL((conv_lds_f32<MODE, BM, BN, WM, false>), grid, dim3(256), 0, st, src, B, bias, Y, g,
+                           (int)acc, pmean, pm2);
+    return hipGetLastError();
+}
+
+// Spatially tiled variant (stride-1 data gradients and any forward pass with
+// Cs % 16 == 0 whose tile shape fits): a workgroup computes OH full output
+// rows of one image (TP = OH * Wo pixels) for BN output channels.  For each
+// group of 16 source channels it loads the input rows the tile reads, halo
+// and padding included (IH x IW pixels), and the filter slice (BN x R*S x
+// 16) into LDS once, then runs every tap from LDS: the 3x3 halo is fetched
+// from memory once instead of once per tap.  The data gradient of a stride-1
+// conv is a forward conv of dY with the filter flipped and padding R-1-pad.
+struct TileGeom { int OH, IH, IW, pad_eff, tiles_per_img; };
+
+template <int MODE, int WM, int TM, int TN, bool STATS>
+__global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
+                                                     const float* __restrict__ bias, float* __restrict__ Y,
+                                                     ConvGeom g, TileGeom t, int accumulate, float* __restrict__ pmean,
+                                                      float* __restrict__ pm2) {
+    constexpr int WN = 4 / WM;
+    constexpr int TP = WM * TM * 16, BN = WN * TN * 16;
+    constexpr int LDW = 20;
+    extern __shared__ float lds[];
+    const int RS = g.R * g.S;
+    float* Xs = lds;                              // [IH*IW][LDW]
+    float* Ws = lds + t.IH * t.IW * LDW;          // [BN*RS][LDW]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % WM, wn = wave / WM;
+    const int gi = lane >> 4, li = lane & 15;
+    const int img = blockIdx.x / t.tiles_per_img;
+    const int oh0 = (blockIdx.x - img * t.tiles_per_img) * t.OH;
+    const int n0 = blockIdx.y * BN;
+    const int st = g.stride;
+    const int h_org = oh0 * st - t.pad_eff, w_org = -t.pad_eff;
+    const int npix = t.OH * g.Wo;
+
+    // LDS offset of the input pixel each of this lane's output rows reads at tap (0,0)
+    int abase[TM];
+#pragma unroll
+    for (int x = 0; x < TM; ++x) {
+        int p = (wm * TM + x) * 16 + li;
+        p = p < npix ? p : npix - 1;
+        const int oh = p / g.Wo, ow = p - (p / g.Wo) * g.Wo;
+        abase[x] = (oh * st * t.IW + ow * st) * LDW + gi * 4;
+    }
+
+    f4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    const int ngroups = g.Cs >> 4;
+    const int Ktot = RS * g.Cs;
+    for (int cgp = 0; cgp < ngroups; ++cgp) {
+        const int c0 = cgp * 16;
+        for (int idx = tid; idx < t.IH * t.IW * 4; idx += 256) {
+            const int q = idx & 3, pix = idx >> 2;
+            const int ih = pix / t.IW, iw = pix - ih * t.IW;
+            const int h = h_org + ih, w = w_org + iw;
+            f4 v = f4{0.f, 0.f, 0.f, 0.f};
+            if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
+                v = *(const f4*)(src + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + c0 + q * 4);
+            *(f4*)(Xs + pix * LDW + q * 4) = v;
+        }
+        for (int idx = tid; idx < BN * RS * 4; idx += 256) {
+            const int q = idx & 3, rest = idx >> 2;
+            const int tap = rest % RS, nl = rest / RS;
+            const int n = n0 + nl;
+            const int stap = MODE == CONV_FWD ? tap : RS - 1 - tap;
+            f4 v = f4{0.f, 0.f, 0.f, 0.f};
+            if (n < g.Ncols) v = *(const f4*)(B + ((long)n * RS + stap) * g.Cs + c0 + q * 4);
+            *(f4*)(Ws + rest * LDW + q * 4) = v;
+        }
+        __syncthreads();
+        for (int r = 0; r < g.R; ++r)
+            for (int sx = 0; sx < g.S; ++sx) {
+                const int toff = (r * t.IW + sx) * LDW;
+                const int tap = r * g.S + sx;
+                f4 a[TM], b[TN];
+#pragma unroll
+                for (int x = 0; x < TM; ++x) a[x] = *(const f4*)(Xs + abase[x] + toff);
+#pragma unroll
+                for (int y = 0; y < TN; ++y)
+                    b[y] = *(const f4*)(Ws + (((wn * TN + y) * 16 + li) * RS + tap) * LDW + gi * 4);
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int x = 0; x < TM; ++x)
+#pragma unroll
+                        for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(a[x][j], b[y][j], acc[x][y]);
+            }
+        __syncthreads();
+    }
+    (void)Ktot;
+
+    const long m0 = (long)blockIdx.x * TP;      // tiles are consecutive runs of the NHWC rows
+    const int M = g.Nb * g.Ho * g.Wo;
+    const int pix_base = wm * TM * 16;
+    const int n_base = n0 + wn * TN * 16;
+#pragma unroll
+    for (int y = 0; y < TN; ++y) {
+        const int n = n_base + y * 16 + li;
+        const float bb = (bias && n < g.Ncols) ? bias[n] : 0.f;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[x][y][i] += bb;
+        if (n >= g.Ncols) continue;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int p = pix_base + x * 16 + gi * 4 + i;
+                if (p >= npix) continue;
+                const long o = (m0 + p) * g.Ncols + n;
+                const float v = acc[x][y][i];
+                Y[o] = accumulate ? Y[o] + v : v;
+            }
+    }
+    if (STATS) {
+        __shared__ float red[WM][BN];
+        __shared__ float tile_mean[BN];
+        const int rows = min(npix, M - (int)m0);
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            float sacc = 0.f;
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (pix_base + x * 16 + gi * 4 + i < npix) sacc += acc[x][y][i];
+            sacc += __shfl_xor(sacc, 16);
+            sacc += __shfl_xor(sacc, 32);
+            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = sacc;
+        }
+        __syncthreads();
+        if (threadIdx.x < BN) {
+            float tt = 0.f;
+            for (int w = 0; w < WM; ++w) tt += red[w][threadIdx.x];
+            tile_mean[threadIdx.x] = tt / (float)rows;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            const float mu = tile_mean[wn * TN * 16 + y * 16 + li];
+            float q = 0.f;
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (pix_base + x * 16 + gi * 4 + i < npix) {
+                        const float dv = acc[x][y][i] - mu;
+                        q += dv * dv;
+                    }
+            q += __shfl_xor(q, 16);
+            q += __shfl_xor(q, 32);
+            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = q;
+        }
+        __syncthreads();
+        if (threadIdx.x < BN) {
+            const int n = n0 + threadIdx.x;
+            if (n < g.Ncols) {
+                float tt = 0.f;
+                for (int w = 0; w < WM; ++w) tt += red[w][threadIdx.x];
+                pmean[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
+                pm2[(long)blockIdx.x * g.Ncols + n] = tt;
+            }
+        }
+    }
+}
+
+// Picks (WM, TM, TN) and the tile rows OH for the spatial kernel, or returns
+// false when no shape fits (the GEMM-style kernels take those passes).
+struct TileCfg { int wm, tm, tn; TileGeom t; size_t lds; };
+static bool pick_tile(int mode, const ConvGeom& g, TileCfg& out) {
+    if (g.Cs % 16 != 0) return false;
+    if (mode == CONV_DGRAD && g.stride != 1) return false;
+    static const int cands[][3] = {
+        // wm, tm, tn  (tile pixels = wm*tm*16, output channels = (4/wm)*tn*16)
+        {4, 4, 1}, {4, 2, 1}, {2, 4, 1}, {2, 2, 1}, {1, 4, 1}, {2, 2, 2}, {1, 4, 2}, {4, 1, 1}, {2, 1, 1}, {1, 2, 1},
+        {1, 1, 1}};
+    const long M = (long)g.Nb * g.Ho * g.Wo;
+    for (auto& c : cands) {
+        const int wm = c[0], tm = c[1], tn = c[2];
+        const int tp = wm * tm * 16, bn = (4 / wm) * tn * 16;
+        if (bn > 16 && g.Ncols <= bn / 2) continue;             // output width too small for this tile
+        if (g.Ncols > 16 && bn == 16 && g.Ncols % 32 == 0 && wm != 4) continue;
+        if (tp % g.Wo) continue;
+        const int oh = tp / g.Wo;
+        if (oh < 1 || g.Ho % oh) continue;
+        const int pad_eff = mode == CONV_FWD ? g.pad : g.R - 1 - g.pad;
+        const int ih = (oh - 1) * g.stride + g.R, iw = (g.Wo - 1) * g.stride + g.S;
+        const size_t lds = sizeof(float) * 20 * ((size_t)ih * iw + (size_t)bn * g.R * g.S);
+        if (lds > 60 * 1024) continue;   // leaves room for the static statistics arrays
+        const long tiles = M / tp;
+        if (tiles * ((g.Ncols + bn - 1) / bn) < 128) continue;
+        out = {wm, tm, tn, {oh, ih, iw, pad_eff, g.Ho / oh}, lds};
+        return true;
+    }
+    return false;
+}
+
+template <int MODE, int WM, int TM, int TN>
+static hipError_t launch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
+                              const TileCfg& c, bool acc, float* pmean, float* pm2, hipStream_t st) {
+    constexpr int BN = (4 / WM) * TN * 16;
+    dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
+    if (pmean)
+        hipLaunchKernelGGL((conv_tile_f32<MODE, WM, TM, TN, true>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
+                           c.t, (int)acc, pmean, pm2);
+    else
+        hipLaunchKernelGGL((conv_tile_f32<MODE, WM, TM, TN, false>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
+                           c.t, (int)acc, pmean, pm2);
+    return hipGetLastError();
+}
+
+template <int MODE>
+static hipError_t dispatch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
+                                const TileCfg& c, bool acc, float* pmean, float* pm2, hipStream_t st) {
+#define TILE(WM_, TM_, TN_)                                                                          \
+    if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_)                                                   \
+        return launch_tile<MODE, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, pmean, pm2, st);
+    TILE(4, 4, 1) TILE(4, 2, 1) TILE(2, 4, 1) TILE(2, 2, 1) TILE(1, 4, 1) TILE(2, 2, 2) TILE(1, 4, 2)
+    TILE(4, 1, 1) TILE(2, 1, 1) TILE(1, 2, 1) TILE(1, 1, 1)
+#undef TILE
+    return hipErrorInvalidValue;
+}
+
 template <int MODE, int WM, int TM, int TN>
 static hipError_t launch_cfg(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
                              bool acc, float* pmean, float* pm2, hipStream_t st) {
@@ -260,28 +676,53 @@ static hipError_t launch_cfg(const float* src, const float* B, const float* bias
     return hipGetLastError();
 }
 
-// Tile configuration for a pass: (WM, TM, TN) by output width and rows.
-struct ConvCfg { int wm, tm, tn; };
+// Tile configuration.  Cs % 16 == 0 uses the LDS kernel with (BM, BN, WM)
+// by output width and rows; other passes (the padded image) the direct one.
+struct ConvCfg { int lds, bm, bn, wm, tm, tn; };
 static ConvCfg pick_cfg(const ConvGeom& g) {
     const long M = (long)g.Nb * g.Ho * g.Wo;
-    if (g.Ncols <= 16) return {4, 2, 1};
-    if (g.Ncols <= 32) return {4, 2, 2};
-    if (g.Ncols <= 64 || M < 64L * 512) {
-        if (M >= 64L * 512) return {2, 2, 2};
-        return {2, 1, 2};
+    if (g.Cs % 16 == 0) {
+        if (g.Ncols <= 16) return {1, M >= 256L * 256 ? 256 : 64, 16, 4, 0, 0};
+        if (g.Ncols <= 32) return {1, M >= 128L * 256 ? 128 : 64, 32, M >= 128L * 256 ? 4 : 2, 0, 0};
+        if (g.Ncols <= 64) return {1, M >= 64L * 256 ? 64 : 32, 64, M >= 64L * 256 ? 2 : 1, 0, 0};
+        return {1, 64, 128, 2, 0, 0};
     }
-    return {2, 2, 4};
+    if (g.Ncols <= 16) return {0, 128, 16, 4, 2, 1};
+    if (g.Ncols <= 32) return {0, 128, 32, 4, 2, 2};
+    if (g.Ncols <= 64 || M < 64L * 512) {
+        if (M >= 64L * 512) return {0, 64, 64, 2, 2, 2};
+        return {0, 32, 64, 2, 1, 2};
+    }
+    return {0, 64, 128, 2, 2, 4};
 }
 
 int conv_tile_rows(const ConvGeom& g) {
-    ConvCfg c = pick_cfg(g);
-    return c.wm * c.tm * 16;
+    TileCfg t;
+    if (pick_tile(CONV_FWD, g, t)) return t.wm * t.tm * 16;
+    return pick_cfg(g).bm;
 }
 
 template <int MODE>
 static hipError_t launch_mode(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
                               bool acc, float* pmean, float* pm2, hipStream_t st) {
+    TileCfg tc;
+    if (pick_tile(MODE, g, tc)) return dispatch_tile<MODE>(src, B, bias, Y, g, tc, acc, pmean, pm2, st);
     ConvCfg c = pick_cfg(g);
+    if (c.lds) {
+        if (c.bn == 16) {
+            if (c.bm == 256) return launch_lds<MODE, 256, 16, 4>(src, B, bias, Y, g, acc, pmean, pm2, st);
+            return launch_lds<MODE, 64, 16, 4>(src, B, bias, Y, g, acc, pmean, pm2, st);
+        }
+        if (c.bn == 32) {
+            if (c.bm == 128) return launch_lds<MODE, 128, 32, 4>(src, B, bias, Y, g, acc, pmean, pm2, st);
+            return launch_lds<MODE, 64, 32, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
+        }
+        if (c.bn == 64) {
+            if (c.bm == 64) return launch_lds<MODE, 64, 64, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
+            return launch_lds<MODE, 32, 64, 1>(src, B, bias, Y, g, acc, pmean, pm2, st);
+        }
+        return launch_lds<MODE, 64, 128, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
+    }
     if (c.wm == 4 && c.tn == 1) return launch_cfg<MODE, 4, 2, 1>(src, B, bias, Y, g, acc, pmean, pm2, st);
     if (c.wm == 4) return launch_cfg<MODE, 4, 2, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
     if (c.tn == 4) return launch_cfg<MODE, 2, 2, 4>(src, B, bias, Y, g, acc, pmean, pm2, st);
