@@ -22,7 +22,12 @@
 // im2col rows as loaded, float4 along channels); each wave reduces 16 of the
 // chunk's pixels; waves are summed in a fixed order and every split of the
 // pixel range writes its own partial, summed in order by a second kernel.
-// No atomics anywhere: results are bitwise reproducible.
+// Convolution outputs and weight gradients use no atomics and are bitwise
+// reproducible; only the batch-norm sums of the forward epilogue are merged
+// across workgroups by fp64 atomic adds (bnacc.h).
+#include <algorithm>
+
+#include "bnacc.h"
 #include "kernels.h"
 
 namespace lpp {
@@ -31,6 +36,28 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f4 mfma16x16x4(float a, float b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Copies n float4 into LDS: addr(i, src, dst) names element i's source (null:
+// zero) and LDS destination.  Each thread issues NB global loads before their
+// LDS stores, so the load latencies overlap instead of adding up.
+template <int NB, class Addr>
+__device__ __forceinline__ void lds_stage(int n, Addr addr) {
+    for (int base = threadIdx.x; base < n; base += NB * 256) {
+        f4 v[NB];
+        float* d[NB];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int i = base + u * 256;
+            const float* src = nullptr;
+            d[u] = nullptr;
+            if (i < n) addr(i, src, d[u]);
+            v[u] = src ? *(const f4*)src : f4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int u = 0; u < NB; ++u)
+            if (d[u]) *(f4*)d[u] = v[u];
+    }
 }
 
 // Offset of source pixel (n, hs, ws) feeding output pixel (n, p, q) through
@@ -59,14 +86,13 @@ __device__ __forceinline__ int src_pixel(int n, int p, int q, int r, int s, cons
 
 // WM waves along m (4/WM along n); each wave owns TM x TN tiles of 16x16.
 // FAST: Cs % 16 == 0, so a group of four float4 chunks never straddles a tap.
-// STATS: also write, per output channel, the mean and the sum of squared
-// deviations from it over this workgroup's BM output rows (the batch-norm
-// statistics of the output, one partial per row tile).
+// STATS: also form, per output channel, the mean and the sum of squared
+// deviations over this workgroup's BM output rows and add the tile's share of
+// the batch sums (sum y, sum y^2) into the batch-norm accumulators.
 template <int MODE, int WM, int TM, int TN, bool FAST, bool STATS>
 __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                       const float* __restrict__ bias, float* __restrict__ Y,
-                                                      ConvGeom g, int accumulate, float* __restrict__ pmean,
-                                                      float* __restrict__ pm2) {
+                                                      ConvGeom g, int accumulate, double* __restrict__ stats) {
     constexpr int WN = 4 / WM;
     constexpr int BM = WM * TM * 16, BN = WN * TN * 16;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -228,8 +254,9 @@ __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ 
             if (n < g.Ncols) {
                 float t = 0.f;
                 for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
-                pmean[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
-                pm2[(long)blockIdx.x * g.Ncols + n] = t;
+                const double mu = tile_mean[threadIdx.x], nr = (double)rows;
+                acc_add(stats, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
+                acc_add(stats, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)t + nr * mu * mu);
             }
         }
     }
@@ -245,8 +272,7 @@ __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ 
 template <int MODE, int BM, int BN, int WM, bool STATS>
 __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                     const float* __restrict__ bias, float* __restrict__ Y,
-                                                    ConvGeom g, int accumulate, float* __restrict__ pmean,
-                                                      float* __restrict__ pm2) {
+                                                    ConvGeom g, int accumulate, double* __restrict__ stats) {
     constexpr int WN = 4 / WM;
     constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
     constexpr int LDW = 20;                                  // 16 floats + 4 pad per LDS row
@@ -405,8 +431,9 @@ __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ sr
             if (n < g.Ncols) {
                 float t = 0.f;
                 for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
-                pmean[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
-                pm2[(long)blockIdx.x * g.Ncols + n] = t;
+                const double mu = tile_mean[threadIdx.x], nr = (double)rows;
+                acc_add(stats, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
+                acc_add(stats, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)t + nr * mu * mu);
             }
         }
     }
@@ -414,15 +441,15 @@ __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ sr
 
 template <int MODE, int BM, int BN, int WM>
 static hipError_t launch_lds(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                             bool acc, float* pmean, float* pm2, hipStream_t st) {
+                             bool acc, double* stats, hipStream_t st) {
     const long M = (long)g.Nb * g.Ho * g.Wo;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
-    if (pmean)
+    if (stats)
         hipLaunchKernelGGL((conv_lds_f32<MODE, BM, BN, WM, true>), grid, dim3(256), 0, st, src, B, bias, Y, g,
-                           (int)acc, pmean, pm2);
+                           (int)acc, stats);
     else
         hipLaunchKernelGGL((conv_lds_f32<MODE, BM, BN, WM, false>), grid, dim3(256), 0, st, src, B, bias, Y, g,
-                           (int)acc, pmean, pm2);
+                           (int)acc, stats);
     return hipGetLastError();
 }
 
@@ -439,8 +466,7 @@ struct TileGeom { int OH, IH, IW, pad_eff, tiles_per_img; };
 template <int MODE, int WM, int TM, int TN, bool STATS>
 __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                      const float* __restrict__ bias, float* __restrict__ Y,
-                                                     ConvGeom g, TileGeom t, int accumulate, float* __restrict__ pmean,
-                                                      float* __restrict__ pm2) {
+                                                     ConvGeom g, TileGeom t, int accumulate, double* __restrict__ stats) {
     constexpr int WN = 4 / WM;
     constexpr int TP = WM * TM * 16, BN = WN * TN * 16;
     constexpr int LDW = 20;
@@ -475,27 +501,26 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
         for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
     const int ngroups = g.Cs >> 4;
-    const int Ktot = RS * g.Cs;
     for (int cgp = 0; cgp < ngroups; ++cgp) {
         const int c0 = cgp * 16;
-        for (int idx = tid; idx < t.IH * t.IW * 4; idx += 256) {
-            const int q = idx & 3, pix = idx >> 2;
-            const int ih = pix / t.IW, iw = pix - ih * t.IW;
-            const int h = h_org + ih, w = w_org + iw;
-            f4 v = f4{0.f, 0.f, 0.f, 0.f};
-            if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
-                v = *(const f4*)(src + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + c0 + q * 4);
-            *(f4*)(Xs + pix * LDW + q * 4) = v;
-        }
-        for (int idx = tid; idx < BN * RS * 4; idx += 256) {
-            const int q = idx & 3, rest = idx >> 2;
-            const int tap = rest % RS, nl = rest / RS;
-            const int n = n0 + nl;
-            const int stap = MODE == CONV_FWD ? tap : RS - 1 - tap;
-            f4 v = f4{0.f, 0.f, 0.f, 0.f};
-            if (n < g.Ncols) v = *(const f4*)(B + ((long)n * RS + stap) * g.Cs + c0 + q * 4);
-            *(f4*)(Ws + rest * LDW + q * 4) = v;
-        }
+        const int nx = t.IH * t.IW * 4;
+        lds_stage<8>(nx + BN * RS * 4, [&](int idx, const float*& sp, float*& dp) {
+            if (idx < nx) {
+                const int q = idx & 3, pix = idx >> 2;
+                const int ih = pix / t.IW, iw = pix - ih * t.IW;
+                const int h = h_org + ih, w = w_org + iw;
+                if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
+                    sp = src + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + c0 + q * 4;
+                dp = Xs + pix * LDW + q * 4;
+            } else {
+                const int e = idx - nx, q = e & 3, rest = e >> 2;
+                const int tap = rest % RS, nl = rest / RS;
+                const int n = n0 + nl;
+                const int stap = MODE == CONV_FWD ? tap : RS - 1 - tap;
+                if (n < g.Ncols) sp = B + ((long)n * RS + stap) * g.Cs + c0 + q * 4;
+                dp = Ws + rest * LDW + q * 4;
+            }
+        });
         __syncthreads();
         for (int r = 0; r < g.R; ++r)
             for (int sx = 0; sx < g.S; ++sx) {
@@ -516,10 +541,8 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
             }
         __syncthreads();
     }
-    (void)Ktot;
 
     const long m0 = (long)blockIdx.x * TP;      // tiles are consecutive runs of the NHWC rows
-    const int M = g.Nb * g.Ho * g.Wo;
     const int pix_base = wm * TM * 16;
     const int n_base = n0 + wn * TN * 16;
 #pragma unroll
@@ -545,7 +568,6 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
     if (STATS) {
         __shared__ float red[WM][BN];
         __shared__ float tile_mean[BN];
-        const int rows = min(npix, M - (int)m0);
 #pragma unroll
         for (int y = 0; y < TN; ++y) {
             float sacc = 0.f;
@@ -562,7 +584,7 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
         if (threadIdx.x < BN) {
             float tt = 0.f;
             for (int w = 0; w < WM; ++w) tt += red[w][threadIdx.x];
-            tile_mean[threadIdx.x] = tt / (float)rows;
+            tile_mean[threadIdx.x] = tt / (float)npix;
         }
         __syncthreads();
 #pragma unroll
@@ -587,8 +609,9 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
             if (n < g.Ncols) {
                 float tt = 0.f;
                 for (int w = 0; w < WM; ++w) tt += red[w][threadIdx.x];
-                pmean[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
-                pm2[(long)blockIdx.x * g.Ncols + n] = tt;
+                const double mu = tile_mean[threadIdx.x], nr = (double)npix;
+                acc_add(stats, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
+                acc_add(stats, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)tt + nr * mu * mu);
             }
         }
     }
@@ -627,51 +650,225 @@ static bool pick_tile(int mode, const ConvGeom& g, TileCfg& out) {
 
 template <int MODE, int WM, int TM, int TN>
 static hipError_t launch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              const TileCfg& c, bool acc, float* pmean, float* pm2, hipStream_t st) {
+                              const TileCfg& c, bool acc, double* stats, hipStream_t st) {
     constexpr int BN = (4 / WM) * TN * 16;
     dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
-    if (pmean)
+    if (stats)
         hipLaunchKernelGGL((conv_tile_f32<MODE, WM, TM, TN, true>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
-                           c.t, (int)acc, pmean, pm2);
+                           c.t, (int)acc, stats);
     else
         hipLaunchKernelGGL((conv_tile_f32<MODE, WM, TM, TN, false>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
-                           c.t, (int)acc, pmean, pm2);
+                           c.t, (int)acc, stats);
     return hipGetLastError();
 }
 
 template <int MODE>
 static hipError_t dispatch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                                const TileCfg& c, bool acc, float* pmean, float* pm2, hipStream_t st) {
+                                const TileCfg& c, bool acc, double* stats, hipStream_t st) {
 #define TILE(WM_, TM_, TN_)                                                                          \
     if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_)                                                   \
-        return launch_tile<MODE, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, pmean, pm2, st);
+        return launch_tile<MODE, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, st);
     TILE(4, 4, 1) TILE(4, 2, 1) TILE(2, 4, 1) TILE(2, 2, 1) TILE(1, 4, 1) TILE(2, 2, 2) TILE(1, 4, 2)
     TILE(4, 1, 1) TILE(2, 1, 1) TILE(1, 2, 1) TILE(1, 1, 1)
 #undef TILE
     return hipErrorInvalidValue;
 }
 
+// Data gradient of a stride-2 conv, split by output parity.  dX pixel
+// (2i + a, 2j + b) only receives taps (r, s) with a + pad - r and b + pad - s
+// even, from dY[i + (a + pad - r)/2][j + (b + pad - s)/2]: per parity class
+// (a, b) this is a dense stride-1 correlation over dY with a subset of the
+// taps (for 3x3, pad 1: 1, 2, 2 and 4 taps).  A workgroup takes one class,
+// OH class rows of one image (TP = OH * Wc pixels) and BN input channels;
+// per group of 16 dY channels it stages the dY rows it reads and the class's
+// filter taps in LDS, then runs them all from LDS.  No MFMA is spent on the
+// taps that fall between strides.  Classes without taps write zeros (or leave
+// an accumulated dX as it is).
+struct S2Geom { int OH, IH, IW, Hc, Wc, tiles_per_img, dr0, ds0; };
+
+template <int WM, int TM, int TN>
+__global__ __launch_bounds__(256) void conv_dgrad_s2_f32(const float* __restrict__ dY, const float* __restrict__ B,
+                                                         float* __restrict__ dX, ConvGeom g, S2Geom t,
+                                                         int accumulate) {
+    constexpr int WN = 4 / WM;
+    constexpr int TP = WM * TM * 16, BN = WN * TN * 16;
+    constexpr int LDW = 20;
+    extern __shared__ float lds[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % WM, wn = wave / WM;
+    const int gi = lane >> 4, li = lane & 15;
+    const int cls = blockIdx.z, ca = cls >> 1, cb = cls & 1;
+    const int img = blockIdx.x / t.tiles_per_img;
+    const int i0 = (blockIdx.x - img * t.tiles_per_img) * t.OH;
+    const int n0 = blockIdx.y * BN;
+    const int RS = g.R * g.S;
+
+    // the class's taps (uniform over the workgroup), at most R*S <= 9
+    int tr[9], ts[9], nt = 0;
+    for (int r = 0; r < g.R; ++r)
+        for (int s = 0; s < g.S; ++s)
+            if (((ca + g.pad - r) & 1) == 0 && ((cb + g.pad - s) & 1) == 0 && nt < 9) {
+                tr[nt] = r;
+                ts[nt] = s;
+                ++nt;
+            }
+    float* Xs = lds;                              // [IH*IW][LDW] dY rows
+    float* Ws = lds + t.IH * t.IW * LDW;          // [BN][nt][LDW]
+
+    int abase[TM];
+#pragma unroll
+    for (int x = 0; x < TM; ++x) {
+        const int p = (wm * TM + x) * 16 + li;
+        const int oh = p / t.Wc, ow = p - (p / t.Wc) * t.Wc;
+        abase[x] = (oh * t.IW + ow) * LDW + gi * 4;
+    }
+    f4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    if (nt > 0) {
+        const int h_org = i0 + t.dr0, w_org = t.ds0;
+        for (int c0 = 0; c0 < g.Cs; c0 += 16) {
+            const int nx = t.IH * t.IW * 4;
+            lds_stage<8>(nx + BN * nt * 4, [&](int idx, const float*& sp, float*& dp) {
+                if (idx < nx) {
+                    const int q = idx & 3, pix = idx >> 2;
+                    const int ih = pix / t.IW, iw = pix - ih * t.IW;
+                    const int h = h_org + ih, w = w_org + iw;
+                    if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
+                        sp = dY + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + c0 + q * 4;
+                    dp = Xs + pix * LDW + q * 4;
+                } else {
+                    const int e = idx - nx, q = e & 3, rest = e >> 2;
+                    const int ti = rest % nt, nl = rest / nt;
+                    const int n = n0 + nl;
+                    if (n < g.Ncols) sp = B + ((long)n * RS + tr[ti] * g.S + ts[ti]) * g.Cs + c0 + q * 4;
+                    dp = Ws + rest * LDW + q * 4;
+                }
+            });
+            __syncthreads();
+            for (int ti = 0; ti < nt; ++ti) {
+                // source row i + (a + pad - r)/2, column j + (b + pad - s)/2
+                const int dr = (ca + g.pad - tr[ti]) / 2 - t.dr0, ds = (cb + g.pad - ts[ti]) / 2 - t.ds0;
+                const int toff = (dr * t.IW + ds) * LDW;
+                f4 av[TM], bv[TN];
+#pragma unroll
+                for (int x = 0; x < TM; ++x) av[x] = *(const f4*)(Xs + abase[x] + toff);
+#pragma unroll
+                for (int y = 0; y < TN; ++y)
+                    bv[y] = *(const f4*)(Ws + (((wn * TN + y) * 16 + li) * nt + ti) * LDW + gi * 4);
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int x = 0; x < TM; ++x)
+#pragma unroll
+                        for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(av[x][j], bv[y][j], acc[x][y]);
+            }
+            __syncthreads();
+        }
+    } else if (accumulate) {
+        return;
+    }
+
+    const int pix_base = wm * TM * 16;
+    const int n_base = n0 + wn * TN * 16;
+#pragma unroll
+    for (int y = 0; y < TN; ++y) {
+        const int n = n_base + y * 16 + li;
+        if (n >= g.Ncols) continue;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int p = pix_base + x * 16 + gi * 4 + i;
+                const int oh = p / t.Wc, ow = p - (p / t.Wc) * t.Wc;
+                const int h = 2 * (i0 + oh) + ca, w = 2 * ow + cb;
+                const long o = ((long)(img * g.Ho + h) * g.Wo + w) * g.Ncols + n;
+                const float v = acc[x][y][i];
+                dX[o] = accumulate ? dX[o] + v : v;
+            }
+    }
+}
+
+// Tile shape of the parity-split stride-2 data gradient, or false when it
+// does not apply.
+struct S2Cfg { int wm, tm, tn; S2Geom t; size_t lds; };
+static bool pick_s2(const ConvGeom& g, S2Cfg& out) {
+    if (g.stride != 2 || g.Cs % 16 || (g.Ho & 1) || (g.Wo & 1) || g.R > 3 || g.S > 3) return false;
+    const int Hc = g.Ho / 2, Wc = g.Wo / 2;
+    // source offsets (a + pad - r)/2 over every class and tap
+    int dr0 = 1 << 20, dr1 = -(1 << 20), ds0 = 1 << 20, ds1 = -(1 << 20);
+    for (int a = 0; a < 2; ++a)
+        for (int r = 0; r < g.R; ++r)
+            if (((a + g.pad - r) & 1) == 0) {
+                dr0 = std::min(dr0, (a + g.pad - r) / 2);
+                dr1 = std::max(dr1, (a + g.pad - r) / 2);
+            }
+    for (int b = 0; b < 2; ++b)
+        for (int s = 0; s < g.S; ++s)
+            if (((b + g.pad - s) & 1) == 0) {
+                ds0 = std::min(ds0, (b + g.pad - s) / 2);
+                ds1 = std::max(ds1, (b + g.pad - s) / 2);
+            }
+    if (dr0 > dr1 || ds0 > ds1) return false;
+    static const int cands[][3] = {{4, 4, 1}, {4, 2, 1}, {2, 2, 1}, {4, 1, 1}, {2, 1, 1}, {1, 2, 1}, {1, 1, 1}};
+    for (auto& c : cands) {
+        const int wm = c[0], tm = c[1], tn = c[2];
+        const int tp = wm * tm * 16, bn = (4 / wm) * tn * 16;
+        if (bn > 16 && g.Ncols <= bn / 2) continue;
+        if (tp % Wc) continue;
+        const int oh = tp / Wc;
+        if (oh < 1 || Hc % oh) continue;
+        const int ih = oh + dr1 - dr0, iw = Wc + ds1 - ds0;
+        const size_t lds = sizeof(float) * 20 * ((size_t)ih * iw + (size_t)bn * g.R * g.S);
+        if (lds > 60 * 1024) continue;
+        out = {wm, tm, tn, {oh, ih, iw, Hc, Wc, Hc / oh, dr0, ds0}, lds};
+        return true;
+    }
+    return false;
+}
+
+template <int WM, int TM, int TN>
+static hipError_t launch_s2(const float* dY, const float* B, float* dX, const ConvGeom& g, const S2Cfg& c, bool acc,
+                            hipStream_t st) {
+    constexpr int BN = (4 / WM) * TN * 16;
+    dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN), 4u);
+    hipLaunchKernelGGL((conv_dgrad_s2_f32<WM, TM, TN>), grid, dim3(256), c.lds, st, dY, B, dX, g, c.t, (int)acc);
+    return hipGetLastError();
+}
+
+static hipError_t dispatch_s2(const float* dY, const float* B, float* dX, const ConvGeom& g, const S2Cfg& c, bool acc,
+                              hipStream_t st) {
+#define S2(WM_, TM_, TN_) \
+    if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) return launch_s2<WM_, TM_, TN_>(dY, B, dX, g, c, acc, st);
+    S2(4, 4, 1) S2(4, 2, 1) S2(2, 2, 1) S2(4, 1, 1) S2(2, 1, 1) S2(1, 2, 1) S2(1, 1, 1)
+#undef S2
+    return hipErrorInvalidValue;
+}
+
 template <int MODE, int WM, int TM, int TN>
 static hipError_t launch_cfg(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                             bool acc, float* pmean, float* pm2, hipStream_t st) {
+                             bool acc, double* stats, hipStream_t st) {
     constexpr int BM = WM * TM * 16, BN = (4 / WM) * TN * 16;
     const long M = (long)g.Nb * g.Ho * g.Wo;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
     const bool fast = g.Cs % 16 == 0;
-    if (pmean) {
+    if (stats) {
         if (fast)
             hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true, true>), grid, dim3(256), 0, st, src, B, bias,
-                               Y, g, (int)acc, pmean, pm2);
+                               Y, g, (int)acc, stats);
         else
             hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false, true>), grid, dim3(256), 0, st, src, B, bias,
-                               Y, g, (int)acc, pmean, pm2);
+                               Y, g, (int)acc, stats);
     } else {
         if (fast)
             hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true, false>), grid, dim3(256), 0, st, src, B, bias,
-                               Y, g, (int)acc, pmean, pm2);
+                               Y, g, (int)acc, stats);
         else
             hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false, false>), grid, dim3(256), 0, st, src, B, bias,
-                               Y, g, (int)acc, pmean, pm2);
+                               Y, g, (int)acc, stats);
     }
     return hipGetLastError();
 }
@@ -696,44 +893,42 @@ static ConvCfg pick_cfg(const ConvGeom& g) {
     return {0, 64, 128, 2, 2, 4};
 }
 
-int conv_tile_rows(const ConvGeom& g) {
-    TileCfg t;
-    if (pick_tile(CONV_FWD, g, t)) return t.wm * t.tm * 16;
-    return pick_cfg(g).bm;
-}
-
 template <int MODE>
 static hipError_t launch_mode(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              bool acc, float* pmean, float* pm2, hipStream_t st) {
+                              bool acc, double* stats, hipStream_t st) {
     TileCfg tc;
-    if (pick_tile(MODE, g, tc)) return dispatch_tile<MODE>(src, B, bias, Y, g, tc, acc, pmean, pm2, st);
+    if (pick_tile(MODE, g, tc)) return dispatch_tile<MODE>(src, B, bias, Y, g, tc, acc, stats, st);
+    if (MODE == CONV_DGRAD) {
+        S2Cfg sc;
+        if (pick_s2(g, sc)) return dispatch_s2(src, B, Y, g, sc, acc, st);
+    }
     ConvCfg c = pick_cfg(g);
     if (c.lds) {
         if (c.bn == 16) {
-            if (c.bm == 256) return launch_lds<MODE, 256, 16, 4>(src, B, bias, Y, g, acc, pmean, pm2, st);
-            return launch_lds<MODE, 64, 16, 4>(src, B, bias, Y, g, acc, pmean, pm2, st);
+            if (c.bm == 256) return launch_lds<MODE, 256, 16, 4>(src, B, bias, Y, g, acc, stats, st);
+            return launch_lds<MODE, 64, 16, 4>(src, B, bias, Y, g, acc, stats, st);
         }
         if (c.bn == 32) {
-            if (c.bm == 128) return launch_lds<MODE, 128, 32, 4>(src, B, bias, Y, g, acc, pmean, pm2, st);
-            return launch_lds<MODE, 64, 32, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
+            if (c.bm == 128) return launch_lds<MODE, 128, 32, 4>(src, B, bias, Y, g, acc, stats, st);
+            return launch_lds<MODE, 64, 32, 2>(src, B, bias, Y, g, acc, stats, st);
         }
         if (c.bn == 64) {
-            if (c.bm == 64) return launch_lds<MODE, 64, 64, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
-            return launch_lds<MODE, 32, 64, 1>(src, B, bias, Y, g, acc, pmean, pm2, st);
+            if (c.bm == 64) return launch_lds<MODE, 64, 64, 2>(src, B, bias, Y, g, acc, stats, st);
+            return launch_lds<MODE, 32, 64, 1>(src, B, bias, Y, g, acc, stats, st);
         }
-        return launch_lds<MODE, 64, 128, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
+        return launch_lds<MODE, 64, 128, 2>(src, B, bias, Y, g, acc, stats, st);
     }
-    if (c.wm == 4 && c.tn == 1) return launch_cfg<MODE, 4, 2, 1>(src, B, bias, Y, g, acc, pmean, pm2, st);
-    if (c.wm == 4) return launch_cfg<MODE, 4, 2, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
-    if (c.tn == 4) return launch_cfg<MODE, 2, 2, 4>(src, B, bias, Y, g, acc, pmean, pm2, st);
-    if (c.tm == 2) return launch_cfg<MODE, 2, 2, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
-    return launch_cfg<MODE, 2, 1, 2>(src, B, bias, Y, g, acc, pmean, pm2, st);
+    if (c.wm == 4 && c.tn == 1) return launch_cfg<MODE, 4, 2, 1>(src, B, bias, Y, g, acc, stats, st);
+    if (c.wm == 4) return launch_cfg<MODE, 4, 2, 2>(src, B, bias, Y, g, acc, stats, st);
+    if (c.tn == 4) return launch_cfg<MODE, 2, 2, 4>(src, B, bias, Y, g, acc, stats, st);
+    if (c.tm == 2) return launch_cfg<MODE, 2, 2, 2>(src, B, bias, Y, g, acc, stats, st);
+    return launch_cfg<MODE, 2, 1, 2>(src, B, bias, Y, g, acc, stats, st);
 }
 
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, float* pmean, float* pm2, hipStream_t st) {
-    if (mode == CONV_FWD) return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, pmean, pm2, st);
-    return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, nullptr, nullptr, st);
+                             const ConvGeom& g, bool accumulate, double* stats, hipStream_t st) {
+    if (mode == CONV_FWD) return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, stats, st);
+    return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, nullptr, st);
 }
 
 // ------------------------------------------------------------------------
@@ -865,8 +1060,157 @@ __global__ __launch_bounds__(256) void conv_wgrad_f32(const float* __restrict__ 
     }
 }
 
-WgradPlan wgrad_plan(int Cout, int Ktot, long M) {
-    WgradPlan p;
+// Spatially tiled weight gradient (Cs % 16 == 0): a workgroup takes a tile
+// of TP output pixels (OH full rows of one image, or IMGS whole images), 16
+// output channels and 16 input channels, and produces the partial
+//     dW[co][r][s][c] = sum over the tile's pixels p of dY[p][co] * X[src(p, r, s)][c]
+// for every tap.  The tile's input rows (halo and padding included; for a
+// 1x1 conv just the pixels it reads) are staged in LDS once; each wave takes
+// NG groups of 16 pixels, keeps their dY values in registers and runs all
+// taps over them, so dY is read once and X once per channel block.  The
+// reduction dimension k of v_mfma_f32_16x16x4_f32 is the pixel: lane
+// (li, gi) supplies dY[p][co0 + li] and X[src(p)][c0 + li] for the same four
+// pixels p = 16 g + 4 gi + j.  Waves are summed in a fixed order and every
+// tile writes its own partial part[tile][co][(r, s, c)], summed in order by
+// the reduce kernel.
+struct WgTileGeom { int OH, IMGS, IH, IW, tiles_per_img, TP; };
+
+template <int RS, int NG, int ST, bool K1>
+__global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restrict__ dY, const float* __restrict__ X,
+                                                           float* __restrict__ part, WgArgs a, WgTileGeom t) {
+    constexpr int LDW = 20;
+    constexpr int JST = (K1 ? 1 : ST) * LDW;   // LDS distance between a lane's four pixels
+    extern __shared__ float lds[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int gi = lane >> 4, li = lane & 15;
+    const int tile = blockIdx.x;
+    const int co0 = blockIdx.y * 16, c0 = blockIdx.z * 16;
+    const int img0 = t.IMGS == 1 ? tile / t.tiles_per_img : tile * t.IMGS;
+    const int oh0 = t.IMGS == 1 ? (tile - img0 * t.tiles_per_img) * t.OH : 0;
+    const int Ktot = RS * a.Cin_p;
+    const long m0 = (long)tile * t.TP;
+    const int ohw = t.OH * a.Wo;
+
+    // this lane's pixels p = 16 (wave NG + g) + 4 gi + j: four consecutive
+    // pixels of one output row (Wo % 4 == 0), so one LDS base per group
+    f4 av[NG];
+    int boff[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        const int p = (wave * NG + g) * 16 + gi * 4;
+        const int il = p / ohw, rem = p - il * ohw;
+        const int ohl = rem / a.Wo, ow = rem - ohl * a.Wo;
+        boff[g] = (K1 ? p : (il * t.IH + ohl * ST) * t.IW + ow * ST) * LDW + li;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) av[g][j] = dY[(m0 + p + j) * a.Cout + co0 + li];
+    }
+
+    float* Xs = lds;
+    const int npix = t.IMGS * t.IH * t.IW;
+    lds_stage<8>(npix * 4, [&](int idx, const float*& sp, float*& dp) {
+        const int q = idx & 3, pix = idx >> 2;
+        const int il = pix / (t.IH * t.IW), rem = pix - il * (t.IH * t.IW);
+        const int ih = rem / t.IW, iw = rem - ih * t.IW;
+        const int h = K1 ? (oh0 + ih) * ST : oh0 * ST - a.pad + ih;
+        const int w = K1 ? iw * ST : iw - a.pad;
+        if (h >= 0 && h < a.Hi && w >= 0 && w < a.Wi)
+            sp = X + ((long)((img0 + il) * a.Hi + h) * a.Wi + w) * a.Cin_p + c0 + q * 4;
+        dp = Xs + pix * LDW + q * 4;
+    });
+    int toff[RS];
+#pragma unroll
+    for (int k = 0; k < RS; ++k) toff[k] = K1 ? 0 : ((k / 3) * t.IW + k % 3) * LDW;
+    __syncthreads();
+
+    f4 acc[RS];
+#pragma unroll
+    for (int k = 0; k < RS; ++k) acc[k] = f4{0.f, 0.f, 0.f, 0.f};
+    // per group: all RS x 4 operands are read before its MFMAs, the next
+    // group's reads are issued before this group's MFMAs
+    float bv[2][RS][4];
+#pragma unroll
+    for (int k = 0; k < RS; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bv[0][k][j] = Xs[boff[0] + toff[k] + j * JST];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        if (g + 1 < NG) {
+#pragma unroll
+            for (int k = 0; k < RS; ++k)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) bv[(g + 1) & 1][k][j] = Xs[boff[g + 1] + toff[k] + j * JST];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int k = 0; k < RS; ++k) acc[k] = mfma16x16x4(av[g][j], bv[g & 1][k][j], acc[k]);
+    }
+    __syncthreads();   // the X tile is dead: its space takes the wave sums
+
+    float* red = lds;   // [RS][16 co][16 c]
+    for (int w = 0; w < 4; ++w) {
+        if (wave == w) {
+#pragma unroll
+            for (int k = 0; k < RS; ++k)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float* slot = red + (k * 16 + gi * 4 + i) * 16 + li;
+                    *slot = w == 0 ? acc[k][i] : *slot + acc[k][i];
+                }
+        }
+        __syncthreads();
+    }
+    float* out = part + (long)tile * a.Cout * Ktot;
+    for (int e = tid; e < RS * 256; e += 256) {
+        const int k = e >> 8, col = (e >> 4) & 15, c = e & 15;
+        out[(long)(co0 + col) * Ktot + k * a.Cin_p + c0 + c] = red[e];
+    }
+}
+
+// Tile shape for the spatially tiled weight gradient, or false when it does
+// not apply (the GEMM-style kernel takes those passes).
+static bool pick_wgrad_tile(int Nb, int Hi, int Wi, int Cin_p, int Ho, int Wo, int Cout, int R, int S, int stride,
+                            int pad, WgTileGeom& t) {
+    if (Cin_p % 16 || Cout % 16 || Wo % 4 || (stride != 1 && stride != 2)) return false;
+    if (!((R == 3 && S == 3) || (R == 1 && S == 1 && pad == 0))) return false;
+    const bool k1 = R == 1;
+    for (int tp : {256, 128, 64}) {
+        int oh, imgs;
+        if (Ho * Wo >= tp) {
+            if (tp % Wo) continue;
+            oh = tp / Wo;
+            if (Ho % oh) continue;
+            imgs = 1;
+        } else {
+            if (tp % (Ho * Wo)) continue;
+            oh = Ho;
+            imgs = tp / (Ho * Wo);
+            if (Nb % imgs) continue;
+        }
+        const int ih = k1 ? oh : (oh - 1) * stride + R, iw = k1 ? Wo : (Wo - 1) * stride + S;
+        const size_t lds = sizeof(float) * std::max<size_t>((size_t)imgs * ih * iw * 20, (size_t)R * S * 256);
+        if (lds > 60 * 1024) continue;
+        t = WgTileGeom{oh, imgs, ih, iw, imgs == 1 ? Ho / oh : 0, tp};
+        return true;
+    }
+    return false;
+}
+
+WgradPlan wgrad_plan(int Nb, int Hi, int Wi, int Cin_p, int Ho, int Wo, int Cout, int R, int S, int stride, int pad) {
+    WgradPlan p{};
+    const long M = (long)Nb * Ho * Wo;
+    const int Ktot = R * S * Cin_p;
+    WgTileGeom t;
+    if (pick_wgrad_tile(Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, R, S, stride, pad, t)) {
+        p.tile = 1;
+        p.oh = t.OH;
+        p.imgs = t.IMGS;
+        p.splits = (int)(M / t.TP);
+        p.pix_per_split = t.TP;
+        p.part_floats = (long)p.splits * Cout * Ktot;
+        return p;
+    }
+
     p.tm = Cout <= 16 ? 1 : (Cout <= 32 ? 2 : 4);
     p.tn = 4;
     const long tiles = (long)((Cout + 16 * p.tm - 1) / (16 * p.tm)) * ((Ktot + 16 * p.tn - 1) / (16 * p.tn));
@@ -893,31 +1237,65 @@ static hipError_t launch_wg(const float* dY, const float* X, float* part, const 
     return hipGetLastError();
 }
 
+template <int RS, int NG, int ST, bool K1>
+static hipError_t launch_wg_tile(const float* dY, const float* X, float* part, const WgArgs& a, const WgTileGeom& t,
+                                 hipStream_t st) {
+    const long M = (long)a.Nb * a.Ho * a.Wo;
+    dim3 grid((unsigned)(M / t.TP), (unsigned)(a.Cout / 16), (unsigned)(a.Cin_p / 16));
+    const size_t lds = sizeof(float) * std::max<size_t>((size_t)t.IMGS * t.IH * t.IW * 20, (size_t)RS * 256);
+    hipLaunchKernelGGL((conv_wgrad_tile_f32<RS, NG, ST, K1>), grid, dim3(256), lds, st, dY, X, part, a, t);
+    return hipGetLastError();
+}
+
+template <int RS, int ST, bool K1>
+static hipError_t launch_wg_tile_ng(const float* dY, const float* X, float* part, const WgArgs& a,
+                                    const WgTileGeom& t, hipStream_t st) {
+    const int ng = t.TP / 64;
+    if (ng == 4) return launch_wg_tile<RS, 4, ST, K1>(dY, X, part, a, t, st);
+    if (ng == 2) return launch_wg_tile<RS, 2, ST, K1>(dY, X, part, a, t, st);
+    return launch_wg_tile<RS, 1, ST, K1>(dY, X, part, a, t, st);
+}
+
 hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int Nb, int Hi, int Wi, int Cin_p,
                              int Ho, int Wo, int Cout, int R, int S, int stride, int pad, const WgradPlan& p,
                              hipStream_t st) {
     WgArgs a{Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, R, S, stride, pad, p.pix_per_split};
+    if (p.tile) {
+        WgTileGeom t;
+        if (!pick_wgrad_tile(Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, R, S, stride, pad, t) || t.OH != p.oh ||
+            t.IMGS != p.imgs)
+            return hipErrorInvalidValue;
+        if (R == 1) {
+            if (stride == 1) return launch_wg_tile_ng<1, 1, true>(dY, X, part, a, t, st);
+            return launch_wg_tile_ng<1, 2, true>(dY, X, part, a, t, st);
+        }
+        if (stride == 1) return launch_wg_tile_ng<9, 1, false>(dY, X, part, a, t, st);
+        return launch_wg_tile_ng<9, 2, false>(dY, X, part, a, t, st);
+    }
     if (p.tm == 1) return launch_wg<1, 4>(dY, X, part, a, p, st);
     if (p.tm == 2) return launch_wg<2, 4>(dY, X, part, a, p, st);
     return launch_wg<4, 4>(dY, X, part, a, p, st);
 }
 
-// 64 outputs per workgroup; four lanes per output each sum a fixed,
-// interleaved subset of the splits, then the four are added in order.
-__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ part, int splits, int Cout,
-                                                           int Ktot, int Cin, int Cin_p, int R, int S,
-                                                           float* __restrict__ g) {
-    __shared__ float red[4][64];
+// 64 outputs per workgroup; L lanes per output (L = 4, 8 or 16 by the split
+// count, 64 L threads) each sum a fixed, interleaved subset of the splits,
+// then the L partial sums are added in order.
+__global__ __launch_bounds__(1024) void wgrad_reduce_kernel(const float* __restrict__ part, int splits, int Cout,
+                                                            int Ktot, int Cin, int Cin_p, int R, int S,
+                                                            float* __restrict__ g) {
+    __shared__ float red[16][64];
+    const int L = blockDim.x >> 6;
     const int j = threadIdx.x & 63, sl = threadIdx.x >> 6;
     const long idx = (long)blockIdx.x * 64 + j;
     const long total = (long)Cout * Ktot;
     float s = 0.f;
     if (idx < total)
-        for (int k = sl; k < splits; k += 4) s += part[(long)k * total + idx];
+        for (int k = sl; k < splits; k += L) s += part[(long)k * total + idx];
     red[sl][j] = s;
     __syncthreads();
     if (sl != 0 || idx >= total) return;
-    s = ((red[0][j] + red[1][j]) + red[2][j]) + red[3][j];
+    s = red[0][j];
+    for (int l = 1; l < L; ++l) s += red[l][j];
     const int co = (int)(idx / Ktot), col = (int)(idx - (long)co * Ktot);
     const int tap = col / Cin_p, c = col - tap * Cin_p;
     if (c >= Cin) return;
@@ -928,8 +1306,9 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restri
 hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
                                float* g, hipStream_t st) {
     const long n = (long)Cout * Ktot;
-    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, part, splits, Cout,
-                       Ktot, Cin, Cin_p, R, S, g);
+    const int L = splits >= 256 ? 16 : (splits >= 64 ? 8 : 4);
+    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64 * L), 0, st, part, splits,
+                       Cout, Ktot, Cin, Cin_p, R, S, g);
     return hipGetLastError();
 }
 

@@ -28,18 +28,24 @@ struct StepArgs {
 };
 hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* labels, float lr, hipStream_t st);
 
+// Batch-norm reductions are merged across workgroups by fp64 atomic adds
+// into per-channel accumulators acc[q][kAccSlots][C] (q selects the sum);
+// see bnacc.h.  The first kernel of a step zeroes them.
+constexpr int kAccSlots = 32;
+
 // Y[m][n] (+)= sum_k A[m][k] B[n][k] (+ bias[n]); see ConvGeom.  Forward
-// passes with pmean/pm2 non-null also write per-row-tile batch-norm
-// statistics of Y (tile mean and sum of squared deviations, [T][Ncols],
-// T = ceil(M / conv_tile_rows(g))).
+// passes with stats non-null also add the batch sums of Y (q = 0: sum y,
+// q = 1: sum y^2, per output channel; each row tile's share is formed from
+// its mean and sum of squared deviations) into stats [2][kAccSlots][Ncols].
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, float* pmean, float* pm2, hipStream_t st);
-int conv_tile_rows(const ConvGeom& g);
+                             const ConvGeom& g, bool accumulate, double* stats, hipStream_t st);
 
 // Weight gradient: part[split][Cout][Ktot] = partial sums over pixel ranges
-// of dY[p][cout] * im2col(X)[p][(r,s,c)] (wgrad_plan chooses the splits).
-struct WgradPlan { int tm, tn, splits, pix_per_split; long part_floats; };
-WgradPlan wgrad_plan(int Cout, int Ktot, long M);
+// of dY[p][cout] * im2col(X)[p][(r,s,c)].  wgrad_plan chooses the kernel:
+// spatial tiles (tile = 1: a split is a tile of OH rows of one image or of
+// `imgs` whole images) or GEMM tiles over ranges of pix_per_split pixels.
+struct WgradPlan { int tm, tn, splits, pix_per_split; long part_floats; int tile, oh, imgs; };
+WgradPlan wgrad_plan(int Nb, int Hi, int Wi, int Cin_p, int Ho, int Wo, int Cout, int R, int S, int stride, int pad);
 hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int Nb, int Hi, int Wi, int Cin_p,
                              int Ho, int Wo, int Cout, int R, int S, int stride, int pad, const WgradPlan& p,
                              hipStream_t st);
@@ -52,18 +58,30 @@ hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot
 constexpr int kStatRows = 256;   // rows per tile of the stand-alone kernels
 int stats_tiles(long M);
 // per tile of kStatRows rows: mean and sum of squared deviations per channel
-hipError_t launch_stats_partial(const float* x, long M, int C, float* pmean, float* pm2, hipStream_t st);
-// merges T tiles of R rows (fp64, fixed order): mean, rstd = 1/sqrt(var+eps)
-// with the biased variance, scale = gamma*rstd, shift = beta - mean*scale
-hipError_t launch_stats_finalize(const float* pmean, const float* pm2, int T, int R, long M, int C,
-                                 const float* gamma, const float* beta, float eps, float* mean, float* rstd,
-                                 float* scale, float* shift, hipStream_t st);
+// into pmean / pm2 [T][C] (acc null), or the tile's share of the batch sums
+// added into acc [2][kAccSlots][C] (sum x, sum x^2)
+hipError_t launch_stats_partial(const float* x, long M, int C, float* pmean, float* pm2, double* acc,
+                                hipStream_t st);
 // out[c] = sum_t rows_t * pmean[t][c]: column sums from tile means
 hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C, float* out, hipStream_t st);
-// y = relu?(x1*s1 + t1 [+ r | + x2*s2 + t2])  (r: residual tensor; x2: a second
+// A training-mode batch norm as the per-channel map x*scale + shift.  With
+// acc set, scale and shift come from the batch sums acc [2][kAccSlots][C]
+// over M rows (mean, biased variance, rstd = 1/sqrt(var + eps),
+// scale = gamma*rstd, shift = beta - mean*scale) and the kernel's first
+// workgroup stores [mean | rstd | scale | shift] into aux; with acc null they
+// are read from aux + 2C and aux + 3C.
+struct BnFwd {
+    const double* acc;
+    const float* gamma;
+    const float* beta;
+    float eps;
+    long M;
+    float* aux;
+};
+// y = relu?(bn1(x1) [+ r | + bn2(x2)])  (r: residual tensor; x2: a second
 // normalised input, used when both branches of a residual add end in BN)
-hipError_t launch_bn_act(const float* x1, const float* s1, const float* t1, const float* r, const float* x2,
-                         const float* s2, const float* t2, bool relu, float* y, long M, int C, hipStream_t st);
+hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const float* x2, const BnFwd* b2,
+                         bool relu, float* y, long M, int C, hipStream_t st);
 
 // ---- batch-norm backward (with the group's ReLU mask and residual fan-out) ----
 struct BnBwdArgs {
@@ -74,18 +92,23 @@ struct BnBwdArgs {
     long M;
     int C;
 };
-// per tile of kStatRows rows: sum g, sum g*xhat1, sum g*xhat2
-hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, float* p0, float* p1, float* p2, hipStream_t st);
-// gg/gb (dgamma, dbeta; null = not wanted) and coef = [gamma*rstd | mean g |
-// mean g*xhat] per channel; the second set for a dual group (coef2 null if not)
-hipError_t launch_bn_bwd_finalize(const float* p0, const float* p1, const float* p2, int T, long M, int C,
-                                  const float* gamma1, const float* rstd1, float* gg1, float* gb1, float* coef1,
-                                  const float* gamma2, const float* rstd2, float* gg2, float* gb2, float* coef2,
-                                  hipStream_t st);
+// per tile of kStatRows rows, the tile's sum g, sum g*xhat1 and sum g*xhat2
+// added into acc [3][kAccSlots][C]
+hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, double* acc, hipStream_t st);
+// Coefficients of the backward apply, derived in its prologue from the sums
+// acc [3][kAccSlots][C]: per batch norm a = gamma*rstd, mean g and mean
+// g*xhat; its first workgroup also stores dgamma = sum g*xhat and dbeta =
+// sum g (null pointers: not wanted).  acc null: no batch-norm input gradient
+// is formed (only dres).
+struct BnBwdCoef {
+    const double* acc;
+    const float* gamma1; float* gg1; float* gb1;
+    const float* gamma2; float* gg2; float* gb2;
+};
 // dx = a*(g - mean g - xhat*mean g*xhat) into dx1 / dx2 (null = skip), and g
 // into dres (the residual branch) -- each written or accumulated
-hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const float* coef1, const float* coef2, float* dx1, bool acc1,
-                               float* dx2, bool acc2, float* dres, bool accres, hipStream_t st);
+hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const BnBwdCoef& k, float* dx1, bool acc1, float* dx2, bool acc2,
+                               float* dres, bool accres, hipStream_t st);
 
 // ---- fused classifier head: global average pool, linear, softmax CE ----
 hipError_t launch_head_fwd(const float* x, int Nb, int HW, int C, const float* W, const float* b, int O,
@@ -120,9 +143,10 @@ hipError_t launch_linear_bwd_x(const float* dz, const float* W, float* dx, int N
 hipError_t launch_softmax_ce(const float* z, const StepArgs* args, float* dz, float* loss, int Nb, int Cls,
                              hipStream_t st);
 
-// the step's NCHW images (C channels) -> NHWC (Cp >= C channels, zero-padded)
-hipError_t launch_nchw_to_nhwc(const StepArgs* args, float* dst, int Nb, int C, int H, int W, int Cp,
-                               hipStream_t st);
+// the step's NCHW images (C channels) -> NHWC (Cp >= C channels, zero-padded);
+// also zeroes the step's n_zero reduction accumulators at zero
+hipError_t launch_nchw_to_nhwc(const StepArgs* args, float* dst, int Nb, int C, int H, int W, int Cp, double* zero,
+                               long n_zero, hipStream_t st);
 // NHWC (Cp) -> NCHW (C), for inspection
 hipError_t launch_nhwc_to_nchw(const float* src, float* dst, int Nb, int C, int H, int W, int Cp, hipStream_t st);
 

@@ -3,9 +3,10 @@
 // average pool, the linear head, softmax cross-entropy, layout conversions,
 // the replica snapshot, the block SGD update and replica averaging.
 //
-// Activations are NHWC float32.  Channel reductions run in two fixed-order
-// stages (per-workgroup fp64 partials, then one pass over the partials), so
-// every result is bitwise reproducible run to run.
+// Activations are NHWC float32.  Batch-norm reductions are merged across
+// workgroups by fp64 atomic adds into per-channel accumulators (bnacc.h);
+// every other reduction runs in a fixed order.
+#include "bnacc.h"
 #include "kernels.h"
 
 namespace lpp {
@@ -16,8 +17,8 @@ static inline unsigned nblocks(long n, int per) { return (unsigned)((n + per - 1
 
 // ------------------------------------------------------------------------
 // batch-norm statistics: per row tile, per channel, the tile mean and the
-// sum of squared deviations from it (two passes over the tile); merged over
-// tiles in fp64 by a fixed-order finalize
+// sum of squared deviations from it (two passes over the tile), written as
+// partials or added to the batch sums
 // ------------------------------------------------------------------------
 
 int stats_tiles(long M) { return (int)((M + kStatRows - 1) / kStatRows); }
@@ -30,7 +31,8 @@ __device__ __forceinline__ void quad_layout(int C4, int qbase, int& nq, int& rl)
 }
 
 __global__ __launch_bounds__(256) void stats_partial_k(const float* __restrict__ x, long M, int C,
-                                                       float* __restrict__ pmean, float* __restrict__ pm2) {
+                                                       float* __restrict__ pmean, float* __restrict__ pm2,
+                                                       double* __restrict__ acc) {
     __shared__ f4 red[256];
     __shared__ float mean_s[1024];
     const int tid = threadIdx.x;
@@ -70,9 +72,16 @@ __global__ __launch_bounds__(256) void stats_partial_k(const float* __restrict__
             f4 t = f4{0.f, 0.f, 0.f, 0.f};
             for (int l = 0; l < rl; ++l) t += red[l * nq + tid];
             for (int k = 0; k < 4; ++k) {
-                const long o = (long)blockIdx.x * C + (qbase + tid) * 4 + k;
-                pmean[o] = mean_s[(tid * 4 + k) & 1023];
-                pm2[o] = t[k];
+                const int c = (qbase + tid) * 4 + k;
+                const float mu = mean_s[(tid * 4 + k) & 1023];
+                if (acc) {
+                    const double n = (double)rows, m = (double)mu;
+                    acc_add(acc, 0, blockIdx.x % kAccSlots, C, c, m * n);
+                    acc_add(acc, 1, blockIdx.x % kAccSlots, C, c, (double)t[k] + n * m * m);
+                } else {
+                    pmean[(long)blockIdx.x * C + c] = mu;
+                    pm2[(long)blockIdx.x * C + c] = t[k];
+                }
             }
         }
         __syncthreads();
@@ -95,34 +104,6 @@ __device__ __forceinline__ double tree_sum256(double v, double* red) {
     return r;
 }
 
-__global__ __launch_bounds__(256) void stats_finalize_k(const float* __restrict__ pmean, const float* __restrict__ pm2,
-                                                        int T, int R, long M, int C, const float* __restrict__ gamma,
-                                                        const float* __restrict__ beta, float eps, float* mean,
-                                                        float* rstd, float* scale, float* shift) {
-    __shared__ double red[256];
-    const int c = blockIdx.x;
-    double s = 0.0;
-#pragma unroll 4
-    for (int t = threadIdx.x; t < T; t += 256)
-        s += (double)min((long)R, M - (long)t * R) * (double)pmean[(long)t * C + c];
-    const double mu = tree_sum256(s, red) / (double)M;
-    double q = 0.0;
-#pragma unroll 4
-    for (int t = threadIdx.x; t < T; t += 256) {
-        const double d = (double)pmean[(long)t * C + c] - mu;
-        q += (double)pm2[(long)t * C + c] + (double)min((long)R, M - (long)t * R) * d * d;
-    }
-    q = tree_sum256(q, red);
-    if (threadIdx.x == 0) {
-        const double r = 1.0 / sqrt(q / (double)M + (double)eps);
-        const double sc = (double)gamma[c] * r;
-        mean[c] = (float)mu;
-        rstd[c] = (float)r;
-        scale[c] = (float)sc;
-        shift[c] = (float)((double)beta[c] - mu * sc);
-    }
-}
-
 // out[c] = sum over tiles of n_t * mean_t (the column sum), fixed order
 __global__ __launch_bounds__(256) void sum_from_tiles_k(const float* __restrict__ pmean, int T, int R, long M, int C,
                                                         float* __restrict__ out) {
@@ -140,45 +121,46 @@ hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C
     return hipGetLastError();
 }
 
-hipError_t launch_stats_partial(const float* x, long M, int C, float* pmean, float* pm2, hipStream_t st) {
-    hipLaunchKernelGGL(stats_partial_k, dim3(stats_tiles(M)), dim3(256), 0, st, x, M, C, pmean, pm2);
+hipError_t launch_stats_partial(const float* x, long M, int C, float* pmean, float* pm2, double* acc,
+                                hipStream_t st) {
+    hipLaunchKernelGGL(stats_partial_k, dim3(stats_tiles(M)), dim3(256), 0, st, x, M, C, pmean, pm2, acc);
     return hipGetLastError();
 }
 
-hipError_t launch_stats_finalize(const float* pmean, const float* pm2, int T, int R, long M, int C,
-                                 const float* gamma, const float* beta, float eps, float* mean, float* rstd,
-                                 float* scale, float* shift, hipStream_t st) {
-    hipLaunchKernelGGL(stats_finalize_k, dim3(C), dim3(256), 0, st, pmean, pm2, T, R, M, C, gamma, beta, eps, mean,
-                       rstd, scale, shift);
-    return hipGetLastError();
-}
 
 // ------------------------------------------------------------------------
 // batch-norm apply, fused with the residual add and the ReLU that follow it
 //   y = act(x1*s1 + t1 [+ r | + x2*s2 + t2])
 // ------------------------------------------------------------------------
 
+// Workgroups derive the batch-norm coefficients into LDS first; each thread
+// then walks quads i, i + stride, ... whose channel advances by a fixed step.
 template <int RES, bool RELU>
-__global__ void bn_act_k(const f4* __restrict__ x1, const float* __restrict__ s1, const float* __restrict__ t1,
-                         const f4* __restrict__ r, const f4* __restrict__ x2, const float* __restrict__ s2,
-                         const float* __restrict__ t2, f4* __restrict__ y, long n4, int C) {
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
-        const int c = (int)((i * 4) % C);
+__global__ __launch_bounds__(256) void bn_act_k(const f4* __restrict__ x1, BnFwd b1, const f4* __restrict__ r,
+                                                const f4* __restrict__ x2, BnFwd b2, f4* __restrict__ y, long n4,
+                                                int C) {
+    extern __shared__ float co[];   // scale1 | shift1 | scale2 | shift2
+    bn_fwd_coeffs(b1, C, co, co + C);
+    if (RES == 2) bn_fwd_coeffs(b2, C, co + 2 * C, co + 3 * C);
+    __syncthreads();
+    const int C4 = C >> 2;
+    const long stride = (long)gridDim.x * blockDim.x;
+    long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    int q = (int)(i % C4);
+    const int qstep = (int)(stride % C4);
+    for (; i < n4; i += stride) {
+        const int c = q * 4;
         const f4 a = x1[i];
-        f4 o;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) o[k] = a[k] * s1[c + k] + t1[c + k];
+        f4 o = a * *(const f4*)(co + c) + *(const f4*)(co + C + c);
         if (RES == 1) o += r[i];
-        if (RES == 2) {
-            const f4 b = x2[i];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) o[k] += b[k] * s2[c + k] + t2[c + k];
-        }
+        if (RES == 2) o += x2[i] * *(const f4*)(co + 2 * C + c) + *(const f4*)(co + 3 * C + c);
         if (RELU) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) o[k] = o[k] > 0.f ? o[k] : 0.f;
         }
         y[i] = o;
+        q += qstep;
+        if (q >= C4) q -= C4;
     }
 }
 
@@ -187,13 +169,24 @@ static unsigned ew_grid(long n4) {
     return (unsigned)(b < 8192 ? (b < 1 ? 1 : b) : 8192);
 }
 
-hipError_t launch_bn_act(const float* x1, const float* s1, const float* t1, const float* r, const float* x2,
-                         const float* s2, const float* t2, bool relu, float* y, long M, int C, hipStream_t st) {
+// batch-norm kernels: at most 1024 workgroups, so the coefficient prologue
+// is paid a bounded number of times
+static unsigned bn_grid(long n4) {
+    long b = (n4 + 255) / 256;
+    return (unsigned)(b < 1024 ? (b < 1 ? 1 : b) : 1024);
+}
+
+hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const float* x2, const BnFwd* b2,
+                         bool relu, float* y, long M, int C, hipStream_t st) {
+    if (C % 4) return hipErrorInvalidValue;
     const long n4 = M * C / 4;
     const int res = r ? 1 : (x2 ? 2 : 0);
-#define BNACT(RS, RL)                                                                                       \
-    hipLaunchKernelGGL((bn_act_k<RS, RL>), dim3(ew_grid(n4)), dim3(256), 0, st, (const f4*)x1, s1, t1,      \
-                       (const f4*)r, (const f4*)x2, s2, t2, (f4*)y, n4, C)
+    if (res == 2 && !b2) return hipErrorInvalidValue;
+    const BnFwd bb = b2 ? *b2 : BnFwd{};
+    const size_t lds = sizeof(float) * 4 * C;
+#define BNACT(RS, RL)                                                                                  \
+    hipLaunchKernelGGL((bn_act_k<RS, RL>), dim3(bn_grid(n4)), dim3(256), lds, st, (const f4*)x1, b1,   \
+                       (const f4*)r, (const f4*)x2, bb, (f4*)y, n4, C)
     if (res == 0) { if (relu) BNACT(0, true); else BNACT(0, false); }
     else if (res == 1) { if (relu) BNACT(1, true); else BNACT(1, false); }
     else { if (relu) BNACT(2, true); else BNACT(2, false); }
@@ -209,8 +202,7 @@ hipError_t launch_bn_act(const float* x1, const float* s1, const float* t1, cons
 // ------------------------------------------------------------------------
 
 template <bool MASK, bool DUAL>
-__global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, float* __restrict__ p0, float* __restrict__ p1,
-                                                       float* __restrict__ p2) {
+__global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, double* __restrict__ acc) {
     __shared__ f4 red[3][256];
     const int tid = threadIdx.x;
     const int C = a.C, C4 = C >> 2;
@@ -254,120 +246,112 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, float* __res
                 t1 += red[1][l * nq + tid];
                 t2 += red[2][l * nq + tid];
             }
+            const int slot = blockIdx.x % kAccSlots;
             for (int k = 0; k < 4; ++k) {
-                const long o = (long)blockIdx.x * C + (qbase + tid) * 4 + k;
-                p0[o] = t0[k];
-                p1[o] = t1[k];
-                if (DUAL) p2[o] = t2[k];
+                const int c = (qbase + tid) * 4 + k;
+                acc_add(acc, 0, slot, C, c, (double)t0[k]);
+                acc_add(acc, 1, slot, C, c, (double)t1[k]);
+                if (DUAL) acc_add(acc, 2, slot, C, c, (double)t2[k]);
             }
         }
         __syncthreads();
     }
 }
 
-__global__ __launch_bounds__(256) void bn_bwd_finalize_k(const float* __restrict__ p0, const float* __restrict__ p1,
-                                                         const float* __restrict__ p2, int T, long M, int C,
-                                                         const float* __restrict__ gamma1,
-                                                         const float* __restrict__ rstd1, float* gg1, float* gb1,
-                                                         float* coef1, const float* __restrict__ gamma2,
-                                                         const float* __restrict__ rstd2, float* gg2, float* gb2,
-                                                         float* coef2) {
-    __shared__ double red[256];
-    const int c = blockIdx.x;
-    const bool dual = coef2 != nullptr;
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0;
-#pragma unroll 4
-    for (int t = threadIdx.x; t < T; t += 256) {
-        s0 += (double)p0[(long)t * C + c];
-        s1 += (double)p1[(long)t * C + c];
-        if (dual) s2 += (double)p2[(long)t * C + c];
-    }
-    const double t0 = tree_sum256(s0, red);
-    const double t1 = tree_sum256(s1, red);
-    const double t2 = dual ? tree_sum256(s2, red) : 0.0;
-    if (threadIdx.x != 0) return;
-    if (gg1) gg1[c] = (float)t1;
-    if (gb1) gb1[c] = (float)t0;
-    coef1[c] = gamma1[c] * rstd1[c];
-    coef1[C + c] = (float)(t0 / (double)M);
-    coef1[2 * C + c] = (float)(t1 / (double)M);
-    if (dual) {
-        if (gg2) gg2[c] = (float)t2;
-        if (gb2) gb2[c] = (float)t0;
-        coef2[c] = gamma2[c] * rstd2[c];
-        coef2[C + c] = (float)(t0 / (double)M);
-        coef2[2 * C + c] = (float)(t2 / (double)M);
-    }
-}
-
+// Prologue: per channel a = gamma*rstd, mean g, mean g*xhat (and the second
+// set) from the accumulated sums, plus mean and rstd, into LDS; the first
+// workgroup stores dgamma and dbeta.
 template <bool MASK>
-__global__ void bn_bwd_apply_k(BnBwdArgs a, const float* __restrict__ coef1, const float* __restrict__ coef2,
-                               float* __restrict__ dx1, int acc1, float* __restrict__ dx2, int acc2,
-                               float* __restrict__ dres, int accres) {
-    const long n4 = a.M * a.C / 4;
+__global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, float* __restrict__ dx1, int acc1,
+                                                      float* __restrict__ dx2, int acc2, float* __restrict__ dres,
+                                                      int accres) {
+    extern __shared__ float cf[];   // a1 | mg | mgx1 | mean1 | rstd1 | a2 | mgx2 | mean2 | rstd2
     const int C = a.C;
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
-        const int c = (int)((i * 4) % C);
+    const bool dual = a.x2 != nullptr;
+    if (k.acc) {
+        for (int c = threadIdx.x; c < C; c += blockDim.x) {
+            const double t0 = acc_read(k.acc, 0, C, c), t1 = acc_read(k.acc, 1, C, c);
+            cf[c] = k.gamma1[c] * a.rstd1[c];
+            cf[C + c] = (float)(t0 / (double)a.M);
+            cf[2 * C + c] = (float)(t1 / (double)a.M);
+            cf[3 * C + c] = a.mean1[c];
+            cf[4 * C + c] = a.rstd1[c];
+            if (blockIdx.x == 0) {
+                if (k.gg1) k.gg1[c] = (float)t1;
+                if (k.gb1) k.gb1[c] = (float)t0;
+            }
+            if (dual) {
+                const double t2 = acc_read(k.acc, 2, C, c);
+                cf[5 * C + c] = k.gamma2[c] * a.rstd2[c];
+                cf[6 * C + c] = (float)(t2 / (double)a.M);
+                cf[7 * C + c] = a.mean2[c];
+                cf[8 * C + c] = a.rstd2[c];
+                if (blockIdx.x == 0) {
+                    if (k.gg2) k.gg2[c] = (float)t2;
+                    if (k.gb2) k.gb2[c] = (float)t0;
+                }
+            }
+        }
+    }
+    __syncthreads();
+    const long n4 = a.M * C / 4;
+    const int C4 = C >> 2;
+    const long stride = (long)gridDim.x * blockDim.x;
+    long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    int q = (int)(i % C4);
+    const int qstep = (int)(stride % C4);
+    for (; i < n4; i += stride) {
+        const int c = q * 4;
         f4 g = ((const f4*)a.dy)[i];
         if (MASK) {
-            const f4 y = ((const f4*)a.mask)[i];
+            const f4 yv = ((const f4*)a.mask)[i];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) g[k] = y[k] > 0.f ? g[k] : 0.f;
+            for (int j = 0; j < 4; ++j) g[j] = yv[j] > 0.f ? g[j] : 0.f;
         }
         if (dx1) {
-            const f4 x = ((const f4*)a.x1)[i];
-            f4 o = acc1 ? ((f4*)dx1)[i] : f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const float xh = (x[k] - a.mean1[c + k]) * a.rstd1[c + k];
-                o[k] += coef1[c + k] * (g[k] - coef1[C + c + k] - xh * coef1[2 * C + c + k]);
-            }
-            ((f4*)dx1)[i] = o;
+            const f4 xh = (((const f4*)a.x1)[i] - *(const f4*)(cf + 3 * C + c)) * *(const f4*)(cf + 4 * C + c);
+            const f4 v = *(const f4*)(cf + c) *
+                         (g - *(const f4*)(cf + C + c) - xh * *(const f4*)(cf + 2 * C + c));
+            ((f4*)dx1)[i] = acc1 ? ((f4*)dx1)[i] + v : v;
         }
         if (dx2) {
-            const f4 x = ((const f4*)a.x2)[i];
-            f4 o = acc2 ? ((f4*)dx2)[i] : f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const float xh = (x[k] - a.mean2[c + k]) * a.rstd2[c + k];
-                o[k] += coef2[c + k] * (g[k] - coef2[C + c + k] - xh * coef2[2 * C + c + k]);
-            }
-            ((f4*)dx2)[i] = o;
+            const f4 xh = (((const f4*)a.x2)[i] - *(const f4*)(cf + 7 * C + c)) * *(const f4*)(cf + 8 * C + c);
+            const f4 v = *(const f4*)(cf + 5 * C + c) *
+                         (g - *(const f4*)(cf + C + c) - xh * *(const f4*)(cf + 6 * C + c));
+            ((f4*)dx2)[i] = acc2 ? ((f4*)dx2)[i] + v : v;
         }
         if (dres) ((f4*)dres)[i] = accres ? ((f4*)dres)[i] + g : g;
+        q += qstep;
+        if (q >= C4) q -= C4;
     }
 }
 
-hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, float* p0, float* p1, float* p2, hipStream_t st) {
+hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, double* acc, hipStream_t st) {
     const dim3 grid(stats_tiles(a.M));
     if (a.mask) {
-        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<true, true>), grid, dim3(256), 0, st, a, p0, p1, p2);
-        else hipLaunchKernelGGL((bn_bwd_reduce_k<true, false>), grid, dim3(256), 0, st, a, p0, p1, p2);
+        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<true, true>), grid, dim3(256), 0, st, a, acc);
+        else hipLaunchKernelGGL((bn_bwd_reduce_k<true, false>), grid, dim3(256), 0, st, a, acc);
     } else {
-        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<false, true>), grid, dim3(256), 0, st, a, p0, p1, p2);
-        else hipLaunchKernelGGL((bn_bwd_reduce_k<false, false>), grid, dim3(256), 0, st, a, p0, p1, p2);
+        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<false, true>), grid, dim3(256), 0, st, a, acc);
+        else hipLaunchKernelGGL((bn_bwd_reduce_k<false, false>), grid, dim3(256), 0, st, a, acc);
     }
     return hipGetLastError();
 }
 
-hipError_t launch_bn_bwd_finalize(const float* p0, const float* p1, const float* p2, int T, long M, int C,
-                                  const float* gamma1, const float* rstd1, float* gg1, float* gb1, float* coef1,
-                                  const float* gamma2, const float* rstd2, float* gg2, float* gb2, float* coef2,
-                                  hipStream_t st) {
-    hipLaunchKernelGGL(bn_bwd_finalize_k, dim3(C), dim3(256), 0, st, p0, p1, p2, T, M, C, gamma1, rstd1, gg1, gb1,
-                       coef1, gamma2, rstd2, gg2, gb2, coef2);
-    return hipGetLastError();
-}
 
-hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const float* coef1, const float* coef2, float* dx1, bool acc1,
-                               float* dx2, bool acc2, float* dres, bool accres, hipStream_t st) {
+hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const BnBwdCoef& k, float* dx1, bool acc1, float* dx2, bool acc2,
+                               float* dres, bool accres, hipStream_t st) {
+    if (a.C % 4) return hipErrorInvalidValue;
+    if ((dx1 || dx2) && !k.acc) return hipErrorInvalidValue;
     const long n4 = a.M * a.C / 4;
+    const unsigned grid = (dx1 || dx2 || dres) ? bn_grid(n4) : 1u;   // one workgroup: dgamma, dbeta only
+    const size_t lds = sizeof(float) * 9 * a.C;
     if (a.mask)
-        hipLaunchKernelGGL((bn_bwd_apply_k<true>), dim3(ew_grid(n4)), dim3(256), 0, st, a, coef1, coef2, dx1,
-                           (int)acc1, dx2, (int)acc2, dres, (int)accres);
+        hipLaunchKernelGGL((bn_bwd_apply_k<true>), dim3(grid), dim3(256), lds, st, a, k, dx1, (int)acc1, dx2,
+                           (int)acc2, dres, (int)accres);
     else
-        hipLaunchKernelGGL((bn_bwd_apply_k<false>), dim3(ew_grid(n4)), dim3(256), 0, st, a, coef1, coef2, dx1,
-                           (int)acc1, dx2, (int)acc2, dres, (int)accres);
+        hipLaunchKernelGGL((bn_bwd_apply_k<false>), dim3(grid), dim3(256), lds, st, a, k, dx1, (int)acc1, dx2,
+                           (int)acc2, dres, (int)accres);
     return hipGetLastError();
 }
 
@@ -741,9 +725,10 @@ hipError_t launch_softmax_ce(const float* z, const StepArgs* args, float* dz, fl
 // ------------------------------------------------------------------------
 
 __global__ void nchw_to_nhwc_k(const StepArgs* __restrict__ args, float* __restrict__ d, int Nb, int C, int H,
-                               int W, int Cp) {
+                               int W, int Cp, double* __restrict__ zero, long n_zero) {
     const float* __restrict__ s = args->images;
     const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    for (long z = idx; z < n_zero; z += (long)gridDim.x * blockDim.x) zero[z] = 0.0;
     const long total = (long)Nb * H * W * Cp;
     if (idx >= total) return;
     const int c = (int)(idx % Cp);
@@ -769,10 +754,11 @@ __global__ void nhwc_to_nchw_k(const float* __restrict__ s, float* __restrict__ 
     d[idx] = s[(((long)n * H + h) * W + w) * Cp + c];
 }
 
-hipError_t launch_nchw_to_nhwc(const StepArgs* args, float* dst, int Nb, int C, int H, int W, int Cp,
-                               hipStream_t st) {
+hipError_t launch_nchw_to_nhwc(const StepArgs* args, float* dst, int Nb, int C, int H, int W, int Cp, double* zero,
+                               long n_zero, hipStream_t st) {
     const long total = (long)Nb * H * W * Cp;
-    hipLaunchKernelGGL(nchw_to_nhwc_k, dim3(nblocks(total, 256)), dim3(256), 0, st, args, dst, Nb, C, H, W, Cp);
+    hipLaunchKernelGGL(nchw_to_nhwc_k, dim3(nblocks(total, 256)), dim3(256), 0, st, args, dst, Nb, C, H, W, Cp,
+                       zero, n_zero);
     return hipGetLastError();
 }
 hipError_t launch_nhwc_to_nchw(const float* src, float* dst, int Nb, int C, int H, int W, int Cp, hipStream_t st) {

@@ -50,8 +50,10 @@ struct Layer {
     long wf_off = -1, wd_off = -1;// conv: W_f / W_d in the worker's weight buffer (floats)
     double macs = 0;              // forward multiply-adds (conv, linear)
     lpp::WgradPlan wg{};
-    // workspace offsets (bytes) of this layer's output, its gradient and aux data
-    size_t act = 0, dact = 0, aux = 0;
+    // workspace offsets (bytes) of this layer's output, its gradient and aux
+    // data; BN: its reduction accumulators (doubles [5][kAccSlots][C]: batch
+    // sums of the forward, then sums of the backward)
+    size_t act = 0, dact = 0, aux = 0, acc = 0;
 };
 
 struct Plan {
@@ -399,7 +401,8 @@ struct lpp_ctx {
     long wbuf_floats = 0;
     size_t ws_bytes = 0;
     size_t off_v = 0, off_wbuf = 0, off_g = 0, off_m = 0, off_loss = 0, off_img = 0, off_ps = 0, off_wpart = 0,
-           off_args = 0;
+           off_args = 0, off_acc = 0;
+    long n_acc = 0;                          // doubles zeroed at the start of every step
     bool graphs = true;
     long ps_floats = 0;
     std::unique_ptr<std::atomic<long>[]> counters;
@@ -409,6 +412,10 @@ struct lpp_ctx {
     float* act(Worker& w, int l) { return (float*)(w.ws + M.layers[l].act); }
     float* dact(Worker& w, int l) { return (float*)(w.ws + M.layers[l].dact); }
     float* aux(Worker& w, int l) { return (float*)(w.ws + M.layers[l].aux); }
+    double* acc_fwd(Worker& w, int l) { return (double*)(w.ws + M.layers[l].acc); }
+    double* acc_bwd(Worker& w, int l) {
+        return (double*)(w.ws + M.layers[l].acc) + 2L * lpp::kAccSlots * M.layers[l].out.c;
+    }
 };
 
 namespace {
@@ -492,12 +499,9 @@ int bn_stats_standalone(lpp_ctx* c, Worker& w, int b) {
     const int N = M.desc.batch, C = B.out.c;
     const long rows = (long)N * B.in0.h * B.in0.w;
     const float* x = c->act(w, B.L.in0);
-    float* ax = c->aux(w, b);
     hipStream_t st = w.stream;
-    LAUNCH("bn_stats", 4.0 * rows * C, st, lpp::launch_stats_partial(x, rows, C, w.ps0, w.ps1, st));
-    LAUNCH("bn_stats", 0.0, st,
-           lpp::launch_stats_finalize(w.ps0, w.ps1, lpp::stats_tiles(rows), lpp::kStatRows, rows, C, w.v + B.poff,
-                                      w.v + B.poff + C, M.desc.bn_eps, ax, ax + C, ax + 2 * C, ax + 3 * C, st));
+    LAUNCH("bn_stats", 4.0 * rows * C, st,
+           lpp::launch_stats_partial(x, rows, C, nullptr, nullptr, c->acc_fwd(w, b), st));
     return LPP_OK;
 }
 
@@ -507,7 +511,8 @@ int run_forward(lpp_ctx* c, Worker& w) {
     const int N = M.desc.batch;
     hipStream_t st = w.stream;
     LAUNCH("image", 8.0 * N * M.desc.in_c * M.desc.in_h * M.desc.in_w, st,
-           lpp::launch_nchw_to_nhwc(w.args, w.img, N, M.desc.in_c, M.desc.in_h, M.desc.in_w, M.img_cp, st));
+           lpp::launch_nchw_to_nhwc(w.args, w.img, N, M.desc.in_c, M.desc.in_h, M.desc.in_w, M.img_cp,
+                                     (double*)(w.ws + c->off_acc), c->n_acc, st));
     bool loss_done = false;
     for (const Group& G : M.groups) {
         Layer& Y = M.layers[G.a];
@@ -517,21 +522,9 @@ int run_forward(lpp_ctx* c, Worker& w) {
         case G_CONV: {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride, Y.L.pad};
             const float* bias = Y.L.bias ? w.v + Y.poff + Y.wcount : nullptr;
-            const bool st_on = G.stats_bn >= 0;
             LAUNCH("conv_fwd", 2.0 * Y.macs, st,
                    lpp::launch_conv_igemm(lpp::CONV_FWD, x0, w.wbuf + Y.wf_off, bias, c->act(w, G.a), g, false,
-                                          st_on ? w.ps0 : nullptr, st_on ? w.ps1 : nullptr, st));
-            if (st_on) {
-                const Layer& B = M.layers[G.stats_bn];
-                const long rows = (long)N * Y.out.h * Y.out.w;
-                const int R = lpp::conv_tile_rows(g);
-                const int T = (int)((rows + R - 1) / R);
-                float* ax = c->aux(w, G.stats_bn);
-                LAUNCH("bn_stats", 0.0, st,
-                       lpp::launch_stats_finalize(w.ps0, w.ps1, T, R, rows, Y.L.cout, w.v + B.poff,
-                                                  w.v + B.poff + Y.L.cout, M.desc.bn_eps, ax, ax + Y.L.cout,
-                                                  ax + 2 * Y.L.cout, ax + 3 * Y.L.cout, st));
-            }
+                                          G.stats_bn >= 0 ? c->acc_fwd(w, G.stats_bn) : nullptr, st));
             break;
         }
         case G_BNACT: {
@@ -544,14 +537,21 @@ int run_forward(lpp_ctx* c, Worker& w) {
                 int rc = bn_stats_standalone(c, w, G.bn2);
                 if (rc) return rc;
             }
-            const float* ax = c->aux(w, G.a);
-            const float* ax2 = G.bn2 >= 0 ? c->aux(w, G.bn2) : nullptr;
+            const Layer& B1 = M.layers[G.a];
+            const lpp::BnFwd b1{c->acc_fwd(w, G.a), w.v + B1.poff, w.v + B1.poff + C, M.desc.bn_eps, Mrows,
+                                c->aux(w, G.a)};
+            lpp::BnFwd b2{};
+            if (G.bn2 >= 0) {
+                const Layer& B2 = M.layers[G.bn2];
+                b2 = lpp::BnFwd{c->acc_fwd(w, G.bn2), w.v + B2.poff, w.v + B2.poff + C, M.desc.bn_eps, Mrows,
+                                c->aux(w, G.bn2)};
+            }
             const float* x2 = G.bn2 >= 0 ? c->act(w, M.layers[G.bn2].L.in0) : nullptr;
             const float* r = G.res >= 0 ? c->act(w, G.res) : nullptr;
             const double bytes = 8.0 * Mrows * C + (r || x2 ? 4.0 * Mrows * C : 0.0);
             LAUNCH("bn_act", bytes, st,
-                   lpp::launch_bn_act(x0, ax + 2 * C, ax + 3 * C, r, x2, ax2 ? ax2 + 2 * C : nullptr,
-                                      ax2 ? ax2 + 3 * C : nullptr, G.relu >= 0, c->act(w, G.out), Mrows, C, st));
+                   lpp::launch_bn_act(x0, b1, r, x2, G.bn2 >= 0 ? &b2 : nullptr, G.relu >= 0, c->act(w, G.out),
+                                      Mrows, C, st));
             break;
         }
         case G_RELU:
@@ -628,7 +628,7 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                     // column sums of dY, from per-tile means
                     const long Mo = (long)N * Y.out.h * Y.out.w;
                     LAUNCH("bias_grad", 4.0 * Mo * Y.L.cout, st,
-                           lpp::launch_stats_partial(dy, Mo, Y.L.cout, w.ps0, w.ps1, st));
+                           lpp::launch_stats_partial(dy, Mo, Y.L.cout, w.ps0, w.ps1, nullptr, st));
                     LAUNCH("bias_grad", 0.0, st,
                            lpp::launch_sum_from_tiles(w.ps0, lpp::stats_tiles(Mo), lpp::kStatRows, Mo, Y.L.cout,
                                                       w.g + Y.poff + Y.wcount, st));
@@ -639,7 +639,7 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                                 Y.L.pad};
                 LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
                        lpp::launch_conv_igemm(lpp::CONV_DGRAD, dy, w.wbuf + Y.wd_off, nullptr, dx0, g,
-                                              pl.acc0[G.a] != 0, nullptr, nullptr, st));
+                                              pl.acc0[G.a] != 0, nullptr, st));
             }
             break;
         }
@@ -660,29 +660,25 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
             lpp::BnBwdArgs a{dy, G.relu >= 0 ? c->act(w, G.out) : nullptr, x0, ax, ax + C,
                              want2 ? c->act(w, Y2->L.in0) : nullptr, want2 ? ax2 : nullptr,
                              want2 ? ax2 + C : nullptr, Min, C};
-            if (want1 || want2) {
-                const int T = lpp::stats_tiles(Min);
+            if (want1 || want2)
                 LAUNCH("bn_bwd", (a.mask ? 12.0 : 8.0) * Min * C + (want2 ? 4.0 * Min * C : 0.0), st,
-                       lpp::launch_bn_bwd_reduce(a, w.ps0, w.ps1, w.ps2, st));
-                float* gg1 = pl.wgrad[G.a] ? w.g + Y.poff : nullptr;
-                float* gb1 = pl.wgrad[G.a] ? w.g + Y.poff + C : nullptr;
-                float* gg2 = want2 && pl.wgrad[b2] ? w.g + Y2->poff : nullptr;
-                float* gb2 = want2 && pl.wgrad[b2] ? w.g + Y2->poff + C : nullptr;
-                LAUNCH("bn_bwd", 0.0, st,
-                       lpp::launch_bn_bwd_finalize(w.ps0, w.ps1, w.ps2, T, Min, C, w.v + Y.poff, ax + C, gg1, gb1,
-                                                   ax + 4 * C, want2 ? w.v + Y2->poff : nullptr,
-                                                   want2 ? ax2 + C : nullptr, gg2, gb2,
-                                                   want2 ? ax2 + 4 * C : nullptr, st));
-            }
+                       lpp::launch_bn_bwd_reduce(a, c->acc_bwd(w, G.a), st));
+            const lpp::BnBwdCoef k{want1 || want2 ? c->acc_bwd(w, G.a) : nullptr,
+                                   w.v + Y.poff,
+                                   pl.wgrad[G.a] ? w.g + Y.poff : nullptr,
+                                   pl.wgrad[G.a] ? w.g + Y.poff + C : nullptr,
+                                   want2 ? w.v + Y2->poff : nullptr,
+                                   want2 && pl.wgrad[b2] ? w.g + Y2->poff : nullptr,
+                                   want2 && pl.wgrad[b2] ? w.g + Y2->poff + C : nullptr};
             float* d1 = want1 && pl.din0[G.a] ? dx0 : nullptr;
             float* d2 = want2 && pl.din0[b2] ? c->dact(w, Y2->L.in0) : nullptr;
             float* dr = want_res ? c->dact(w, G.res) : nullptr;
-            if (d1 || d2 || dr) {
+            if (d1 || d2 || dr || want1 || want2) {
                 const double bytes = ((a.mask ? 8.0 : 4.0) + (d1 ? 12.0 : 0.0) + (d2 ? 12.0 : 0.0) +
                                       (dr ? (acc_res ? 8.0 : 4.0) : 0.0)) * Min * C;
                 LAUNCH("bn_bwd", bytes, st,
-                       lpp::launch_bn_bwd_apply(a, ax + 4 * C, want2 ? ax2 + 4 * C : nullptr, d1, pl.acc0[G.a] != 0,
-                                                d2, want2 && pl.acc0[b2] != 0, dr, acc_res, st));
+                       lpp::launch_bn_bwd_apply(a, k, d1, pl.acc0[G.a] != 0, d2, want2 && pl.acc0[b2] != 0, dr,
+                                                acc_res, st));
             }
             break;
         }
@@ -826,7 +822,8 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         Y.wd_off = wf;
         wf += (nd + 63) / 64 * 64;
         snaps.push_back({Y.poff, Y.np, Y.L.cout, Y.L.cin, Y.cin_p, Y.L.k, Y.L.k, Y.wf_off, Y.wd_off});
-        Y.wg = lpp::wgrad_plan(Y.L.cout, Y.L.k * Y.L.k * Y.cin_p, (long)N * Y.out.h * Y.out.w);
+        Y.wg = lpp::wgrad_plan(N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k,
+                               Y.L.stride, Y.L.pad);
     }
     c->wbuf_floats = wf;
     c->n_snap = (int)snaps.size();
@@ -856,16 +853,15 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         if (Y.L.op == LPP_BN) Y.aux = take(sizeof(float) * 7 * Y.out.c);
         if (Y.L.op == LPP_MAXPOOL) Y.aux = take((size_t)rows_out * Y.out.c);
         const long rin = (long)N * Y.in0.h * Y.in0.w;
-        if (Y.L.op == LPP_BN) ps = std::max<long>(ps, (long)lpp::stats_tiles(rin) * Y.out.c);
         if (Y.L.op == LPP_CONV) {
-            lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
-                            Y.L.pad};
-            const long tiles = (rows_out + lpp::conv_tile_rows(g) - 1) / lpp::conv_tile_rows(g);
-            ps = std::max<long>(ps, tiles * Y.L.cout);
             ps = std::max<long>(ps, (long)lpp::stats_tiles(rows_out) * Y.L.cout);
             wpart = std::max<long>(wpart, Y.wg.part_floats);
         }
     }
+    c->off_acc = off;
+    for (Layer& Y : M.layers)
+        if (Y.L.op == LPP_BN) Y.acc = take(sizeof(double) * 5 * lpp::kAccSlots * Y.out.c);
+    c->n_acc = (long)((off - c->off_acc) / sizeof(double));
     c->ps_floats = ps;
     c->off_ps = take(sizeof(float) * 3 * ps);
     c->off_wpart = take(sizeof(float) * wpart);
@@ -1114,17 +1110,18 @@ static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* 
         const int b = layer == G->bn2 ? G->bn2 : G->a;
         const float* ax = c->aux(w, b);
         const float* x = c->act(w, M.layers[b].L.in0);
-        const float *r = nullptr, *x2 = nullptr, *s2 = nullptr, *t2 = nullptr;
+        const float *r = nullptr, *x2 = nullptr;
+        lpp::BnFwd b2{};
         if (layer == G->add) {
             r = G->res >= 0 ? c->act(w, G->res) : nullptr;
             if (G->bn2 >= 0) {
-                const float* ax2 = c->aux(w, G->bn2);
+                b2.aux = c->aux(w, G->bn2);
                 x2 = c->act(w, M.layers[G->bn2].L.in0);
-                s2 = ax2 + 2 * C;
-                t2 = ax2 + 3 * C;
             }
         }
-        e = lpp::launch_bn_act(x, ax + 2 * C, ax + 3 * C, r, x2, s2, t2, false, tmp + n, rows, C, w.stream);
+        lpp::BnFwd b1{};
+        b1.aux = (float*)ax;
+        e = lpp::launch_bn_act(x, b1, r, x2, x2 ? &b2 : nullptr, false, tmp + n, rows, C, w.stream);
         src = tmp + n;
     } else if (!grad) {
         src = c->act(w, layer);
