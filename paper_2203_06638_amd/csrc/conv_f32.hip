@@ -461,17 +461,20 @@ static hipError_t launch_lds(const float* src, const float* B, const float* bias
 // 16) into LDS once, then runs every tap from LDS: the 3x3 halo is fetched
 // from memory once instead of once per tap.  The data gradient of a stride-1
 // conv is a forward conv of dY with the filter flipped and padding R-1-pad.
-struct TileGeom { int OH, IH, IW, pad_eff, tiles_per_img; };
+// IW_inv = ceil(2^32 / IW): pix / IW == umulhi(pix, IW_inv) for the pixel
+// counts of an LDS tile (pix * IW < 2^32).
+struct TileGeom { int OH, IH, IW, pad_eff, tiles_per_img; unsigned IW_inv; };
 
-template <int MODE, int WM, int TM, int TN, bool STATS>
+template <int MODE, int KS, int WM, int TM, int TN, bool STATS>
 __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                      const float* __restrict__ bias, float* __restrict__ Y,
                                                      ConvGeom g, TileGeom t, int accumulate, double* __restrict__ stats) {
     constexpr int WN = 4 / WM;
     constexpr int TP = WM * TM * 16, BN = WN * TN * 16;
     constexpr int LDW = 20;
+    constexpr int RS = KS * KS;
+    constexpr int NU = 8;                         // float4 loads in flight per thread
     extern __shared__ float lds[];
-    const int RS = g.R * g.S;
     float* Xs = lds;                              // [IH*IW][LDW]
     float* Ws = lds + t.IH * t.IW * LDW;          // [BN*RS][LDW]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -500,70 +503,101 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
+    // loader: element e = tid + 256 u has quad q = tid & 3 in both parts
+    const int q = tid & 3;
+    const int nx = t.IH * t.IW * 4, ntot = nx + BN * RS * 4;
     const int ngroups = g.Cs >> 4;
     for (int cgp = 0; cgp < ngroups; ++cgp) {
-        const int c0 = cgp * 16;
-        const int nx = t.IH * t.IW * 4;
-        lds_stage<8>(nx + BN * RS * 4, [&](int idx, const float*& sp, float*& dp) {
-            if (idx < nx) {
-                const int q = idx & 3, pix = idx >> 2;
-                const int ih = pix / t.IW, iw = pix - ih * t.IW;
-                const int h = h_org + ih, w = w_org + iw;
-                if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
-                    sp = src + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + c0 + q * 4;
-                dp = Xs + pix * LDW + q * 4;
-            } else {
-                const int e = idx - nx, q = e & 3, rest = e >> 2;
-                const int tap = rest % RS, nl = rest / RS;
-                const int n = n0 + nl;
-                const int stap = MODE == CONV_FWD ? tap : RS - 1 - tap;
-                if (n < g.Ncols) sp = B + ((long)n * RS + stap) * g.Cs + c0 + q * 4;
-                dp = Ws + rest * LDW + q * 4;
+        const int c0 = cgp * 16 + q * 4;
+        for (int base = tid; base < ntot; base += NU * 256) {
+            f4 v[NU];
+            int d[NU];
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const int e = base + u * 256;
+                const float* sp = nullptr;
+                d[u] = -1;
+                if (e < nx) {
+                    const int pix = e >> 2;
+                    const int ih = (int)__umulhi((unsigned)pix, t.IW_inv);
+                    const int iw = pix - ih * t.IW;
+                    const int h = h_org + ih, w = w_org + iw;
+                    if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
+                        sp = src + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + c0;
+                    d[u] = pix * LDW + q * 4;
+                } else if (e < ntot) {
+                    const int rest = (e - nx) >> 2;
+                    const int tap = rest % RS, nl = rest / RS;
+                    const int n = n0 + nl;
+                    const int stap = MODE == CONV_FWD ? tap : RS - 1 - tap;
+                    if (n < g.Ncols) sp = B + ((long)n * RS + stap) * g.Cs + c0;
+                    d[u] = t.IH * t.IW * LDW + rest * LDW + q * 4;
+                }
+                v[u] = sp ? *(const f4*)sp : f4{0.f, 0.f, 0.f, 0.f};
             }
-        });
+#pragma unroll
+            for (int u = 0; u < NU; ++u)
+                if (d[u] >= 0) *(f4*)(lds + d[u]) = v[u];
+        }
         __syncthreads();
-        for (int r = 0; r < g.R; ++r)
-            for (int sx = 0; sx < g.S; ++sx) {
-                const int toff = (r * t.IW + sx) * LDW;
-                const int tap = r * g.S + sx;
-                f4 a[TM], b[TN];
 #pragma unroll
-                for (int x = 0; x < TM; ++x) a[x] = *(const f4*)(Xs + abase[x] + toff);
+        for (int tap = 0; tap < RS; ++tap) {
+            const int toff = ((tap / KS) * t.IW + tap % KS) * LDW;
+            f4 a[TM], b[TN];
 #pragma unroll
-                for (int y = 0; y < TN; ++y)
-                    b[y] = *(const f4*)(Ws + (((wn * TN + y) * 16 + li) * RS + tap) * LDW + gi * 4);
+            for (int x = 0; x < TM; ++x) a[x] = *(const f4*)(Xs + abase[x] + toff);
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+            for (int y = 0; y < TN; ++y)
+                b[y] = *(const f4*)(Ws + (((wn * TN + y) * 16 + li) * RS + tap) * LDW + gi * 4);
 #pragma unroll
-                    for (int x = 0; x < TM; ++x)
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-                        for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(a[x][j], b[y][j], acc[x][y]);
-            }
+                for (int x = 0; x < TM; ++x)
+#pragma unroll
+                    for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(a[x][j], b[y][j], acc[x][y]);
+        }
         __syncthreads();
     }
 
     const long m0 = (long)blockIdx.x * TP;      // tiles are consecutive runs of the NHWC rows
     const int pix_base = wm * TM * 16;
     const int n_base = n0 + wn * TN * 16;
+    if (bias) {
 #pragma unroll
-    for (int y = 0; y < TN; ++y) {
-        const int n = n_base + y * 16 + li;
-        const float bb = (bias && n < g.Ncols) ? bias[n] : 0.f;
+        for (int y = 0; y < TN; ++y) {
+            const int n = n_base + y * 16 + li;
+            const float bb = n < g.Ncols ? bias[n] : 0.f;
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[x][y][i] += bb;
+        }
+    }
+    // the wave's TM*16 x TN*16 output block, transposed through LDS (the
+    // X/W tiles are dead) so that every lane stores whole float4 channel
+    // quads of one pixel
+    {
+        constexpr int OP = TN * 16 + 4;           // LDS pitch of a pixel row
+        float* Ot = lds + wave * (TM * 16 * OP);
 #pragma unroll
         for (int x = 0; x < TM; ++x)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) acc[x][y][i] += bb;
-        if (n >= g.Ncols) continue;
+            for (int y = 0; y < TN; ++y)
 #pragma unroll
-        for (int x = 0; x < TM; ++x)
+                for (int i = 0; i < 4; ++i) Ot[(x * 16 + gi * 4 + i) * OP + y * 16 + li] = acc[x][y][i];
+        __builtin_amdgcn_wave_barrier();          // a wave's LDS accesses execute in order
+        constexpr int QPP = TN * 4;               // float4 quads per pixel of the block
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int p = pix_base + x * 16 + gi * 4 + i;
-                if (p >= npix) continue;
-                const long o = (m0 + p) * g.Ncols + n;
-                const float v = acc[x][y][i];
-                Y[o] = accumulate ? Y[o] + v : v;
+        for (int k = 0; k < TM * 16 * QPP / 64; ++k) {
+            const int e = k * 64 + lane;
+            const int p = e / QPP, qd = e - (e / QPP) * QPP;
+            const int n = n_base + qd * 4;
+            if (n < g.Ncols) {
+                const f4 v = *(const f4*)(Ot + p * OP + qd * 4);
+                f4* o = (f4*)(Y + (m0 + pix_base + p) * g.Ncols + n);
+                *o = accumulate ? *o + v : v;
             }
+        }
     }
     if (STATS) {
         __shared__ float red[WM][BN];
@@ -574,8 +608,7 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
 #pragma unroll
             for (int x = 0; x < TM; ++x)
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (pix_base + x * 16 + gi * 4 + i < npix) sacc += acc[x][y][i];
+                for (int i = 0; i < 4; ++i) sacc += acc[x][y][i];
             sacc += __shfl_xor(sacc, 16);
             sacc += __shfl_xor(sacc, 32);
             if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = sacc;
@@ -590,18 +623,17 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
 #pragma unroll
         for (int y = 0; y < TN; ++y) {
             const float mu = tile_mean[wn * TN * 16 + y * 16 + li];
-            float q = 0.f;
+            float qs = 0.f;
 #pragma unroll
             for (int x = 0; x < TM; ++x)
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (pix_base + x * 16 + gi * 4 + i < npix) {
-                        const float dv = acc[x][y][i] - mu;
-                        q += dv * dv;
-                    }
-            q += __shfl_xor(q, 16);
-            q += __shfl_xor(q, 32);
-            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = q;
+                for (int i = 0; i < 4; ++i) {
+                    const float dv = acc[x][y][i] - mu;
+                    qs += dv * dv;
+                }
+            qs += __shfl_xor(qs, 16);
+            qs += __shfl_xor(qs, 32);
+            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = qs;
         }
         __syncthreads();
         if (threadIdx.x < BN) {
@@ -621,7 +653,8 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
 // false when no shape fits (the GEMM-style kernels take those passes).
 struct TileCfg { int wm, tm, tn; TileGeom t; size_t lds; };
 static bool pick_tile(int mode, const ConvGeom& g, TileCfg& out) {
-    if (g.Cs % 16 != 0) return false;
+    if (g.Cs % 16 != 0 || g.Ncols % 4 != 0) return false;
+    if (!((g.R == 3 && g.S == 3) || (g.R == 1 && g.S == 1))) return false;
     if (mode == CONV_DGRAD && g.stride != 1) return false;
     static const int cands[][3] = {
         // wm, tm, tn  (tile pixels = wm*tm*16, output channels = (4/wm)*tn*16)
@@ -638,36 +671,41 @@ static bool pick_tile(int mode, const ConvGeom& g, TileCfg& out) {
         if (oh < 1 || g.Ho % oh) continue;
         const int pad_eff = mode == CONV_FWD ? g.pad : g.R - 1 - g.pad;
         const int ih = (oh - 1) * g.stride + g.R, iw = (g.Wo - 1) * g.stride + g.S;
-        const size_t lds = sizeof(float) * 20 * ((size_t)ih * iw + (size_t)bn * g.R * g.S);
+        // staged X and W tiles; the epilogue's transpose reuses the space
+        const size_t lds = sizeof(float) * std::max<size_t>(20 * ((size_t)ih * iw + (size_t)bn * g.R * g.S),
+                                                            (size_t)4 * tm * 16 * (tn * 16 + 4));
         if (lds > 60 * 1024) continue;   // leaves room for the static statistics arrays
         const long tiles = M / tp;
         if (tiles * ((g.Ncols + bn - 1) / bn) < 128) continue;
-        out = {wm, tm, tn, {oh, ih, iw, pad_eff, g.Ho / oh}, lds};
+        const unsigned inv = (unsigned)((0x100000000ull + iw - 1) / iw);
+        out = {wm, tm, tn, {oh, ih, iw, pad_eff, g.Ho / oh, inv}, lds};
         return true;
     }
     return false;
 }
 
-template <int MODE, int WM, int TM, int TN>
+template <int MODE, int KS, int WM, int TM, int TN>
 static hipError_t launch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
                               const TileCfg& c, bool acc, double* stats, hipStream_t st) {
     constexpr int BN = (4 / WM) * TN * 16;
     dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
     if (stats)
-        hipLaunchKernelGGL((conv_tile_f32<MODE, WM, TM, TN, true>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
-                           c.t, (int)acc, stats);
+        hipLaunchKernelGGL((conv_tile_f32<MODE, KS, WM, TM, TN, true>), grid, dim3(256), c.lds, st, src, B, bias, Y,
+                           g, c.t, (int)acc, stats);
     else
-        hipLaunchKernelGGL((conv_tile_f32<MODE, WM, TM, TN, false>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
-                           c.t, (int)acc, stats);
+        hipLaunchKernelGGL((conv_tile_f32<MODE, KS, WM, TM, TN, false>), grid, dim3(256), c.lds, st, src, B, bias, Y,
+                           g, c.t, (int)acc, stats);
     return hipGetLastError();
 }
 
 template <int MODE>
 static hipError_t dispatch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
                                 const TileCfg& c, bool acc, double* stats, hipStream_t st) {
-#define TILE(WM_, TM_, TN_)                                                                          \
-    if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_)                                                   \
-        return launch_tile<MODE, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, st);
+#define TILE(WM_, TM_, TN_)                                                                                  \
+    if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) {                                                         \
+        if (g.R == 3) return launch_tile<MODE, 3, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, st);     \
+        return launch_tile<MODE, 1, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, st);                   \
+    }
     TILE(4, 4, 1) TILE(4, 2, 1) TILE(2, 4, 1) TILE(2, 2, 1) TILE(1, 4, 1) TILE(2, 2, 2) TILE(1, 4, 2)
     TILE(4, 1, 1) TILE(2, 1, 1) TILE(1, 2, 1) TILE(1, 1, 1)
 #undef TILE
