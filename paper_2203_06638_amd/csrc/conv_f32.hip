@@ -503,43 +503,34 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-    // loader: element e = tid + 256 u has quad q = tid & 3 in both parts
+    // loader: element e = tid + 256 u has quad q = tid & 3 in both parts.
+    // When a channel group fits one batch (ntot <= NU*256), the addresses
+    // are decoded once and the next group's loads -- the same addresses 16
+    // channels on -- are issued before this group's MFMAs.
     const int q = tid & 3;
     const int nx = t.IH * t.IW * 4, ntot = nx + BN * RS * 4;
     const int ngroups = g.Cs >> 4;
-    for (int cgp = 0; cgp < ngroups; ++cgp) {
-        const int c0 = cgp * 16 + q * 4;
-        for (int base = tid; base < ntot; base += NU * 256) {
-            f4 v[NU];
-            int d[NU];
-#pragma unroll
-            for (int u = 0; u < NU; ++u) {
-                const int e = base + u * 256;
-                const float* sp = nullptr;
-                d[u] = -1;
-                if (e < nx) {
-                    const int pix = e >> 2;
-                    const int ih = (int)__umulhi((unsigned)pix, t.IW_inv);
-                    const int iw = pix - ih * t.IW;
-                    const int h = h_org + ih, w = w_org + iw;
-                    if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
-                        sp = src + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + c0;
-                    d[u] = pix * LDW + q * 4;
-                } else if (e < ntot) {
-                    const int rest = (e - nx) >> 2;
-                    const int tap = rest % RS, nl = rest / RS;
-                    const int n = n0 + nl;
-                    const int stap = MODE == CONV_FWD ? tap : RS - 1 - tap;
-                    if (n < g.Ncols) sp = B + ((long)n * RS + stap) * g.Cs + c0;
-                    d[u] = t.IH * t.IW * LDW + rest * LDW + q * 4;
-                }
-                v[u] = sp ? *(const f4*)sp : f4{0.f, 0.f, 0.f, 0.f};
-            }
-#pragma unroll
-            for (int u = 0; u < NU; ++u)
-                if (d[u] >= 0) *(f4*)(lds + d[u]) = v[u];
+    auto decode = [&](int e, const float*& sp, int& d) {
+        sp = nullptr;
+        d = -1;
+        if (e < nx) {
+            const int pix = e >> 2;
+            const int ih = (int)__umulhi((unsigned)pix, t.IW_inv);
+            const int iw = pix - ih * t.IW;
+            const int h = h_org + ih, w = w_org + iw;
+            if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
+                sp = src + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + q * 4;
+            d = pix * LDW + q * 4;
+        } else if (e < ntot) {
+            const int rest = (e - nx) >> 2;
+            const int tap = rest % RS, nl = rest / RS;
+            const int n = n0 + nl;
+            const int stap = MODE == CONV_FWD ? tap : RS - 1 - tap;
+            if (n < g.Ncols) sp = B + ((long)n * RS + stap) * g.Cs + q * 4;
+            d = t.IH * t.IW * LDW + rest * LDW + q * 4;
         }
-        __syncthreads();
+    };
+    auto compute = [&]() {
 #pragma unroll
         for (int tap = 0; tap < RS; ++tap) {
             const int toff = ((tap / KS) * t.IW + tap % KS) * LDW;
@@ -556,7 +547,49 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
 #pragma unroll
                     for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(a[x][j], b[y][j], acc[x][y]);
         }
-        __syncthreads();
+    };
+    if (ntot <= NU * 256) {
+        const float* sp[NU];
+        int d[NU];
+        f4 v[NU];
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            decode(tid + u * 256, sp[u], d[u]);
+            v[u] = sp[u] ? *(const f4*)sp[u] : f4{0.f, 0.f, 0.f, 0.f};
+        }
+        for (int cgp = 0; cgp < ngroups; ++cgp) {
+#pragma unroll
+            for (int u = 0; u < NU; ++u)
+                if (d[u] >= 0) *(f4*)(lds + d[u]) = v[u];
+            __syncthreads();
+            if (cgp + 1 < ngroups) {
+                const int c1 = (cgp + 1) * 16;
+#pragma unroll
+                for (int u = 0; u < NU; ++u) v[u] = sp[u] ? *(const f4*)(sp[u] + c1) : f4{0.f, 0.f, 0.f, 0.f};
+            }
+            compute();
+            __syncthreads();
+        }
+    } else {
+        for (int cgp = 0; cgp < ngroups; ++cgp) {
+            const int c0 = cgp * 16;
+            for (int base = tid; base < ntot; base += NU * 256) {
+                f4 v[NU];
+                int d[NU];
+#pragma unroll
+                for (int u = 0; u < NU; ++u) {
+                    const float* sp;
+                    decode(base + u * 256, sp, d[u]);
+                    v[u] = sp ? *(const f4*)(sp + c0) : f4{0.f, 0.f, 0.f, 0.f};
+                }
+#pragma unroll
+                for (int u = 0; u < NU; ++u)
+                    if (d[u] >= 0) *(f4*)(lds + d[u]) = v[u];
+            }
+            __syncthreads();
+            compute();
+            __syncthreads();
+        }
     }
 
     const long m0 = (long)blockIdx.x * TP;      // tiles are consecutive runs of the NHWC rows
@@ -716,42 +749,33 @@ static hipError_t dispatch_tile(const float* src, const float* B, const float* b
 // (2i + a, 2j + b) only receives taps (r, s) with a + pad - r and b + pad - s
 // even, from dY[i + (a + pad - r)/2][j + (b + pad - s)/2]: per parity class
 // (a, b) this is a dense stride-1 correlation over dY with a subset of the
-// taps (for 3x3, pad 1: 1, 2, 2 and 4 taps).  A workgroup takes one class,
-// OH class rows of one image (TP = OH * Wc pixels) and BN input channels;
-// per group of 16 dY channels it stages the dY rows it reads and the class's
-// filter taps in LDS, then runs them all from LDS.  No MFMA is spent on the
-// taps that fall between strides.  Classes without taps write zeros (or leave
-// an accumulated dX as it is).
-struct S2Geom { int OH, IH, IW, Hc, Wc, tiles_per_img, dr0, ds0; };
+// taps (3x3, pad 1: 1, 2, 2 and 4 taps; 1x1, pad 0: one tap, class (0, 0)).
+// A workgroup takes OH class rows of one image for all four classes (a dX
+// tile of 2 OH rows), so every workgroup runs all R*S taps once and the dY
+// rows it reads are staged in LDS once per 16 dY channels; no MFMA is spent
+// on taps that fall between strides.  The finished tile is transposed
+// through LDS and stored as float4 channel quads.
+struct S2Geom { int OH, IH, IW, Hc, Wc, tiles_per_img, dr0, ds0; unsigned IW_inv; };
 
-template <int WM, int TM, int TN>
+template <int KS, int PAD, int WM, int TM, int TN>
 __global__ __launch_bounds__(256) void conv_dgrad_s2_f32(const float* __restrict__ dY, const float* __restrict__ B,
                                                          float* __restrict__ dX, ConvGeom g, S2Geom t,
                                                          int accumulate) {
     constexpr int WN = 4 / WM;
     constexpr int TP = WM * TM * 16, BN = WN * TN * 16;
     constexpr int LDW = 20;
+    constexpr int RS = KS * KS;
+    constexpr int NU = 8;
     extern __shared__ float lds[];
+    float* Xs = lds;                              // [IH*IW][LDW] dY rows
+    float* Ws = lds + t.IH * t.IW * LDW;          // [BN][RS][LDW]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WM, wn = wave / WM;
     const int gi = lane >> 4, li = lane & 15;
-    const int cls = blockIdx.z, ca = cls >> 1, cb = cls & 1;
     const int img = blockIdx.x / t.tiles_per_img;
     const int i0 = (blockIdx.x - img * t.tiles_per_img) * t.OH;
     const int n0 = blockIdx.y * BN;
-    const int RS = g.R * g.S;
-
-    // the class's taps (uniform over the workgroup), at most R*S <= 9
-    int tr[9], ts[9], nt = 0;
-    for (int r = 0; r < g.R; ++r)
-        for (int s = 0; s < g.S; ++s)
-            if (((ca + g.pad - r) & 1) == 0 && ((cb + g.pad - s) & 1) == 0 && nt < 9) {
-                tr[nt] = r;
-                ts[nt] = s;
-                ++nt;
-            }
-    float* Xs = lds;                              // [IH*IW][LDW] dY rows
-    float* Ws = lds + t.IH * t.IW * LDW;          // [BN][nt][LDW]
+    const int h_org = i0 + t.dr0, w_org = t.ds0;
 
     int abase[TM];
 #pragma unroll
@@ -760,73 +784,135 @@ __global__ __launch_bounds__(256) void conv_dgrad_s2_f32(const float* __restrict
         const int oh = p / t.Wc, ow = p - (p / t.Wc) * t.Wc;
         abase[x] = (oh * t.IW + ow) * LDW + gi * 4;
     }
-    f4 acc[TM][TN];
+    f4 acc[4][TM][TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int c = 0; c < 4; ++c)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[c][i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-    if (nt > 0) {
-        const int h_org = i0 + t.dr0, w_org = t.ds0;
-        for (int c0 = 0; c0 < g.Cs; c0 += 16) {
-            const int nx = t.IH * t.IW * 4;
-            lds_stage<8>(nx + BN * nt * 4, [&](int idx, const float*& sp, float*& dp) {
-                if (idx < nx) {
-                    const int q = idx & 3, pix = idx >> 2;
-                    const int ih = pix / t.IW, iw = pix - ih * t.IW;
-                    const int h = h_org + ih, w = w_org + iw;
-                    if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
-                        sp = dY + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + c0 + q * 4;
-                    dp = Xs + pix * LDW + q * 4;
-                } else {
-                    const int e = idx - nx, q = e & 3, rest = e >> 2;
-                    const int ti = rest % nt, nl = rest / nt;
-                    const int n = n0 + nl;
-                    if (n < g.Ncols) sp = B + ((long)n * RS + tr[ti] * g.S + ts[ti]) * g.Cs + c0 + q * 4;
-                    dp = Ws + rest * LDW + q * 4;
+    const int q = tid & 3;
+    const int nx = t.IH * t.IW * 4, ntot = nx + BN * RS * 4;
+    auto decode = [&](int e, const float*& sp, int& d) {
+        sp = nullptr;
+        d = -1;
+        if (e < nx) {
+            const int pix = e >> 2;
+            const int ih = (int)__umulhi((unsigned)pix, t.IW_inv);
+            const int iw = pix - ih * t.IW;
+            const int h = h_org + ih, w = w_org + iw;
+            if (h >= 0 && h < g.Hs && w >= 0 && w < g.Ws)
+                sp = dY + ((long)(img * g.Hs + h) * g.Ws + w) * g.Cs + q * 4;
+            d = pix * LDW + q * 4;
+        } else if (e < ntot) {
+            const int rest = (e - nx) >> 2;
+            const int tap = rest % RS, nl = rest / RS;
+            const int n = n0 + nl;
+            if (n < g.Ncols) sp = B + ((long)n * RS + tap) * g.Cs + q * 4;
+            d = t.IH * t.IW * LDW + rest * LDW + q * 4;
+        }
+    };
+    auto compute = [&]() {
+#pragma unroll
+        for (int cls = 0; cls < 4; ++cls) {
+            const int ca = cls >> 1, cb = cls & 1;
+#pragma unroll
+            for (int r = 0; r < KS; ++r)
+#pragma unroll
+                for (int sx = 0; sx < KS; ++sx) {
+                    if (((ca + PAD - r) & 1) || ((cb + PAD - sx) & 1)) continue;
+                    // source row i + (a + pad - r)/2, column j + (b + pad - s)/2
+                    const int dr = (ca + PAD - r) / 2 - t.dr0, ds = (cb + PAD - sx) / 2 - t.ds0;
+                    const int toff = (dr * t.IW + ds) * LDW;
+                    const int tap = r * KS + sx;
+                    f4 av[TM], bv[TN];
+#pragma unroll
+                    for (int x = 0; x < TM; ++x) av[x] = *(const f4*)(Xs + abase[x] + toff);
+#pragma unroll
+                    for (int y = 0; y < TN; ++y)
+                        bv[y] = *(const f4*)(Ws + (((wn * TN + y) * 16 + li) * RS + tap) * LDW + gi * 4);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+#pragma unroll
+                        for (int x = 0; x < TM; ++x)
+#pragma unroll
+                            for (int y = 0; y < TN; ++y)
+                                acc[cls][x][y] = mfma16x16x4(av[x][j], bv[y][j], acc[cls][x][y]);
                 }
-            });
+        }
+    };
+    const int ngroups = g.Cs >> 4;
+    if (ntot <= NU * 256) {
+        const float* sp[NU];
+        int d[NU];
+        f4 v[NU];
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            decode(tid + u * 256, sp[u], d[u]);
+            v[u] = sp[u] ? *(const f4*)sp[u] : f4{0.f, 0.f, 0.f, 0.f};
+        }
+        for (int cgp = 0; cgp < ngroups; ++cgp) {
+#pragma unroll
+            for (int u = 0; u < NU; ++u)
+                if (d[u] >= 0) *(f4*)(lds + d[u]) = v[u];
             __syncthreads();
-            for (int ti = 0; ti < nt; ++ti) {
-                // source row i + (a + pad - r)/2, column j + (b + pad - s)/2
-                const int dr = (ca + g.pad - tr[ti]) / 2 - t.dr0, ds = (cb + g.pad - ts[ti]) / 2 - t.ds0;
-                const int toff = (dr * t.IW + ds) * LDW;
-                f4 av[TM], bv[TN];
+            if (cgp + 1 < ngroups) {
+                const int c1 = (cgp + 1) * 16;
 #pragma unroll
-                for (int x = 0; x < TM; ++x) av[x] = *(const f4*)(Xs + abase[x] + toff);
-#pragma unroll
-                for (int y = 0; y < TN; ++y)
-                    bv[y] = *(const f4*)(Ws + (((wn * TN + y) * 16 + li) * nt + ti) * LDW + gi * 4);
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int x = 0; x < TM; ++x)
-#pragma unroll
-                        for (int y = 0; y < TN; ++y) acc[x][y] = mfma16x16x4(av[x][j], bv[y][j], acc[x][y]);
+                for (int u = 0; u < NU; ++u) v[u] = sp[u] ? *(const f4*)(sp[u] + c1) : f4{0.f, 0.f, 0.f, 0.f};
             }
+            compute();
             __syncthreads();
         }
-    } else if (accumulate) {
-        return;
+    } else {
+        for (int cgp = 0; cgp < ngroups; ++cgp) {
+            const int c0 = cgp * 16;
+            for (int base = tid; base < ntot; base += NU * 256) {
+                f4 v[NU];
+                int d[NU];
+#pragma unroll
+                for (int u = 0; u < NU; ++u) {
+                    const float* sp;
+                    decode(base + u * 256, sp, d[u]);
+                    v[u] = sp ? *(const f4*)(sp + c0) : f4{0.f, 0.f, 0.f, 0.f};
+                }
+#pragma unroll
+                for (int u = 0; u < NU; ++u)
+                    if (d[u] >= 0) *(f4*)(lds + d[u]) = v[u];
+            }
+            __syncthreads();
+            compute();
+            __syncthreads();
+        }
     }
 
-    const int pix_base = wm * TM * 16;
-    const int n_base = n0 + wn * TN * 16;
+    // the dX tile (2 OH rows x 2 Wc columns x BN channels) in LDS, pixel-major
+    constexpr int OP = BN + 4;
+    const int tw = 2 * t.Wc;
 #pragma unroll
-    for (int y = 0; y < TN; ++y) {
-        const int n = n_base + y * 16 + li;
-        if (n >= g.Ncols) continue;
+    for (int cls = 0; cls < 4; ++cls)
 #pragma unroll
         for (int x = 0; x < TM; ++x)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int p = pix_base + x * 16 + gi * 4 + i;
-                const int oh = p / t.Wc, ow = p - (p / t.Wc) * t.Wc;
-                const int h = 2 * (i0 + oh) + ca, w = 2 * ow + cb;
-                const long o = ((long)(img * g.Ho + h) * g.Wo + w) * g.Ncols + n;
-                const float v = acc[x][y][i];
-                dX[o] = accumulate ? dX[o] + v : v;
-            }
+            for (int y = 0; y < TN; ++y)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int p = (wm * TM + x) * 16 + gi * 4 + i;
+                    const int oh = p / t.Wc, ow = p - (p / t.Wc) * t.Wc;
+                    const int tp = (2 * oh + (cls >> 1)) * tw + 2 * ow + (cls & 1);
+                    lds[tp * OP + (wn * TN + y) * 16 + li] = acc[cls][x][y][i];
+                }
+    __syncthreads();
+    constexpr int QPP = BN / 4;
+    for (int e = tid; e < 4 * TP * QPP; e += 256) {
+        const int tp = e / QPP, qd = e - (e / QPP) * QPP;
+        const int n = n0 + qd * 4;
+        if (n >= g.Ncols) continue;
+        const int hr = tp / tw, wc = tp - (tp / tw) * tw;
+        const f4 v = *(const f4*)(lds + tp * OP + qd * 4);
+        f4* o = (f4*)(dX + ((long)(img * g.Ho + 2 * i0 + hr) * g.Wo + wc) * g.Ncols + n);
+        *o = accumulate ? *o + v : v;
     }
 }
 
@@ -834,54 +920,57 @@ __global__ __launch_bounds__(256) void conv_dgrad_s2_f32(const float* __restrict
 // does not apply.
 struct S2Cfg { int wm, tm, tn; S2Geom t; size_t lds; };
 static bool pick_s2(const ConvGeom& g, S2Cfg& out) {
-    if (g.stride != 2 || g.Cs % 16 || (g.Ho & 1) || (g.Wo & 1) || g.R > 3 || g.S > 3) return false;
+    if (g.stride != 2 || g.Cs % 16 || g.Ncols % 4 || (g.Ho & 1) || (g.Wo & 1)) return false;
+    if (!((g.R == 3 && g.S == 3 && g.pad == 1) || (g.R == 1 && g.S == 1 && g.pad == 0))) return false;
     const int Hc = g.Ho / 2, Wc = g.Wo / 2;
     // source offsets (a + pad - r)/2 over every class and tap
-    int dr0 = 1 << 20, dr1 = -(1 << 20), ds0 = 1 << 20, ds1 = -(1 << 20);
+    int dr0 = 1 << 20, dr1 = -(1 << 20);
     for (int a = 0; a < 2; ++a)
         for (int r = 0; r < g.R; ++r)
             if (((a + g.pad - r) & 1) == 0) {
                 dr0 = std::min(dr0, (a + g.pad - r) / 2);
                 dr1 = std::max(dr1, (a + g.pad - r) / 2);
             }
-    for (int b = 0; b < 2; ++b)
-        for (int s = 0; s < g.S; ++s)
-            if (((b + g.pad - s) & 1) == 0) {
-                ds0 = std::min(ds0, (b + g.pad - s) / 2);
-                ds1 = std::max(ds1, (b + g.pad - s) / 2);
-            }
-    if (dr0 > dr1 || ds0 > ds1) return false;
-    static const int cands[][3] = {{4, 4, 1}, {4, 2, 1}, {2, 2, 1}, {4, 1, 1}, {2, 1, 1}, {1, 2, 1}, {1, 1, 1}};
-    for (auto& c : cands) {
-        const int wm = c[0], tm = c[1], tn = c[2];
-        const int tp = wm * tm * 16, bn = (4 / wm) * tn * 16;
-        if (bn > 16 && g.Ncols <= bn / 2) continue;
-        if (tp % Wc) continue;
-        const int oh = tp / Wc;
-        if (oh < 1 || Hc % oh) continue;
-        const int ih = oh + dr1 - dr0, iw = Wc + ds1 - ds0;
-        const size_t lds = sizeof(float) * 20 * ((size_t)ih * iw + (size_t)bn * g.R * g.S);
-        if (lds > 60 * 1024) continue;
-        out = {wm, tm, tn, {oh, ih, iw, Hc, Wc, Hc / oh, dr0, ds0}, lds};
-        return true;
-    }
+    static const int cands[][3] = {{4, 4, 1}, {4, 2, 1}, {4, 1, 1}, {2, 2, 1}, {2, 1, 1}, {1, 1, 1}};
+    for (int pass = 0; pass < 2; ++pass)
+        for (auto& c : cands) {
+            const int wm = c[0], tm = c[1], tn = c[2];
+            const int tp = wm * tm * 16, bn = (4 / wm) * tn * 16;
+            if (bn > 16 && g.Ncols <= bn / 2) continue;
+            if (tp % Wc) continue;
+            const int oh = tp / Wc;
+            if (oh < 1 || Hc % oh) continue;
+            const long wgs = (long)g.Nb * (Hc / oh) * ((g.Ncols + bn - 1) / bn);
+            if (pass == 0 && wgs < 256) continue;     // first look for shapes that fill the chip
+            const int ih = oh + dr1 - dr0, iw = Wc + dr1 - dr0;
+            const size_t lds = sizeof(float) * std::max<size_t>(20 * ((size_t)ih * iw + (size_t)bn * g.R * g.S),
+                                                                (size_t)4 * tp * (bn + 4));
+            if (lds > 60 * 1024) continue;
+            const unsigned inv = (unsigned)((0x100000000ull + iw - 1) / iw);
+            out = {wm, tm, tn, {oh, ih, iw, Hc, Wc, Hc / oh, dr0, dr0, inv}, lds};
+            return true;
+        }
     return false;
 }
 
-template <int WM, int TM, int TN>
+template <int KS, int PAD, int WM, int TM, int TN>
 static hipError_t launch_s2(const float* dY, const float* B, float* dX, const ConvGeom& g, const S2Cfg& c, bool acc,
                             hipStream_t st) {
     constexpr int BN = (4 / WM) * TN * 16;
-    dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN), 4u);
-    hipLaunchKernelGGL((conv_dgrad_s2_f32<WM, TM, TN>), grid, dim3(256), c.lds, st, dY, B, dX, g, c.t, (int)acc);
+    dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
+    hipLaunchKernelGGL((conv_dgrad_s2_f32<KS, PAD, WM, TM, TN>), grid, dim3(256), c.lds, st, dY, B, dX, g, c.t,
+                       (int)acc);
     return hipGetLastError();
 }
 
 static hipError_t dispatch_s2(const float* dY, const float* B, float* dX, const ConvGeom& g, const S2Cfg& c, bool acc,
                               hipStream_t st) {
-#define S2(WM_, TM_, TN_) \
-    if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) return launch_s2<WM_, TM_, TN_>(dY, B, dX, g, c, acc, st);
-    S2(4, 4, 1) S2(4, 2, 1) S2(2, 2, 1) S2(4, 1, 1) S2(2, 1, 1) S2(1, 2, 1) S2(1, 1, 1)
+#define S2(WM_, TM_, TN_)                                                                              \
+    if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) {                                                   \
+        if (g.R == 3) return launch_s2<3, 1, WM_, TM_, TN_>(dY, B, dX, g, c, acc, st);                 \
+        return launch_s2<1, 0, WM_, TM_, TN_>(dY, B, dX, g, c, acc, st);                               \
+    }
+    S2(4, 4, 1) S2(4, 2, 1) S2(4, 1, 1) S2(2, 2, 1) S2(2, 1, 1) S2(1, 1, 1)
 #undef S2
     return hipErrorInvalidValue;
 }
