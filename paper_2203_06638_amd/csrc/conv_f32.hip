@@ -1200,13 +1200,15 @@ __global__ __launch_bounds__(256) void conv_wgrad_f32(const float* __restrict__ 
 // pixels p = 16 g + 4 gi + j.  Waves are summed in a fixed order and every
 // tile writes its own partial part[tile][co][(r, s, c)], summed in order by
 // the reduce kernel.
-struct WgTileGeom { int OH, IMGS, IH, IW, tiles_per_img, TP; };
+struct WgTileGeom { int OH, IMGS, IH, IW, tiles_per_img, TP; unsigned IW_inv, IHW_inv; };
 
 template <int RS, int NG, int ST, bool K1>
 __global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restrict__ dY, const float* __restrict__ X,
                                                            float* __restrict__ part, WgArgs a, WgTileGeom t) {
     constexpr int LDW = 20;
     constexpr int JST = (K1 ? 1 : ST) * LDW;   // LDS distance between a lane's four pixels
+    constexpr int TP = NG * 64;
+    constexpr int NU = 8;
     extern __shared__ float lds[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int gi = lane >> 4, li = lane & 15;
@@ -1215,12 +1217,50 @@ __global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restri
     const int img0 = t.IMGS == 1 ? tile / t.tiles_per_img : tile * t.IMGS;
     const int oh0 = t.IMGS == 1 ? (tile - img0 * t.tiles_per_img) * t.OH : 0;
     const int Ktot = RS * a.Cin_p;
-    const long m0 = (long)tile * t.TP;
+    const long m0 = (long)tile * TP;
     const int ohw = t.OH * a.Wo;
+    const int npix = t.IMGS * t.IH * t.IW;
+    float* Xs = lds;                         // [npix][LDW] input rows of the tile
+    float* Ds = lds + npix * LDW;            // [TP][LDW] dY of the tile, 16 channels
+
+    // stage X rows and the dY tile: element e = tid + 256 u has quad tid & 3
+    {
+        const int q = tid & 3;
+        const int nx = npix * 4, ntot = nx + TP * 4;
+        for (int base = tid; base < ntot; base += NU * 256) {
+            f4 v[NU];
+            int d[NU];
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const int e = base + u * 256;
+                const float* sp = nullptr;
+                d[u] = -1;
+                if (e < nx) {
+                    const int pix = e >> 2;
+                    const int il = (int)__umulhi((unsigned)pix, t.IHW_inv);
+                    const int rem = pix - il * (t.IH * t.IW);
+                    const int ih = (int)__umulhi((unsigned)rem, t.IW_inv);
+                    const int iw = rem - ih * t.IW;
+                    const int h = K1 ? (oh0 + ih) * ST : oh0 * ST - a.pad + ih;
+                    const int w = K1 ? iw * ST : iw - a.pad;
+                    if (h >= 0 && h < a.Hi && w >= 0 && w < a.Wi)
+                        sp = X + ((long)((img0 + il) * a.Hi + h) * a.Wi + w) * a.Cin_p + c0 + q * 4;
+                    d[u] = pix * LDW + q * 4;
+                } else if (e < ntot) {
+                    const int p = (e - nx) >> 2;
+                    sp = dY + (m0 + p) * a.Cout + co0 + q * 4;
+                    d[u] = (npix + p) * LDW + q * 4;
+                }
+                v[u] = sp ? *(const f4*)sp : f4{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int u = 0; u < NU; ++u)
+                if (d[u] >= 0) *(f4*)(lds + d[u]) = v[u];
+        }
+    }
 
     // this lane's pixels p = 16 (wave NG + g) + 4 gi + j: four consecutive
     // pixels of one output row (Wo % 4 == 0), so one LDS base per group
-    f4 av[NG];
     int boff[NG];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
@@ -1228,22 +1268,7 @@ __global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restri
         const int il = p / ohw, rem = p - il * ohw;
         const int ohl = rem / a.Wo, ow = rem - ohl * a.Wo;
         boff[g] = (K1 ? p : (il * t.IH + ohl * ST) * t.IW + ow * ST) * LDW + li;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) av[g][j] = dY[(m0 + p + j) * a.Cout + co0 + li];
     }
-
-    float* Xs = lds;
-    const int npix = t.IMGS * t.IH * t.IW;
-    lds_stage<8>(npix * 4, [&](int idx, const float*& sp, float*& dp) {
-        const int q = idx & 3, pix = idx >> 2;
-        const int il = pix / (t.IH * t.IW), rem = pix - il * (t.IH * t.IW);
-        const int ih = rem / t.IW, iw = rem - ih * t.IW;
-        const int h = K1 ? (oh0 + ih) * ST : oh0 * ST - a.pad + ih;
-        const int w = K1 ? iw * ST : iw - a.pad;
-        if (h >= 0 && h < a.Hi && w >= 0 && w < a.Wi)
-            sp = X + ((long)((img0 + il) * a.Hi + h) * a.Wi + w) * a.Cin_p + c0 + q * 4;
-        dp = Xs + pix * LDW + q * 4;
-    });
     int toff[RS];
 #pragma unroll
     for (int k = 0; k < RS; ++k) toff[k] = K1 ? 0 : ((k / 3) * t.IW + k % 3) * LDW;
@@ -1252,9 +1277,12 @@ __global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restri
     f4 acc[RS];
 #pragma unroll
     for (int k = 0; k < RS; ++k) acc[k] = f4{0.f, 0.f, 0.f, 0.f};
-    // per group: all RS x 4 operands are read before its MFMAs, the next
-    // group's reads are issued before this group's MFMAs
+    // per group: the four dY values and all RS x 4 X operands are read before
+    // its MFMAs, the next group's reads are issued before this group's MFMAs
     float bv[2][RS][4];
+    f4 av[2];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) av[0][j] = Ds[(wave * NG * 16 + gi * 4 + j) * LDW + li];
 #pragma unroll
     for (int k = 0; k < RS; ++k)
 #pragma unroll
@@ -1263,6 +1291,8 @@ __global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restri
     for (int g = 0; g < NG; ++g) {
         if (g + 1 < NG) {
 #pragma unroll
+            for (int j = 0; j < 4; ++j) av[(g + 1) & 1][j] = Ds[(((wave * NG + g + 1) * 16) + gi * 4 + j) * LDW + li];
+#pragma unroll
             for (int k = 0; k < RS; ++k)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) bv[(g + 1) & 1][k][j] = Xs[boff[g + 1] + toff[k] + j * JST];
@@ -1270,27 +1300,23 @@ __global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restri
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int k = 0; k < RS; ++k) acc[k] = mfma16x16x4(av[g][j], bv[g & 1][k][j], acc[k]);
+            for (int k = 0; k < RS; ++k) acc[k] = mfma16x16x4(av[g & 1][j], bv[g & 1][k][j], acc[k]);
     }
-    __syncthreads();   // the X tile is dead: its space takes the wave sums
+    __syncthreads();   // the staged tiles are dead: their space takes the wave sums
 
-    float* red = lds;   // [RS][16 co][16 c]
-    for (int w = 0; w < 4; ++w) {
-        if (wave == w) {
+    // each wave's RS x 16 x 16 block into its own LDS slice, then the four
+    // slices summed in order
+    float* red = lds;   // [4][RS][16 co][16 c]
 #pragma unroll
-            for (int k = 0; k < RS; ++k)
+    for (int k = 0; k < RS; ++k)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    float* slot = red + (k * 16 + gi * 4 + i) * 16 + li;
-                    *slot = w == 0 ? acc[k][i] : *slot + acc[k][i];
-                }
-        }
-        __syncthreads();
-    }
+        for (int i = 0; i < 4; ++i) red[((wave * RS + k) * 16 + gi * 4 + i) * 16 + li] = acc[k][i];
+    __syncthreads();
     float* out = part + (long)tile * a.Cout * Ktot;
     for (int e = tid; e < RS * 256; e += 256) {
         const int k = e >> 8, col = (e >> 4) & 15, c = e & 15;
-        out[(long)(co0 + col) * Ktot + k * a.Cin_p + c0 + c] = red[e];
+        const float v = ((red[e] + red[RS * 256 + e]) + red[2 * RS * 256 + e]) + red[3 * RS * 256 + e];
+        out[(long)(co0 + col) * Ktot + k * a.Cin_p + c0 + c] = v;
     }
 }
 
@@ -1315,9 +1341,11 @@ static bool pick_wgrad_tile(int Nb, int Hi, int Wi, int Cin_p, int Ho, int Wo, i
             if (Nb % imgs) continue;
         }
         const int ih = k1 ? oh : (oh - 1) * stride + R, iw = k1 ? Wo : (Wo - 1) * stride + S;
-        const size_t lds = sizeof(float) * std::max<size_t>((size_t)imgs * ih * iw * 20, (size_t)R * S * 256);
+        const size_t lds = sizeof(float) * std::max<size_t>(((size_t)imgs * ih * iw + tp) * 20, (size_t)4 * R * S * 256);
         if (lds > 60 * 1024) continue;
-        t = WgTileGeom{oh, imgs, ih, iw, imgs == 1 ? Ho / oh : 0, tp};
+        const unsigned iw_inv = (unsigned)((0x100000000ull + iw - 1) / iw);
+        const unsigned ihw_inv = (unsigned)((0x100000000ull + ih * iw - 1) / (ih * iw));
+        t = WgTileGeom{oh, imgs, ih, iw, imgs == 1 ? Ho / oh : 0, tp, iw_inv, ihw_inv};
         return true;
     }
     return false;
@@ -1369,7 +1397,7 @@ static hipError_t launch_wg_tile(const float* dY, const float* X, float* part, c
                                  hipStream_t st) {
     const long M = (long)a.Nb * a.Ho * a.Wo;
     dim3 grid((unsigned)(M / t.TP), (unsigned)(a.Cout / 16), (unsigned)(a.Cin_p / 16));
-    const size_t lds = sizeof(float) * std::max<size_t>((size_t)t.IMGS * t.IH * t.IW * 20, (size_t)RS * 256);
+    const size_t lds = sizeof(float) * std::max<size_t>(((size_t)t.IMGS * t.IH * t.IW + t.TP) * 20, (size_t)4 * RS * 256);
     hipLaunchKernelGGL((conv_wgrad_tile_f32<RS, NG, ST, K1>), grid, dim3(256), lds, st, dY, X, part, a, t);
     return hipGetLastError();
 }
