@@ -133,47 +133,51 @@ hipError_t launch_stats_partial(const float* x, long M, int C, float* pmean, flo
 //   y = act(x1*s1 + t1 [+ r | + x2*s2 + t2])
 // ------------------------------------------------------------------------
 
-// Workgroups derive the batch-norm coefficients into LDS first; each thread
-// then walks quads i, i + stride, ... whose channel advances by a fixed step.
-template <int RES, bool RELU>
+// Each thread takes E quads (i = blockIdx.x * 256 E + u * 256 + tid) and
+// issues their loads before the workgroup derives the batch-norm
+// coefficients into LDS, so the two latencies overlap.
+template <int RES, bool RELU, int E>
 __global__ __launch_bounds__(256) void bn_act_k(const f4* __restrict__ x1, BnFwd b1, const f4* __restrict__ r,
                                                 const f4* __restrict__ x2, BnFwd b2, f4* __restrict__ y, long n4,
                                                 int C) {
     extern __shared__ float co[];   // scale1 | shift1 | scale2 | shift2
+    const long i0 = (long)blockIdx.x * 256 * E + threadIdx.x;
+    f4 xa[E], xb[E];
+#pragma unroll
+    for (int u = 0; u < E; ++u) {
+        const long i = i0 + u * 256;
+        if (i < n4) {
+            xa[u] = x1[i];
+            if (RES == 1) xb[u] = r[i];
+            if (RES == 2) xb[u] = x2[i];
+        }
+    }
     bn_fwd_coeffs(b1, C, co, co + C);
     if (RES == 2) bn_fwd_coeffs(b2, C, co + 2 * C, co + 3 * C);
     __syncthreads();
     const int C4 = C >> 2;
-    const long stride = (long)gridDim.x * blockDim.x;
-    long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    int q = (int)(i % C4);
-    const int qstep = (int)(stride % C4);
-    for (; i < n4; i += stride) {
-        const int c = q * 4;
-        const f4 a = x1[i];
-        f4 o = a * *(const f4*)(co + c) + *(const f4*)(co + C + c);
-        if (RES == 1) o += r[i];
-        if (RES == 2) o += x2[i] * *(const f4*)(co + 2 * C + c) + *(const f4*)(co + 3 * C + c);
+#pragma unroll
+    for (int u = 0; u < E; ++u) {
+        const long i = i0 + u * 256;
+        if (i >= n4) continue;
+        const int c = (int)(i % C4) * 4;
+        f4 o = xa[u] * *(const f4*)(co + c) + *(const f4*)(co + C + c);
+        if (RES == 1) o += xb[u];
+        if (RES == 2) o += xb[u] * *(const f4*)(co + 2 * C + c) + *(const f4*)(co + 3 * C + c);
         if (RELU) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) o[k] = o[k] > 0.f ? o[k] : 0.f;
         }
         y[i] = o;
-        q += qstep;
-        if (q >= C4) q -= C4;
     }
 }
+
+// quads per thread of the batch-norm kernels: at most about 1024 workgroups
+static int bn_quads_per_thread(long n4) { return n4 > 256L * 1024 * 2 ? 4 : (n4 > 256L * 1024 ? 2 : 1); }
 
 static unsigned ew_grid(long n4) {
     long b = (n4 + 255) / 256;
     return (unsigned)(b < 8192 ? (b < 1 ? 1 : b) : 8192);
-}
-
-// batch-norm kernels: at most 1024 workgroups, so the coefficient prologue
-// is paid a bounded number of times
-static unsigned bn_grid(long n4) {
-    long b = (n4 + 255) / 256;
-    return (unsigned)(b < 1024 ? (b < 1 ? 1 : b) : 1024);
 }
 
 hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const float* x2, const BnFwd* b2,
@@ -184,12 +188,17 @@ hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const
     if (res == 2 && !b2) return hipErrorInvalidValue;
     const BnFwd bb = b2 ? *b2 : BnFwd{};
     const size_t lds = sizeof(float) * 4 * C;
-#define BNACT(RS, RL)                                                                                  \
-    hipLaunchKernelGGL((bn_act_k<RS, RL>), dim3(bn_grid(n4)), dim3(256), lds, st, (const f4*)x1, b1,   \
+    const int E = bn_quads_per_thread(n4);
+    const unsigned grid = (unsigned)((n4 + 256L * E - 1) / (256L * E));
+#define BNACT(RS, RL, EE)                                                                                \
+    hipLaunchKernelGGL((bn_act_k<RS, RL, EE>), dim3(grid), dim3(256), lds, st, (const f4*)x1, b1,        \
                        (const f4*)r, (const f4*)x2, bb, (f4*)y, n4, C)
-    if (res == 0) { if (relu) BNACT(0, true); else BNACT(0, false); }
-    else if (res == 1) { if (relu) BNACT(1, true); else BNACT(1, false); }
-    else { if (relu) BNACT(2, true); else BNACT(2, false); }
+#define BNACT_E(RS, RL) \
+    do { if (E == 4) BNACT(RS, RL, 4); else if (E == 2) BNACT(RS, RL, 2); else BNACT(RS, RL, 1); } while (0)
+    if (res == 0) { if (relu) BNACT_E(0, true); else BNACT_E(0, false); }
+    else if (res == 1) { if (relu) BNACT_E(1, true); else BNACT_E(1, false); }
+    else { if (relu) BNACT_E(2, true); else BNACT_E(2, false); }
+#undef BNACT_E
 #undef BNACT
     return hipGetLastError();
 }
@@ -201,6 +210,10 @@ hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const
 // dx = gamma*rstd*(g - mean(g) - xhat*mean(g*xhat)).
 // ------------------------------------------------------------------------
 
+// Per tile of kStatRows rows: threads form nq channel quads x rl row lanes;
+// each thread's rows are loaded four at a time before use, the row lanes
+// meet in a fixed-shape LDS tree, and lane 0 of each quad adds the tile's
+// sums to the accumulators.
 template <bool MASK, bool DUAL>
 __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, double* __restrict__ acc) {
     __shared__ f4 red[3][256];
@@ -214,38 +227,55 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, double* __re
         const int q = qbase + tid % nq, lr = tid / nq;
         f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0, s2 = s0;
         if (lr < rl) {
-            f4 m1, r1v, m2 = s0, r2v = s0;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                m1[k] = a.mean1[q * 4 + k];
-                r1v[k] = a.rstd1[q * 4 + k];
-                if (DUAL) { m2[k] = a.mean2[q * 4 + k]; r2v[k] = a.rstd2[q * 4 + k]; }
+            const f4 m1 = *(const f4*)(a.mean1 + q * 4), r1v = *(const f4*)(a.rstd1 + q * 4);
+            f4 m2 = s0, r2v = s0;
+            if (DUAL) {
+                m2 = *(const f4*)(a.mean2 + q * 4);
+                r2v = *(const f4*)(a.rstd2 + q * 4);
             }
-            for (long r = r0 + lr; r < r1; r += rl) {
-                const long o = r * C + q * 4;
-                f4 g = *(const f4*)(a.dy + o);
-                if (MASK) {
-                    const f4 y = *(const f4*)(a.mask + o);
+            for (long rb = r0 + lr; rb < r1; rb += 4L * rl) {
+                f4 gv[4], yv[4], xv[4], x2v[4];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) g[k] = y[k] > 0.f ? g[k] : 0.f;
+                for (int k = 0; k < 4; ++k) {
+                    const long r = rb + (long)k * rl;
+                    const long o = (r < r1 ? r : r0) * C + q * 4;
+                    gv[k] = *(const f4*)(a.dy + o);
+                    if (MASK) yv[k] = *(const f4*)(a.mask + o);
+                    xv[k] = *(const f4*)(a.x1 + o);
+                    if (DUAL) x2v[k] = *(const f4*)(a.x2 + o);
                 }
-                const f4 xh = (*(const f4*)(a.x1 + o) - m1) * r1v;
-                s0 += g;
-                s1 += g * xh;
-                if (DUAL) s2 += g * ((*(const f4*)(a.x2 + o) - m2) * r2v);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    if (rb + (long)k * rl >= r1) continue;
+                    f4 g = gv[k];
+                    if (MASK) {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) g[j] = yv[k][j] > 0.f ? g[j] : 0.f;
+                    }
+                    s0 += g;
+                    s1 += g * ((xv[k] - m1) * r1v);
+                    if (DUAL) s2 += g * ((x2v[k] - m2) * r2v);
+                }
             }
         }
         red[0][tid] = s0;
         red[1][tid] = s1;
         red[2][tid] = s2;
         __syncthreads();
-        if (tid < nq) {
-            f4 t0 = f4{0.f, 0.f, 0.f, 0.f}, t1 = t0, t2 = t0;
-            for (int l = 0; l < rl; ++l) {
-                t0 += red[0][l * nq + tid];
-                t1 += red[1][l * nq + tid];
-                t2 += red[2][l * nq + tid];
+        // fixed-shape tree over the rl row lanes (any rl): lanes [0, n - h) add lane + h
+        for (int n = rl; n > 1;) {
+            const int h = (n + 1) >> 1;
+            if (lr < n - h) {
+                const int o = (lr + h) * nq + (tid % nq);
+                red[0][tid] += red[0][o];
+                red[1][tid] += red[1][o];
+                if (DUAL) red[2][tid] += red[2][o];
             }
+            __syncthreads();
+            n = h;
+        }
+        if (tid < nq) {
+            const f4 t0 = red[0][tid], t1 = red[1][tid], t2 = red[2][tid];
             const int slot = blockIdx.x % kAccSlots;
             for (int k = 0; k < 4; ++k) {
                 const int c = (qbase + tid) * 4 + k;
@@ -258,16 +288,30 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, double* __re
     }
 }
 
-// Prologue: per channel a = gamma*rstd, mean g, mean g*xhat (and the second
+// Each thread takes E quads and issues their loads first; the prologue then
+// derives per channel a = gamma*rstd, mean g, mean g*xhat (and the second
 // set) from the accumulated sums, plus mean and rstd, into LDS; the first
 // workgroup stores dgamma and dbeta.
-template <bool MASK>
+template <bool MASK, int E>
 __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, float* __restrict__ dx1, int acc1,
                                                       float* __restrict__ dx2, int acc2, float* __restrict__ dres,
                                                       int accres) {
     extern __shared__ float cf[];   // a1 | mg | mgx1 | mean1 | rstd1 | a2 | mgx2 | mean2 | rstd2
     const int C = a.C;
     const bool dual = a.x2 != nullptr;
+    const long n4 = a.M * C / 4;
+    const long i0 = (long)blockIdx.x * 256 * E + threadIdx.x;
+    f4 gv[E], yv[E], x1v[E], x2v[E];
+#pragma unroll
+    for (int u = 0; u < E; ++u) {
+        const long i = i0 + u * 256;
+        if (i < n4) {
+            gv[u] = ((const f4*)a.dy)[i];
+            if (MASK) yv[u] = ((const f4*)a.mask)[i];
+            if (dx1) x1v[u] = ((const f4*)a.x1)[i];
+            if (dx2) x2v[u] = ((const f4*)a.x2)[i];
+        }
+    }
     if (k.acc) {
         for (int c = threadIdx.x; c < C; c += blockDim.x) {
             const double t0 = acc_read(k.acc, 0, C, c), t1 = acc_read(k.acc, 1, C, c);
@@ -294,35 +338,30 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, 
         }
     }
     __syncthreads();
-    const long n4 = a.M * C / 4;
     const int C4 = C >> 2;
-    const long stride = (long)gridDim.x * blockDim.x;
-    long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    int q = (int)(i % C4);
-    const int qstep = (int)(stride % C4);
-    for (; i < n4; i += stride) {
-        const int c = q * 4;
-        f4 g = ((const f4*)a.dy)[i];
-        if (MASK) {
-            const f4 yv = ((const f4*)a.mask)[i];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) g[j] = yv[j] > 0.f ? g[j] : 0.f;
+    for (int u = 0; u < E; ++u) {
+        const long i = i0 + u * 256;
+        if (i >= n4) continue;
+        const int c = (int)(i % C4) * 4;
+        f4 g = gv[u];
+        if (MASK) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) g[j] = yv[u][j] > 0.f ? g[j] : 0.f;
         }
         if (dx1) {
-            const f4 xh = (((const f4*)a.x1)[i] - *(const f4*)(cf + 3 * C + c)) * *(const f4*)(cf + 4 * C + c);
+            const f4 xh = (x1v[u] - *(const f4*)(cf + 3 * C + c)) * *(const f4*)(cf + 4 * C + c);
             const f4 v = *(const f4*)(cf + c) *
                          (g - *(const f4*)(cf + C + c) - xh * *(const f4*)(cf + 2 * C + c));
             ((f4*)dx1)[i] = acc1 ? ((f4*)dx1)[i] + v : v;
         }
         if (dx2) {
-            const f4 xh = (((const f4*)a.x2)[i] - *(const f4*)(cf + 7 * C + c)) * *(const f4*)(cf + 8 * C + c);
+            const f4 xh = (x2v[u] - *(const f4*)(cf + 7 * C + c)) * *(const f4*)(cf + 8 * C + c);
             const f4 v = *(const f4*)(cf + 5 * C + c) *
                          (g - *(const f4*)(cf + C + c) - xh * *(const f4*)(cf + 6 * C + c));
             ((f4*)dx2)[i] = acc2 ? ((f4*)dx2)[i] + v : v;
         }
         if (dres) ((f4*)dres)[i] = accres ? ((f4*)dres)[i] + g : g;
-        q += qstep;
-        if (q >= C4) q -= C4;
     }
 }
 
@@ -344,14 +383,19 @@ hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const BnBwdCoef& k, float* dx
     if (a.C % 4) return hipErrorInvalidValue;
     if ((dx1 || dx2) && !k.acc) return hipErrorInvalidValue;
     const long n4 = a.M * a.C / 4;
-    const unsigned grid = (dx1 || dx2 || dres) ? bn_grid(n4) : 1u;   // one workgroup: dgamma, dbeta only
+    const int E = bn_quads_per_thread(n4);
+    // one workgroup when only dgamma and dbeta are wanted
+    const unsigned grid = (dx1 || dx2 || dres) ? (unsigned)((n4 + 256L * E - 1) / (256L * E)) : 1u;
     const size_t lds = sizeof(float) * 9 * a.C;
-    if (a.mask)
-        hipLaunchKernelGGL((bn_bwd_apply_k<true>), dim3(grid), dim3(256), lds, st, a, k, dx1, (int)acc1, dx2,
-                           (int)acc2, dres, (int)accres);
-    else
-        hipLaunchKernelGGL((bn_bwd_apply_k<false>), dim3(grid), dim3(256), lds, st, a, k, dx1, (int)acc1, dx2,
-                           (int)acc2, dres, (int)accres);
+#define BNBA(MK, EE)                                                                                         \
+    hipLaunchKernelGGL((bn_bwd_apply_k<MK, EE>), dim3(grid), dim3(256), lds, st, a, k, dx1, (int)acc1, dx2, \
+                       (int)acc2, dres, (int)accres)
+#define BNBA_E(MK) \
+    do { if (E == 4) BNBA(MK, 4); else if (E == 2) BNBA(MK, 2); else BNBA(MK, 1); } while (0)
+    if (a.mask) BNBA_E(true);
+    else BNBA_E(false);
+#undef BNBA_E
+#undef BNBA
     return hipGetLastError();
 }
 
