@@ -199,11 +199,15 @@ def main():
     dt = time.perf_counter() - t0
     issue_ms = issue[0] / a.steps * 1e3
     pos += a.steps
-    # roofline pass: the same steps again with every launch of the dominant
-    # family bracketed by HIP events on its own stream
-    rsteps = min(a.steps, 1000)
+    # roofline pass: worker 0 alone on its stream, partitions cycling, every
+    # launch of the dominant family bracketed by HIP events on that stream
+    # (with the other streams idle the events time the kernel itself)
+    rsteps = min(a.steps, 400)
+    ctx.sync()
     ctx.timer_enable(dom)
-    run(rsteps, pos)
+    for s in range(rsteps):
+        img, lab = pool[s % len(pool)]
+        ctx.step(0, img, lab, s % P + 1, 0.1)
     ms, launches, work = ctx.timer_read()
     ctx.timer_enable(None)
     losses = [ctx.get_loss(w) for w in range(K * P)]
@@ -237,8 +241,8 @@ def main():
         "roofline": {"kernel": dom, "bound": "mfma" if mfma else "hbm", "achieved": round(achieved, 2),
                      "peak": peak, "unit": "TFLOP/s" if mfma else "GB/s", "frac": round(achieved / peak, 4),
                      "traffic": None, "launches": launches, "avg_launch_us": round(ms / launches * 1e3, 2),
-                     "timed": "HIP events around each launch of the family, on its stream, over %d steps run "
-                              "right after the timed region (kernels launched one by one)" % rsteps,
+                     "timed": "HIP events around each launch of the family on worker 0's stream, %d steps of "
+                              "worker 0 alone (partitions 1..4 in turn) right after the timed region" % rsteps,
                      "family_ms_probe": {k: round(v, 3) for k, v in sorted(fam_time.items(), key=lambda t: -t[1])}},
         "final_losses": [round(l, 4) for l in losses],
     }

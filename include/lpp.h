@@ -65,6 +65,11 @@ enum lpp_op {
 };
 
 enum lpp_dtype { LPP_FP32 = 0, LPP_BF16 = 1 };
+/* Sequential: lpp_step and lpp_average wait for their work; batch-norm sums
+ * are merged across workgroups in a fixed order, so repeated runs are
+ * bitwise identical.  Async: calls return at once (Alg. 1's lock-free
+ * updaters); batch-norm sums are merged by fp64 atomic adds, whose order
+ * varies, so runs agree to rounding but not bit for bit. */
 enum lpp_mode { LPP_SEQUENTIAL = 0, LPP_ASYNC = 1 };
 
 typedef struct {

@@ -92,7 +92,7 @@ __device__ __forceinline__ int src_pixel(int n, int p, int q, int r, int s, cons
 template <int MODE, int WM, int TM, int TN, bool FAST, bool STATS>
 __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                       const float* __restrict__ bias, float* __restrict__ Y,
-                                                      ConvGeom g, int accumulate, double* __restrict__ stats) {
+                                                      ConvGeom g, int accumulate, BnSums sums) {
     constexpr int WN = 4 / WM;
     constexpr int BM = WM * TM * 16, BN = WN * TN * 16;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -254,9 +254,14 @@ __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ 
             if (n < g.Ncols) {
                 float t = 0.f;
                 for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
-                const double mu = tile_mean[threadIdx.x], nr = (double)rows;
-                acc_add(stats, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
-                acc_add(stats, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)t + nr * mu * mu);
+                if (sums.acc) {
+                    const double mu = tile_mean[threadIdx.x], nr = (double)rows;
+                    acc_add(sums.acc, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
+                    acc_add(sums.acc, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)t + nr * mu * mu);
+                } else {
+                    sums.p0[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
+                    sums.p1[(long)blockIdx.x * g.Ncols + n] = t;
+                }
             }
         }
     }
@@ -272,7 +277,7 @@ __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ 
 template <int MODE, int BM, int BN, int WM, bool STATS>
 __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                     const float* __restrict__ bias, float* __restrict__ Y,
-                                                    ConvGeom g, int accumulate, double* __restrict__ stats) {
+                                                    ConvGeom g, int accumulate, BnSums sums) {
     constexpr int WN = 4 / WM;
     constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
     constexpr int LDW = 20;                                  // 16 floats + 4 pad per LDS row
@@ -431,9 +436,14 @@ __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ sr
             if (n < g.Ncols) {
                 float t = 0.f;
                 for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
-                const double mu = tile_mean[threadIdx.x], nr = (double)rows;
-                acc_add(stats, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
-                acc_add(stats, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)t + nr * mu * mu);
+                if (sums.acc) {
+                    const double mu = tile_mean[threadIdx.x], nr = (double)rows;
+                    acc_add(sums.acc, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
+                    acc_add(sums.acc, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)t + nr * mu * mu);
+                } else {
+                    sums.p0[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
+                    sums.p1[(long)blockIdx.x * g.Ncols + n] = t;
+                }
             }
         }
     }
@@ -441,15 +451,15 @@ __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ sr
 
 template <int MODE, int BM, int BN, int WM>
 static hipError_t launch_lds(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                             bool acc, double* stats, hipStream_t st) {
+                             bool acc, const BnSums* stats, hipStream_t st) {
     const long M = (long)g.Nb * g.Ho * g.Wo;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
     if (stats)
         hipLaunchKernelGGL((conv_lds_f32<MODE, BM, BN, WM, true>), grid, dim3(256), 0, st, src, B, bias, Y, g,
-                           (int)acc, stats);
+                           (int)acc, stats ? *stats : BnSums{});
     else
         hipLaunchKernelGGL((conv_lds_f32<MODE, BM, BN, WM, false>), grid, dim3(256), 0, st, src, B, bias, Y, g,
-                           (int)acc, stats);
+                           (int)acc, stats ? *stats : BnSums{});
     return hipGetLastError();
 }
 
@@ -468,7 +478,7 @@ struct TileGeom { int OH, IH, IW, pad_eff, tiles_per_img; unsigned IW_inv; };
 template <int MODE, int KS, int WM, int TM, int TN, bool STATS>
 __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                      const float* __restrict__ bias, float* __restrict__ Y,
-                                                     ConvGeom g, TileGeom t, int accumulate, double* __restrict__ stats) {
+                                                     ConvGeom g, TileGeom t, int accumulate, BnSums sums) {
     constexpr int WN = 4 / WM;
     constexpr int TP = WM * TM * 16, BN = WN * TN * 16;
     constexpr int LDW = 20;
@@ -674,9 +684,14 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
             if (n < g.Ncols) {
                 float tt = 0.f;
                 for (int w = 0; w < WM; ++w) tt += red[w][threadIdx.x];
-                const double mu = tile_mean[threadIdx.x], nr = (double)npix;
-                acc_add(stats, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
-                acc_add(stats, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)tt + nr * mu * mu);
+                if (sums.acc) {
+                    const double mu = tile_mean[threadIdx.x], nr = (double)npix;
+                    acc_add(sums.acc, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
+                    acc_add(sums.acc, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)tt + nr * mu * mu);
+                } else {
+                    sums.p0[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
+                    sums.p1[(long)blockIdx.x * g.Ncols + n] = tt;
+                }
             }
         }
     }
@@ -719,21 +734,21 @@ static bool pick_tile(int mode, const ConvGeom& g, TileCfg& out) {
 
 template <int MODE, int KS, int WM, int TM, int TN>
 static hipError_t launch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              const TileCfg& c, bool acc, double* stats, hipStream_t st) {
+                              const TileCfg& c, bool acc, const BnSums* stats, hipStream_t st) {
     constexpr int BN = (4 / WM) * TN * 16;
     dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
     if (stats)
         hipLaunchKernelGGL((conv_tile_f32<MODE, KS, WM, TM, TN, true>), grid, dim3(256), c.lds, st, src, B, bias, Y,
-                           g, c.t, (int)acc, stats);
+                           g, c.t, (int)acc, stats ? *stats : BnSums{});
     else
         hipLaunchKernelGGL((conv_tile_f32<MODE, KS, WM, TM, TN, false>), grid, dim3(256), c.lds, st, src, B, bias, Y,
-                           g, c.t, (int)acc, stats);
+                           g, c.t, (int)acc, stats ? *stats : BnSums{});
     return hipGetLastError();
 }
 
 template <int MODE>
 static hipError_t dispatch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                                const TileCfg& c, bool acc, double* stats, hipStream_t st) {
+                                const TileCfg& c, bool acc, const BnSums* stats, hipStream_t st) {
 #define TILE(WM_, TM_, TN_)                                                                                  \
     if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) {                                                         \
         if (g.R == 3) return launch_tile<MODE, 3, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, st);     \
@@ -977,7 +992,7 @@ static hipError_t dispatch_s2(const float* dY, const float* B, float* dX, const 
 
 template <int MODE, int WM, int TM, int TN>
 static hipError_t launch_cfg(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                             bool acc, double* stats, hipStream_t st) {
+                             bool acc, const BnSums* stats, hipStream_t st) {
     constexpr int BM = WM * TM * 16, BN = (4 / WM) * TN * 16;
     const long M = (long)g.Nb * g.Ho * g.Wo;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
@@ -985,17 +1000,17 @@ static hipError_t launch_cfg(const float* src, const float* B, const float* bias
     if (stats) {
         if (fast)
             hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true, true>), grid, dim3(256), 0, st, src, B, bias,
-                               Y, g, (int)acc, stats);
+                               Y, g, (int)acc, stats ? *stats : BnSums{});
         else
             hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false, true>), grid, dim3(256), 0, st, src, B, bias,
-                               Y, g, (int)acc, stats);
+                               Y, g, (int)acc, stats ? *stats : BnSums{});
     } else {
         if (fast)
             hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true, false>), grid, dim3(256), 0, st, src, B, bias,
-                               Y, g, (int)acc, stats);
+                               Y, g, (int)acc, stats ? *stats : BnSums{});
         else
             hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false, false>), grid, dim3(256), 0, st, src, B, bias,
-                               Y, g, (int)acc, stats);
+                               Y, g, (int)acc, stats ? *stats : BnSums{});
     }
     return hipGetLastError();
 }
@@ -1022,7 +1037,7 @@ static ConvCfg pick_cfg(const ConvGeom& g) {
 
 template <int MODE>
 static hipError_t launch_mode(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              bool acc, double* stats, hipStream_t st) {
+                              bool acc, const BnSums* stats, hipStream_t st) {
     TileCfg tc;
     if (pick_tile(MODE, g, tc)) return dispatch_tile<MODE>(src, B, bias, Y, g, tc, acc, stats, st);
     if (MODE == CONV_DGRAD) {
@@ -1052,8 +1067,14 @@ static hipError_t launch_mode(const float* src, const float* B, const float* bia
     return launch_cfg<MODE, 2, 1, 2>(src, B, bias, Y, g, acc, stats, st);
 }
 
+int conv_tile_rows(const ConvGeom& g) {
+    TileCfg t;
+    if (pick_tile(CONV_FWD, g, t)) return t.wm * t.tm * 16;
+    return pick_cfg(g).bm;
+}
+
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, double* stats, hipStream_t st) {
+                             const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st) {
     if (mode == CONV_FWD) return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, stats, st);
     return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, nullptr, st);
 }

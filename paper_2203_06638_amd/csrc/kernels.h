@@ -28,17 +28,28 @@ struct StepArgs {
 };
 hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* labels, float lr, hipStream_t st);
 
-// Batch-norm reductions are merged across workgroups by fp64 atomic adds
-// into per-channel accumulators acc[q][kAccSlots][C] (q selects the sum);
-// see bnacc.h.  The first kernel of a step zeroes them.
+// Where a batch-norm reduction goes.  With acc set, every workgroup adds its
+// tile's sums into per-channel fp64 accumulators acc[q][kAccSlots][C] (q
+// selects the sum; bnacc.h), merged across workgroups in arrival order; the
+// first kernel of a step zeroes them.  Otherwise tile t writes its partials
+// to p0..p2 [T][C] and a finalize kernel merges them in a fixed order, so the
+// result is bitwise reproducible.
 constexpr int kAccSlots = 32;
+struct BnSums {
+    double* acc;
+    float* p0;
+    float* p1;
+    float* p2;
+};
 
 // Y[m][n] (+)= sum_k A[m][k] B[n][k] (+ bias[n]); see ConvGeom.  Forward
-// passes with stats non-null also add the batch sums of Y (q = 0: sum y,
-// q = 1: sum y^2, per output channel; each row tile's share is formed from
-// its mean and sum of squared deviations) into stats [2][kAccSlots][Ncols].
+// passes with stats non-null also produce the batch-norm sums of Y: into
+// acc, q = 0: sum y and q = 1: sum y^2 (each row tile's share formed from its
+// mean and sum of squared deviations); as partials, the tile mean (p0) and
+// sum of squared deviations (p1), T = ceil(M / conv_tile_rows(g)) tiles.
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, double* stats, hipStream_t st);
+                             const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st);
+int conv_tile_rows(const ConvGeom& g);
 
 // Weight gradient: part[split][Cout][Ktot] = partial sums over pixel ranges
 // of dY[p][cout] * im2col(X)[p][(r,s,c)].  wgrad_plan chooses the kernel:
@@ -58,10 +69,14 @@ hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot
 constexpr int kStatRows = 256;   // rows per tile of the stand-alone kernels
 int stats_tiles(long M);
 // per tile of kStatRows rows: mean and sum of squared deviations per channel
-// into pmean / pm2 [T][C] (acc null), or the tile's share of the batch sums
-// added into acc [2][kAccSlots][C] (sum x, sum x^2)
-hipError_t launch_stats_partial(const float* x, long M, int C, float* pmean, float* pm2, double* acc,
-                                hipStream_t st);
+// into p0 / p1 [T][C], or the tile's share of the batch sums added into
+// acc [2][kAccSlots][C] (sum x, sum x^2)
+hipError_t launch_stats_partial(const float* x, long M, int C, const BnSums& out, hipStream_t st);
+// merges T tiles of R rows (fp64, fixed order) into aux = [mean | rstd |
+// scale | shift]: rstd = 1/sqrt(var + eps) with the biased variance,
+// scale = gamma*rstd, shift = beta - mean*scale
+hipError_t launch_stats_finalize(const float* pmean, const float* pm2, int T, int R, long M, int C,
+                                 const float* gamma, const float* beta, float eps, float* aux, hipStream_t st);
 // out[c] = sum_t rows_t * pmean[t][c]: column sums from tile means
 hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C, float* out, hipStream_t st);
 // A training-mode batch norm as the per-channel map x*scale + shift.  With
@@ -93,17 +108,26 @@ struct BnBwdArgs {
     int C;
 };
 // per tile of kStatRows rows, the tile's sum g, sum g*xhat1 and sum g*xhat2
-// added into acc [3][kAccSlots][C]
-hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, double* acc, hipStream_t st);
-// Coefficients of the backward apply, derived in its prologue from the sums
-// acc [3][kAccSlots][C]: per batch norm a = gamma*rstd, mean g and mean
-// g*xhat; its first workgroup also stores dgamma = sum g*xhat and dbeta =
-// sum g (null pointers: not wanted).  acc null: no batch-norm input gradient
-// is formed (only dres).
+// added into acc [3][kAccSlots][C], or written to p0..p2 [T][C]
+hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, const BnSums& out, hipStream_t st);
+// fixed-order merge of T tile partials: gg/gb (dgamma, dbeta; null = not
+// wanted) and coef = [gamma*rstd | mean g | mean g*xhat] per channel; the
+// second set for a dual group (coef2 null if not)
+hipError_t launch_bn_bwd_finalize(const float* p0, const float* p1, const float* p2, int T, long M, int C,
+                                  const float* gamma1, const float* rstd1, float* gg1, float* gb1, float* coef1,
+                                  const float* gamma2, const float* rstd2, float* gg2, float* gb2, float* coef2,
+                                  hipStream_t st);
+// Coefficients of the backward apply.  With acc set they are derived in its
+// prologue from the sums acc [3][kAccSlots][C]: per batch norm a =
+// gamma*rstd, mean g and mean g*xhat, and its first workgroup also stores
+// dgamma = sum g*xhat and dbeta = sum g (null pointers: not wanted).
+// Otherwise they are read from coef1 / coef2 (written by the finalize).
+// Neither: no batch-norm input gradient is formed (only dres).
 struct BnBwdCoef {
     const double* acc;
     const float* gamma1; float* gg1; float* gb1;
     const float* gamma2; float* gg2; float* gb2;
+    const float* coef1; const float* coef2;
 };
 // dx = a*(g - mean g - xhat*mean g*xhat) into dx1 / dx2 (null = skip), and g
 // into dres (the residual branch) -- each written or accumulated

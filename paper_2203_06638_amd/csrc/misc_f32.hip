@@ -30,9 +30,7 @@ __device__ __forceinline__ void quad_layout(int C4, int qbase, int& nq, int& rl)
     rl = 256 / nq;
 }
 
-__global__ __launch_bounds__(256) void stats_partial_k(const float* __restrict__ x, long M, int C,
-                                                       float* __restrict__ pmean, float* __restrict__ pm2,
-                                                       double* __restrict__ acc) {
+__global__ __launch_bounds__(256) void stats_partial_k(const float* __restrict__ x, long M, int C, BnSums out) {
     __shared__ f4 red[256];
     __shared__ float mean_s[1024];
     const int tid = threadIdx.x;
@@ -74,13 +72,13 @@ __global__ __launch_bounds__(256) void stats_partial_k(const float* __restrict__
             for (int k = 0; k < 4; ++k) {
                 const int c = (qbase + tid) * 4 + k;
                 const float mu = mean_s[(tid * 4 + k) & 1023];
-                if (acc) {
+                if (out.acc) {
                     const double n = (double)rows, m = (double)mu;
-                    acc_add(acc, 0, blockIdx.x % kAccSlots, C, c, m * n);
-                    acc_add(acc, 1, blockIdx.x % kAccSlots, C, c, (double)t[k] + n * m * m);
+                    acc_add(out.acc, 0, blockIdx.x % kAccSlots, C, c, m * n);
+                    acc_add(out.acc, 1, blockIdx.x % kAccSlots, C, c, (double)t[k] + n * m * m);
                 } else {
-                    pmean[(long)blockIdx.x * C + c] = mu;
-                    pm2[(long)blockIdx.x * C + c] = t[k];
+                    out.p0[(long)blockIdx.x * C + c] = mu;
+                    out.p1[(long)blockIdx.x * C + c] = t[k];
                 }
             }
         }
@@ -121,9 +119,44 @@ hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C
     return hipGetLastError();
 }
 
-hipError_t launch_stats_partial(const float* x, long M, int C, float* pmean, float* pm2, double* acc,
-                                hipStream_t st) {
-    hipLaunchKernelGGL(stats_partial_k, dim3(stats_tiles(M)), dim3(256), 0, st, x, M, C, pmean, pm2, acc);
+hipError_t launch_stats_partial(const float* x, long M, int C, const BnSums& out, hipStream_t st) {
+    hipLaunchKernelGGL(stats_partial_k, dim3(stats_tiles(M)), dim3(256), 0, st, x, M, C, out);
+    return hipGetLastError();
+}
+
+// One workgroup per channel: thread j takes tiles j, j + 256, ... and the
+// partial sums meet in the fixed tree.  mean = sum n_t m_t / M,
+// M2 = sum (M2_t + n_t (m_t - mean)^2).
+__global__ __launch_bounds__(256) void stats_finalize_k(const float* __restrict__ pmean, const float* __restrict__ pm2,
+                                                        int T, int R, long M, int C, const float* __restrict__ gamma,
+                                                        const float* __restrict__ beta, float eps, float* aux) {
+    __shared__ double red[256];
+    const int c = blockIdx.x;
+    double s = 0.0;
+#pragma unroll 4
+    for (int t = threadIdx.x; t < T; t += 256)
+        s += (double)min((long)R, M - (long)t * R) * (double)pmean[(long)t * C + c];
+    const double mu = tree_sum256(s, red) / (double)M;
+    double q = 0.0;
+#pragma unroll 4
+    for (int t = threadIdx.x; t < T; t += 256) {
+        const double d = (double)pmean[(long)t * C + c] - mu;
+        q += (double)pm2[(long)t * C + c] + (double)min((long)R, M - (long)t * R) * d * d;
+    }
+    q = tree_sum256(q, red);
+    if (threadIdx.x == 0) {
+        const double r = 1.0 / sqrt(q / (double)M + (double)eps);
+        const double sc = (double)gamma[c] * r;
+        aux[c] = (float)mu;
+        aux[C + c] = (float)r;
+        aux[2 * C + c] = (float)sc;
+        aux[3 * C + c] = (float)((double)beta[c] - mu * sc);
+    }
+}
+
+hipError_t launch_stats_finalize(const float* pmean, const float* pm2, int T, int R, long M, int C,
+                                 const float* gamma, const float* beta, float eps, float* aux, hipStream_t st) {
+    hipLaunchKernelGGL(stats_finalize_k, dim3(C), dim3(256), 0, st, pmean, pm2, T, R, M, C, gamma, beta, eps, aux);
     return hipGetLastError();
 }
 
@@ -215,7 +248,7 @@ hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const
 // meet in a fixed-shape LDS tree, and lane 0 of each quad adds the tile's
 // sums to the accumulators.
 template <bool MASK, bool DUAL>
-__global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, double* __restrict__ acc) {
+__global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, BnSums out) {
     __shared__ f4 red[3][256];
     const int tid = threadIdx.x;
     const int C = a.C, C4 = C >> 2;
@@ -279,9 +312,16 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, double* __re
             const int slot = blockIdx.x % kAccSlots;
             for (int k = 0; k < 4; ++k) {
                 const int c = (qbase + tid) * 4 + k;
-                acc_add(acc, 0, slot, C, c, (double)t0[k]);
-                acc_add(acc, 1, slot, C, c, (double)t1[k]);
-                if (DUAL) acc_add(acc, 2, slot, C, c, (double)t2[k]);
+                if (out.acc) {
+                    acc_add(out.acc, 0, slot, C, c, (double)t0[k]);
+                    acc_add(out.acc, 1, slot, C, c, (double)t1[k]);
+                    if (DUAL) acc_add(out.acc, 2, slot, C, c, (double)t2[k]);
+                } else {
+                    const long o = (long)blockIdx.x * C + c;
+                    out.p0[o] = t0[k];
+                    out.p1[o] = t1[k];
+                    if (DUAL) out.p2[o] = t2[k];
+                }
             }
         }
         __syncthreads();
@@ -336,6 +376,20 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, 
                 }
             }
         }
+    } else if (k.coef1) {
+        for (int c = threadIdx.x; c < C; c += blockDim.x) {
+            cf[c] = k.coef1[c];
+            cf[C + c] = k.coef1[C + c];
+            cf[2 * C + c] = k.coef1[2 * C + c];
+            cf[3 * C + c] = a.mean1[c];
+            cf[4 * C + c] = a.rstd1[c];
+            if (dual && k.coef2) {
+                cf[5 * C + c] = k.coef2[c];
+                cf[6 * C + c] = k.coef2[2 * C + c];
+                cf[7 * C + c] = a.mean2[c];
+                cf[8 * C + c] = a.rstd2[c];
+            }
+        }
     }
     __syncthreads();
     const int C4 = C >> 2;
@@ -365,15 +419,59 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, 
     }
 }
 
-hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, double* acc, hipStream_t st) {
+hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, const BnSums& out, hipStream_t st) {
     const dim3 grid(stats_tiles(a.M));
     if (a.mask) {
-        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<true, true>), grid, dim3(256), 0, st, a, acc);
-        else hipLaunchKernelGGL((bn_bwd_reduce_k<true, false>), grid, dim3(256), 0, st, a, acc);
+        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<true, true>), grid, dim3(256), 0, st, a, out);
+        else hipLaunchKernelGGL((bn_bwd_reduce_k<true, false>), grid, dim3(256), 0, st, a, out);
     } else {
-        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<false, true>), grid, dim3(256), 0, st, a, acc);
-        else hipLaunchKernelGGL((bn_bwd_reduce_k<false, false>), grid, dim3(256), 0, st, a, acc);
+        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<false, true>), grid, dim3(256), 0, st, a, out);
+        else hipLaunchKernelGGL((bn_bwd_reduce_k<false, false>), grid, dim3(256), 0, st, a, out);
     }
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void bn_bwd_finalize_k(const float* __restrict__ p0, const float* __restrict__ p1,
+                                                         const float* __restrict__ p2, int T, long M, int C,
+                                                         const float* __restrict__ gamma1,
+                                                         const float* __restrict__ rstd1, float* gg1, float* gb1,
+                                                         float* coef1, const float* __restrict__ gamma2,
+                                                         const float* __restrict__ rstd2, float* gg2, float* gb2,
+                                                         float* coef2) {
+    __shared__ double red[256];
+    const int c = blockIdx.x;
+    const bool dual = coef2 != nullptr;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0;
+#pragma unroll 4
+    for (int t = threadIdx.x; t < T; t += 256) {
+        s0 += (double)p0[(long)t * C + c];
+        s1 += (double)p1[(long)t * C + c];
+        if (dual) s2 += (double)p2[(long)t * C + c];
+    }
+    const double t0 = tree_sum256(s0, red);
+    const double t1 = tree_sum256(s1, red);
+    const double t2 = dual ? tree_sum256(s2, red) : 0.0;
+    if (threadIdx.x != 0) return;
+    if (gg1) gg1[c] = (float)t1;
+    if (gb1) gb1[c] = (float)t0;
+    coef1[c] = gamma1[c] * rstd1[c];
+    coef1[C + c] = (float)(t0 / (double)M);
+    coef1[2 * C + c] = (float)(t1 / (double)M);
+    if (dual) {
+        if (gg2) gg2[c] = (float)t2;
+        if (gb2) gb2[c] = (float)t0;
+        coef2[c] = gamma2[c] * rstd2[c];
+        coef2[C + c] = (float)(t0 / (double)M);
+        coef2[2 * C + c] = (float)(t2 / (double)M);
+    }
+}
+
+hipError_t launch_bn_bwd_finalize(const float* p0, const float* p1, const float* p2, int T, long M, int C,
+                                  const float* gamma1, const float* rstd1, float* gg1, float* gb1, float* coef1,
+                                  const float* gamma2, const float* rstd2, float* gg2, float* gb2, float* coef2,
+                                  hipStream_t st) {
+    hipLaunchKernelGGL(bn_bwd_finalize_k, dim3(C), dim3(256), 0, st, p0, p1, p2, T, M, C, gamma1, rstd1, gg1, gb1,
+                       coef1, gamma2, rstd2, gg2, gb2, coef2);
     return hipGetLastError();
 }
 
@@ -381,7 +479,8 @@ hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, double* acc, hipStream_t st)
 hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const BnBwdCoef& k, float* dx1, bool acc1, float* dx2, bool acc2,
                                float* dres, bool accres, hipStream_t st) {
     if (a.C % 4) return hipErrorInvalidValue;
-    if ((dx1 || dx2) && !k.acc) return hipErrorInvalidValue;
+    if ((dx1 || dx2) && !k.acc && !k.coef1) return hipErrorInvalidValue;
+    if (dx2 && !k.acc && !k.coef2) return hipErrorInvalidValue;
     const long n4 = a.M * a.C / 4;
     const int E = bn_quads_per_thread(n4);
     // one workgroup when only dgamma and dbeta are wanted

@@ -403,6 +403,9 @@ struct lpp_ctx {
     size_t off_v = 0, off_wbuf = 0, off_g = 0, off_m = 0, off_loss = 0, off_img = 0, off_ps = 0, off_wpart = 0,
            off_args = 0, off_acc = 0;
     long n_acc = 0;                          // doubles zeroed at the start of every step
+    // sequential mode merges batch-norm reductions in a fixed order (bitwise
+    // reproducible); async mode through atomic accumulators
+    bool fixed_order = true;
     bool graphs = true;
     long ps_floats = 0;
     std::unique_ptr<std::atomic<long>[]> counters;
@@ -500,8 +503,16 @@ int bn_stats_standalone(lpp_ctx* c, Worker& w, int b) {
     const long rows = (long)N * B.in0.h * B.in0.w;
     const float* x = c->act(w, B.L.in0);
     hipStream_t st = w.stream;
-    LAUNCH("bn_stats", 4.0 * rows * C, st,
-           lpp::launch_stats_partial(x, rows, C, nullptr, nullptr, c->acc_fwd(w, b), st));
+    if (c->fixed_order) {
+        const lpp::BnSums out{nullptr, w.ps0, w.ps1, nullptr};
+        LAUNCH("bn_stats", 4.0 * rows * C, st, lpp::launch_stats_partial(x, rows, C, out, st));
+        LAUNCH("bn_stats", 0.0, st,
+               lpp::launch_stats_finalize(w.ps0, w.ps1, lpp::stats_tiles(rows), lpp::kStatRows, rows, C,
+                                          w.v + B.poff, w.v + B.poff + C, M.desc.bn_eps, c->aux(w, b), st));
+    } else {
+        const lpp::BnSums out{c->acc_fwd(w, b), nullptr, nullptr, nullptr};
+        LAUNCH("bn_stats", 4.0 * rows * C, st, lpp::launch_stats_partial(x, rows, C, out, st));
+    }
     return LPP_OK;
 }
 
@@ -522,9 +533,21 @@ int run_forward(lpp_ctx* c, Worker& w) {
         case G_CONV: {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride, Y.L.pad};
             const float* bias = Y.L.bias ? w.v + Y.poff + Y.wcount : nullptr;
+            lpp::BnSums sums{};
+            if (G.stats_bn >= 0) sums = c->fixed_order ? lpp::BnSums{nullptr, w.ps0, w.ps1, nullptr}
+                                                       : lpp::BnSums{c->acc_fwd(w, G.stats_bn), nullptr, nullptr, nullptr};
             LAUNCH("conv_fwd", 2.0 * Y.macs, st,
                    lpp::launch_conv_igemm(lpp::CONV_FWD, x0, w.wbuf + Y.wf_off, bias, c->act(w, G.a), g, false,
-                                          G.stats_bn >= 0 ? c->acc_fwd(w, G.stats_bn) : nullptr, st));
+                                          G.stats_bn >= 0 ? &sums : nullptr, st));
+            if (G.stats_bn >= 0 && c->fixed_order) {
+                const Layer& B = M.layers[G.stats_bn];
+                const long rows = (long)N * Y.out.h * Y.out.w;
+                const int R = lpp::conv_tile_rows(g);
+                const int T = (int)((rows + R - 1) / R);
+                LAUNCH("bn_stats", 0.0, st,
+                       lpp::launch_stats_finalize(w.ps0, w.ps1, T, R, rows, Y.L.cout, w.v + B.poff,
+                                                  w.v + B.poff + Y.L.cout, M.desc.bn_eps, c->aux(w, G.stats_bn), st));
+            }
             break;
         }
         case G_BNACT: {
@@ -538,13 +561,13 @@ int run_forward(lpp_ctx* c, Worker& w) {
                 if (rc) return rc;
             }
             const Layer& B1 = M.layers[G.a];
-            const lpp::BnFwd b1{c->acc_fwd(w, G.a), w.v + B1.poff, w.v + B1.poff + C, M.desc.bn_eps, Mrows,
-                                c->aux(w, G.a)};
+            const lpp::BnFwd b1{c->fixed_order ? nullptr : c->acc_fwd(w, G.a), w.v + B1.poff, w.v + B1.poff + C,
+                                M.desc.bn_eps, Mrows, c->aux(w, G.a)};
             lpp::BnFwd b2{};
             if (G.bn2 >= 0) {
                 const Layer& B2 = M.layers[G.bn2];
-                b2 = lpp::BnFwd{c->acc_fwd(w, G.bn2), w.v + B2.poff, w.v + B2.poff + C, M.desc.bn_eps, Mrows,
-                                c->aux(w, G.bn2)};
+                b2 = lpp::BnFwd{c->fixed_order ? nullptr : c->acc_fwd(w, G.bn2), w.v + B2.poff, w.v + B2.poff + C,
+                                M.desc.bn_eps, Mrows, c->aux(w, G.bn2)};
             }
             const float* x2 = G.bn2 >= 0 ? c->act(w, M.layers[G.bn2].L.in0) : nullptr;
             const float* r = G.res >= 0 ? c->act(w, G.res) : nullptr;
@@ -627,8 +650,8 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                 if (Y.L.bias) {
                     // column sums of dY, from per-tile means
                     const long Mo = (long)N * Y.out.h * Y.out.w;
-                    LAUNCH("bias_grad", 4.0 * Mo * Y.L.cout, st,
-                           lpp::launch_stats_partial(dy, Mo, Y.L.cout, w.ps0, w.ps1, nullptr, st));
+                    const lpp::BnSums tiles{nullptr, w.ps0, w.ps1, nullptr};
+                    LAUNCH("bias_grad", 4.0 * Mo * Y.L.cout, st, lpp::launch_stats_partial(dy, Mo, Y.L.cout, tiles, st));
                     LAUNCH("bias_grad", 0.0, st,
                            lpp::launch_sum_from_tiles(w.ps0, lpp::stats_tiles(Mo), lpp::kStatRows, Mo, Y.L.cout,
                                                       w.g + Y.poff + Y.wcount, st));
@@ -660,20 +683,35 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
             lpp::BnBwdArgs a{dy, G.relu >= 0 ? c->act(w, G.out) : nullptr, x0, ax, ax + C,
                              want2 ? c->act(w, Y2->L.in0) : nullptr, want2 ? ax2 : nullptr,
                              want2 ? ax2 + C : nullptr, Min, C};
-            if (want1 || want2)
-                LAUNCH("bn_bwd", (a.mask ? 12.0 : 8.0) * Min * C + (want2 ? 4.0 * Min * C : 0.0), st,
-                       lpp::launch_bn_bwd_reduce(a, c->acc_bwd(w, G.a), st));
-            const lpp::BnBwdCoef k{want1 || want2 ? c->acc_bwd(w, G.a) : nullptr,
-                                   w.v + Y.poff,
-                                   pl.wgrad[G.a] ? w.g + Y.poff : nullptr,
-                                   pl.wgrad[G.a] ? w.g + Y.poff + C : nullptr,
-                                   want2 ? w.v + Y2->poff : nullptr,
-                                   want2 && pl.wgrad[b2] ? w.g + Y2->poff : nullptr,
-                                   want2 && pl.wgrad[b2] ? w.g + Y2->poff + C : nullptr};
+            float* gg1 = pl.wgrad[G.a] ? w.g + Y.poff : nullptr;
+            float* gb1 = pl.wgrad[G.a] ? w.g + Y.poff + C : nullptr;
+            float* gg2 = want2 && pl.wgrad[b2] ? w.g + Y2->poff : nullptr;
+            float* gb2 = want2 && pl.wgrad[b2] ? w.g + Y2->poff + C : nullptr;
+            lpp::BnBwdCoef k{};
+            if (want1 || want2) {
+                const double bytes = (a.mask ? 12.0 : 8.0) * Min * C + (want2 ? 4.0 * Min * C : 0.0);
+                if (c->fixed_order) {
+                    const lpp::BnSums out{nullptr, w.ps0, w.ps1, w.ps2};
+                    LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(a, out, st));
+                    LAUNCH("bn_bwd", 0.0, st,
+                           lpp::launch_bn_bwd_finalize(w.ps0, w.ps1, w.ps2, lpp::stats_tiles(Min), Min, C,
+                                                       w.v + Y.poff, ax + C, gg1, gb1, ax + 4 * C,
+                                                       want2 ? w.v + Y2->poff : nullptr, want2 ? ax2 + C : nullptr,
+                                                       gg2, gb2, want2 ? ax2 + 4 * C : nullptr, st));
+                    k.coef1 = ax + 4 * C;
+                    k.coef2 = want2 ? ax2 + 4 * C : nullptr;
+                } else {
+                    const lpp::BnSums out{c->acc_bwd(w, G.a), nullptr, nullptr, nullptr};
+                    LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(a, out, st));
+                    k = lpp::BnBwdCoef{c->acc_bwd(w, G.a), w.v + Y.poff, gg1, gb1,
+                                       want2 ? w.v + Y2->poff : nullptr, gg2, gb2, nullptr, nullptr};
+                }
+            }
             float* d1 = want1 && pl.din0[G.a] ? dx0 : nullptr;
             float* d2 = want2 && pl.din0[b2] ? c->dact(w, Y2->L.in0) : nullptr;
             float* dr = want_res ? c->dact(w, G.res) : nullptr;
-            if (d1 || d2 || dr || want1 || want2) {
+            // (with atomic sums the apply kernel also writes dgamma and dbeta)
+            if (d1 || d2 || dr || (k.acc && (gg1 || gb1 || gg2 || gb2))) {
                 const double bytes = ((a.mask ? 8.0 : 4.0) + (d1 ? 12.0 : 0.0) + (d2 ? 12.0 : 0.0) +
                                       (dr ? (acc_res ? 8.0 : 4.0) : 0.0)) * Min * C;
                 LAUNCH("bn_bwd", bytes, st,
@@ -801,6 +839,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
     c->K = K;
     c->P = P;
     c->mode = opt ? opt->mode : LPP_SEQUENTIAL;
+    c->fixed_order = c->mode == LPP_SEQUENTIAL;
     if (c->mode != LPP_SEQUENTIAL && c->mode != LPP_ASYNC) return fail(LPP_EINVAL, "unknown mode");
     build_groups(c->M, !(opt && opt->unfused));
     c->graphs = !(opt && opt->no_graphs);
@@ -853,7 +892,12 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         if (Y.L.op == LPP_BN) Y.aux = take(sizeof(float) * 7 * Y.out.c);
         if (Y.L.op == LPP_MAXPOOL) Y.aux = take((size_t)rows_out * Y.out.c);
         const long rin = (long)N * Y.in0.h * Y.in0.w;
+        if (Y.L.op == LPP_BN) ps = std::max<long>(ps, (long)lpp::stats_tiles(rin) * Y.out.c);
         if (Y.L.op == LPP_CONV) {
+            lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
+                            Y.L.pad};
+            const long tiles = (rows_out + lpp::conv_tile_rows(g) - 1) / lpp::conv_tile_rows(g);
+            ps = std::max<long>(ps, tiles * Y.L.cout);
             ps = std::max<long>(ps, (long)lpp::stats_tiles(rows_out) * Y.L.cout);
             wpart = std::max<long>(wpart, Y.wg.part_floats);
         }

@@ -212,17 +212,19 @@ def test_tiny_cnn_ten_steps():
         assert max(errs.values()) < T.TOL_PARAM, T.worst(errs)
 
 
-def _partition_step(o, p, x, m0, img, lab, partition, lr=0.1, mu=0.9, band=None, unfused=False):
+def _partition_step(o, p, x, m0, img, lab, partition, lr=0.1, mu=0.9, band=None, unfused=False,
+                    mode=lpp.SEQUENTIAL):
     xr = x.astype(np.float64)
     mr = m0.astype(np.float64)
     _, sc = R.grad_scale(o, xr, img, lab)
     g, loss, logits = R.step(o, xr, mr, img, lab, partition, lr, mu)
     n = img.shape[0]
-    with lpp.Context(p, K=1, batch=n, momentum=mu, unfused=unfused) as ctx:
+    with lpp.Context(p, K=1, batch=n, momentum=mu, unfused=unfused, mode=mode) as ctx:
         ctx.set_params(x)
         w = max(partition - 1, 0)
         ctx.set_momentum(w, m0)
         ctx.step(w, *dev(img, lab), partition, lr)
+        ctx.sync()
         if band is not None:
             T.assert_decisions_match(o, ctx, w, x, img, band)
         assert T.relerr(ctx.get_logits(w), logits, T.TAU_LOGITS) < T.TOL_LOGITS
@@ -401,6 +403,19 @@ def test_full_size_relu_free_resnet20_gradients(partition):
     img, lab = T.inputs(82, 128, o.in_shape, 10)
     m0 = np.zeros(o.d, np.float32)
     _partition_step(o, p, x, m0, img, lab, partition)
+
+
+@pytest.mark.parametrize("unfused,batch,partition", [(False, 128, 0), (False, 128, 2), (True, 16, 1)],
+                         ids=["fused-b128-p0", "fused-b128-p2", "unfused-b16-p1"])
+def test_async_mode_atomic_reductions_match_oracle(unfused, batch, partition):
+    """Async mode merges batch-norm sums across workgroups through fp64
+    atomic accumulators (sequential mode through fixed-order partials); one
+    step issued alone must meet the same bars against the oracle."""
+    o, p = OM.resnet20_p4(relu=False), PM.resnet20(act=False)
+    x = T.init_x(o.specs, 85 + batch)
+    img, lab = T.inputs(86 + batch, batch, o.in_shape, 10)
+    m0 = (np.random.default_rng(3).standard_normal(o.d) * 1e-2).astype(np.float32)
+    _partition_step(o, p, x, m0, img, lab, partition, unfused=unfused, mode=lpp.ASYNC)
 
 
 def test_full_size_resnet20_forward_and_gradient_invariants():
