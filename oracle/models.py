@@ -190,11 +190,12 @@ def resnet_cifar(n_per_stage=3, widths=(16, 32, 64), n_classes=10, hw=32, relu=T
     return net
 
 
-def _preact_unit(net, x, cin, cout, stride):
+def _preact_unit(net, x, cin, cout, stride, relu=True):
     net.next_unit()
-    o1 = net.relu(net.bn(x, cin))
+    act = net.relu if relu else (lambda t: t)
+    o1 = act(net.bn(x, cin))
     h = net.conv(o1, cin, cout, 3, stride, 1)
-    h = net.relu(net.bn(h, cout))
+    h = act(net.bn(h, cout))
     h = net.conv(h, cout, cout, 3, 1, 1)
     if stride != 1 or cin != cout:
         s = net.conv(o1, cin, cout, 1, stride, 0)
@@ -203,10 +204,10 @@ def _preact_unit(net, x, cin, cout, stride):
     return net.add(h, s)
 
 
-def wrn(depth=16, widen=8, n_classes=100, hw=32):
+def wrn(depth=16, widen=8, n_classes=100, hw=32, relu=True):
     """Pre-activation Wide ResNet-depth-widen.  Units: 0 = stem, then
     3*(depth-4)/6 residual units, then the head (final BN-ReLU, pool,
-    linear)."""
+    linear).  relu=False drops every ReLU (the decision-free twin)."""
     n = (depth - 4) // 6
     widths = (16 * widen, 32 * widen, 64 * widen)
     net = Net("wrn%d_%d" % (depth, widen), 3, hw, hw, n_classes)
@@ -215,28 +216,32 @@ def wrn(depth=16, widen=8, n_classes=100, hw=32):
     for si, w in enumerate(widths):
         for b in range(n):
             stride = 2 if (si > 0 and b == 0) else 1
-            x = _preact_unit(net, x, cin, w, stride)
+            x = _preact_unit(net, x, cin, w, stride, relu)
             cin = w
     net.next_unit()
-    x = net.relu(net.bn(x, cin))
+    x = net.bn(x, cin)
+    if relu:
+        x = net.relu(x)
     x = net.gap(x)
     net.linear(x, cin, n_classes)
     return net
 
 
-def resnet_imagenet(units_per_stage=(2, 2, 2, 2), widths=(64, 128, 256, 512), n_classes=1000, hw=224):
+def resnet_imagenet(units_per_stage=(2, 2, 2, 2), widths=(64, 128, 256, 512), n_classes=1000, hw=224, relu=True):
     """ImageNet ResNet with basic units (ResNet-18 by default): 7x7/2 stem,
-    BN, ReLU, 3x3/2 max pool, four stages, projection shortcuts."""
+    BN, ReLU, 3x3/2 max pool, four stages, projection shortcuts.
+    relu=False drops every ReLU (the max pool stays)."""
     net = Net("resnet%d" % (2 + 2 * sum(units_per_stage)), 3, hw, hw, n_classes)
     x = net.conv(-1, 3, widths[0], 7, 2, 3)
     x = net.bn(x, widths[0])
-    x = net.relu(x)
+    if relu:
+        x = net.relu(x)
     x = net.maxpool(x, 3, 2, 1)
     cin = widths[0]
     for si, (w, nu) in enumerate(zip(widths, units_per_stage)):
         for b in range(nu):
             stride = 2 if (si > 0 and b == 0) else 1
-            x = _basic_unit(net, x, cin, w, stride)
+            x = _basic_unit(net, x, cin, w, stride, relu)
             cin = w
     net.next_unit()
     x = net.gap(x)

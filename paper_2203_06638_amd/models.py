@@ -108,14 +108,16 @@ def post_act_unit(m, x, cout, stride, act=True):
     return relu(m.add(y, sc))
 
 
-def pre_act_unit(m, x, cout, stride):
+def pre_act_unit(m, x, cout, stride, act=True):
     """BN-ReLU-conv3x3-BN-ReLU-conv3x3 (+ identity, or 1x1 conv of the
-    pre-activated input when the shape changes)."""
+    pre-activated input when the shape changes).  act=False leaves the ReLUs
+    out."""
     m.new_unit()
+    relu = m.relu if act else (lambda t: t)
     cin = m.shapes[x][0]
-    a = m.relu(m.bn(x))
+    a = relu(m.bn(x))
     y = m.conv(a, cout, 3, stride)
-    y = m.conv(m.relu(m.bn(y)), cout, 3, 1)
+    y = m.conv(relu(m.bn(y)), cout, 3, 1)
     sc = m.conv(a, cout, 1, stride, 0) if (stride != 1 or cin != cout) else x
     return m.add(y, sc)
 
@@ -153,15 +155,16 @@ def resnet20(n_classes=10, act=True):
     return resnet_cifar(20, (16, 32, 64), n_classes, blocks=[1, 1, 1, 2, 2, 3, 3, 3, 4, 4, 4], act=act)
 
 
-def wide_resnet(depth=16, k=8, n_classes=100, hw=32, blocks=None):
+def wide_resnet(depth=16, k=8, n_classes=100, hw=32, blocks=None, act=True):
     n = (depth - 4) // 6
     m = Model("wrn%d_%d" % (depth, k), (3, hw, hw), n_classes)
     x = m.conv(-1, 16, 3)
     for si, wdt in enumerate((16 * k, 32 * k, 64 * k)):
         for u in range(n):
-            x = pre_act_unit(m, x, wdt, 2 if (si and not u) else 1)
+            x = pre_act_unit(m, x, wdt, 2 if (si and not u) else 1, act)
     m.new_unit()
-    m.linear(m.gap(m.relu(m.bn(x))), n_classes)
+    x = m.bn(x)
+    m.linear(m.gap(m.relu(x) if act else x), n_classes)
     return m.assign_blocks(blocks or [1] * m.n_units)
 
 
@@ -170,12 +173,13 @@ def wrn16_8(n_classes=100):
     return wide_resnet(16, 8, n_classes, blocks=[1, 1, 1, 2, 3, 3, 4, 4])
 
 
-def resnet_imagenet(units=(2, 2, 2, 2), widths=(64, 128, 256, 512), n_classes=1000, hw=224, blocks=None):
+def resnet_imagenet(units=(2, 2, 2, 2), widths=(64, 128, 256, 512), n_classes=1000, hw=224, blocks=None, act=True):
     m = Model("resnet%d" % (2 + 2 * sum(units)), (3, hw, hw), n_classes)
-    x = m.maxpool(m.relu(m.bn(m.conv(-1, widths[0], 7, 2, 3))), 3, 2, 1)
+    x = m.bn(m.conv(-1, widths[0], 7, 2, 3))
+    x = m.maxpool(m.relu(x) if act else x, 3, 2, 1)
     for si, (wdt, nu) in enumerate(zip(widths, units)):
         for u in range(nu):
-            x = post_act_unit(m, x, wdt, 2 if (si and not u) else 1)
+            x = post_act_unit(m, x, wdt, 2 if (si and not u) else 1, act)
     m.new_unit()
     m.linear(m.gap(x), n_classes)
     return m.assign_blocks(blocks or [1] * m.n_units)

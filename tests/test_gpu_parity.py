@@ -393,6 +393,65 @@ def test_resnet20_100_replicas_sequential_schedule():
 
 
 # ---------------------------------------------------------------------------
+# the other architectures of the workloads, on small instances: pre-activation
+# Wide ResNet (final BN-ReLU head) and ImageNet-style ResNet (7x7/2 stem, 3x3/2
+# max pool, projection shortcuts), on seeds whose decisions all keep a margin
+# above the band (oracle side) and whose GPU values deviate by less than half
+# of it (GPU side).  In the ImageNet ResNet a max pool reads a ReLU output, so
+# windows of zeros tie exactly; its gradients are compared on the ReLU-free
+# twin (max pool kept) and its forward with the ReLUs.
+# ---------------------------------------------------------------------------
+
+def _rn_mini_o(relu=True):
+    return OM.resnet_imagenet((1, 1, 1, 1), (16, 32, 64, 128), 10, 128, relu=relu).set_blocks([1, 1, 2, 3, 4, 4])
+
+
+def _rn_mini_p(act=True):
+    return PM.resnet_imagenet((1, 1, 1, 1), (16, 32, 64, 128), 10, 128, blocks=[1, 1, 2, 3, 4, 4], act=act)
+
+
+MINIS = {
+    "wrn10_2": (lambda: OM.wrn(10, 2, 10, 16).set_blocks([1, 1, 2, 3, 4]),
+                lambda: PM.wide_resnet(10, 2, 10, 16, blocks=[1, 1, 2, 3, 4]), 4),
+    "resnet_imagenet_mini_relu_free": (lambda: _rn_mini_o(False), lambda: _rn_mini_p(False), 2),
+}
+
+
+def test_resnet_imagenet_mini_forward_with_relu():
+    o, p = _rn_mini_o(), _rn_mini_p()
+    shapes = R.shapes(o)
+    x = T.init_x(o.specs, 2101)
+    img, lab = T.inputs(2102, 2, o.in_shape, 10)
+    _, logits, _ = R.forward_backward(o, x, img, lab, grad=False)
+    with lpp.Context(p, K=1, batch=2, unfused=True) as ctx:
+        ctx.set_params(x)
+        ctx.step(0, *dev(img, lab), 0, 0.0)
+        assert T.relerr(ctx.get_logits(0), logits, T.TAU_LOGITS) < T.TOL_LOGITS
+        for layer in range(len(o.layers)):
+            ref = R.activation(o, x, img, layer)
+            got = ctx.get_activation(0, layer, shapes[layer])
+            assert T.relerr(got, ref, T.TAU_LOGITS) < 1e-3, layer
+
+
+@pytest.mark.parametrize("name", sorted(MINIS))
+def test_architecture_minis_all_partitions(name):
+    mk_o, mk_p, n = MINIS[name]
+    o, p = mk_o(), mk_p()
+    band = 1e-5
+
+    def make(seed):
+        return T.init_x(o.specs, seed).astype(np.float64), T.inputs(seed + 7, n, o.in_shape, 10)[0]
+
+    seed, margin = T.well_posed_seed(o, make, seeds=range(2000, 2400), band=band)
+    say(name, "seed", seed, "margin %.2e" % margin)
+    x = T.init_x(o.specs, seed)
+    img, lab = T.inputs(seed + 7, n, o.in_shape, 10)
+    m0 = (np.random.default_rng(5).standard_normal(o.d) * 1e-2).astype(np.float32)
+    for part in range(0, 5):
+        _partition_step(o, p, x, m0, img, lab, part, band=band)
+
+
+# ---------------------------------------------------------------------------
 # the headline workload's full size (batch 128, momentum 0.9)
 # ---------------------------------------------------------------------------
 

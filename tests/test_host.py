@@ -19,6 +19,11 @@ PAIRS = [
     ("resnet20_100", lambda: PM.resnet20(100), lambda: OM.resnet20_p4(100)),
     ("wrn16_8", PM.wrn16_8, OM.wrn16_8_p4),
     ("resnet18", PM.resnet18, OM.resnet18_p4),
+    ("wrn10_2_mini", lambda: PM.wide_resnet(10, 2, 10, 16, blocks=[1, 1, 2, 3, 4]),
+     lambda: OM.wrn(10, 2, 10, 16).set_blocks([1, 1, 2, 3, 4])),
+    ("resnet_imagenet_mini", lambda: PM.resnet_imagenet((1, 1, 1, 1), (16, 32, 64, 128), 10, 64,
+                                                        blocks=[1, 1, 2, 3, 4, 4]),
+     lambda: OM.resnet_imagenet((1, 1, 1, 1), (16, 32, 64, 128), 10, 64).set_blocks([1, 1, 2, 3, 4, 4])),
 ]
 
 
