@@ -1,0 +1,541 @@
+// conv_bf16.hip -- convolution passes with bfloat16 activations and weights on
+// gfx950 matrix cores (v_mfma_f32_16x16x32_bf16), float32 accumulation.
+//
+// Forward and data-gradient passes are one implicit GEMM
+//     Y[m][n] = sum_k A[m][k] * B[n][k]
+// with m a pixel of the pass's output grid, n an output channel and k = (tap,
+// c) a filter tap and a source channel.  A is gathered from the NHWC bf16
+// source; B rows are the snapshot's bf16 weight layouts, [n][r][s][c] with c
+// contiguous (W_f[cout][r][s][cin] forward, W_d[cin][r][s][cout] for the
+// data gradient).  A pass is described by its taps: output pixel (i, j) reads
+// source pixel (i*ss + dh, j*ss + dw) through weight tap (r, s), with
+//   forward                 dh = r - pad,            ss = stride
+//   data gradient, stride 1  dh = pad - r,            ss = 1
+//   data gradient, stride 2  one pass per output parity class (a, b): the dX
+//                            pixels (2i + a, 2j + b) receive only the taps
+//                            with a + pad - r and b + pad - s even, from dY
+//                            pixel (i + (a + pad - r)/2, j + (b + pad - s)/2)
+// (likewise for columns), so no multiply is spent on taps between strides.
+//
+// Lane layout of v_mfma_f32_16x16x32_bf16 (64 lanes): lane l supplies
+// A[row l%16][k = 8*(l/16) .. +8] and B[col l%16][same k] and receives
+// D[rows 4*(l/16) .. +4][col l%16].  A K-step is 32 values of k: four 8-channel
+// chunks, each from one tap (a tap holds Cs/8 chunks; for Cs < 32 a K-step
+// spans several taps).  Operand tiles go through LDS with a row pitch of 40
+// bf16 (80 bytes), which keeps the 16-byte fragment reads of 16 lanes on
+// distinct banks; tiles are double-buffered, the next K-step's global loads
+// are in flight during the current step's MFMAs, one barrier per step.
+//
+// Weight gradient: dW[cout][(tap, c)] = sum over output pixels p of
+// dY[p][cout] * X[src(p, tap)][c]: a GEMM whose reduction runs over pixels.
+// Both operands are pixel-major in memory, so each K-step of 32 pixels is
+// written into LDS transposed (pairs of pixels packed into 32-bit words),
+// after which the MFMA fragments are read exactly as in the forward kernel.
+// Pixel ranges (splits) write float32 partials that a second kernel sums in
+// a fixed order; nothing here uses atomics except the batch-norm sums of the
+// forward epilogue in async mode (bnacc.h).
+#include <algorithm>
+
+#include "act.h"
+#include "bnacc.h"
+#include "kernels.h"
+
+namespace lpp {
+
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+
+constexpr int kBfPitch = 40;
+
+__device__ __forceinline__ f4 mfma_bf16(bf8 a, bf8 b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// One pass of the implicit GEMM (see the header comment).
+struct BfPass {
+    int Hv, Wv;              // output grid of the pass
+    int os, oa, ob;          // destination pixel (i*os + oa, j*os + ob)
+    int Hd, Wd;              // destination tensor grid
+    int ss;                  // source stride
+    int nr, ns, r0, s0, step;// taps r = r0 + step*x (x < nr), s = s0 + step*y (y < ns)
+    int offh, offw, sgn, shift;  // dh = (offh + sgn*r) >> shift, dw = (offw + sgn*s) >> shift
+};
+
+// Output channels in the epilogue: BM x BN tile, bf16, pitch BN + 8.
+template <int BM, int BN, bool STATS>
+__global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src, const bf16* __restrict__ B,
+                                                   const float* __restrict__ bias, bf16* __restrict__ Y, ConvGeom g,
+                                                   BfPass ps, int accumulate, BnSums sums) {
+    constexpr int TM = BM / 32, TN = BN / 32;     // 16x16 blocks per wave; waves 2 x 2
+    constexpr int AL = BM / 64, BL = BN / 64;     // 16-byte operand loads per thread per K-step
+    constexpr int P = kBfPitch;
+    constexpr int STAGE = (BM + BN) * P;
+    constexpr int OP = BN + 8;
+    static_assert(BM * OP <= 2 * STAGE, "the epilogue tile reuses the operand buffers");
+    __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    const long Mv = (long)g.Nb * ps.Hv * ps.Wv;
+    const long m0 = (long)blockIdx.x * BM;
+    const int n0 = blockIdx.y * BN;
+    const int j = tid & 3, rr = tid >> 2;
+    const int RS = g.R * g.S;
+
+    // the output rows whose A values this thread loads
+    int a_img[AL], a_h[AL], a_w[AL];
+    bool a_ok[AL];
+#pragma unroll
+    for (int u = 0; u < AL; ++u) {
+        const long m = m0 + rr + 64 * u;
+        a_ok[u] = m < Mv;
+        const long mm = a_ok[u] ? m : 0;
+        const int ow = (int)(mm % ps.Wv);
+        const long t = mm / ps.Wv;
+        a_img[u] = (int)(t / ps.Hv) * g.Hs;
+        a_h[u] = (int)(t % ps.Hv) * ps.ss;
+        a_w[u] = ow * ps.ss;
+    }
+    const bf16* b_row[BL];
+#pragma unroll
+    for (int u = 0; u < BL; ++u) {
+        const int n = n0 + rr + 64 * u;
+        b_row[u] = n < g.Ncols ? B + (long)n * RS * g.Cs : nullptr;
+    }
+    const int cpt = g.Cs >> 3;                    // 8-channel chunks per tap
+    const int ntap = ps.nr * ps.ns;
+    const int nks = (ntap * cpt + 3) >> 2;
+
+    uint4 ra[AL], rb[BL];
+    auto load = [&](int ks) {
+        const int kc = ks * 4 + j;
+        const int tap = kc / cpt;
+        const int ch = (kc - tap * cpt) * 8;
+        const bool tok = tap < ntap;
+        const int x = tap / ps.ns, y = tap - (tap / ps.ns) * ps.ns;
+        const int r = ps.r0 + ps.step * x, s = ps.s0 + ps.step * y;
+        const int dh = (ps.offh + ps.sgn * r) >> ps.shift, dw = (ps.offw + ps.sgn * s) >> ps.shift;
+        const long woff = (long)(r * g.S + s) * g.Cs + ch;
+#pragma unroll
+        for (int u = 0; u < AL; ++u) {
+            const int h = a_h[u] + dh, w = a_w[u] + dw;
+            const bool ok = tok && a_ok[u] && h >= 0 && h < g.Hs && w >= 0 && w < g.Ws;
+            ra[u] = ok ? *(const uint4*)(src + ((long)(a_img[u] + h) * g.Ws + w) * g.Cs + ch) : uint4{0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int u = 0; u < BL; ++u)
+            rb[u] = (tok && b_row[u]) ? *(const uint4*)(b_row[u] + woff) : uint4{0, 0, 0, 0};
+    };
+    auto store = [&](int buf) {
+        bf16* As = lds + buf * STAGE;
+        bf16* Bs = As + BM * P;
+#pragma unroll
+        for (int u = 0; u < AL; ++u) *(uint4*)(As + (rr + 64 * u) * P + j * 8) = ra[u];
+#pragma unroll
+        for (int u = 0; u < BL; ++u) *(uint4*)(Bs + (rr + 64 * u) * P + j * 8) = rb[u];
+    };
+
+    f4 acc[TM][TN];
+#pragma unroll
+    for (int x = 0; x < TM; ++x)
+#pragma unroll
+        for (int y = 0; y < TN; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
+
+    if (nks > 0) {
+        load(0);
+        store(0);
+    }
+    __syncthreads();
+    for (int ks = 0; ks < nks; ++ks) {
+        const int cur = ks & 1;
+        if (ks + 1 < nks) load(ks + 1);
+        const bf16* As = lds + cur * STAGE;
+        const bf16* Bs = As + BM * P;
+        bf8 a[TM], b[TN];
+#pragma unroll
+        for (int x = 0; x < TM; ++x) a[x] = *(const bf8*)(As + ((wm * TM + x) * 16 + (lane & 15)) * P + (lane >> 4) * 8);
+#pragma unroll
+        for (int y = 0; y < TN; ++y) b[y] = *(const bf8*)(Bs + ((wn * TN + y) * 16 + (lane & 15)) * P + (lane >> 4) * 8);
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int y = 0; y < TN; ++y) acc[x][y] = mfma_bf16(a[x], b[y], acc[x][y]);
+        if (ks + 1 < nks) store(cur ^ 1);
+        __syncthreads();
+    }
+
+    // epilogue: bias, rounding to bf16 (the stored values, which the batch
+    // statistics describe), transpose through LDS, 16-byte channel stores
+    const int nvalid = (int)min((long)BM, Mv - m0);
+    bf16* Ot = lds;
+    float colsum[TN];
+#pragma unroll
+    for (int y = 0; y < TN; ++y) {
+        const int col = (wn * TN + y) * 16 + (lane & 15);
+        const float bb = (bias && n0 + col < g.Ncols) ? bias[n0 + col] : 0.f;
+        colsum[y] = 0.f;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int row = (wm * TM + x) * 16 + (lane >> 4) * 4 + i;
+                const bf16 h = to_bf16(acc[x][y][i] + bb);
+                acc[x][y][i] = from_bf16(h);
+                if (STATS && row < nvalid) colsum[y] += acc[x][y][i];
+                Ot[row * OP + col] = h;
+            }
+    }
+    __syncthreads();
+    constexpr int CPR = BN / 8;                   // 16-byte chunks per tile row
+    for (int e = tid; e < BM * CPR; e += 256) {
+        const int row = e / CPR, ch = (e - (e / CPR) * CPR) * 8;
+        const long m = m0 + row;
+        if (m >= Mv || n0 + ch >= g.Ncols) continue;
+        const int ow = (int)(m % ps.Wv);
+        const long t = m / ps.Wv;
+        const int oh = (int)(t % ps.Hv), img = (int)(t / ps.Hv);
+        bf16* dp = Y + ((long)(img * ps.Hd + oh * ps.os + ps.oa) * ps.Wd + ow * ps.os + ps.ob) * g.Ncols + n0 + ch;
+        uint4 v = *(const uint4*)(Ot + row * OP + ch);
+        if (accumulate) {
+            const uint4 o = *(const uint4*)dp;
+            const uint32_t* pv = (const uint32_t*)&v;
+            const uint32_t* po = (const uint32_t*)&o;
+            uint32_t w[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float lo = __uint_as_float(pv[q] << 16) + __uint_as_float(po[q] << 16);
+                const float hi = __uint_as_float(pv[q] & 0xffff0000u) + __uint_as_float(po[q] & 0xffff0000u);
+                w[q] = pack_bf16x2(lo, hi);
+            }
+            v = uint4{w[0], w[1], w[2], w[3]};
+        }
+        *(uint4*)dp = v;
+    }
+    if (STATS) {
+        // per output channel of the tile: mean, then the sum of squared
+        // deviations from it, over the tile's valid rows
+        __shared__ float red[2][BN];
+        __shared__ float tmean[BN];
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            float s = colsum[y];
+            s += __shfl_xor(s, 16);
+            s += __shfl_xor(s, 32);
+            if (lane < 16) red[wm][(wn * TN + y) * 16 + lane] = s;
+        }
+        __syncthreads();
+        if (tid < BN) tmean[tid] = (red[0][tid] + red[1][tid]) / (float)nvalid;
+        __syncthreads();
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            const int col = (wn * TN + y) * 16 + (lane & 15);
+            const float mu = tmean[col];
+            float q = 0.f;
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int row = (wm * TM + x) * 16 + (lane >> 4) * 4 + i;
+                    const float dv = acc[x][y][i] - mu;
+                    if (row < nvalid) q += dv * dv;
+                }
+            q += __shfl_xor(q, 16);
+            q += __shfl_xor(q, 32);
+            if (lane < 16) red[wm][col - (lane & 15) + lane] = q;
+        }
+        __syncthreads();
+        if (tid < BN && n0 + tid < g.Ncols) {
+            const int n = n0 + tid;
+            const float m2 = red[0][tid] + red[1][tid];
+            if (sums.acc) {
+                const double mu = tmean[tid], nr = (double)nvalid;
+                acc_add(sums.acc, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
+                acc_add(sums.acc, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)m2 + nr * mu * mu);
+            } else {
+                sums.p0[(long)blockIdx.x * g.Ncols + n] = tmean[tid];
+                sums.p1[(long)blockIdx.x * g.Ncols + n] = m2;
+            }
+        }
+    }
+}
+
+// Tile shape of a pass: BN = 128 for wide outputs, else 64; BM = 128 unless
+// that leaves fewer than 512 workgroups.
+static void pick_bf16(long Mv, int Ncols, int& bm, int& bn) {
+    bn = Ncols >= 128 ? 128 : 64;
+    const long nt = (Ncols + bn - 1) / bn;
+    bm = ((Mv + 127) / 128) * nt >= 512 ? 128 : 64;
+}
+
+int conv_bf16_tile_rows(const ConvGeom& g) {
+    int bm, bn;
+    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, bm, bn);
+    return bm;
+}
+
+bool conv_bf16_supported(int mode, const ConvGeom& g) {
+    if (g.Cs % 8 || g.Ncols % 8) return false;
+    if (mode == CONV_DGRAD && g.stride != 1 && g.stride != 2) return false;
+    return g.R <= 32 && g.S <= 32 && g.pad < 32;
+}
+
+template <int BM, int BN>
+static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const ConvGeom& g,
+                                   const BfPass& ps, bool acc, const BnSums* stats, hipStream_t st) {
+    const long Mv = (long)g.Nb * ps.Hv * ps.Wv;
+    if (Mv == 0) return hipSuccess;
+    dim3 grid((unsigned)((Mv + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
+    if (stats)
+        hipLaunchKernelGGL((conv_bf16_k<BM, BN, true>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc,
+                           *stats);
+    else
+        hipLaunchKernelGGL((conv_bf16_k<BM, BN, false>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc,
+                           BnSums{});
+    return hipGetLastError();
+}
+
+static hipError_t run_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const ConvGeom& g,
+                                const BfPass& ps, bool acc, const BnSums* stats, int bm, int bn, hipStream_t st) {
+    if (bm == 128 && bn == 128) return launch_bf16_pass<128, 128>(src, B, bias, Y, g, ps, acc, stats, st);
+    if (bm == 128) return launch_bf16_pass<128, 64>(src, B, bias, Y, g, ps, acc, stats, st);
+    if (bn == 128) return launch_bf16_pass<64, 128>(src, B, bias, Y, g, ps, acc, stats, st);
+    return launch_bf16_pass<64, 64>(src, B, bias, Y, g, ps, acc, stats, st);
+}
+
+hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const float* bias, bf16* Y, const ConvGeom& g,
+                            bool accumulate, const BnSums* stats, hipStream_t st) {
+    if (!conv_bf16_supported(mode, g)) return hipErrorInvalidValue;
+    int bm, bn;
+    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, bm, bn);
+    BfPass ps{};
+    ps.Hd = g.Ho;
+    ps.Wd = g.Wo;
+    ps.nr = g.R;
+    ps.ns = g.S;
+    ps.step = 1;
+    if (mode == CONV_FWD) {
+        ps.Hv = g.Ho;
+        ps.Wv = g.Wo;
+        ps.os = 1;
+        ps.ss = g.stride;
+        ps.offh = ps.offw = -g.pad;
+        ps.sgn = 1;
+        return run_bf16_pass(src, B, bias, Y, g, ps, accumulate, stats, bm, bn, st);
+    }
+    if (stats) return hipErrorInvalidValue;
+    ps.ss = 1;
+    ps.sgn = -1;
+    if (g.stride == 1) {
+        ps.Hv = g.Ho;
+        ps.Wv = g.Wo;
+        ps.os = 1;
+        ps.offh = ps.offw = g.pad;
+        return run_bf16_pass(src, B, bias, Y, g, ps, accumulate, nullptr, bm, bn, st);
+    }
+    // stride 2: one pass per parity class of the dX pixels
+    ps.os = 2;
+    ps.step = 2;
+    ps.shift = 1;
+    for (int a = 0; a < 2; ++a)
+        for (int b = 0; b < 2; ++b) {
+            BfPass q = ps;
+            q.oa = a;
+            q.ob = b;
+            q.Hv = (g.Ho - a + 1) / 2;
+            q.Wv = (g.Wo - b + 1) / 2;
+            q.r0 = (a + g.pad) & 1;
+            q.s0 = (b + g.pad) & 1;
+            q.nr = q.r0 < g.R ? (g.R - q.r0 + 1) / 2 : 0;
+            q.ns = q.s0 < g.S ? (g.S - q.s0 + 1) / 2 : 0;
+            q.offh = a + g.pad;
+            q.offw = b + g.pad;
+            int qbm, qbn;
+            pick_bf16((long)g.Nb * q.Hv * q.Wv, g.Ncols, qbm, qbn);
+            const hipError_t e = run_bf16_pass(src, B, nullptr, Y, g, q, accumulate, nullptr, qbm, qbn, st);
+            if (e != hipSuccess) return e;
+        }
+    return hipSuccess;
+}
+
+// ------------------------------------------------------------------------
+// weight gradient
+// ------------------------------------------------------------------------
+
+struct WgB {
+    int Nb, Hi, Wi, Cs, Ho, Wo, Cout, S, stride, pad, Ktot;
+    long P;        // output pixels N*Ho*Wo
+    int pps;       // pixels per split (multiple of 32)
+};
+
+// part[split][cout][col], col = (r*S + s)*Cs + c, over the split's pixels.
+// Operand loads: pixel pairs (2q, 2q + 1) of the K-step, q = e & 15, with
+// 8-channel chunk e >> 4 (A: output channels, B: columns).
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void wgrad_bf16_k(const bf16* __restrict__ dY, const bf16* __restrict__ X,
+                                                    float* __restrict__ part, WgB g) {
+    constexpr int TM = BM / 32, TN = BN / 32;
+    constexpr int P = kBfPitch;
+    constexpr int STAGE = (BM + BN) * P;
+    constexpr int AE = (BM * 2 + 255) / 256, BE = (BN * 2 + 255) / 256;
+    __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int n0 = blockIdx.x * BN;               // first column
+    const int m0 = blockIdx.y * BM;               // first output channel
+    const long p_lo = (long)blockIdx.z * g.pps;
+    const long p_hi = min(g.P, p_lo + g.pps);
+    const int nks = (int)((p_hi - p_lo + 31) / 32);
+    const int pq = tid & 15;
+
+    // per load slot: A channel offset, B column tap offsets and channel
+    int a_c[AE];
+    bool a_ok[AE];
+    int b_r[BE], b_s[BE], b_c[BE];
+    bool b_ok[BE];
+#pragma unroll
+    for (int u = 0; u < AE; ++u) {
+        const int e = tid + 256 * u;
+        a_c[u] = m0 + (e >> 4) * 8;
+        a_ok[u] = e < BM * 2 && a_c[u] < g.Cout;
+    }
+#pragma unroll
+    for (int u = 0; u < BE; ++u) {
+        const int e = tid + 256 * u;
+        const int col = n0 + (e >> 4) * 8;
+        b_ok[u] = e < BN * 2 && col < g.Ktot;
+        const int tap = col / g.Cs;
+        b_c[u] = col - tap * g.Cs;
+        b_r[u] = tap / g.S;
+        b_s[u] = tap - (tap / g.S) * g.S;
+    }
+
+    uint4 ra[AE][2], rb[BE][2];
+    auto load = [&](int ks) {
+        int img[2], oh[2], ow[2];
+        bool pv[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const long p = p_lo + (long)ks * 32 + 2 * pq + h;
+            pv[h] = p < p_hi;
+            const long pp = pv[h] ? p : p_lo;
+            ow[h] = (int)(pp % g.Wo);
+            const long t = pp / g.Wo;
+            oh[h] = (int)(t % g.Ho);
+            img[h] = (int)(t / g.Ho);
+#pragma unroll
+            for (int u = 0; u < AE; ++u)
+                ra[u][h] = (pv[h] && a_ok[u]) ? *(const uint4*)(dY + pp * g.Cout + a_c[u]) : uint4{0, 0, 0, 0};
+#pragma unroll
+            for (int u = 0; u < BE; ++u) {
+                const int hh = oh[h] * g.stride - g.pad + b_r[u], ww = ow[h] * g.stride - g.pad + b_s[u];
+                const bool ok = pv[h] && b_ok[u] && hh >= 0 && hh < g.Hi && ww >= 0 && ww < g.Wi;
+                rb[u][h] = ok ? *(const uint4*)(X + ((long)(img[h] * g.Hi + hh) * g.Wi + ww) * g.Cs + b_c[u])
+                              : uint4{0, 0, 0, 0};
+            }
+        }
+    };
+    // element i of an 8-channel chunk of pixels (2q, 2q+1) -> one 32-bit word
+    // of row (chunk*8 + i), columns 2q, 2q+1
+    auto put = [&](bf16* base, int e, const uint4& v0, const uint4& v1) {
+        const uint32_t* w0 = (const uint32_t*)&v0;
+        const uint32_t* w1 = (const uint32_t*)&v1;
+        bf16* rowp = base + ((e >> 4) * 8) * P + 2 * pq;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t x0 = w0[i >> 1], x1 = w1[i >> 1];
+            const uint32_t word = (i & 1) ? ((x0 >> 16) | (x1 & 0xffff0000u)) : ((x0 & 0xffffu) | (x1 << 16));
+            *(uint32_t*)(rowp + i * P) = word;
+        }
+    };
+    auto store = [&](int buf) {
+        bf16* As = lds + buf * STAGE;
+        bf16* Bs = As + BM * P;
+#pragma unroll
+        for (int u = 0; u < AE; ++u)
+            if (tid + 256 * u < BM * 2) put(As, tid + 256 * u, ra[u][0], ra[u][1]);
+#pragma unroll
+        for (int u = 0; u < BE; ++u)
+            if (tid + 256 * u < BN * 2) put(Bs, tid + 256 * u, rb[u][0], rb[u][1]);
+    };
+
+    f4 acc[TM][TN];
+#pragma unroll
+    for (int x = 0; x < TM; ++x)
+#pragma unroll
+        for (int y = 0; y < TN; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
+    if (nks > 0) {
+        load(0);
+        store(0);
+    }
+    __syncthreads();
+    for (int ks = 0; ks < nks; ++ks) {
+        const int cur = ks & 1;
+        if (ks + 1 < nks) load(ks + 1);
+        const bf16* As = lds + cur * STAGE;
+        const bf16* Bs = As + BM * P;
+        bf8 a[TM], b[TN];
+#pragma unroll
+        for (int x = 0; x < TM; ++x) a[x] = *(const bf8*)(As + ((wm * TM + x) * 16 + (lane & 15)) * P + (lane >> 4) * 8);
+#pragma unroll
+        for (int y = 0; y < TN; ++y) b[y] = *(const bf8*)(Bs + ((wn * TN + y) * 16 + (lane & 15)) * P + (lane >> 4) * 8);
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int y = 0; y < TN; ++y) acc[x][y] = mfma_bf16(a[x], b[y], acc[x][y]);
+        if (ks + 1 < nks) store(cur ^ 1);
+        __syncthreads();
+    }
+    float* out = part + (long)blockIdx.z * g.Cout * g.Ktot;
+#pragma unroll
+    for (int x = 0; x < TM; ++x)
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            const int col = n0 + (wn * TN + y) * 16 + (lane & 15);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int row = m0 + (wm * TM + x) * 16 + (lane >> 4) * 4 + i;
+                if (row < g.Cout && col < g.Ktot) out[(long)row * g.Ktot + col] = acc[x][y][i];
+            }
+        }
+}
+
+// Tiles of 128 (64 when narrower) output channels x 128 columns; about 512
+// workgroups per pass, each over at least 512 pixels.
+WgradPlan wgrad_plan_bf16(int Nb, int Ho, int Wo, int Cin_p, int Cout, int R, int S) {
+    WgradPlan p{};
+    const long M = (long)Nb * Ho * Wo;
+    const int Ktot = R * S * Cin_p;
+    p.tm = Cout >= 128 ? 128 : 64;
+    p.tn = Ktot >= 128 ? 128 : 64;
+    const long tiles = (long)((Cout + p.tm - 1) / p.tm) * ((Ktot + p.tn - 1) / p.tn);
+    long splits = (512 + tiles - 1) / tiles;
+    const long max_splits = (M + 511) / 512;
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    long pps = (M + splits - 1) / splits;
+    pps = (pps + 31) / 32 * 32;
+    p.pix_per_split = (int)pps;
+    p.splits = (int)((M + pps - 1) / pps);
+    p.part_floats = (long)p.splits * Cout * Ktot;
+    return p;
+}
+
+template <int BM, int BN>
+static hipError_t launch_wg_bf16(const bf16* dY, const bf16* X, float* part, const WgB& a, int splits,
+                                 hipStream_t st) {
+    dim3 grid((unsigned)((a.Ktot + BN - 1) / BN), (unsigned)((a.Cout + BM - 1) / BM), (unsigned)splits);
+    hipLaunchKernelGGL((wgrad_bf16_k<BM, BN>), grid, dim3(256), 0, st, dY, X, part, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_wgrad_bf16(const bf16* dY, const bf16* X, float* part, int Nb, int Hi, int Wi, int Cin_p,
+                                  int Ho, int Wo, int Cout, int R, int S, int stride, int pad, const WgradPlan& p,
+                                  hipStream_t st) {
+    if (Cin_p % 8 || Cout % 8) return hipErrorInvalidValue;
+    const WgB a{Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, S, stride, pad, R * S * Cin_p, (long)Nb * Ho * Wo,
+                p.pix_per_split};
+    if (p.tm == 128 && p.tn == 128) return launch_wg_bf16<128, 128>(dY, X, part, a, p.splits, st);
+    if (p.tm == 128) return launch_wg_bf16<128, 64>(dY, X, part, a, p.splits, st);
+    if (p.tn == 128) return launch_wg_bf16<64, 128>(dY, X, part, a, p.splits, st);
+    return launch_wg_bf16<64, 64>(dY, X, part, a, p.splits, st);
+}
+
+}  // namespace lpp

@@ -1,10 +1,16 @@
 // kernels.h -- launchers of the gfx950 kernels used by the runtime.
 // Every launcher enqueues on `st` and returns hipGetLastError() of the launch.
+// Launchers that take `int dt` read and write activations stored as DT_F32
+// (float) or DT_BF16 (bfloat16 bit patterns, act.h) through void pointers;
+// parameters, gradients, batch-norm statistics and the head's features and
+// logits are always float32.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <cstdint>
 
 namespace lpp {
+
+enum DType { DT_F32 = 0, DT_BF16 = 1 };
 
 // Geometry of an implicit-GEMM convolution pass.
 //   forward : output pixels (Nb, Ho, Wo) x Ncols = Cout, source = conv input
@@ -65,13 +71,30 @@ hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int N
 hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
                                float* g, hipStream_t st);
 
+// ---- bf16 convolution passes (conv_bf16.hip): bf16 source, weights and
+// output, float32 accumulation; geometry as for the float32 passes.  The
+// forward epilogue's batch-norm sums describe the stored (rounded) output;
+// partials come per row tile of conv_bf16_tile_rows(g) rows.  Cs and Ncols
+// must be multiples of 8; data gradients of stride 1 or 2.
+hipError_t launch_conv_bf16(int mode, const uint16_t* src, const uint16_t* B, const float* bias, uint16_t* Y,
+                            const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st);
+int conv_bf16_tile_rows(const ConvGeom& g);
+bool conv_bf16_supported(int mode, const ConvGeom& g);
+// weight gradient from bf16 dY and X into float32 partials part[split][Cout]
+// [R*S*Cin_p] (summed by launch_wgrad_reduce); plan.tm / plan.tn hold the
+// tile's output channels and columns
+WgradPlan wgrad_plan_bf16(int Nb, int Ho, int Wo, int Cin_p, int Cout, int R, int S);
+hipError_t launch_conv_wgrad_bf16(const uint16_t* dY, const uint16_t* X, float* part, int Nb, int Hi, int Wi,
+                                  int Cin_p, int Ho, int Wo, int Cout, int R, int S, int stride, int pad,
+                                  const WgradPlan& p, hipStream_t st);
+
 // ---- batch-norm statistics over [M][C] NHWC rows ----
 constexpr int kStatRows = 256;   // rows per tile of the stand-alone kernels
 int stats_tiles(long M);
 // per tile of kStatRows rows: mean and sum of squared deviations per channel
 // into p0 / p1 [T][C], or the tile's share of the batch sums added into
 // acc [2][kAccSlots][C] (sum x, sum x^2)
-hipError_t launch_stats_partial(const float* x, long M, int C, const BnSums& out, hipStream_t st);
+hipError_t launch_stats_partial(int dt, const void* x, long M, int C, const BnSums& out, hipStream_t st);
 // merges T tiles of R rows (fp64, fixed order) into aux = [mean | rstd |
 // scale | shift]: rstd = 1/sqrt(var + eps) with the biased variance,
 // scale = gamma*rstd, shift = beta - mean*scale
@@ -95,21 +118,21 @@ struct BnFwd {
 };
 // y = relu?(bn1(x1) [+ r | + bn2(x2)])  (r: residual tensor; x2: a second
 // normalised input, used when both branches of a residual add end in BN)
-hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const float* x2, const BnFwd* b2,
-                         bool relu, float* y, long M, int C, hipStream_t st);
+hipError_t launch_bn_act(int dt, const void* x1, const BnFwd& b1, const void* r, const void* x2, const BnFwd* b2,
+                         bool relu, void* y, long M, int C, hipStream_t st);
 
 // ---- batch-norm backward (with the group's ReLU mask and residual fan-out) ----
 struct BnBwdArgs {
-    const float* dy;                                   // gradient at the group output
-    const float* mask;                                 // ReLU output (g = dy where > 0) or null
-    const float* x1; const float* mean1; const float* rstd1;   // BN input and statistics
-    const float* x2; const float* mean2; const float* rstd2;   // second BN of a dual group, or null
+    const void* dy;                                    // gradient at the group output
+    const void* mask;                                  // ReLU output (g = dy where > 0) or null
+    const void* x1; const float* mean1; const float* rstd1;    // BN input and statistics
+    const void* x2; const float* mean2; const float* rstd2;    // second BN of a dual group, or null
     long M;
     int C;
 };
 // per tile of kStatRows rows, the tile's sum g, sum g*xhat1 and sum g*xhat2
 // added into acc [3][kAccSlots][C], or written to p0..p2 [T][C]
-hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, const BnSums& out, hipStream_t st);
+hipError_t launch_bn_bwd_reduce(int dt, const BnBwdArgs& a, const BnSums& out, hipStream_t st);
 // fixed-order merge of T tile partials: gg/gb (dgamma, dbeta; null = not
 // wanted) and coef = [gamma*rstd | mean g | mean g*xhat] per channel; the
 // second set for a dual group (coef2 null if not)
@@ -131,31 +154,32 @@ struct BnBwdCoef {
 };
 // dx = a*(g - mean g - xhat*mean g*xhat) into dx1 / dx2 (null = skip), and g
 // into dres (the residual branch) -- each written or accumulated
-hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const BnBwdCoef& k, float* dx1, bool acc1, float* dx2, bool acc2,
-                               float* dres, bool accres, hipStream_t st);
+hipError_t launch_bn_bwd_apply(int dt, const BnBwdArgs& a, const BnBwdCoef& k, void* dx1, bool acc1, void* dx2,
+                               bool acc2, void* dres, bool accres, hipStream_t st);
 
 // ---- fused classifier head: global average pool, linear, softmax CE ----
-hipError_t launch_head_fwd(const float* x, int Nb, int HW, int C, const float* W, const float* b, int O,
+hipError_t launch_head_fwd(int dt, const void* x, int Nb, int HW, int C, const float* W, const float* b, int O,
                            const StepArgs* args, float* feat, float* logits, float* dz, float* loss_per,
                            hipStream_t st);
 // gW/gb (null: only the loss) and the batch-mean loss
 hipError_t launch_head_bwd_w(const float* dz, const float* feat, int Nb, int C, int O, float* gW, float* gb,
                              const float* loss_per, float* loss, hipStream_t st);
-hipError_t launch_head_bwd_x(const float* dz, const float* W, int Nb, int HW, int C, int O, float* dx, bool acc,
-                             hipStream_t st);
+hipError_t launch_head_bwd_x(int dt, const float* dz, const float* W, int Nb, int HW, int C, int O, void* dx,
+                             bool acc, hipStream_t st);
 
 // elementwise (n multiple of 4)
-hipError_t launch_relu_fwd(const float* x, float* y, long n, hipStream_t st);
-hipError_t launch_relu_bwd(const float* dy, const float* x, float* dx, long n, bool accumulate, hipStream_t st);
-hipError_t launch_add_fwd(const float* a, const float* b, float* y, long n, hipStream_t st);
-hipError_t launch_copy_acc(const float* src, float* dst, long n, bool accumulate, hipStream_t st);
+hipError_t launch_relu_fwd(int dt, const void* x, void* y, long n, hipStream_t st);
+hipError_t launch_relu_bwd(int dt, const void* dy, const void* x, void* dx, long n, bool accumulate, hipStream_t st);
+hipError_t launch_add_fwd(int dt, const void* a, const void* b, void* y, long n, hipStream_t st);
+hipError_t launch_copy_acc(int dt, const void* src, void* dst, long n, bool accumulate, hipStream_t st);
 
-hipError_t launch_maxpool_fwd(const float* x, float* y, uint8_t* arg, int Nb, int H, int W, int C, int Ho, int Wo,
-                              int k, int stride, int pad, hipStream_t st);
-hipError_t launch_maxpool_bwd(const float* dy, const uint8_t* arg, float* dx, int Nb, int H, int W, int C, int Ho,
-                              int Wo, int k, int stride, int pad, bool accumulate, hipStream_t st);
-hipError_t launch_gap_fwd(const float* x, float* y, int Nb, int HW, int C, hipStream_t st);
-hipError_t launch_gap_bwd(const float* dy, float* dx, int Nb, int HW, int C, bool accumulate, hipStream_t st);
+hipError_t launch_maxpool_fwd(int dt, const void* x, void* y, uint8_t* arg, int Nb, int H, int W, int C, int Ho,
+                              int Wo, int k, int stride, int pad, hipStream_t st);
+hipError_t launch_maxpool_bwd(int dt, const void* dy, const uint8_t* arg, void* dx, int Nb, int H, int W, int C,
+                              int Ho, int Wo, int k, int stride, int pad, bool accumulate, hipStream_t st);
+// pooled features are float32
+hipError_t launch_gap_fwd(int dt, const void* x, float* y, int Nb, int HW, int C, hipStream_t st);
+hipError_t launch_gap_bwd(int dt, const float* dy, void* dx, int Nb, int HW, int C, bool accumulate, hipStream_t st);
 hipError_t launch_linear_fwd(const float* x, const float* W, const float* b, float* y, int Nb, int I, int O,
                              hipStream_t st);
 hipError_t launch_linear_bwd_w(const float* dz, const float* x, float* gW, float* gb, int Nb, int I, int O,
@@ -169,17 +193,20 @@ hipError_t launch_softmax_ce(const float* z, const StepArgs* args, float* dz, fl
 
 // the step's NCHW images (C channels) -> NHWC (Cp >= C channels, zero-padded);
 // also zeroes the step's n_zero reduction accumulators at zero
-hipError_t launch_nchw_to_nhwc(const StepArgs* args, float* dst, int Nb, int C, int H, int W, int Cp, double* zero,
-                               long n_zero, hipStream_t st);
-// NHWC (Cp) -> NCHW (C), for inspection
-hipError_t launch_nhwc_to_nchw(const float* src, float* dst, int Nb, int C, int H, int W, int Cp, hipStream_t st);
+hipError_t launch_nchw_to_nhwc(int dt, const StepArgs* args, void* dst, int Nb, int C, int H, int W, int Cp,
+                               double* zero, long n_zero, hipStream_t st);
+// NHWC (Cp) -> NCHW (C) float32, for inspection
+hipError_t launch_nhwc_to_nchw(int dt, const void* src, float* dst, int Nb, int C, int H, int W, int Cp,
+                               hipStream_t st);
 
 // Snapshot of the shared replica (Alg. 1: lock-free read of every entry):
 // v[e] = x[e] for e < d, and each conv weight also into its forward layout
-// W_f[cout][r][s][cin_p] and dgrad layout W_d[cin][r][s][cout].
+// W_f[cout][r][s][cin_p] and dgrad layout W_d[cin][r][s][cout], stored in
+// the activation type (the bf16 cast of the mixed-precision workloads);
+// dst_f / dst_d count elements of that type.
 struct SnapConv { long src, n; int cout, cin, cin_p, R, S; long dst_f, dst_d; };
-hipError_t launch_snapshot(const float* x, float* v, long d, const SnapConv* convs_dev, int n_convs, float* wbase,
-                           hipStream_t st);
+hipError_t launch_snapshot(int dt, const float* x, float* v, long d, const SnapConv* convs_dev, int n_convs,
+                           void* wbase, hipStream_t st);
 
 // Block update (Alg. 1 updater's last step), e in [lo, hi):
 //   m = mu*m + g + wd*x; x -= lr*m   (m == null: x -= lr*(g + wd*x))

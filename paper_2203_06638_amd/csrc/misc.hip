@@ -1,17 +1,19 @@
-// misc_f32.hip -- the non-convolution kernels of the step: batch-norm
+// misc.hip -- the non-convolution kernels of the step: batch-norm
 // statistics / apply / backward, ReLU, residual add, max pool, global
 // average pool, the linear head, softmax cross-entropy, layout conversions,
 // the replica snapshot, the block SGD update and replica averaging.
 //
-// Activations are NHWC float32.  Batch-norm reductions are merged across
-// workgroups by fp64 atomic adds into per-channel accumulators (bnacc.h);
-// every other reduction runs in a fixed order.
+// Activations are NHWC, stored as float32 or bfloat16 (act.h); every kernel
+// that touches them is a template over the storage type and computes in
+// float32.  Batch-norm reductions are merged across workgroups either in a
+// fixed order (partials and a finalize kernel) or by fp64 atomic adds into
+// per-channel accumulators (bnacc.h); every other reduction runs in a fixed
+// order.
+#include "act.h"
 #include "bnacc.h"
 #include "kernels.h"
 
 namespace lpp {
-
-typedef float f4 __attribute__((ext_vector_type(4)));
 
 static inline unsigned nblocks(long n, int per) { return (unsigned)((n + per - 1) / per); }
 
@@ -30,7 +32,8 @@ __device__ __forceinline__ void quad_layout(int C4, int qbase, int& nq, int& rl)
     rl = 256 / nq;
 }
 
-__global__ __launch_bounds__(256) void stats_partial_k(const float* __restrict__ x, long M, int C, BnSums out) {
+template <class T>
+__global__ __launch_bounds__(256) void stats_partial_k(const T* __restrict__ x, long M, int C, BnSums out) {
     __shared__ f4 red[256];
     __shared__ float mean_s[1024];
     const int tid = threadIdx.x;
@@ -45,7 +48,7 @@ __global__ __launch_bounds__(256) void stats_partial_k(const float* __restrict__
         const bool act = lr < rl;
         f4 s = f4{0.f, 0.f, 0.f, 0.f};
         if (act)
-            for (long r = r0 + lr; r < r1; r += rl) s += *(const f4*)(x + r * C + q * 4);
+            for (long r = r0 + lr; r < r1; r += rl) s += ld4(x, r * C4 + q);
         red[tid] = s;
         __syncthreads();
         if (tid < nq) {
@@ -60,7 +63,7 @@ __global__ __launch_bounds__(256) void stats_partial_k(const float* __restrict__
         f4 v = f4{0.f, 0.f, 0.f, 0.f};
         if (act)
             for (long r = r0 + lr; r < r1; r += rl) {
-                const f4 d = *(const f4*)(x + r * C + q * 4) - mu;
+                const f4 d = ld4(x, r * C4 + q) - mu;
                 v += d * d;
             }
         __syncthreads();
@@ -119,8 +122,11 @@ hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C
     return hipGetLastError();
 }
 
-hipError_t launch_stats_partial(const float* x, long M, int C, const BnSums& out, hipStream_t st) {
-    hipLaunchKernelGGL(stats_partial_k, dim3(stats_tiles(M)), dim3(256), 0, st, x, M, C, out);
+hipError_t launch_stats_partial(int dt, const void* x, long M, int C, const BnSums& out, hipStream_t st) {
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(stats_partial_k<bf16>, dim3(stats_tiles(M)), dim3(256), 0, st, (const bf16*)x, M, C, out);
+    else
+        hipLaunchKernelGGL(stats_partial_k<float>, dim3(stats_tiles(M)), dim3(256), 0, st, (const float*)x, M, C, out);
     return hipGetLastError();
 }
 
@@ -169,9 +175,9 @@ hipError_t launch_stats_finalize(const float* pmean, const float* pm2, int T, in
 // Each thread takes E quads (i = blockIdx.x * 256 E + u * 256 + tid) and
 // issues their loads before the workgroup derives the batch-norm
 // coefficients into LDS, so the two latencies overlap.
-template <int RES, bool RELU, int E>
-__global__ __launch_bounds__(256) void bn_act_k(const f4* __restrict__ x1, BnFwd b1, const f4* __restrict__ r,
-                                                const f4* __restrict__ x2, BnFwd b2, f4* __restrict__ y, long n4,
+template <class T, int RES, bool RELU, int E>
+__global__ __launch_bounds__(256) void bn_act_k(const T* __restrict__ x1, BnFwd b1, const T* __restrict__ r,
+                                                const T* __restrict__ x2, BnFwd b2, T* __restrict__ y, long n4,
                                                 int C) {
     extern __shared__ float co[];   // scale1 | shift1 | scale2 | shift2
     const long i0 = (long)blockIdx.x * 256 * E + threadIdx.x;
@@ -180,9 +186,9 @@ __global__ __launch_bounds__(256) void bn_act_k(const f4* __restrict__ x1, BnFwd
     for (int u = 0; u < E; ++u) {
         const long i = i0 + u * 256;
         if (i < n4) {
-            xa[u] = x1[i];
-            if (RES == 1) xb[u] = r[i];
-            if (RES == 2) xb[u] = x2[i];
+            xa[u] = ld4(x1, i);
+            if (RES == 1) xb[u] = ld4(r, i);
+            if (RES == 2) xb[u] = ld4(x2, i);
         }
     }
     bn_fwd_coeffs(b1, C, co, co + C);
@@ -201,7 +207,7 @@ __global__ __launch_bounds__(256) void bn_act_k(const f4* __restrict__ x1, BnFwd
 #pragma unroll
             for (int k = 0; k < 4; ++k) o[k] = o[k] > 0.f ? o[k] : 0.f;
         }
-        y[i] = o;
+        st4(y, i, o);
     }
 }
 
@@ -213,8 +219,9 @@ static unsigned ew_grid(long n4) {
     return (unsigned)(b < 8192 ? (b < 1 ? 1 : b) : 8192);
 }
 
-hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const float* x2, const BnFwd* b2,
-                         bool relu, float* y, long M, int C, hipStream_t st) {
+template <class T>
+static hipError_t bn_act_t(const T* x1, const BnFwd& b1, const T* r, const T* x2, const BnFwd* b2, bool relu, T* y,
+                           long M, int C, hipStream_t st) {
     if (C % 4) return hipErrorInvalidValue;
     const long n4 = M * C / 4;
     const int res = r ? 1 : (x2 ? 2 : 0);
@@ -224,8 +231,7 @@ hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const
     const int E = bn_quads_per_thread(n4);
     const unsigned grid = (unsigned)((n4 + 256L * E - 1) / (256L * E));
 #define BNACT(RS, RL, EE)                                                                                \
-    hipLaunchKernelGGL((bn_act_k<RS, RL, EE>), dim3(grid), dim3(256), lds, st, (const f4*)x1, b1,        \
-                       (const f4*)r, (const f4*)x2, bb, (f4*)y, n4, C)
+    hipLaunchKernelGGL((bn_act_k<T, RS, RL, EE>), dim3(grid), dim3(256), lds, st, x1, b1, r, x2, bb, y, n4, C)
 #define BNACT_E(RS, RL) \
     do { if (E == 4) BNACT(RS, RL, 4); else if (E == 2) BNACT(RS, RL, 2); else BNACT(RS, RL, 1); } while (0)
     if (res == 0) { if (relu) BNACT_E(0, true); else BNACT_E(0, false); }
@@ -234,6 +240,13 @@ hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const
 #undef BNACT_E
 #undef BNACT
     return hipGetLastError();
+}
+
+hipError_t launch_bn_act(int dt, const void* x1, const BnFwd& b1, const void* r, const void* x2, const BnFwd* b2,
+                         bool relu, void* y, long M, int C, hipStream_t st) {
+    if (dt == DT_BF16)
+        return bn_act_t((const bf16*)x1, b1, (const bf16*)r, (const bf16*)x2, b2, relu, (bf16*)y, M, C, st);
+    return bn_act_t((const float*)x1, b1, (const float*)r, (const float*)x2, b2, relu, (float*)y, M, C, st);
 }
 
 // ------------------------------------------------------------------------
@@ -247,8 +260,12 @@ hipError_t launch_bn_act(const float* x1, const BnFwd& b1, const float* r, const
 // each thread's rows are loaded four at a time before use, the row lanes
 // meet in a fixed-shape LDS tree, and lane 0 of each quad adds the tile's
 // sums to the accumulators.
-template <bool MASK, bool DUAL>
+template <class T, bool MASK, bool DUAL>
 __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, BnSums out) {
+    const T* __restrict__ dy = (const T*)a.dy;
+    const T* __restrict__ mask = (const T*)a.mask;
+    const T* __restrict__ x1 = (const T*)a.x1;
+    const T* __restrict__ x2 = (const T*)a.x2;
     __shared__ f4 red[3][256];
     const int tid = threadIdx.x;
     const int C = a.C, C4 = C >> 2;
@@ -271,11 +288,11 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, BnSums out) 
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const long r = rb + (long)k * rl;
-                    const long o = (r < r1 ? r : r0) * C + q * 4;
-                    gv[k] = *(const f4*)(a.dy + o);
-                    if (MASK) yv[k] = *(const f4*)(a.mask + o);
-                    xv[k] = *(const f4*)(a.x1 + o);
-                    if (DUAL) x2v[k] = *(const f4*)(a.x2 + o);
+                    const long o = (r < r1 ? r : r0) * C4 + q;
+                    gv[k] = ld4(dy, o);
+                    if (MASK) yv[k] = ld4(mask, o);
+                    xv[k] = ld4(x1, o);
+                    if (DUAL) x2v[k] = ld4(x2, o);
                 }
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
@@ -332,9 +349,9 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, BnSums out) 
 // derives per channel a = gamma*rstd, mean g, mean g*xhat (and the second
 // set) from the accumulated sums, plus mean and rstd, into LDS; the first
 // workgroup stores dgamma and dbeta.
-template <bool MASK, int E>
-__global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, float* __restrict__ dx1, int acc1,
-                                                      float* __restrict__ dx2, int acc2, float* __restrict__ dres,
+template <class T, bool MASK, int E>
+__global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, T* __restrict__ dx1, int acc1,
+                                                      T* __restrict__ dx2, int acc2, T* __restrict__ dres,
                                                       int accres) {
     extern __shared__ float cf[];   // a1 | mg | mgx1 | mean1 | rstd1 | a2 | mgx2 | mean2 | rstd2
     const int C = a.C;
@@ -346,10 +363,10 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, 
     for (int u = 0; u < E; ++u) {
         const long i = i0 + u * 256;
         if (i < n4) {
-            gv[u] = ((const f4*)a.dy)[i];
-            if (MASK) yv[u] = ((const f4*)a.mask)[i];
-            if (dx1) x1v[u] = ((const f4*)a.x1)[i];
-            if (dx2) x2v[u] = ((const f4*)a.x2)[i];
+            gv[u] = ld4((const T*)a.dy, i);
+            if (MASK) yv[u] = ld4((const T*)a.mask, i);
+            if (dx1) x1v[u] = ld4((const T*)a.x1, i);
+            if (dx2) x2v[u] = ld4((const T*)a.x2, i);
         }
     }
     if (k.acc) {
@@ -407,27 +424,33 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, 
             const f4 xh = (x1v[u] - *(const f4*)(cf + 3 * C + c)) * *(const f4*)(cf + 4 * C + c);
             const f4 v = *(const f4*)(cf + c) *
                          (g - *(const f4*)(cf + C + c) - xh * *(const f4*)(cf + 2 * C + c));
-            ((f4*)dx1)[i] = acc1 ? ((f4*)dx1)[i] + v : v;
+            st4(dx1, i, acc1 ? ld4(dx1, i) + v : v);
         }
         if (dx2) {
             const f4 xh = (x2v[u] - *(const f4*)(cf + 7 * C + c)) * *(const f4*)(cf + 8 * C + c);
             const f4 v = *(const f4*)(cf + 5 * C + c) *
                          (g - *(const f4*)(cf + C + c) - xh * *(const f4*)(cf + 6 * C + c));
-            ((f4*)dx2)[i] = acc2 ? ((f4*)dx2)[i] + v : v;
+            st4(dx2, i, acc2 ? ld4(dx2, i) + v : v);
         }
-        if (dres) ((f4*)dres)[i] = accres ? ((f4*)dres)[i] + g : g;
+        if (dres) st4(dres, i, accres ? ld4(dres, i) + g : g);
     }
 }
 
-hipError_t launch_bn_bwd_reduce(const BnBwdArgs& a, const BnSums& out, hipStream_t st) {
+template <class T>
+static void bn_bwd_reduce_t(const BnBwdArgs& a, const BnSums& out, hipStream_t st) {
     const dim3 grid(stats_tiles(a.M));
     if (a.mask) {
-        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<true, true>), grid, dim3(256), 0, st, a, out);
-        else hipLaunchKernelGGL((bn_bwd_reduce_k<true, false>), grid, dim3(256), 0, st, a, out);
+        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<T, true, true>), grid, dim3(256), 0, st, a, out);
+        else hipLaunchKernelGGL((bn_bwd_reduce_k<T, true, false>), grid, dim3(256), 0, st, a, out);
     } else {
-        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<false, true>), grid, dim3(256), 0, st, a, out);
-        else hipLaunchKernelGGL((bn_bwd_reduce_k<false, false>), grid, dim3(256), 0, st, a, out);
+        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<T, false, true>), grid, dim3(256), 0, st, a, out);
+        else hipLaunchKernelGGL((bn_bwd_reduce_k<T, false, false>), grid, dim3(256), 0, st, a, out);
     }
+}
+
+hipError_t launch_bn_bwd_reduce(int dt, const BnBwdArgs& a, const BnSums& out, hipStream_t st) {
+    if (dt == DT_BF16) bn_bwd_reduce_t<bf16>(a, out, st);
+    else bn_bwd_reduce_t<float>(a, out, st);
     return hipGetLastError();
 }
 
@@ -476,8 +499,9 @@ hipError_t launch_bn_bwd_finalize(const float* p0, const float* p1, const float*
 }
 
 
-hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const BnBwdCoef& k, float* dx1, bool acc1, float* dx2, bool acc2,
-                               float* dres, bool accres, hipStream_t st) {
+template <class T>
+static hipError_t bn_bwd_apply_t(const BnBwdArgs& a, const BnBwdCoef& k, T* dx1, bool acc1, T* dx2, bool acc2,
+                                 T* dres, bool accres, hipStream_t st) {
     if (a.C % 4) return hipErrorInvalidValue;
     if ((dx1 || dx2) && !k.acc && !k.coef1) return hipErrorInvalidValue;
     if (dx2 && !k.acc && !k.coef2) return hipErrorInvalidValue;
@@ -487,7 +511,7 @@ hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const BnBwdCoef& k, float* dx
     const unsigned grid = (dx1 || dx2 || dres) ? (unsigned)((n4 + 256L * E - 1) / (256L * E)) : 1u;
     const size_t lds = sizeof(float) * 9 * a.C;
 #define BNBA(MK, EE)                                                                                         \
-    hipLaunchKernelGGL((bn_bwd_apply_k<MK, EE>), dim3(grid), dim3(256), lds, st, a, k, dx1, (int)acc1, dx2, \
+    hipLaunchKernelGGL((bn_bwd_apply_k<T, MK, EE>), dim3(grid), dim3(256), lds, st, a, k, dx1, (int)acc1, dx2, \
                        (int)acc2, dres, (int)accres)
 #define BNBA_E(MK) \
     do { if (E == 4) BNBA(MK, 4); else if (E == 2) BNBA(MK, 2); else BNBA(MK, 1); } while (0)
@@ -498,57 +522,83 @@ hipError_t launch_bn_bwd_apply(const BnBwdArgs& a, const BnBwdCoef& k, float* dx
     return hipGetLastError();
 }
 
+hipError_t launch_bn_bwd_apply(int dt, const BnBwdArgs& a, const BnBwdCoef& k, void* dx1, bool acc1, void* dx2,
+                               bool acc2, void* dres, bool accres, hipStream_t st) {
+    if (dt == DT_BF16)
+        return bn_bwd_apply_t(a, k, (bf16*)dx1, acc1, (bf16*)dx2, acc2, (bf16*)dres, accres, st);
+    return bn_bwd_apply_t(a, k, (float*)dx1, acc1, (float*)dx2, acc2, (float*)dres, accres, st);
+}
+
 // ------------------------------------------------------------------------
 // elementwise (unfused per-layer mode)
 // ------------------------------------------------------------------------
 
-__global__ void relu_fwd_k(const f4* __restrict__ x, f4* __restrict__ y, long n4) {
+template <class T>
+__global__ void relu_fwd_k(const T* __restrict__ x, T* __restrict__ y, long n4) {
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
-        f4 v = x[i];
+        f4 v = ld4(x, i);
 #pragma unroll
         for (int k = 0; k < 4; ++k) v[k] = v[k] > 0.f ? v[k] : 0.f;
-        y[i] = v;
+        st4(y, i, v);
     }
 }
 
-__global__ void relu_bwd_k(const f4* __restrict__ dy, const f4* __restrict__ x, f4* __restrict__ dx, long n4,
-                           int acc) {
+template <class T>
+__global__ void relu_bwd_k(const T* __restrict__ dy, const T* __restrict__ x, T* __restrict__ dx, long n4, int acc) {
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
-        f4 g = dy[i], v = x[i];
-        f4 o = acc ? dx[i] : f4{0.f, 0.f, 0.f, 0.f};
+        const f4 g = ld4(dy, i), v = ld4(x, i);
+        f4 o = acc ? ld4(dx, i) : f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int k = 0; k < 4; ++k) o[k] += v[k] > 0.f ? g[k] : 0.f;
-        dx[i] = o;
+        st4(dx, i, o);
     }
 }
 
-__global__ void add_fwd_k(const f4* __restrict__ a, const f4* __restrict__ b, f4* __restrict__ y, long n4) {
+template <class T>
+__global__ void add_fwd_k(const T* __restrict__ a, const T* __restrict__ b, T* __restrict__ y, long n4) {
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x)
-        y[i] = a[i] + b[i];
+        st4(y, i, ld4(a, i) + ld4(b, i));
 }
 
-__global__ void copy_acc_k(const f4* __restrict__ s, f4* __restrict__ d, long n4, int acc) {
+template <class T>
+__global__ void copy_acc_k(const T* __restrict__ s, T* __restrict__ d, long n4, int acc) {
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x)
-        d[i] = acc ? d[i] + s[i] : s[i];
+        st4(d, i, acc ? ld4(d, i) + ld4(s, i) : ld4(s, i));
 }
 
-hipError_t launch_relu_fwd(const float* x, float* y, long n, hipStream_t st) {
-    hipLaunchKernelGGL(relu_fwd_k, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const f4*)x, (f4*)y, n / 4);
+hipError_t launch_relu_fwd(int dt, const void* x, void* y, long n, hipStream_t st) {
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(relu_fwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)x, (bf16*)y, n / 4);
+    else
+        hipLaunchKernelGGL(relu_fwd_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)x, (float*)y,
+                           n / 4);
     return hipGetLastError();
 }
-hipError_t launch_relu_bwd(const float* dy, const float* x, float* dx, long n, bool accumulate, hipStream_t st) {
-    hipLaunchKernelGGL(relu_bwd_k, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const f4*)dy, (const f4*)x, (f4*)dx,
-                       n / 4, (int)accumulate);
+hipError_t launch_relu_bwd(int dt, const void* dy, const void* x, void* dx, long n, bool accumulate, hipStream_t st) {
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(relu_bwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)dy, (const bf16*)x,
+                           (bf16*)dx, n / 4, (int)accumulate);
+    else
+        hipLaunchKernelGGL(relu_bwd_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)dy,
+                           (const float*)x, (float*)dx, n / 4, (int)accumulate);
     return hipGetLastError();
 }
-hipError_t launch_add_fwd(const float* a, const float* b, float* y, long n, hipStream_t st) {
-    hipLaunchKernelGGL(add_fwd_k, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const f4*)a, (const f4*)b, (f4*)y,
-                       n / 4);
+hipError_t launch_add_fwd(int dt, const void* a, const void* b, void* y, long n, hipStream_t st) {
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(add_fwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)a, (const bf16*)b,
+                           (bf16*)y, n / 4);
+    else
+        hipLaunchKernelGGL(add_fwd_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)a,
+                           (const float*)b, (float*)y, n / 4);
     return hipGetLastError();
 }
-hipError_t launch_copy_acc(const float* src, float* dst, long n, bool accumulate, hipStream_t st) {
-    hipLaunchKernelGGL(copy_acc_k, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const f4*)src, (f4*)dst, n / 4,
-                       (int)accumulate);
+hipError_t launch_copy_acc(int dt, const void* src, void* dst, long n, bool accumulate, hipStream_t st) {
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(copy_acc_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)src, (bf16*)dst,
+                           n / 4, (int)accumulate);
+    else
+        hipLaunchKernelGGL(copy_acc_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)src, (float*)dst,
+                           n / 4, (int)accumulate);
     return hipGetLastError();
 }
 
@@ -557,7 +607,8 @@ hipError_t launch_copy_acc(const float* src, float* dst, long n, bool accumulate
 // ------------------------------------------------------------------------
 
 // arg holds the winning tap r*k + s (first maximum in row-major scan order)
-__global__ void maxpool_fwd_k(const float* __restrict__ x, float* __restrict__ y, uint8_t* __restrict__ arg,
+template <class T>
+__global__ void maxpool_fwd_k(const T* __restrict__ x, T* __restrict__ y, uint8_t* __restrict__ arg,
                               int Nb, int H, int W, int C, int Ho, int Wo, int k, int st, int pad) {
     const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
     const long total = (long)Nb * Ho * Wo * C;
@@ -576,15 +627,16 @@ __global__ void maxpool_fwd_k(const float* __restrict__ x, float* __restrict__ y
         for (int s = 0; s < k; ++s) {
             const int wi = q * st - pad + s;
             if (wi < 0 || wi >= W) continue;
-            const float v = x[(((long)n * H + hi) * W + wi) * C + c];
+            const float v = ld1(x, (((long)n * H + hi) * W + wi) * C + c);
             if (v > m) { m = v; am = r * k + s; }
         }
     }
-    y[idx] = m;
+    st1(y, idx, m);
     arg[idx] = (uint8_t)am;
 }
 
-__global__ void maxpool_bwd_k(const float* __restrict__ dy, const uint8_t* __restrict__ arg, float* __restrict__ dx,
+template <class T>
+__global__ void maxpool_bwd_k(const T* __restrict__ dy, const uint8_t* __restrict__ arg, T* __restrict__ dx,
                               int Nb, int H, int W, int C, int Ho, int Wo, int k, int st, int pad, int acc) {
     const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
     const long total = (long)Nb * H * W * C;
@@ -604,50 +656,67 @@ __global__ void maxpool_bwd_k(const float* __restrict__ dy, const uint8_t* __res
             const int r = h - (p * st - pad), ss = w - (q * st - pad);
             if (r < 0 || r >= k || ss < 0 || ss >= k) continue;
             const long o = (((long)n * Ho + p) * Wo + q) * C + c;
-            if (arg[o] == r * k + ss) s += dy[o];
+            if (arg[o] == r * k + ss) s += ld1(dy, o);
         }
-    dx[idx] = acc ? dx[idx] + s : s;
+    st1(dx, idx, acc ? ld1(dx, idx) + s : s);
 }
 
-__global__ void gap_fwd_k(const float* __restrict__ x, float* __restrict__ y, int Nb, int HW, int C) {
+template <class T>
+__global__ void gap_fwd_k(const T* __restrict__ x, float* __restrict__ y, int Nb, int HW, int C) {
     const int idx = blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= Nb * C) return;
     const int n = idx / C, c = idx - n * C;
     float s = 0.f;
-    for (int e = 0; e < HW; ++e) s += x[((long)n * HW + e) * C + c];
+    for (int e = 0; e < HW; ++e) s += ld1(x, ((long)n * HW + e) * C + c);
     y[idx] = s / (float)HW;
 }
 
-__global__ void gap_bwd_k(const float* __restrict__ dy, float* __restrict__ dx, int Nb, int HW, int C, int acc) {
+template <class T>
+__global__ void gap_bwd_k(const float* __restrict__ dy, T* __restrict__ dx, int Nb, int HW, int C, int acc) {
     const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= (long)Nb * HW * C) return;
     const int c = (int)(idx % C);
     const int n = (int)(idx / ((long)HW * C));
     const float v = dy[n * C + c] / (float)HW;
-    dx[idx] = acc ? dx[idx] + v : v;
+    st1(dx, idx, acc ? ld1(dx, idx) + v : v);
 }
 
-hipError_t launch_maxpool_fwd(const float* x, float* y, uint8_t* arg, int Nb, int H, int W, int C, int Ho, int Wo,
-                              int k, int stride, int pad, hipStream_t st) {
-    const long total = (long)Nb * Ho * Wo * C;
-    hipLaunchKernelGGL(maxpool_fwd_k, dim3(nblocks(total, 256)), dim3(256), 0, st, x, y, arg, Nb, H, W, C, Ho, Wo, k,
-                       stride, pad);
+hipError_t launch_maxpool_fwd(int dt, const void* x, void* y, uint8_t* arg, int Nb, int H, int W, int C, int Ho,
+                              int Wo, int k, int stride, int pad, hipStream_t st) {
+    const dim3 grid(nblocks((long)Nb * Ho * Wo * C, 256));
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(maxpool_fwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)x, (bf16*)y, arg, Nb, H, W, C,
+                           Ho, Wo, k, stride, pad);
+    else
+        hipLaunchKernelGGL(maxpool_fwd_k<float>, grid, dim3(256), 0, st, (const float*)x, (float*)y, arg, Nb, H, W, C,
+                           Ho, Wo, k, stride, pad);
     return hipGetLastError();
 }
-hipError_t launch_maxpool_bwd(const float* dy, const uint8_t* arg, float* dx, int Nb, int H, int W, int C, int Ho,
-                              int Wo, int k, int stride, int pad, bool accumulate, hipStream_t st) {
-    const long total = (long)Nb * H * W * C;
-    hipLaunchKernelGGL(maxpool_bwd_k, dim3(nblocks(total, 256)), dim3(256), 0, st, dy, arg, dx, Nb, H, W, C, Ho, Wo,
-                       k, stride, pad, (int)accumulate);
+hipError_t launch_maxpool_bwd(int dt, const void* dy, const uint8_t* arg, void* dx, int Nb, int H, int W, int C,
+                              int Ho, int Wo, int k, int stride, int pad, bool accumulate, hipStream_t st) {
+    const dim3 grid(nblocks((long)Nb * H * W * C, 256));
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(maxpool_bwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)dy, arg, (bf16*)dx, Nb, H, W, C,
+                           Ho, Wo, k, stride, pad, (int)accumulate);
+    else
+        hipLaunchKernelGGL(maxpool_bwd_k<float>, grid, dim3(256), 0, st, (const float*)dy, arg, (float*)dx, Nb, H, W,
+                           C, Ho, Wo, k, stride, pad, (int)accumulate);
     return hipGetLastError();
 }
-hipError_t launch_gap_fwd(const float* x, float* y, int Nb, int HW, int C, hipStream_t st) {
-    hipLaunchKernelGGL(gap_fwd_k, dim3(nblocks((long)Nb * C, 256)), dim3(256), 0, st, x, y, Nb, HW, C);
+hipError_t launch_gap_fwd(int dt, const void* x, float* y, int Nb, int HW, int C, hipStream_t st) {
+    const dim3 grid(nblocks((long)Nb * C, 256));
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(gap_fwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)x, y, Nb, HW, C);
+    else
+        hipLaunchKernelGGL(gap_fwd_k<float>, grid, dim3(256), 0, st, (const float*)x, y, Nb, HW, C);
     return hipGetLastError();
 }
-hipError_t launch_gap_bwd(const float* dy, float* dx, int Nb, int HW, int C, bool accumulate, hipStream_t st) {
-    hipLaunchKernelGGL(gap_bwd_k, dim3(nblocks((long)Nb * HW * C, 256)), dim3(256), 0, st, dy, dx, Nb, HW, C,
-                       (int)accumulate);
+hipError_t launch_gap_bwd(int dt, const float* dy, void* dx, int Nb, int HW, int C, bool accumulate, hipStream_t st) {
+    const dim3 grid(nblocks((long)Nb * HW * C, 256));
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(gap_bwd_k<bf16>, grid, dim3(256), 0, st, dy, (bf16*)dx, Nb, HW, C, (int)accumulate);
+    else
+        hipLaunchKernelGGL(gap_bwd_k<float>, grid, dim3(256), 0, st, dy, (float*)dx, Nb, HW, C, (int)accumulate);
     return hipGetLastError();
 }
 
@@ -722,7 +791,8 @@ __global__ void loss_mean_k(const float* __restrict__ loss_per, int Nb, float* _
 // dz = (softmax - onehot)/N and the sample's loss.  Reductions over classes
 // run as fixed-shape trees in LDS.
 constexpr int kHeadMaxC = 2048, kHeadMaxO = 4096;
-__global__ __launch_bounds__(256) void head_fwd_k(const float* __restrict__ x, int Nb, int HW, int C,
+template <class T>
+__global__ __launch_bounds__(256) void head_fwd_k(const T* __restrict__ x, int Nb, int HW, int C,
                                                   const float* __restrict__ W, const float* __restrict__ b, int O,
                                                   const StepArgs* __restrict__ args, float* __restrict__ feat,
                                                   float* __restrict__ logits, float* __restrict__ dz,
@@ -733,7 +803,7 @@ __global__ __launch_bounds__(256) void head_fwd_k(const float* __restrict__ x, i
     const int n = blockIdx.x, t = threadIdx.x;
     for (int c = t; c < C; c += 256) {
         float s = 0.f;
-        for (int e = 0; e < HW; ++e) s += x[((long)n * HW + e) * C + c];
+        for (int e = 0; e < HW; ++e) s += ld1(x, ((long)n * HW + e) * C + c);
         const float f = s / (float)HW;
         f_s[c] = f;
         feat[(long)n * C + c] = f;
@@ -797,8 +867,9 @@ __global__ void head_bwd_w_k(const float* __restrict__ dz, const float* __restri
 }
 
 // one workgroup per sample: df = (dz W) / HW, broadcast over the HW pixels
+template <class T>
 __global__ __launch_bounds__(256) void head_bwd_x_k(const float* __restrict__ dz, const float* __restrict__ W,
-                                                    int Nb, int HW, int C, int O, float* __restrict__ dx, int acc) {
+                                                    int Nb, int HW, int C, int O, T* __restrict__ dx, int acc) {
     __shared__ float df[kHeadMaxC];
     const int n = blockIdx.x, t = threadIdx.x;
     for (int c = t; c < C; c += 256) {
@@ -808,20 +879,24 @@ __global__ __launch_bounds__(256) void head_bwd_x_k(const float* __restrict__ dz
     }
     __syncthreads();
     const int C4 = C >> 2;
-    f4* out = (f4*)(dx + (long)n * HW * C);
+    T* out = dx + (long)n * HW * C;
     for (int i = t; i < HW * C4; i += 256) {
         const int c = (i % C4) * 4;
         const f4 v = f4{df[c], df[c + 1], df[c + 2], df[c + 3]};
-        out[i] = acc ? out[i] + v : v;
+        st4(out, i, acc ? ld4(out, i) + v : v);
     }
 }
 
-hipError_t launch_head_fwd(const float* x, int Nb, int HW, int C, const float* W, const float* b, int O,
+hipError_t launch_head_fwd(int dt, const void* x, int Nb, int HW, int C, const float* W, const float* b, int O,
                            const StepArgs* args, float* feat, float* logits, float* dz, float* loss_per,
                            hipStream_t st) {
     if (C > kHeadMaxC || O > kHeadMaxO) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(head_fwd_k, dim3(Nb), dim3(256), 0, st, x, Nb, HW, C, W, b, O, args, feat, logits, dz,
-                       loss_per);
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(head_fwd_k<bf16>, dim3(Nb), dim3(256), 0, st, (const bf16*)x, Nb, HW, C, W, b, O, args,
+                           feat, logits, dz, loss_per);
+    else
+        hipLaunchKernelGGL(head_fwd_k<float>, dim3(Nb), dim3(256), 0, st, (const float*)x, Nb, HW, C, W, b, O, args,
+                           feat, logits, dz, loss_per);
     return hipGetLastError();
 }
 hipError_t launch_head_bwd_w(const float* dz, const float* feat, int Nb, int C, int O, float* gW, float* gb,
@@ -831,10 +906,14 @@ hipError_t launch_head_bwd_w(const float* dz, const float* feat, int Nb, int C, 
                        loss);
     return hipGetLastError();
 }
-hipError_t launch_head_bwd_x(const float* dz, const float* W, int Nb, int HW, int C, int O, float* dx, bool acc,
-                             hipStream_t st) {
+hipError_t launch_head_bwd_x(int dt, const float* dz, const float* W, int Nb, int HW, int C, int O, void* dx,
+                             bool acc, hipStream_t st) {
     if (C > kHeadMaxC) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(head_bwd_x_k, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, dx, (int)acc);
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(head_bwd_x_k<bf16>, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, (bf16*)dx, (int)acc);
+    else
+        hipLaunchKernelGGL(head_bwd_x_k<float>, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, (float*)dx,
+                           (int)acc);
     return hipGetLastError();
 }
 
@@ -867,8 +946,9 @@ hipError_t launch_softmax_ce(const float* z, const StepArgs* args, float* dz, fl
 // layouts
 // ------------------------------------------------------------------------
 
-__global__ void nchw_to_nhwc_k(const StepArgs* __restrict__ args, float* __restrict__ d, int Nb, int C, int H,
-                               int W, int Cp, double* __restrict__ zero, long n_zero) {
+template <class T>
+__global__ void nchw_to_nhwc_k(const StepArgs* __restrict__ args, T* __restrict__ d, int Nb, int C, int H, int W,
+                               int Cp, double* __restrict__ zero, long n_zero) {
     const float* __restrict__ s = args->images;
     const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
     for (long z = idx; z < n_zero; z += (long)gridDim.x * blockDim.x) zero[z] = 0.0;
@@ -880,11 +960,11 @@ __global__ void nchw_to_nhwc_k(const StepArgs* __restrict__ args, float* __restr
     const long t = pix / W;
     const int h = (int)(t % H);
     const int n = (int)(t / H);
-    d[idx] = c < C ? s[(((long)n * C + c) * H + h) * W + w] : 0.f;
+    st1(d, idx, c < C ? s[(((long)n * C + c) * H + h) * W + w] : 0.f);
 }
 
-__global__ void nhwc_to_nchw_k(const float* __restrict__ s, float* __restrict__ d, int Nb, int C, int H, int W,
-                               int Cp) {
+template <class T>
+__global__ void nhwc_to_nchw_k(const T* __restrict__ s, float* __restrict__ d, int Nb, int C, int H, int W, int Cp) {
     const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
     const long total = (long)Nb * C * H * W;
     if (idx >= total) return;
@@ -894,19 +974,27 @@ __global__ void nhwc_to_nchw_k(const float* __restrict__ s, float* __restrict__ 
     t /= H;
     const int c = (int)(t % C);
     const int n = (int)(t / C);
-    d[idx] = s[(((long)n * H + h) * W + w) * Cp + c];
+    d[idx] = ld1(s, (((long)n * H + h) * W + w) * Cp + c);
 }
 
-hipError_t launch_nchw_to_nhwc(const StepArgs* args, float* dst, int Nb, int C, int H, int W, int Cp, double* zero,
-                               long n_zero, hipStream_t st) {
-    const long total = (long)Nb * H * W * Cp;
-    hipLaunchKernelGGL(nchw_to_nhwc_k, dim3(nblocks(total, 256)), dim3(256), 0, st, args, dst, Nb, C, H, W, Cp,
-                       zero, n_zero);
+hipError_t launch_nchw_to_nhwc(int dt, const StepArgs* args, void* dst, int Nb, int C, int H, int W, int Cp,
+                               double* zero, long n_zero, hipStream_t st) {
+    const dim3 grid(nblocks((long)Nb * H * W * Cp, 256));
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(nchw_to_nhwc_k<bf16>, grid, dim3(256), 0, st, args, (bf16*)dst, Nb, C, H, W, Cp, zero,
+                           n_zero);
+    else
+        hipLaunchKernelGGL(nchw_to_nhwc_k<float>, grid, dim3(256), 0, st, args, (float*)dst, Nb, C, H, W, Cp, zero,
+                           n_zero);
     return hipGetLastError();
 }
-hipError_t launch_nhwc_to_nchw(const float* src, float* dst, int Nb, int C, int H, int W, int Cp, hipStream_t st) {
-    const long total = (long)Nb * H * W * C;
-    hipLaunchKernelGGL(nhwc_to_nchw_k, dim3(nblocks(total, 256)), dim3(256), 0, st, src, dst, Nb, C, H, W, Cp);
+hipError_t launch_nhwc_to_nchw(int dt, const void* src, float* dst, int Nb, int C, int H, int W, int Cp,
+                               hipStream_t st) {
+    const dim3 grid(nblocks((long)Nb * H * W * C, 256));
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(nhwc_to_nchw_k<bf16>, grid, dim3(256), 0, st, (const bf16*)src, dst, Nb, C, H, W, Cp);
+    else
+        hipLaunchKernelGGL(nhwc_to_nchw_k<float>, grid, dim3(256), 0, st, (const float*)src, dst, Nb, C, H, W, Cp);
     return hipGetLastError();
 }
 
@@ -927,8 +1015,9 @@ hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* l
 // snapshot, block update, averaging
 // ------------------------------------------------------------------------
 
+template <class T>
 __global__ void snapshot_k(const float* __restrict__ x, float* __restrict__ v, long d,
-                           const SnapConv* __restrict__ convs, int nc, float* __restrict__ wbase) {
+                           const SnapConv* __restrict__ convs, int nc, T* __restrict__ wbase) {
     for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < d; e += (long)gridDim.x * blockDim.x) {
         const float val = x[e];
         v[e] = val;
@@ -948,16 +1037,21 @@ __global__ void snapshot_k(const float* __restrict__ x, float* __restrict__ v, l
         t /= cv.R;
         const int c = (int)(t % cv.cin);
         const int k = (int)(t / cv.cin);
-        wbase[cv.dst_f + (((long)k * cv.R + r) * cv.S + s) * cv.cin_p + c] = val;
-        wbase[cv.dst_d + (((long)c * cv.R + r) * cv.S + s) * cv.cout + k] = val;
+        st1(wbase, cv.dst_f + (((long)k * cv.R + r) * cv.S + s) * cv.cin_p + c, val);
+        st1(wbase, cv.dst_d + (((long)c * cv.R + r) * cv.S + s) * cv.cout + k, val);
     }
 }
 
-hipError_t launch_snapshot(const float* x, float* v, long d, const SnapConv* convs_dev, int n_convs, float* wbase,
-                           hipStream_t st) {
+hipError_t launch_snapshot(int dt, const float* x, float* v, long d, const SnapConv* convs_dev, int n_convs,
+                           void* wbase, hipStream_t st) {
     long b = (d + 255) / 256;
     if (b > 16384) b = 16384;
-    hipLaunchKernelGGL(snapshot_k, dim3((unsigned)b), dim3(256), 0, st, x, v, d, convs_dev, n_convs, wbase);
+    if (dt == DT_BF16)
+        hipLaunchKernelGGL(snapshot_k<bf16>, dim3((unsigned)b), dim3(256), 0, st, x, v, d, convs_dev, n_convs,
+                           (bf16*)wbase);
+    else
+        hipLaunchKernelGGL(snapshot_k<float>, dim3((unsigned)b), dim3(256), 0, st, x, v, d, convs_dev, n_convs,
+                           (float*)wbase);
     return hipGetLastError();
 }
 

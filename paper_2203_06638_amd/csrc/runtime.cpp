@@ -44,10 +44,11 @@ struct Shape {
 struct Layer {
     lpp_layer L{};
     Shape in0, in1, out;
+    int dt = lpp::DT_F32;         // storage type of this layer's output and its gradient
     long poff = -1, np = 0;       // canonical parameter range
     long wcount = 0;              // conv/linear weight count (before the bias)
     int cin_p = 0;                // conv: stored channels of the input
-    long wf_off = -1, wd_off = -1;// conv: W_f / W_d in the worker's weight buffer (floats)
+    long wf_off = -1, wd_off = -1;// conv: W_f / W_d in the worker's weight buffer (elements)
     double macs = 0;              // forward multiply-adds (conv, linear)
     lpp::WgradPlan wg{};
     // workspace offsets (bytes) of this layer's output, its gradient and aux
@@ -83,6 +84,7 @@ struct Group {
 struct Model {
     lpp_model_desc desc{};
     std::vector<Layer> layers;
+    int dt = lpp::DT_F32;         // activation storage type (bf16 for LPP_BF16)
     int P = 0;
     long d = 0;
     std::vector<long> blo, bhi;   // block ranges 0..P
@@ -96,6 +98,8 @@ struct Model {
 };
 
 int ceil4(int c) { return (c + 3) / 4 * 4; }
+int ceil8(int c) { return (c + 7) / 8 * 8; }
+size_t dt_size(int dt) { return dt == lpp::DT_BF16 ? 2 : 4; }
 
 // Validates the description and fills shapes, parameter layout, blocks and
 // plans.  Returns LPP_OK or an error code with g_err set.
@@ -107,14 +111,15 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
     if (D.batch < 1 || D.in_c < 1 || D.in_h < 1 || D.in_w < 1 || D.n_classes < 1)
         return fail(LPP_EINVAL, "batch, image shape and n_classes must be positive");
     if (D.dtype != LPP_FP32 && D.dtype != LPP_BF16) return fail(LPP_EINVAL, "unknown dtype");
-    if (D.dtype == LPP_BF16) return fail(LPP_EUNSUPPORTED, "bf16 activations are not built yet");
     if (!(D.bn_eps > 0.f) || !std::isfinite(D.bn_eps)) return fail(LPP_EINVAL, "bn_eps must be positive");
     if (!(D.momentum >= 0.f) || !std::isfinite(D.momentum) || !std::isfinite(D.weight_decay))
         return fail(LPP_EINVAL, "momentum must be >= 0 and finite; weight_decay finite");
     M.desc = D;
     M.desc.layers = nullptr;
     M.P = P;
-    M.img_cp = ceil4(D.in_c);
+    M.dt = D.dtype == LPP_BF16 ? lpp::DT_BF16 : lpp::DT_F32;
+    const bool bf = M.dt == lpp::DT_BF16;
+    M.img_cp = bf ? ceil8(D.in_c) : ceil4(D.in_c);
     const int n = D.n_layers;
     M.layers.assign(n, Layer{});
     const Shape img{D.in_c, D.in_h, D.in_w};
@@ -147,6 +152,10 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
             if (L.cout % 4) return fail(LPP_EUNSUPPORTED, std::string(where) + "cout must be a multiple of 4");
             Y.cin_p = L.in0 < 0 ? M.img_cp : L.cin;
             if (Y.cin_p % 4) return fail(LPP_EUNSUPPORTED, std::string(where) + "cin must be a multiple of 4");
+            if (bf && (Y.cin_p % 8 || L.cout % 8))
+                return fail(LPP_EUNSUPPORTED, std::string(where) + "bf16 convs need cin and cout multiples of 8");
+            if (bf && L.in0 >= 0 && L.stride > 2)
+                return fail(LPP_EUNSUPPORTED, std::string(where) + "bf16 data gradients need stride 1 or 2");
             Y.wcount = (long)L.cout * L.cin * L.k * L.k;
             Y.np = Y.wcount + (L.bias ? L.cout : 0);
             Y.macs = (double)D.batch * o.h * o.w * L.cout * (double)L.cin * L.k * L.k;
@@ -181,6 +190,8 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
             if (Y.in0.h != 1 || Y.in0.w != 1)
                 return fail(LPP_EUNSUPPORTED, std::string(where) + "linear input must be 1x1 (pool first)");
             if (L.cin != Y.in0.c || L.cout < 1) return fail(LPP_EINVAL, std::string(where) + "bad linear shape");
+            if (bf && (L.in0 < 0 || D.layers[L.in0].op != LPP_GAP))
+                return fail(LPP_EUNSUPPORTED, std::string(where) + "with bf16 a linear layer must read a pool");
             o.c = L.cout;
             Y.wcount = (long)L.cout * L.cin;
             Y.np = Y.wcount + (L.bias ? L.cout : 0);
@@ -190,6 +201,7 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
             return fail(LPP_EINVAL, std::string(where) + "unknown op");
         }
         Y.out = o;
+        Y.dt = (L.op == LPP_GAP || L.op == LPP_LINEAR) ? lpp::DT_F32 : M.dt;
         if (L.op != LPP_LINEAR && o.c % 4)
             return fail(LPP_EUNSUPPORTED, std::string(where) + "channel counts must be multiples of 4");
         if ((double)D.batch * o.numel() >= 2147483647.0 || (double)D.batch * Y.in0.h * Y.in0.w * ceil4(Y.in0.c) >= 2147483647.0)
@@ -372,11 +384,11 @@ struct Worker {
     bool own_stream = false;
     char* ws = nullptr;
     float* v = nullptr;
-    float* wbuf = nullptr;
+    void* wbuf = nullptr;   // conv weights in the kernels' layouts, activation type
     float* g = nullptr;
     float* m = nullptr;
     float* loss = nullptr;
-    float* img = nullptr;
+    void* img = nullptr;    // the step's images, NHWC, activation type
     float* ps0 = nullptr;   // per-tile partial statistics (3 arrays)
     float* ps1 = nullptr;
     float* ps2 = nullptr;
@@ -412,8 +424,14 @@ struct lpp_ctx {
     Timer timer;
     int device = 0;
 
-    float* act(Worker& w, int l) { return (float*)(w.ws + M.layers[l].act); }
-    float* dact(Worker& w, int l) { return (float*)(w.ws + M.layers[l].dact); }
+    void* act(Worker& w, int l) { return w.ws + M.layers[l].act; }
+    void* dact(Worker& w, int l) { return w.ws + M.layers[l].dact; }
+    // a layer input: the image (l < 0) or a stored layer output
+    const void* input(Worker& w, int l) { return l < 0 ? w.img : act(w, l); }
+    // the weights of conv layer Y in forward / data-gradient layout
+    const void* wf(Worker& w, const Layer& Y) { return (const char*)w.wbuf + Y.wf_off * lpp_dt_size(); }
+    const void* wdg(Worker& w, const Layer& Y) { return (const char*)w.wbuf + Y.wd_off * lpp_dt_size(); }
+    size_t lpp_dt_size() const { return M.dt == lpp::DT_BF16 ? 2 : 4; }
     float* aux(Worker& w, int l) { return (float*)(w.ws + M.layers[l].aux); }
     double* acc_fwd(Worker& w, int l) { return (double*)(w.ws + M.layers[l].acc); }
     double* acc_bwd(Worker& w, int l) {
@@ -501,17 +519,19 @@ int bn_stats_standalone(lpp_ctx* c, Worker& w, int b) {
     Layer& B = M.layers[b];
     const int N = M.desc.batch, C = B.out.c;
     const long rows = (long)N * B.in0.h * B.in0.w;
-    const float* x = c->act(w, B.L.in0);
+    const void* x = c->act(w, B.L.in0);
+    const int dt = M.layers[B.L.in0].dt;
+    const double eb = (double)dt_size(dt);
     hipStream_t st = w.stream;
     if (c->fixed_order) {
         const lpp::BnSums out{nullptr, w.ps0, w.ps1, nullptr};
-        LAUNCH("bn_stats", 4.0 * rows * C, st, lpp::launch_stats_partial(x, rows, C, out, st));
+        LAUNCH("bn_stats", eb * rows * C, st, lpp::launch_stats_partial(dt, x, rows, C, out, st));
         LAUNCH("bn_stats", 0.0, st,
                lpp::launch_stats_finalize(w.ps0, w.ps1, lpp::stats_tiles(rows), lpp::kStatRows, rows, C,
                                           w.v + B.poff, w.v + B.poff + C, M.desc.bn_eps, c->aux(w, b), st));
     } else {
         const lpp::BnSums out{c->acc_fwd(w, b), nullptr, nullptr, nullptr};
-        LAUNCH("bn_stats", 4.0 * rows * C, st, lpp::launch_stats_partial(x, rows, C, out, st));
+        LAUNCH("bn_stats", eb * rows * C, st, lpp::launch_stats_partial(dt, x, rows, C, out, st));
     }
     return LPP_OK;
 }
@@ -521,13 +541,16 @@ int run_forward(lpp_ctx* c, Worker& w) {
     Model& M = c->M;
     const int N = M.desc.batch;
     hipStream_t st = w.stream;
-    LAUNCH("image", 8.0 * N * M.desc.in_c * M.desc.in_h * M.desc.in_w, st,
-           lpp::launch_nchw_to_nhwc(w.args, w.img, N, M.desc.in_c, M.desc.in_h, M.desc.in_w, M.img_cp,
+    const int dt = M.dt;
+    const bool bf = dt == lpp::DT_BF16;
+    const double eb = (double)dt_size(dt);   // bytes per stored activation element
+    LAUNCH("image", (4.0 + eb) * N * M.desc.in_c * M.desc.in_h * M.desc.in_w, st,
+           lpp::launch_nchw_to_nhwc(dt, w.args, w.img, N, M.desc.in_c, M.desc.in_h, M.desc.in_w, M.img_cp,
                                      (double*)(w.ws + c->off_acc), c->n_acc, st));
     bool loss_done = false;
     for (const Group& G : M.groups) {
         Layer& Y = M.layers[G.a];
-        const float* x0 = Y.L.in0 < 0 ? w.img : c->act(w, Y.L.in0);
+        const void* x0 = c->input(w, Y.L.in0);
         const long Mrows = (long)N * Y.in0.h * Y.in0.w;
         switch (G.kind) {
         case G_CONV: {
@@ -536,13 +559,19 @@ int run_forward(lpp_ctx* c, Worker& w) {
             lpp::BnSums sums{};
             if (G.stats_bn >= 0) sums = c->fixed_order ? lpp::BnSums{nullptr, w.ps0, w.ps1, nullptr}
                                                        : lpp::BnSums{c->acc_fwd(w, G.stats_bn), nullptr, nullptr, nullptr};
-            LAUNCH("conv_fwd", 2.0 * Y.macs, st,
-                   lpp::launch_conv_igemm(lpp::CONV_FWD, x0, w.wbuf + Y.wf_off, bias, c->act(w, G.a), g, false,
-                                          G.stats_bn >= 0 ? &sums : nullptr, st));
+            const lpp::BnSums* sp = G.stats_bn >= 0 ? &sums : nullptr;
+            if (bf)
+                LAUNCH("conv_fwd", 2.0 * Y.macs, st,
+                       lpp::launch_conv_bf16(lpp::CONV_FWD, (const uint16_t*)x0, (const uint16_t*)c->wf(w, Y), bias,
+                                             (uint16_t*)c->act(w, G.a), g, false, sp, st));
+            else
+                LAUNCH("conv_fwd", 2.0 * Y.macs, st,
+                       lpp::launch_conv_igemm(lpp::CONV_FWD, (const float*)x0, (const float*)c->wf(w, Y), bias,
+                                              (float*)c->act(w, G.a), g, false, sp, st));
             if (G.stats_bn >= 0 && c->fixed_order) {
                 const Layer& B = M.layers[G.stats_bn];
                 const long rows = (long)N * Y.out.h * Y.out.w;
-                const int R = lpp::conv_tile_rows(g);
+                const int R = bf ? lpp::conv_bf16_tile_rows(g) : lpp::conv_tile_rows(g);
                 const int T = (int)((rows + R - 1) / R);
                 LAUNCH("bn_stats", 0.0, st,
                        lpp::launch_stats_finalize(w.ps0, w.ps1, T, R, rows, Y.L.cout, w.v + B.poff,
@@ -569,44 +598,46 @@ int run_forward(lpp_ctx* c, Worker& w) {
                 b2 = lpp::BnFwd{c->fixed_order ? nullptr : c->acc_fwd(w, G.bn2), w.v + B2.poff, w.v + B2.poff + C,
                                 M.desc.bn_eps, Mrows, c->aux(w, G.bn2)};
             }
-            const float* x2 = G.bn2 >= 0 ? c->act(w, M.layers[G.bn2].L.in0) : nullptr;
-            const float* r = G.res >= 0 ? c->act(w, G.res) : nullptr;
-            const double bytes = 8.0 * Mrows * C + (r || x2 ? 4.0 * Mrows * C : 0.0);
+            const void* x2 = G.bn2 >= 0 ? c->act(w, M.layers[G.bn2].L.in0) : nullptr;
+            const void* r = G.res >= 0 ? c->act(w, G.res) : nullptr;
+            const double bytes = 2.0 * eb * Mrows * C + (r || x2 ? eb * Mrows * C : 0.0);
             LAUNCH("bn_act", bytes, st,
-                   lpp::launch_bn_act(x0, b1, r, x2, G.bn2 >= 0 ? &b2 : nullptr, G.relu >= 0, c->act(w, G.out),
+                   lpp::launch_bn_act(dt, x0, b1, r, x2, G.bn2 >= 0 ? &b2 : nullptr, G.relu >= 0, c->act(w, G.out),
                                       Mrows, C, st));
             break;
         }
         case G_RELU:
-            LAUNCH("relu", 8.0 * Mrows * Y.out.c, st, lpp::launch_relu_fwd(x0, c->act(w, G.a), Mrows * Y.out.c, st));
+            LAUNCH("relu", 2.0 * eb * Mrows * Y.out.c, st,
+                   lpp::launch_relu_fwd(dt, x0, c->act(w, G.a), Mrows * Y.out.c, st));
             break;
         case G_ADD:
-            LAUNCH("add", 12.0 * Mrows * Y.out.c, st,
-                   lpp::launch_add_fwd(x0, c->act(w, Y.L.in1), c->act(w, G.a), Mrows * Y.out.c, st));
+            LAUNCH("add", 3.0 * eb * Mrows * Y.out.c, st,
+                   lpp::launch_add_fwd(dt, x0, c->act(w, Y.L.in1), c->act(w, G.a), Mrows * Y.out.c, st));
             break;
         case G_MAXPOOL:
-            LAUNCH("maxpool", 4.0 * Mrows * Y.out.c, st,
-                   lpp::launch_maxpool_fwd(x0, c->act(w, G.a), (uint8_t*)c->aux(w, G.a), N, Y.in0.h, Y.in0.w,
+            LAUNCH("maxpool", eb * Mrows * Y.out.c, st,
+                   lpp::launch_maxpool_fwd(dt, x0, c->act(w, G.a), (uint8_t*)c->aux(w, G.a), N, Y.in0.h, Y.in0.w,
                                            Y.in0.c, Y.out.h, Y.out.w, Y.L.k, Y.L.stride, Y.L.pad, st));
             break;
         case G_GAP:
-            LAUNCH("gap", 4.0 * Mrows * Y.out.c, st,
-                   lpp::launch_gap_fwd(x0, c->act(w, G.a), N, Y.in0.h * Y.in0.w, Y.in0.c, st));
+            LAUNCH("gap", eb * Mrows * Y.out.c, st,
+                   lpp::launch_gap_fwd(dt, x0, (float*)c->act(w, G.a), N, Y.in0.h * Y.in0.w, Y.in0.c, st));
             break;
         case G_LINEAR: {
             const float* W = w.v + Y.poff;
             const float* bias = Y.L.bias ? W + Y.wcount : nullptr;
             LAUNCH("linear", 2.0 * Y.macs, st,
-                   lpp::launch_linear_fwd(x0, W, bias, c->act(w, G.a), N, Y.L.cin, Y.L.cout, st));
+                   lpp::launch_linear_fwd((const float*)x0, W, bias, (float*)c->act(w, G.a), N, Y.L.cin, Y.L.cout,
+                                          st));
             break;
         }
         case G_HEAD: {
             const Layer& L = M.layers[G.lin];
             const float* W = w.v + L.poff;
-            LAUNCH("head", 4.0 * Mrows * Y.in0.c + 2.0 * L.macs, st,
-                   lpp::launch_head_fwd(x0, N, Y.in0.h * Y.in0.w, Y.in0.c, W, L.L.bias ? W + L.wcount : nullptr,
-                                        L.L.cout, w.args, c->act(w, G.a), c->act(w, G.lin), c->dact(w, G.lin),
-                                        w.loss + 1, st));
+            LAUNCH("head", eb * Mrows * Y.in0.c + 2.0 * L.macs, st,
+                   lpp::launch_head_fwd(dt, x0, N, Y.in0.h * Y.in0.w, Y.in0.c, W, L.L.bias ? W + L.wcount : nullptr,
+                                        L.L.cout, w.args, (float*)c->act(w, G.a), (float*)c->act(w, G.lin),
+                                        (float*)c->dact(w, G.lin), w.loss + 1, st));
             loss_done = true;
             break;
         }
@@ -615,8 +646,8 @@ int run_forward(lpp_ctx* c, Worker& w) {
     if (!loss_done) {
         const int last = (int)M.layers.size() - 1;
         LAUNCH("softmax_ce", 0.0, st,
-               lpp::launch_softmax_ce(c->act(w, last), w.args, c->dact(w, last), w.loss, N, M.desc.n_classes,
-                                      st));
+               lpp::launch_softmax_ce((const float*)c->act(w, last), w.args, (float*)c->dact(w, last), w.loss, N,
+                                      M.desc.n_classes, st));
     }
     return LPP_OK;
 }
@@ -627,23 +658,33 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
     Model& M = c->M;
     const Plan& pl = M.plans[partition];
     const int N = M.desc.batch;
+    const int dt = M.dt;
+    const bool bf = dt == lpp::DT_BF16;
+    const double eb = (double)dt_size(dt);
     hipStream_t st = w.stream;
     bool loss_done = false;
     for (int gi = (int)M.groups.size() - 1; gi >= 0; --gi) {
         const Group& G = M.groups[gi];
         if (!pl.run[G.out]) continue;
         Layer& Y = M.layers[G.a];
-        const float* x0 = Y.L.in0 < 0 ? w.img : c->act(w, Y.L.in0);
-        float* dy = c->dact(w, G.out);
-        float* dx0 = pl.din0[G.a] ? c->dact(w, Y.L.in0) : nullptr;
+        const void* x0 = c->input(w, Y.L.in0);
+        void* dy = c->dact(w, G.out);
+        void* dx0 = pl.din0[G.a] ? c->dact(w, Y.L.in0) : nullptr;
         const long Min = (long)N * Y.in0.h * Y.in0.w;
         switch (G.kind) {
         case G_CONV: {
             if (pl.wgrad[G.a]) {
                 const int Ktot = Y.L.k * Y.L.k * Y.cin_p;
-                LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
-                       lpp::launch_conv_wgrad(dy, x0, w.wpart, N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w,
-                                              Y.L.cout, Y.L.k, Y.L.k, Y.L.stride, Y.L.pad, Y.wg, st));
+                if (bf)
+                    LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
+                           lpp::launch_conv_wgrad_bf16((const uint16_t*)dy, (const uint16_t*)x0, w.wpart, N, Y.in0.h,
+                                                       Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k,
+                                                       Y.L.stride, Y.L.pad, Y.wg, st));
+                else
+                    LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
+                           lpp::launch_conv_wgrad((const float*)dy, (const float*)x0, w.wpart, N, Y.in0.h, Y.in0.w,
+                                                  Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
+                                                  Y.L.pad, Y.wg, st));
                 LAUNCH("wgrad_reduce", 4.0 * Y.wg.part_floats, st,
                        lpp::launch_wgrad_reduce(w.wpart, Y.wg.splits, Y.L.cout, Ktot, Y.L.cin, Y.cin_p, Y.L.k,
                                                 Y.L.k, w.g + Y.poff, st));
@@ -651,7 +692,8 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                     // column sums of dY, from per-tile means
                     const long Mo = (long)N * Y.out.h * Y.out.w;
                     const lpp::BnSums tiles{nullptr, w.ps0, w.ps1, nullptr};
-                    LAUNCH("bias_grad", 4.0 * Mo * Y.L.cout, st, lpp::launch_stats_partial(dy, Mo, Y.L.cout, tiles, st));
+                    LAUNCH("bias_grad", eb * Mo * Y.L.cout, st,
+                           lpp::launch_stats_partial(dt, dy, Mo, Y.L.cout, tiles, st));
                     LAUNCH("bias_grad", 0.0, st,
                            lpp::launch_sum_from_tiles(w.ps0, lpp::stats_tiles(Mo), lpp::kStatRows, Mo, Y.L.cout,
                                                       w.g + Y.poff + Y.wcount, st));
@@ -660,9 +702,14 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
             if (dx0) {
                 lpp::ConvGeom g{N, Y.out.h, Y.out.w, Y.L.cout, Y.in0.h, Y.in0.w, Y.L.cin, Y.L.k, Y.L.k, Y.L.stride,
                                 Y.L.pad};
-                LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
-                       lpp::launch_conv_igemm(lpp::CONV_DGRAD, dy, w.wbuf + Y.wd_off, nullptr, dx0, g,
-                                              pl.acc0[G.a] != 0, nullptr, st));
+                if (bf)
+                    LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
+                           lpp::launch_conv_bf16(lpp::CONV_DGRAD, (const uint16_t*)dy, (const uint16_t*)c->wdg(w, Y),
+                                                 nullptr, (uint16_t*)dx0, g, pl.acc0[G.a] != 0, nullptr, st));
+                else
+                    LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
+                           lpp::launch_conv_igemm(lpp::CONV_DGRAD, (const float*)dy, (const float*)c->wdg(w, Y),
+                                                  nullptr, (float*)dx0, g, pl.acc0[G.a] != 0, nullptr, st));
             }
             break;
         }
@@ -689,10 +736,10 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
             float* gb2 = want2 && pl.wgrad[b2] ? w.g + Y2->poff + C : nullptr;
             lpp::BnBwdCoef k{};
             if (want1 || want2) {
-                const double bytes = (a.mask ? 12.0 : 8.0) * Min * C + (want2 ? 4.0 * Min * C : 0.0);
+                const double bytes = (a.mask ? 3.0 : 2.0) * eb * Min * C + (want2 ? eb * Min * C : 0.0);
                 if (c->fixed_order) {
                     const lpp::BnSums out{nullptr, w.ps0, w.ps1, w.ps2};
-                    LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(a, out, st));
+                    LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(dt, a, out, st));
                     LAUNCH("bn_bwd", 0.0, st,
                            lpp::launch_bn_bwd_finalize(w.ps0, w.ps1, w.ps2, lpp::stats_tiles(Min), Min, C,
                                                        w.v + Y.poff, ax + C, gg1, gb1, ax + 4 * C,
@@ -702,72 +749,76 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                     k.coef2 = want2 ? ax2 + 4 * C : nullptr;
                 } else {
                     const lpp::BnSums out{c->acc_bwd(w, G.a), nullptr, nullptr, nullptr};
-                    LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(a, out, st));
+                    LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(dt, a, out, st));
                     k = lpp::BnBwdCoef{c->acc_bwd(w, G.a), w.v + Y.poff, gg1, gb1,
                                        want2 ? w.v + Y2->poff : nullptr, gg2, gb2, nullptr, nullptr};
                 }
             }
-            float* d1 = want1 && pl.din0[G.a] ? dx0 : nullptr;
-            float* d2 = want2 && pl.din0[b2] ? c->dact(w, Y2->L.in0) : nullptr;
-            float* dr = want_res ? c->dact(w, G.res) : nullptr;
+            void* d1 = want1 && pl.din0[G.a] ? dx0 : nullptr;
+            void* d2 = want2 && pl.din0[b2] ? c->dact(w, Y2->L.in0) : nullptr;
+            void* dr = want_res ? c->dact(w, G.res) : nullptr;
             // (with atomic sums the apply kernel also writes dgamma and dbeta)
             if (d1 || d2 || dr || (k.acc && (gg1 || gb1 || gg2 || gb2))) {
-                const double bytes = ((a.mask ? 8.0 : 4.0) + (d1 ? 12.0 : 0.0) + (d2 ? 12.0 : 0.0) +
-                                      (dr ? (acc_res ? 8.0 : 4.0) : 0.0)) * Min * C;
+                const double bytes = ((a.mask ? 2.0 : 1.0) + (d1 ? 3.0 : 0.0) + (d2 ? 3.0 : 0.0) +
+                                      (dr ? (acc_res ? 2.0 : 1.0) : 0.0)) * eb * Min * C;
                 LAUNCH("bn_bwd", bytes, st,
-                       lpp::launch_bn_bwd_apply(a, k, d1, pl.acc0[G.a] != 0, d2, want2 && pl.acc0[b2] != 0, dr,
+                       lpp::launch_bn_bwd_apply(dt, a, k, d1, pl.acc0[G.a] != 0, d2, want2 && pl.acc0[b2] != 0, dr,
                                                 acc_res, st));
             }
             break;
         }
         case G_RELU:
             if (dx0)
-                LAUNCH("relu", 12.0 * Min * Y.out.c, st,
-                       lpp::launch_relu_bwd(dy, x0, dx0, Min * Y.out.c, pl.acc0[G.a] != 0, st));
+                LAUNCH("relu", 3.0 * eb * Min * Y.out.c, st,
+                       lpp::launch_relu_bwd(dt, dy, x0, dx0, Min * Y.out.c, pl.acc0[G.a] != 0, st));
             break;
         case G_ADD:
             if (dx0)
-                LAUNCH("add", 8.0 * Min * Y.out.c, st,
-                       lpp::launch_copy_acc(dy, dx0, Min * Y.out.c, pl.acc0[G.a] != 0, st));
+                LAUNCH("add", 2.0 * eb * Min * Y.out.c, st,
+                       lpp::launch_copy_acc(dt, dy, dx0, Min * Y.out.c, pl.acc0[G.a] != 0, st));
             if (pl.din1[G.a])
-                LAUNCH("add", 8.0 * Min * Y.out.c, st,
-                       lpp::launch_copy_acc(dy, c->dact(w, Y.L.in1), Min * Y.out.c, pl.acc1[G.a] != 0, st));
+                LAUNCH("add", 2.0 * eb * Min * Y.out.c, st,
+                       lpp::launch_copy_acc(dt, dy, c->dact(w, Y.L.in1), Min * Y.out.c, pl.acc1[G.a] != 0, st));
             break;
         case G_MAXPOOL:
             if (dx0)
-                LAUNCH("maxpool", 8.0 * Min * Y.out.c, st,
-                       lpp::launch_maxpool_bwd(dy, (const uint8_t*)c->aux(w, G.a), dx0, N, Y.in0.h, Y.in0.w,
+                LAUNCH("maxpool", 2.0 * eb * Min * Y.out.c, st,
+                       lpp::launch_maxpool_bwd(dt, dy, (const uint8_t*)c->aux(w, G.a), dx0, N, Y.in0.h, Y.in0.w,
                                                Y.in0.c, Y.out.h, Y.out.w, Y.L.k, Y.L.stride, Y.L.pad,
                                                pl.acc0[G.a] != 0, st));
             break;
         case G_GAP:
             if (dx0)
-                LAUNCH("gap", 4.0 * Min * Y.in0.c, st,
-                       lpp::launch_gap_bwd(dy, dx0, N, Y.in0.h * Y.in0.w, Y.in0.c, pl.acc0[G.a] != 0, st));
+                LAUNCH("gap", eb * Min * Y.in0.c, st,
+                       lpp::launch_gap_bwd(dt, (const float*)dy, dx0, N, Y.in0.h * Y.in0.w, Y.in0.c,
+                                           pl.acc0[G.a] != 0, st));
             break;
         case G_LINEAR: {
             const float* W = w.v + Y.poff;
             if (pl.wgrad[G.a])
                 LAUNCH("linear", 2.0 * Y.macs, st,
-                       lpp::launch_linear_bwd_w(dy, x0, w.g + Y.poff, Y.L.bias ? w.g + Y.poff + Y.wcount : nullptr,
-                                                N, Y.L.cin, Y.L.cout, st));
+                       lpp::launch_linear_bwd_w((const float*)dy, (const float*)x0, w.g + Y.poff,
+                                                Y.L.bias ? w.g + Y.poff + Y.wcount : nullptr, N, Y.L.cin, Y.L.cout,
+                                                st));
             if (dx0)
                 LAUNCH("linear", 2.0 * Y.macs, st,
-                       lpp::launch_linear_bwd_x(dy, W, dx0, N, Y.L.cin, Y.L.cout, pl.acc0[G.a] != 0, st));
+                       lpp::launch_linear_bwd_x((const float*)dy, W, (float*)dx0, N, Y.L.cin, Y.L.cout,
+                                                pl.acc0[G.a] != 0, st));
             break;
         }
         case G_HEAD: {
             const Layer& L = M.layers[G.lin];
             const bool wg = pl.wgrad[G.lin];
             LAUNCH("head", wg ? 2.0 * L.macs : 0.0, st,
-                   lpp::launch_head_bwd_w(dy, c->act(w, G.a), N, L.L.cin, L.L.cout, wg ? w.g + L.poff : nullptr,
+                   lpp::launch_head_bwd_w((const float*)dy, (const float*)c->act(w, G.a), N, L.L.cin, L.L.cout,
+                                          wg ? w.g + L.poff : nullptr,
                                           wg && L.L.bias ? w.g + L.poff + L.wcount : nullptr, w.loss + 1, w.loss,
                                           st));
             loss_done = true;
             if (dx0)
-                LAUNCH("head", 2.0 * L.macs + 4.0 * Min * Y.in0.c, st,
-                       lpp::launch_head_bwd_x(dy, w.v + L.poff, N, Y.in0.h * Y.in0.w, Y.in0.c, L.L.cout, dx0,
-                                              pl.acc0[G.a] != 0, st));
+                LAUNCH("head", 2.0 * L.macs + eb * Min * Y.in0.c, st,
+                       lpp::launch_head_bwd_x(dt, (const float*)dy, w.v + L.poff, N, Y.in0.h * Y.in0.w, Y.in0.c,
+                                              L.L.cout, dx0, pl.acc0[G.a] != 0, st));
             break;
         }
         }
@@ -789,7 +840,8 @@ int enqueue_step(lpp_ctx* c, Worker& w, int worker, int partition) {
     float* xq = c->replicas + (long)q * c->dpad;
     const long d = c->M.d;
     hipStream_t st = w.stream;
-    LAUNCH("snapshot", 8.0 * d, st, lpp::launch_snapshot(xq, w.v, d, c->snap_dev, c->n_snap, w.wbuf, st));
+    LAUNCH("snapshot", 8.0 * d, st,
+           lpp::launch_snapshot(c->M.dt, xq, w.v, d, c->snap_dev, c->n_snap, w.wbuf, st));
     int rc = run_forward(c, w);
     if (rc) return rc;
     rc = run_backward(c, w, partition);
@@ -861,8 +913,9 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         Y.wd_off = wf;
         wf += (nd + 63) / 64 * 64;
         snaps.push_back({Y.poff, Y.np, Y.L.cout, Y.L.cin, Y.cin_p, Y.L.k, Y.L.k, Y.wf_off, Y.wd_off});
-        Y.wg = lpp::wgrad_plan(N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k,
-                               Y.L.stride, Y.L.pad);
+        Y.wg = M.dt == lpp::DT_BF16 ? lpp::wgrad_plan_bf16(N, Y.out.h, Y.out.w, Y.cin_p, Y.L.cout, Y.L.k, Y.L.k)
+                                     : lpp::wgrad_plan(N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout,
+                                                       Y.L.k, Y.L.k, Y.L.stride, Y.L.pad);
     }
     c->wbuf_floats = wf;
     c->n_snap = (int)snaps.size();
@@ -875,19 +928,20 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         return o;
     };
     c->off_v = take(sizeof(float) * c->dpad);
-    c->off_wbuf = take(sizeof(float) * std::max<long>(wf, 1));
+    const size_t eb = dt_size(M.dt);
+    c->off_wbuf = take(eb * std::max<long>(wf, 1));
     c->off_g = take(sizeof(float) * c->dpad);
     c->off_m = take(sizeof(float) * c->dpad);
     c->off_loss = take(sizeof(float) * (1 + N));
     c->off_args = take(sizeof(lpp::StepArgs));
-    c->off_img = take(sizeof(float) * (size_t)N * M.desc.in_h * M.desc.in_w * M.img_cp);
+    c->off_img = take(eb * (size_t)N * M.desc.in_h * M.desc.in_w * M.img_cp);
     long ps = 1, wpart = 1;
     for (int l = 0; l < (int)M.layers.size(); ++l) {
         Layer& Y = M.layers[l];
         const long rows_out = (long)N * Y.out.h * Y.out.w;
         if (M.stored[l]) {
-            Y.act = take(sizeof(float) * (size_t)rows_out * Y.out.c);
-            Y.dact = take(sizeof(float) * (size_t)rows_out * Y.out.c);
+            Y.act = take(dt_size(Y.dt) * (size_t)rows_out * Y.out.c);
+            Y.dact = take(dt_size(Y.dt) * (size_t)rows_out * Y.out.c);
         }
         if (Y.L.op == LPP_BN) Y.aux = take(sizeof(float) * 7 * Y.out.c);
         if (Y.L.op == LPP_MAXPOOL) Y.aux = take((size_t)rows_out * Y.out.c);
@@ -896,7 +950,8 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         if (Y.L.op == LPP_CONV) {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
                             Y.L.pad};
-            const long tiles = (rows_out + lpp::conv_tile_rows(g) - 1) / lpp::conv_tile_rows(g);
+            const int tr = M.dt == lpp::DT_BF16 ? lpp::conv_bf16_tile_rows(g) : lpp::conv_tile_rows(g);
+            const long tiles = (rows_out + tr - 1) / tr;
             ps = std::max<long>(ps, tiles * Y.L.cout);
             ps = std::max<long>(ps, (long)lpp::stats_tiles(rows_out) * Y.L.cout);
             wpart = std::max<long>(wpart, Y.wg.part_floats);
@@ -935,11 +990,11 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
             return fail(LPP_ENOMEM, "worker workspace allocation failed");
         HIPCHK(hipMemset(w.ws, 0, c->ws_bytes));
         w.v = (float*)(w.ws + c->off_v);
-        w.wbuf = (float*)(w.ws + c->off_wbuf);
+        w.wbuf = w.ws + c->off_wbuf;
         w.g = (float*)(w.ws + c->off_g);
         w.m = (float*)(w.ws + c->off_m);
         w.loss = (float*)(w.ws + c->off_loss);
-        w.img = (float*)(w.ws + c->off_img);
+        w.img = w.ws + c->off_img;
         w.ps0 = (float*)(w.ws + c->off_ps);
         w.ps1 = w.ps0 + c->ps_floats;
         w.ps2 = w.ps1 + c->ps_floats;
@@ -1146,15 +1201,15 @@ static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* 
     float* tmp = nullptr;
     if (hipMalloc((void**)&tmp, sizeof(float) * n * (G ? 2 : 1)) != hipSuccess)
         return fail(LPP_ENOMEM, "temporary allocation");
-    const float* src = grad ? c->dact(w, layer) : nullptr;
+    const void* src = grad ? c->dact(w, layer) : nullptr;
     hipError_t e = hipSuccess;
     if (G) {
         const int C = Y.out.c;
         const long rows = (long)N * Y.out.h * Y.out.w;
         const int b = layer == G->bn2 ? G->bn2 : G->a;
         const float* ax = c->aux(w, b);
-        const float* x = c->act(w, M.layers[b].L.in0);
-        const float *r = nullptr, *x2 = nullptr;
+        const void* x = c->act(w, M.layers[b].L.in0);
+        const void *r = nullptr, *x2 = nullptr;
         lpp::BnFwd b2{};
         if (layer == G->add) {
             r = G->res >= 0 ? c->act(w, G->res) : nullptr;
@@ -1165,12 +1220,13 @@ static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* 
         }
         lpp::BnFwd b1{};
         b1.aux = (float*)ax;
-        e = lpp::launch_bn_act(x, b1, r, x2, x2 ? &b2 : nullptr, false, tmp + n, rows, C, w.stream);
+        e = lpp::launch_bn_act(Y.dt, x, b1, r, x2, x2 ? &b2 : nullptr, false, tmp + n, rows, C, w.stream);
         src = tmp + n;
     } else if (!grad) {
         src = c->act(w, layer);
     }
-    if (e == hipSuccess) e = lpp::launch_nhwc_to_nchw(src, tmp, N, Y.out.c, Y.out.h, Y.out.w, Y.out.c, w.stream);
+    if (e == hipSuccess)
+        e = lpp::launch_nhwc_to_nchw(Y.dt, src, tmp, N, Y.out.c, Y.out.h, Y.out.w, Y.out.c, w.stream);
     if (e == hipSuccess) e = hipStreamSynchronize(w.stream);
     if (e == hipSuccess) e = hipMemcpy(host, tmp, sizeof(float) * n, hipMemcpyDeviceToHost);
     hipFree(tmp);
