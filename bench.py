@@ -11,13 +11,20 @@ region (inputs resident in HBM before it starts).
 
 Also reported, on the same JSON line:
   roofline      the dominant kernel family's algorithmic flops per launch
-                over its average launch time, timed with HIP events on its
-                own streams during the timed region, against the fp32
-                matrix peak;
+                over its average launch time (HIP events recorded in the
+                kernels' own dispatch packets, worker 0 alone right after the
+                timed region), against the fp32 matrix peak;
   cpu_baseline  the fp64 oracle's step timed on the host cores on a bounded
                 sample (a baseline, not a target);
   hbm_kernels   the block-update and replica-averaging kernels on 1 GiB-
-                scale buffers, as achieved HBM GB/s.
+                scale buffers, as achieved HBM GB/s;
+  workloads     the other configurations, each on a short run: ResNet-20
+                with 100 classes and K = 4 replicas of P = 4 workers
+                (averaging every 8 steps per replica), WRN-16-8 (bf16
+                activations, fp32 master weights, K = 2, averaging every 4)
+                and ResNet-18 at 224x224 (bf16, K = 2, averaging every 8),
+                with samples/s and their dominant kernel family's fraction
+                of the matrix peak of their dtype.
 """
 from __future__ import annotations
 
@@ -35,6 +42,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "train samples/sec (fwd+partial bwd+update), ResNet-20 b128; MFMA util, HBM GB/s"
 PEAK_FP32_TFLOPS = 157.3
+PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 FAMILIES = ["conv_fwd", "conv_dgrad", "conv_wgrad", "wgrad_reduce", "bn_stats", "bn_act", "bn_bwd", "head",
             "relu", "add", "maxpool", "gap", "linear", "softmax_ce", "bias_grad", "snapshot", "image", "sgd_update"]
@@ -54,6 +62,10 @@ def parse():
                     help="issue steps to only the first n workers (0 = all); for latency studies")
     ap.add_argument("--issue-threads", type=int, default=1,
                     help="host threads issuing steps; each owns a fixed set of workers")
+    ap.add_argument("--no-workloads", action="store_true", help="skip the other configurations")
+    ap.add_argument("--workloads", default="resnet20_100_k4,wrn16_8_bf16,resnet18_bf16",
+                    help="comma-separated subset of the other configurations")
+    ap.add_argument("--workload-steps", type=int, default=64)
     return ap.parse_args()
 
 
@@ -95,6 +107,93 @@ def hbm_kernels(torch, lpp):
     del x, y, g
     torch.cuda.empty_cache()
     return out
+
+
+# the other configurations: (model builder, input shape, classes, dtype, K, H)
+def _workloads():
+    from paper_2203_06638_amd import models as PM
+    from paper_2203_06638_amd import lpp
+    return {
+        "resnet20_100_k4": (lambda: PM.resnet20(100), (3, 32, 32), 100, lpp.FP32, 4, 8,
+                            "ResNet-20 (100 classes), batch 128, fp32, K=4 replicas x P=4 workers on 16 HIP "
+                            "streams, averaging every 8 steps per replica, momentum 0.9, async"),
+        "wrn16_8_bf16": (lambda: PM.wrn16_8(100), (3, 32, 32), 100, lpp.BF16, 2, 4,
+                         "WRN-16-8 (100 classes), batch 128, bf16 activations / fp32 master weights, K=2 x P=4 "
+                         "workers on 8 HIP streams, averaging every 4 steps per replica, momentum 0.9, async"),
+        "resnet18_bf16": (lambda: PM.resnet18(1000), (3, 224, 224), 1000, lpp.BF16, 2, 8,
+                          "ResNet-18 (1000 classes), batch 128 of 3x224x224, bf16 activations / fp32 master "
+                          "weights, K=2 x P=4 workers on 8 HIP streams, averaging every 8 steps per replica, "
+                          "momentum 0.9, async"),
+    }
+
+
+def run_workload(torch, lpp, name, steps, B=128, P=4):
+    """Short async run of one configuration: warm-up (graphs captured),
+    then `steps` worker steps issued round-robin over the K*P workers with
+    an averaging round whenever every replica has advanced H steps; then
+    the kernel families on worker 0 alone."""
+    import synth
+    build, shape, ncls, dtype, K, H, desc = _workloads()[name]
+    model = build()
+    info = lpp.describe(model, B, dtype=dtype)
+    pool = []
+    for b in range(4):
+        img = synth.images(200 + b, B, *shape)
+        if dtype == lpp.BF16:
+            img = synth.round_to_bf16(img)
+        pool.append((torch.from_numpy(img).cuda(), torch.from_numpy(synth.labels(200 + b, B, ncls)).cuda()))
+    streams = [torch.cuda.Stream() for _ in range(K * P)]
+    ctx = lpp.Context(model, K=K, batch=B, mode=lpp.ASYNC, dtype=dtype, momentum=0.9, streams=streams,
+                      avg_stream=torch.cuda.Stream())
+    ctx.set_params(synth.init_params(model.specs, 2))
+    nw = K * P
+
+    def issue(n, start):
+        for s in range(start, start + n):
+            w = s % nw
+            img, lab = pool[(s // nw) % len(pool)]
+            ctx.step(w, img, lab, w % P + 1, 0.05)
+            if (s + 1) % (H * K) == 0:
+                ctx.average()
+
+    issue(2 * nw, 0)
+    ctx.sync()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    issue(steps, 2 * nw)
+    ctx.sync()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    fams = {}
+    for f in ("conv_fwd", "conv_dgrad", "conv_wgrad", "wgrad_reduce", "bn_stats", "bn_act", "bn_bwd", "head",
+              "maxpool", "add", "snapshot", "image", "sgd_update"):
+        ctx.timer_enable(f)
+        for s in range(P):
+            img, lab = pool[s % len(pool)]
+            ctx.step(0, img, lab, s + 1, 0.0)
+        ms, n, work = ctx.timer_read()
+        fams[f] = (ms, n, work)
+    ctx.timer_enable(None)
+    loss = ctx.get_loss(0)
+    ctx.close()
+    dom = max(fams, key=lambda f: fams[f][0])
+    ms, n, work = fams[dom]
+    mfma = dom.startswith("conv_")
+    peak = (PEAK_BF16_TFLOPS if dtype == lpp.BF16 else PEAK_FP32_TFLOPS) if mfma else PEAK_HBM_GBS
+    ach = work / (ms / 1e3) / (1e12 if mfma else 1e9) if ms > 0 else 0.0
+    mean_flops = info.fwd_flops + sum(info.bwd_flops[i] for i in range(1, P + 1)) / P
+    conv = {f: round(fams[f][2] / (fams[f][0] / 1e3) / 1e12, 1) for f in ("conv_fwd", "conv_dgrad", "conv_wgrad")
+            if fams[f][0] > 0}
+    return {"workload": desc, "dtype": "bf16" if dtype == lpp.BF16 else "f32", "value": round(B * steps / dt, 1),
+            "unit": "samples/s", "steps": steps, "ms_per_step": round(dt / steps * 1e3, 4),
+            "mean_step_gflop": round(mean_flops / 1e9, 2), "model_tflops": round(mean_flops * steps / dt / 1e12, 2),
+            "roofline": {"kernel": dom, "bound": "mfma" if mfma else "hbm", "achieved": round(ach, 2),
+                         "peak": peak, "unit": "TFLOP/s" if mfma else "GB/s", "frac": round(ach / peak, 4),
+                         "timed": "HIP events in the dispatch packets of each launch, worker 0 alone, "
+                                   "partitions 1..4"},
+            "conv_tflops_by_family": conv,
+            "family_ms_per_4_steps": {f: round(v[0], 3) for f, v in sorted(fams.items(), key=lambda t: -t[1][0])},
+            "final_loss_worker0": round(loss, 4)}
 
 
 def cpu_baseline(steps, batch):
@@ -241,13 +340,19 @@ def main():
         "roofline": {"kernel": dom, "bound": "mfma" if mfma else "hbm", "achieved": round(achieved, 2),
                      "peak": peak, "unit": "TFLOP/s" if mfma else "GB/s", "frac": round(achieved / peak, 4),
                      "traffic": None, "launches": launches, "avg_launch_us": round(ms / launches * 1e3, 2),
-                     "timed": "HIP events around each launch of the family on worker 0's stream, %d steps of "
-                              "worker 0 alone (partitions 1..4 in turn) right after the timed region" % rsteps,
+                     "timed": "HIP events recorded in the dispatch packets of each launch of the family "
+                              "(start with its first kernel, stop with its last) on worker 0's stream, %d steps "
+                              "of worker 0 alone (partitions 1..4 in turn) right after the timed region" % rsteps,
                      "family_ms_probe": {k: round(v, 3) for k, v in sorted(fam_time.items(), key=lambda t: -t[1])}},
         "final_losses": [round(l, 4) for l in losses],
     }
     if not a.no_hbm:
         res["hbm_kernels"] = hbm_kernels(torch, lpp)
+    if not a.no_workloads:
+        res["workloads"] = {}
+        for name in [w for w in a.workloads.split(",") if w]:
+            res["workloads"][name] = run_workload(torch, lpp, name, a.workload_steps)
+            torch.cuda.empty_cache()
     if not a.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(a.cpu_steps, B)
     print(json.dumps(res), flush=True)

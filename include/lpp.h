@@ -214,13 +214,15 @@ int lpp_destroy(lpp_ctx* ctx);
 const char* lpp_last_error(void);
 
 /*
- * Kernel timing.  lpp_timer_enable(ctx, name) brackets every launch of the
+ * Kernel timing.  lpp_timer_enable(ctx, name) times every launch of the
  * kernel family `name` (e.g. "conv_fwd", "conv_wgrad", "sgd_update",
- * "average") with HIP events on the stream it runs on; lpp_timer_read
- * returns the summed event time (ms), the number of launches and the
- * summed algorithmic work of those launches (flops for convolutions, bytes
- * for the streaming kernels).  name NULL disables timing.  Reading waits
- * for all outstanding work.
+ * "average"): HIP events recorded in the dispatch packets of the family's
+ * kernels themselves (start with the first kernel of a launch, stop with the
+ * last), so each interval is the kernels' execution on the GPU without the
+ * stream's dispatch gaps.  lpp_timer_read returns the summed event time
+ * (ms), the number of launches and the summed algorithmic work of those
+ * launches (flops for convolutions, bytes for the streaming kernels).  name
+ * NULL disables timing.  Reading waits for all outstanding work.
  */
 int lpp_timer_enable(lpp_ctx* ctx, const char* name);
 int lpp_timer_read(lpp_ctx* ctx, double* ms, long* launches, double* work);

@@ -39,6 +39,7 @@
 #include "act.h"
 #include "bnacc.h"
 #include "kernels.h"
+#include "launch.h"
 
 namespace lpp {
 
@@ -284,10 +285,10 @@ static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* 
     if (Mv == 0) return hipSuccess;
     dim3 grid((unsigned)((Mv + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
     if (stats)
-        hipLaunchKernelGGL((conv_bf16_k<BM, BN, true>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc,
+        launch((conv_bf16_k<BM, BN, true>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc,
                            *stats);
     else
-        hipLaunchKernelGGL((conv_bf16_k<BM, BN, false>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc,
+        launch((conv_bf16_k<BM, BN, false>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc,
                            BnSums{});
     return hipGetLastError();
 }
@@ -522,7 +523,7 @@ template <int BM, int BN>
 static hipError_t launch_wg_bf16(const bf16* dY, const bf16* X, float* part, const WgB& a, int splits,
                                  hipStream_t st) {
     dim3 grid((unsigned)((a.Ktot + BN - 1) / BN), (unsigned)((a.Cout + BM - 1) / BM), (unsigned)splits);
-    hipLaunchKernelGGL((wgrad_bf16_k<BM, BN>), grid, dim3(256), 0, st, dY, X, part, a);
+    launch((wgrad_bf16_k<BM, BN>), grid, dim3(256), 0, st, dY, X, part, a);
     return hipGetLastError();
 }
 

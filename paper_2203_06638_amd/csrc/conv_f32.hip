@@ -29,6 +29,7 @@
 
 #include "bnacc.h"
 #include "kernels.h"
+#include "launch.h"
 
 namespace lpp {
 
@@ -455,10 +456,10 @@ static hipError_t launch_lds(const float* src, const float* B, const float* bias
     const long M = (long)g.Nb * g.Ho * g.Wo;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
     if (stats)
-        hipLaunchKernelGGL((conv_lds_f32<MODE, BM, BN, WM, true>), grid, dim3(256), 0, st, src, B, bias, Y, g,
+        launch((conv_lds_f32<MODE, BM, BN, WM, true>), grid, dim3(256), 0, st, src, B, bias, Y, g,
                            (int)acc, stats ? *stats : BnSums{});
     else
-        hipLaunchKernelGGL((conv_lds_f32<MODE, BM, BN, WM, false>), grid, dim3(256), 0, st, src, B, bias, Y, g,
+        launch((conv_lds_f32<MODE, BM, BN, WM, false>), grid, dim3(256), 0, st, src, B, bias, Y, g,
                            (int)acc, stats ? *stats : BnSums{});
     return hipGetLastError();
 }
@@ -738,10 +739,10 @@ static hipError_t launch_tile(const float* src, const float* B, const float* bia
     constexpr int BN = (4 / WM) * TN * 16;
     dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
     if (stats)
-        hipLaunchKernelGGL((conv_tile_f32<MODE, KS, WM, TM, TN, true>), grid, dim3(256), c.lds, st, src, B, bias, Y,
+        launch((conv_tile_f32<MODE, KS, WM, TM, TN, true>), grid, dim3(256), c.lds, st, src, B, bias, Y,
                            g, c.t, (int)acc, stats ? *stats : BnSums{});
     else
-        hipLaunchKernelGGL((conv_tile_f32<MODE, KS, WM, TM, TN, false>), grid, dim3(256), c.lds, st, src, B, bias, Y,
+        launch((conv_tile_f32<MODE, KS, WM, TM, TN, false>), grid, dim3(256), c.lds, st, src, B, bias, Y,
                            g, c.t, (int)acc, stats ? *stats : BnSums{});
     return hipGetLastError();
 }
@@ -973,7 +974,7 @@ static hipError_t launch_s2(const float* dY, const float* B, float* dX, const Co
                             hipStream_t st) {
     constexpr int BN = (4 / WM) * TN * 16;
     dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
-    hipLaunchKernelGGL((conv_dgrad_s2_f32<KS, PAD, WM, TM, TN>), grid, dim3(256), c.lds, st, dY, B, dX, g, c.t,
+    launch((conv_dgrad_s2_f32<KS, PAD, WM, TM, TN>), grid, dim3(256), c.lds, st, dY, B, dX, g, c.t,
                        (int)acc);
     return hipGetLastError();
 }
@@ -999,17 +1000,17 @@ static hipError_t launch_cfg(const float* src, const float* B, const float* bias
     const bool fast = g.Cs % 16 == 0;
     if (stats) {
         if (fast)
-            hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true, true>), grid, dim3(256), 0, st, src, B, bias,
+            launch((conv_igemm_f32<MODE, WM, TM, TN, true, true>), grid, dim3(256), 0, st, src, B, bias,
                                Y, g, (int)acc, stats ? *stats : BnSums{});
         else
-            hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false, true>), grid, dim3(256), 0, st, src, B, bias,
+            launch((conv_igemm_f32<MODE, WM, TM, TN, false, true>), grid, dim3(256), 0, st, src, B, bias,
                                Y, g, (int)acc, stats ? *stats : BnSums{});
     } else {
         if (fast)
-            hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, true, false>), grid, dim3(256), 0, st, src, B, bias,
+            launch((conv_igemm_f32<MODE, WM, TM, TN, true, false>), grid, dim3(256), 0, st, src, B, bias,
                                Y, g, (int)acc, stats ? *stats : BnSums{});
         else
-            hipLaunchKernelGGL((conv_igemm_f32<MODE, WM, TM, TN, false, false>), grid, dim3(256), 0, st, src, B, bias,
+            launch((conv_igemm_f32<MODE, WM, TM, TN, false, false>), grid, dim3(256), 0, st, src, B, bias,
                                Y, g, (int)acc, stats ? *stats : BnSums{});
     }
     return hipGetLastError();
@@ -1409,7 +1410,7 @@ static hipError_t launch_wg(const float* dY, const float* X, float* part, const 
     const int Ktot = a.R * a.S * a.Cin_p;
     dim3 grid((unsigned)((a.Cout + TM * 16 - 1) / (TM * 16)), (unsigned)((Ktot + TN * 16 - 1) / (TN * 16)),
               (unsigned)p.splits);
-    hipLaunchKernelGGL((conv_wgrad_f32<TM, TN>), grid, dim3(256), 0, st, dY, X, part, a);
+    launch((conv_wgrad_f32<TM, TN>), grid, dim3(256), 0, st, dY, X, part, a);
     return hipGetLastError();
 }
 
@@ -1419,7 +1420,7 @@ static hipError_t launch_wg_tile(const float* dY, const float* X, float* part, c
     const long M = (long)a.Nb * a.Ho * a.Wo;
     dim3 grid((unsigned)(M / t.TP), (unsigned)(a.Cout / 16), (unsigned)(a.Cin_p / 16));
     const size_t lds = sizeof(float) * std::max<size_t>(((size_t)t.IMGS * t.IH * t.IW + t.TP) * 20, (size_t)4 * RS * 256);
-    hipLaunchKernelGGL((conv_wgrad_tile_f32<RS, NG, ST, K1>), grid, dim3(256), lds, st, dY, X, part, a, t);
+    launch((conv_wgrad_tile_f32<RS, NG, ST, K1>), grid, dim3(256), lds, st, dY, X, part, a, t);
     return hipGetLastError();
 }
 
@@ -1483,7 +1484,7 @@ hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot
                                float* g, hipStream_t st) {
     const long n = (long)Cout * Ktot;
     const int L = splits >= 256 ? 16 : (splits >= 64 ? 8 : 4);
-    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64 * L), 0, st, part, splits,
+    launch(wgrad_reduce_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64 * L), 0, st, part, splits,
                        Cout, Ktot, Cin, Cin_p, R, S, g);
     return hipGetLastError();
 }

@@ -12,6 +12,7 @@
 #include "act.h"
 #include "bnacc.h"
 #include "kernels.h"
+#include "launch.h"
 
 namespace lpp {
 
@@ -118,15 +119,15 @@ __global__ __launch_bounds__(256) void sum_from_tiles_k(const float* __restrict_
 }
 
 hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C, float* out, hipStream_t st) {
-    hipLaunchKernelGGL(sum_from_tiles_k, dim3(C), dim3(256), 0, st, pmean, T, R, M, C, out);
+    launch(sum_from_tiles_k, dim3(C), dim3(256), 0, st, pmean, T, R, M, C, out);
     return hipGetLastError();
 }
 
 hipError_t launch_stats_partial(int dt, const void* x, long M, int C, const BnSums& out, hipStream_t st) {
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(stats_partial_k<bf16>, dim3(stats_tiles(M)), dim3(256), 0, st, (const bf16*)x, M, C, out);
+        launch(stats_partial_k<bf16>, dim3(stats_tiles(M)), dim3(256), 0, st, (const bf16*)x, M, C, out);
     else
-        hipLaunchKernelGGL(stats_partial_k<float>, dim3(stats_tiles(M)), dim3(256), 0, st, (const float*)x, M, C, out);
+        launch(stats_partial_k<float>, dim3(stats_tiles(M)), dim3(256), 0, st, (const float*)x, M, C, out);
     return hipGetLastError();
 }
 
@@ -162,7 +163,7 @@ __global__ __launch_bounds__(256) void stats_finalize_k(const float* __restrict_
 
 hipError_t launch_stats_finalize(const float* pmean, const float* pm2, int T, int R, long M, int C,
                                  const float* gamma, const float* beta, float eps, float* aux, hipStream_t st) {
-    hipLaunchKernelGGL(stats_finalize_k, dim3(C), dim3(256), 0, st, pmean, pm2, T, R, M, C, gamma, beta, eps, aux);
+    launch(stats_finalize_k, dim3(C), dim3(256), 0, st, pmean, pm2, T, R, M, C, gamma, beta, eps, aux);
     return hipGetLastError();
 }
 
@@ -231,7 +232,7 @@ static hipError_t bn_act_t(const T* x1, const BnFwd& b1, const T* r, const T* x2
     const int E = bn_quads_per_thread(n4);
     const unsigned grid = (unsigned)((n4 + 256L * E - 1) / (256L * E));
 #define BNACT(RS, RL, EE)                                                                                \
-    hipLaunchKernelGGL((bn_act_k<T, RS, RL, EE>), dim3(grid), dim3(256), lds, st, x1, b1, r, x2, bb, y, n4, C)
+    launch((bn_act_k<T, RS, RL, EE>), dim3(grid), dim3(256), lds, st, x1, b1, r, x2, bb, y, n4, C)
 #define BNACT_E(RS, RL) \
     do { if (E == 4) BNACT(RS, RL, 4); else if (E == 2) BNACT(RS, RL, 2); else BNACT(RS, RL, 1); } while (0)
     if (res == 0) { if (relu) BNACT_E(0, true); else BNACT_E(0, false); }
@@ -440,11 +441,11 @@ template <class T>
 static void bn_bwd_reduce_t(const BnBwdArgs& a, const BnSums& out, hipStream_t st) {
     const dim3 grid(stats_tiles(a.M));
     if (a.mask) {
-        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<T, true, true>), grid, dim3(256), 0, st, a, out);
-        else hipLaunchKernelGGL((bn_bwd_reduce_k<T, true, false>), grid, dim3(256), 0, st, a, out);
+        if (a.x2) launch((bn_bwd_reduce_k<T, true, true>), grid, dim3(256), 0, st, a, out);
+        else launch((bn_bwd_reduce_k<T, true, false>), grid, dim3(256), 0, st, a, out);
     } else {
-        if (a.x2) hipLaunchKernelGGL((bn_bwd_reduce_k<T, false, true>), grid, dim3(256), 0, st, a, out);
-        else hipLaunchKernelGGL((bn_bwd_reduce_k<T, false, false>), grid, dim3(256), 0, st, a, out);
+        if (a.x2) launch((bn_bwd_reduce_k<T, false, true>), grid, dim3(256), 0, st, a, out);
+        else launch((bn_bwd_reduce_k<T, false, false>), grid, dim3(256), 0, st, a, out);
     }
 }
 
@@ -493,7 +494,7 @@ hipError_t launch_bn_bwd_finalize(const float* p0, const float* p1, const float*
                                   const float* gamma1, const float* rstd1, float* gg1, float* gb1, float* coef1,
                                   const float* gamma2, const float* rstd2, float* gg2, float* gb2, float* coef2,
                                   hipStream_t st) {
-    hipLaunchKernelGGL(bn_bwd_finalize_k, dim3(C), dim3(256), 0, st, p0, p1, p2, T, M, C, gamma1, rstd1, gg1, gb1,
+    launch(bn_bwd_finalize_k, dim3(C), dim3(256), 0, st, p0, p1, p2, T, M, C, gamma1, rstd1, gg1, gb1,
                        coef1, gamma2, rstd2, gg2, gb2, coef2);
     return hipGetLastError();
 }
@@ -511,7 +512,7 @@ static hipError_t bn_bwd_apply_t(const BnBwdArgs& a, const BnBwdCoef& k, T* dx1,
     const unsigned grid = (dx1 || dx2 || dres) ? (unsigned)((n4 + 256L * E - 1) / (256L * E)) : 1u;
     const size_t lds = sizeof(float) * 9 * a.C;
 #define BNBA(MK, EE)                                                                                         \
-    hipLaunchKernelGGL((bn_bwd_apply_k<T, MK, EE>), dim3(grid), dim3(256), lds, st, a, k, dx1, (int)acc1, dx2, \
+    launch((bn_bwd_apply_k<T, MK, EE>), dim3(grid), dim3(256), lds, st, a, k, dx1, (int)acc1, dx2, \
                        (int)acc2, dres, (int)accres)
 #define BNBA_E(MK) \
     do { if (E == 4) BNBA(MK, 4); else if (E == 2) BNBA(MK, 2); else BNBA(MK, 1); } while (0)
@@ -568,36 +569,36 @@ __global__ void copy_acc_k(const T* __restrict__ s, T* __restrict__ d, long n4, 
 
 hipError_t launch_relu_fwd(int dt, const void* x, void* y, long n, hipStream_t st) {
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(relu_fwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)x, (bf16*)y, n / 4);
+        launch(relu_fwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)x, (bf16*)y, n / 4);
     else
-        hipLaunchKernelGGL(relu_fwd_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)x, (float*)y,
+        launch(relu_fwd_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)x, (float*)y,
                            n / 4);
     return hipGetLastError();
 }
 hipError_t launch_relu_bwd(int dt, const void* dy, const void* x, void* dx, long n, bool accumulate, hipStream_t st) {
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(relu_bwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)dy, (const bf16*)x,
+        launch(relu_bwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)dy, (const bf16*)x,
                            (bf16*)dx, n / 4, (int)accumulate);
     else
-        hipLaunchKernelGGL(relu_bwd_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)dy,
+        launch(relu_bwd_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)dy,
                            (const float*)x, (float*)dx, n / 4, (int)accumulate);
     return hipGetLastError();
 }
 hipError_t launch_add_fwd(int dt, const void* a, const void* b, void* y, long n, hipStream_t st) {
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(add_fwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)a, (const bf16*)b,
+        launch(add_fwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)a, (const bf16*)b,
                            (bf16*)y, n / 4);
     else
-        hipLaunchKernelGGL(add_fwd_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)a,
+        launch(add_fwd_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)a,
                            (const float*)b, (float*)y, n / 4);
     return hipGetLastError();
 }
 hipError_t launch_copy_acc(int dt, const void* src, void* dst, long n, bool accumulate, hipStream_t st) {
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(copy_acc_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)src, (bf16*)dst,
+        launch(copy_acc_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)src, (bf16*)dst,
                            n / 4, (int)accumulate);
     else
-        hipLaunchKernelGGL(copy_acc_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)src, (float*)dst,
+        launch(copy_acc_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)src, (float*)dst,
                            n / 4, (int)accumulate);
     return hipGetLastError();
 }
@@ -685,10 +686,10 @@ hipError_t launch_maxpool_fwd(int dt, const void* x, void* y, uint8_t* arg, int 
                               int Wo, int k, int stride, int pad, hipStream_t st) {
     const dim3 grid(nblocks((long)Nb * Ho * Wo * C, 256));
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(maxpool_fwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)x, (bf16*)y, arg, Nb, H, W, C,
+        launch(maxpool_fwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)x, (bf16*)y, arg, Nb, H, W, C,
                            Ho, Wo, k, stride, pad);
     else
-        hipLaunchKernelGGL(maxpool_fwd_k<float>, grid, dim3(256), 0, st, (const float*)x, (float*)y, arg, Nb, H, W, C,
+        launch(maxpool_fwd_k<float>, grid, dim3(256), 0, st, (const float*)x, (float*)y, arg, Nb, H, W, C,
                            Ho, Wo, k, stride, pad);
     return hipGetLastError();
 }
@@ -696,27 +697,27 @@ hipError_t launch_maxpool_bwd(int dt, const void* dy, const uint8_t* arg, void* 
                               int Ho, int Wo, int k, int stride, int pad, bool accumulate, hipStream_t st) {
     const dim3 grid(nblocks((long)Nb * H * W * C, 256));
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(maxpool_bwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)dy, arg, (bf16*)dx, Nb, H, W, C,
+        launch(maxpool_bwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)dy, arg, (bf16*)dx, Nb, H, W, C,
                            Ho, Wo, k, stride, pad, (int)accumulate);
     else
-        hipLaunchKernelGGL(maxpool_bwd_k<float>, grid, dim3(256), 0, st, (const float*)dy, arg, (float*)dx, Nb, H, W,
+        launch(maxpool_bwd_k<float>, grid, dim3(256), 0, st, (const float*)dy, arg, (float*)dx, Nb, H, W,
                            C, Ho, Wo, k, stride, pad, (int)accumulate);
     return hipGetLastError();
 }
 hipError_t launch_gap_fwd(int dt, const void* x, float* y, int Nb, int HW, int C, hipStream_t st) {
     const dim3 grid(nblocks((long)Nb * C, 256));
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(gap_fwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)x, y, Nb, HW, C);
+        launch(gap_fwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)x, y, Nb, HW, C);
     else
-        hipLaunchKernelGGL(gap_fwd_k<float>, grid, dim3(256), 0, st, (const float*)x, y, Nb, HW, C);
+        launch(gap_fwd_k<float>, grid, dim3(256), 0, st, (const float*)x, y, Nb, HW, C);
     return hipGetLastError();
 }
 hipError_t launch_gap_bwd(int dt, const float* dy, void* dx, int Nb, int HW, int C, bool accumulate, hipStream_t st) {
     const dim3 grid(nblocks((long)Nb * HW * C, 256));
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(gap_bwd_k<bf16>, grid, dim3(256), 0, st, dy, (bf16*)dx, Nb, HW, C, (int)accumulate);
+        launch(gap_bwd_k<bf16>, grid, dim3(256), 0, st, dy, (bf16*)dx, Nb, HW, C, (int)accumulate);
     else
-        hipLaunchKernelGGL(gap_bwd_k<float>, grid, dim3(256), 0, st, dy, (float*)dx, Nb, HW, C, (int)accumulate);
+        launch(gap_bwd_k<float>, grid, dim3(256), 0, st, dy, (float*)dx, Nb, HW, C, (int)accumulate);
     return hipGetLastError();
 }
 
@@ -892,17 +893,17 @@ hipError_t launch_head_fwd(int dt, const void* x, int Nb, int HW, int C, const f
                            hipStream_t st) {
     if (C > kHeadMaxC || O > kHeadMaxO) return hipErrorInvalidValue;
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(head_fwd_k<bf16>, dim3(Nb), dim3(256), 0, st, (const bf16*)x, Nb, HW, C, W, b, O, args,
+        launch(head_fwd_k<bf16>, dim3(Nb), dim3(256), 0, st, (const bf16*)x, Nb, HW, C, W, b, O, args,
                            feat, logits, dz, loss_per);
     else
-        hipLaunchKernelGGL(head_fwd_k<float>, dim3(Nb), dim3(256), 0, st, (const float*)x, Nb, HW, C, W, b, O, args,
+        launch(head_fwd_k<float>, dim3(Nb), dim3(256), 0, st, (const float*)x, Nb, HW, C, W, b, O, args,
                            feat, logits, dz, loss_per);
     return hipGetLastError();
 }
 hipError_t launch_head_bwd_w(const float* dz, const float* feat, int Nb, int C, int O, float* gW, float* gb,
                              const float* loss_per, float* loss, hipStream_t st) {
     const long n = gW ? (long)O * C + O : 1;
-    hipLaunchKernelGGL(head_bwd_w_k, dim3(nblocks(n, 256)), dim3(256), 0, st, dz, feat, Nb, C, O, gW, gb, loss_per,
+    launch(head_bwd_w_k, dim3(nblocks(n, 256)), dim3(256), 0, st, dz, feat, Nb, C, O, gW, gb, loss_per,
                        loss);
     return hipGetLastError();
 }
@@ -910,35 +911,35 @@ hipError_t launch_head_bwd_x(int dt, const float* dz, const float* W, int Nb, in
                              bool acc, hipStream_t st) {
     if (C > kHeadMaxC) return hipErrorInvalidValue;
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(head_bwd_x_k<bf16>, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, (bf16*)dx, (int)acc);
+        launch(head_bwd_x_k<bf16>, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, (bf16*)dx, (int)acc);
     else
-        hipLaunchKernelGGL(head_bwd_x_k<float>, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, (float*)dx,
+        launch(head_bwd_x_k<float>, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, (float*)dx,
                            (int)acc);
     return hipGetLastError();
 }
 
 hipError_t launch_linear_fwd(const float* x, const float* W, const float* b, float* y, int Nb, int I, int O,
                              hipStream_t st) {
-    hipLaunchKernelGGL(linear_fwd_k, dim3(nblocks((long)Nb * O, 256)), dim3(256), 0, st, x, W, b, y, Nb, I, O);
+    launch(linear_fwd_k, dim3(nblocks((long)Nb * O, 256)), dim3(256), 0, st, x, W, b, y, Nb, I, O);
     return hipGetLastError();
 }
 hipError_t launch_linear_bwd_w(const float* dz, const float* x, float* gW, float* gb, int Nb, int I, int O,
                                hipStream_t st) {
-    hipLaunchKernelGGL(linear_bwd_w_k, dim3(nblocks((long)O * I + O, 256)), dim3(256), 0, st, dz, x, gW, gb, Nb, I,
+    launch(linear_bwd_w_k, dim3(nblocks((long)O * I + O, 256)), dim3(256), 0, st, dz, x, gW, gb, Nb, I,
                        O);
     return hipGetLastError();
 }
 hipError_t launch_linear_bwd_x(const float* dz, const float* W, float* dx, int Nb, int I, int O, bool accumulate,
                                hipStream_t st) {
-    hipLaunchKernelGGL(linear_bwd_x_k, dim3(nblocks((long)Nb * I, 256)), dim3(256), 0, st, dz, W, dx, Nb, I, O,
+    launch(linear_bwd_x_k, dim3(nblocks((long)Nb * I, 256)), dim3(256), 0, st, dz, W, dx, Nb, I, O,
                        (int)accumulate);
     return hipGetLastError();
 }
 hipError_t launch_softmax_ce(const float* z, const StepArgs* args, float* dz, float* loss, int Nb, int Cls,
                              hipStream_t st) {
     // per-sample losses live just after the loss scalar (caller sizes loss to 1 + Nb floats)
-    hipLaunchKernelGGL(softmax_ce_k, dim3(nblocks(Nb, 64)), dim3(64), 0, st, z, args, dz, loss + 1, Nb, Cls);
-    hipLaunchKernelGGL(loss_mean_k, dim3(1), dim3(64), 0, st, loss + 1, Nb, loss);
+    launch(softmax_ce_k, dim3(nblocks(Nb, 64)), dim3(64), 0, st, z, args, dz, loss + 1, Nb, Cls);
+    launch(loss_mean_k, dim3(1), dim3(64), 0, st, loss + 1, Nb, loss);
     return hipGetLastError();
 }
 
@@ -981,10 +982,10 @@ hipError_t launch_nchw_to_nhwc(int dt, const StepArgs* args, void* dst, int Nb, 
                                double* zero, long n_zero, hipStream_t st) {
     const dim3 grid(nblocks((long)Nb * H * W * Cp, 256));
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(nchw_to_nhwc_k<bf16>, grid, dim3(256), 0, st, args, (bf16*)dst, Nb, C, H, W, Cp, zero,
+        launch(nchw_to_nhwc_k<bf16>, grid, dim3(256), 0, st, args, (bf16*)dst, Nb, C, H, W, Cp, zero,
                            n_zero);
     else
-        hipLaunchKernelGGL(nchw_to_nhwc_k<float>, grid, dim3(256), 0, st, args, (float*)dst, Nb, C, H, W, Cp, zero,
+        launch(nchw_to_nhwc_k<float>, grid, dim3(256), 0, st, args, (float*)dst, Nb, C, H, W, Cp, zero,
                            n_zero);
     return hipGetLastError();
 }
@@ -992,9 +993,9 @@ hipError_t launch_nhwc_to_nchw(int dt, const void* src, float* dst, int Nb, int 
                                hipStream_t st) {
     const dim3 grid(nblocks((long)Nb * H * W * C, 256));
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(nhwc_to_nchw_k<bf16>, grid, dim3(256), 0, st, (const bf16*)src, dst, Nb, C, H, W, Cp);
+        launch(nhwc_to_nchw_k<bf16>, grid, dim3(256), 0, st, (const bf16*)src, dst, Nb, C, H, W, Cp);
     else
-        hipLaunchKernelGGL(nhwc_to_nchw_k<float>, grid, dim3(256), 0, st, (const float*)src, dst, Nb, C, H, W, Cp);
+        launch(nhwc_to_nchw_k<float>, grid, dim3(256), 0, st, (const float*)src, dst, Nb, C, H, W, Cp);
     return hipGetLastError();
 }
 
@@ -1007,7 +1008,7 @@ __global__ void set_step_args_k(StepArgs* dst, const float* images, const int* l
 }
 
 hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* labels, float lr, hipStream_t st) {
-    hipLaunchKernelGGL(set_step_args_k, dim3(1), dim3(64), 0, st, dst, images, labels, lr);
+    launch(set_step_args_k, dim3(1), dim3(64), 0, st, dst, images, labels, lr);
     return hipGetLastError();
 }
 
@@ -1047,45 +1048,77 @@ hipError_t launch_snapshot(int dt, const float* x, float* v, long d, const SnapC
     long b = (d + 255) / 256;
     if (b > 16384) b = 16384;
     if (dt == DT_BF16)
-        hipLaunchKernelGGL(snapshot_k<bf16>, dim3((unsigned)b), dim3(256), 0, st, x, v, d, convs_dev, n_convs,
+        launch(snapshot_k<bf16>, dim3((unsigned)b), dim3(256), 0, st, x, v, d, convs_dev, n_convs,
                            (bf16*)wbase);
     else
-        hipLaunchKernelGGL(snapshot_k<float>, dim3((unsigned)b), dim3(256), 0, st, x, v, d, convs_dev, n_convs,
+        launch(snapshot_k<float>, dim3((unsigned)b), dim3(256), 0, st, x, v, d, convs_dev, n_convs,
                            (float*)wbase);
     return hipGetLastError();
 }
 
-// Each thread owns an aligned quad [4t, 4t+4) of the index space shifted to
-// the aligned start below lo; whole quads use 16-byte accesses.
-__global__ void sgd_update_k(float* __restrict__ x, float* __restrict__ m, const float* __restrict__ g, long lo,
-                             long hi, const StepArgs* __restrict__ args, float lr_value, float mu, float wd) {
+// The index space is cut into aligned quads [4q, 4q+4) from the aligned start
+// below lo.  Each thread takes kUpdQuads quads per pass (strided by the
+// workgroup size) and issues all their loads before any arithmetic, so
+// several 16-byte loads per thread are in flight; whole quads use
+// nontemporal 16-byte accesses (streamed once, no reuse within the kernel),
+// the quads cut by lo or hi fall back to scalar accesses.
+constexpr int kUpdQuads = 4;
+
+__device__ __forceinline__ void update_quad(f4& xv, f4& mv, const f4 gv, bool mom, float lr, float mu, float wd) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const float dir = gv[k] + wd * xv[k];
+        if (mom) {
+            mv[k] = mu * mv[k] + dir;
+            xv[k] -= lr * mv[k];
+        } else {
+            xv[k] -= lr * dir;
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void sgd_update_k(float* __restrict__ x, float* __restrict__ m,
+                                                    const float* __restrict__ g, long lo, long hi,
+                                                    const StepArgs* __restrict__ args, float lr_value, float mu,
+                                                    float wd) {
     const float lr = args ? args->lr : lr_value;
     const long base = lo & ~3L;
     const long nq = (hi - base + 3) / 4;
-    for (long q = (long)blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += (long)gridDim.x * blockDim.x) {
-        const long e0 = base + 4 * q;
-        if (e0 >= lo && e0 + 4 <= hi) {
-            f4 xv = *(f4*)(x + e0);
-            const f4 gv = *(const f4*)(g + e0);
-            if (m) {
-                f4 mv = *(f4*)(m + e0);
+    const bool mom = m != nullptr;
+    const long stride = (long)gridDim.x * blockDim.x * kUpdQuads;
+    for (long q0 = (long)blockIdx.x * blockDim.x * kUpdQuads + threadIdx.x; q0 < nq; q0 += stride) {
+        f4 xv[kUpdQuads], mv[kUpdQuads], gv[kUpdQuads];
+        bool whole[kUpdQuads];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    mv[k] = mu * mv[k] + (gv[k] + wd * xv[k]);
-                    xv[k] -= lr * mv[k];
-                }
-                *(f4*)(m + e0) = mv;
-            } else {
-#pragma unroll
-                for (int k = 0; k < 4; ++k) xv[k] -= lr * (gv[k] + wd * xv[k]);
+        for (int u = 0; u < kUpdQuads; ++u) {
+            const long q = q0 + (long)u * blockDim.x;
+            const long e0 = base + 4 * q;
+            whole[u] = q < nq && e0 >= lo && e0 + 4 <= hi;
+            if (whole[u]) {
+                xv[u] = __builtin_nontemporal_load((const f4*)(x + e0));
+                gv[u] = __builtin_nontemporal_load((const f4*)(g + e0));
+                if (mom) mv[u] = __builtin_nontemporal_load((const f4*)(m + e0));
             }
-            *(f4*)(x + e0) = xv;
-        } else {
-            for (long e = e0; e < e0 + 4; ++e) {
-                if (e < lo || e >= hi) continue;
-                float dir = g[e] + wd * x[e];
-                if (m) { m[e] = mu * m[e] + dir; dir = m[e]; }
-                x[e] -= lr * dir;
+        }
+#pragma unroll
+        for (int u = 0; u < kUpdQuads; ++u) {
+            const long q = q0 + (long)u * blockDim.x;
+            if (q >= nq) continue;
+            const long e0 = base + 4 * q;
+            if (whole[u]) {
+                update_quad(xv[u], mv[u], gv[u], mom, lr, mu, wd);
+                if (mom) __builtin_nontemporal_store(mv[u], (f4*)(m + e0));
+                __builtin_nontemporal_store(xv[u], (f4*)(x + e0));
+            } else {
+                for (long e = e0; e < e0 + 4; ++e) {
+                    if (e < lo || e >= hi) continue;
+                    float dir = g[e] + wd * x[e];
+                    if (mom) {
+                        m[e] = mu * m[e] + dir;
+                        dir = m[e];
+                    }
+                    x[e] -= lr * dir;
+                }
             }
         }
     }
@@ -1095,15 +1128,21 @@ hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long h
                              float mu, float wd, hipStream_t st) {
     if (hi <= lo) return hipSuccess;
     const long nq = (hi - (lo & ~3L) + 3) / 4;
-    long b = (nq + 255) / 256;
-    if (b > 8192) b = 8192;
-    hipLaunchKernelGGL(sgd_update_k, dim3((unsigned)b), dim3(256), 0, st, x, m, g, lo, hi, args, lr, mu, wd);
+    long b = (nq + 256L * kUpdQuads - 1) / (256L * kUpdQuads);
+    if (b > 16384) b = 16384;
+    launch(sgd_update_k, dim3((unsigned)b), dim3(256), 0, st, x, m, g, lo, hi, args, lr, mu, wd);
     return hipGetLastError();
 }
 
-// v_k = x_k[e]; vbar = (sum_k v_k) / n; x_k[e] = x_k[e] (re-read) + (vbar - v_k)
+// v_k = x_k[e]; vbar = (sum_k v_k) / n; x_k[e] = x_k[e] (re-read) + (vbar - v_k).
+// One quad per thread per pass, 512-thread workgroups and up to 8M threads in
+// flight.  The re-read of x_k is a volatile load, so it is a fresh read that
+// the compiler cannot merge with the snapshot load: block updates that land
+// between the two survive the write (Alg. 1's averager).
+constexpr int kAvgThreads = 512;
+
 template <int NR>
-__global__ void average_k(RepPtrs reps, int n_rep, long n) {
+__global__ __launch_bounds__(kAvgThreads) void average_k(RepPtrs reps, int n_rep, long n) {
     const long nq = n / 4;
     const float inv_div = (float)n_rep;
     for (long q = (long)blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += (long)gridDim.x * blockDim.x) {
@@ -1121,7 +1160,7 @@ __global__ void average_k(RepPtrs reps, int n_rep, long n) {
         for (int k = 0; k < NR; ++k) {
             if (k < n_rep) {
                 f4* p = (f4*)(reps.p[k] + 4 * q);
-                *p = *p + (vbar - v[k]);
+                *p = *(volatile f4*)p + (vbar - v[k]);
             }
         }
     }
@@ -1137,22 +1176,19 @@ __global__ void average_k(RepPtrs reps, int n_rep, long n) {
         const float vbar = s / inv_div;
 #pragma unroll
         for (int k = 0; k < NR; ++k)
-            if (k < n_rep) reps.p[k][e] = reps.p[k][e] + (vbar - vv[k]);
+            if (k < n_rep) reps.p[k][e] = *(volatile float*)&reps.p[k][e] + (vbar - vv[k]);
     }
 }
 
 hipError_t launch_average(const RepPtrs& reps, int n_rep, long n, hipStream_t st) {
-    long b = (n / 4 + 255) / 256;
+    long b = (n / 4 + kAvgThreads - 1) / kAvgThreads;
     if (b < 1) b = 1;
-    if (b > 8192) b = 8192;
-    if (n_rep <= 2)
-        hipLaunchKernelGGL(average_k<2>, dim3((unsigned)b), dim3(256), 0, st, reps, n_rep, n);
-    else if (n_rep <= 4)
-        hipLaunchKernelGGL(average_k<4>, dim3((unsigned)b), dim3(256), 0, st, reps, n_rep, n);
-    else if (n_rep <= 8)
-        hipLaunchKernelGGL(average_k<8>, dim3((unsigned)b), dim3(256), 0, st, reps, n_rep, n);
-    else
-        hipLaunchKernelGGL(average_k<16>, dim3((unsigned)b), dim3(256), 0, st, reps, n_rep, n);
+    if (b > 16384) b = 16384;
+    const dim3 grid((unsigned)b), block(kAvgThreads);
+    if (n_rep <= 2) launch(average_k<2>, grid, block, 0, st, reps, n_rep, n);
+    else if (n_rep <= 4) launch(average_k<4>, grid, block, 0, st, reps, n_rep, n);
+    else if (n_rep <= 8) launch(average_k<8>, grid, block, 0, st, reps, n_rep, n);
+    else launch(average_k<16>, grid, block, 0, st, reps, n_rep, n);
     return hipGetLastError();
 }
 

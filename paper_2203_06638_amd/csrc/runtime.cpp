@@ -20,6 +20,14 @@
 
 #include "../../include/lpp.h"
 #include "kernels.h"
+#include "launch.h"
+
+namespace lpp {
+LaunchTiming& launch_timing() {
+    thread_local LaunchTiming t;
+    return t;
+}
+}  // namespace lpp
 
 namespace {
 
@@ -460,12 +468,21 @@ hipError_t timed_launch(lpp_ctx* c, const char* family, double work, hipStream_t
             }
         }
     }
-    if (on) hipEventRecord(a, st);
+    // the events are recorded in the dispatch packets of the launcher's
+    // kernels (launch.h): the interval is the kernels' own execution
+    lpp::LaunchTiming& lt = lpp::launch_timing();
+    if (on) lt = lpp::LaunchTiming{a, b};
     hipError_t e = f();
     if (on) {
-        hipEventRecord(b, st);
+        const bool started = lt.start == nullptr;   // a kernel took the start event
+        lt = lpp::LaunchTiming{};
         std::lock_guard<std::mutex> g(T.mu);
-        T.recs.push_back({a, b, work});
+        if (started) {
+            T.recs.push_back({a, b, work});
+        } else {
+            T.pool.push_back(a);
+            T.pool.push_back(b);
+        }
     }
     return e;
 }
