@@ -62,7 +62,11 @@ struct BfPass {
 };
 
 // Output channels in the epilogue: BM x BN tile, bf16, pitch BN + 8.
-template <int BM, int BN, bool STATS>
+// FASTK (Cs % 32 == 0): a K-step is 32 channels of one tap, and the tap and
+// channel counters advance incrementally (no divisions in the loop);
+// otherwise a K-step's four 8-channel chunks are decoded one by one (Cs = 8
+// or 16 spans several taps per K-step).
+template <int BM, int BN, bool STATS, bool FASTK>
 __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src, const bf16* __restrict__ B,
                                                    const float* __restrict__ bias, bf16* __restrict__ Y, ConvGeom g,
                                                    BfPass ps, int accumulate, BnSums sums) {
@@ -81,19 +85,21 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
     const int j = tid & 3, rr = tid >> 2;
     const int RS = g.R * g.S;
 
-    // the output rows whose A values this thread loads
-    int a_img[AL], a_h[AL], a_w[AL];
-    bool a_ok[AL];
+    // the output rows whose A values this thread loads: the element offset of
+    // the source pixel at tap offset (0, 0), and that pixel's coordinates
+    int a_off[AL], a_h[AL], a_w[AL];
 #pragma unroll
     for (int u = 0; u < AL; ++u) {
         const long m = m0 + rr + 64 * u;
-        a_ok[u] = m < Mv;
-        const long mm = a_ok[u] ? m : 0;
+        const bool ok = m < Mv;
+        const long mm = ok ? m : 0;
         const int ow = (int)(mm % ps.Wv);
         const long t = mm / ps.Wv;
-        a_img[u] = (int)(t / ps.Hv) * g.Hs;
+        const int img = (int)(t / ps.Hv);
         a_h[u] = (int)(t % ps.Hv) * ps.ss;
         a_w[u] = ow * ps.ss;
+        a_off[u] = ((img * g.Hs + a_h[u]) * g.Ws + a_w[u]) * g.Cs;
+        if (!ok) a_h[u] = -(1 << 20);             // every tap falls outside
     }
     const bf16* b_row[BL];
 #pragma unroll
@@ -106,24 +112,40 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
     const int nks = (ntap * cpt + 3) >> 2;
 
     uint4 ra[AL], rb[BL];
-    auto load = [&](int ks) {
-        const int kc = ks * 4 + j;
-        const int tap = kc / cpt;
-        const int ch = (kc - tap * cpt) * 8;
-        const bool tok = tap < ntap;
-        const int x = tap / ps.ns, y = tap - (tap / ps.ns) * ps.ns;
-        const int r = ps.r0 + ps.step * x, s = ps.s0 + ps.step * y;
+    // FASTK iteration state: tap (tx, ty) and the K-step's first channel c0
+    int tx = 0, ty = 0, c0 = 0;
+    auto load_tap = [&](int r, int s, int ch, bool tok) {
         const int dh = (ps.offh + ps.sgn * r) >> ps.shift, dw = (ps.offw + ps.sgn * s) >> ps.shift;
-        const long woff = (long)(r * g.S + s) * g.Cs + ch;
+        const int aoff = (dh * g.Ws + dw) * g.Cs + ch;
+        const int woff = (r * g.S + s) * g.Cs + ch;
 #pragma unroll
         for (int u = 0; u < AL; ++u) {
             const int h = a_h[u] + dh, w = a_w[u] + dw;
-            const bool ok = tok && a_ok[u] && h >= 0 && h < g.Hs && w >= 0 && w < g.Ws;
-            ra[u] = ok ? *(const uint4*)(src + ((long)(a_img[u] + h) * g.Ws + w) * g.Cs + ch) : uint4{0, 0, 0, 0};
+            const bool ok = tok && (unsigned)h < (unsigned)g.Hs && (unsigned)w < (unsigned)g.Ws;
+            ra[u] = ok ? *(const uint4*)(src + a_off[u] + aoff) : uint4{0, 0, 0, 0};
         }
 #pragma unroll
         for (int u = 0; u < BL; ++u)
             rb[u] = (tok && b_row[u]) ? *(const uint4*)(b_row[u] + woff) : uint4{0, 0, 0, 0};
+    };
+    auto load = [&](int ks) {
+        if (FASTK) {
+            load_tap(ps.r0 + ps.step * tx, ps.s0 + ps.step * ty, c0 + 8 * j, true);
+            c0 += 32;
+            if (c0 == g.Cs) {
+                c0 = 0;
+                if (++ty == ps.ns) {
+                    ty = 0;
+                    ++tx;
+                }
+            }
+        } else {
+            const int kc = ks * 4 + j;
+            const int tap = kc / cpt;
+            const int ch = (kc - tap * cpt) * 8;
+            const int x = tap / ps.ns, y = tap - (tap / ps.ns) * ps.ns;
+            load_tap(ps.r0 + ps.step * x, ps.s0 + ps.step * y, ch, tap < ntap);
+        }
     };
     auto store = [&](int buf) {
         bf16* As = lds + buf * STAGE;
@@ -145,16 +167,17 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
         store(0);
     }
     __syncthreads();
+    const int a_rd = ((wm * TM) * 16 + (lane & 15)) * P + (lane >> 4) * 8;
+    const int b_rd = BM * P + ((wn * TN) * 16 + (lane & 15)) * P + (lane >> 4) * 8;
     for (int ks = 0; ks < nks; ++ks) {
         const int cur = ks & 1;
         if (ks + 1 < nks) load(ks + 1);
-        const bf16* As = lds + cur * STAGE;
-        const bf16* Bs = As + BM * P;
+        const bf16* base = lds + cur * STAGE;
         bf8 a[TM], b[TN];
 #pragma unroll
-        for (int x = 0; x < TM; ++x) a[x] = *(const bf8*)(As + ((wm * TM + x) * 16 + (lane & 15)) * P + (lane >> 4) * 8);
+        for (int x = 0; x < TM; ++x) a[x] = *(const bf8*)(base + a_rd + x * 16 * P);
 #pragma unroll
-        for (int y = 0; y < TN; ++y) b[y] = *(const bf8*)(Bs + ((wn * TN + y) * 16 + (lane & 15)) * P + (lane >> 4) * 8);
+        for (int y = 0; y < TN; ++y) b[y] = *(const bf8*)(base + b_rd + y * 16 * P);
 #pragma unroll
         for (int x = 0; x < TM; ++x)
 #pragma unroll
@@ -284,12 +307,14 @@ static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* 
     const long Mv = (long)g.Nb * ps.Hv * ps.Wv;
     if (Mv == 0) return hipSuccess;
     dim3 grid((unsigned)((Mv + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
-    if (stats)
-        launch((conv_bf16_k<BM, BN, true>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc,
-                           *stats);
-    else
-        launch((conv_bf16_k<BM, BN, false>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc,
-                           BnSums{});
+    const BnSums sm = stats ? *stats : BnSums{};
+    if (g.Cs % 32 == 0) {
+        if (stats) launch((conv_bf16_k<BM, BN, true, true>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, true>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+    } else {
+        if (stats) launch((conv_bf16_k<BM, BN, true, false>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, false>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+    }
     return hipGetLastError();
 }
 
