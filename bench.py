@@ -66,6 +66,14 @@ def parse():
     ap.add_argument("--workloads", default="resnet20_100_k4,wrn16_8_bf16,resnet18_bf16",
                     help="comma-separated subset of the other configurations")
     ap.add_argument("--workload-steps", type=int, default=64)
+    ap.add_argument("--only-workload", default=None, help="run just one of the other configurations (for profiling)")
+    # HBM traffic of the roofline kernel (run each under rocprofv3 --pmc):
+    ap.add_argument("--roofline-only", metavar="FAMILY", default=None,
+                    help="only the roofline pass: worker 0 alone, kernels of FAMILY launched one by one")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only a plain device copy of 256 MiB, ten times (counter calibration)")
+    ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
+                    help="turn the four counter runs into the traffic summary under profiles/")
     return ap.parse_args()
 
 
@@ -196,6 +204,80 @@ def run_workload(torch, lpp, name, steps, B=128, P=4):
             "final_loss_worker0": round(loss, 4)}
 
 
+# ---------------------------------------------------------------------------
+# HBM traffic of the roofline kernel: FETCH_SIZE and WRITE_SIZE per dispatch
+# from two rocprofv3 --pmc runs of --roofline-only, each scaled by what the
+# same counter reads for a plain copy of known size (--copy-calibration).
+# The summary records a hash of the kernel sources; a later change to them
+# makes the figure stale and bench.py then reports traffic as null.
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_fwd_resnet20_b128_fp32_traffic.md")
+TRAFFIC_SOURCES = ["paper_2203_06638_amd/csrc/conv_f32.hip", "paper_2203_06638_amd/csrc/launch.h",
+                   "paper_2203_06638_amd/csrc/bnacc.h"]
+COPY_BYTES = 256 << 20
+# kernel-name prefixes of each timed family (the library's launchers)
+FAMILY_KERNELS = {"conv_fwd": ("void lpp::conv_tile_f32<0,", "void lpp::conv_igemm_f32<0,", "void lpp::conv_lds_f32<0,",
+                               "void lpp::conv_bf16_k<")}
+
+
+def _sources_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def _counter_rows(d, counter):
+    """(kernel name, value) per dispatch from a rocprofv3 counter-collection
+    CSV under directory d."""
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    rows.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return rows
+
+
+def summarize_traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, family="conv_fwd"):
+    pref = FAMILY_KERNELS[family]
+    out = {}
+    for key, d, cd, counter in (("fetch", fetch_dir, cfetch_dir, "FETCH_SIZE"),
+                                ("write", write_dir, cwrite_dir, "WRITE_SIZE")):
+        fam = [v for k, v in _counter_rows(d, counter) if k.startswith(pref)]
+        cal = _counter_rows(cd, counter)
+        # the copy kernel: the dispatches with the largest reading
+        top = max(v for _, v in cal)
+        cal_vals = [v for _, v in cal if v >= 0.9 * top]
+        kib = sum(cal_vals) / len(cal_vals)
+        factor = COPY_BYTES / (kib * 1024.0)
+        out[key] = {"launches": len(fam), "kib_per_launch": round(sum(fam) / len(fam), 1),
+                    "copy_kib": round(kib, 1), "copy_bytes": COPY_BYTES, "factor": round(factor, 4),
+                    "bytes_per_launch": round(sum(fam) / len(fam) * 1024.0 * factor)}
+    out["traffic_bytes_per_launch"] = out["fetch"]["bytes_per_launch"] + out["write"]["bytes_per_launch"]
+    out["family"] = family
+    out["sources_sha256"] = _sources_hash()
+    return out
+
+
+def read_traffic():
+    """Bytes per launch of the roofline family from the committed summary,
+    or None if there is none or the kernel sources changed since."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            for line in fh:
+                if line.startswith("TRAFFIC_JSON "):
+                    t = json.loads(line[len("TRAFFIC_JSON "):])
+                    return t["traffic_bytes_per_launch"] if t["sources_sha256"] == _sources_hash() else None
+    except OSError:
+        return None
+    return None
+
+
 def cpu_baseline(steps, batch):
     """The oracle (fp64 C, OpenMP) on `steps` ResNet-20 worker steps at the
     same batch, partitions cycling over the four blocks."""
@@ -220,6 +302,10 @@ def cpu_baseline(steps, batch):
 
 def main():
     a = parse()
+    if a.summarize_traffic:
+        t = summarize_traffic(*a.summarize_traffic)
+        print("TRAFFIC_JSON " + json.dumps(t))
+        return
     if a.gpus != 1:
         print("bench.py measures one GPU only: this build runs the per-node step on a single MI355X "
               "(--gpus %d is not supported)" % a.gpus, file=sys.stderr)
@@ -231,6 +317,19 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.init()
+    if a.copy_calibration:
+        x = torch.empty(COPY_BYTES // 4, device="cuda")
+        y = torch.empty_like(x)
+        x.fill_(1.0)
+        for _ in range(10):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print("copied %d bytes ten times" % COPY_BYTES)
+        return
+    if a.only_workload:
+        from paper_2203_06638_amd import lpp as _lpp
+        print(json.dumps(run_workload(torch, _lpp, a.only_workload, a.workload_steps)), flush=True)
+        return
     B, P, K = a.batch, 4, a.replicas
     model = PM.resnet20(10)
     info = lpp.describe(model, B)
@@ -272,6 +371,17 @@ def main():
 
     run(a.warmup, 0)
     ctx.sync()
+    if a.roofline_only:
+        ctx.timer_enable(a.roofline_only)
+        for s in range(a.steps):
+            img, lab = pool[s % len(pool)]
+            ctx.step(0, img, lab, s % P + 1, 0.1)
+        ms, launches, work = ctx.timer_read()
+        ctx.timer_enable(None)
+        ctx.close()
+        print(json.dumps({"family": a.roofline_only, "launches": launches, "avg_launch_us": ms / launches * 1e3,
+                          "work_per_launch": work / launches}))
+        return
     # find the dominant kernel family on a short untimed pass (a kernel timer
     # makes the library launch kernels one by one so each can be bracketed)
     fam_time = {}
@@ -339,7 +449,7 @@ def main():
                    "model_tflops": round(mean_flops * a.steps / dt / 1e12, 2)},
         "roofline": {"kernel": dom, "bound": "mfma" if mfma else "hbm", "achieved": round(achieved, 2),
                      "peak": peak, "unit": "TFLOP/s" if mfma else "GB/s", "frac": round(achieved / peak, 4),
-                     "traffic": None, "launches": launches, "avg_launch_us": round(ms / launches * 1e3, 2),
+                     "traffic": read_traffic() if dom == "conv_fwd" else None, "launches": launches, "avg_launch_us": round(ms / launches * 1e3, 2),
                      "timed": "HIP events recorded in the dispatch packets of each launch of the family "
                               "(start with its first kernel, stop with its last) on worker 0's stream, %d steps "
                               "of worker 0 alone (partitions 1..4 in turn) right after the timed region" % rsteps,
