@@ -67,6 +67,8 @@ def parse():
                     help="comma-separated subset of the other configurations")
     ap.add_argument("--workload-steps", type=int, default=64)
     ap.add_argument("--only-workload", default=None, help="run just one of the other configurations (for profiling)")
+    ap.add_argument("--delays", action="store_true",
+                    help="only the delay statistics of traced async runs (ResNet-20, K=2 x P=4) against H")
     # HBM traffic of the roofline kernel (run each under rocprofv3 --pmc):
     ap.add_argument("--roofline-only", metavar="FAMILY", default=None,
                     help="only the roofline pass: worker 0 alone, kernels of FAMILY launched one by one")
@@ -278,6 +280,35 @@ def read_traffic():
     return None
 
 
+def delay_statistics(torch, Hs=(1, 2, 4, 8, 16), T=256, B=128):
+    """Traced async runs of the LPP-SGD policy (ResNet-20, K = 2 replicas x
+    P = 4 workers, T updates per replica, T_st = T/10) for several
+    synchronization periods H: the estimated probability of Assumption 1's
+    good iterates and the staleness of the snapshots."""
+    import synth
+    from paper_2203_06638_amd import delays as D
+    from paper_2203_06638_amd import lpp
+    from paper_2203_06638_amd import models as PM
+    from paper_2203_06638_amd import policy as PL
+    model = PM.resnet20(10)
+    pool = [(torch.from_numpy(synth.images(300 + b, B, 3, 32, 32)).cuda(),
+             torch.from_numpy(synth.labels(300 + b, B, 10)).cuda()) for b in range(4)]
+    out = {"workload": "ResNet-20 (10 classes), batch %d, fp32, K=2 replicas x P=4 workers, async, T=%d updates "
+                       "per replica, T_st=T/10, warm-up + cosine LR" % (B, T), "runs": {}}
+    for H in Hs:
+        ctx = lpp.Context(model, K=2, batch=B, mode=lpp.ASYNC, momentum=0.9,
+                          streams=[torch.cuda.Stream() for _ in range(8)], avg_stream=torch.cuda.Stream())
+        ctx.set_params(synth.init_params(model.specs, 3))
+        ctx.trace_enable(4 * T)
+        PL.run(ctx, pool, PL.Schedule(T=T, T_st=T // 10, H=H, base_lr=0.05, warm_lr=0.125, warmup=T // 10))
+        steps, rounds, khz = ctx.trace_read()
+        ctx.close()
+        _, summ = D.analyze(steps, rounds)
+        summ.pop("staleness_hist")
+        out["runs"]["H=%d" % H] = summ
+    return out
+
+
 def cpu_baseline(steps, batch):
     """The oracle (fp64 C, OpenMP) on `steps` ResNet-20 worker steps at the
     same batch, partitions cycling over the four blocks."""
@@ -325,6 +356,9 @@ def main():
             y.copy_(x)
         torch.cuda.synchronize()
         print("copied %d bytes ten times" % COPY_BYTES)
+        return
+    if a.delays:
+        print(json.dumps(delay_statistics(torch)), flush=True)
         return
     if a.only_workload:
         from paper_2203_06638_amd import lpp as _lpp

@@ -228,6 +228,39 @@ int lpp_timer_enable(lpp_ctx* ctx, const char* name);
 int lpp_timer_read(lpp_ctx* ctx, double* ms, long* launches, double* work);
 
 /*
+ * Step tracing: the orders of the paper's delay model (Sec. 5 "snapshot
+ * order", "update order", "iteration order"; their definitions in the
+ * appendix) observed on the device.  lpp_trace_enable(ctx, capacity)
+ * allocates logs for `capacity` steps and `capacity` averaging rounds
+ * (capacity 0 frees them and stops tracing); while it is on, every
+ * lpp_step brackets its snapshot and its block update with timestamp
+ * kernels and every lpp_average brackets its averaging kernel (timestamps of
+ * the device's constant-rate clock, lpp_trace_clock_khz ticks per ms; a
+ * timestamp kernel runs in stream order between its neighbours, so the
+ * intervals contain the bracketed kernels).  Traced steps replay graphs of
+ * their own; untraced steps are unchanged.  Steps and rounds beyond the
+ * capacity run untraced.  lpp_trace_read waits for all work and copies the
+ * records in issue order (NULL arrays: counts only); LPP_ESTATE when
+ * tracing is off, LPP_EINVAL when an array is too small.
+ */
+typedef struct {
+    int worker, replica, partition;
+    long counter;               /* C^q the step read (its snapshot order)    */
+    unsigned long long t[4];    /* before the snapshot, after it, before the
+                                   block update, after it                    */
+} lpp_trace_step;
+typedef struct {
+    long index;                 /* averaging round j (the iteration order)   */
+    int n_replicas;
+    long counter_min;           /* smallest replica counter when issued      */
+    unsigned long long t[2];    /* before and after the averaging kernel     */
+} lpp_trace_avg;
+int lpp_trace_enable(lpp_ctx* ctx, long capacity);
+int lpp_trace_read(lpp_ctx* ctx, lpp_trace_step* steps, long max_steps, long* n_steps, lpp_trace_avg* avgs,
+                   long max_avgs, long* n_avgs);
+long lpp_trace_clock_khz(const lpp_ctx* ctx);
+
+/*
  * Stand-alone launches of the two streaming kernels on caller buffers, for
  * bandwidth measurement at arbitrary sizes.  All pointers are device
  * pointers; stream may be NULL (default stream).  No allocation.

@@ -31,8 +31,15 @@ struct StepArgs {
     const float* images;
     const int* labels;
     float lr;
+    long trace_slot;   // this step's row of the timestamp log, or -1
 };
-hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* labels, float lr, hipStream_t st);
+hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* labels, float lr, long trace_slot,
+                                hipStream_t st);
+// Step tracing: one kernel of one thread that stores the device's constant-
+// rate clock (wall_clock64, 100 MHz) into log[slot * 4 + k] with slot =
+// args->trace_slot (nothing when it is negative); kernels of a stream run in
+// order, so a timestamp kernel marks a point between its neighbours.
+hipError_t launch_timestamp(unsigned long long* log, const StepArgs* args, long slot, int k, hipStream_t st);
 
 // Where a batch-norm reduction goes.  With acc set, every workgroup adds its
 // tile's sums into per-channel fp64 accumulators acc[q][kAccSlots][C] (q

@@ -999,16 +999,30 @@ hipError_t launch_nhwc_to_nchw(int dt, const void* src, float* dst, int Nb, int 
     return hipGetLastError();
 }
 
-__global__ void set_step_args_k(StepArgs* dst, const float* images, const int* labels, float lr) {
+__global__ void set_step_args_k(StepArgs* dst, const float* images, const int* labels, float lr, long trace_slot) {
     if (threadIdx.x == 0 && blockIdx.x == 0) {
         dst->images = images;
         dst->labels = labels;
         dst->lr = lr;
+        dst->trace_slot = trace_slot;
     }
 }
 
-hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* labels, float lr, hipStream_t st) {
-    launch(set_step_args_k, dim3(1), dim3(64), 0, st, dst, images, labels, lr);
+hipError_t launch_set_step_args(StepArgs* dst, const float* images, const int* labels, float lr, long trace_slot,
+                                hipStream_t st) {
+    launch(set_step_args_k, dim3(1), dim3(64), 0, st, dst, images, labels, lr, trace_slot);
+    return hipGetLastError();
+}
+
+// slot from the step arguments (args non-null) or from the argument
+__global__ void timestamp_k(unsigned long long* log, const StepArgs* args, long slot, int k) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    const long s = args ? args->trace_slot : slot;
+    if (s >= 0) log[s * 4 + k] = wall_clock64();
+}
+
+hipError_t launch_timestamp(unsigned long long* log, const StepArgs* args, long slot, int k, hipStream_t st) {
+    launch(timestamp_k, dim3(1), dim3(64), 0, st, log, args, slot, k);
     return hipGetLastError();
 }
 

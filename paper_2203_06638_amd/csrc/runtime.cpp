@@ -403,6 +403,7 @@ struct Worker {
     float* wpart = nullptr;
     lpp::StepArgs* args = nullptr;          // device: this step's images, labels, lr
     std::vector<hipGraphExec_t> graphs;     // one per partition, captured on first use
+    std::vector<hipGraphExec_t> tgraphs;    // the same with the step-trace timestamps
     int last_partition = -1;
 };
 
@@ -431,6 +432,15 @@ struct lpp_ctx {
     std::unique_ptr<std::atomic<long>[]> counters;
     Timer timer;
     int device = 0;
+    // step tracing (lpp_trace_enable): device timestamps per traced step
+    // [slot][4] and per averaging round [slot][4], host records of both
+    unsigned long long* trace_log = nullptr;
+    unsigned long long* avg_log = nullptr;
+    long trace_cap = 0;
+    std::atomic<long> trace_next{0}, avg_next{0};
+    std::mutex trace_mu;
+    std::vector<lpp_trace_step> trace_steps;
+    std::vector<lpp_trace_avg> trace_avgs;
 
     void* act(Worker& w, int l) { return w.ws + M.layers[l].act; }
     void* dact(Worker& w, int l) { return w.ws + M.layers[l].dact; }
@@ -514,6 +524,8 @@ void destroy_ctx(lpp_ctx* c) {
         if (w.stream) hipStreamSynchronize(w.stream);
         for (auto g : w.graphs)
             if (g) hipGraphExecDestroy(g);
+        for (auto g : w.tgraphs)
+            if (g) hipGraphExecDestroy(g);
         if (w.ws) hipFree(w.ws);
         if (w.own_stream && w.stream) hipStreamDestroy(w.stream);
     }
@@ -521,6 +533,8 @@ void destroy_ctx(lpp_ctx* c) {
     if (c->own_avg && c->avg_stream) hipStreamDestroy(c->avg_stream);
     if (c->replicas) hipFree(c->replicas);
     if (c->snap_dev) hipFree(c->snap_dev);
+    if (c->trace_log) hipFree(c->trace_log);
+    if (c->avg_log) hipFree(c->avg_log);
     for (auto& r : c->timer.recs) {
         hipEventDestroy(r.a);
         hipEventDestroy(r.b);
@@ -851,23 +865,28 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
 
 // The device work of one updater iteration on the worker's stream: snapshot
 // of the replica, forward, truncated backward, block update.  Per-step
-// arguments are read from w.args.
-int enqueue_step(lpp_ctx* c, Worker& w, int worker, int partition) {
+// arguments are read from w.args.  `traced` brackets the snapshot and the
+// update with timestamp kernels (their log row comes from w.args).
+int enqueue_step(lpp_ctx* c, Worker& w, int worker, int partition, bool traced) {
     const int q = worker / c->P;
     float* xq = c->replicas + (long)q * c->dpad;
     const long d = c->M.d;
     hipStream_t st = w.stream;
+    if (traced) HIPCHK(lpp::launch_timestamp(c->trace_log, w.args, -1, 0, st));
     LAUNCH("snapshot", 8.0 * d, st,
            lpp::launch_snapshot(c->M.dt, xq, w.v, d, c->snap_dev, c->n_snap, w.wbuf, st));
+    if (traced) HIPCHK(lpp::launch_timestamp(c->trace_log, w.args, -1, 1, st));
     int rc = run_forward(c, w);
     if (rc) return rc;
     rc = run_backward(c, w, partition);
     if (rc) return rc;
     const long lo = c->M.blo[partition], hi = c->M.bhi[partition];
     const bool mom = c->M.desc.momentum != 0.f;
+    if (traced) HIPCHK(lpp::launch_timestamp(c->trace_log, w.args, -1, 2, st));
     LAUNCH("sgd_update", (mom ? 20.0 : 12.0) * (hi - lo), st,
            lpp::launch_sgd_update(xq, mom ? w.m : nullptr, w.g, lo, hi, w.args, 0.f, c->M.desc.momentum,
                                   c->M.desc.weight_decay, st));
+    if (traced) HIPCHK(lpp::launch_timestamp(c->trace_log, w.args, -1, 3, st));
     return LPP_OK;
 }
 
@@ -1018,6 +1037,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         w.wpart = (float*)(w.ws + c->off_wpart);
         w.args = (lpp::StepArgs*)(w.ws + c->off_args);
         w.graphs.assign(P + 1, nullptr);
+        w.tgraphs.assign(P + 1, nullptr);
     }
     if (opt && opt->avg_stream) {
         c->avg_stream = (hipStream_t)opt->avg_stream;
@@ -1045,9 +1065,23 @@ int lpp_step(lpp_ctx* c, int worker, const lpp_batch* batch, int partition, floa
     if (!std::isfinite(lr)) return fail(LPP_EINVAL, "lr must be finite");
     Worker& w = c->workers[worker];
     const int q = worker / c->P;
-    c->counters[q].fetch_add(1);                 // s := read&inc(C^q)
+    const long s_read = c->counters[q].fetch_add(1);   // s := read&inc(C^q)
     hipStream_t st = w.stream;
-    LAUNCH("args", 0.0, st, lpp::launch_set_step_args(w.args, batch->images, batch->labels, lr, st));
+    const bool traced = c->trace_log != nullptr;
+    long slot = -1;
+    if (traced) {
+        const long k = c->trace_next.fetch_add(1);
+        if (k < c->trace_cap) {
+            slot = k;
+            std::lock_guard<std::mutex> g(c->trace_mu);
+            lpp_trace_step& r = c->trace_steps[k];
+            r.worker = worker;
+            r.replica = q;
+            r.partition = partition;
+            r.counter = s_read;
+        }
+    }
+    LAUNCH("args", 0.0, st, lpp::launch_set_step_args(w.args, batch->images, batch->labels, lr, slot, st));
     bool timing;
     {
         std::lock_guard<std::mutex> g(c->timer.mu);
@@ -1056,10 +1090,10 @@ int lpp_step(lpp_ctx* c, int worker, const lpp_batch* batch, int partition, floa
     if (c->graphs && !timing) {
         // one graph per (worker, partition): snapshot, forward, truncated
         // backward and update, captured once and replayed
-        hipGraphExec_t& ge = w.graphs[partition];
+        hipGraphExec_t& ge = traced ? w.tgraphs[partition] : w.graphs[partition];
         if (!ge) {
             HIPCHK(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
-            rc = enqueue_step(c, w, worker, partition);
+            rc = enqueue_step(c, w, worker, partition, traced);
             hipGraph_t graph = nullptr;
             hipError_t e = hipStreamEndCapture(st, &graph);
             if (rc) {
@@ -1076,7 +1110,7 @@ int lpp_step(lpp_ctx* c, int worker, const lpp_batch* batch, int partition, floa
         }
         HIPCHK(hipGraphLaunch(ge, st));
     } else {
-        rc = enqueue_step(c, w, worker, partition);
+        rc = enqueue_step(c, w, worker, partition, traced);
         if (rc) return rc;
     }
     w.last_partition = partition;
@@ -1104,7 +1138,22 @@ int lpp_average(lpp_ctx* c, const int* replicas, int n_replicas) {
     if (c->mode == LPP_SEQUENTIAL)
         for (auto& w : c->workers) HIPCHK(hipStreamSynchronize(w.stream));
     hipStream_t st = c->avg_stream;
+    long slot = -1;
+    if (c->avg_log) {
+        const long k = c->avg_next.fetch_add(1);
+        if (k < c->trace_cap) {
+            slot = k;
+            std::lock_guard<std::mutex> g(c->trace_mu);
+            lpp_trace_avg& r = c->trace_avgs[k];
+            r.index = k;
+            r.n_replicas = n;
+            r.counter_min = c->counters[0].load();
+            for (int q = 1; q < c->K; ++q) r.counter_min = std::min(r.counter_min, c->counters[q].load());
+        }
+        HIPCHK(lpp::launch_timestamp(c->avg_log, nullptr, slot, 0, st));
+    }
     LAUNCH("average", 8.0 * n * c->M.d, st, lpp::launch_average(rp, n, c->M.d, st));
+    if (c->avg_log) HIPCHK(lpp::launch_timestamp(c->avg_log, nullptr, slot, 1, st));
     if (c->mode == LPP_SEQUENTIAL) HIPCHK(hipStreamSynchronize(st));
     return LPP_OK;
 }
@@ -1309,6 +1358,75 @@ int lpp_timer_read(lpp_ctx* c, double* ms, long* launches, double* work) {
     *launches = c->timer.launches;
     *work = c->timer.work;
     return LPP_OK;
+}
+
+int lpp_trace_enable(lpp_ctx* c, long capacity) {
+    if (!c) return fail(LPP_EINVAL, "ctx is NULL");
+    if (capacity < 0 || capacity > (1L << 26)) return fail(LPP_EINVAL, "capacity must be in [0, 2^26]");
+    int rc = sync_all(c);
+    if (rc) return rc;
+    if (c->trace_log) hipFree(c->trace_log);
+    if (c->avg_log) hipFree(c->avg_log);
+    c->trace_log = c->avg_log = nullptr;
+    c->trace_cap = 0;
+    c->trace_next.store(0);
+    c->avg_next.store(0);
+    c->trace_steps.clear();
+    c->trace_avgs.clear();
+    if (capacity == 0) return LPP_OK;
+    const size_t bytes = sizeof(unsigned long long) * 4 * (size_t)capacity;
+    if (hipMalloc((void**)&c->trace_log, bytes) != hipSuccess) return fail(LPP_ENOMEM, "trace log allocation");
+    if (hipMalloc((void**)&c->avg_log, bytes) != hipSuccess) {
+        hipFree(c->trace_log);
+        c->trace_log = nullptr;
+        return fail(LPP_ENOMEM, "trace log allocation");
+    }
+    HIPCHK(hipMemset(c->trace_log, 0, bytes));
+    HIPCHK(hipMemset(c->avg_log, 0, bytes));
+    c->trace_cap = capacity;
+    c->trace_steps.assign(capacity, lpp_trace_step{});
+    c->trace_avgs.assign(capacity, lpp_trace_avg{});
+    return LPP_OK;
+}
+
+int lpp_trace_read(lpp_ctx* c, lpp_trace_step* steps, long max_steps, long* n_steps, lpp_trace_avg* avgs,
+                   long max_avgs, long* n_avgs) {
+    if (!c || !n_steps || !n_avgs) return fail(LPP_EINVAL, "NULL argument");
+    if (!c->trace_log) return fail(LPP_ESTATE, "tracing is not enabled");
+    int rc = sync_all(c);
+    if (rc) return rc;
+    const long ns = std::min(c->trace_next.load(), c->trace_cap);
+    const long na = std::min(c->avg_next.load(), c->trace_cap);
+    *n_steps = ns;
+    *n_avgs = na;
+    std::vector<unsigned long long> t(4 * (size_t)std::max(ns, na));
+    if (steps && ns > 0) {
+        if (max_steps < ns) return fail(LPP_EINVAL, "max_steps is smaller than the number of traced steps");
+        HIPCHK(hipMemcpy(t.data(), c->trace_log, sizeof(unsigned long long) * 4 * ns, hipMemcpyDeviceToHost));
+        std::lock_guard<std::mutex> g(c->trace_mu);
+        for (long i = 0; i < ns; ++i) {
+            steps[i] = c->trace_steps[i];
+            for (int k = 0; k < 4; ++k) steps[i].t[k] = t[4 * i + k];
+        }
+    }
+    if (avgs && na > 0) {
+        if (max_avgs < na) return fail(LPP_EINVAL, "max_avgs is smaller than the number of traced rounds");
+        HIPCHK(hipMemcpy(t.data(), c->avg_log, sizeof(unsigned long long) * 4 * na, hipMemcpyDeviceToHost));
+        std::lock_guard<std::mutex> g(c->trace_mu);
+        for (long i = 0; i < na; ++i) {
+            avgs[i] = c->trace_avgs[i];
+            avgs[i].t[0] = t[4 * i];
+            avgs[i].t[1] = t[4 * i + 1];
+        }
+    }
+    return LPP_OK;
+}
+
+long lpp_trace_clock_khz(const lpp_ctx* c) {
+    if (!c) return -1;
+    int khz = 0;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->device) != hipSuccess) return -1;
+    return khz;
 }
 
 int lpp_kernel_sgd_update(float* x, float* m, const float* g, long n, float lr, float mu, float wd, void* stream) {

@@ -49,6 +49,15 @@ class Batch(C.Structure):
     _fields_ = [("images", C.c_void_p), ("labels", C.c_void_p), ("n", C.c_int)]
 
 
+class TraceStep(C.Structure):
+    _fields_ = [("worker", C.c_int), ("replica", C.c_int), ("partition", C.c_int), ("counter", C.c_long),
+                ("t", C.c_ulonglong * 4)]
+
+
+class TraceAvg(C.Structure):
+    _fields_ = [("index", C.c_long), ("n_replicas", C.c_int), ("counter_min", C.c_long), ("t", C.c_ulonglong * 2)]
+
+
 class ModelInfo(C.Structure):
     _fields_ = [("d", C.c_long), ("P", C.c_int), ("block_lo", C.c_long * 65), ("block_hi", C.c_long * 65),
                 ("fwd_flops", C.c_double), ("bwd_flops", C.c_double * 65)]
@@ -84,6 +93,10 @@ def lib():
             "lpp_last_error": ([], C.c_char_p),
             "lpp_timer_enable": ([ctx, C.c_char_p], C.c_int),
             "lpp_timer_read": ([ctx, C.POINTER(C.c_double), C.POINTER(C.c_long), C.POINTER(C.c_double)], C.c_int),
+            "lpp_trace_enable": ([ctx, C.c_long], C.c_int),
+            "lpp_trace_read": ([ctx, C.POINTER(TraceStep), C.c_long, C.POINTER(C.c_long), C.POINTER(TraceAvg), C.c_long,
+                                C.POINTER(C.c_long)], C.c_int),
+            "lpp_trace_clock_khz": ([ctx], C.c_long),
             "lpp_kernel_sgd_update": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_long, C.c_float, C.c_float,
                                        C.c_float, C.c_void_p], C.c_int),
             "lpp_kernel_average": ([C.POINTER(C.c_void_p), C.c_int, C.c_long, C.c_void_p], C.c_int),
@@ -223,6 +236,22 @@ class Context:
         ms, n, work = C.c_double(), C.c_long(), C.c_double()
         _check(lib().lpp_timer_read(self._ctx, C.byref(ms), C.byref(n), C.byref(work)))
         return ms.value, n.value, work.value
+
+    def trace_enable(self, capacity):
+        _check(lib().lpp_trace_enable(self._ctx, capacity))
+
+    def trace_read(self):
+        """(steps, rounds, clock_khz): lists of dicts in issue order."""
+        ns, na = C.c_long(), C.c_long()
+        _check(lib().lpp_trace_read(self._ctx, None, 0, C.byref(ns), None, 0, C.byref(na)))
+        st = (TraceStep * max(1, ns.value))()
+        av = (TraceAvg * max(1, na.value))()
+        _check(lib().lpp_trace_read(self._ctx, st, ns.value, C.byref(ns), av, na.value, C.byref(na)))
+        steps = [dict(worker=r.worker, replica=r.replica, partition=r.partition, counter=r.counter, t=list(r.t))
+                 for r in st[:ns.value]]
+        rounds = [dict(index=r.index, n_replicas=r.n_replicas, counter_min=r.counter_min, t=list(r.t))
+                  for r in av[:na.value]]
+        return steps, rounds, int(lib().lpp_trace_clock_khz(self._ctx))
 
     def close(self):
         if self._ctx:

@@ -91,3 +91,59 @@ def test_policy_async_training_curve():
         for i in range(1, P + 1):
             lo, hi = ctx.block_range(i)
             assert not np.array_equal(xn[lo:hi], x[lo:hi])
+
+
+# ---------------------------------------------------------------------------
+# step tracing: the orders of the delay model observed on the device
+# ---------------------------------------------------------------------------
+
+def _traced_run(p, K, P, sched, pool, mode, x, trace):
+    with lpp.Context(p, K=K, batch=pool[0][0].shape[0], momentum=0.9, mode=mode) as ctx:
+        ctx.set_params(x)
+        if trace:
+            ctx.trace_enable(4096)
+        PL.run(ctx, pool, sched)
+        tr = ctx.trace_read() if trace else None
+        return [ctx.get_params(q) for q in range(K)], tr
+
+
+def test_trace_sequential_orders_and_no_effect_on_results():
+    from paper_2203_06638_amd import delays as D
+    p = PM.resnet20()
+    K, P = 2, 4
+    sched = PL.Schedule(T=16, T_st=4, H=2, base_lr=0.02, warm_lr=0.05, warmup=4)
+    x = T.init_x(p.specs, 701)
+    pool = [dev(*T.inputs(702 + b, 8, p.in_shape, 10)) for b in range(3)]
+    plain, _ = _traced_run(p, K, P, sched, pool, lpp.SEQUENTIAL, x, False)
+    traced, (steps, rounds, khz) = _traced_run(p, K, P, sched, pool, lpp.SEQUENTIAL, x, True)
+    for q in range(K):
+        assert np.array_equal(plain[q], traced[q])                # tracing changes nothing
+    pl = PL.plan(sched, K, P)
+    assert len(steps) == len(pl.steps) and len(rounds) == sum(1 for e in pl.events if e[0] == "average")
+    assert khz > 0
+    for s, e in zip(steps, pl.steps):
+        assert (s["worker"], s["partition"]) == (e[1], e[2]) and s["counter"] == e[4]
+        assert s["t"][0] <= s["t"][1] <= s["t"][2] <= s["t"][3]
+    # sequential: nothing overlaps, in issue order
+    evs = sorted([tuple(s["t"][::3]) for s in steps] + [tuple(r["t"]) for r in rounds])
+    assert all(evs[i][1] <= evs[i + 1][0] for i in range(len(evs) - 1))
+    ann, summ = D.analyze(steps, rounds)
+    say("sequential trace", summ)
+    assert summ["staleness_max"] == 0 and summ["p_good"] == 1.0 and summ["order_inversions"] == 0
+
+
+def test_trace_async_delay_statistics():
+    from paper_2203_06638_amd import delays as D
+    p = PM.resnet20()
+    K, P = 2, 4
+    x = T.init_x(p.specs, 711)
+    pool = [dev(*T.inputs(712 + b, 32, p.in_shape, 10)) for b in range(4)]
+    for H in (1, 8):
+        sched = PL.Schedule(T=48, T_st=4, H=H, base_lr=0.02, warm_lr=0.05, warmup=4)
+        _, (steps, rounds, khz) = _traced_run(p, K, P, sched, pool, lpp.ASYNC, x, True)
+        assert len(steps) == K * sched.T
+        assert all(s["t"][0] <= s["t"][1] <= s["t"][2] <= s["t"][3] for s in steps)
+        assert all(r["t"][0] <= r["t"][1] for r in rounds)
+        ann, summ = D.analyze(steps, rounds)
+        say("async trace H=%d" % H, summ)
+        assert 0.0 <= summ["p_good"] <= 1.0 and summ["staleness_max"] >= 0
