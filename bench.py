@@ -63,7 +63,7 @@ def parse():
     ap.add_argument("--issue-threads", type=int, default=1,
                     help="host threads issuing steps; each owns a fixed set of workers")
     ap.add_argument("--no-workloads", action="store_true", help="skip the other configurations")
-    ap.add_argument("--workloads", default="resnet20_100_k4,wrn16_8_bf16,resnet18_bf16",
+    ap.add_argument("--workloads", default="resnet20_100_k4,wrn16_8_bf16,resnet18_bf16,resnet50_bf16",
                     help="comma-separated subset of the other configurations")
     ap.add_argument("--workload-steps", type=int, default=64)
     ap.add_argument("--only-workload", default=None, help="run just one of the other configurations (for profiling)")
@@ -134,6 +134,10 @@ def _workloads():
                           "ResNet-18 (1000 classes), batch 128 of 3x224x224, bf16 activations / fp32 master "
                           "weights, K=2 x P=4 workers on 8 HIP streams, averaging every 8 steps per replica, "
                           "momentum 0.9, async"),
+        "resnet50_bf16": (lambda: PM.resnet50(1000), (3, 224, 224), 1000, lpp.BF16, 2, 8,
+                          "ResNet-50 (1000 classes), batch 32 of 3x224x224, bf16 activations / fp32 master "
+                          "weights, K=2 x P=4 workers on 8 HIP streams, averaging every 8 steps per replica, "
+                          "momentum 0.9, async", 32),
     }
 
 
@@ -143,7 +147,8 @@ def run_workload(torch, lpp, name, steps, B=128, P=4):
     an averaging round whenever every replica has advanced H steps; then
     the kernel families on worker 0 alone."""
     import synth
-    build, shape, ncls, dtype, K, H, desc = _workloads()[name]
+    build, shape, ncls, dtype, K, H, desc = _workloads()[name][:7]
+    B = (_workloads()[name][7:] or (B,))[0]
     model = build()
     info = lpp.describe(model, B, dtype=dtype)
     pool = []

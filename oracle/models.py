@@ -249,6 +249,45 @@ def resnet_imagenet(units_per_stage=(2, 2, 2, 2), widths=(64, 128, 256, 512), n_
     return net
 
 
+def _bottleneck(net, x, cin, width, stride, relu=True):
+    """Bottleneck residual unit: 1x1 conv to `width`, 3x3 conv (carrying the
+    stride), 1x1 conv to 4*width, each followed by BN (and ReLU but the
+    last); the shortcut is the input or a 1x1 strided conv + BN; ReLU after
+    the sum."""
+    net.next_unit()
+    out = 4 * width
+    h = net.bn(net.conv(x, cin, width, 1, 1, 0), width)
+    if relu:
+        h = net.relu(h)
+    h = net.bn(net.conv(h, width, width, 3, stride, 1), width)
+    if relu:
+        h = net.relu(h)
+    h = net.bn(net.conv(h, width, out, 1, 1, 0), out)
+    s = x if (stride == 1 and cin == out) else net.bn(net.conv(x, cin, out, 1, stride, 0), out)
+    h = net.add(h, s)
+    return net.relu(h) if relu else h
+
+
+def resnet_bottleneck(units_per_stage=(3, 4, 6, 3), widths=(64, 128, 256, 512), n_classes=1000, hw=224, relu=True):
+    """ImageNet ResNet with bottleneck units (ResNet-50 by default): 7x7/2
+    stem, BN, ReLU, 3x3/2 max pool, four stages (the first unit of stages
+    2-4 strides in its 3x3 conv), global pool, linear."""
+    net = Net("resnet%d" % (2 + 3 * sum(units_per_stage)), 3, hw, hw, n_classes)
+    x = net.bn(net.conv(-1, 3, widths[0], 7, 2, 3), widths[0])
+    if relu:
+        x = net.relu(x)
+    x = net.maxpool(x, 3, 2, 1)
+    cin = widths[0]
+    for si, (w, nu) in enumerate(zip(widths, units_per_stage)):
+        for b in range(nu):
+            x = _bottleneck(net, x, cin, w, 2 if (si > 0 and b == 0) else 1, relu)
+            cin = 4 * w
+    net.next_unit()
+    x = net.gap(x)
+    net.linear(x, cin, n_classes)
+    return net
+
+
 # ---- the workloads' models with their partitions (units -> blocks) ----
 
 def tiny_p2():
@@ -269,3 +308,11 @@ def wrn16_8_p4(n_classes=100):
 def resnet18_p4(n_classes=1000):
     # units: stem, s1u1, s1u2, s2u1, s2u2, s3u1, s3u2, s4u1, s4u2, head
     return resnet_imagenet().set_blocks([1, 1, 2, 2, 2, 3, 3, 4, 4, 4])
+
+
+def resnet50_p4(n_classes=1000, relu=True):
+    # units: stem, s1u1..s1u3, s2u1..s2u4, s3u1..s3u6, s4u1..s4u3, head
+    # blocks: {stem,s1u1-3,s2u1} {s2u2-4,s3u1} {s3u2-5} {s3u6,s4u1-3,head}
+    return resnet_bottleneck(n_classes=n_classes, relu=relu).set_blocks(
+        [1, 1, 1, 1, 1, 2, 2, 2, 2, 3, 3, 3, 3, 4, 4, 4, 4, 4])
+

@@ -96,9 +96,11 @@ hipError_t launch_conv_wgrad_bf16(const uint16_t* dY, const uint16_t* X, float* 
                                   const WgradPlan& p, hipStream_t st);
 
 // ---- batch-norm statistics over [M][C] NHWC rows ----
-constexpr int kStatRows = 256;   // rows per tile of the stand-alone kernels
-int stats_tiles(long M);
-// per tile of kStatRows rows: mean and sum of squared deviations per channel
+// row tiles of the stand-alone kernels: stats_rows(M, C) rows each (256, or
+// fewer for short tensors), stats_tiles(M, C) of them
+int stats_rows(long M, int C);
+int stats_tiles(long M, int C);
+// per row tile: mean and sum of squared deviations per channel
 // into p0 / p1 [T][C], or the tile's share of the batch sums added into
 // acc [2][kAccSlots][C] (sum x, sum x^2)
 hipError_t launch_stats_partial(int dt, const void* x, long M, int C, const BnSums& out, hipStream_t st);
@@ -128,6 +130,14 @@ struct BnFwd {
 hipError_t launch_bn_act(int dt, const void* x1, const BnFwd& b1, const void* r, const void* x2, const BnFwd* b2,
                          bool relu, void* y, long M, int C, hipStream_t st);
 
+// Async mode, wide layers: the coefficients derived once per batch norm by a
+// kernel of one thread per channel instead of in the prologue of every
+// apply workgroup (which re-reads C x kAccSlots sums per workgroup).
+// Forward: aux = [mean | rstd | scale | shift] from acc [2][kAccSlots][C].
+hipError_t launch_bn_fwd_coef(const BnFwd& b, int C, hipStream_t st);
+// workgroups the apply kernels launch for M rows of C channels
+int bn_apply_groups(long M, int C);
+
 // ---- batch-norm backward (with the group's ReLU mask and residual fan-out) ----
 struct BnBwdArgs {
     const void* dy;                                    // gradient at the group output
@@ -137,7 +147,7 @@ struct BnBwdArgs {
     long M;
     int C;
 };
-// per tile of kStatRows rows, the tile's sum g, sum g*xhat1 and sum g*xhat2
+// per row tile (stats_rows), the tile's sum g, sum g*xhat1 and sum g*xhat2
 // added into acc [3][kAccSlots][C], or written to p0..p2 [T][C]
 hipError_t launch_bn_bwd_reduce(int dt, const BnBwdArgs& a, const BnSums& out, hipStream_t st);
 // fixed-order merge of T tile partials: gg/gb (dgamma, dbeta; null = not
@@ -159,6 +169,10 @@ struct BnBwdCoef {
     const float* gamma2; float* gg2; float* gb2;
     const float* coef1; const float* coef2;
 };
+// Async mode, wide layers: coef1 (and coef2) = [gamma*rstd | mean g |
+// mean g*xhat] and dgamma / dbeta (k.gg*, k.gb*, null = not wanted) from the
+// sums k.acc [3][kAccSlots][C], one thread per channel.
+hipError_t launch_bn_bwd_coef(const BnBwdArgs& a, const BnBwdCoef& k, float* coef1, float* coef2, hipStream_t st);
 // dx = a*(g - mean g - xhat*mean g*xhat) into dx1 / dx2 (null = skip), and g
 // into dres (the residual branch) -- each written or accumulated
 hipError_t launch_bn_bwd_apply(int dt, const BnBwdArgs& a, const BnBwdCoef& k, void* dx1, bool acc1, void* dx2,

@@ -24,7 +24,18 @@ static inline unsigned nblocks(long n, int per) { return (unsigned)((n + per - 1
 // partials or added to the batch sums
 // ------------------------------------------------------------------------
 
-int stats_tiles(long M) { return (int)((M + kStatRows - 1) / kStatRows); }
+// Row tiles of the stand-alone reductions: 256 rows, fewer when that would
+// leave less than about 128 workgroups (grid.y takes chunks of 256 channel
+// quads).
+int stats_rows(long M, int C) {
+    const long gy = ((C >> 2) + 255) / 256;
+    long r = (M * gy + 127) / 128;
+    return (int)(r < 16 ? 16 : (r > 256 ? 256 : r));
+}
+int stats_tiles(long M, int C) {
+    const int R = stats_rows(M, C);
+    return (int)((M + R - 1) / R);
+}
 
 // Threads tile the rows x channel-quads of one row tile; quads beyond 256
 // are handled in chunks.  Returns nq (quads in this chunk) and rl (row lanes).
@@ -34,15 +45,15 @@ __device__ __forceinline__ void quad_layout(int C4, int qbase, int& nq, int& rl)
 }
 
 template <class T>
-__global__ __launch_bounds__(256) void stats_partial_k(const T* __restrict__ x, long M, int C, BnSums out) {
+__global__ __launch_bounds__(256) void stats_partial_k(const T* __restrict__ x, long M, int C, int R, BnSums out) {
     __shared__ f4 red[256];
     __shared__ float mean_s[1024];
     const int tid = threadIdx.x;
     const int C4 = C >> 2;
-    const long r0 = (long)blockIdx.x * kStatRows;
-    const long r1 = min(M, r0 + kStatRows);
+    const long r0 = (long)blockIdx.x * R;
+    const long r1 = min(M, r0 + R);
     const float rows = (float)(r1 - r0);
-    for (int qbase = 0; qbase < C4; qbase += 256) {
+    for (int qbase = blockIdx.y * 256; qbase < min(C4, (int)(blockIdx.y + 1) * 256); qbase += 256) {
         int nq, rl;
         quad_layout(C4, qbase, nq, rl);
         const int q = qbase + tid % nq, lr = tid / nq;
@@ -124,10 +135,12 @@ hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C
 }
 
 hipError_t launch_stats_partial(int dt, const void* x, long M, int C, const BnSums& out, hipStream_t st) {
+    const dim3 grid(stats_tiles(M, C), ((C >> 2) + 255) / 256);
+    const int R = stats_rows(M, C);
     if (dt == DT_BF16)
-        launch(stats_partial_k<bf16>, dim3(stats_tiles(M)), dim3(256), 0, st, (const bf16*)x, M, C, out);
+        launch(stats_partial_k<bf16>, grid, dim3(256), 0, st, (const bf16*)x, M, C, R, out);
     else
-        launch(stats_partial_k<float>, dim3(stats_tiles(M)), dim3(256), 0, st, (const float*)x, M, C, out);
+        launch(stats_partial_k<float>, grid, dim3(256), 0, st, (const float*)x, M, C, R, out);
     return hipGetLastError();
 }
 
@@ -212,8 +225,34 @@ __global__ __launch_bounds__(256) void bn_act_k(const T* __restrict__ x1, BnFwd 
     }
 }
 
+__global__ __launch_bounds__(256) void bn_fwd_coef_k(BnFwd b, int C) {
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= C) return;
+    const double mu = acc_read(b.acc, 0, C, c) / (double)b.M;
+    double var = acc_read(b.acc, 1, C, c) / (double)b.M - mu * mu;
+    var = var > 0.0 ? var : 0.0;
+    const double r = 1.0 / sqrt(var + (double)b.eps);
+    const double sc = (double)b.gamma[c] * r;
+    b.aux[c] = (float)mu;
+    b.aux[C + c] = (float)r;
+    b.aux[2 * C + c] = (float)sc;
+    b.aux[3 * C + c] = (float)((double)b.beta[c] - mu * sc);
+}
+
+hipError_t launch_bn_fwd_coef(const BnFwd& b, int C, hipStream_t st) {
+    if (!b.acc || !b.aux) return hipErrorInvalidValue;
+    launch(bn_fwd_coef_k, dim3((C + 255) / 256), dim3(256), 0, st, b, C);
+    return hipGetLastError();
+}
+
 // quads per thread of the batch-norm kernels: at most about 1024 workgroups
 static int bn_quads_per_thread(long n4) { return n4 > 256L * 1024 * 2 ? 4 : (n4 > 256L * 1024 ? 2 : 1); }
+
+int bn_apply_groups(long M, int C) {
+    const long n4 = M * C / 4;
+    const int E = bn_quads_per_thread(n4);
+    return (int)((n4 + 256L * E - 1) / (256L * E));
+}
 
 static unsigned ew_grid(long n4) {
     long b = (n4 + 255) / 256;
@@ -257,12 +296,13 @@ hipError_t launch_bn_act(int dt, const void* x1, const BnFwd& b1, const void* r,
 // dx = gamma*rstd*(g - mean(g) - xhat*mean(g*xhat)).
 // ------------------------------------------------------------------------
 
-// Per tile of kStatRows rows: threads form nq channel quads x rl row lanes;
+// Per tile of R rows (and chunk of 256 channel quads, grid.y): threads form nq
+// channel quads x rl row lanes;
 // each thread's rows are loaded four at a time before use, the row lanes
 // meet in a fixed-shape LDS tree, and lane 0 of each quad adds the tile's
 // sums to the accumulators.
 template <class T, bool MASK, bool DUAL>
-__global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, BnSums out) {
+__global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, int R, BnSums out) {
     const T* __restrict__ dy = (const T*)a.dy;
     const T* __restrict__ mask = (const T*)a.mask;
     const T* __restrict__ x1 = (const T*)a.x1;
@@ -270,9 +310,9 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, BnSums out) 
     __shared__ f4 red[3][256];
     const int tid = threadIdx.x;
     const int C = a.C, C4 = C >> 2;
-    const long r0 = (long)blockIdx.x * kStatRows;
-    const long r1 = min(a.M, r0 + kStatRows);
-    for (int qbase = 0; qbase < C4; qbase += 256) {
+    const long r0 = (long)blockIdx.x * R;
+    const long r1 = min(a.M, r0 + R);
+    for (int qbase = blockIdx.y * 256; qbase < min(C4, (int)(blockIdx.y + 1) * 256); qbase += 256) {
         int nq, rl;
         quad_layout(C4, qbase, nq, rl);
         const int q = qbase + tid % nq, lr = tid / nq;
@@ -439,13 +479,14 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, 
 
 template <class T>
 static void bn_bwd_reduce_t(const BnBwdArgs& a, const BnSums& out, hipStream_t st) {
-    const dim3 grid(stats_tiles(a.M));
+    const dim3 grid(stats_tiles(a.M, a.C), ((a.C >> 2) + 255) / 256);
+    const int R = stats_rows(a.M, a.C);
     if (a.mask) {
-        if (a.x2) launch((bn_bwd_reduce_k<T, true, true>), grid, dim3(256), 0, st, a, out);
-        else launch((bn_bwd_reduce_k<T, true, false>), grid, dim3(256), 0, st, a, out);
+        if (a.x2) launch((bn_bwd_reduce_k<T, true, true>), grid, dim3(256), 0, st, a, R, out);
+        else launch((bn_bwd_reduce_k<T, true, false>), grid, dim3(256), 0, st, a, R, out);
     } else {
-        if (a.x2) launch((bn_bwd_reduce_k<T, false, true>), grid, dim3(256), 0, st, a, out);
-        else launch((bn_bwd_reduce_k<T, false, false>), grid, dim3(256), 0, st, a, out);
+        if (a.x2) launch((bn_bwd_reduce_k<T, false, true>), grid, dim3(256), 0, st, a, R, out);
+        else launch((bn_bwd_reduce_k<T, false, false>), grid, dim3(256), 0, st, a, R, out);
     }
 }
 
@@ -488,6 +529,32 @@ __global__ __launch_bounds__(256) void bn_bwd_finalize_k(const float* __restrict
         coef2[C + c] = (float)(t0 / (double)M);
         coef2[2 * C + c] = (float)(t2 / (double)M);
     }
+}
+
+__global__ __launch_bounds__(256) void bn_bwd_coef_k(BnBwdArgs a, BnBwdCoef k, float* coef1, float* coef2) {
+    const int C = a.C;
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= C) return;
+    const double t0 = acc_read(k.acc, 0, C, c), t1 = acc_read(k.acc, 1, C, c);
+    coef1[c] = k.gamma1[c] * a.rstd1[c];
+    coef1[C + c] = (float)(t0 / (double)a.M);
+    coef1[2 * C + c] = (float)(t1 / (double)a.M);
+    if (k.gg1) k.gg1[c] = (float)t1;
+    if (k.gb1) k.gb1[c] = (float)t0;
+    if (coef2) {
+        const double t2 = acc_read(k.acc, 2, C, c);
+        coef2[c] = k.gamma2[c] * a.rstd2[c];
+        coef2[C + c] = (float)(t0 / (double)a.M);
+        coef2[2 * C + c] = (float)(t2 / (double)a.M);
+        if (k.gg2) k.gg2[c] = (float)t2;
+        if (k.gb2) k.gb2[c] = (float)t0;
+    }
+}
+
+hipError_t launch_bn_bwd_coef(const BnBwdArgs& a, const BnBwdCoef& k, float* coef1, float* coef2, hipStream_t st) {
+    if (!k.acc || !coef1 || (coef2 && (!k.gamma2 || !a.rstd2))) return hipErrorInvalidValue;
+    launch(bn_bwd_coef_k, dim3((a.C + 255) / 256), dim3(256), 0, st, a, k, coef1, coef2);
+    return hipGetLastError();
 }
 
 hipError_t launch_bn_bwd_finalize(const float* p0, const float* p1, const float* p2, int T, long M, int C,

@@ -505,6 +505,15 @@ hipError_t timed_launch(lpp_ctx* c, const char* family, double work, hipStream_t
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// In async mode a batch norm's coefficients come either from the prologue of
+// every apply workgroup (each re-reads C x kAccSlots fp64 sums: cheap for
+// narrow layers, one launch fewer) or from one coefficient kernel, when that
+// re-reading would exceed this many sums per launch.
+constexpr double kPrologueSums = 4.0e6;
+bool use_coef_kernel(long M, int C, int nsums) {
+    return (double)lpp::bn_apply_groups(M, C) * C * lpp::kAccSlots * nsums > kPrologueSums;
+}
+
 int check_worker(const lpp_ctx* c, int w) {
     if (!c) return fail(LPP_EINVAL, "ctx is NULL");
     if (w < 0 || w >= c->K * c->P) return fail(LPP_EINVAL, "worker out of range");
@@ -558,7 +567,7 @@ int bn_stats_standalone(lpp_ctx* c, Worker& w, int b) {
         const lpp::BnSums out{nullptr, w.ps0, w.ps1, nullptr};
         LAUNCH("bn_stats", eb * rows * C, st, lpp::launch_stats_partial(dt, x, rows, C, out, st));
         LAUNCH("bn_stats", 0.0, st,
-               lpp::launch_stats_finalize(w.ps0, w.ps1, lpp::stats_tiles(rows), lpp::kStatRows, rows, C,
+               lpp::launch_stats_finalize(w.ps0, w.ps1, lpp::stats_tiles(rows, C), lpp::stats_rows(rows, C), rows, C,
                                           w.v + B.poff, w.v + B.poff + C, M.desc.bn_eps, c->aux(w, b), st));
     } else {
         const lpp::BnSums out{c->acc_fwd(w, b), nullptr, nullptr, nullptr};
@@ -621,13 +630,21 @@ int run_forward(lpp_ctx* c, Worker& w) {
                 if (rc) return rc;
             }
             const Layer& B1 = M.layers[G.a];
-            const lpp::BnFwd b1{c->fixed_order ? nullptr : c->acc_fwd(w, G.a), w.v + B1.poff, w.v + B1.poff + C,
-                                M.desc.bn_eps, Mrows, c->aux(w, G.a)};
+            lpp::BnFwd b1{c->fixed_order ? nullptr : c->acc_fwd(w, G.a), w.v + B1.poff, w.v + B1.poff + C,
+                          M.desc.bn_eps, Mrows, c->aux(w, G.a)};
             lpp::BnFwd b2{};
             if (G.bn2 >= 0) {
                 const Layer& B2 = M.layers[G.bn2];
                 b2 = lpp::BnFwd{c->fixed_order ? nullptr : c->acc_fwd(w, G.bn2), w.v + B2.poff, w.v + B2.poff + C,
                                 M.desc.bn_eps, Mrows, c->aux(w, G.bn2)};
+            }
+            if (!c->fixed_order && use_coef_kernel(Mrows, C, G.bn2 >= 0 ? 4 : 2)) {
+                LAUNCH("bn_act", 0.0, st, lpp::launch_bn_fwd_coef(b1, C, st));
+                b1.acc = nullptr;
+                if (G.bn2 >= 0) {
+                    LAUNCH("bn_act", 0.0, st, lpp::launch_bn_fwd_coef(b2, C, st));
+                    b2.acc = nullptr;
+                }
             }
             const void* x2 = G.bn2 >= 0 ? c->act(w, M.layers[G.bn2].L.in0) : nullptr;
             const void* r = G.res >= 0 ? c->act(w, G.res) : nullptr;
@@ -726,7 +743,7 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                     LAUNCH("bias_grad", eb * Mo * Y.L.cout, st,
                            lpp::launch_stats_partial(dt, dy, Mo, Y.L.cout, tiles, st));
                     LAUNCH("bias_grad", 0.0, st,
-                           lpp::launch_sum_from_tiles(w.ps0, lpp::stats_tiles(Mo), lpp::kStatRows, Mo, Y.L.cout,
+                           lpp::launch_sum_from_tiles(w.ps0, lpp::stats_tiles(Mo, Y.L.cout), lpp::stats_rows(Mo, Y.L.cout), Mo, Y.L.cout,
                                                       w.g + Y.poff + Y.wcount, st));
                 }
             }
@@ -772,7 +789,7 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                     const lpp::BnSums out{nullptr, w.ps0, w.ps1, w.ps2};
                     LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(dt, a, out, st));
                     LAUNCH("bn_bwd", 0.0, st,
-                           lpp::launch_bn_bwd_finalize(w.ps0, w.ps1, w.ps2, lpp::stats_tiles(Min), Min, C,
+                           lpp::launch_bn_bwd_finalize(w.ps0, w.ps1, w.ps2, lpp::stats_tiles(Min, C), Min, C,
                                                        w.v + Y.poff, ax + C, gg1, gb1, ax + 4 * C,
                                                        want2 ? w.v + Y2->poff : nullptr, want2 ? ax2 + C : nullptr,
                                                        gg2, gb2, want2 ? ax2 + 4 * C : nullptr, st));
@@ -783,6 +800,12 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                     LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(dt, a, out, st));
                     k = lpp::BnBwdCoef{c->acc_bwd(w, G.a), w.v + Y.poff, gg1, gb1,
                                        want2 ? w.v + Y2->poff : nullptr, gg2, gb2, nullptr, nullptr};
+                    if (use_coef_kernel(Min, C, want2 ? 3 : 2)) {
+                        float* cf1 = ax + 4 * C;
+                        float* cf2 = want2 ? ax2 + 4 * C : nullptr;
+                        LAUNCH("bn_bwd", 0.0, st, lpp::launch_bn_bwd_coef(a, k, cf1, cf2, st));
+                        k = lpp::BnBwdCoef{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, cf1, cf2};
+                    }
                 }
             }
             void* d1 = want1 && pl.din0[G.a] ? dx0 : nullptr;
@@ -982,14 +1005,14 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         if (Y.L.op == LPP_BN) Y.aux = take(sizeof(float) * 7 * Y.out.c);
         if (Y.L.op == LPP_MAXPOOL) Y.aux = take((size_t)rows_out * Y.out.c);
         const long rin = (long)N * Y.in0.h * Y.in0.w;
-        if (Y.L.op == LPP_BN) ps = std::max<long>(ps, (long)lpp::stats_tiles(rin) * Y.out.c);
+        if (Y.L.op == LPP_BN) ps = std::max<long>(ps, (long)lpp::stats_tiles(rin, Y.out.c) * Y.out.c);
         if (Y.L.op == LPP_CONV) {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
                             Y.L.pad};
             const int tr = M.dt == lpp::DT_BF16 ? lpp::conv_bf16_tile_rows(g) : lpp::conv_tile_rows(g);
             const long tiles = (rows_out + tr - 1) / tr;
             ps = std::max<long>(ps, tiles * Y.L.cout);
-            ps = std::max<long>(ps, (long)lpp::stats_tiles(rows_out) * Y.L.cout);
+            ps = std::max<long>(ps, (long)lpp::stats_tiles(rows_out, Y.L.cout) * Y.L.cout);
             wpart = std::max<long>(wpart, Y.wg.part_floats);
         }
     }

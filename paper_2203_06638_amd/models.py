@@ -122,6 +122,21 @@ def pre_act_unit(m, x, cout, stride, act=True):
     return m.add(y, sc)
 
 
+def bottleneck_unit(m, x, mid, stride, act=True):
+    """conv1x1 (mid) - BN - ReLU - conv3x3 (mid, stride) - BN - ReLU - conv1x1
+    (4 mid) - BN (+ identity, or 1x1/stride conv + BN projection when the
+    shape changes), ReLU.  act=False leaves the ReLUs out."""
+    m.new_unit()
+    relu = m.relu if act else (lambda t: t)
+    cin = m.shapes[x][0]
+    cout = 4 * mid
+    y = relu(m.bn(m.conv(x, mid, 1, 1, 0)))
+    y = relu(m.bn(m.conv(y, mid, 3, stride)))
+    y = m.bn(m.conv(y, cout, 1, 1, 0))
+    sc = m.bn(m.conv(x, cout, 1, stride, 0)) if (stride != 1 or cin != cout) else x
+    return relu(m.add(y, sc))
+
+
 # ---------------------------------------------------------------------------
 # the workloads
 
@@ -189,3 +204,28 @@ def resnet18(n_classes=1000):
     """ResNet-18, P = 4: {stem, s1u1} {s1u2, s2u1, s2u2} {s3u1, s3u2}
     {s4u1, s4u2, head}."""
     return resnet_imagenet(n_classes=n_classes, blocks=[1, 1, 2, 2, 2, 3, 3, 4, 4, 4])
+
+
+def resnet_bottleneck(units=(3, 4, 6, 3), widths=(64, 128, 256, 512), n_classes=1000, hw=224, blocks=None,
+                      act=True):
+    """ImageNet ResNet with bottleneck units (ResNet-50 by default): 7x7/2
+    stem, BN, ReLU, 3x3/2 max pool, four stages whose first unit strides on
+    its 3x3 conv (stages 2-4), global pool, linear."""
+    m = Model("resnet%d" % (2 + 3 * sum(units)), (3, hw, hw), n_classes)
+    x = m.bn(m.conv(-1, widths[0], 7, 2, 3))
+    x = m.maxpool(m.relu(x) if act else x, 3, 2, 1)
+    for si, (wdt, nu) in enumerate(zip(widths, units)):
+        for u in range(nu):
+            x = bottleneck_unit(m, x, wdt, 2 if (si and not u) else 1, act)
+    m.new_unit()
+    m.linear(m.gap(x), n_classes)
+    return m.assign_blocks(blocks or [1] * m.n_units)
+
+
+def resnet50(n_classes=1000, act=True):
+    """ResNet-50, P = 4 blocks of units cut nearest to the quartiles of the
+    forward work: {stem, s1u1..s1u3, s2u1} {s2u2..s2u4, s3u1}
+    {s3u2..s3u5} {s3u6, s4u1..s4u3, head}."""
+    return resnet_bottleneck(n_classes=n_classes, act=act,
+                             blocks=[1, 1, 1, 1, 1, 2, 2, 2, 2, 3, 3, 3, 3, 4, 4, 4, 4, 4])
+

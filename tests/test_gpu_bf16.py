@@ -128,7 +128,15 @@ def _rn_mini(relu):
             PM.resnet_imagenet((1, 1, 1, 1), (16, 32, 64, 128), 10, 128, blocks=[1, 1, 2, 3, 4, 4], act=relu))
 
 
-MINIS = {"wrn10_2": (_wrn_mini, 4), "resnet_imagenet_mini": (_rn_mini, 2)}
+def _bottleneck_mini(relu):
+    return (OM.resnet_bottleneck((1, 2, 1, 1), (8, 16, 16, 32), 10, 64, relu=relu).set_blocks([1, 1, 2, 2, 3, 4, 4]),
+            PM.resnet_bottleneck((1, 2, 1, 1), (8, 16, 16, 32), 10, 64, blocks=[1, 1, 2, 2, 3, 4, 4], act=relu))
+
+
+# batch sizes: the bottleneck mini's last stage is 2x2 at 64x64 input, so its
+# batch norm sees 4 values per image and channel; batch 8 keeps the
+# normalisation from amplifying bf16 rounding (at batch 2, 8 values)
+MINIS = {"wrn10_2": (_wrn_mini, 4), "resnet_imagenet_mini": (_rn_mini, 2), "resnet_bottleneck_mini": (_bottleneck_mini, 8)}
 
 
 def _routing_lo(o):
@@ -261,13 +269,16 @@ def _teacher_forced_convs(o, ctx, x, img, rng, samples=96):
     return worst_f, worst_w
 
 
-@pytest.mark.parametrize("which", ["wrn16_8", "resnet18"])
+@pytest.mark.parametrize("which", ["wrn16_8", "resnet18", "resnet50"])
 def test_bf16_full_size_teacher_forced(which):
+    n = 128
     if which == "wrn16_8":
         o, p = OM.wrn16_8_p4(), PM.wrn16_8()
-    else:
+    elif which == "resnet18":
         o, p = OM.resnet18_p4(), PM.resnet18()
-    n = 128
+    else:
+        o, p = OM.resnet50_p4(), PM.resnet50()
+        n = 32                                # the paper's local batch for ResNet-50
     x = T.init_x(o.specs, 3041)
     img, lab = T.inputs(3042, n, o.in_shape, o.n_classes)
     img = bf(img)

@@ -414,6 +414,10 @@ MINIS = {
     "wrn10_2": (lambda: OM.wrn(10, 2, 10, 16).set_blocks([1, 1, 2, 3, 4]),
                 lambda: PM.wide_resnet(10, 2, 10, 16, blocks=[1, 1, 2, 3, 4]), 4),
     "resnet_imagenet_mini_relu_free": (lambda: _rn_mini_o(False), lambda: _rn_mini_p(False), 2),
+    # bottleneck units (the ResNet-50 family), ReLU-free with the max pool kept
+    "resnet_bottleneck_mini_relu_free": (
+        lambda: OM.resnet_bottleneck((1, 2, 1, 1), (8, 16, 16, 32), 10, 64, relu=False).set_blocks([1, 1, 2, 2, 3, 4, 4]),
+        lambda: PM.resnet_bottleneck((1, 2, 1, 1), (8, 16, 16, 32), 10, 64, blocks=[1, 1, 2, 2, 3, 4, 4], act=False), 2),
 }
 
 

@@ -21,6 +21,10 @@ PAIRS = [
     ("resnet18", PM.resnet18, OM.resnet18_p4),
     ("wrn10_2_mini", lambda: PM.wide_resnet(10, 2, 10, 16, blocks=[1, 1, 2, 3, 4]),
      lambda: OM.wrn(10, 2, 10, 16).set_blocks([1, 1, 2, 3, 4])),
+    ("resnet50", PM.resnet50, OM.resnet50_p4),
+    ("resnet_bottleneck_mini", lambda: PM.resnet_bottleneck((1, 2, 1, 1), (8, 16, 16, 32), 10, 64,
+                                                            blocks=[1, 1, 2, 2, 3, 4, 4]),
+     lambda: OM.resnet_bottleneck((1, 2, 1, 1), (8, 16, 16, 32), 10, 64).set_blocks([1, 1, 2, 2, 3, 4, 4])),
     ("resnet_imagenet_mini", lambda: PM.resnet_imagenet((1, 1, 1, 1), (16, 32, 64, 128), 10, 64,
                                                         blocks=[1, 1, 2, 3, 4, 4]),
      lambda: OM.resnet_imagenet((1, 1, 1, 1), (16, 32, 64, 128), 10, 64).set_blocks([1, 1, 2, 3, 4, 4])),

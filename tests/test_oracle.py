@@ -80,6 +80,8 @@ MINI_NETS = {
     "wrn_mini": lambda: M.wrn(10, 1, n_classes=7, hw=8).set_blocks([1, 1, 2, 3, 3]),
     "resnet18_mini": lambda: M.resnet_imagenet((1, 1, 1, 1), (4, 8, 8, 16), n_classes=12, hw=32)
     .set_blocks([1, 1, 2, 3, 4, 4]),
+    "resnet50_mini": lambda: M.resnet_bottleneck((1, 2, 1, 1), (2, 4, 4, 8), n_classes=9, hw=32)
+    .set_blocks([1, 1, 2, 2, 3, 4, 4]),
 }
 
 
@@ -127,7 +129,9 @@ def test_param_counts():
     assert round(M.wrn16_8_p4(100).d / 1e6, 1) == 11.0
     assert M.resnet20_p4(10).d == 272_474
     assert M.resnet20_p4(100).d == 278_324
-    for b in (M.tiny_p2, M.resnet20_p4, M.wrn16_8_p4, M.resnet18_p4):
+    # ResNet-50 (bottleneck units): the widely published 25,557,032
+    assert M.resnet50_p4().d == 25_557_032
+    for b in (M.tiny_p2, M.resnet20_p4, M.wrn16_8_p4, M.resnet18_p4, M.resnet50_p4):
         net = b()
         assert R.num_params(net) == net.d
 
@@ -149,6 +153,8 @@ def test_forward_macs():
     ~1.82 GMAC; CIFAR ResNet-20 ~41 MMAC; the 10-class ResNet-20 at batch 128
     gives 10.45 GFLOP forward."""
     assert abs(_fwd_macs(M.resnet18_p4()) / 1e9 - 1.82) < 0.01
+    # ResNet-50 at 224x224: the widely published ~4.09 GMAC
+    assert abs(_fwd_macs(M.resnet50_p4()) / 1e9 - 4.09) < 0.01
     r20 = _fwd_macs(M.resnet20_p4())
     assert abs(r20 * 2 * 128 / 1e9 - 10.45) < 0.02
     S = R.shapes(M.resnet18_p4())
@@ -318,7 +324,7 @@ def test_finite_differences_tiny_all_params():
     assert _fd_check(net, x, img, lab, range(net.d)) < 1e-5
 
 
-@pytest.mark.parametrize("name", ["resnet_mini", "wrn_mini", "resnet18_mini"])
+@pytest.mark.parametrize("name", ["resnet_mini", "wrn_mini", "resnet18_mini", "resnet50_mini"])
 def test_finite_differences_sampled(name):
     net = MINI_NETS[name]()
     x, img, lab = _inputs(net, 3, 32)
