@@ -178,15 +178,21 @@ hipError_t launch_bn_bwd_coef(const BnBwdArgs& a, const BnBwdCoef& k, float* coe
 hipError_t launch_bn_bwd_apply(int dt, const BnBwdArgs& a, const BnBwdCoef& k, void* dx1, bool acc1, void* dx2,
                                bool acc2, void* dres, bool accres, hipStream_t st);
 
-// ---- fused classifier head: global average pool, linear, softmax CE ----
+// ---- classifier head: global average pool, linear, softmax CE ----
+// Wide heads (C % 16 == 0, C*O >= kHeadWideMin) run as pooling + a matrix-core
+// product + softmax; narrow ones as one fused kernel per sample.
+constexpr long kHeadWideMin = 16384;
+bool head_wide(int C, int O);
 hipError_t launch_head_fwd(int dt, const void* x, int Nb, int HW, int C, const float* W, const float* b, int O,
                            const StepArgs* args, float* feat, float* logits, float* dz, float* loss_per,
                            hipStream_t st);
 // gW/gb (null: only the loss) and the batch-mean loss
 hipError_t launch_head_bwd_w(const float* dz, const float* feat, int Nb, int C, int O, float* gW, float* gb,
                              const float* loss_per, float* loss, hipStream_t st);
+// dx (written or accumulated) = (dz W) / HW broadcast over the pixels;
+// scratch: Nb*C floats, used by the wide form
 hipError_t launch_head_bwd_x(int dt, const float* dz, const float* W, int Nb, int HW, int C, int O, void* dx,
-                             bool acc, hipStream_t st);
+                             bool acc, float* scratch, hipStream_t st);
 
 // elementwise (n multiple of 4)
 hipError_t launch_relu_fwd(int dt, const void* x, void* y, long n, hipStream_t st);

@@ -1,6 +1,6 @@
 // misc.hip -- the non-convolution kernels of the step: batch-norm
 // statistics / apply / backward, ReLU, residual add, max pool, global
-// average pool, the linear head, softmax cross-entropy, layout conversions,
+// average pool, the plain linear layer, softmax cross-entropy, layout conversions,
 // the replica snapshot, the block SGD update and replica averaging.
 //
 // Activations are NHWC, stored as float32 or bfloat16 (act.h); every kernel
@@ -851,138 +851,6 @@ __global__ void loss_mean_k(const float* __restrict__ loss_per, int Nb, float* _
     float s = 0.f;
     for (int n = 0; n < Nb; ++n) s += loss_per[n];
     loss[0] = s / (float)Nb;
-}
-
-// Fused head, one workgroup per sample: global average pool of the sample's
-// HW x C activation, logits = W f + b, softmax cross-entropy against its
-// label.  Writes the pooled features (for the weight gradient), the logits,
-// dz = (softmax - onehot)/N and the sample's loss.  Reductions over classes
-// run as fixed-shape trees in LDS.
-constexpr int kHeadMaxC = 2048, kHeadMaxO = 4096;
-template <class T>
-__global__ __launch_bounds__(256) void head_fwd_k(const T* __restrict__ x, int Nb, int HW, int C,
-                                                  const float* __restrict__ W, const float* __restrict__ b, int O,
-                                                  const StepArgs* __restrict__ args, float* __restrict__ feat,
-                                                  float* __restrict__ logits, float* __restrict__ dz,
-                                                  float* __restrict__ loss_per) {
-    __shared__ float f_s[kHeadMaxC];
-    __shared__ float z_s[kHeadMaxO];
-    __shared__ float red[256];
-    const int n = blockIdx.x, t = threadIdx.x;
-    for (int c = t; c < C; c += 256) {
-        float s = 0.f;
-        for (int e = 0; e < HW; ++e) s += ld1(x, ((long)n * HW + e) * C + c);
-        const float f = s / (float)HW;
-        f_s[c] = f;
-        feat[(long)n * C + c] = f;
-    }
-    __syncthreads();
-    float mx = -INFINITY;
-    for (int o = t; o < O; o += 256) {
-        float z = b ? b[o] : 0.f;
-        const float* w = W + (long)o * C;
-        for (int c = 0; c < C; ++c) z += w[c] * f_s[c];
-        z_s[o] = z;
-        logits[(long)n * O + o] = z;
-        mx = fmaxf(mx, z);
-    }
-    red[t] = mx;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-        if (t < w) red[t] = fmaxf(red[t], red[t + w]);
-        __syncthreads();
-    }
-    const float zmax = red[0];
-    __syncthreads();
-    float se = 0.f;
-    for (int o = t; o < O; o += 256) se += expf(z_s[o] - zmax);
-    red[t] = se;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-        if (t < w) red[t] += red[t + w];
-        __syncthreads();
-    }
-    const float lse = zmax + logf(red[0]);
-    const int y = args->labels[n];
-    for (int o = t; o < O; o += 256)
-        dz[(long)n * O + o] = (expf(z_s[o] - lse) - (o == y ? 1.f : 0.f)) / (float)Nb;
-    if (t == 0) loss_per[n] = lse - z_s[y];
-}
-
-// dW[o][c] = sum_n dz[n][o] f[n][c]; db[o] = sum_n dz[n][o]; block 0 thread 0
-// also forms the batch-mean loss.
-__global__ void head_bwd_w_k(const float* __restrict__ dz, const float* __restrict__ feat, int Nb, int C, int O,
-                             float* __restrict__ gW, float* __restrict__ gb, const float* __restrict__ loss_per,
-                             float* __restrict__ loss) {
-    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx == 0) {
-        float s = 0.f;
-        for (int n = 0; n < Nb; ++n) s += loss_per[n];
-        loss[0] = s / (float)Nb;
-    }
-    if (!gW) return;
-    if (idx < (long)O * C) {
-        const int o = (int)(idx / C), c = (int)(idx - (long)o * C);
-        float s = 0.f;
-        for (int n = 0; n < Nb; ++n) s += dz[(long)n * O + o] * feat[(long)n * C + c];
-        gW[idx] = s;
-    } else if (gb && idx < (long)O * C + O) {
-        const int o = (int)(idx - (long)O * C);
-        float s = 0.f;
-        for (int n = 0; n < Nb; ++n) s += dz[(long)n * O + o];
-        gb[o] = s;
-    }
-}
-
-// one workgroup per sample: df = (dz W) / HW, broadcast over the HW pixels
-template <class T>
-__global__ __launch_bounds__(256) void head_bwd_x_k(const float* __restrict__ dz, const float* __restrict__ W,
-                                                    int Nb, int HW, int C, int O, T* __restrict__ dx, int acc) {
-    __shared__ float df[kHeadMaxC];
-    const int n = blockIdx.x, t = threadIdx.x;
-    for (int c = t; c < C; c += 256) {
-        float s = 0.f;
-        for (int o = 0; o < O; ++o) s += dz[(long)n * O + o] * W[(long)o * C + c];
-        df[c] = s / (float)HW;
-    }
-    __syncthreads();
-    const int C4 = C >> 2;
-    T* out = dx + (long)n * HW * C;
-    for (int i = t; i < HW * C4; i += 256) {
-        const int c = (i % C4) * 4;
-        const f4 v = f4{df[c], df[c + 1], df[c + 2], df[c + 3]};
-        st4(out, i, acc ? ld4(out, i) + v : v);
-    }
-}
-
-hipError_t launch_head_fwd(int dt, const void* x, int Nb, int HW, int C, const float* W, const float* b, int O,
-                           const StepArgs* args, float* feat, float* logits, float* dz, float* loss_per,
-                           hipStream_t st) {
-    if (C > kHeadMaxC || O > kHeadMaxO) return hipErrorInvalidValue;
-    if (dt == DT_BF16)
-        launch(head_fwd_k<bf16>, dim3(Nb), dim3(256), 0, st, (const bf16*)x, Nb, HW, C, W, b, O, args,
-                           feat, logits, dz, loss_per);
-    else
-        launch(head_fwd_k<float>, dim3(Nb), dim3(256), 0, st, (const float*)x, Nb, HW, C, W, b, O, args,
-                           feat, logits, dz, loss_per);
-    return hipGetLastError();
-}
-hipError_t launch_head_bwd_w(const float* dz, const float* feat, int Nb, int C, int O, float* gW, float* gb,
-                             const float* loss_per, float* loss, hipStream_t st) {
-    const long n = gW ? (long)O * C + O : 1;
-    launch(head_bwd_w_k, dim3(nblocks(n, 256)), dim3(256), 0, st, dz, feat, Nb, C, O, gW, gb, loss_per,
-                       loss);
-    return hipGetLastError();
-}
-hipError_t launch_head_bwd_x(int dt, const float* dz, const float* W, int Nb, int HW, int C, int O, void* dx,
-                             bool acc, hipStream_t st) {
-    if (C > kHeadMaxC) return hipErrorInvalidValue;
-    if (dt == DT_BF16)
-        launch(head_bwd_x_k<bf16>, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, (bf16*)dx, (int)acc);
-    else
-        launch(head_bwd_x_k<float>, dim3(Nb), dim3(256), 0, st, dz, W, Nb, HW, C, O, (float*)dx,
-                           (int)acc);
-    return hipGetLastError();
 }
 
 hipError_t launch_linear_fwd(const float* x, const float* W, const float* b, float* y, int Nb, int I, int O,

@@ -872,7 +872,7 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
             if (dx0)
                 LAUNCH("head", 2.0 * L.macs + eb * Min * Y.in0.c, st,
                        lpp::launch_head_bwd_x(dt, (const float*)dy, w.v + L.poff, N, Y.in0.h * Y.in0.w, Y.in0.c,
-                                              L.L.cout, dx0, pl.acc0[G.a] != 0, st));
+                                              L.L.cout, dx0, pl.acc0[G.a] != 0, w.ps0, st));
             break;
         }
         }
@@ -1006,6 +1006,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         if (Y.L.op == LPP_MAXPOOL) Y.aux = take((size_t)rows_out * Y.out.c);
         const long rin = (long)N * Y.in0.h * Y.in0.w;
         if (Y.L.op == LPP_BN) ps = std::max<long>(ps, (long)lpp::stats_tiles(rin, Y.out.c) * Y.out.c);
+        if (Y.L.op == LPP_LINEAR) ps = std::max<long>(ps, (long)N * Y.L.cin);   // the wide head's dfeat
         if (Y.L.op == LPP_CONV) {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
                             Y.L.pad};

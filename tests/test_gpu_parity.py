@@ -455,6 +455,23 @@ def test_architecture_minis_all_partitions(name):
         _partition_step(o, p, x, m0, img, lab, part, band=band)
 
 
+@pytest.mark.parametrize("n_classes,n", [(130, 20), (256, 136)])
+def test_wide_head_all_partitions(n_classes, n):
+    """Heads wide enough (C * O >= 16384) for the matrix-core form: 128 pooled
+    features and 130 classes (a ragged last tile of 16 outputs, a class count
+    that is not a multiple of 4) at batch 20, and 256 classes at batch 136
+    (more than one workgroup of sample tiles, ragged last tile).  ReLU-free
+    CIFAR ResNet with one unit per stage, every partition."""
+    o = OM.resnet_cifar(1, (16, 32, 128), n_classes, 16, relu=False).set_blocks([1, 1, 2, 3, 4])
+    p = PM.resnet_cifar(8, (16, 32, 128), n_classes, 16, blocks=[1, 1, 2, 3, 4], act=False)
+    x = T.init_x(o.specs, 3301 + n)
+    img, lab = T.inputs(3302 + n, n, o.in_shape, n_classes)
+    m0 = (np.random.default_rng(6).standard_normal(o.d) * 1e-2).astype(np.float32)
+    for part in range(0, 5):
+        say("wide head", n_classes, n, "partition", part)
+        _partition_step(o, p, x, m0, img, lab, part)
+
+
 # ---------------------------------------------------------------------------
 # the headline workload's full size (batch 128, momentum 0.9)
 # ---------------------------------------------------------------------------
