@@ -28,7 +28,7 @@
 #include <string.h>
 
 /* ---- layer records (the oracle's own; mirrored by oracle/lppref.py) ---- */
-enum { R_CONV = 0, R_BN = 1, R_RELU = 2, R_ADD = 3, R_MAXPOOL = 4, R_GAP = 5, R_LINEAR = 6 };
+enum { R_CONV = 0, R_BN = 1, R_RELU = 2, R_ADD = 3, R_MAXPOOL = 4, R_GAP = 5, R_LINEAR = 6, R_CONCAT = 7 };
 
 typedef struct {
     int op;
@@ -65,6 +65,12 @@ static int infer_shapes(const ref_layer* L, int nl, shp img, shp* S) {
             o.h = (a.h + 2 * L[l].pad - L[l].k) / L[l].stride + 1;
             o.w = (a.w + 2 * L[l].pad - L[l].k) / L[l].stride + 1;
             break;
+        case R_CONCAT: {   /* channels of in0, then channels of in1 */
+            shp b = in_shape(S, L[l].in1, img);
+            if (b.h != a.h || b.w != a.w) return -1;
+            o.c = a.c + b.c;
+            break;
+        }
         case R_GAP: o.h = 1; o.w = 1; break;
         case R_LINEAR:
             if (a.c * a.h * a.w != L[l].cin) return -1;
@@ -356,6 +362,16 @@ static void run_forward(const ref_layer* L, int nl, int N, shp img, const shp* S
         case R_MAXPOOL:
             maxpool_fwd(X0, a, N, y->k, y->stride, y->pad, act[l], S[l]);
             break;
+        case R_CONCAT: {
+            shp b = in_shape(S, y->in1, img);
+            const double* X1 = y->in1 < 0 ? images : act[y->in1];
+            long na = (long)a.c * a.h * a.w, nb = (long)b.c * b.h * b.w;
+            for (int n = 0; n < N; ++n) {
+                memcpy(act[l] + n * (na + nb), X0 + n * na, sizeof(double) * (size_t)na);
+                memcpy(act[l] + n * (na + nb) + na, X1 + n * nb, sizeof(double) * (size_t)nb);
+            }
+            break;
+        }
         case R_GAP: {
             long hw = (long)a.h * a.w;
             for (long nc = 0; nc < (long)N * a.c; ++nc) {
@@ -469,6 +485,16 @@ static int forward_backward_impl(const ref_layer* L, int nl, int N, int C, int H
             case R_MAXPOOL:
                 if (dX0) maxpool_bwd(X0, a, N, y->k, y->stride, y->pad, dY, S[l], dX0);
                 break;
+            case R_CONCAT: {
+                shp b = in_shape(S, y->in1, img);
+                double* dX1 = y->in1 < 0 ? NULL : dact[y->in1];
+                long na = (long)a.c * a.h * a.w, nb = (long)b.c * b.h * b.w;
+                for (int n = 0; n < N; ++n) {
+                    if (dX0) for (long i = 0; i < na; ++i) dX0[n * na + i] += dY[n * (na + nb) + i];
+                    if (dX1) for (long i = 0; i < nb; ++i) dX1[n * nb + i] += dY[n * (na + nb) + na + i];
+                }
+                break;
+            }
             case R_GAP: {
                 long hw = (long)a.h * a.w;
                 if (dX0)

@@ -24,10 +24,16 @@ notes):
             linear
   resnet18  ImageNet ResNet-18: 7x7 stride-2 stem + BN + ReLU + 3x3 stride-2
             max pool, four stages of two basic units, projection shortcuts
+  resnet50  ImageNet ResNet-50: the same stem, bottleneck units (3, 4, 6, 3)
+  squeezenet  SqueezeNet v1.0's Fire modules (squeeze 1x1, expand 1x1 and
+            3x3, outputs concatenated along channels) on 32x32 inputs: 3x3
+            stem, max pools after the stem, fire4 and fire8, a 1x1 conv
+            classifier with ReLU, global average pool (the logits); every
+            conv has a bias, no batch norm
 """
 from __future__ import annotations
 
-CONV, BN, RELU, ADD, MAXPOOL, GAP, LINEAR = range(7)
+CONV, BN, RELU, ADD, MAXPOOL, GAP, LINEAR, CONCAT = range(8)
 
 
 class Net:
@@ -83,6 +89,10 @@ class Net:
 
     def gap(self, x):
         return self._plain(GAP, x)
+
+    def concat(self, x, y):
+        """Channels of x followed by channels of y (same spatial size)."""
+        return self._plain(CONCAT, x, y)
 
     def linear(self, x, cin, cout):
         rec = dict(op=LINEAR, in0=x, in1=-1, cin=cin, cout=cout, k=0, stride=1, pad=0, bias=1,
@@ -288,6 +298,45 @@ def resnet_bottleneck(units_per_stage=(3, 4, 6, 3), widths=(64, 128, 256, 512), 
     return net
 
 
+# SqueezeNet v1.0's Fire modules (squeeze, expand 1x1, expand 3x3)
+SQUEEZENET_FIRES = ((16, 64, 64), (16, 64, 64), (32, 128, 128), (32, 128, 128),
+                    (48, 192, 192), (48, 192, 192), (64, 256, 256), (64, 256, 256))
+
+
+def _fire(net, x, cin, s, e1, e3, relu=True):
+    """Fire module: squeeze 1x1 conv (s) + ReLU, then expand 1x1 (e1) and
+    expand 3x3 (e3, padding 1) convs on the squeezed map, each + ReLU, their
+    outputs concatenated (e1 channels first).  One unit."""
+    net.next_unit()
+    act = net.relu if relu else (lambda t: t)
+    sq = act(net.conv(x, cin, s, 1, 1, 0, bias=True))
+    a = act(net.conv(sq, s, e1, 1, 1, 0, bias=True))
+    b = act(net.conv(sq, s, e3, 3, 1, 1, bias=True))
+    return net.concat(a, b)
+
+
+def squeezenet(n_classes=10, hw=32, stem=96, fires=SQUEEZENET_FIRES, pools_after=(2, 6), relu=True):
+    """SqueezeNet v1.0 for 32x32 inputs.  Units: 0 = stem (3x3 conv + ReLU,
+    3x3/2 max pool), one per Fire module (a 3x3/2 max pool follows the
+    modules listed in pools_after: fire4 and fire8), last = the classifier
+    (1x1 conv to the classes + ReLU, global average pool).  relu=False drops
+    every ReLU."""
+    net = Net("squeezenet", 3, hw, hw, n_classes)
+    act = net.relu if relu else (lambda t: t)
+    x = act(net.conv(-1, 3, stem, 3, 1, 1, bias=True))
+    x = net.maxpool(x, 3, 2, 1)
+    cin = stem
+    for i, (s, e1, e3) in enumerate(fires):
+        x = _fire(net, x, cin, s, e1, e3, relu)
+        cin = e1 + e3
+        if i in pools_after:
+            x = net.maxpool(x, 3, 2, 1)
+    net.next_unit()
+    x = act(net.conv(x, cin, n_classes, 1, 1, 0, bias=True))
+    net.gap(x)
+    return net
+
+
 # ---- the workloads' models with their partitions (units -> blocks) ----
 
 def tiny_p2():
@@ -316,3 +365,9 @@ def resnet50_p4(n_classes=1000, relu=True):
     return resnet_bottleneck(n_classes=n_classes, relu=relu).set_blocks(
         [1, 1, 1, 1, 1, 2, 2, 2, 2, 3, 3, 3, 3, 4, 4, 4, 4, 4])
 
+
+def squeezenet_p4(n_classes=10, relu=True):
+    # units: stem, fire2..fire9, classifier; cuts nearest to the quartiles of
+    # the forward work: {stem, fire2, fire3} {fire4, fire5} {fire6, fire7}
+    # {fire8, fire9, classifier}
+    return squeezenet(n_classes, relu=relu).set_blocks([1, 1, 1, 2, 2, 3, 3, 4, 4, 4])

@@ -48,6 +48,8 @@ def torch_loss(net, x, images, labels):
             y = F.max_pool2d(a, rec["k"], rec["stride"], rec["pad"])
         elif op == M.GAP:
             y = a.mean(dim=(2, 3), keepdim=True)
+        elif op == M.CONCAT:
+            y = torch.cat([a, img if rec["in1"] < 0 else acts[rec["in1"]]], dim=1)
         elif op == M.LINEAR:
             n = rec["cout"] * rec["cin"]
             w = x[rec["poff"]:rec["poff"] + n].view(rec["cout"], rec["cin"])
@@ -82,6 +84,8 @@ MINI_NETS = {
     .set_blocks([1, 1, 2, 3, 4, 4]),
     "resnet50_mini": lambda: M.resnet_bottleneck((1, 2, 1, 1), (2, 4, 4, 8), n_classes=9, hw=32)
     .set_blocks([1, 1, 2, 2, 3, 4, 4]),
+    "squeezenet_mini": lambda: M.squeezenet(7, 16, 8, ((4, 4, 8), (4, 8, 4), (8, 8, 8)), (1,))
+    .set_blocks([1, 1, 2, 3, 4]),
 }
 
 
@@ -102,7 +106,8 @@ def test_block_subtraction_worked_example():
     assert a.tolist() == g["expected"]
 
 
-@pytest.mark.parametrize("builder", [M.tiny_p2, M.resnet20_p4, M.wrn16_8_p4, M.resnet18_p4])
+@pytest.mark.parametrize("builder", [M.tiny_p2, M.resnet20_p4, M.wrn16_8_p4, M.resnet18_p4, M.resnet50_p4,
+                                     M.squeezenet_p4])
 def test_partition_definition(builder):
     """Sec. 3 eq. (partition): b_0 = 0 < b_1 < ... < b_P = d, block 0 is the
     whole vector, blocks 1..P are disjoint and cover it."""
@@ -131,7 +136,12 @@ def test_param_counts():
     assert M.resnet20_p4(100).d == 278_324
     # ResNet-50 (bottleneck units): the widely published 25,557,032
     assert M.resnet50_p4().d == 25_557_032
-    for b in (M.tiny_p2, M.resnet20_p4, M.wrn16_8_p4, M.resnet18_p4, M.resnet50_p4):
+    # SqueezeNet v1.0 has the published 1,248,424 parameters at 1000 classes
+    # with its 7x7 stem (7*7*3*96 + 96 = 14,208); the 32x32 variant's 3x3
+    # stem has 3*3*3*96 + 96 = 2,688 and its classifier 512*C + C
+    assert M.squeezenet_p4(10).d == 1_248_424 - 14_208 + 2_688 - (512 * 1000 + 1000) + (512 * 10 + 10) == 729_034
+    assert M.squeezenet_p4(100).d == 729_034 + 90 * 513
+    for b in (M.tiny_p2, M.resnet20_p4, M.wrn16_8_p4, M.resnet18_p4, M.resnet50_p4, M.squeezenet_p4):
         net = b()
         assert R.num_params(net) == net.d
 
@@ -324,7 +334,7 @@ def test_finite_differences_tiny_all_params():
     assert _fd_check(net, x, img, lab, range(net.d)) < 1e-5
 
 
-@pytest.mark.parametrize("name", ["resnet_mini", "wrn_mini", "resnet18_mini", "resnet50_mini"])
+@pytest.mark.parametrize("name", ["resnet_mini", "wrn_mini", "resnet18_mini", "resnet50_mini", "squeezenet_mini"])
 def test_finite_differences_sampled(name):
     net = MINI_NETS[name]()
     x, img, lab = _inputs(net, 3, 32)
@@ -418,3 +428,28 @@ def test_sequential_schedule_composes_to_averaged_update():
     np.testing.assert_allclose(reps[0], x0 - lr / K * total, rtol=0, atol=1e-14)
     # x_k + (vbar - x_k) equals vbar only up to one rounding per replica
     np.testing.assert_allclose(reps[0], reps[1], rtol=0, atol=1e-15)
+
+
+def test_concat_forward_and_backward_closed_form():
+    """Concatenation along channels: the output holds x's channels then y's,
+    and the gradient reaching each input is its slice of the output's.  A
+    two-branch net (1x1 convs a, b of the image, concatenated, pooled) has
+    logits = [mean(a), mean(b)] and the loss gradient of each branch's bias
+    is the matching slice of dlogits summed over the batch."""
+    net = M.Net("cat", 3, 4, 4, 5)
+    a = net.conv(-1, 3, 2, 1, 1, 0, bias=True)
+    b = net.conv(-1, 3, 3, 1, 1, 0, bias=True)
+    net.gap(net.concat(a, b))
+    net.set_blocks([1])
+    x, img, lab = _inputs(net, 4, 41)
+    loss, logits, g = R.forward_backward(net, x, img, lab)
+    wa, ba = x[0:6].reshape(2, 3), x[6:8]
+    wb, bb = x[8:17].reshape(3, 3), x[17:20]
+    m = img.astype(np.float64).mean(axis=(2, 3))    # [N, 3]
+    want = np.concatenate([m @ wa.T + ba, m @ wb.T + bb], axis=1)
+    np.testing.assert_allclose(logits, want, rtol=0, atol=1e-13)
+    z = want - want.max(axis=1, keepdims=True)
+    p = np.exp(z) / np.exp(z).sum(axis=1, keepdims=True)
+    dz = (p - np.eye(5)[lab]) / len(lab)
+    np.testing.assert_allclose(g[6:8], dz[:, :2].sum(axis=0), rtol=0, atol=1e-14)
+    np.testing.assert_allclose(g[17:20], dz[:, 2:].sum(axis=0), rtol=0, atol=1e-14)
