@@ -45,7 +45,8 @@ PEAK_FP32_TFLOPS = 157.3
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 FAMILIES = ["conv_fwd", "conv_dgrad", "conv_wgrad", "wgrad_reduce", "bn_stats", "bn_act", "bn_bwd", "head",
-            "relu", "add", "maxpool", "gap", "linear", "softmax_ce", "bias_grad", "snapshot", "image", "sgd_update"]
+            "relu", "add", "concat", "maxpool", "gap", "linear", "softmax_ce", "bias_grad", "snapshot", "image",
+            "sgd_update"]
 
 
 def parse():
@@ -63,7 +64,7 @@ def parse():
     ap.add_argument("--issue-threads", type=int, default=1,
                     help="host threads issuing steps; each owns a fixed set of workers")
     ap.add_argument("--no-workloads", action="store_true", help="skip the other configurations")
-    ap.add_argument("--workloads", default="resnet20_100_k4,wrn16_8_bf16,resnet18_bf16,resnet50_bf16",
+    ap.add_argument("--workloads", default="resnet20_100_k4,wrn16_8_bf16,resnet18_bf16,resnet50_bf16,squeezenet_k2",
                     help="comma-separated subset of the other configurations")
     ap.add_argument("--workload-steps", type=int, default=64)
     ap.add_argument("--only-workload", default=None, help="run just one of the other configurations (for profiling)")
@@ -138,6 +139,9 @@ def _workloads():
                           "ResNet-50 (1000 classes), batch 32 of 3x224x224, bf16 activations / fp32 master "
                           "weights, K=2 x P=4 workers on 8 HIP streams, averaging every 8 steps per replica, "
                           "momentum 0.9, async", 32),
+        "squeezenet_k2": (lambda: PM.squeezenet_p4(10), (3, 32, 32), 10, lpp.FP32, 2, 8,
+                          "SqueezeNet v1.0 (10 classes, 32x32), batch 128, fp32, K=2 replicas x P=4 workers on 8 "
+                          "HIP streams, averaging every 8 steps per replica, momentum 0.9, async"),
     }
 
 
@@ -180,8 +184,7 @@ def run_workload(torch, lpp, name, steps, B=128, P=4):
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     fams = {}
-    for f in ("conv_fwd", "conv_dgrad", "conv_wgrad", "wgrad_reduce", "bn_stats", "bn_act", "bn_bwd", "head",
-              "maxpool", "add", "snapshot", "image", "sgd_update"):
+    for f in FAMILIES:
         ctx.timer_enable(f)
         for s in range(P):
             img, lab = pool[s % len(pool)]

@@ -61,7 +61,8 @@ enum lpp_op {
     LPP_ADD = 3,     /* elementwise sum of in0 and in1                        */
     LPP_MAXPOOL = 4, /* k x k window, stride, pad; padding never wins         */
     LPP_GAP = 5,     /* mean over H x W                                       */
-    LPP_LINEAR = 6   /* y = x W^T + b on the flattened input; params W, b     */
+    LPP_LINEAR = 6,  /* y = x W^T + b on the flattened input; params W, b     */
+    LPP_CONCAT = 7   /* channels of in0 followed by channels of in1 (same H, W) */
 };
 
 enum lpp_dtype { LPP_FP32 = 0, LPP_BF16 = 1 };
@@ -132,7 +133,12 @@ typedef struct {
  * d, the block ranges (Sec. 3, eq. (partition)) and the flops of the
  * forward pass and of the truncated backward pass of each partition.
  * Blocks must be contiguous runs of layers in parameter order numbered
- * 1..P without gaps.  Returns LPP_EINVAL for an invalid description.
+ * 1..P without gaps.  The last layer (a linear layer or a global pool) has
+ * n_classes outputs: the logits.  Channel counts are multiples of 4 (of 8 for
+ * bf16 convs), except the output of a 1x1, stride-1, unpadded fp32 conv,
+ * which may then feed only ReLU, pooling or linear layers.  Returns
+ * LPP_EINVAL for an invalid description, LPP_EUNSUPPORTED for a valid one
+ * outside these limits.
  */
 int lpp_describe(const lpp_model_desc* desc, int P, lpp_model_info* out);
 

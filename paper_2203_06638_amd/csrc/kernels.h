@@ -199,6 +199,12 @@ hipError_t launch_relu_fwd(int dt, const void* x, void* y, long n, hipStream_t s
 hipError_t launch_relu_bwd(int dt, const void* dy, const void* x, void* dx, long n, bool accumulate, hipStream_t st);
 hipError_t launch_add_fwd(int dt, const void* a, const void* b, void* y, long n, hipStream_t st);
 hipError_t launch_copy_acc(int dt, const void* src, void* dst, long n, bool accumulate, hipStream_t st);
+// channel concatenation of two NHWC tensors with `rows` pixels (ca, cb
+// multiples of 4) and its backward (da / db null when not wanted)
+hipError_t launch_concat_fwd(int dt, const void* a, int ca, const void* b, int cb, void* y, long rows,
+                             hipStream_t st);
+hipError_t launch_concat_bwd(int dt, const void* dy, long rows, int ca, int cb, void* da, bool acc_a, void* db,
+                             bool acc_b, hipStream_t st);
 
 hipError_t launch_maxpool_fwd(int dt, const void* x, void* y, uint8_t* arg, int Nb, int H, int W, int C, int Ho,
                               int Wo, int k, int stride, int pad, hipStream_t st);

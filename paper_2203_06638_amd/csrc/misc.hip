@@ -1,6 +1,7 @@
 // misc.hip -- the non-convolution kernels of the step: batch-norm
 // statistics / apply / backward, ReLU, residual add, max pool, global
-// average pool, the plain linear layer, softmax cross-entropy, layout conversions,
+// average pool, channel concatenation, the plain linear layer, softmax
+// cross-entropy, layout conversions,
 // the replica snapshot, the block SGD update and replica averaging.
 //
 // Activations are NHWC, stored as float32 or bfloat16 (act.h); every kernel
@@ -667,6 +668,66 @@ hipError_t launch_copy_acc(int dt, const void* src, void* dst, long n, bool accu
     else
         launch(copy_acc_k<float>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const float*)src, (float*)dst,
                            n / 4, (int)accumulate);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------
+// channel concatenation: y[r] = (a[r], b[r]) per pixel row r, ca then cb
+// channels (both multiples of 4); one thread per output channel quad
+// ------------------------------------------------------------------------
+
+template <class T>
+__global__ void concat_fwd_k(const T* __restrict__ a, const T* __restrict__ b, T* __restrict__ y, long rows, int aq,
+                             int bq) {
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    const int cq = aq + bq;
+    if (i >= rows * cq) return;
+    const long r = i / cq;
+    const int q = (int)(i - r * cq);
+    st4(y, i, q < aq ? ld4(a, r * aq + q) : ld4(b, r * bq + (q - aq)));
+}
+
+// da / db (null: not wanted) receive their slices of dy, written or added
+template <class T>
+__global__ void concat_bwd_k(const T* __restrict__ dy, long rows, int aq, int bq, T* __restrict__ da, int acc_a,
+                             T* __restrict__ db, int acc_b) {
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    const int cq = aq + bq;
+    if (i >= rows * cq) return;
+    const long r = i / cq;
+    const int q = (int)(i - r * cq);
+    const f4 g = ld4(dy, i);
+    if (q < aq) {
+        if (da) st4(da, r * aq + q, acc_a ? ld4(da, r * aq + q) + g : g);
+    } else if (db) {
+        const long j = r * bq + (q - aq);
+        st4(db, j, acc_b ? ld4(db, j) + g : g);
+    }
+}
+
+hipError_t launch_concat_fwd(int dt, const void* a, int ca, const void* b, int cb, void* y, long rows,
+                             hipStream_t st) {
+    if ((ca | cb) & 3) return hipErrorInvalidValue;
+    const dim3 grid(nblocks(rows * ((ca + cb) / 4), 256));
+    if (dt == DT_BF16)
+        launch(concat_fwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)a, (const bf16*)b, (bf16*)y, rows, ca / 4,
+               cb / 4);
+    else
+        launch(concat_fwd_k<float>, grid, dim3(256), 0, st, (const float*)a, (const float*)b, (float*)y, rows,
+               ca / 4, cb / 4);
+    return hipGetLastError();
+}
+hipError_t launch_concat_bwd(int dt, const void* dy, long rows, int ca, int cb, void* da, bool acc_a, void* db,
+                             bool acc_b, hipStream_t st) {
+    if ((ca | cb) & 3) return hipErrorInvalidValue;
+    if (!da && !db) return hipSuccess;
+    const dim3 grid(nblocks(rows * ((ca + cb) / 4), 256));
+    if (dt == DT_BF16)
+        launch(concat_bwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)dy, rows, ca / 4, cb / 4, (bf16*)da,
+               (int)acc_a, (bf16*)db, (int)acc_b);
+    else
+        launch(concat_bwd_k<float>, grid, dim3(256), 0, st, (const float*)dy, rows, ca / 4, cb / 4, (float*)da,
+               (int)acc_a, (float*)db, (int)acc_b);
     return hipGetLastError();
 }
 

@@ -56,6 +56,8 @@ struct Layer {
     long poff = -1, np = 0;       // canonical parameter range
     long wcount = 0;              // conv/linear weight count (before the bias)
     int cin_p = 0;                // conv: stored channels of the input
+    bool pw = false;              // conv: 1x1, stride 1, no padding, output channels not a multiple of 4 --
+                                  //   run as a linear layer applied to every pixel (fp32)
     long wf_off = -1, wd_off = -1;// conv: W_f / W_d in the worker's weight buffer (elements)
     double macs = 0;              // forward multiply-adds (conv, linear)
     lpp::WgradPlan wg{};
@@ -76,7 +78,10 @@ struct Plan {
 // Execution groups.  A group runs one fused kernel sequence and
 // materialises exactly one layer output (`out`); layers inside a group whose
 // outputs feed nothing else are never stored.
-enum GKind { G_CONV, G_BNACT, G_RELU, G_ADD, G_MAXPOOL, G_GAP, G_LINEAR, G_HEAD };
+enum GKind { G_CONV, G_BNACT, G_RELU, G_ADD, G_MAXPOOL, G_GAP, G_LINEAR, G_HEAD, G_CONCAT };
+
+// ops that read a second input (in1)
+inline bool two_inputs(int op) { return op == LPP_ADD || op == LPP_CONCAT; }
 struct Group {
     GKind kind = G_CONV;
     int out = -1;       // the layer whose output this group stores
@@ -157,7 +162,12 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
             o.w = (Y.in0.w + 2 * L.pad - L.k) / L.stride + 1;
             if (Y.in0.h + 2 * L.pad < L.k || Y.in0.w + 2 * L.pad < L.k || o.h < 1 || o.w < 1)
                 return fail(LPP_EINVAL, std::string(where) + "conv output is empty");
-            if (L.cout % 4) return fail(LPP_EUNSUPPORTED, std::string(where) + "cout must be a multiple of 4");
+            if (L.cout % 4) {
+                if (bf || L.k != 1 || L.stride != 1 || L.pad != 0 || L.in0 < 0)
+                    return fail(LPP_EUNSUPPORTED, std::string(where) +
+                                "cout must be a multiple of 4 (except for 1x1, stride-1, unpadded fp32 convs)");
+                Y.pw = true;
+            }
             Y.cin_p = L.in0 < 0 ? M.img_cp : L.cin;
             if (Y.cin_p % 4) return fail(LPP_EUNSUPPORTED, std::string(where) + "cin must be a multiple of 4");
             if (bf && (Y.cin_p % 8 || L.cout % 8))
@@ -182,6 +192,16 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
             consumers[L.in1]++;
             if (Y.in1.c != Y.in0.c || Y.in1.h != Y.in0.h || Y.in1.w != Y.in0.w)
                 return fail(LPP_EINVAL, std::string(where) + "add inputs differ in shape");
+            break;
+        case LPP_CONCAT:
+            if (L.in1 < -1 || L.in1 >= l) return fail(LPP_EINVAL, std::string(where) + "in1 must be an earlier layer");
+            if (L.in1 < 0) return fail(LPP_EUNSUPPORTED, std::string(where) + "concat cannot read the image");
+            Y.in1 = M.layers[L.in1].out;
+            consumers[L.in1]++;
+            if (Y.in1.h != Y.in0.h || Y.in1.w != Y.in0.w)
+                return fail(LPP_EINVAL, std::string(where) + "concat inputs differ in spatial size");
+            if (Y.in1.c % 4) return fail(LPP_EUNSUPPORTED, std::string(where) + "concat channels must be multiples of 4");
+            o.c = Y.in0.c + Y.in1.c;
             break;
         case LPP_MAXPOOL:
             if (L.k < 1 || L.stride < 1 || L.pad < 0 || L.pad >= L.k || L.k * L.k > 255)
@@ -210,8 +230,16 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
         }
         Y.out = o;
         Y.dt = (L.op == LPP_GAP || L.op == LPP_LINEAR) ? lpp::DT_F32 : M.dt;
-        if (L.op != LPP_LINEAR && o.c % 4)
+        // tensors whose channels are not a multiple of 4 (a pointwise conv's
+        // output) may only feed ReLU, pooling and linear layers
+        const bool any_c = L.op == LPP_LINEAR || L.op == LPP_GAP || L.op == LPP_RELU;
+        if (o.c % 4 && !any_c && !Y.pw)
             return fail(LPP_EUNSUPPORTED, std::string(where) + "channel counts must be multiples of 4");
+        if (L.in0 >= 0 && Y.in0.c % 4 && !any_c)
+            return fail(LPP_EUNSUPPORTED, std::string(where) +
+                        "only ReLU, pooling and linear layers may read channels that are not a multiple of 4");
+        if (L.op == LPP_RELU && ((long)D.batch * o.numel()) % 4)
+            return fail(LPP_EUNSUPPORTED, std::string(where) + "relu element count must be a multiple of 4");
         if ((double)D.batch * o.numel() >= 2147483647.0 || (double)D.batch * Y.in0.h * Y.in0.w * ceil4(Y.in0.c) >= 2147483647.0)
             return fail(LPP_EUNSUPPORTED, std::string(where) + "activation exceeds 2^31 elements");
         if (Y.np > 0) {
@@ -227,8 +255,8 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
     for (int i = 1; i <= P; ++i)
         if (!block_seen[i]) return fail(LPP_EINVAL, "every block 1..P must own parameters");
     const Layer& last = M.layers[n - 1];
-    if (last.L.op != LPP_LINEAR || last.out.c != D.n_classes)
-        return fail(LPP_EINVAL, "the last layer must be a linear layer with n_classes outputs");
+    if ((last.L.op != LPP_LINEAR && last.L.op != LPP_GAP) || last.out.c != D.n_classes)
+        return fail(LPP_EINVAL, "the last layer must be a linear layer or a global pool with n_classes outputs");
     for (int l = 0; l < n - 1; ++l)
         if (consumers[l] == 0) return fail(LPP_EINVAL, "every layer but the last must feed another layer");
     if (consumers[n - 1] != 0) return fail(LPP_EINVAL, "the logits layer cannot feed another layer");
@@ -265,7 +293,7 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
             const bool inblk = Y.np > 0 && (i == 0 || Y.L.block == i);
             pl.wgrad[l] = inblk;
             pl.run[l] = inblk || (Y.L.in0 >= 0 && pl.run[Y.L.in0]) ||
-                        (Y.L.op == LPP_ADD && Y.L.in1 >= 0 && pl.run[Y.L.in1]);
+                        (two_inputs(Y.L.op) && Y.L.in1 >= 0 && pl.run[Y.L.in1]);
         }
         std::vector<char> written(n, 0);
         for (int l = n - 1; l >= 0; --l) {
@@ -277,7 +305,7 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
                 pl.acc0[l] = written[a];
                 written[a] = 1;
             }
-            if (Y.L.op == LPP_ADD) {
+            if (two_inputs(Y.L.op)) {
                 const int b = Y.L.in1;
                 if (b >= 0 && pl.run[b]) {
                     pl.din1[l] = 1;
@@ -295,7 +323,7 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
     for (int l = 0; l < n; ++l) {
         const lpp_layer& L = M.layers[l].L;
         if (L.in0 >= 0) M.consumers[L.in0].push_back(l);
-        if (L.op == LPP_ADD && L.in1 >= 0 && L.in1 != L.in0) M.consumers[L.in1].push_back(l);
+        if (two_inputs(L.op) && L.in1 >= 0 && L.in1 != L.in0) M.consumers[L.in1].push_back(l);
     }
     return LPP_OK;
 }
@@ -349,7 +377,7 @@ void build_groups(Model& M, bool fused) {
             }
         } else if (op_l == LPP_GAP) {
             const int c = fused ? sole(l) : -1;
-            if (c == n - 1 && op(c) == LPP_LINEAR) {
+            if (c == n - 1 && op(c) == LPP_LINEAR && M.layers[l].in0.c % 4 == 0) {
                 g.kind = G_HEAD;
                 g.a = l;
                 g.lin = g.out = c;
@@ -358,8 +386,11 @@ void build_groups(Model& M, bool fused) {
                 g.a = g.out = l;
             }
         } else {
-            g.kind = op_l == LPP_RELU ? G_RELU : op_l == LPP_ADD ? G_ADD : op_l == LPP_MAXPOOL ? G_MAXPOOL
-                                                                                              : G_LINEAR;
+            g.kind = op_l == LPP_RELU      ? G_RELU
+                     : op_l == LPP_ADD     ? G_ADD
+                     : op_l == LPP_MAXPOOL ? G_MAXPOOL
+                     : op_l == LPP_CONCAT  ? G_CONCAT
+                                           : G_LINEAR;
             g.a = g.out = l;
         }
         for (int x : {g.a, g.bn2, g.add, g.relu, g.lin})
@@ -600,7 +631,11 @@ int run_forward(lpp_ctx* c, Worker& w) {
             if (G.stats_bn >= 0) sums = c->fixed_order ? lpp::BnSums{nullptr, w.ps0, w.ps1, nullptr}
                                                        : lpp::BnSums{c->acc_fwd(w, G.stats_bn), nullptr, nullptr, nullptr};
             const lpp::BnSums* sp = G.stats_bn >= 0 ? &sums : nullptr;
-            if (bf)
+            if (Y.pw)
+                LAUNCH("conv_fwd", 2.0 * Y.macs, st,
+                       lpp::launch_linear_fwd((const float*)x0, w.v + Y.poff, bias, (float*)c->act(w, G.a), Mrows,
+                                              Y.L.cin, Y.L.cout, st));
+            else if (bf)
                 LAUNCH("conv_fwd", 2.0 * Y.macs, st,
                        lpp::launch_conv_bf16(lpp::CONV_FWD, (const uint16_t*)x0, (const uint16_t*)c->wf(w, Y), bias,
                                              (uint16_t*)c->act(w, G.a), g, false, sp, st));
@@ -662,6 +697,10 @@ int run_forward(lpp_ctx* c, Worker& w) {
             LAUNCH("add", 3.0 * eb * Mrows * Y.out.c, st,
                    lpp::launch_add_fwd(dt, x0, c->act(w, Y.L.in1), c->act(w, G.a), Mrows * Y.out.c, st));
             break;
+        case G_CONCAT:
+            LAUNCH("concat", 2.0 * eb * Mrows * Y.out.c, st,
+                   lpp::launch_concat_fwd(dt, x0, Y.in0.c, c->act(w, Y.L.in1), Y.in1.c, c->act(w, G.a), Mrows, st));
+            break;
         case G_MAXPOOL:
             LAUNCH("maxpool", eb * Mrows * Y.out.c, st,
                    lpp::launch_maxpool_fwd(dt, x0, c->act(w, G.a), (uint8_t*)c->aux(w, G.a), N, Y.in0.h, Y.in0.w,
@@ -721,6 +760,18 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
         const long Min = (long)N * Y.in0.h * Y.in0.w;
         switch (G.kind) {
         case G_CONV: {
+            if (Y.pw) {
+                if (pl.wgrad[G.a])
+                    LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
+                           lpp::launch_linear_bwd_w((const float*)dy, (const float*)x0, w.g + Y.poff,
+                                                    Y.L.bias ? w.g + Y.poff + Y.wcount : nullptr, (int)Min, Y.L.cin,
+                                                    Y.L.cout, st));
+                if (dx0)
+                    LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
+                           lpp::launch_linear_bwd_x((const float*)dy, w.v + Y.poff, (float*)dx0, (int)Min, Y.L.cin,
+                                                    Y.L.cout, pl.acc0[G.a] != 0, st));
+                break;
+            }
             if (pl.wgrad[G.a]) {
                 const int Ktot = Y.L.k * Y.L.k * Y.cin_p;
                 if (bf)
@@ -833,6 +884,12 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
             if (pl.din1[G.a])
                 LAUNCH("add", 2.0 * eb * Min * Y.out.c, st,
                        lpp::launch_copy_acc(dt, dy, c->dact(w, Y.L.in1), Min * Y.out.c, pl.acc1[G.a] != 0, st));
+            break;
+        case G_CONCAT:
+            if (dx0 || pl.din1[G.a])
+                LAUNCH("concat", (1.0 + (dx0 ? 1.0 : 0.0) + (pl.din1[G.a] ? 1.0 : 0.0)) * eb * Min * Y.out.c, st,
+                       lpp::launch_concat_bwd(dt, dy, Min, Y.in0.c, Y.in1.c, dx0, pl.acc0[G.a] != 0,
+                                              pl.din1[G.a] ? c->dact(w, Y.L.in1) : nullptr, pl.acc1[G.a] != 0, st));
             break;
         case G_MAXPOOL:
             if (dx0)
@@ -964,7 +1021,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
     std::vector<lpp::SnapConv> snaps;
     long wf = 0;
     for (auto& Y : M.layers) {
-        if (Y.L.op != LPP_CONV) continue;
+        if (Y.L.op != LPP_CONV || Y.pw) continue;
         const long nf = (long)Y.L.cout * Y.L.k * Y.L.k * Y.cin_p;
         const long nd = (long)Y.L.cin * Y.L.k * Y.L.k * Y.L.cout;
         Y.wf_off = wf;
@@ -1007,7 +1064,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         const long rin = (long)N * Y.in0.h * Y.in0.w;
         if (Y.L.op == LPP_BN) ps = std::max<long>(ps, (long)lpp::stats_tiles(rin, Y.out.c) * Y.out.c);
         if (Y.L.op == LPP_LINEAR) ps = std::max<long>(ps, (long)N * Y.L.cin);   // the wide head's dfeat
-        if (Y.L.op == LPP_CONV) {
+        if (Y.L.op == LPP_CONV && !Y.pw) {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
                             Y.L.pad};
             const int tr = M.dt == lpp::DT_BF16 ? lpp::conv_bf16_tile_rows(g) : lpp::conv_tile_rows(g);

@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liblpp.so")
 _LIB = None
 
-CONV, BN, RELU, ADD, MAXPOOL, GAP, LINEAR = range(7)
+CONV, BN, RELU, ADD, MAXPOOL, GAP, LINEAR, CONCAT = range(8)
 FP32, BF16 = 0, 1
 SEQUENTIAL, ASYNC = 0, 1
 STATUS = {0: "LPP_OK", -1: "LPP_EINVAL", -2: "LPP_ENOMEM", -3: "LPP_EHIP", -4: "LPP_ESTATE", -5: "LPP_EUNSUPPORTED"}

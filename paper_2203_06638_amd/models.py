@@ -12,7 +12,7 @@ every layer.
 """
 from __future__ import annotations
 
-from .lpp import ADD, BN, CONV, GAP, LINEAR, MAXPOOL, RELU
+from .lpp import ADD, BN, CONCAT, CONV, GAP, LINEAR, MAXPOOL, RELU
 
 
 class Model:
@@ -68,6 +68,11 @@ class Model:
 
     def gap(self, x):
         return self._emit((GAP, x, -1, 0, 0, 0, 1, 0, 0, 0), (self._shape(x)[0], 1, 1))
+
+    def concat(self, x, y):
+        (cx, h, w), (cy, hy, wy) = self._shape(x), self._shape(y)
+        assert (h, w) == (hy, wy)
+        return self._emit((CONCAT, x, y, 0, 0, 0, 1, 0, 0, 0), (cx + cy, h, w))
 
     def linear(self, x, cout):
         cin = self._shape(x)[0]
@@ -229,3 +234,43 @@ def resnet50(n_classes=1000, act=True):
     return resnet_bottleneck(n_classes=n_classes, act=act,
                              blocks=[1, 1, 1, 1, 1, 2, 2, 2, 2, 3, 3, 3, 3, 4, 4, 4, 4, 4])
 
+
+# SqueezeNet v1.0's Fire modules: (squeeze, expand 1x1, expand 3x3) channels
+SQUEEZENET_FIRES = ((16, 64, 64), (16, 64, 64), (32, 128, 128), (32, 128, 128),
+                    (48, 192, 192), (48, 192, 192), (64, 256, 256), (64, 256, 256))
+
+
+def fire_unit(m, x, s, e1, e3, act=True):
+    """Fire module: squeeze 1x1 conv + ReLU, expand 1x1 and expand 3x3
+    (padding 1) convs of the squeezed map, each + ReLU, concatenated (1x1
+    channels first); every conv has a bias.  act=False leaves the ReLUs out."""
+    m.new_unit()
+    relu = m.relu if act else (lambda t: t)
+    sq = relu(m.conv(x, s, 1, 1, 0, bias=True))
+    a = relu(m.conv(sq, e1, 1, 1, 0, bias=True))
+    b = relu(m.conv(sq, e3, 3, 1, 1, bias=True))
+    return m.concat(a, b)
+
+
+def squeezenet(n_classes=10, hw=32, stem=96, fires=SQUEEZENET_FIRES, pools_after=(2, 6), blocks=None, act=True):
+    """SqueezeNet v1.0 on hw x hw inputs: 3x3 stem conv + ReLU, 3x3/2 max
+    pool, the Fire modules (a 3x3/2 max pool after those listed in
+    pools_after: fire4 and fire8), a 1x1 conv classifier + ReLU and a global
+    average pool whose output are the logits."""
+    m = Model("squeezenet", (3, hw, hw), n_classes)
+    relu = m.relu if act else (lambda t: t)
+    x = m.maxpool(relu(m.conv(-1, stem, 3, 1, 1, bias=True)), 3, 2, 1)
+    for i, (s, e1, e3) in enumerate(fires):
+        x = fire_unit(m, x, s, e1, e3, act)
+        if i in pools_after:
+            x = m.maxpool(x, 3, 2, 1)
+    m.new_unit()
+    m.gap(relu(m.conv(x, n_classes, 1, 1, 0, bias=True)))
+    return m.assign_blocks(blocks or [1] * m.n_units)
+
+
+def squeezenet_p4(n_classes=10, act=True):
+    """SqueezeNet, P = 4 blocks of units cut nearest to the quartiles of the
+    forward work: {stem, fire2, fire3} {fire4, fire5} {fire6, fire7}
+    {fire8, fire9, classifier}."""
+    return squeezenet(n_classes, act=act, blocks=[1, 1, 1, 2, 2, 3, 3, 4, 4, 4])

@@ -207,3 +207,18 @@ def twin_bn_net(cin, c, hw, n_classes=5):
     p.linear(p.gap(x), n_classes)
     p.assign_blocks([1, 2])
     return o, p
+
+
+def routing_lo(o):
+    """First parameter index above every max pool: gradients of the
+    parameters below a max pool pass through its argmax decisions, which a
+    lower-precision forward may take differently (near-ties) from the fp64
+    oracle."""
+    pools = [i for i, r in enumerate(o.layers) if r["op"] == OM.MAXPOOL]
+    if not pools:
+        return 0
+    lo = 0
+    for name, off, n in o.tensors:
+        if int(name[1:name.index(".")]) < max(pools):
+            lo = max(lo, off + n)
+    return lo

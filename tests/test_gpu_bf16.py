@@ -139,20 +139,6 @@ def _bottleneck_mini(relu):
 MINIS = {"wrn10_2": (_wrn_mini, 4), "resnet_imagenet_mini": (_rn_mini, 2), "resnet_bottleneck_mini": (_bottleneck_mini, 8)}
 
 
-def _routing_lo(o):
-    """First parameter index above every max pool: gradients of the
-    parameters below a max pool pass through its argmax decisions, which
-    bf16 rounding may take differently (near-ties) from the fp64 oracle."""
-    pools = [i for i, r in enumerate(o.layers) if r["op"] == OM.MAXPOOL]
-    if not pools:
-        return 0
-    lo = 0
-    for name, off, n in o.tensors:
-        if int(name[1:name.index(".")]) < max(pools):
-            lo = max(lo, off + n)
-    return lo
-
-
 def _bf16_partition_step(o, p, x, m0, img, lab, partition, lr=0.1, mu=0.9):
     xr = x.astype(np.float64)
     mr = m0.astype(np.float64)
@@ -168,7 +154,7 @@ def _bf16_partition_step(o, p, x, m0, img, lab, partition, lr=0.1, mu=0.9):
         say("  logits error %.3e" % el)
         assert el < T.TOL_BF16
         lo, hi = o.block_range(partition)
-        clo = max(lo, _routing_lo(o))
+        clo = max(lo, T.routing_lo(o))
         check(o, ctx.get_grad(w), g, clo, hi, "grad", sc)
         check(o, ctx.get_momentum(w), mr, clo, hi, "momentum", sc)
         # the block's update x_new - x against the oracle's

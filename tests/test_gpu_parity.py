@@ -418,7 +418,37 @@ MINIS = {
     "resnet_bottleneck_mini_relu_free": (
         lambda: OM.resnet_bottleneck((1, 2, 1, 1), (8, 16, 16, 32), 10, 64, relu=False).set_blocks([1, 1, 2, 2, 3, 4, 4]),
         lambda: PM.resnet_bottleneck((1, 2, 1, 1), (8, 16, 16, 32), 10, 64, blocks=[1, 1, 2, 2, 3, 4, 4], act=False), 2),
+    # Fire modules (channel concatenation), max pools, and a 1x1 conv
+    # classifier with 7 outputs (the per-pixel linear path) pooled into the
+    # logits
+    "squeezenet_mini_relu_free": (lambda: _sq_mini_o(False), lambda: _sq_mini_p(False), 4),
 }
+
+
+def _sq_mini_o(relu=True):
+    return OM.squeezenet(7, 16, 8, ((4, 4, 8), (4, 8, 4), (8, 8, 8)), (1,), relu=relu).set_blocks([1, 1, 2, 3, 4])
+
+
+def _sq_mini_p(act=True):
+    return PM.squeezenet(7, 16, 8, ((4, 4, 8), (4, 8, 4), (8, 8, 8)), (1,), blocks=[1, 1, 2, 3, 4], act=act)
+
+
+def test_squeezenet_mini_forward_with_relu():
+    """SqueezeNet mini with its ReLUs: logits and every layer's output (the
+    context keeps every layer) against the oracle at batch 4."""
+    o, p = _sq_mini_o(), _sq_mini_p()
+    shapes = R.shapes(o)
+    x = T.init_x(o.specs, 2201)
+    img, lab = T.inputs(2202, 4, o.in_shape, 7)
+    _, logits, _ = R.forward_backward(o, x, img, lab, grad=False)
+    with lpp.Context(p, K=1, batch=4, unfused=True) as ctx:
+        ctx.set_params(x)
+        ctx.step(0, *dev(img, lab), 0, 0.0)
+        assert T.relerr(ctx.get_logits(0), logits, T.TAU_LOGITS) < T.TOL_LOGITS
+        for layer in range(len(o.layers)):
+            ref = R.activation(o, x, img, layer)
+            got = ctx.get_activation(0, layer, shapes[layer])
+            assert T.relerr(got, ref, T.TAU_LOGITS) < 1e-3, layer
 
 
 def test_resnet_imagenet_mini_forward_with_relu():
@@ -470,6 +500,97 @@ def test_wide_head_all_partitions(n_classes, n):
     for part in range(0, 5):
         say("wide head", n_classes, n, "partition", part)
         _partition_step(o, p, x, m0, img, lab, part)
+
+
+def _teacher_forced_convs_f32(o, ctx, x, img, rng, samples=64):
+    """Every conv of the last step of worker 0: sampled output entries
+    recomputed in fp64 from the GPU's stored input and the fp32 weights, and
+    sampled weight- and bias-gradient entries from the GPU's stored input and
+    output gradient.  Bound: fp32 accumulation, a few units of 2^-24 of the
+    terms' magnitude sum (1e-5 of it, with 1e-6 of the value).  Returns the
+    worst normalised errors (forward, parameter gradient)."""
+    shapes = R.shapes(o)
+    n = img.shape[0]
+    xw = x.astype(np.float64)
+    gvec = ctx.get_grad(0).astype(np.float64)
+    worst_f = worst_w = 0.0
+    for li, rec in enumerate(o.layers):
+        if rec["op"] != OM.CONV:
+            continue
+        src = img.astype(np.float64) if rec["in0"] < 0 else \
+            ctx.get_activation(0, rec["in0"], shapes[rec["in0"]]).astype(np.float64)
+        out = ctx.get_activation(0, li, shapes[li]).astype(np.float64)
+        dout = ctx.get_activation_grad(0, li, shapes[li]).astype(np.float64)
+        k, s, pd, cin, cout = rec["k"], rec["stride"], rec["pad"], rec["cin"], rec["cout"]
+        nw = cout * cin * k * k
+        W = xw[rec["poff"]:rec["poff"] + nw].reshape(cout, cin, k, k)
+        bias = xw[rec["poff"] + nw:rec["poff"] + nw + cout] if rec["bias"] else np.zeros(cout)
+        xp = np.pad(src, ((0, 0), (0, 0), (pd, pd), (pd, pd)))
+        ho, wo = shapes[li][1], shapes[li][2]
+        for _ in range(samples):
+            b, co, i, j = rng.integers(n), rng.integers(cout), rng.integers(ho), rng.integers(wo)
+            terms = xp[b, :, i * s:i * s + k, j * s:j * s + k] * W[co]
+            ref = float(terms.sum()) + bias[co]
+            scale = float(np.abs(terms).sum()) + abs(bias[co]) + 1e-30
+            worst_f = max(worst_f, abs(out[b, co, i, j] - ref) / (1e-6 * abs(ref) + 1e-5 * scale))
+        gW = gvec[rec["poff"]:rec["poff"] + nw].reshape(cout, cin, k, k)
+        for _ in range(samples // 4):
+            co, ci, r, q = rng.integers(cout), rng.integers(cin), rng.integers(k), rng.integers(k)
+            prod = dout[:, co] * xp[:, ci, r:r + (ho - 1) * s + 1:s, q:q + (wo - 1) * s + 1:s]
+            ref, scale = float(prod.sum()), float(np.abs(prod).sum()) + 1e-30
+            worst_w = max(worst_w, abs(gW[co, ci, r, q] - ref) / (1e-6 * abs(ref) + 1e-5 * scale))
+        if rec["bias"]:
+            gb = gvec[rec["poff"] + nw:rec["poff"] + nw + cout]
+            ref = dout.sum(axis=(0, 2, 3))
+            scale = np.abs(dout).sum(axis=(0, 2, 3)) + 1e-30
+            worst_w = max(worst_w, float(np.max(np.abs(gb - ref) / (1e-6 * np.abs(ref) + 1e-5 * scale))))
+    return worst_f, worst_w
+
+
+@pytest.mark.parametrize("n_classes", [10, 100])
+def test_full_size_squeezenet(n_classes):
+    """SqueezeNet at the CIFAR workload's size (batch 128).  With its ReLUs:
+    the logits; every convolution teacher-forced on sampled outputs and
+    sampled weight / bias gradients (the 96-channel stem on the padded image,
+    the Fire convs, the 1x1 classifier with 10 outputs run per pixel or 100
+    on the conv kernels); partial gradients equal the full one restricted,
+    bit for bit.  ReLU-free twin: the last block's update against the oracle
+    on the parameters above the last max pool (below it, gradients pass
+    through argmax decisions that fp32 and fp64 may take differently at
+    near-ties, which at this size always occur)."""
+    o, p = OM.squeezenet_p4(n_classes), PM.squeezenet_p4(n_classes)
+    x = T.init_x(o.specs, 91)
+    img, lab = T.inputs(92, 128, o.in_shape, n_classes)
+    _, logits, _ = R.forward_backward(o, x, img, lab, grad=False)
+    with lpp.Context(p, K=1, batch=128) as ctx:
+        ctx.set_params(x)
+        ti, tl = dev(img, lab)
+        ctx.step(0, ti, tl, 0, 0.0)
+        assert T.relerr(ctx.get_logits(0), logits, T.TAU_LOGITS) < T.TOL_LOGITS
+        wf, ww = _teacher_forced_convs_f32(o, ctx, x, img, np.random.default_rng(9))
+        say("squeezenet", n_classes, "teacher-forced: forward %.3f, gradient %.3f (bar 1)" % (wf, ww))
+        assert wf < 1.0 and ww < 1.0
+        g = ctx.get_grad(0)
+        for part in range(1, 5):
+            ctx.step(part - 1, ti, tl, part, 0.0)
+            lo, hi = o.block_range(part)
+            assert np.array_equal(ctx.get_grad(part - 1)[lo:hi], g[lo:hi]), part
+    o, p = OM.squeezenet_p4(n_classes, relu=False), PM.squeezenet_p4(n_classes, act=False)
+    xr = x.astype(np.float64)
+    _, sc = R.grad_scale(o, xr, img, lab)
+    gr, _, _ = R.step(o, xr, np.zeros(o.d), img, lab, 4, 0.1, 0.0)
+    lo, hi = o.block_range(4)
+    clo = T.routing_lo(o)
+    assert lo < clo < hi
+    with lpp.Context(p, K=1, batch=128, momentum=0.0) as ctx:
+        ctx.set_params(x)
+        ctx.step(3, ti, tl, 4, 0.1)
+        ctx.sync()
+        check_grads(o, ctx.get_grad(3), gr, clo, hi, scale=sc)
+        got = ctx.get_params(0)
+        errs = T.tensor_errors(o, got, xr, clo, hi)
+        assert max(errs.values()) < T.TOL_PARAM, T.worst(errs)
+        assert np.array_equal(got[:lo], x[:lo]) and np.array_equal(got[hi:], x[hi:])
 
 
 # ---------------------------------------------------------------------------

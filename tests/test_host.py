@@ -28,6 +28,11 @@ PAIRS = [
     ("resnet_imagenet_mini", lambda: PM.resnet_imagenet((1, 1, 1, 1), (16, 32, 64, 128), 10, 64,
                                                         blocks=[1, 1, 2, 3, 4, 4]),
      lambda: OM.resnet_imagenet((1, 1, 1, 1), (16, 32, 64, 128), 10, 64).set_blocks([1, 1, 2, 3, 4, 4])),
+    ("squeezenet", PM.squeezenet_p4, OM.squeezenet_p4),
+    ("squeezenet100", lambda: PM.squeezenet_p4(100), lambda: OM.squeezenet_p4(100)),
+    ("squeezenet_mini", lambda: PM.squeezenet(7, 16, 8, ((4, 4, 8), (4, 8, 4), (8, 8, 8)), (1,),
+                                              blocks=[1, 1, 2, 3, 4]),
+     lambda: OM.squeezenet(7, 16, 8, ((4, 4, 8), (4, 8, 4), (8, 8, 8)), (1,)).set_blocks([1, 1, 2, 3, 4])),
 ]
 
 
@@ -53,7 +58,7 @@ def test_layout_matches_oracle_models(name, prod, ref):
     assert len(p.layers) == len(o.layers)
     for a, b in zip(p.layers, o.layers):
         assert tuple(a[:9]) == (b["op"], b["in0"], b["in1"], b["cin"], b["cout"], b["k"], b["stride"], b["pad"],
-                                b["bias"]) or (a[0] in (lpp.RELU, lpp.ADD, lpp.GAP, lpp.MAXPOOL) and
+                                b["bias"]) or (a[0] in (lpp.RELU, lpp.ADD, lpp.GAP, lpp.MAXPOOL, lpp.CONCAT) and
                                                a[0] == b["op"] and a[1] == b["in0"] and a[2] == b["in1"])
 
 
@@ -105,6 +110,36 @@ def test_describe_rejects_bad_models():
     assert _desc_err(m) == -1
     m = PM.tiny_cnn()
     assert _desc_err(m, dtype=7) == -1
+
+
+def test_describe_channel_rules():
+    """Channel counts that are not a multiple of 4 are accepted only on the
+    output of a 1x1 stride-1 unpadded fp32 conv, read by ReLU / pooling /
+    linear layers; concatenation adds channels and needs matching H, W."""
+    assert lpp.describe(PM.squeezenet_p4(10), 4).d == 729_034
+    m = PM.squeezenet_p4(10)
+    assert _desc_err(m, dtype=lpp.BF16) == -5          # bf16 convs need multiples of 8
+    m = PM.squeezenet_p4(10)
+    m.layers[-3][5], m.layers[-3][7] = 3, 1             # classifier as a 3x3 conv with 10 outputs
+    m.layers[-3][3] = m.layers[-3][3]                   # (same cin)
+    assert _desc_err(m) == -5
+    # a BN reading a 10-channel tensor
+    b = PM.Model("bn10", (3, 8, 8), 10)
+    x = b.conv(-1, 8, 3, bias=True)
+    y = b.bn(b.conv(x, 10, 1, 1, 0, bias=True))
+    b.gap(y)
+    b.assign_blocks([1])
+    assert _desc_err(b, P=1) == -5
+    # concat of tensors of different spatial size
+    c = PM.Model("cat", (3, 8, 8), 8)
+    x = c.conv(-1, 4, 3, bias=True)
+    y = c.conv(-1, 4, 3, 2, 1, bias=True)
+    c.layers.append([lpp.CONCAT, x, y, 0, 0, 0, 1, 0, 0, 0])
+    c.unit_of.append(0)
+    c.shapes.append((8, 8, 8))
+    c.gap(len(c.layers) - 1)
+    c.assign_blocks([1])
+    assert _desc_err(c, P=1) == -1
 
 
 def test_describe_accepts_ragged_shapes():
