@@ -61,25 +61,38 @@ __device__ void softmax_ce_row(const float* z_s, int O, int y, int Nb, float* re
 // ---- fused form --------------------------------------------------------
 
 // One workgroup per sample: pooled features f (also written out for the
-// weight gradient), logits W f + b, softmax cross-entropy.
+// weight gradient), logits W f + b, softmax cross-entropy.  Pooling: thread
+// (q, l) sums channel quad q over pixels l, l + rl, ...; the rl partial sums
+// of a quad are added in LDS in a fixed order.  C % 4 == 0.
 template <class T>
 __global__ __launch_bounds__(256) void head_fwd_k(const T* __restrict__ x, int Nb, int HW, int C,
                                                   const float* __restrict__ W, const float* __restrict__ b, int O,
                                                   const StepArgs* __restrict__ args, float* __restrict__ feat,
                                                   float* __restrict__ logits, float* __restrict__ dz,
                                                   float* __restrict__ loss_per) {
-    __shared__ float f_s[kHeadMaxC];
+    __shared__ __attribute__((aligned(16))) float f_s[kHeadMaxC];
     __shared__ float z_s[kHeadMaxO];
     __shared__ float red[256];
+    __shared__ f4 part[256];
     const int n = blockIdx.x, t = threadIdx.x;
-    for (int c = t; c < C; c += 256) {
-        float s = 0.f;
-        for (int e = 0; e < HW; ++e) s += ld1(x, ((long)n * HW + e) * C + c);
-        const float f = s / (float)HW;
-        f_s[c] = f;
-        feat[(long)n * C + c] = f;
+    const int C4 = C >> 2;
+    for (int q0 = 0; q0 < C4; q0 += 256) {
+        const int nq = min(256, C4 - q0), rl = 256 / nq;
+        const int q = q0 + t % nq, l = t / nq;
+        f4 s = f4{0.f, 0.f, 0.f, 0.f};
+        if (l < rl)
+            for (int e = l; e < HW; e += rl) s += ld4(x, ((long)n * HW + e) * C4 + q);
+        part[t] = s;
+        __syncthreads();
+        if (t < nq) {
+            f4 tot = part[t];
+            for (int k = 1; k < rl; ++k) tot += part[k * nq + t];
+            const f4 f = tot / (float)HW;
+            *(f4*)(f_s + 4 * (q0 + t)) = f;
+            *(f4*)(feat + (long)n * C + 4 * (q0 + t)) = f;
+        }
+        __syncthreads();
     }
-    __syncthreads();
     for (int o = t; o < O; o += 256) {
         float z = b ? b[o] : 0.f;
         const float* w = W + (long)o * C;
@@ -113,6 +126,56 @@ __global__ __launch_bounds__(256) void head_bwd_x_k(const float* __restrict__ dz
 }
 
 // ---- weight gradient (both forms) ----------------------------------------
+
+// Narrow heads: one workgroup per class o.  dW[o][:] = sum_n dz[n][o] f[n][:]
+// with thread (q, l) summing channel quad q over samples l, l + rl, ... and the
+// partial sums added in LDS in a fixed order; db[o] likewise.  Workgroup 0
+// also forms the batch-mean loss.  C % 4 == 0.
+__global__ __launch_bounds__(256) void head_bwd_w_rows_k(const float* __restrict__ dz, const float* __restrict__ feat,
+                                                         int Nb, int C, int O, float* __restrict__ gW,
+                                                         float* __restrict__ gb, const float* __restrict__ loss_per,
+                                                         float* __restrict__ loss) {
+    __shared__ f4 part[256];
+    __shared__ float pb[256];
+    const int o = blockIdx.x, t = threadIdx.x;
+    if (o == 0 && t == 0) {
+        float s = 0.f;
+        for (int n = 0; n < Nb; ++n) s += loss_per[n];
+        loss[0] = s / (float)Nb;
+    }
+    if (!gW) return;
+    const int C4 = C >> 2;
+    for (int q0 = 0; q0 < C4; q0 += 256) {
+        const int nq = min(256, C4 - q0), rl = 256 / nq;
+        const int q = q0 + t % nq, l = t / nq;
+        f4 s = f4{0.f, 0.f, 0.f, 0.f};
+        if (l < rl)
+            for (int n = l; n < Nb; n += rl) s += dz[(long)n * O + o] * ld4(feat, (long)n * C4 + q);
+        part[t] = s;
+        __syncthreads();
+        if (t < nq) {
+            f4 tot = part[t];
+            for (int k = 1; k < rl; ++k) tot += part[k * nq + t];
+            float* g = gW + (long)o * C + 4 * (q0 + t);   // any alignment: scalar stores
+            g[0] = tot[0];
+            g[1] = tot[1];
+            g[2] = tot[2];
+            g[3] = tot[3];
+        }
+        __syncthreads();
+    }
+    if (gb) {
+        float s = 0.f;
+        for (int n = t; n < Nb; n += 256) s += dz[(long)n * O + o];
+        pb[t] = s;
+        __syncthreads();
+        for (int w = 128; w > 0; w >>= 1) {
+            if (t < w) pb[t] += pb[t + w];
+            __syncthreads();
+        }
+        if (t == 0) gb[o] = pb[0];
+    }
+}
 
 // dW[o][c] = sum_n dz[n][o] f[n][c], db[o] = sum_n dz[n][o], samples in
 // order; thread 0 of block 0 also forms the batch-mean loss.  Q channels per
@@ -293,7 +356,9 @@ hipError_t launch_head_fwd(int dt, const void* x, int Nb, int HW, int C, const f
 
 hipError_t launch_head_bwd_w(const float* dz, const float* feat, int Nb, int C, int O, float* gW, float* gb,
                              const float* loss_per, float* loss, hipStream_t st) {
-    if (gW && C % 4 == 0) {
+    if (gW && C % 4 == 0 && !head_wide(C, O)) {
+        launch(head_bwd_w_rows_k, dim3(O), dim3(256), 0, st, dz, feat, Nb, C, O, gW, gb, loss_per, loss);
+    } else if (gW && C % 4 == 0) {
         const long n = (long)O * (C / 4) + O;
         launch(head_bwd_w_k<4>, dim3(nblk(n, 256)), dim3(256), 0, st, dz, feat, Nb, C, O, gW, gb, loss_per, loss);
     } else {
