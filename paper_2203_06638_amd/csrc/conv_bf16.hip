@@ -19,12 +19,14 @@
 //
 // Lane layout of v_mfma_f32_16x16x32_bf16 (64 lanes): lane l supplies
 // A[row l%16][k = 8*(l/16) .. +8] and B[col l%16][same k] and receives
-// D[rows 4*(l/16) .. +4][col l%16].  A K-step is 32 values of k: four 8-channel
-// chunks, each from one tap (a tap holds Cs/8 chunks; for Cs < 32 a K-step
-// spans several taps).  Operand tiles go through LDS with a row pitch of 40
-// bf16 (80 bytes), which keeps the 16-byte fragment reads of 16 lanes on
-// distinct banks; tiles are double-buffered, the next K-step's global loads
-// are in flight during the current step's MFMAs, one barrier per step.
+// D[rows 4*(l/16) .. +4][col l%16].  A load step is 32 values of k: four
+// 8-channel chunks, each from one tap (a tap holds Cs/8 chunks; for Cs < 32 a
+// step spans several taps).  Operand tiles go through LDS in rows of 32 bf16
+// (64 bytes) whose four 16-byte chunks are XOR-swizzled by (row / 4) % 4, so
+// both the row-wise stores and the 16-row fragment reads of 16 lanes hit
+// distinct banks.  Tiles are double-buffered and the next step's global loads
+// are in flight during the current step's MFMAs; for Cs >= 128 two load steps
+// share one buffer and one barrier (a 64-wide K-step).
 //
 // Weight gradient: dW[cout][(tap, c)] = sum over output pixels p of
 // dY[p][cout] * X[src(p, tap)][c]: a GEMM whose reduction runs over pixels.
@@ -45,7 +47,11 @@ namespace lpp {
 
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
-constexpr int kBfPitch = 40;
+constexpr int kBfPitch = 32;   // forward / data-gradient operand rows (swizzled)
+constexpr int kWgPitch = 40;   // weight-gradient operand rows (80 bytes, padded)
+
+// LDS position of 16-byte chunk c (0..3) of operand row `row`
+__device__ __forceinline__ int bf_swz(int c, int row) { return c ^ ((row >> 2) & 3); }
 
 __device__ __forceinline__ f4 mfma_bf16(bf8 a, bf8 b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -62,21 +68,23 @@ struct BfPass {
 };
 
 // Output channels in the epilogue: BM x BN tile, bf16, pitch BN + 8.
-// FASTK (Cs % 32 == 0): a K-step is 32 channels of one tap, and the tap and
+// FASTK (Cs % 32 == 0): a load step is 32 channels of one tap, and the tap and
 // channel counters advance incrementally (no divisions in the loop);
-// otherwise a K-step's four 8-channel chunks are decoded one by one (Cs = 8
-// or 16 spans several taps per K-step).
-template <int BM, int BN, bool STATS, bool FASTK>
+// otherwise a step's four 8-channel chunks are decoded one by one (Cs = 8 or
+// 16 spans several taps per step).  KH load steps (1 or 2) form one K-step:
+// one LDS buffer, one barrier.
+template <int BM, int BN, bool STATS, bool FASTK, int KH>
 __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src, const bf16* __restrict__ B,
                                                    const float* __restrict__ bias, bf16* __restrict__ Y, ConvGeom g,
                                                    BfPass ps, int accumulate, BnSums sums) {
     constexpr int TM = BM / 32, TN = BN / 32;     // 16x16 blocks per wave; waves 2 x 2
     constexpr int AL = BM / 64, BL = BN / 64;     // 16-byte operand loads per thread per K-step
     constexpr int P = kBfPitch;
-    constexpr int STAGE = (BM + BN) * P;
+    constexpr int HALF = (BM + BN) * P;           // one load step's A and B tiles
+    constexpr int STAGE = KH * HALF;
     constexpr int OP = BN + 8;
-    static_assert(BM * OP <= 2 * STAGE, "the epilogue tile reuses the operand buffers");
-    __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
+    constexpr int LDSN = BM * OP > 2 * STAGE ? BM * OP : 2 * STAGE;   // the epilogue tile reuses the space
+    __shared__ __attribute__((aligned(16))) bf16 lds[LDSN];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave & 1, wn = wave >> 1;
     const long Mv = (long)g.Nb * ps.Hv * ps.Wv;
@@ -111,10 +119,10 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
     const int ntap = ps.nr * ps.ns;
     const int nks = (ntap * cpt + 3) >> 2;
 
-    uint4 ra[AL], rb[BL];
-    // FASTK iteration state: tap (tx, ty) and the K-step's first channel c0
+    uint4 ra[KH][AL], rb[KH][BL];
+    // FASTK iteration state: tap (tx, ty) and the load step's first channel c0
     int tx = 0, ty = 0, c0 = 0;
-    auto load_tap = [&](int r, int s, int ch, bool tok) {
+    auto load_tap = [&](uint4 (&xa)[AL], uint4 (&xb)[BL], int r, int s, int ch, bool tok) {
         const int dh = (ps.offh + ps.sgn * r) >> ps.shift, dw = (ps.offw + ps.sgn * s) >> ps.shift;
         const int aoff = (dh * g.Ws + dw) * g.Cs + ch;
         const int woff = (r * g.S + s) * g.Cs + ch;
@@ -122,15 +130,16 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
         for (int u = 0; u < AL; ++u) {
             const int h = a_h[u] + dh, w = a_w[u] + dw;
             const bool ok = tok && (unsigned)h < (unsigned)g.Hs && (unsigned)w < (unsigned)g.Ws;
-            ra[u] = ok ? *(const uint4*)(src + a_off[u] + aoff) : uint4{0, 0, 0, 0};
+            xa[u] = ok ? *(const uint4*)(src + a_off[u] + aoff) : uint4{0, 0, 0, 0};
         }
 #pragma unroll
         for (int u = 0; u < BL; ++u)
-            rb[u] = (tok && b_row[u]) ? *(const uint4*)(b_row[u] + woff) : uint4{0, 0, 0, 0};
+            xb[u] = (tok && b_row[u]) ? *(const uint4*)(b_row[u] + woff) : uint4{0, 0, 0, 0};
     };
-    auto load = [&](int ks) {
+    // load step ks (no memory access past the last step)
+    auto load = [&](uint4 (&xa)[AL], uint4 (&xb)[BL], int ks) {
         if (FASTK) {
-            load_tap(ps.r0 + ps.step * tx, ps.s0 + ps.step * ty, c0 + 8 * j, true);
+            load_tap(xa, xb, ps.r0 + ps.step * tx, ps.s0 + ps.step * ty, c0 + 8 * j, ks < nks);
             c0 += 32;
             if (c0 == g.Cs) {
                 c0 = 0;
@@ -144,16 +153,23 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
             const int tap = kc / cpt;
             const int ch = (kc - tap * cpt) * 8;
             const int x = tap / ps.ns, y = tap - (tap / ps.ns) * ps.ns;
-            load_tap(ps.r0 + ps.step * x, ps.s0 + ps.step * y, ch, tap < ntap);
+            load_tap(xa, xb, ps.r0 + ps.step * x, ps.s0 + ps.step * y, ch, tap < ntap);
         }
     };
     auto store = [&](int buf) {
-        bf16* As = lds + buf * STAGE;
-        bf16* Bs = As + BM * P;
 #pragma unroll
-        for (int u = 0; u < AL; ++u) *(uint4*)(As + (rr + 64 * u) * P + j * 8) = ra[u];
+        for (int h = 0; h < KH; ++h) {
+            bf16* As = lds + buf * STAGE + h * HALF;
+            bf16* Bs = As + BM * P;
 #pragma unroll
-        for (int u = 0; u < BL; ++u) *(uint4*)(Bs + (rr + 64 * u) * P + j * 8) = rb[u];
+            for (int u = 0; u < AL; ++u) *(uint4*)(As + (rr + 64 * u) * P + bf_swz(j, rr) * 8) = ra[h][u];
+#pragma unroll
+            for (int u = 0; u < BL; ++u) *(uint4*)(Bs + (rr + 64 * u) * P + bf_swz(j, rr) * 8) = rb[h][u];
+        }
+    };
+    auto load_k = [&](int kk) {
+#pragma unroll
+        for (int h = 0; h < KH; ++h) load(ra[h], rb[h], kk * KH + h);
     };
 
     f4 acc[TM][TN];
@@ -162,27 +178,31 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
 #pragma unroll
         for (int y = 0; y < TN; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
 
-    if (nks > 0) {
-        load(0);
+    const int nk = (nks + KH - 1) / KH;           // K-steps
+    if (nk > 0) {
+        load_k(0);
         store(0);
     }
     __syncthreads();
-    const int a_rd = ((wm * TM) * 16 + (lane & 15)) * P + (lane >> 4) * 8;
-    const int b_rd = BM * P + ((wn * TN) * 16 + (lane & 15)) * P + (lane >> 4) * 8;
-    for (int ks = 0; ks < nks; ++ks) {
-        const int cur = ks & 1;
-        if (ks + 1 < nks) load(ks + 1);
-        const bf16* base = lds + cur * STAGE;
-        bf8 a[TM], b[TN];
+    const int a_rd = ((wm * TM) * 16 + (lane & 15)) * P + bf_swz(lane >> 4, lane & 15) * 8;
+    const int b_rd = BM * P + ((wn * TN) * 16 + (lane & 15)) * P + bf_swz(lane >> 4, lane & 15) * 8;
+    for (int kk = 0; kk < nk; ++kk) {
+        const int cur = kk & 1;
+        if (kk + 1 < nk) load_k(kk + 1);
 #pragma unroll
-        for (int x = 0; x < TM; ++x) a[x] = *(const bf8*)(base + a_rd + x * 16 * P);
+        for (int h = 0; h < KH; ++h) {
+            const bf16* base = lds + cur * STAGE + h * HALF;
+            bf8 a[TM], b[TN];
 #pragma unroll
-        for (int y = 0; y < TN; ++y) b[y] = *(const bf8*)(base + b_rd + y * 16 * P);
+            for (int x = 0; x < TM; ++x) a[x] = *(const bf8*)(base + a_rd + x * 16 * P);
 #pragma unroll
-        for (int x = 0; x < TM; ++x)
+            for (int y = 0; y < TN; ++y) b[y] = *(const bf8*)(base + b_rd + y * 16 * P);
 #pragma unroll
-            for (int y = 0; y < TN; ++y) acc[x][y] = mfma_bf16(a[x], b[y], acc[x][y]);
-        if (ks + 1 < nks) store(cur ^ 1);
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int y = 0; y < TN; ++y) acc[x][y] = mfma_bf16(a[x], b[y], acc[x][y]);
+        }
+        if (kk + 1 < nk) store(cur ^ 1);
         __syncthreads();
     }
 
@@ -308,12 +328,16 @@ static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* 
     if (Mv == 0) return hipSuccess;
     dim3 grid((unsigned)((Mv + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
     const BnSums sm = stats ? *stats : BnSums{};
-    if (g.Cs % 32 == 0) {
-        if (stats) launch((conv_bf16_k<BM, BN, true, true>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, true>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+    // two load steps per K-step (one barrier per 64 channels) for wide sources
+    if (g.Cs >= 128 && g.Cs % 32 == 0) {
+        if (stats) launch((conv_bf16_k<BM, BN, true, true, 2>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, true, 2>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+    } else if (g.Cs % 32 == 0) {
+        if (stats) launch((conv_bf16_k<BM, BN, true, true, 1>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, true, 1>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
     } else {
-        if (stats) launch((conv_bf16_k<BM, BN, true, false>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, false>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+        if (stats) launch((conv_bf16_k<BM, BN, true, false, 1>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, false, 1>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
     }
     return hipGetLastError();
 }
@@ -398,7 +422,7 @@ template <int BM, int BN>
 __global__ __launch_bounds__(256) void wgrad_bf16_k(const bf16* __restrict__ dY, const bf16* __restrict__ X,
                                                     float* __restrict__ part, WgB g) {
     constexpr int TM = BM / 32, TN = BN / 32;
-    constexpr int P = kBfPitch;
+    constexpr int P = kWgPitch;
     constexpr int STAGE = (BM + BN) * P;
     constexpr int AE = (BM * 2 + 255) / 256, BE = (BN * 2 + 255) / 256;
     __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
