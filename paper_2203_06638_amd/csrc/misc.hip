@@ -1145,33 +1145,48 @@ hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long h
 }
 
 // v_k = x_k[e]; vbar = (sum_k v_k) / n; x_k[e] = x_k[e] (re-read) + (vbar - v_k).
-// One quad per thread per pass, 512-thread workgroups and up to 8M threads in
-// flight.  The re-read of x_k is a volatile load, so it is a fresh read that
-// the compiler cannot merge with the snapshot load: block updates that land
-// between the two survive the write (Alg. 1's averager).
+// U quads per thread per pass (1 in use), 512-thread workgroups.  The re-read of x_k sits behind a compiler memory fence, so it is a
+// fresh (cached) load that the compiler cannot merge with the snapshot load:
+// block updates that land between the two survive the write (Alg. 1's
+// averager).  The result is stored nontemporally (x_k is streamed once).
 constexpr int kAvgThreads = 512;
+// one quad per thread over the whole array up to 32M quads (measured: 5.86
+// TB/s against 5.63 with a grid-stride loop over 16384 workgroups)
+constexpr long kAvgMaxBlocks = 65536;
 
-template <int NR>
+template <int NR, int U>
 __global__ __launch_bounds__(kAvgThreads) void average_k(RepPtrs reps, int n_rep, long n) {
     const long nq = n / 4;
     const float inv_div = (float)n_rep;
-    for (long q = (long)blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += (long)gridDim.x * blockDim.x) {
-        f4 v[NR];
-        f4 s = f4{0.f, 0.f, 0.f, 0.f};
+    const long stride = (long)gridDim.x * blockDim.x;
+    for (long q0 = (long)blockIdx.x * blockDim.x + threadIdx.x; q0 < nq; q0 += stride * U) {
+        f4 v[U][NR];
+        f4 vbar[U];
 #pragma unroll
-        for (int k = 0; k < NR; ++k) {
-            if (k < n_rep) {
-                v[k] = *(const f4*)(reps.p[k] + 4 * q);
-                s += v[k];
-            }
+        for (int u = 0; u < U; ++u) {
+            const long q = q0 + u * stride;
+#pragma unroll
+            for (int k = 0; k < NR; ++k)
+                if (k < n_rep && q < nq) v[u][k] = *(const f4*)(reps.p[k] + 4 * q);
         }
-        const f4 vbar = s / inv_div;
 #pragma unroll
-        for (int k = 0; k < NR; ++k) {
-            if (k < n_rep) {
-                f4* p = (f4*)(reps.p[k] + 4 * q);
-                *p = *(volatile f4*)p + (vbar - v[k]);
-            }
+        for (int u = 0; u < U; ++u) {
+            f4 s = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < NR; ++k)
+                if (k < n_rep) s += v[u][k];
+            vbar[u] = s / inv_div;
+        }
+        __asm__ volatile("" ::: "memory");   // the loads below are fresh reads of x_k
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const long q = q0 + u * stride;
+#pragma unroll
+            for (int k = 0; k < NR; ++k)
+                if (k < n_rep && q < nq) {
+                    f4* p = (f4*)(reps.p[k] + 4 * q);
+                    __builtin_nontemporal_store(*(const f4*)p + (vbar[u] - v[u][k]), p);   // streamed out
+                }
         }
     }
     // scalar tail
@@ -1184,21 +1199,27 @@ __global__ __launch_bounds__(kAvgThreads) void average_k(RepPtrs reps, int n_rep
         for (int k = 0; k < NR; ++k)
             if (k < n_rep) { vv[k] = reps.p[k][e]; s += vv[k]; }
         const float vbar = s / inv_div;
+        __asm__ volatile("" ::: "memory");
 #pragma unroll
         for (int k = 0; k < NR; ++k)
-            if (k < n_rep) reps.p[k][e] = *(volatile float*)&reps.p[k][e] + (vbar - vv[k]);
+            if (k < n_rep) reps.p[k][e] = reps.p[k][e] + (vbar - vv[k]);
     }
 }
 
-hipError_t launch_average(const RepPtrs& reps, int n_rep, long n, hipStream_t st) {
-    long b = (n / 4 + kAvgThreads - 1) / kAvgThreads;
+template <int U>
+static void launch_average_u(const RepPtrs& reps, int n_rep, long n, hipStream_t st) {
+    long b = (n / 4 + (long)kAvgThreads * U - 1) / ((long)kAvgThreads * U);
     if (b < 1) b = 1;
-    if (b > 16384) b = 16384;
+    if (b > kAvgMaxBlocks) b = kAvgMaxBlocks;
     const dim3 grid((unsigned)b), block(kAvgThreads);
-    if (n_rep <= 2) launch(average_k<2>, grid, block, 0, st, reps, n_rep, n);
-    else if (n_rep <= 4) launch(average_k<4>, grid, block, 0, st, reps, n_rep, n);
-    else if (n_rep <= 8) launch(average_k<8>, grid, block, 0, st, reps, n_rep, n);
-    else launch(average_k<16>, grid, block, 0, st, reps, n_rep, n);
+    if (n_rep <= 2) launch(average_k<2, U>, grid, block, 0, st, reps, n_rep, n);
+    else if (n_rep <= 4) launch(average_k<4, U>, grid, block, 0, st, reps, n_rep, n);
+    else if (n_rep <= 8) launch(average_k<8, U>, grid, block, 0, st, reps, n_rep, n);
+    else launch(average_k<16, U>, grid, block, 0, st, reps, n_rep, n);
+}
+
+hipError_t launch_average(const RepPtrs& reps, int n_rep, long n, hipStream_t st) {
+    launch_average_u<1>(reps, n_rep, n, st);
     return hipGetLastError();
 }
 
