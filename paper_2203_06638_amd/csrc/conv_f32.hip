@@ -476,10 +476,15 @@ static hipError_t launch_lds(const float* src, const float* B, const float* bias
 // counts of an LDS tile (pix * IW < 2^32).
 struct TileGeom { int OH, IH, IW, pad_eff, tiles_per_img; unsigned IW_inv; };
 
-template <int MODE, int KS, int WM, int TM, int TN, bool STATS>
+// INBN (forward passes): the source is the input of a training-mode batch
+// norm followed by a ReLU; each staged source value becomes
+// relu(fma(x, scale[c], shift[c])) (padding stays zero), with the per-channel
+// coefficients derived in the prologue from the batch sums (or read from aux;
+// bnacc.h).  The normalised tensor is never stored.
+template <int MODE, int KS, int WM, int TM, int TN, bool STATS, bool INBN>
 __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                      const float* __restrict__ bias, float* __restrict__ Y,
-                                                     ConvGeom g, TileGeom t, int accumulate, BnSums sums) {
+                                                     ConvGeom g, TileGeom t, int accumulate, BnSums sums, BnFwd inbn) {
     constexpr int WN = 4 / WM;
     constexpr int TP = WM * TM * 16, BN = WN * TN * 16;
     constexpr int LDW = 20;
@@ -497,6 +502,20 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
     const int st = g.stride;
     const int h_org = oh0 * st - t.pad_eff, w_org = -t.pad_eff;
     const int npix = t.OH * g.Wo;
+
+    __shared__ float in_co[INBN ? 2 * kFoldMaxC : 1];   // scale | shift of the source channels
+    if (INBN) {
+        bn_fwd_coeffs(inbn, g.Cs, in_co, in_co + kFoldMaxC);
+        __syncthreads();
+    }
+    // relu(fma(v, scale, shift)) of source quad c..c+3 (INBN)
+    auto fold = [&](f4 v, int c) {
+        if (INBN) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = fmaxf(__builtin_fmaf(v[k], in_co[c + k], in_co[kFoldMaxC + c + k]), 0.f);
+        }
+        return v;
+    };
 
     // LDS offset of the input pixel each of this lane's output rows reads at tap (0,0)
     int abase[TM];
@@ -571,7 +590,8 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
         for (int cgp = 0; cgp < ngroups; ++cgp) {
 #pragma unroll
             for (int u = 0; u < NU; ++u)
-                if (d[u] >= 0) *(f4*)(lds + d[u]) = v[u];
+                if (d[u] >= 0)
+                    *(f4*)(lds + d[u]) = (INBN && sp[u] && tid + u * 256 < nx) ? fold(v[u], cgp * 16 + q * 4) : v[u];
             __syncthreads();
             if (cgp + 1 < ngroups) {
                 const int c1 = (cgp + 1) * 16;
@@ -592,6 +612,7 @@ __global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ s
                     const float* sp;
                     decode(base + u * 256, sp, d[u]);
                     v[u] = sp ? *(const f4*)(sp + c0) : f4{0.f, 0.f, 0.f, 0.f};
+                    if (INBN && sp && base + u * 256 < nx) v[u] = fold(v[u], c0 + q * 4);
                 }
 #pragma unroll
                 for (int u = 0; u < NU; ++u)
@@ -746,25 +767,36 @@ static bool pick_tile(int mode, const ConvGeom& g, TileCfg& out) {
 
 template <int MODE, int KS, int WM, int TM, int TN>
 static hipError_t launch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              const TileCfg& c, bool acc, const BnSums* stats, hipStream_t st) {
+                              const TileCfg& c, bool acc, const BnSums* stats, const BnFwd* inbn, hipStream_t st) {
     constexpr int BN = (4 / WM) * TN * 16;
     dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
-    if (stats)
-        launch((conv_tile_f32<MODE, KS, WM, TM, TN, true>), grid, dim3(256), c.lds, st, src, B, bias, Y,
-                           g, c.t, (int)acc, stats ? *stats : BnSums{});
-    else
-        launch((conv_tile_f32<MODE, KS, WM, TM, TN, false>), grid, dim3(256), c.lds, st, src, B, bias, Y,
-                           g, c.t, (int)acc, stats ? *stats : BnSums{});
+    const BnSums sm = stats ? *stats : BnSums{};
+    const BnFwd ib = inbn ? *inbn : BnFwd{};
+    if (inbn) {
+        if (MODE != CONV_FWD || g.Cs > kFoldMaxC) return hipErrorInvalidValue;
+        if (stats)
+            launch((conv_tile_f32<MODE, KS, WM, TM, TN, true, true>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
+                   c.t, (int)acc, sm, ib);
+        else
+            launch((conv_tile_f32<MODE, KS, WM, TM, TN, false, true>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
+                   c.t, (int)acc, sm, ib);
+    } else if (stats) {
+        launch((conv_tile_f32<MODE, KS, WM, TM, TN, true, false>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
+               c.t, (int)acc, sm, ib);
+    } else {
+        launch((conv_tile_f32<MODE, KS, WM, TM, TN, false, false>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
+               c.t, (int)acc, sm, ib);
+    }
     return hipGetLastError();
 }
 
 template <int MODE>
 static hipError_t dispatch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                                const TileCfg& c, bool acc, const BnSums* stats, hipStream_t st) {
+                                const TileCfg& c, bool acc, const BnSums* stats, const BnFwd* inbn, hipStream_t st) {
 #define TILE(WM_, TM_, TN_)                                                                                  \
     if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) {                                                         \
-        if (g.R == 3) return launch_tile<MODE, 3, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, st);     \
-        return launch_tile<MODE, 1, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, st);                   \
+        if (g.R == 3) return launch_tile<MODE, 3, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, inbn, st); \
+        return launch_tile<MODE, 1, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, inbn, st);               \
     }
     TILE(4, 4, 1) TILE(4, 2, 1) TILE(2, 4, 1) TILE(2, 2, 1) TILE(1, 4, 1) TILE(2, 2, 2) TILE(1, 4, 2)
     TILE(4, 1, 1) TILE(2, 1, 1) TILE(1, 2, 1) TILE(1, 1, 1)
@@ -1049,9 +1081,10 @@ static ConvCfg pick_cfg(const ConvGeom& g) {
 
 template <int MODE>
 static hipError_t launch_mode(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              bool acc, const BnSums* stats, hipStream_t st) {
+                              bool acc, const BnSums* stats, const BnFwd* inbn, hipStream_t st) {
     TileCfg tc;
-    if (pick_tile(MODE, g, tc)) return dispatch_tile<MODE>(src, B, bias, Y, g, tc, acc, stats, st);
+    if (pick_tile(MODE, g, tc)) return dispatch_tile<MODE>(src, B, bias, Y, g, tc, acc, stats, inbn, st);
+    if (inbn) return hipErrorInvalidValue;   // folding needs the spatial kernel
     if (MODE == CONV_DGRAD) {
         S2Cfg sc;
         if (pick_s2(g, sc)) return dispatch_s2(src, B, Y, g, sc, acc, st);
@@ -1086,9 +1119,16 @@ int conv_tile_rows(const ConvGeom& g) {
 }
 
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st) {
-    if (mode == CONV_FWD) return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, stats, st);
-    return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, nullptr, st);
+                             const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st,
+                             const BnFwd* inbn) {
+    if (mode == CONV_FWD) return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, stats, inbn, st);
+    if (inbn) return hipErrorInvalidValue;
+    return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, nullptr, nullptr, st);
+}
+
+bool conv_fold_ok(const ConvGeom& g, const WgradPlan& p) {
+    TileCfg tc;
+    return g.Cs <= kFoldMaxC && p.tile && pick_tile(CONV_FWD, g, tc);
 }
 
 // ------------------------------------------------------------------------
@@ -1237,7 +1277,8 @@ struct WgTileGeom { int OH, IMGS, IH, IW, tiles_per_img, TP; unsigned IW_inv, IH
 
 template <int RS, int NG, int ST, bool K1>
 __global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restrict__ dY, const float* __restrict__ X,
-                                                           float* __restrict__ part, WgArgs a, WgTileGeom t) {
+                                                           float* __restrict__ part, WgArgs a, WgTileGeom t,
+                                                           const float* __restrict__ in_ss) {
     constexpr int LDW = 20;
     constexpr int JST = (K1 ? 1 : ST) * LDW;   // LDS distance between a lane's four pixels
     constexpr int TP = NG * 64;
@@ -1285,6 +1326,13 @@ __global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restri
                     d[u] = (npix + p) * LDW + q * 4;
                 }
                 v[u] = sp ? *(const f4*)sp : f4{0.f, 0.f, 0.f, 0.f};
+                // X read through a folded BN + ReLU (padding stays zero)
+                if (in_ss && sp && e < nx) {
+                    const int c = c0 + q * 4;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        v[u][k] = fmaxf(__builtin_fmaf(v[u][k], in_ss[c + k], in_ss[a.Cin_p + c + k]), 0.f);
+                }
             }
 #pragma unroll
             for (int u = 0; u < NU; ++u)
@@ -1427,38 +1475,39 @@ static hipError_t launch_wg(const float* dY, const float* X, float* part, const 
 
 template <int RS, int NG, int ST, bool K1>
 static hipError_t launch_wg_tile(const float* dY, const float* X, float* part, const WgArgs& a, const WgTileGeom& t,
-                                 hipStream_t st) {
+                                 const float* in_ss, hipStream_t st) {
     const long M = (long)a.Nb * a.Ho * a.Wo;
     dim3 grid((unsigned)(M / t.TP), (unsigned)(a.Cout / 16), (unsigned)(a.Cin_p / 16));
     const size_t lds = sizeof(float) * std::max<size_t>(((size_t)t.IMGS * t.IH * t.IW + t.TP) * 20, (size_t)4 * RS * 256);
-    launch((conv_wgrad_tile_f32<RS, NG, ST, K1>), grid, dim3(256), lds, st, dY, X, part, a, t);
+    launch((conv_wgrad_tile_f32<RS, NG, ST, K1>), grid, dim3(256), lds, st, dY, X, part, a, t, in_ss);
     return hipGetLastError();
 }
 
 template <int RS, int ST, bool K1>
 static hipError_t launch_wg_tile_ng(const float* dY, const float* X, float* part, const WgArgs& a,
-                                    const WgTileGeom& t, hipStream_t st) {
+                                    const WgTileGeom& t, const float* in_ss, hipStream_t st) {
     const int ng = t.TP / 64;
-    if (ng == 4) return launch_wg_tile<RS, 4, ST, K1>(dY, X, part, a, t, st);
-    if (ng == 2) return launch_wg_tile<RS, 2, ST, K1>(dY, X, part, a, t, st);
-    return launch_wg_tile<RS, 1, ST, K1>(dY, X, part, a, t, st);
+    if (ng == 4) return launch_wg_tile<RS, 4, ST, K1>(dY, X, part, a, t, in_ss, st);
+    if (ng == 2) return launch_wg_tile<RS, 2, ST, K1>(dY, X, part, a, t, in_ss, st);
+    return launch_wg_tile<RS, 1, ST, K1>(dY, X, part, a, t, in_ss, st);
 }
 
 hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int Nb, int Hi, int Wi, int Cin_p,
                              int Ho, int Wo, int Cout, int R, int S, int stride, int pad, const WgradPlan& p,
-                             hipStream_t st) {
+                             hipStream_t st, const float* in_ss) {
     WgArgs a{Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, R, S, stride, pad, p.pix_per_split};
+    if (in_ss && !p.tile) return hipErrorInvalidValue;   // folding needs the spatial kernel
     if (p.tile) {
         WgTileGeom t;
         if (!pick_wgrad_tile(Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, R, S, stride, pad, t) || t.OH != p.oh ||
             t.IMGS != p.imgs)
             return hipErrorInvalidValue;
         if (R == 1) {
-            if (stride == 1) return launch_wg_tile_ng<1, 1, true>(dY, X, part, a, t, st);
-            return launch_wg_tile_ng<1, 2, true>(dY, X, part, a, t, st);
+            if (stride == 1) return launch_wg_tile_ng<1, 1, true>(dY, X, part, a, t, in_ss, st);
+            return launch_wg_tile_ng<1, 2, true>(dY, X, part, a, t, in_ss, st);
         }
-        if (stride == 1) return launch_wg_tile_ng<9, 1, false>(dY, X, part, a, t, st);
-        return launch_wg_tile_ng<9, 2, false>(dY, X, part, a, t, st);
+        if (stride == 1) return launch_wg_tile_ng<9, 1, false>(dY, X, part, a, t, in_ss, st);
+        return launch_wg_tile_ng<9, 2, false>(dY, X, part, a, t, in_ss, st);
     }
     if (p.tm == 1) return launch_wg<1, 4>(dY, X, part, a, p, st);
     if (p.tm == 2) return launch_wg<2, 4>(dY, X, part, a, p, st);

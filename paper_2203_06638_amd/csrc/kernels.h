@@ -55,13 +55,32 @@ struct BnSums {
     float* p2;
 };
 
+// A training-mode batch norm's coefficients: from the batch sums acc
+// [2][kAccSlots][C] (sum y, sum y^2 over M rows) with gamma, beta, eps, or
+// -- acc null -- read from aux = [mean | rstd | scale | shift].
+struct BnFwd {
+    const double* acc;
+    const float* gamma;
+    const float* beta;
+    float eps;
+    long M;
+    float* aux;
+};
+
+// Largest source channel count of a forward pass that folds a BN + ReLU into
+// its operand staging.
+constexpr int kFoldMaxC = 512;
+
 // Y[m][n] (+)= sum_k A[m][k] B[n][k] (+ bias[n]); see ConvGeom.  Forward
 // passes with stats non-null also produce the batch-norm sums of Y: into
 // acc, q = 0: sum y and q = 1: sum y^2 (each row tile's share formed from its
 // mean and sum of squared deviations); as partials, the tile mean (p0) and
 // sum of squared deviations (p1), T = ceil(M / conv_tile_rows(g)) tiles.
+// inbn (forward only; see conv_fold_ok): src is the input of a BN + ReLU
+// and the pass reads relu(bn(src)) without storing it.
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st);
+                             const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st,
+                             const BnFwd* inbn = nullptr);
 int conv_tile_rows(const ConvGeom& g);
 
 // Weight gradient: part[split][Cout][Ktot] = partial sums over pixel ranges
@@ -70,9 +89,15 @@ int conv_tile_rows(const ConvGeom& g);
 // `imgs` whole images) or GEMM tiles over ranges of pix_per_split pixels.
 struct WgradPlan { int tm, tn, splits, pix_per_split; long part_floats; int tile, oh, imgs; };
 WgradPlan wgrad_plan(int Nb, int Hi, int Wi, int Cin_p, int Ho, int Wo, int Cout, int R, int S, int stride, int pad);
+// in_ss (spatial-tile plans only): X is the input of a BN + ReLU whose
+// scale and shift are in_ss[c] and in_ss[Cin_p + c]; the pass reads
+// relu(fma(x, scale, shift)).
 hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int Nb, int Hi, int Wi, int Cin_p,
                              int Ho, int Wo, int Cout, int R, int S, int stride, int pad, const WgradPlan& p,
-                             hipStream_t st);
+                             hipStream_t st, const float* in_ss = nullptr);
+// A forward pass with this geometry and weight-gradient plan can fold a
+// preceding BN + ReLU (spatial kernels, at most kFoldMaxC source channels).
+bool conv_fold_ok(const ConvGeom& g, const WgradPlan& p);
 // Sums the split partials in a fixed order and writes the canonical gradient
 // g[((cout*Cin + c)*R + r)*S + s] for c < Cin.
 hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
@@ -117,14 +142,6 @@ hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C
 // scale = gamma*rstd, shift = beta - mean*scale) and the kernel's first
 // workgroup stores [mean | rstd | scale | shift] into aux; with acc null they
 // are read from aux + 2C and aux + 3C.
-struct BnFwd {
-    const double* acc;
-    const float* gamma;
-    const float* beta;
-    float eps;
-    long M;
-    float* aux;
-};
 // y = relu?(bn1(x1) [+ r | + bn2(x2)])  (r: residual tensor; x2: a second
 // normalised input, used when both branches of a residual add end in BN)
 hipError_t launch_bn_act(int dt, const void* x1, const BnFwd& b1, const void* r, const void* x2, const BnFwd* b2,
@@ -146,6 +163,7 @@ struct BnBwdArgs {
     const void* x2; const float* mean2; const float* rstd2;    // second BN of a dual group, or null
     long M;
     int C;
+    const float* mask_ss = nullptr;   // mask null: ReLU decision fma(x1, scale, shift) > 0, scale | shift here
 };
 // per row tile (stats_rows), the tile's sum g, sum g*xhat1 and sum g*xhat2
 // added into acc [3][kAccSlots][C], or written to p0..p2 [T][C]

@@ -215,7 +215,9 @@ __global__ __launch_bounds__(256) void bn_act_k(const T* __restrict__ x1, BnFwd 
         const long i = i0 + u * 256;
         if (i >= n4) continue;
         const int c = (int)(i % C4) * 4;
-        f4 o = xa[u] * *(const f4*)(co + c) + *(const f4*)(co + C + c);
+        f4 o;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = __builtin_fmaf(xa[u][j], co[c + j], co[C + c + j]);
         if (RES == 1) o += xb[u];
         if (RES == 2) o += xb[u] * *(const f4*)(co + 2 * C + c) + *(const f4*)(co + 3 * C + c);
         if (RELU) {
@@ -302,7 +304,10 @@ hipError_t launch_bn_act(int dt, const void* x1, const BnFwd& b1, const void* r,
 // each thread's rows are loaded four at a time before use, the row lanes
 // meet in a fixed-shape LDS tree, and lane 0 of each quad adds the tile's
 // sums to the accumulators.
-template <class T, bool MASK, bool DUAL>
+// MK: 0 no ReLU; 1 ReLU mask from the stored group output (a.mask); 2 ReLU
+// decision recomputed from the BN input, relu(fma(x1, scale, shift)) > 0 with
+// scale | shift at a.mask_ss (the folded forward's own expression).
+template <class T, int MK, bool DUAL>
 __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, int R, BnSums out) {
     const T* __restrict__ dy = (const T*)a.dy;
     const T* __restrict__ mask = (const T*)a.mask;
@@ -320,6 +325,11 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, int R, BnSum
         f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0, s2 = s0;
         if (lr < rl) {
             const f4 m1 = *(const f4*)(a.mean1 + q * 4), r1v = *(const f4*)(a.rstd1 + q * 4);
+            f4 msc = s0, msh = s0;
+            if (MK == 2) {
+                msc = *(const f4*)(a.mask_ss + q * 4);
+                msh = *(const f4*)(a.mask_ss + C + q * 4);
+            }
             f4 m2 = s0, r2v = s0;
             if (DUAL) {
                 m2 = *(const f4*)(a.mean2 + q * 4);
@@ -332,7 +342,7 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, int R, BnSum
                     const long r = rb + (long)k * rl;
                     const long o = (r < r1 ? r : r0) * C4 + q;
                     gv[k] = ld4(dy, o);
-                    if (MASK) yv[k] = ld4(mask, o);
+                    if (MK == 1) yv[k] = ld4(mask, o);
                     xv[k] = ld4(x1, o);
                     if (DUAL) x2v[k] = ld4(x2, o);
                 }
@@ -340,9 +350,13 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, int R, BnSum
                 for (int k = 0; k < 4; ++k) {
                     if (rb + (long)k * rl >= r1) continue;
                     f4 g = gv[k];
-                    if (MASK) {
+                    if (MK == 1) {
 #pragma unroll
                         for (int j = 0; j < 4; ++j) g[j] = yv[k][j] > 0.f ? g[j] : 0.f;
+                    }
+                    if (MK == 2) {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) g[j] = __builtin_fmaf(xv[k][j], msc[j], msh[j]) > 0.f ? g[j] : 0.f;
                     }
                     s0 += g;
                     s1 += g * ((xv[k] - m1) * r1v);
@@ -391,7 +405,7 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, int R, BnSum
 // derives per channel a = gamma*rstd, mean g, mean g*xhat (and the second
 // set) from the accumulated sums, plus mean and rstd, into LDS; the first
 // workgroup stores dgamma and dbeta.
-template <class T, bool MASK, int E>
+template <class T, int MK, int E>
 __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, T* __restrict__ dx1, int acc1,
                                                       T* __restrict__ dx2, int acc2, T* __restrict__ dres,
                                                       int accres) {
@@ -406,8 +420,8 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, 
         const long i = i0 + u * 256;
         if (i < n4) {
             gv[u] = ld4((const T*)a.dy, i);
-            if (MASK) yv[u] = ld4((const T*)a.mask, i);
-            if (dx1) x1v[u] = ld4((const T*)a.x1, i);
+            if (MK == 1) yv[u] = ld4((const T*)a.mask, i);
+            if (dx1 || MK == 2) x1v[u] = ld4((const T*)a.x1, i);
             if (dx2) x2v[u] = ld4((const T*)a.x2, i);
         }
     }
@@ -458,9 +472,14 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, 
         if (i >= n4) continue;
         const int c = (int)(i % C4) * 4;
         f4 g = gv[u];
-        if (MASK) {
+        if (MK == 1) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) g[j] = yv[u][j] > 0.f ? g[j] : 0.f;
+        }
+        if (MK == 2) {
+            const f4 msc = *(const f4*)(a.mask_ss + c), msh = *(const f4*)(a.mask_ss + C + c);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) g[j] = __builtin_fmaf(x1v[u][j], msc[j], msh[j]) > 0.f ? g[j] : 0.f;
         }
         if (dx1) {
             const f4 xh = (x1v[u] - *(const f4*)(cf + 3 * C + c)) * *(const f4*)(cf + 4 * C + c);
@@ -483,11 +502,14 @@ static void bn_bwd_reduce_t(const BnBwdArgs& a, const BnSums& out, hipStream_t s
     const dim3 grid(stats_tiles(a.M, a.C), ((a.C >> 2) + 255) / 256);
     const int R = stats_rows(a.M, a.C);
     if (a.mask) {
-        if (a.x2) launch((bn_bwd_reduce_k<T, true, true>), grid, dim3(256), 0, st, a, R, out);
-        else launch((bn_bwd_reduce_k<T, true, false>), grid, dim3(256), 0, st, a, R, out);
+        if (a.x2) launch((bn_bwd_reduce_k<T, 1, true>), grid, dim3(256), 0, st, a, R, out);
+        else launch((bn_bwd_reduce_k<T, 1, false>), grid, dim3(256), 0, st, a, R, out);
+    } else if (a.mask_ss) {
+        if (a.x2) launch((bn_bwd_reduce_k<T, 2, true>), grid, dim3(256), 0, st, a, R, out);
+        else launch((bn_bwd_reduce_k<T, 2, false>), grid, dim3(256), 0, st, a, R, out);
     } else {
-        if (a.x2) launch((bn_bwd_reduce_k<T, false, true>), grid, dim3(256), 0, st, a, R, out);
-        else launch((bn_bwd_reduce_k<T, false, false>), grid, dim3(256), 0, st, a, R, out);
+        if (a.x2) launch((bn_bwd_reduce_k<T, 0, true>), grid, dim3(256), 0, st, a, R, out);
+        else launch((bn_bwd_reduce_k<T, 0, false>), grid, dim3(256), 0, st, a, R, out);
     }
 }
 
@@ -584,8 +606,9 @@ static hipError_t bn_bwd_apply_t(const BnBwdArgs& a, const BnBwdCoef& k, T* dx1,
                        (int)acc2, dres, (int)accres)
 #define BNBA_E(MK) \
     do { if (E == 4) BNBA(MK, 4); else if (E == 2) BNBA(MK, 2); else BNBA(MK, 1); } while (0)
-    if (a.mask) BNBA_E(true);
-    else BNBA_E(false);
+    if (a.mask) BNBA_E(1);
+    else if (a.mask_ss) BNBA_E(2);
+    else BNBA_E(0);
 #undef BNBA_E
 #undef BNBA
     return hipGetLastError();

@@ -58,6 +58,7 @@ struct Layer {
     int cin_p = 0;                // conv: stored channels of the input
     bool pw = false;              // conv: 1x1, stride 1, no padding, output channels not a multiple of 4 --
                                   //   run as a linear layer applied to every pixel (fp32)
+    int in_bn = -1;               // conv: reads relu(bn(x)) of this BN layer's input x, folded into its loads
     long wf_off = -1, wd_off = -1;// conv: W_f / W_d in the worker's weight buffer (elements)
     double macs = 0;              // forward multiply-adds (conv, linear)
     lpp::WgradPlan wg{};
@@ -92,6 +93,7 @@ struct Group {
     int res = -1;       // G_BNACT: the residual tensor added unnormalised, if any
     int relu = -1;      // G_BNACT: the closing ReLU, if any
     int lin = -1;       // G_HEAD: the linear layer
+    bool fold = false;  // G_BNACT: BN + ReLU folded into the consuming conv (nothing launched forward)
 };
 
 struct Model {
@@ -406,6 +408,25 @@ void build_groups(Model& M, bool fused) {
     }
 }
 
+// BN + ReLU groups whose only consumer is an fp32 conv that the spatial
+// kernels take (forward and weight gradient): the conv reads the BN's input
+// and applies relu(fma(x, scale, shift)) while staging it, so the group
+// launches nothing in the forward pass and its output is never stored.
+void plan_folds(Model& M, int N) {
+    if (M.dt != lpp::DT_F32) return;
+    for (Group& G : M.groups) {
+        if (G.kind != G_BNACT || G.bn2 >= 0 || G.add >= 0 || G.relu < 0) continue;
+        if (M.consumers[G.out].size() != 1) continue;
+        Layer& Y = M.layers[M.consumers[G.out][0]];
+        if (Y.L.op != LPP_CONV || Y.pw || Y.L.in0 != G.out || Y.cin_p != Y.L.cin) continue;
+        const lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
+                              Y.L.pad};
+        if (!lpp::conv_fold_ok(g, Y.wg)) continue;
+        G.fold = true;
+        Y.in_bn = G.a;
+    }
+}
+
 // ------------------------------------------------------------------------
 
 struct Timer {
@@ -627,6 +648,14 @@ int run_forward(lpp_ctx* c, Worker& w) {
         case G_CONV: {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride, Y.L.pad};
             const float* bias = Y.L.bias ? w.v + Y.poff + Y.wcount : nullptr;
+            // a folded BN + ReLU: read the BN's input, normalised while staged
+            lpp::BnFwd ib{};
+            if (Y.in_bn >= 0) {
+                const Layer& Bn = M.layers[Y.in_bn];
+                x0 = c->act(w, Bn.L.in0);
+                ib = lpp::BnFwd{c->fixed_order ? nullptr : c->acc_fwd(w, Y.in_bn), w.v + Bn.poff,
+                                w.v + Bn.poff + Bn.out.c, M.desc.bn_eps, Mrows, c->aux(w, Y.in_bn)};
+            }
             lpp::BnSums sums{};
             if (G.stats_bn >= 0) sums = c->fixed_order ? lpp::BnSums{nullptr, w.ps0, w.ps1, nullptr}
                                                        : lpp::BnSums{c->acc_fwd(w, G.stats_bn), nullptr, nullptr, nullptr};
@@ -642,7 +671,8 @@ int run_forward(lpp_ctx* c, Worker& w) {
             else
                 LAUNCH("conv_fwd", 2.0 * Y.macs, st,
                        lpp::launch_conv_igemm(lpp::CONV_FWD, (const float*)x0, (const float*)c->wf(w, Y), bias,
-                                              (float*)c->act(w, G.a), g, false, sp, st));
+                                              (float*)c->act(w, G.a), g, false, sp, st,
+                                              Y.in_bn >= 0 ? &ib : nullptr));
             if (G.stats_bn >= 0 && c->fixed_order) {
                 const Layer& B = M.layers[G.stats_bn];
                 const long rows = (long)N * Y.out.h * Y.out.w;
@@ -660,6 +690,7 @@ int run_forward(lpp_ctx* c, Worker& w) {
                 int rc = bn_stats_standalone(c, w, G.a);
                 if (rc) return rc;
             }
+            if (G.fold) break;   // the consuming conv applies it
             if (G.bn2 >= 0 && M.stats_from[G.bn2] < 0) {
                 int rc = bn_stats_standalone(c, w, G.bn2);
                 if (rc) return rc;
@@ -779,6 +810,13 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                            lpp::launch_conv_wgrad_bf16((const uint16_t*)dy, (const uint16_t*)x0, w.wpart, N, Y.in0.h,
                                                        Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k,
                                                        Y.L.stride, Y.L.pad, Y.wg, st));
+                else if (Y.in_bn >= 0)
+                    // X = relu(bn(x)) of the folded BN, rebuilt while staged
+                    LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
+                           lpp::launch_conv_wgrad((const float*)dy, (const float*)c->act(w, M.layers[Y.in_bn].L.in0),
+                                                  w.wpart, N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout,
+                                                  Y.L.k, Y.L.k, Y.L.stride, Y.L.pad, Y.wg, st,
+                                                  c->aux(w, Y.in_bn) + 2 * Y.cin_p));
                 else
                     LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
                            lpp::launch_conv_wgrad((const float*)dy, (const float*)x0, w.wpart, N, Y.in0.h, Y.in0.w,
@@ -826,9 +864,12 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
             float* ax = c->aux(w, G.a);
             float* ax2 = b2 >= 0 ? c->aux(w, b2) : nullptr;
             const Layer* Y2 = b2 >= 0 ? &M.layers[b2] : nullptr;
-            lpp::BnBwdArgs a{dy, G.relu >= 0 ? c->act(w, G.out) : nullptr, x0, ax, ax + C,
+            // plain BN + ReLU (fp32): the ReLU decision is recomputed from the
+            // BN input and its scale and shift instead of read from the output
+            const bool xmask = G.relu >= 0 && G.bn2 < 0 && G.add < 0 && !bf;
+            lpp::BnBwdArgs a{dy, G.relu >= 0 && !xmask ? c->act(w, G.out) : nullptr, x0, ax, ax + C,
                              want2 ? c->act(w, Y2->L.in0) : nullptr, want2 ? ax2 : nullptr,
-                             want2 ? ax2 + C : nullptr, Min, C};
+                             want2 ? ax2 + C : nullptr, Min, C, xmask ? ax + 2 * C : nullptr};
             float* gg1 = pl.wgrad[G.a] ? w.g + Y.poff : nullptr;
             float* gb1 = pl.wgrad[G.a] ? w.g + Y.poff + C : nullptr;
             float* gg2 = want2 && pl.wgrad[b2] ? w.g + Y2->poff : nullptr;
@@ -1033,6 +1074,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
                                      : lpp::wgrad_plan(N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout,
                                                        Y.L.k, Y.L.k, Y.L.stride, Y.L.pad);
     }
+    if (!(opt && opt->unfused)) plan_folds(M, N);
     c->wbuf_floats = wf;
     c->n_snap = (int)snaps.size();
 
@@ -1334,8 +1376,15 @@ static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* 
     Worker& w = c->workers[worker];
     // a fused-away output of a batch-norm group is rebuilt from the group's
     // stored inputs and batch-norm coefficients (the group's own expression
-    // without its ReLU)
+    // without its ReLU; with it for the output of a folded group)
     const Group* G = nullptr;
+    bool relu_out = false;   // rebuild with the group's ReLU (a folded group's output)
+    if (!grad)
+        for (const Group& g : M.groups)
+            if (g.kind == G_BNACT && g.fold && layer == g.out) {
+                G = &g;
+                relu_out = true;
+            }
     if (!M.stored[layer]) {
         for (const Group& g : M.groups)
             if (g.kind == G_BNACT && (layer == g.a || layer == g.add || layer == g.bn2)) G = &g;
@@ -1367,7 +1416,7 @@ static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* 
         }
         lpp::BnFwd b1{};
         b1.aux = (float*)ax;
-        e = lpp::launch_bn_act(Y.dt, x, b1, r, x2, x2 ? &b2 : nullptr, false, tmp + n, rows, C, w.stream);
+        e = lpp::launch_bn_act(Y.dt, x, b1, r, x2, x2 ? &b2 : nullptr, relu_out, tmp + n, rows, C, w.stream);
         src = tmp + n;
     } else if (!grad) {
         src = c->act(w, layer);

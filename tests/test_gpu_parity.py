@@ -593,6 +593,44 @@ def test_full_size_squeezenet(n_classes):
         assert np.array_equal(got[:lo], x[:lo]) and np.array_equal(got[hi:], x[hi:])
 
 
+def test_folded_bn_relu_resnet20_all_partitions():
+    """ResNet-20 with its ReLUs at batch 32, where every BN + ReLU whose output
+    feeds only a conv is folded into that conv's operand staging (forward and
+    weight gradient; the backward recomputes the ReLU decision from the BN
+    input).  The BN shifts are set to 4 so that every ReLU decision keeps a
+    margin above the fp32 / fp64 disagreement of 19 layers (band 1e-5 of a
+    layer's largest input; a few in 1e5 inputs stay below zero); every
+    partition's gradient, momentum and update are compared with the oracle."""
+    o, p = OM.resnet20_p4(), PM.resnet20()
+    n = 32
+
+    def make(seed):
+        x = T.init_x(o.specs, seed)
+        for name, off, cnt in o.tensors:
+            if name.endswith("bn_beta"):
+                x[off:off + cnt] = 4.0
+        return x.astype(np.float64), T.inputs(seed + 7, n, o.in_shape, 10)[0]
+
+    band = 1e-5
+    seed, margin = T.well_posed_seed(o, make, seeds=range(2500, 2540), band=band)
+    say("folded resnet20 seed", seed, "margin %.2e" % margin)
+    x = make(seed)[0].astype(np.float32)
+    img, lab = T.inputs(seed + 7, n, o.in_shape, 10)
+    # the folds are in effect: fewer BN apply launches than BN + ReLU groups
+    with lpp.Context(p, K=1, batch=n) as ctx:
+        ctx.set_params(x)
+        ctx.timer_enable("bn_act")
+        ctx.step(0, *dev(img, lab), 1, 0.0)
+        _, launches, _ = ctx.timer_read()
+        ctx.timer_enable(None)
+    say("bn_act launches per step", launches, "(19 without folding)")
+    assert launches <= 10
+    m0 = (np.random.default_rng(8).standard_normal(o.d) * 1e-2).astype(np.float32)
+    for part in range(0, 5):
+        say("folded resnet20 partition", part)
+        _partition_step(o, p, x, m0, img, lab, part, band=band)
+
+
 # ---------------------------------------------------------------------------
 # the headline workload's full size (batch 128, momentum 0.9)
 # ---------------------------------------------------------------------------
