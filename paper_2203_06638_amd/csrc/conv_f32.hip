@@ -26,6 +26,7 @@
 // reproducible; only the batch-norm sums of the forward epilogue are merged
 // across workgroups by fp64 atomic adds (bnacc.h).
 #include <algorithm>
+#include <cstdint>
 
 #include "bnacc.h"
 #include "kernels.h"
@@ -1514,38 +1515,71 @@ hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int N
     return launch_wg<4, 4>(dY, X, part, a, p, st);
 }
 
-// 64 outputs per workgroup; L lanes per output (L = 4, 8 or 16 by the split
-// count, 64 L threads) each sum a fixed, interleaved subset of the splits,
-// then the L partial sums are added in order.
-__global__ __launch_bounds__(1024) void wgrad_reduce_kernel(const float* __restrict__ part, int splits, int Cout,
-                                                            int Ktot, int Cin, int Cin_p, int R, int S,
-                                                            float* __restrict__ g) {
-    __shared__ float red[16][64];
-    const int L = blockDim.x >> 6;
-    const int j = threadIdx.x & 63, sl = threadIdx.x >> 6;
-    const long idx = (long)blockIdx.x * 64 + j;
-    const long total = (long)Cout * Ktot;
-    float s = 0.f;
-    if (idx < total)
-        for (int k = sl; k < splits; k += L) s += part[(long)k * total + idx];
-    red[sl][j] = s;
+// Workgroup of 1024 threads on one job: L split lanes x Q = 1024 / L output
+// quads.  Thread (l, q) adds the float4 partials of quad q over splits
+// l, l + L, ... (eight loads issued ahead of their adds, which stay in split
+// order); the L lane sums are then halved pairwise in LDS (lane i += lane
+// i + h for h = L/2, L/4, ..., 1).  A wave reads 64 / min(Q, 64) runs of
+// min(Q, 64) consecutive quads of one split.
+__global__ __launch_bounds__(1024) void wgrad_reduce_multi_k(const WgRedTable t) {
+    __shared__ f4 red[1024];
+    int j = 0;
+    while (j + 1 < t.n && (int)blockIdx.x >= t.job[j + 1].wg0) ++j;
+    const WgRedJob& J = t.job[j];
+    const int lg = J.lanes_log2, L = 1 << lg, Q = 1024 >> lg;
+    const int tid = threadIdx.x, sl = tid >> (10 - lg), qi = tid & (Q - 1);
+    const long nq = (long)J.Cout * J.Ktot / 4;
+    const long quad = (long)(blockIdx.x - J.wg0) * Q + qi;
+    f4 s = f4{0.f, 0.f, 0.f, 0.f};
+    if (quad < nq) {
+        const f4* p = (const f4*)J.part + quad;
+        int k = sl;
+        for (; k + 7 * L < J.splits; k += 8 * L) {
+            f4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = p[(long)(k + u * L) * nq];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; k < J.splits; k += L) s += p[(long)k * nq];
+    }
+    red[tid] = s;
     __syncthreads();
-    if (sl != 0 || idx >= total) return;
-    s = red[0][j];
-    for (int l = 1; l < L; ++l) s += red[l][j];
-    const int co = (int)(idx / Ktot), col = (int)(idx - (long)co * Ktot);
-    const int tap = col / Cin_p, c = col - tap * Cin_p;
-    if (c >= Cin) return;
-    const int r = tap / S, q = tap - r * S;
-    g[(((long)co * Cin + c) * R + r) * S + q] = s;
+    for (int h = L >> 1; h > 0; h >>= 1) {
+        if (sl < h) red[tid] = red[tid] + red[tid + h * Q];
+        __syncthreads();
+    }
+    if (sl != 0 || quad >= nq) return;
+    const f4 v = red[qi];
+    const int co = (int)(quad * 4 / J.Ktot);
+    const int col0 = (int)(quad * 4 - (long)co * J.Ktot);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int col = col0 + e, tap = col / J.Cin_p, c = col - tap * J.Cin_p;
+        if (c < J.Cin) J.g[((long)co * J.Cin + c) * J.RS + tap] = v[e];
+    }
 }
 
-hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
-                               float* g, hipStream_t st) {
-    const long n = (long)Cout * Ktot;
-    const int L = splits >= 256 ? 16 : (splits >= 64 ? 8 : 4);
-    launch(wgrad_reduce_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64 * L), 0, st, part, splits,
-                       Cout, Ktot, Cin, Cin_p, R, S, g);
+bool wgred_add(WgRedTable& t, const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
+               float* g) {
+    if (t.n >= kWgRedMaxJobs || Ktot % 4 || Ktot != R * S * Cin_p || splits < 1 ||
+        ((uintptr_t)part & 15))
+        return false;
+    int lg = 0;
+    while (lg < 6 && (8 << lg) < splits) ++lg;   // about eight splits per lane, at most 64 lanes
+    const long nq = (long)Cout * Ktot / 4;
+    const long wgs = (nq + (1024 >> lg) - 1) / (1024 >> lg);
+    if (t.n == 0) t.wgs = 0;
+    if ((long)t.wgs + wgs > 0x7fffffffL) return false;
+    t.job[t.n] = WgRedJob{part, g, splits, Cout, Ktot, Cin, Cin_p, R * S, lg, t.wgs};
+    t.wgs += (int)wgs;
+    ++t.n;
+    return true;
+}
+
+hipError_t launch_wgrad_reduce_multi(const WgRedTable& t, hipStream_t st) {
+    if (t.n == 0) return hipSuccess;
+    launch(wgrad_reduce_multi_k, dim3((unsigned)t.wgs), dim3(1024), 0, st, t);
     return hipGetLastError();
 }
 

@@ -98,10 +98,26 @@ hipError_t launch_conv_wgrad(const float* dY, const float* X, float* part, int N
 // A forward pass with this geometry and weight-gradient plan can fold a
 // preceding BN + ReLU (spatial kernels, at most kFoldMaxC source channels).
 bool conv_fold_ok(const ConvGeom& g, const WgradPlan& p);
-// Sums the split partials in a fixed order and writes the canonical gradient
-// g[((cout*Cin + c)*R + r)*S + s] for c < Cin.
-hipError_t launch_wgrad_reduce(const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
-                               float* g, hipStream_t st);
+// Split sums of several weight gradients in one launch: job j sums its
+// part[split][Cout][Ktot] (16-byte aligned) over the splits and writes the
+// canonical gradient g[((cout*Cin + c)*R + r)*S + s] for c < Cin.  Every
+// output is summed in an order fixed by its job's split count alone: split
+// lane l of L adds splits l, l + L, l + 2L, ... in turn, then the L lane sums
+// are combined by a fixed pairwise tree.
+constexpr int kWgRedMaxJobs = 16;
+struct WgRedJob {
+    const float* part;
+    float* g;
+    int splits, Cout, Ktot, Cin, Cin_p, RS;   // RS = R * S taps
+    int lanes_log2;   // L = 2^lanes_log2 split lanes, 1024 / L output quads per workgroup
+    int wg0;          // the job's first workgroup
+};
+struct WgRedTable { WgRedJob job[kWgRedMaxJobs]; int n, wgs; };
+// appends a job (false when the table is full or the shapes are not
+// reducible in quads)
+bool wgred_add(WgRedTable& t, const float* part, int splits, int Cout, int Ktot, int Cin, int Cin_p, int R, int S,
+               float* g);
+hipError_t launch_wgrad_reduce_multi(const WgRedTable& t, hipStream_t st);
 
 // ---- bf16 convolution passes (conv_bf16.hip): bf16 source, weights and
 // output, float32 accumulation; geometry as for the float32 passes.  The
@@ -113,7 +129,7 @@ hipError_t launch_conv_bf16(int mode, const uint16_t* src, const uint16_t* B, co
 int conv_bf16_tile_rows(const ConvGeom& g);
 bool conv_bf16_supported(int mode, const ConvGeom& g);
 // weight gradient from bf16 dY and X into float32 partials part[split][Cout]
-// [R*S*Cin_p] (summed by launch_wgrad_reduce); plan.tm / plan.tn hold the
+// [R*S*Cin_p] (summed by launch_wgrad_reduce_multi); plan.tm / plan.tn hold the
 // tile's output channels and columns
 WgradPlan wgrad_plan_bf16(int Nb, int Ho, int Wo, int Cin_p, int Cout, int R, int S);
 hipError_t launch_conv_wgrad_bf16(const uint16_t* dY, const uint16_t* X, float* part, int Nb, int Hi, int Wi,

@@ -481,6 +481,7 @@ struct lpp_ctx {
     bool fixed_order = true;
     bool graphs = true;
     long ps_floats = 0;
+    long wpart_floats = 0;                   // weight-gradient partials of one reduce batch
     std::unique_ptr<std::atomic<long>[]> counters;
     Timer timer;
     int device = 0;
@@ -556,6 +557,10 @@ hipError_t timed_launch(lpp_ctx* c, const char* family, double work, hipStream_t
     } while (0)
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+long align64(long x) { return (x + 63) & ~63L; }
+
+// Floats of weight-gradient partials kept for one batched reduce launch.
+constexpr long kWpartBatch = 16L << 20;
 
 // In async mode a batch norm's coefficients come either from the prologue of
 // every apply workgroup (each re-reads C x kAccSlots fp64 sums: cheap for
@@ -781,6 +786,17 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
     const double eb = (double)dt_size(dt);
     hipStream_t st = w.stream;
     bool loss_done = false;
+    // weight-gradient partials accumulate in w.wpart until one launch sums
+    // them all (when the next would not fit, the table is full, and at the end)
+    lpp::WgRedTable red{};
+    long woff = 0;
+    auto flush_reduce = [&]() -> int {
+        if (red.n == 0) return LPP_OK;
+        LAUNCH("wgrad_reduce", 4.0 * woff, st, lpp::launch_wgrad_reduce_multi(red, st));
+        red.n = 0;
+        woff = 0;
+        return LPP_OK;
+    };
     for (int gi = (int)M.groups.size() - 1; gi >= 0; --gi) {
         const Group& G = M.groups[gi];
         if (!pl.run[G.out]) continue;
@@ -805,26 +821,33 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
             }
             if (pl.wgrad[G.a]) {
                 const int Ktot = Y.L.k * Y.L.k * Y.cin_p;
+                const long pf = align64(Y.wg.part_floats);
+                if (red.n == lpp::kWgRedMaxJobs || woff + pf > c->wpart_floats) {
+                    int rc = flush_reduce();
+                    if (rc) return rc;
+                }
+                float* part = w.wpart + woff;
+                if (!lpp::wgred_add(red, part, Y.wg.splits, Y.L.cout, Ktot, Y.L.cin, Y.cin_p, Y.L.k, Y.L.k,
+                                    w.g + Y.poff))
+                    return fail(LPP_EINVAL, "weight-gradient reduce: unsupported shape");
+                woff += pf;
                 if (bf)
                     LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
-                           lpp::launch_conv_wgrad_bf16((const uint16_t*)dy, (const uint16_t*)x0, w.wpart, N, Y.in0.h,
+                           lpp::launch_conv_wgrad_bf16((const uint16_t*)dy, (const uint16_t*)x0, part, N, Y.in0.h,
                                                        Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k,
                                                        Y.L.stride, Y.L.pad, Y.wg, st));
                 else if (Y.in_bn >= 0)
                     // X = relu(bn(x)) of the folded BN, rebuilt while staged
                     LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
                            lpp::launch_conv_wgrad((const float*)dy, (const float*)c->act(w, M.layers[Y.in_bn].L.in0),
-                                                  w.wpart, N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout,
+                                                  part, N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout,
                                                   Y.L.k, Y.L.k, Y.L.stride, Y.L.pad, Y.wg, st,
                                                   c->aux(w, Y.in_bn) + 2 * Y.cin_p));
                 else
                     LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
-                           lpp::launch_conv_wgrad((const float*)dy, (const float*)x0, w.wpart, N, Y.in0.h, Y.in0.w,
+                           lpp::launch_conv_wgrad((const float*)dy, (const float*)x0, part, N, Y.in0.h, Y.in0.w,
                                                   Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
                                                   Y.L.pad, Y.wg, st));
-                LAUNCH("wgrad_reduce", 4.0 * Y.wg.part_floats, st,
-                       lpp::launch_wgrad_reduce(w.wpart, Y.wg.splits, Y.L.cout, Ktot, Y.L.cin, Y.cin_p, Y.L.k,
-                                                Y.L.k, w.g + Y.poff, st));
                 if (Y.L.bias) {
                     // column sums of dY, from per-tile means
                     const long Mo = (long)N * Y.out.h * Y.out.w;
@@ -981,7 +1004,7 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
     if (head && !loss_done)
         LAUNCH("head", 0.0, st,
                lpp::launch_head_bwd_w(nullptr, nullptr, N, 1, 1, nullptr, nullptr, w.loss + 1, w.loss, st));
-    return LPP_OK;
+    return flush_reduce();
 }
 
 // The device work of one updater iteration on the worker's stream: snapshot
@@ -1093,7 +1116,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
     c->off_loss = take(sizeof(float) * (1 + N));
     c->off_args = take(sizeof(lpp::StepArgs));
     c->off_img = take(eb * (size_t)N * M.desc.in_h * M.desc.in_w * M.img_cp);
-    long ps = 1, wpart = 1;
+    long ps = 1, wpart = 1, wsum = 0;
     for (int l = 0; l < (int)M.layers.size(); ++l) {
         Layer& Y = M.layers[l];
         const long rows_out = (long)N * Y.out.h * Y.out.w;
@@ -1113,9 +1136,14 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
             const long tiles = (rows_out + tr - 1) / tr;
             ps = std::max<long>(ps, tiles * Y.L.cout);
             ps = std::max<long>(ps, (long)lpp::stats_tiles(rows_out, Y.L.cout) * Y.L.cout);
-            wpart = std::max<long>(wpart, Y.wg.part_floats);
+            wpart = std::max<long>(wpart, align64(Y.wg.part_floats));
+            wsum += align64(Y.wg.part_floats);
         }
     }
+    // the partials of consecutive weight gradients stay until one reduce
+    // launch sums them (at most kWpartBatch floats, or one gradient's)
+    wpart = std::max<long>(wpart, std::min<long>(wsum, kWpartBatch));
+    c->wpart_floats = wpart;
     c->off_acc = off;
     for (Layer& Y : M.layers)
         if (Y.L.op == LPP_BN) Y.acc = take(sizeof(double) * 5 * lpp::kAccSlots * Y.out.c);
