@@ -482,8 +482,12 @@ struct TileGeom { int OH, IH, IW, pad_eff, tiles_per_img; unsigned IW_inv; };
 // relu(fma(x, scale[c], shift[c])) (padding stays zero), with the per-channel
 // coefficients derived in the prologue from the batch sums (or read from aux;
 // bnacc.h).  The normalised tensor is never stored.
+// Variants with at most two row blocks per wave and no epilogue statistics
+// or folded input fit 128 registers without spilling: they are held to that,
+// for four waves per SIMD instead of three.
 template <int MODE, int KS, int WM, int TM, int TN, bool STATS, bool INBN>
-__global__ __launch_bounds__(256) void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu((TM <= 2 && !INBN && !STATS) ? 4 : 1, 8)))
+void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                      const float* __restrict__ bias, float* __restrict__ Y,
                                                      ConvGeom g, TileGeom t, int accumulate, BnSums sums, BnFwd inbn) {
     constexpr int WN = 4 / WM;
@@ -1276,8 +1280,11 @@ __global__ __launch_bounds__(256) void conv_wgrad_f32(const float* __restrict__ 
 // the reduce kernel.
 struct WgTileGeom { int OH, IMGS, IH, IW, tiles_per_img, TP; unsigned IW_inv, IHW_inv; };
 
+// Held to 128 registers (four waves per SIMD) where that needs no spilling:
+// every variant but the strided 1x1 one.
 template <int RS, int NG, int ST, bool K1>
-__global__ __launch_bounds__(256) void conv_wgrad_tile_f32(const float* __restrict__ dY, const float* __restrict__ X,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu((RS == 9 || ST == 1) ? 4 : 1, 8)))
+void conv_wgrad_tile_f32(const float* __restrict__ dY, const float* __restrict__ X,
                                                            float* __restrict__ part, WgArgs a, WgTileGeom t,
                                                            const float* __restrict__ in_ss) {
     constexpr int LDW = 20;

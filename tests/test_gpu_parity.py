@@ -600,7 +600,9 @@ def test_folded_bn_relu_resnet20_all_partitions():
     input).  The BN shifts are set to 4 so that every ReLU decision keeps a
     margin above the fp32 / fp64 disagreement of 19 layers (band 1e-5 of a
     layer's largest input; a few in 1e5 inputs stay below zero); every
-    partition's gradient, momentum and update are compared with the oracle."""
+    partition's gradient, momentum and update are compared with the oracle
+    in sequential mode, two partitions in async mode, and the gradient at
+    every conv output layer by layer."""
     o, p = OM.resnet20_p4(), PM.resnet20()
     n = 32
 
@@ -629,6 +631,18 @@ def test_folded_bn_relu_resnet20_all_partitions():
     for part in range(0, 5):
         say("folded resnet20 partition", part)
         _partition_step(o, p, x, m0, img, lab, part, band=band)
+    for part in (0, 2):
+        say("folded resnet20 async partition", part)
+        _partition_step(o, p, x, m0, img, lab, part, band=band, mode=lpp.ASYNC)
+    shapes = R.shapes(o)
+    convs = [li for li, r in enumerate(o.layers) if r["op"] == OM.CONV]
+    with lpp.Context(p, K=1, batch=n) as ctx:
+        ctx.set_params(x)
+        ctx.step(0, *dev(img, lab), 0, 0.0)
+        for li in convs:
+            ref = R.activation_grad(o, x, img, lab, li)
+            got = ctx.get_activation_grad(0, li, shapes[li])
+            assert T.relerr(got, ref, T.TAU) < T.TOL_GRAD, (li, T.relerr(got, ref, T.TAU))
 
 
 # ---------------------------------------------------------------------------
