@@ -66,7 +66,7 @@ def parse():
     ap.add_argument("--hw-queues", type=int, default=8, help="GPU_MAX_HW_QUEUES for the headline run (1..32)")
     ap.add_argument("--workload-hw-queues", type=int, default=4, help="GPU_MAX_HW_QUEUES for the other workloads")
     ap.add_argument("--no-hbm", action="store_true")
-    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--cpu-steps", type=int, default=8)
     ap.add_argument("--replicas", type=int, default=1, help="K (the headline workload has K = 1)")
     ap.add_argument("--workers-used", type=int, default=0,
                     help="issue steps to only the first n workers (0 = all); for latency studies")
