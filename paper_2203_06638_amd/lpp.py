@@ -20,6 +20,7 @@ _LIB = None
 CONV, BN, RELU, ADD, MAXPOOL, GAP, LINEAR, CONCAT = range(8)
 FP32, BF16 = 0, 1
 SEQUENTIAL, ASYNC = 0, 1
+OK, EINVAL, ENOMEM, EHIP, ESTATE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 STATUS = {0: "LPP_OK", -1: "LPP_EINVAL", -2: "LPP_ENOMEM", -3: "LPP_EHIP", -4: "LPP_ESTATE", -5: "LPP_EUNSUPPORTED"}
 
 
