@@ -77,6 +77,8 @@ def parse():
                     help="comma-separated subset of the other configurations")
     ap.add_argument("--workload-steps", type=int, default=64)
     ap.add_argument("--only-workload", default=None, help="run just one of the other configurations (for profiling)")
+    ap.add_argument("--extras", action="store_true",
+                    help="only the partial- vs full-backward throughput and the worker-stream sweep (ResNet-20)")
     ap.add_argument("--delays", action="store_true",
                     help="only the delay statistics of traced async runs (ResNet-20, K=2 x P=4) against H")
     # HBM traffic of the roofline kernel (run each under rocprofv3 --pmc):
@@ -311,6 +313,57 @@ def read_traffic():
     return None
 
 
+def mode_and_stream_extras(torch, steps=400, warmup=40, B=128):
+    """Two extras on the headline workload (ResNet-20, batch 128, async,
+    momentum 0.9, one worker per stream): the partial backward's throughput
+    against the full one (every worker on its own block = LPP, every worker on
+    the whole model = LAP, and the policy's steady state of alternating the
+    two), and the throughput against the number of blocks and worker streams
+    P (units split into P runs of consecutive units; P = 4 is the balanced
+    split of the headline)."""
+    import synth
+    from paper_2203_06638_amd import lpp
+    from paper_2203_06638_amd import models as PM
+    pool = []
+    for b in range(8):
+        pool.append((torch.from_numpy(synth.images(300 + b, B, 3, 32, 32)).cuda(),
+                     torch.from_numpy(synth.labels(300 + b, B, 10)).cuda()))
+
+    def rate(model, part_of):
+        P = model.P
+        streams = [torch.cuda.Stream() for _ in range(P)]
+        ctx = lpp.Context(model, K=1, batch=B, mode=lpp.ASYNC, momentum=0.9, streams=streams)
+        ctx.set_params(synth.init_params(model.specs, 1))
+
+        def issue(n, start):
+            for s in range(start, start + n):
+                w = s % P
+                img, lab = pool[(s // P) % len(pool)]
+                ctx.step(w, img, lab, part_of(w, s // P), 0.1)
+
+        issue(warmup + 2 * P, 0)      # every (worker, partition) graph captured
+        ctx.sync()
+        t0 = time.perf_counter()
+        issue(steps, warmup + 2 * P)
+        ctx.sync()
+        dt = time.perf_counter() - t0
+        ctx.close()
+        return round(B * steps / dt, 1)
+
+    m4 = PM.resnet20(10)
+    modes = {"lpp": rate(m4, lambda w, it: w + 1),
+             "lap": rate(m4, lambda w, it: 0),
+             "alternating": rate(m4, lambda w, it: 0 if it % 2 == 0 else w + 1)}
+    modes["lpp_over_lap"] = round(modes["lpp"] / modes["lap"], 3)
+    sweep = {}
+    for P in (1, 2, 4, 6, 8):
+        n_units = 11
+        blocks = [1, 1, 1, 2, 2, 3, 3, 3, 4, 4, 4] if P == 4 else [u * P // n_units + 1 for u in range(n_units)]
+        sweep[str(P)] = rate(PM.resnet_cifar(20, (16, 32, 64), 10, blocks=blocks), lambda w, it: w + 1)
+    return {"workload": "ResNet-20 (10 classes), batch 128, fp32, async, momentum 0.9, one worker per stream",
+            "steps": steps, "modes_samples_per_s": modes, "streams_samples_per_s": sweep}
+
+
 def delay_statistics(torch, Hs=(1, 2, 4, 8, 16), T=256, B=128):
     """Traced async runs of the LPP-SGD policy (ResNet-20, K = 2 replicas x
     P = 4 workers, T updates per replica, T_st = T/10) for several
@@ -395,6 +448,9 @@ def main():
         return
     if a.delays:
         print(json.dumps(delay_statistics(torch)), flush=True)
+        return
+    if a.extras:
+        print(json.dumps(mode_and_stream_extras(torch)), flush=True)
         return
     if a.only_workload:
         from paper_2203_06638_amd import lpp as _lpp
