@@ -93,9 +93,9 @@ def parse():
 
 def hbm_kernels(torch, lpp):
     """Block update (20 B/param with momentum) and 2-replica averaging
-    (16 B/param) on 64M-float (256 MiB) arrays: far beyond the 256 MB
-    last-level cache per pass."""
-    n = 64 << 20
+    (16 B/param) on 256M-float (1 GiB) arrays: each array four times the
+    256 MB last-level cache, so every pass streams from HBM."""
+    n = 256 << 20
     out = {}
     x, m, g = (torch.randn(n, device="cuda") for _ in range(3))
     for _ in range(3):

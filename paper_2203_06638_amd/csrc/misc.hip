@@ -1162,7 +1162,7 @@ hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long h
     if (hi <= lo) return hipSuccess;
     const long nq = (hi - (lo & ~3L) + 3) / 4;
     long b = (nq + 256L * kUpdQuads - 1) / (256L * kUpdQuads);
-    if (b > 16384) b = 16384;
+    if (b > (1L << 20)) b = 1L << 20;   // one pass up to 4G parameters (5.84 against 5.73 TB/s on 1 GiB arrays)
     launch(sgd_update_k, dim3((unsigned)b), dim3(256), 0, st, x, m, g, lo, hi, args, lr, mu, wd);
     return hipGetLastError();
 }
@@ -1173,9 +1173,10 @@ hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long h
 // block updates that land between the two survive the write (Alg. 1's
 // averager).  The result is stored nontemporally (x_k is streamed once).
 constexpr int kAvgThreads = 512;
-// one quad per thread over the whole array up to 32M quads (measured: 5.86
-// TB/s against 5.63 with a grid-stride loop over 16384 workgroups)
-constexpr long kAvgMaxBlocks = 65536;
+// one quad per thread over the whole array up to 512M quads (measured on
+// 1 GiB replicas: 5.71 TB/s against 5.53 with a two-pass grid-stride loop
+// over 65536 workgroups)
+constexpr long kAvgMaxBlocks = 1L << 20;
 
 template <int NR, int U>
 __global__ __launch_bounds__(kAvgThreads) void average_k(RepPtrs reps, int n_rep, long n) {
