@@ -88,6 +88,10 @@ def parse():
                     help="only a plain device copy of 256 MiB, ten times (counter calibration)")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
                     help="turn the four counter runs into the traffic summary under profiles/")
+    ap.add_argument("--traffic-family", default="conv_fwd", choices=("conv_fwd", "sgd_update", "average"),
+                    help="kernel family --summarize-traffic reads")
+    ap.add_argument("--hbm-only", action="store_true",
+                    help="only the update and averaging kernels on 1 GiB arrays (for their counters)")
     return ap.parse_args()
 
 
@@ -252,7 +256,9 @@ TRAFFIC_SOURCES = ["paper_2203_06638_amd/csrc/conv_f32.hip", "paper_2203_06638_a
 COPY_BYTES = 256 << 20
 # kernel-name prefixes of each timed family (the library's launchers)
 FAMILY_KERNELS = {"conv_fwd": ("void lpp::conv_tile_f32<0,", "void lpp::conv_igemm_f32<0,", "void lpp::conv_lds_f32<0,",
-                               "void lpp::conv_bf16_k<")}
+                               "void lpp::conv_bf16_k<"),
+                  "sgd_update": ("lpp::sgd_update_k(",),
+                  "average": ("void lpp::average_k<",)}
 
 
 def _sources_hash():
@@ -418,7 +424,7 @@ def cpu_baseline(steps, batch):
 def main():
     a = parse()
     if a.summarize_traffic:
-        t = summarize_traffic(*a.summarize_traffic)
+        t = summarize_traffic(*a.summarize_traffic, family=a.traffic_family)
         print("TRAFFIC_JSON " + json.dumps(t))
         return
     if a.gpus != 1:
@@ -451,6 +457,9 @@ def main():
         return
     if a.extras:
         print(json.dumps(mode_and_stream_extras(torch)), flush=True)
+        return
+    if a.hbm_only:
+        print(json.dumps(hbm_kernels(torch, lpp)), flush=True)
         return
     if a.only_workload:
         from paper_2203_06638_amd import lpp as _lpp
