@@ -291,8 +291,8 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
             const float m2 = red[0][tid] + red[1][tid];
             if (sums.acc) {
                 const double mu = tmean[tid], nr = (double)nvalid;
-                acc_add(sums.acc, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
-                acc_add(sums.acc, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)m2 + nr * mu * mu);
+                acc_add(sums.acc, 0, (int)blockIdx.x, g.Ncols, n, mu * nr);
+                acc_add(sums.acc, 1, (int)blockIdx.x, g.Ncols, n, (double)m2 + nr * mu * mu);
             } else {
                 sums.p0[(long)blockIdx.x * g.Ncols + n] = tmean[tid];
                 sums.p1[(long)blockIdx.x * g.Ncols + n] = m2;

@@ -258,8 +258,8 @@ __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ 
                 for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
                 if (sums.acc) {
                     const double mu = tile_mean[threadIdx.x], nr = (double)rows;
-                    acc_add(sums.acc, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
-                    acc_add(sums.acc, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)t + nr * mu * mu);
+                    acc_add(sums.acc, 0, (int)blockIdx.x, g.Ncols, n, mu * nr);
+                    acc_add(sums.acc, 1, (int)blockIdx.x, g.Ncols, n, (double)t + nr * mu * mu);
                 } else {
                     sums.p0[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
                     sums.p1[(long)blockIdx.x * g.Ncols + n] = t;
@@ -440,8 +440,8 @@ __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ sr
                 for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
                 if (sums.acc) {
                     const double mu = tile_mean[threadIdx.x], nr = (double)rows;
-                    acc_add(sums.acc, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
-                    acc_add(sums.acc, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)t + nr * mu * mu);
+                    acc_add(sums.acc, 0, (int)blockIdx.x, g.Ncols, n, mu * nr);
+                    acc_add(sums.acc, 1, (int)blockIdx.x, g.Ncols, n, (double)t + nr * mu * mu);
                 } else {
                     sums.p0[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
                     sums.p1[(long)blockIdx.x * g.Ncols + n] = t;
@@ -713,8 +713,8 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
                 for (int w = 0; w < WM; ++w) tt += red[w][threadIdx.x];
                 if (sums.acc) {
                     const double mu = tile_mean[threadIdx.x], nr = (double)npix;
-                    acc_add(sums.acc, 0, blockIdx.x % kAccSlots, g.Ncols, n, mu * nr);
-                    acc_add(sums.acc, 1, blockIdx.x % kAccSlots, g.Ncols, n, (double)tt + nr * mu * mu);
+                    acc_add(sums.acc, 0, (int)blockIdx.x, g.Ncols, n, mu * nr);
+                    acc_add(sums.acc, 1, (int)blockIdx.x, g.Ncols, n, (double)tt + nr * mu * mu);
                 } else {
                     sums.p0[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
                     sums.p1[(long)blockIdx.x * g.Ncols + n] = tt;

@@ -46,12 +46,13 @@ hipError_t launch_timestamp(unsigned long long* log, const StepArgs* args, long 
 // selects the sum; bnacc.h), merged across workgroups in arrival order; the
 // first kernel of a step zeroes them.  Otherwise tile t writes its partials
 // to p0..p2 [T][C] and a finalize kernel merges them in a fixed order, so the
-// result is bitwise reproducible.  Eight copies per channel (workgroup b
-// adds to copy b mod 8): with 512-workgroup producers 64 adds meet at an
-// address, and every consumer workgroup reads 8 per sum.  Measured against
+// result is bitwise reproducible.  Eight copies per channel (a power of two;
+// acc_add picks workgroup b's copy): with 512-workgroup producers 64 adds
+// meet at an address, and every consumer workgroup reads 8 per sum.  Measured against
 // 1, 2, 4, 16 and 32 copies: 8 is the fastest on ResNet-20 (332K samples/s
 // against 316K with 32, 291K with 2) and on every other workload.
 constexpr int kAccSlots = 8;
+static_assert((kAccSlots & (kAccSlots - 1)) == 0, "kAccSlots must be a power of two");
 struct BnSums {
     double* acc;
     float* p0;

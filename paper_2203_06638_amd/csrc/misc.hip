@@ -90,8 +90,8 @@ __global__ __launch_bounds__(256) void stats_partial_k(const T* __restrict__ x, 
                 const float mu = mean_s[(tid * 4 + k) & 1023];
                 if (out.acc) {
                     const double n = (double)rows, m = (double)mu;
-                    acc_add(out.acc, 0, blockIdx.x % kAccSlots, C, c, m * n);
-                    acc_add(out.acc, 1, blockIdx.x % kAccSlots, C, c, (double)t[k] + n * m * m);
+                    acc_add(out.acc, 0, (int)blockIdx.x, C, c, m * n);
+                    acc_add(out.acc, 1, (int)blockIdx.x, C, c, (double)t[k] + n * m * m);
                 } else {
                     out.p0[(long)blockIdx.x * C + c] = mu;
                     out.p1[(long)blockIdx.x * C + c] = t[k];
@@ -382,13 +382,13 @@ __global__ __launch_bounds__(256) void bn_bwd_reduce_k(BnBwdArgs a, int R, BnSum
         }
         if (tid < nq) {
             const f4 t0 = red[0][tid], t1 = red[1][tid], t2 = red[2][tid];
-            const int slot = blockIdx.x % kAccSlots;
+            const int wg = (int)blockIdx.x;
             for (int k = 0; k < 4; ++k) {
                 const int c = (qbase + tid) * 4 + k;
                 if (out.acc) {
-                    acc_add(out.acc, 0, slot, C, c, (double)t0[k]);
-                    acc_add(out.acc, 1, slot, C, c, (double)t1[k]);
-                    if (DUAL) acc_add(out.acc, 2, slot, C, c, (double)t2[k]);
+                    acc_add(out.acc, 0, wg, C, c, (double)t0[k]);
+                    acc_add(out.acc, 1, wg, C, c, (double)t1[k]);
+                    if (DUAL) acc_add(out.acc, 2, wg, C, c, (double)t2[k]);
                 } else {
                     const long o = (long)blockIdx.x * C + c;
                     out.p0[o] = t0[k];
