@@ -112,6 +112,22 @@ def test_describe_rejects_bad_models():
     assert _desc_err(m, dtype=7) == -1
 
 
+def test_empty_and_out_of_range_sizes_are_rejected():
+    """A batch of zero (or negative) images is rejected by the description
+    check, and a replica count outside [1, 16] by lpp_init before anything
+    touches a device."""
+    m = PM.tiny_cnn()
+    for b in (0, -1):
+        with pytest.raises(lpp.LppError) as e:
+            lpp.describe(m, batch=b)
+        assert e.value.code == lpp.EINVAL
+    desc = lpp.make_desc(m, 4)
+    for k in (0, 17):
+        ctx = lpp.C.c_void_p()
+        rc = lpp.lib().lpp_init(lpp.C.byref(desc), k, m.P, None, lpp.C.byref(ctx))
+        assert rc == lpp.EINVAL and not ctx.value
+
+
 def test_describe_channel_rules():
     """Channel counts that are not a multiple of 4 are accepted only on the
     output of a 1x1 stride-1 unpadded fp32 conv, read by ReLU / pooling /
