@@ -489,7 +489,8 @@ template <int MODE, int KS, int WM, int TM, int TN, bool STATS, bool INBN>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu((TM <= 2 && !INBN && !STATS) ? 4 : 1, 8)))
 void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
                                                      const float* __restrict__ bias, float* __restrict__ Y,
-                                                     ConvGeom g, TileGeom t, int accumulate, BnSums sums, BnFwd inbn) {
+                                                     ConvGeom g, TileGeom t, int accumulate, BnSums sums, BnFwd inbn,
+                                                     BnBwdSum bs) {
     constexpr int WN = 4 / WM;
     constexpr int TP = WM * TM * 16, BN = WN * TN * 16;
     constexpr int LDW = 20;
@@ -632,6 +633,7 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
     const long m0 = (long)blockIdx.x * TP;      // tiles are consecutive runs of the NHWC rows
     const int pix_base = wm * TM * 16;
     const int n_base = n0 + wn * TN * 16;
+    f4 bs0 = f4{0.f, 0.f, 0.f, 0.f}, bs1 = bs0;   // data gradient with STATS: sum gm, sum gm*xhat
     if (bias) {
 #pragma unroll
         for (int y = 0; y < TN; ++y) {
@@ -657,6 +659,18 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
                 for (int i = 0; i < 4; ++i) Ot[(x * 16 + gi * 4 + i) * OP + y * 16 + li] = acc[x][y][i];
         __builtin_amdgcn_wave_barrier();          // a wave's LDS accesses execute in order
         constexpr int QPP = TN * 4;               // float4 quads per pixel of the block
+        // data gradient with STATS: this lane's channel quad is fixed (64 %
+        // QPP == 0); its BN's mean, rstd, scale and shift
+        f4 bmu{}, brs{}, bsc{}, bsh{};
+        if (MODE == CONV_DGRAD && STATS) {
+            const int n = n_base + (lane % QPP) * 4;
+            if (n < g.Ncols) {
+                bmu = *(const f4*)(bs.aux + n);
+                brs = *(const f4*)(bs.aux + g.Ncols + n);
+                bsc = *(const f4*)(bs.aux + 2 * g.Ncols + n);
+                bsh = *(const f4*)(bs.aux + 3 * g.Ncols + n);
+            }
+        }
 #pragma unroll
         for (int k = 0; k < TM * 16 * QPP / 64; ++k) {
             const int e = k * 64 + lane;
@@ -666,10 +680,62 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
                 const f4 v = *(const f4*)(Ot + p * OP + qd * 4);
                 f4* o = (f4*)(Y + (m0 + pix_base + p) * g.Ncols + n);
                 *o = accumulate ? *o + v : v;
+                if (MODE == CONV_DGRAD && STATS) {
+                    // gm = v where the forward's ReLU passed, xhat of the BN input
+                    const f4 x = *(const f4*)(bs.x1 + (m0 + pix_base + p) * g.Ncols + n);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float gm = __builtin_fmaf(x[j], bsc[j], bsh[j]) > 0.f ? v[j] : 0.f;
+                        bs0[j] += gm;
+                        bs1[j] += gm * ((x[j] - bmu[j]) * brs[j]);
+                    }
+                }
             }
         }
     }
-    if (STATS) {
+    if constexpr (MODE == CONV_DGRAD && STATS) {
+        // lanes of one channel quad (lane mod QPP) summed by a fixed xor tree,
+        // then the WM waves of this channel block in order
+        constexpr int QPP = TN * 4;
+        static_assert(64 % QPP == 0, "a lane keeps one channel quad");
+#pragma unroll
+        for (int o = QPP; o < 64; o <<= 1) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                bs0[j] += __shfl_xor(bs0[j], o);
+                bs1[j] += __shfl_xor(bs1[j], o);
+            }
+        }
+        __shared__ f4 bred[4][2][QPP];
+        __syncthreads();
+        if (lane < QPP) {
+            bred[wave][0][lane] = bs0;
+            bred[wave][1][lane] = bs1;
+        }
+        __syncthreads();
+        if (threadIdx.x < WN * QPP) {
+            const int wnb = threadIdx.x / QPP, qd = threadIdx.x - wnb * QPP;
+            f4 t0 = bred[wnb * WM][0][qd], t1 = bred[wnb * WM][1][qd];
+            for (int w = 1; w < WM; ++w) {
+                t0 += bred[wnb * WM + w][0][qd];
+                t1 += bred[wnb * WM + w][1][qd];
+            }
+            const int nb = n0 + wnb * TN * 16 + qd * 4;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int c = nb + j;
+                if (c >= g.Ncols) continue;
+                if (sums.acc) {
+                    acc_add(sums.acc, 0, (int)blockIdx.x, g.Ncols, c, (double)t0[j]);
+                    acc_add(sums.acc, 1, (int)blockIdx.x, g.Ncols, c, (double)t1[j]);
+                } else {
+                    sums.p0[(long)blockIdx.x * g.Ncols + c] = t0[j];
+                    sums.p1[(long)blockIdx.x * g.Ncols + c] = t1[j];
+                }
+            }
+        }
+    }
+    if (MODE == CONV_FWD && STATS) {
         __shared__ float red[WM][BN];
         __shared__ float tile_mean[BN];
 #pragma unroll
@@ -772,36 +838,41 @@ static bool pick_tile(int mode, const ConvGeom& g, TileCfg& out) {
 
 template <int MODE, int KS, int WM, int TM, int TN>
 static hipError_t launch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              const TileCfg& c, bool acc, const BnSums* stats, const BnFwd* inbn, hipStream_t st) {
+                              const TileCfg& c, bool acc, const BnSums* stats, const BnFwd* inbn,
+                              const BnBwdSum* bsv, hipStream_t st) {
     constexpr int BN = (4 / WM) * TN * 16;
     dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
     const BnSums sm = stats ? *stats : BnSums{};
     const BnFwd ib = inbn ? *inbn : BnFwd{};
+    const BnBwdSum bsum = bsv ? *bsv : BnBwdSum{};
+    // a data gradient's statistics are the sums of a BN backward (bsv)
+    if (MODE == CONV_DGRAD && stats && (!bsv || acc)) return hipErrorInvalidValue;
     if (inbn) {
         if (MODE != CONV_FWD || g.Cs > kFoldMaxC) return hipErrorInvalidValue;
         if (stats)
             launch((conv_tile_f32<MODE, KS, WM, TM, TN, true, true>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
-                   c.t, (int)acc, sm, ib);
+                   c.t, (int)acc, sm, ib, bsum);
         else
             launch((conv_tile_f32<MODE, KS, WM, TM, TN, false, true>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
-                   c.t, (int)acc, sm, ib);
+                   c.t, (int)acc, sm, ib, bsum);
     } else if (stats) {
         launch((conv_tile_f32<MODE, KS, WM, TM, TN, true, false>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
-               c.t, (int)acc, sm, ib);
+               c.t, (int)acc, sm, ib, bsum);
     } else {
         launch((conv_tile_f32<MODE, KS, WM, TM, TN, false, false>), grid, dim3(256), c.lds, st, src, B, bias, Y, g,
-               c.t, (int)acc, sm, ib);
+               c.t, (int)acc, sm, ib, bsum);
     }
     return hipGetLastError();
 }
 
 template <int MODE>
 static hipError_t dispatch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                                const TileCfg& c, bool acc, const BnSums* stats, const BnFwd* inbn, hipStream_t st) {
-#define TILE(WM_, TM_, TN_)                                                                                  \
-    if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) {                                                         \
-        if (g.R == 3) return launch_tile<MODE, 3, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, inbn, st); \
-        return launch_tile<MODE, 1, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, inbn, st);               \
+                                const TileCfg& c, bool acc, const BnSums* stats, const BnFwd* inbn,
+                                const BnBwdSum* bsv, hipStream_t st) {
+#define TILE(WM_, TM_, TN_)                                                                                        \
+    if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) {                                                               \
+        if (g.R == 3) return launch_tile<MODE, 3, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, inbn, bsv, st); \
+        return launch_tile<MODE, 1, WM_, TM_, TN_>(src, B, bias, Y, g, c, acc, stats, inbn, bsv, st);               \
     }
     TILE(4, 4, 1) TILE(4, 2, 1) TILE(2, 4, 1) TILE(2, 2, 1) TILE(1, 4, 1) TILE(2, 2, 2) TILE(1, 4, 2)
     TILE(4, 1, 1) TILE(2, 1, 1) TILE(1, 2, 1) TILE(1, 1, 1)
@@ -1086,10 +1157,10 @@ static ConvCfg pick_cfg(const ConvGeom& g) {
 
 template <int MODE>
 static hipError_t launch_mode(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              bool acc, const BnSums* stats, const BnFwd* inbn, hipStream_t st) {
+                              bool acc, const BnSums* stats, const BnFwd* inbn, const BnBwdSum* bsv, hipStream_t st) {
     TileCfg tc;
-    if (pick_tile(MODE, g, tc)) return dispatch_tile<MODE>(src, B, bias, Y, g, tc, acc, stats, inbn, st);
-    if (inbn) return hipErrorInvalidValue;   // folding needs the spatial kernel
+    if (pick_tile(MODE, g, tc)) return dispatch_tile<MODE>(src, B, bias, Y, g, tc, acc, stats, inbn, bsv, st);
+    if (inbn || bsv) return hipErrorInvalidValue;   // folding and backward sums need the spatial kernel
     if (MODE == CONV_DGRAD) {
         S2Cfg sc;
         if (pick_s2(g, sc)) return dispatch_s2(src, B, Y, g, sc, acc, st);
@@ -1125,10 +1196,19 @@ int conv_tile_rows(const ConvGeom& g) {
 
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
                              const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st,
-                             const BnFwd* inbn) {
-    if (mode == CONV_FWD) return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, stats, inbn, st);
-    if (inbn) return hipErrorInvalidValue;
-    return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, nullptr, nullptr, st);
+                             const BnFwd* inbn, const BnBwdSum* bsum) {
+    if (mode == CONV_FWD) {
+        if (bsum) return hipErrorInvalidValue;
+        return launch_mode<CONV_FWD>(src, B, bias, Y, g, accumulate, stats, inbn, nullptr, st);
+    }
+    if (inbn || (bsum != nullptr) != (stats != nullptr)) return hipErrorInvalidValue;
+    return launch_mode<CONV_DGRAD>(src, B, bias, Y, g, accumulate, stats, nullptr, bsum, st);
+}
+
+int conv_dgrad_sum_tiles(const ConvGeom& gd) {
+    TileCfg tc;
+    if (!pick_tile(CONV_DGRAD, gd, tc)) return 0;
+    return gd.Nb * tc.t.tiles_per_img;
 }
 
 bool conv_fold_ok(const ConvGeom& g, const WgradPlan& p) {

@@ -83,9 +83,21 @@ constexpr int kFoldMaxC = 512;
 // sum of squared deviations (p1), T = ceil(M / conv_tile_rows(g)) tiles.
 // inbn (forward only; see conv_fold_ok): src is the input of a BN + ReLU
 // and the pass reads relu(bn(src)) without storing it.
+// Data gradients with stats (and bsum): the output g is the gradient at a
+// training-mode BN + ReLU whose input x1 has g's layout; the pass also forms
+// that BN backward's sums, q = 0: sum gm and q = 1: sum gm*xhat, gm = g
+// where fma(x1, scale, shift) > 0, xhat = (x1 - mean) rstd, from aux =
+// [mean | rstd | scale | shift]: into stats->acc, or as partials p0/p1 per
+// tile, conv_dgrad_sum_tiles(g) tiles (spatial kernel only; not accumulating).
+struct BnBwdSum {
+    const float* x1;
+    const float* aux;
+};
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
                              const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st,
-                             const BnFwd* inbn = nullptr);
+                             const BnFwd* inbn = nullptr, const BnBwdSum* bsum = nullptr);
+// Tiles of the spatial data-gradient kernel for g, or 0 when it does not take g.
+int conv_dgrad_sum_tiles(const ConvGeom& g);
 int conv_tile_rows(const ConvGeom& g);
 
 // Weight gradient: part[split][Cout][Ktot] = partial sums over pixel ranges

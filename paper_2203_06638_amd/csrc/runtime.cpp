@@ -59,6 +59,8 @@ struct Layer {
     bool pw = false;              // conv: 1x1, stride 1, no padding, output channels not a multiple of 4 --
                                   //   run as a linear layer applied to every pixel (fp32)
     int in_bn = -1;               // conv: reads relu(bn(x)) of this BN layer's input x, folded into its loads
+    int gsum_bn = -1;             // conv: its data gradient (the gradient at that BN + ReLU's output) also
+                                  //   forms the sums of this BN's backward
     long wf_off = -1, wd_off = -1;// conv: W_f / W_d in the worker's weight buffer (elements)
     double macs = 0;              // forward multiply-adds (conv, linear)
     lpp::WgradPlan wg{};
@@ -94,6 +96,7 @@ struct Group {
     int relu = -1;      // G_BNACT: the closing ReLU, if any
     int lin = -1;       // G_HEAD: the linear layer
     bool fold = false;  // G_BNACT: BN + ReLU folded into the consuming conv (nothing launched forward)
+    bool rsum = false;  // G_BNACT (folded): its backward sums come from the consuming conv's data gradient
 };
 
 struct Model {
@@ -424,6 +427,19 @@ void plan_folds(Model& M, int N) {
         if (!lpp::conv_fold_ok(g, Y.wg)) continue;
         G.fold = true;
         Y.in_bn = G.a;
+        // the conv's data gradient is the whole gradient at the group output
+        // (its only consumer): its epilogue also forms the BN backward's sums
+        const lpp::ConvGeom gd{N, Y.out.h, Y.out.w, Y.L.cout, Y.in0.h, Y.in0.w, Y.L.cin, Y.L.k, Y.L.k, Y.L.stride,
+                               Y.L.pad};
+        // (only when the conv's group runs right after this group, so that in
+        // the backward nothing runs between them that reuses the partials)
+        const long gi = &G - M.groups.data();
+        const bool next = gi + 1 < (long)M.groups.size() && M.groups[gi + 1].kind == G_CONV &&
+                          M.groups[gi + 1].a == M.consumers[G.out][0];
+        if (next && lpp::conv_dgrad_sum_tiles(gd) > 0) {
+            G.rsum = true;
+            Y.gsum_bn = G.a;
+        }
     }
 }
 
@@ -866,7 +882,19 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                     LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
                            lpp::launch_conv_bf16(lpp::CONV_DGRAD, (const uint16_t*)dy, (const uint16_t*)c->wdg(w, Y),
                                                  nullptr, (uint16_t*)dx0, g, pl.acc0[G.a] != 0, nullptr, st));
-                else
+                else if (Y.gsum_bn >= 0) {
+                    // dx0 is the whole gradient at a folded BN + ReLU's output:
+                    // the pass also forms that BN backward's sums
+                    const lpp::BnSums out = c->fixed_order ? lpp::BnSums{nullptr, w.ps0, w.ps1, nullptr}
+                                                           : lpp::BnSums{c->acc_bwd(w, Y.gsum_bn), nullptr, nullptr,
+                                                                         nullptr};
+                    const lpp::BnBwdSum bsum{(const float*)c->act(w, M.layers[Y.gsum_bn].L.in0),
+                                             c->aux(w, Y.gsum_bn)};
+                    LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
+                           lpp::launch_conv_igemm(lpp::CONV_DGRAD, (const float*)dy, (const float*)c->wdg(w, Y),
+                                                  nullptr, (float*)dx0, g, pl.acc0[G.a] != 0, &out, st, nullptr,
+                                                  &bsum));
+                } else
                     LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
                            lpp::launch_conv_igemm(lpp::CONV_DGRAD, (const float*)dy, (const float*)c->wdg(w, Y),
                                                   nullptr, (float*)dx0, g, pl.acc0[G.a] != 0, nullptr, st));
@@ -876,6 +904,13 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
         case G_BNACT: {
             const int C = Y.out.c;
             const int b2 = G.bn2;
+            int rsum_tiles = 0;   // partials of the consuming conv's data gradient (folded groups)
+            if (G.rsum) {
+                const Layer& Y2 = M.layers[M.consumers[G.out][0]];
+                rsum_tiles = lpp::conv_dgrad_sum_tiles(lpp::ConvGeom{N, Y2.out.h, Y2.out.w, Y2.L.cout, Y2.in0.h,
+                                                                     Y2.in0.w, Y2.L.cin, Y2.L.k, Y2.L.k,
+                                                                     Y2.L.stride, Y2.L.pad});
+            }
             const bool want1 = pl.run[G.a] && (pl.wgrad[G.a] || pl.din0[G.a]);
             const bool want2 = b2 >= 0 && pl.run[b2] && (pl.wgrad[b2] || pl.din0[b2]);
             bool want_res = false, acc_res = false;
@@ -902,9 +937,10 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                 const double bytes = (a.mask ? 3.0 : 2.0) * eb * Min * C + (want2 ? eb * Min * C : 0.0);
                 if (c->fixed_order) {
                     const lpp::BnSums out{nullptr, w.ps0, w.ps1, w.ps2};
-                    LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(dt, a, out, st));
+                    // (a folded group's sums came from the consuming conv's data gradient)
+                    if (!G.rsum) LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(dt, a, out, st));
                     LAUNCH("bn_bwd", 0.0, st,
-                           lpp::launch_bn_bwd_finalize(w.ps0, w.ps1, w.ps2, lpp::stats_tiles(Min, C), Min, C,
+                           lpp::launch_bn_bwd_finalize(w.ps0, w.ps1, w.ps2, G.rsum ? rsum_tiles : lpp::stats_tiles(Min, C), Min, C,
                                                        w.v + Y.poff, ax + C, gg1, gb1, ax + 4 * C,
                                                        want2 ? w.v + Y2->poff : nullptr, want2 ? ax2 + C : nullptr,
                                                        gg2, gb2, want2 ? ax2 + 4 * C : nullptr, st));
@@ -912,7 +948,7 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                     k.coef2 = want2 ? ax2 + 4 * C : nullptr;
                 } else {
                     const lpp::BnSums out{c->acc_bwd(w, G.a), nullptr, nullptr, nullptr};
-                    LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(dt, a, out, st));
+                    if (!G.rsum) LAUNCH("bn_bwd", bytes, st, lpp::launch_bn_bwd_reduce(dt, a, out, st));
                     k = lpp::BnBwdCoef{c->acc_bwd(w, G.a), w.v + Y.poff, gg1, gb1,
                                        want2 ? w.v + Y2->poff : nullptr, gg2, gb2, nullptr, nullptr};
                     if (use_coef_kernel(Min, C, want2 ? 3 : 2)) {
@@ -1136,6 +1172,11 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
             const long tiles = (rows_out + tr - 1) / tr;
             ps = std::max<long>(ps, tiles * Y.L.cout);
             ps = std::max<long>(ps, (long)lpp::stats_tiles(rows_out, Y.L.cout) * Y.L.cout);
+            if (Y.gsum_bn >= 0) {
+                const lpp::ConvGeom gd{N, Y.out.h, Y.out.w, Y.L.cout, Y.in0.h, Y.in0.w, Y.L.cin, Y.L.k, Y.L.k,
+                                       Y.L.stride, Y.L.pad};
+                ps = std::max<long>(ps, (long)lpp::conv_dgrad_sum_tiles(gd) * Y.L.cin);
+            }
             wpart = std::max<long>(wpart, align64(Y.wg.part_floats));
             wsum += align64(Y.wg.part_floats);
         }
