@@ -428,7 +428,7 @@ def main():
         print("TRAFFIC_JSON " + json.dumps(t))
         return
     if a.gpus != 1:
-        print("bench.py measures one GPU only: this build runs the per-node step on a single MI355X "
+        print("bench.py measures one GPU only: the library runs the per-node step on a single MI355X "
               "(--gpus %d is not supported)" % a.gpus, file=sys.stderr)
         sys.exit(2)
     if not (1 <= a.hw_queues <= 32 and 1 <= a.workload_hw_queues <= 32):

@@ -51,7 +51,7 @@ enum lpp_status {
     LPP_ENOMEM = -2,       /* device or host allocation failed              */
     LPP_EHIP = -3,         /* a HIP runtime call failed                     */
     LPP_ESTATE = -4,       /* call not valid in the context's current state */
-    LPP_EUNSUPPORTED = -5  /* valid request this build does not implement   */
+    LPP_EUNSUPPORTED = -5  /* valid request the library does not implement  */
 };
 
 enum lpp_op {
