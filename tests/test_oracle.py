@@ -26,6 +26,12 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 def torch_loss(net, x, images, labels):
     """Loss and logits of the layer list computed with torch.nn.functional
     (fp64, CPU); x is a torch leaf so autograd gives the gradient."""
+    loss, logits, _ = torch_forward(net, x, images, labels)
+    return loss, logits
+
+
+def torch_forward(net, x, images, labels):
+    """As torch_loss, also returning every layer's output tensor."""
     acts = []
     img = torch.as_tensor(np.asarray(images, np.float64))
     for rec in net.layers:
@@ -58,7 +64,7 @@ def torch_loss(net, x, images, labels):
         acts.append(y)
     logits = acts[-1].reshape(img.shape[0], -1)
     loss = F.cross_entropy(logits, torch.as_tensor(np.asarray(labels, np.int64)))
-    return loss, logits
+    return loss, logits, acts
 
 
 def torch_grad(net, x0, images, labels):
@@ -453,3 +459,217 @@ def test_concat_forward_and_backward_closed_form():
     dz = (p - np.eye(5)[lab]) / len(lab)
     np.testing.assert_allclose(g[6:8], dz[:, :2].sum(axis=0), rtol=0, atol=1e-14)
     np.testing.assert_allclose(g[17:20], dz[:, 2:].sum(axis=0), rtol=0, atol=1e-14)
+
+
+# --------------------------------------------------------------------------
+# the oracle's helper outputs: activation gradients, condition scales and
+# kink margins, each against a definition computed outside the oracle
+# --------------------------------------------------------------------------
+
+def _torch_layer_grads(net, x0, images, labels):
+    """PyTorch fp64 autograd with retain_grad on every layer output: returns
+    (layer outputs, their loss gradients, parameter gradient)."""
+    x = torch.tensor(np.asarray(x0, np.float64), requires_grad=True)
+    loss, _, acts = torch_forward(net, x, images, labels)
+    for a in acts:
+        a.retain_grad()
+    loss.backward()
+    outs = [a.detach().numpy() for a in acts]
+    grads = [np.zeros(a.shape) if a.grad is None else a.grad.numpy() for a in acts]
+    return outs, grads, x.grad.numpy()
+
+
+@pytest.mark.parametrize("name", sorted(MINI_NETS))
+def test_activation_grad_matches_autograd_every_layer(name):
+    """ref_activation_grad(layer) is dL/d(output of layer) of the full
+    backward (Sec. 2: the chain rule through every layer).  Against PyTorch
+    fp64 autograd with retain_grad, for every layer of every mini net."""
+    net = MINI_NETS[name]()
+    x, img, lab = _inputs(net, 4, 61)
+    _, tgrads, _ = _torch_layer_grads(net, x, img, lab)
+    for l in range(len(net.layers)):
+        got = R.activation_grad(net, x, img, lab, l)
+        want = tgrads[l].reshape(got.shape)
+        scale = max(np.max(np.abs(want)), 1e-300)
+        assert np.max(np.abs(got - want)) <= 1e-12 * scale, (name, l)
+
+
+def _windows(xp, k, st, oh, ow):
+    """xp[N, C, H, W] (already padded) -> [N, C, oh, ow, k, k] windows."""
+    n, c = xp.shape[:2]
+    out = np.empty((n, c, oh, ow, k, k))
+    for r in range(k):
+        for s in range(k):
+            out[..., r, s] = xp[:, :, r:r + st * oh:st, s:s + st * ow:st]
+    return out
+
+
+def _scale_net():
+    """conv(+bias) -> BN -> ReLU -> conv 3x3/2 -> BN -> ReLU -> GAP ->
+    linear: every kind of parameter gradient the oracle scales."""
+    net = M.Net("scale", 3, 8, 8, 5)
+    a = net.conv(-1, 3, 4, 3, 1, 1, bias=True)
+    a = net.relu(net.bn(a, 4))
+    a = net.conv(a, 4, 6, 3, 2, 1)
+    a = net.relu(net.bn(a, 6))
+    net.linear(net.gap(a), 6, 5)
+    net.set_blocks([1])
+    return net
+
+
+def test_grad_scale_definition_from_autograd():
+    """ref_grad_scale's C_e is, for each parameter gradient entry (a sum of
+    products), the sum of the magnitudes of those products.  Written out
+    from autograd's layer inputs X and output gradients dY (fp64):
+    conv weight C[k,c,r,s] = sum_{n,p,q} |dY[n,k,p,q]| |X_pad[n,c,p*st+r,q*st+s]|,
+    conv bias sum |dY|; BN gamma sum |dY * xhat|, beta sum |dY|; linear
+    weight |dz|^T |F|, bias sum |dz|."""
+    net = _scale_net()
+    x, img, lab = _inputs(net, 5, 62, perturb=0.3)
+    outs, grads, gt = _torch_layer_grads(net, x, img, lab)
+    g, sc = R.grad_scale(net, x, img, lab)
+    np.testing.assert_allclose(g, gt, rtol=1e-10, atol=1e-14)
+    img64 = np.asarray(img, np.float64)
+    want = np.zeros(net.d)
+    for l, rec in enumerate(net.layers):
+        X = img64 if rec["in0"] < 0 else outs[rec["in0"]]
+        dY = grads[l]
+        po = rec["poff"]
+        if rec["op"] == M.CONV:
+            k, st, pad = rec["k"], rec["stride"], rec["pad"]
+            xp = np.pad(np.abs(X), ((0, 0), (0, 0), (pad, pad), (pad, pad)))
+            oh, ow = dY.shape[2:]
+            win = _windows(xp, k, st, oh, ow)                  # [N, C, oh, ow, k, k]
+            cw = np.einsum("nkpq,ncpqrs->kcrs", np.abs(dY), win)
+            n = cw.size
+            want[po:po + n] = cw.ravel()
+            if rec["bias"]:
+                want[po + n:po + n + rec["cout"]] = np.abs(dY).sum(axis=(0, 2, 3))
+        elif rec["op"] == M.BN:
+            c = rec["cout"]
+            mu = X.mean(axis=(0, 2, 3), keepdims=True)
+            var = X.var(axis=(0, 2, 3), keepdims=True)
+            xhat = (X - mu) / np.sqrt(var + R.BN_EPS)
+            want[po:po + c] = np.abs(dY * xhat).sum(axis=(0, 2, 3))
+            want[po + c:po + 2 * c] = np.abs(dY).sum(axis=(0, 2, 3))
+        elif rec["op"] == M.LINEAR:
+            Fm = np.abs(X.reshape(X.shape[0], -1))
+            dz = np.abs(dY.reshape(dY.shape[0], -1))
+            n = rec["cout"] * rec["cin"]
+            want[po:po + n] = (dz.T @ Fm).ravel()
+            want[po + n:po + n + rec["cout"]] = dz.sum(axis=0)
+    np.testing.assert_allclose(sc, want, rtol=1e-10, atol=0)
+    # a scale that dropped a term or took |sum| instead of sum|.| would be
+    # at most |g|; the definition gives strictly more wherever terms cancel
+    assert np.all(sc >= np.abs(gt) * (1 - 1e-12))
+    assert np.mean(sc > 1.5 * np.abs(gt)) > 0.5
+
+
+@pytest.mark.parametrize("name", sorted(MINI_NETS))
+def test_grad_scale_bounds_gradient_on_minis(name):
+    """|g_e| = |sum of terms| <= sum |terms| = C_e for every entry (triangle
+    inequality), with equality only where no terms cancel; the gradient the
+    function returns is the oracle's full gradient."""
+    net = MINI_NETS[name]()
+    x, img, lab = _inputs(net, 4, 63)
+    g, sc = R.grad_scale(net, x, img, lab)
+    _, _, gref = R.forward_backward(net, x, img, lab)
+    assert np.array_equal(g, gref)
+    assert np.all(sc >= np.abs(g) * (1 - 1e-12) - 1e-300)
+    assert np.all(np.isfinite(sc)) and np.max(sc) > 0
+
+
+def _relu_probe_net(c, h, w):
+    net = M.Net("relu_probe", c, h, w, 3)
+    a = net.relu(-1)
+    net.linear(net.gap(a), c, 3)
+    net.set_blocks([1])
+    return net
+
+
+def _pool_probe_net(c, h, w, k, st, pad):
+    net = M.Net("pool_probe", c, h, w, 3)
+    a = net.maxpool(-1, k, st, pad)
+    net.linear(net.gap(a), c, 3)
+    net.set_blocks([1])
+    return net
+
+
+def test_kink_margin_relu_closed_form():
+    """For a ReLU reading the images directly, the margin is
+    min|v| / max|v| over the images: built with every value of magnitude
+    in [0.5, 4] except one of magnitude 0.02 (and one of 4), it is 0.005."""
+    rng = np.random.default_rng(7)
+    img = rng.uniform(0.5, 3.5, size=(2, 3, 4, 4)) * rng.choice([-1.0, 1.0], size=(2, 3, 4, 4))
+    img[1, 2, 3, 0] = -0.02
+    img[0, 1, 0, 2] = 4.0
+    net = _relu_probe_net(3, 4, 4)
+    x = synth.init_params(net.specs, 1).astype(np.float64)
+    assert R.kink_margin(net, x, img) == pytest.approx(0.02 / 4.0, rel=1e-15)
+    img[1, 2, 3, 0] = 0.0
+    assert R.kink_margin(net, x, img) == 0.0
+
+
+def test_kink_margin_maxpool_closed_form():
+    """For a max pool reading the images, the margin is the smallest gap
+    between a window's largest and second largest value, over max|v|.
+    2x2/2 windows without padding: each window holds {t, t - gap_w, lower
+    values}; the smallest gap is 0.03 and max|v| is 6, so 0.005.  A window
+    with a repeated maximum gives 0 (both argmax choices are valid)."""
+    rng = np.random.default_rng(8)
+    n, c, h, w = 2, 2, 4, 4
+    img = np.zeros((n, c, h, w))
+    gaps = rng.uniform(0.2, 1.0, size=(n, c, 2, 2))
+    gaps[1, 0, 1, 1] = 0.03
+    for b in range(n):
+        for ch in range(c):
+            for i in range(2):
+                for j in range(2):
+                    t = rng.uniform(1.0, 5.0)
+                    vals = [t, t - gaps[b, ch, i, j], t - 2.0 - rng.uniform(), t - 3.5]
+                    perm = rng.permutation(4)
+                    for m, v in zip(perm, vals):
+                        img[b, ch, 2 * i + m // 2, 2 * j + m % 2] = v
+    img[0, 0, 0, 0] = 6.0
+    img[0, 0, 0, 1] = 5.0
+    img[0, 0, 1, 0] = 0.0
+    img[0, 0, 1, 1] = -1.0
+    net = _pool_probe_net(c, h, w, 2, 2, 0)
+    x = synth.init_params(net.specs, 1).astype(np.float64)
+    want = min(0.03, 1.0) / 6.0
+    assert R.kink_margin(net, x, img) == pytest.approx(want, rel=1e-12)
+    img[1, 1, 2, 2] = img[1, 1, 2:4, 2:4].max()
+    img[1, 1, 3, 3] = img[1, 1, 2, 2]
+    assert R.kink_margin(net, x, img) == 0.0
+
+
+def test_kink_margin_padded_pool_and_min_over_layers():
+    """3x3/2 pad-1 windows ignore the padding (it never counts as a
+    runner-up): a 1x1 image has one-element windows only, so no pool
+    margin exists; with a ReLU after the pool the margin is the ReLU's.
+    The result is the minimum over every ReLU and pool layer, each
+    relative to its own input's largest magnitude."""
+    net = M.Net("mix", 1, 3, 3, 2)
+    a = net.maxpool(-1, 3, 2, 1)          # 3x3 -> 2x2
+    a = net.relu(a)
+    net.linear(net.gap(a), 1, 2)
+    net.set_blocks([1])
+    x = synth.init_params(net.specs, 2).astype(np.float64)
+    img = np.array([[[[1.0, -2.0, 0.5],
+                      [3.0, 8.0, -0.25],
+                      [-4.0, 0.75, -0.1]]]])
+    # windows (rows/cols clipped to the image): (0,0): {1,-2,3,8} -> 8 vs 3;
+    # (0,1): {-2,0.5,8,-0.25} -> 8 vs 0.5; (1,0): {3,8,-4,0.75} -> 8 vs 3;
+    # (1,1): {8,-0.25,0.75,-0.1} -> 8 vs 0.75.  Pool margin 5 / 8.
+    # pool output is all 8: ReLU margin 8 / 8 = 1.
+    assert R.kink_margin(net, x, img) == pytest.approx(5.0 / 8.0, rel=1e-15)
+    img[0, 0, 2, 1] = 7.96       # window (1,1): 8 vs 7.96; (1,0): 8 vs 7.96
+    assert R.kink_margin(net, x, img) == pytest.approx(0.04 / 8.0, rel=1e-12)
+    one = M.Net("one", 1, 1, 1, 2)
+    a = one.maxpool(-1, 3, 2, 1)
+    a = one.relu(a)
+    one.linear(one.gap(a), 1, 2)
+    one.set_blocks([1])
+    x1 = synth.init_params(one.specs, 2).astype(np.float64)
+    # no window has a runner-up, so only the ReLU counts: |-0.5| / 0.5 = 1
+    assert R.kink_margin(one, x1, np.array([[[[-0.5]]]])) == 1.0
