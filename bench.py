@@ -16,8 +16,9 @@ Also reported, on the same JSON line:
                 timed region), against the fp32 matrix peak;
   cpu_baseline  the fp64 oracle's step timed on the host cores on a bounded
                 sample (a baseline, not a target);
-  hbm_kernels   the block-update and replica-averaging kernels on 1 GiB-
-                scale buffers, as achieved HBM GB/s;
+  hbm_kernels   the block-update, replica-averaging and snapshot kernels
+                on 1 GiB-scale buffers (and the snapshot at the bf16
+                workloads' sizes), as achieved HBM GB/s;
   workloads     the other configurations, each on a short run: ResNet-20
                 with 100 classes and K = 4 replicas of P = 4 workers
                 (averaging every 8 steps per replica), WRN-16-8 (bf16
@@ -95,43 +96,114 @@ def parse():
     return ap.parse_args()
 
 
+def _time_launches(torch, fn, reps, warm=3):
+    """Average GPU time (s) of fn() over reps launches, HIP events on the
+    current stream around the whole run (the launches queue back to back)."""
+    for _ in range(warm):
+        fn(0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(reps):
+        fn(i)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps / 1e3
+
+
+def _hbm_entry(nbytes, t, **kw):
+    gbs = nbytes / t / 1e9
+    out = {"GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 3), "us_per_launch": round(t * 1e6, 2)}
+    out.update(kw)
+    return out
+
+
+def _model_snap_convs(model, dtype, lpp):
+    """Conv descriptors of a model's parameter vector for the stand-alone
+    snapshot (the same layouts lpp_init gives the worker buffers) and the
+    algorithmic bytes of one snapshot."""
+    vw = 8 if dtype == lpp.BF16 else 4
+    eb = 2 if dtype == lpp.BF16 else 4
+    convs, poff, wf, nconv = [], 0, 0, 0
+    for rec in model.layers:
+        op, in0, _, cin, cout, k, _, _, bias = rec[:9]
+        if op == lpp.CONV:
+            cin_p = (cin + vw - 1) // vw * vw if in0 < 0 else cin
+            nf, nd = cout * k * k * cin_p, cin * k * k * cout
+            convs.append((poff, cout, cin, cin_p, k, k, wf, wf + (nf + 63) // 64 * 64))
+            wf += (nf + 63) // 64 * 64 + (nd + 63) // 64 * 64
+            nconv += cout * cin * k * k
+            poff += cout * cin * k * k + (cout if bias else 0)
+        elif op == lpp.BN:
+            poff += 2 * cout
+        elif op == lpp.LINEAR:
+            poff += cout * cin + cout
+    return convs, poff, wf, (4 + 2 * eb) * nconv + 8 * (poff - nconv)
+
+
 def hbm_kernels(torch, lpp):
-    """Block update (20 B/param with momentum) and 2-replica averaging
-    (16 B/param) on 256M-float (1 GiB) arrays: each array four times the
-    256 MB last-level cache, so every pass streams from HBM."""
+    """The streaming kernels as achieved HBM GB/s (algorithmic bytes over
+    the average launch time):
+      sgd_update   block update with momentum, 20 B/param, on 256M-float
+                   (1 GiB) arrays, each four times the 256 MB last-level cache;
+      average_k2/4 averaging rounds over 2 and 4 replicas of 1 GiB
+                   (8 B per parameter per replica);
+      snapshot_*   the snapshot on a 236M-parameter vector of 3x3 convs
+                   512 -> 512 separated by 1024 other parameters (fp32:
+                   12 B per conv weight, bf16 cast: 8 B), and at the WRN-16-8
+                   and ResNet-18 parameter vectors (bf16), rotating over
+                   buffer sets whose footprint exceeds the last-level cache."""
+    from paper_2203_06638_amd import models as PM
     n = 256 << 20
     out = {}
     x, m, g = (torch.randn(n, device="cuda") for _ in range(3))
-    for _ in range(3):
-        lpp.kernel_sgd_update(x, m, g, 1e-3, 0.9, 0.0)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 20
-    e0.record()
-    for _ in range(reps):
-        lpp.kernel_sgd_update(x, m, g, 1e-3, 0.9, 0.0)
-    e1.record()
-    torch.cuda.synchronize()
-    t = e0.elapsed_time(e1) / reps / 1e3
-    gbs = 20.0 * n / t / 1e9
-    out["sgd_update"] = {"GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 3), "bytes_per_param": 20,
-                         "params": n}
-    del m
-    y = torch.randn(n, device="cuda")
-    for _ in range(3):
-        lpp.kernel_average([x, y])
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(reps):
-        lpp.kernel_average([x, y])
-    e1.record()
-    torch.cuda.synchronize()
-    t = e0.elapsed_time(e1) / reps / 1e3
-    gbs = 16.0 * n / t / 1e9
-    out["average_k2"] = {"GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 3), "bytes_per_param": 16,
-                         "params": n}
-    del x, y, g
+    t = _time_launches(torch, lambda i: lpp.kernel_sgd_update(x, m, g, 1e-3, 0.9, 0.0), 20)
+    out["sgd_update"] = _hbm_entry(20.0 * n, t, bytes_per_param=20, params=n)
+    del m, g
+    reps = [x] + [torch.randn(n, device="cuda") for _ in range(3)]
+    for k in (2, 4):
+        t = _time_launches(torch, lambda i: lpp.kernel_average(reps[:k]), 20)
+        out["average_k%d" % k] = _hbm_entry(8.0 * k * n, t, bytes_per_param=8 * k, params=n)
+    del reps, x
     torch.cuda.empty_cache()
+    # snapshot on a 1 GiB-scale parameter vector
+    nconv, co, ci, gap = 100, 512, 512, 1024
+    per = co * ci * 9
+    for dtype, name in ((lpp.FP32, "snapshot_f32"), (lpp.BF16, "snapshot_bf16")):
+        vw = 8 if dtype == lpp.BF16 else 4
+        convs, pos, wf = [], 0, 0
+        for _ in range(nconv):
+            convs.append((pos, co, ci, ci, 3, 3, wf, wf + per))
+            wf += 2 * per
+            pos += per + gap
+        d = pos
+        plan = lpp.SnapshotPlan(convs, d, dtype, wf)
+        xs = torch.randn(d, device="cuda")
+        vs = torch.empty(d, device="cuda")
+        wb = torch.zeros(wf, device="cuda", dtype=torch.float32 if dtype == lpp.FP32 else torch.bfloat16)
+        t = _time_launches(torch, lambda i: plan.run(xs, vs, wb), 10)
+        eb = 4 if dtype == lpp.FP32 else 2
+        by = (4 + 2 * eb) * nconv * per + 8 * (d - nconv * per)
+        out[name] = _hbm_entry(by, t, bytes_per_launch=by, params=d,
+                               what="%d 3x3 convs 512->512, %d other parameters between them" % (nconv, gap))
+        plan.close()
+        del xs, vs, wb
+        torch.cuda.empty_cache()
+    # snapshot at the bf16 workloads' sizes, rotating over buffer sets
+    for mname, build in (("wrn16_8", lambda: PM.wrn16_8(100)), ("resnet18", lambda: PM.resnet18(1000))):
+        model = build()
+        convs, d, wf, by = _model_snap_convs(model, lpp.BF16, lpp)
+        plan = lpp.SnapshotPlan(convs, d, lpp.BF16, wf)
+        sets = 8
+        bufs = [(torch.randn(d, device="cuda"), torch.empty(d, device="cuda"),
+                 torch.zeros(wf, device="cuda", dtype=torch.bfloat16)) for _ in range(sets)]
+        t = _time_launches(torch, lambda i: plan.run(*bufs[i % sets]), 64)
+        out["snapshot_" + mname] = _hbm_entry(by, t, bytes_per_launch=by, params=d,
+                                              what="bf16 cast, %d buffer sets in rotation (%.0f MB touched)"
+                                                   % (sets, sets * (by / 1e6)))
+        plan.close()
+        del bufs
+        torch.cuda.empty_cache()
     return out
 
 
@@ -231,6 +303,8 @@ def run_workload(torch, lpp, name, steps, B=128, P=4):
     mean_flops = info.fwd_flops + sum(info.bwd_flops[i] for i in range(1, P + 1)) / P
     conv = {f: round(fams[f][2] / (fams[f][0] / 1e3) / 1e12, 1) for f in ("conv_fwd", "conv_dgrad", "conv_wgrad")
             if fams[f][0] > 0}
+    hbm = {f: round(fams[f][2] / (fams[f][0] / 1e3) / 1e9, 1) for f in ("snapshot", "sgd_update")
+           if fams[f][0] > 0}
     return {"workload": desc, "dtype": "bf16" if dtype == lpp.BF16 else "f32", "value": round(B * steps / dt, 1),
             "unit": "samples/s", "steps": steps, "ms_per_step": round(dt / steps * 1e3, 4),
             "mean_step_gflop": round(mean_flops / 1e9, 2), "model_tflops": round(mean_flops * steps / dt / 1e12, 2),
@@ -239,6 +313,7 @@ def run_workload(torch, lpp, name, steps, B=128, P=4):
                          "timed": "HIP events in the dispatch packets of each launch, worker 0 alone, "
                                    "partitions 1..4"},
             "conv_tflops_by_family": conv,
+            "hbm_gbs_by_family": hbm,
             "family_ms_per_4_steps": {f: round(v[0], 3) for f, v in sorted(fams.items(), key=lambda t: -t[1][0])},
             "final_loss_worker0": round(loss, 4)}
 

@@ -177,9 +177,12 @@ int lpp_step(lpp_ctx* ctx, int worker, const lpp_batch* batch, int partition, fl
  * One averaging round over the listed replicas (Alg. 1, averaging loop with
  * the all-reduce over peers done in HBM): per entry e, v_k = x_k[e] for each
  * listed k, vbar = (sum of v_k in list order) / n, x_k[e] += vbar - v_k,
- * re-reading x_k[e] just before the write so concurrent block updates are
- * kept.  replicas == NULL with n_replicas == 0 means all K in order.  Runs
- * on the averaging stream, concurrently with steps in async mode.
+ * re-reading x_k[e] (past the compute unit's cache) just before the write,
+ * so a concurrent block update written back between the two reads is kept.
+ * One that lands after the re-read, or is not yet visible to the averaging
+ * kernel, is overwritten: a lost update, as lock-free updates permit.
+ * replicas == NULL with n_replicas == 0 means all K in order.  Runs on the
+ * averaging stream, concurrently with steps in async mode.
  */
 int lpp_average(lpp_ctx* ctx, const int* replicas, int n_replicas);
 
@@ -277,6 +280,48 @@ long lpp_trace_clock_khz(const lpp_ctx* ctx);
  */
 int lpp_kernel_sgd_update(float* x, float* m, const float* g, long n, float lr, float mu, float wd, void* stream);
 int lpp_kernel_average(float* const* replicas, int n_rep, long n, void* stream);
+
+/*
+ * Stand-alone snapshot (Alg. 1, updater: "collect a snapshot" of the shared
+ * model), the kernel lpp_step runs first, on caller buffers.  A parameter
+ * vector x of d floats (device) holds conv weight tensors, each described by
+ * an lpp_snap_conv; the snapshot writes
+ *   - every conv weight W[cout][cin][kh][kw] (canonical, at x + src) into
+ *     wbuf in the two layouts the conv kernels read: the forward layout
+ *     W_f[cout][kh][kw][cin_p] at element dst_f (input channels cin..cin_p-1
+ *     are never written: keep them zero) and the data-gradient layout
+ *     W_d[cin][kh][kw][cout] at element dst_d, as float32 (dtype LPP_FP32)
+ *     or as bf16 rounded to nearest even (LPP_BF16: wbuf holds 16-bit
+ *     elements);
+ *   - every other entry of x into v[e] (device, d floats); v's conv weight
+ *     entries are not written.
+ * Algorithmic traffic: 4 + 2 x (4 or 2) bytes per conv weight, 8 per other
+ * entry.  Descriptors are sorted by src with disjoint weight ranges inside
+ * [0, d); cout and cin_p are multiples of 4 (8 for bf16), cin <= cin_p;
+ * dst_f and dst_d are multiples of 4 (8 for bf16) and both layouts lie
+ * inside wbuf's wbuf_elems elements, else LPP_EINVAL before anything is
+ * launched.
+ *
+ * lpp_snapshot_plan_create validates the list and builds the kernel's work
+ * table (host array of convs, copied; it allocates the table in device
+ * memory: at most 2 n_convs + 1 entries of 72 bytes).  lpp_kernel_snapshot
+ * enqueues the snapshot on `stream` (hipStream_t, NULL = default stream)
+ * and returns at once; x, v and wbuf must stay valid until it has run.  A
+ * plan may be used from several threads; destroy it after its last
+ * snapshot has run.
+ */
+typedef struct {
+    long src;          /* index of the tensor's first element in x              */
+    int cout, cin;     /* output / input channels                              */
+    int cin_p;         /* input channels stored per W_f row                    */
+    int kh, kw;        /* filter height and width                              */
+    long dst_f, dst_d; /* element offsets of W_f and W_d in wbuf               */
+} lpp_snap_conv;
+typedef struct lpp_snap_plan lpp_snap_plan;
+int lpp_snapshot_plan_create(const lpp_snap_conv* convs, int n_convs, long d, int dtype, long wbuf_elems,
+                             lpp_snap_plan** out);
+int lpp_kernel_snapshot(const lpp_snap_plan* plan, const float* x, float* v, void* wbuf, void* stream);
+int lpp_snapshot_plan_destroy(lpp_snap_plan* plan);
 
 #ifdef __cplusplus
 }

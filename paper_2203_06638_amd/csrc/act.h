@@ -32,6 +32,12 @@ __device__ __forceinline__ void st4(float* p, long q, f4 v) { ((f4*)p)[q] = v; }
 __device__ __forceinline__ void st4(bf16* p, long q, f4 v) {
     ((uint2*)p)[q] = uint2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
 }
+// 16 bytes of storage-type values (4 floats or 8 bf16) from floats, one store
+__device__ __forceinline__ void st16(float* p, const float* v) { *(f4*)p = f4{v[0], v[1], v[2], v[3]}; }
+__device__ __forceinline__ void st16(bf16* p, const float* v) {
+    *(uint4*)p = uint4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                       pack_bf16x2(v[6], v[7])};
+}
 __device__ __forceinline__ float ld1(const float* p, long i) { return p[i]; }
 __device__ __forceinline__ float ld1(const bf16* p, long i) { return from_bf16(p[i]); }
 __device__ __forceinline__ void st1(float* p, long i, float v) { p[i] = v; }

@@ -283,13 +283,41 @@ hipError_t launch_nchw_to_nhwc(int dt, const StepArgs* args, void* dst, int Nb, 
 hipError_t launch_nhwc_to_nchw(int dt, const void* src, float* dst, int Nb, int C, int H, int W, int Cp,
                                hipStream_t st);
 
-// Snapshot of the shared replica (Alg. 1: lock-free read of every entry):
-// v[e] = x[e] for e < d, and each conv weight also into its forward layout
-// W_f[cout][r][s][cin_p] and dgrad layout W_d[cin][r][s][cout], stored in
-// the activation type (the bf16 cast of the mixed-precision workloads);
-// dst_f / dst_d count elements of that type.
-struct SnapConv { long src, n; int cout, cin, cin_p, R, S; long dst_f, dst_d; };
-hipError_t launch_snapshot(int dt, const float* x, float* v, long d, const SnapConv* convs_dev, int n_convs,
+// Snapshot of the shared replica (Alg. 1: lock-free read of every entry).
+// Each conv weight W[cout][cin][R][S] (canonical, in x) goes into its forward
+// layout W_f[cout][R][S][cin_p] (channels cin..cin_p-1 stay zero) and its
+// data-gradient layout W_d[cin][R][S][cout], stored in the activation type
+// (the bf16 cast of the mixed-precision workloads); every other parameter
+// (batch-norm gamma/beta, biases, linear weights, per-pixel linear convs) is
+// copied into v at its canonical index.  Conv weights are not copied into v:
+// no kernel reads them there.
+//
+// The work is a table of entries, each a run of workgroups: a copy entry
+// moves [src, src + n) in chunks of kSnapCopy floats, a conv entry covers one
+// conv in kt x ct channel tiles (all R*S taps), each transposed through LDS.
+struct SnapEntry {
+    long src;       // canonical index: first element (copy) or the weight tensor (conv)
+    long n;         // copy: elements
+    long dst_f;     // conv: W_f base (elements of the activation type)
+    long dst_d;     // conv: W_d base
+    long tile0;     // first workgroup of this entry
+    int kind;       // 0 copy, 1 conv
+    int cout, cin, cin_p, RS;
+    int kt, ct, nkt;   // conv: tile of kt output x ct input channels; nkt tiles along cout
+};
+struct SnapConvDesc { long src; int cout, cin, cin_p, R, S; long dst_f, dst_d; };
+constexpr int kSnapCopy = 4096;       // floats per copy workgroup
+constexpr int kSnapLds = 9216;        // floats of a conv tile in LDS (36 KB)
+// Entry table over parameter vector [0, d): the given convs' weights (sorted
+// by src, disjoint, channel counts multiples of the 16-byte vector width) as
+// conv entries, everything else as copy entries, into out[0 .. *n_out)
+// (at most 2 * n_convs + 1 entries; max_out is out's capacity).  Returns
+// the number of workgroups, or -1 for an invalid list or too small an out;
+// *bytes gets the algorithmic HBM bytes (4 read + 2 x element size written
+// per conv weight, 8 per copied float).
+long snapshot_table(const SnapConvDesc* convs, int n_convs, long d, int dt, SnapEntry* out, int max_out,
+                    int* n_out, double* bytes);
+hipError_t launch_snapshot(int dt, const float* x, float* v, const SnapEntry* tab_dev, int n_ent, long n_tiles,
                            void* wbase, hipStream_t st);
 
 // Block update (Alg. 1 updater's last step), e in [lo, hi):

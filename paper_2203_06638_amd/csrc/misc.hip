@@ -10,6 +10,8 @@
 // fixed order (partials and a finalize kernel) or by fp64 atomic adds into
 // per-channel accumulators (bnacc.h); every other reduction runs in a fixed
 // order.
+#include <algorithm>
+
 #include "act.h"
 #include "bnacc.h"
 #include "kernels.h"
@@ -966,21 +968,28 @@ hipError_t launch_softmax_ce(const float* z, const StepArgs* args, float* dz, fl
 // layouts
 // ------------------------------------------------------------------------
 
+// One thread per pixel: the C channel values from the C planes (consecutive
+// threads read consecutive pixels of a plane), written as 16-byte vectors of
+// the padded channel row (channels C..Cp-1 zero).  The first n_zero doubles
+// of `zero` (the step's fp64 accumulators) are cleared on the way.
 template <class T>
-__global__ void nchw_to_nhwc_k(const StepArgs* __restrict__ args, T* __restrict__ d, int Nb, int C, int H, int W,
-                               int Cp, double* __restrict__ zero, long n_zero) {
+__global__ __launch_bounds__(256) void nchw_to_nhwc_k(const StepArgs* __restrict__ args, T* __restrict__ d, int Nb,
+                                                      int C, int H, int W, int Cp, double* __restrict__ zero,
+                                                      long n_zero) {
+    constexpr int VW = 16 / (int)sizeof(T);
     const float* __restrict__ s = args->images;
     const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
     for (long z = idx; z < n_zero; z += (long)gridDim.x * blockDim.x) zero[z] = 0.0;
-    const long total = (long)Nb * H * W * Cp;
-    if (idx >= total) return;
-    const int c = (int)(idx % Cp);
-    const long pix = idx / Cp;
-    const int w = (int)(pix % W);
-    const long t = pix / W;
-    const int h = (int)(t % H);
-    const int n = (int)(t / H);
-    st1(d, idx, c < C ? s[(((long)n * C + c) * H + h) * W + w] : 0.f);
+    const long hw = (long)H * W;
+    if (idx >= (long)Nb * hw) return;
+    const long n = idx / hw;
+    const float* __restrict__ sp = s + n * C * hw + (idx - n * hw);
+    for (int c0 = 0; c0 < Cp; c0 += VW) {
+        float vals[VW];
+#pragma unroll
+        for (int u = 0; u < VW; ++u) vals[u] = c0 + u < C ? sp[(long)(c0 + u) * hw] : 0.f;
+        st16(d + idx * Cp + c0, vals);
+    }
 }
 
 template <class T>
@@ -999,7 +1008,8 @@ __global__ void nhwc_to_nchw_k(const T* __restrict__ s, float* __restrict__ d, i
 
 hipError_t launch_nchw_to_nhwc(int dt, const StepArgs* args, void* dst, int Nb, int C, int H, int W, int Cp,
                                double* zero, long n_zero, hipStream_t st) {
-    const dim3 grid(nblocks((long)Nb * H * W * Cp, 256));
+    if (Cp % (dt == DT_BF16 ? 8 : 4) || C > Cp) return hipErrorInvalidValue;
+    const dim3 grid(nblocks((long)Nb * H * W, 256));
     if (dt == DT_BF16)
         launch(nchw_to_nhwc_k<bf16>, grid, dim3(256), 0, st, args, (bf16*)dst, Nb, C, H, W, Cp, zero,
                            n_zero);
@@ -1049,43 +1059,214 @@ hipError_t launch_timestamp(unsigned long long* log, const StepArgs* args, long 
 // snapshot, block update, averaging
 // ------------------------------------------------------------------------
 
+// floor(n / d) for n * d < 2^32: n itself for d == 1, else the high word of
+// n * m with m = ceil(2^32 / d) (snap_magic, once per workgroup).  With
+// n = q d + r the product n m / 2^32 exceeds q + r/d by less than n / 2^32,
+// which keeps it below q + 1 while n d < 2^32.
+__device__ __forceinline__ unsigned snap_magic(unsigned d) { return d <= 1 ? 0u : 0xffffffffu / d + 1u; }
+__device__ __forceinline__ unsigned snap_div(unsigned n, unsigned d, unsigned m) {
+    return d <= 1 ? n : __umulhi(n, m);
+}
+
+constexpr int kSnapThreads = 256;
+
+// One workgroup per table tile.  The entry is found by a binary search over
+// the entries' first workgroups (uniform, once per workgroup).  Copy entries
+// move up to kSnapCopy floats in 16-byte quads (partial quads at the ends
+// element by element).  A conv tile loads kt output channels' rows of ct
+// input channels x R*S taps (contiguous runs of the canonical tensor, 16-byte
+// loads where the runs are aligned, all issued before any LDS store) into LDS
+// rows of odd pitch, then writes the W_f rows (one tap of one output channel:
+// ct input channels) and the W_d rows (one tap of one input channel: kt
+// output channels) as 16-byte vectors.
 template <class T>
-__global__ void snapshot_k(const float* __restrict__ x, float* __restrict__ v, long d,
-                           const SnapConv* __restrict__ convs, int nc, T* __restrict__ wbase) {
-    for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < d; e += (long)gridDim.x * blockDim.x) {
-        const float val = x[e];
-        v[e] = val;
-        // conv segments are sorted by src; find the last with src <= e
-        int lo = 0, hi = nc - 1, f = -1;
-        while (lo <= hi) {
-            const int mid = (lo + hi) >> 1;
-            if (convs[mid].src <= e) { f = mid; lo = mid + 1; } else hi = mid - 1;
+__global__ __launch_bounds__(kSnapThreads) void snapshot_k(const float* __restrict__ x, float* __restrict__ v,
+                                                           const SnapEntry* __restrict__ tab, int n_ent,
+                                                           T* __restrict__ wb) {
+    constexpr int VW = 16 / (int)sizeof(T);
+    __shared__ float sm[kSnapLds + 64];
+    const long b = blockIdx.x;
+    int lo = 0, hi = n_ent - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (tab[mid].tile0 <= b) lo = mid;
+        else hi = mid - 1;
+    }
+    const SnapEntry& E = tab[lo];
+    const int tid = threadIdx.x;
+    const long t = b - E.tile0;
+    if (E.kind == 0) {
+        // chunk t of the quad-aligned run from (src & ~3)
+        const long base = (E.src & ~3L) + t * kSnapCopy;
+        const long e0 = base > E.src ? base : E.src;
+        const long e1 = base + kSnapCopy < E.src + E.n ? base + kSnapCopy : E.src + E.n;
+        constexpr int U = kSnapCopy / 4 / kSnapThreads;
+        f4 buf[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+            const long a = base + 4L * (tid + j * kSnapThreads);
+            if (a >= e0 && a + 4 <= e1) buf[j] = *(const f4*)(x + a);
         }
-        if (f < 0) continue;
-        const SnapConv cv = convs[f];
-        const long o = e - cv.src;
-        if (o >= (long)cv.cout * cv.cin * cv.R * cv.S) continue;   // bias / beyond the weight
-        const int s = (int)(o % cv.S);
-        long t = o / cv.S;
-        const int r = (int)(t % cv.R);
-        t /= cv.R;
-        const int c = (int)(t % cv.cin);
-        const int k = (int)(t / cv.cin);
-        st1(wbase, cv.dst_f + (((long)k * cv.R + r) * cv.S + s) * cv.cin_p + c, val);
-        st1(wbase, cv.dst_d + (((long)c * cv.R + r) * cv.S + s) * cv.cout + k, val);
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+            const long a = base + 4L * (tid + j * kSnapThreads);
+            if (a >= e1 || a + 4 <= e0) continue;
+            if (a >= e0 && a + 4 <= e1) {
+                *(f4*)(v + a) = buf[j];
+            } else {
+                for (long e = a; e < a + 4; ++e)
+                    if (e >= e0 && e < e1) v[e] = x[e];
+            }
+        }
+        return;
+    }
+    const int RS = E.RS, cout = E.cout, cin = E.cin, cin_p = E.cin_p;
+    const int kti = (int)(t % E.nkt), cti = (int)(t / E.nkt);
+    const int k0 = kti * E.kt, c0 = cti * E.ct;
+    const int ktn = min(E.kt, cout - k0);          // output channels of the tile
+    const int ctn = min(E.ct, cin - c0);           // input channels loaded
+    const int ctf = c0 + E.ct >= cin ? cin_p - c0 : E.ct;   // W_f channels written (the last tile pads to cin_p)
+    const int rowlen = ctn * RS;
+    const int pitch = rowlen | 1;
+    const long rstride = (long)cin * RS;
+    const float* __restrict__ src = x + E.src + (long)k0 * rstride + (long)c0 * RS;
+    if (((E.src + (long)k0 * rstride + (long)c0 * RS) & 3) == 0 && (rstride & 3) == 0 && (rowlen & 3) == 0) {
+        const unsigned nq = (unsigned)rowlen >> 2, mq = snap_magic(nq);
+        const unsigned tot = (unsigned)ktn * nq;
+        constexpr int U = kSnapLds / 4 / kSnapThreads;
+        f4 buf[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+            const unsigned i = tid + j * kSnapThreads;
+            if (i < tot) {
+                const unsigned kk = snap_div(i, nq, mq), qq = i - kk * nq;
+                buf[j] = *(const f4*)(src + (long)kk * rstride + 4 * qq);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+            const unsigned i = tid + j * kSnapThreads;
+            if (i < tot) {
+                const unsigned kk = snap_div(i, nq, mq), qq = i - kk * nq;
+                float* d = sm + kk * pitch + 4 * qq;
+                d[0] = buf[j][0];
+                d[1] = buf[j][1];
+                d[2] = buf[j][2];
+                d[3] = buf[j][3];
+            }
+        }
+    } else {
+        const unsigned mr = snap_magic(rowlen);
+        const unsigned tot = (unsigned)ktn * rowlen;
+        for (unsigned i = tid; i < tot; i += kSnapThreads) {
+            const unsigned kk = snap_div(i, rowlen, mr), j = i - kk * rowlen;
+            sm[kk * pitch + j] = src[(long)kk * rstride + j];
+        }
+    }
+    __syncthreads();
+    const unsigned mrs = snap_magic(RS);
+    {   // W_f rows: (output channel kk, tap rs) -> ctf input channels, VW per lane
+        const int nch = ctf / VW;
+        int lg = 0;
+        while ((1 << lg) < nch) ++lg;
+        const int chunk = tid & ((1 << lg) - 1);
+        const int rows = ktn * RS;
+        if (chunk < nch)
+            for (int r = tid >> lg; r < rows; r += kSnapThreads >> lg) {
+                const int kk = (int)snap_div(r, RS, mrs), rs = r - kk * RS;
+                float vals[VW];
+#pragma unroll
+                for (int u = 0; u < VW; ++u) {
+                    const int cc = chunk * VW + u;
+                    vals[u] = cc < ctn ? sm[kk * pitch + cc * RS + rs] : 0.f;
+                }
+                st16(wb + E.dst_f + ((long)(k0 + kk) * RS + rs) * cin_p + c0 + chunk * VW, vals);
+            }
+    }
+    {   // W_d rows: (input channel cc, tap rs) -> ktn output channels, VW per lane
+        const int nch = ktn / VW;
+        int lg = 0;
+        while ((1 << lg) < nch) ++lg;
+        const int chunk = tid & ((1 << lg) - 1);
+        const int rows = ctn * RS;
+        if (chunk < nch)
+            for (int r = tid >> lg; r < rows; r += kSnapThreads >> lg) {
+                const int cc = (int)snap_div(r, RS, mrs), rs = r - cc * RS;
+                float vals[VW];
+#pragma unroll
+                for (int u = 0; u < VW; ++u) vals[u] = sm[(chunk * VW + u) * pitch + cc * RS + rs];
+                st16(wb + E.dst_d + ((long)(c0 + cc) * RS + rs) * cout + k0 + chunk * VW, vals);
+            }
     }
 }
 
-hipError_t launch_snapshot(int dt, const float* x, float* v, long d, const SnapConv* convs_dev, int n_convs,
+long snapshot_table(const SnapConvDesc* convs, int n_convs, long d, int dt, SnapEntry* out, int max_out,
+                    int* n_out, double* bytes) {
+    const int VW = dt == DT_BF16 ? 8 : 4;
+    const double eb = dt == DT_BF16 ? 2.0 : 4.0;
+    int n = 0;
+    long tiles = 0, pos = 0;
+    double by = 0.0;
+    if (n_convs < 0 || d < 0 || max_out < 2 * n_convs + 1) return -1;
+    auto add_copy = [&](long a, long e) {
+        if (e <= a) return;
+        SnapEntry& c = out[n++];
+        c = SnapEntry{};
+        c.kind = 0;
+        c.src = a;
+        c.n = e - a;
+        c.tile0 = tiles;
+        tiles += (e - (a & ~3L) + kSnapCopy - 1) / kSnapCopy;
+        by += 8.0 * (double)(e - a);
+    };
+    auto rup = [](int a, int m) { return (a + m - 1) / m * m; };
+    for (int i = 0; i < n_convs; ++i) {
+        const SnapConvDesc& c = convs[i];
+        const int RS = c.R * c.S;
+        if (c.src < pos || c.cout % VW || c.cin_p % VW || c.cin > c.cin_p || RS < 1 || c.cout < 1 || c.cin < 1 ||
+            c.src + (long)c.cout * c.cin * RS > d)
+            return -1;
+        add_copy(pos, c.src);
+        int kt = RS == 1 ? 64 : 32, ct = RS == 1 ? 128 : 32;
+        kt = std::min(kt, rup(c.cout, VW));
+        ct = std::min(ct, rup(c.cin, VW));
+        while ((long)kt * ct * RS > kSnapLds && ct > VW) ct = std::max(VW, ct / 2 / VW * VW);
+        while ((long)kt * ct * RS > kSnapLds && kt > VW) kt = std::max(VW, kt / 2 / VW * VW);
+        if ((long)kt * ct * RS > kSnapLds) return -1;
+        SnapEntry& e = out[n++];
+        e = SnapEntry{};
+        e.kind = 1;
+        e.src = c.src;
+        e.dst_f = c.dst_f;
+        e.dst_d = c.dst_d;
+        e.tile0 = tiles;
+        e.cout = c.cout;
+        e.cin = c.cin;
+        e.cin_p = c.cin_p;
+        e.RS = RS;
+        e.kt = kt;
+        e.ct = ct;
+        e.nkt = (c.cout + kt - 1) / kt;
+        tiles += (long)e.nkt * ((c.cin + ct - 1) / ct);
+        const long nw = (long)c.cout * c.cin * RS;
+        by += (4.0 + 2.0 * eb) * (double)nw;
+        pos = c.src + nw;
+    }
+    add_copy(pos, d);
+    if (bytes) *bytes = by;
+    *n_out = n;
+    return tiles;
+}
+
+hipError_t launch_snapshot(int dt, const float* x, float* v, const SnapEntry* tab_dev, int n_ent, long n_tiles,
                            void* wbase, hipStream_t st) {
-    long b = (d + 255) / 256;
-    if (b > 16384) b = 16384;
+    if (n_ent <= 0 || n_tiles <= 0) return hipSuccess;
     if (dt == DT_BF16)
-        launch(snapshot_k<bf16>, dim3((unsigned)b), dim3(256), 0, st, x, v, d, convs_dev, n_convs,
-                           (bf16*)wbase);
+        launch(snapshot_k<bf16>, dim3((unsigned)n_tiles), dim3(kSnapThreads), 0, st, x, v, tab_dev, n_ent,
+               (bf16*)wbase);
     else
-        launch(snapshot_k<float>, dim3((unsigned)b), dim3(256), 0, st, x, v, d, convs_dev, n_convs,
-                           (float*)wbase);
+        launch(snapshot_k<float>, dim3((unsigned)n_tiles), dim3(kSnapThreads), 0, st, x, v, tab_dev, n_ent,
+               (float*)wbase);
     return hipGetLastError();
 }
 
@@ -1168,15 +1349,24 @@ hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long h
 }
 
 // v_k = x_k[e]; vbar = (sum_k v_k) / n; x_k[e] = x_k[e] (re-read) + (vbar - v_k).
-// U quads per thread per pass (1 in use), 512-thread workgroups.  The re-read of x_k sits behind a compiler memory fence, so it is a
-// fresh (cached) load that the compiler cannot merge with the snapshot load:
-// block updates that land between the two survive the write (Alg. 1's
-// averager).  The result is stored nontemporally (x_k is streamed once).
+// U quads per thread per pass (1 in use), 512-thread workgroups.  The re-read
+// of x_k is a relaxed agent-scope atomic load per float: it cannot be merged
+// with the first read and does not hit the compute unit's own cache, so a
+// block update that another stream's kernel has written back between the two
+// reads is kept (Alg. 1's averager adds vbar - v_k to x_k in place).  The
+// window is not closed: an update landing after the re-read, or still held in
+// another XCD's cache, is overwritten -- a lost update, which the lock-free
+// updaters of the method permit.  The result is stored nontemporally (x_k is
+// streamed once).
 constexpr int kAvgThreads = 512;
 // one quad per thread over the whole array up to 512M quads (measured on
 // 1 GiB replicas: 5.71 TB/s against 5.53 with a two-pass grid-stride loop
 // over 65536 workgroups)
 constexpr long kAvgMaxBlocks = 1L << 20;
+
+__device__ __forceinline__ float reread(const float* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 template <int NR, int U>
 __global__ __launch_bounds__(kAvgThreads) void average_k(RepPtrs reps, int n_rep, long n) {
@@ -1201,15 +1391,15 @@ __global__ __launch_bounds__(kAvgThreads) void average_k(RepPtrs reps, int n_rep
                 if (k < n_rep) s += v[u][k];
             vbar[u] = s / inv_div;
         }
-        __asm__ volatile("" ::: "memory");   // the loads below are fresh reads of x_k
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const long q = q0 + u * stride;
 #pragma unroll
             for (int k = 0; k < NR; ++k)
                 if (k < n_rep && q < nq) {
-                    f4* p = (f4*)(reps.p[k] + 4 * q);
-                    __builtin_nontemporal_store(*(const f4*)p + (vbar[u] - v[u][k]), p);   // streamed out
+                    float* p = reps.p[k] + 4 * q;
+                    const f4 cur = f4{reread(p), reread(p + 1), reread(p + 2), reread(p + 3)};
+                    __builtin_nontemporal_store(cur + (vbar[u] - v[u][k]), (f4*)p);   // streamed out
                 }
         }
     }
@@ -1223,10 +1413,9 @@ __global__ __launch_bounds__(kAvgThreads) void average_k(RepPtrs reps, int n_rep
         for (int k = 0; k < NR; ++k)
             if (k < n_rep) { vv[k] = reps.p[k][e]; s += vv[k]; }
         const float vbar = s / inv_div;
-        __asm__ volatile("" ::: "memory");
 #pragma unroll
         for (int k = 0; k < NR; ++k)
-            if (k < n_rep) reps.p[k][e] = reps.p[k][e] + (vbar - vv[k]);
+            if (k < n_rep) reps.p[k][e] = reread(reps.p[k] + e) + (vbar - vv[k]);
     }
 }
 

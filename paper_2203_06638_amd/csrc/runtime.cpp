@@ -485,8 +485,10 @@ struct lpp_ctx {
     std::vector<Worker> workers;
     hipStream_t avg_stream = nullptr;
     bool own_avg = false;
-    lpp::SnapConv* snap_dev = nullptr;
+    lpp::SnapEntry* snap_dev = nullptr;   // snapshot work table (entries)
     int n_snap = 0;
+    long snap_tiles = 0;                  // its workgroups
+    double snap_bytes = 0;                // algorithmic bytes of one snapshot
     long wbuf_floats = 0;
     size_t ws_bytes = 0;
     size_t off_v = 0, off_wbuf = 0, off_g = 0, off_m = 0, off_loss = 0, off_img = 0, off_ps = 0, off_wpart = 0,
@@ -1050,11 +1052,10 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
 int enqueue_step(lpp_ctx* c, Worker& w, int worker, int partition, bool traced) {
     const int q = worker / c->P;
     float* xq = c->replicas + (long)q * c->dpad;
-    const long d = c->M.d;
     hipStream_t st = w.stream;
     if (traced) HIPCHK(lpp::launch_timestamp(c->trace_log, w.args, -1, 0, st));
-    LAUNCH("snapshot", 8.0 * d, st,
-           lpp::launch_snapshot(c->M.dt, xq, w.v, d, c->snap_dev, c->n_snap, w.wbuf, st));
+    LAUNCH("snapshot", c->snap_bytes, st,
+           lpp::launch_snapshot(c->M.dt, xq, w.v, c->snap_dev, c->n_snap, c->snap_tiles, w.wbuf, st));
     if (traced) HIPCHK(lpp::launch_timestamp(c->trace_log, w.args, -1, 1, st));
     int rc = run_forward(c, w);
     if (rc) return rc;
@@ -1118,7 +1119,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
     c->dpad = (d + 63) / 64 * 64;
 
     // conv weight layouts and the snapshot table
-    std::vector<lpp::SnapConv> snaps;
+    std::vector<lpp::SnapConvDesc> snaps;
     long wf = 0;
     for (auto& Y : M.layers) {
         if (Y.L.op != LPP_CONV || Y.pw) continue;
@@ -1128,14 +1129,19 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         wf += (nf + 63) / 64 * 64;
         Y.wd_off = wf;
         wf += (nd + 63) / 64 * 64;
-        snaps.push_back({Y.poff, Y.np, Y.L.cout, Y.L.cin, Y.cin_p, Y.L.k, Y.L.k, Y.wf_off, Y.wd_off});
+        snaps.push_back({Y.poff, Y.L.cout, Y.L.cin, Y.cin_p, Y.L.k, Y.L.k, Y.wf_off, Y.wd_off});
         Y.wg = M.dt == lpp::DT_BF16 ? lpp::wgrad_plan_bf16(N, Y.out.h, Y.out.w, Y.cin_p, Y.L.cout, Y.L.k, Y.L.k)
                                      : lpp::wgrad_plan(N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout,
                                                        Y.L.k, Y.L.k, Y.L.stride, Y.L.pad);
     }
     if (!(opt && opt->unfused)) plan_folds(M, N);
     c->wbuf_floats = wf;
-    c->n_snap = (int)snaps.size();
+    std::vector<lpp::SnapEntry> snap_tab(2 * snaps.size() + 1);
+    c->snap_tiles = lpp::snapshot_table(snaps.data(), (int)snaps.size(), d, M.dt, snap_tab.data(),
+                                        (int)snap_tab.size(), &c->n_snap, &c->snap_bytes);
+    if (c->snap_tiles < 0)
+        return fail(LPP_EUNSUPPORTED, "conv output channels must be multiples of 4 (8 for bf16) for the snapshot");
+    snap_tab.resize(c->n_snap);
 
     // workspace layout (bytes)
     size_t off = 0;
@@ -1198,10 +1204,11 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
     if (hipMalloc((void**)&c->replicas, sizeof(float) * c->dpad * K) != hipSuccess)
         return fail(LPP_ENOMEM, "replica allocation failed");
     HIPCHK(hipMemset(c->replicas, 0, sizeof(float) * c->dpad * K));
-    if (!snaps.empty()) {
-        if (hipMalloc((void**)&c->snap_dev, sizeof(lpp::SnapConv) * snaps.size()) != hipSuccess)
+    if (!snap_tab.empty()) {
+        if (hipMalloc((void**)&c->snap_dev, sizeof(lpp::SnapEntry) * snap_tab.size()) != hipSuccess)
             return fail(LPP_ENOMEM, "snapshot table allocation failed");
-        HIPCHK(hipMemcpy(c->snap_dev, snaps.data(), sizeof(lpp::SnapConv) * snaps.size(), hipMemcpyHostToDevice));
+        HIPCHK(hipMemcpy(c->snap_dev, snap_tab.data(), sizeof(lpp::SnapEntry) * snap_tab.size(),
+                         hipMemcpyHostToDevice));
     }
     c->counters.reset(new std::atomic<long>[K]);
     for (int q = 0; q < K; ++q) c->counters[q].store(0);
@@ -1633,6 +1640,93 @@ int lpp_kernel_sgd_update(float* x, float* m, const float* g, long n, float lr, 
     if (((uintptr_t)x | (uintptr_t)g | (uintptr_t)m) & 15) return fail(LPP_EINVAL, "buffers must be 16-byte aligned");
     hipError_t e = lpp::launch_sgd_update(x, m, g, 0, n, nullptr, lr, mu, wd, (hipStream_t)stream);
     if (e != hipSuccess) return fail(LPP_EHIP, std::string("sgd_update: ") + hipGetErrorString(e));
+    return LPP_OK;
+}
+
+}  // extern "C"
+
+struct lpp_snap_plan {
+    lpp::SnapEntry* tab = nullptr;   // device
+    int n_ent = 0;
+    long tiles = 0;
+    int dt = 0;
+    long d = 0;
+};
+
+namespace {
+// Validates a stand-alone snapshot's conv list (see lpp_snapshot_plan_create)
+// into out[0 .. n); returns an error message or nullptr.
+const char* snap_convs(const lpp_snap_conv* convs, int n, long d, int dtype, long wbuf_elems,
+                       lpp::SnapConvDesc* out) {
+    if (dtype != LPP_FP32 && dtype != LPP_BF16) return "unknown dtype";
+    if (n < 0 || d < 0 || wbuf_elems < 0 || (n > 0 && !convs)) return "bad arguments";
+    const int vw = dtype == LPP_BF16 ? 8 : 4;
+    long pos = 0;
+    for (int i = 0; i < n; ++i) {
+        const lpp_snap_conv& c = convs[i];
+        if (c.cout < 1 || c.cin < 1 || c.kh < 1 || c.kw < 1 || c.cin_p < c.cin) return "bad conv shape";
+        if (c.cout % vw || c.cin_p % vw) return "cout and cin_p must be multiples of 4 (8 for bf16)";
+        const long nw = (long)c.cout * c.cin * c.kh * c.kw;
+        if (c.src < pos || c.src + nw > d) return "conv weights must be sorted, disjoint and inside [0, d)";
+        pos = c.src + nw;
+        const long nf = (long)c.cout * c.kh * c.kw * c.cin_p, nd = (long)c.cin * c.kh * c.kw * c.cout;
+        if (c.dst_f < 0 || c.dst_d < 0 || c.dst_f % vw || c.dst_d % vw || c.dst_f + nf > wbuf_elems ||
+            c.dst_d + nd > wbuf_elems)
+            return "conv layouts must be aligned and inside wbuf";
+        out[i] = lpp::SnapConvDesc{c.src, c.cout, c.cin, c.cin_p, c.kh, c.kw, c.dst_f, c.dst_d};
+    }
+    return nullptr;
+}
+}  // namespace
+
+extern "C" {
+
+int lpp_snapshot_plan_create(const lpp_snap_conv* convs, int n_convs, long d, int dtype, long wbuf_elems,
+                             lpp_snap_plan** out) {
+    if (!out) return fail(LPP_EINVAL, "null output pointer");
+    *out = nullptr;
+    if (n_convs < 0 || n_convs > (1 << 20)) return fail(LPP_EINVAL, "bad conv count");
+    std::vector<lpp::SnapConvDesc> cv((size_t)n_convs);
+    if (const char* e = snap_convs(convs, n_convs, d, dtype, wbuf_elems, cv.data())) return fail(LPP_EINVAL, e);
+    std::vector<lpp::SnapEntry> tab(2 * (size_t)n_convs + 1);
+    int n_ent = 0;
+    double bytes = 0;
+    const long tiles = lpp::snapshot_table(cv.data(), n_convs, d, dtype, tab.data(), (int)tab.size(), &n_ent, &bytes);
+    if (tiles < 0) return fail(LPP_EINVAL, "invalid conv list");
+    std::unique_ptr<lpp_snap_plan> p(new lpp_snap_plan);
+    p->n_ent = n_ent;
+    p->tiles = tiles;
+    p->dt = dtype;
+    p->d = d;
+    if (n_ent > 0) {
+        if (hipMalloc((void**)&p->tab, sizeof(lpp::SnapEntry) * n_ent) != hipSuccess)
+            return fail(LPP_ENOMEM, "snapshot table allocation failed");
+        hipError_t e = hipMemcpy(p->tab, tab.data(), sizeof(lpp::SnapEntry) * n_ent, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            (void)hipFree(p->tab);
+            return fail(LPP_EHIP, std::string("snapshot table copy: ") + hipGetErrorString(e));
+        }
+    }
+    *out = p.release();
+    return LPP_OK;
+}
+
+int lpp_kernel_snapshot(const lpp_snap_plan* plan, const float* x, float* v, void* wbuf, void* stream) {
+    if (!plan) return fail(LPP_EINVAL, "null plan");
+    if (plan->tiles > 0 && (!x || !v || !wbuf)) return fail(LPP_EINVAL, "null buffer");
+    if (((uintptr_t)x | (uintptr_t)v | (uintptr_t)wbuf) & 15) return fail(LPP_EINVAL, "buffers must be 16-byte aligned");
+    hipError_t e = lpp::launch_snapshot(plan->dt, x, v, plan->tab, plan->n_ent, plan->tiles, wbuf, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(LPP_EHIP, std::string("snapshot: ") + hipGetErrorString(e));
+    return LPP_OK;
+}
+
+int lpp_snapshot_plan_destroy(lpp_snap_plan* plan) {
+    if (!plan) return LPP_OK;
+    if (plan->tab && hipFree(plan->tab) != hipSuccess) {
+        delete plan;
+        return fail(LPP_EHIP, "snapshot table free failed");
+    }
+    delete plan;
     return LPP_OK;
 }
 

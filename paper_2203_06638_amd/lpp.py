@@ -59,6 +59,11 @@ class TraceAvg(C.Structure):
     _fields_ = [("index", C.c_long), ("n_replicas", C.c_int), ("counter_min", C.c_long), ("t", C.c_ulonglong * 2)]
 
 
+class SnapConv(C.Structure):
+    _fields_ = [("src", C.c_long), ("cout", C.c_int), ("cin", C.c_int), ("cin_p", C.c_int), ("kh", C.c_int),
+                ("kw", C.c_int), ("dst_f", C.c_long), ("dst_d", C.c_long)]
+
+
 class ModelInfo(C.Structure):
     _fields_ = [("d", C.c_long), ("P", C.c_int), ("block_lo", C.c_long * 65), ("block_hi", C.c_long * 65),
                 ("fwd_flops", C.c_double), ("bwd_flops", C.c_double * 65)]
@@ -101,6 +106,10 @@ def lib():
             "lpp_kernel_sgd_update": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_long, C.c_float, C.c_float,
                                        C.c_float, C.c_void_p], C.c_int),
             "lpp_kernel_average": ([C.POINTER(C.c_void_p), C.c_int, C.c_long, C.c_void_p], C.c_int),
+            "lpp_snapshot_plan_create": ([C.POINTER(SnapConv), C.c_int, C.c_long, C.c_int, C.c_long,
+                                          C.POINTER(C.c_void_p)], C.c_int),
+            "lpp_kernel_snapshot": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+            "lpp_snapshot_plan_destroy": ([C.c_void_p], C.c_int),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -282,3 +291,35 @@ def kernel_average(reps, stream=None):
     """In-place averaging round over a list of equally sized device tensors."""
     arr = (C.c_void_p * len(reps))(*[r.data_ptr() for r in reps])
     _check(lib().lpp_kernel_average(arr, len(reps), reps[0].numel(), _stream_handle(stream)))
+
+
+def _snap_convs(convs):
+    """host array of lpp_snap_conv from (src, cout, cin, cin_p, kh, kw, dst_f, dst_d) tuples"""
+    return (SnapConv * max(1, len(convs)))(*[SnapConv(*c) for c in convs])
+
+
+class SnapshotPlan:
+    """lpp_snapshot_plan_create / lpp_kernel_snapshot / lpp_snapshot_plan_destroy.
+    convs: (src, cout, cin, cin_p, kh, kw, dst_f, dst_d) tuples sorted by src."""
+
+    def __init__(self, convs, d, dtype, wbuf_elems):
+        arr = _snap_convs(convs)
+        self._p = C.c_void_p()
+        _check(lib().lpp_snapshot_plan_create(arr, len(convs), d, dtype, wbuf_elems, C.byref(self._p)))
+
+    def run(self, x, v, wbuf, stream=None):
+        """x, v: device float32 tensors of d floats; wbuf: device tensor of
+        wbuf_elems float32 (FP32) or 16-bit (BF16) elements."""
+        _check(lib().lpp_kernel_snapshot(self._p, x.data_ptr(), v.data_ptr(), wbuf.data_ptr(),
+                                         _stream_handle(stream)))
+
+    def close(self):
+        if self._p:
+            _check(lib().lpp_snapshot_plan_destroy(self._p))
+            self._p = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -649,7 +649,7 @@ def test_folded_bn_relu_resnet20_all_partitions():
 # the headline workload's full size (batch 128, momentum 0.9)
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("partition", [1, 4])
+@pytest.mark.parametrize("partition", [1, 3, 4])
 def test_full_size_relu_free_resnet20_gradients(partition):
     o, p = OM.resnet20_p4(relu=False), PM.resnet20(act=False)
     x = T.init_x(o.specs, 81)

@@ -145,5 +145,12 @@ def test_trace_async_delay_statistics():
         assert all(s["t"][0] <= s["t"][1] <= s["t"][2] <= s["t"][3] for s in steps)
         assert all(r["t"][0] <= r["t"][1] for r in rounds)
         ann, summ = D.analyze(steps, rounds)
-        say("async trace H=%d" % H, summ)
+        # Alg. 1: the averager runs concurrently with the updaters.  Rounds
+        # whose kernel interval overlaps an updater iteration (snapshot start
+        # to update end) of some worker, and overlaps a block update itself.
+        ov_iter = sum(1 for r in rounds if any(s["t"][0] < r["t"][1] and r["t"][0] < s["t"][3] for s in steps))
+        ov_upd = sum(1 for r in rounds if any(s["t"][2] < r["t"][1] and r["t"][0] < s["t"][3] for s in steps))
+        say("async trace H=%d" % H, summ, "rounds overlapping an iteration %d, an update %d of %d"
+            % (ov_iter, ov_upd, len(rounds)))
         assert 0.0 <= summ["p_good"] <= 1.0 and summ["staleness_max"] >= 0
+        assert ov_iter >= 1, "no averaging round ran concurrently with an updater"
