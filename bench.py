@@ -474,26 +474,51 @@ def delay_statistics(torch, Hs=(1, 2, 4, 8, 16), T=256, B=128):
     return out
 
 
-def cpu_baseline(steps, batch):
-    """The oracle (fp64 C, OpenMP) on `steps` ResNet-20 worker steps at the
-    same batch, partitions cycling over the four blocks."""
+def _oracle_rate(o, shape, ncls, batch, steps, bf16, seed):
+    """Samples/s of the oracle's updater iteration (snapshot, forward, full
+    backward restricted to the block, update) over `steps` steps, partitions
+    cycling over the blocks."""
     import synth
     from oracle import lppref as R
-    from oracle import models as OM
-    o = OM.resnet20_p4()
-    x = synth.init_params(o.specs, 1).astype(np.float64)
+    x = synth.init_params(o.specs, seed).astype(np.float64)
     m = np.zeros(o.d)
-    img = synth.images(7, batch, 3, 32, 32)
-    lab = synth.labels(7, batch, 10)
-    R.step(o, x, m, img[:2], lab[:2], 4, 0.0, 0.9)   # load and warm the library
+    img = synth.images(seed + 6, batch, *shape)
+    if bf16:
+        img = synth.round_to_bf16(img)
+    lab = synth.labels(seed + 6, batch, ncls)
+    R.step(o, x, m, img[:1], lab[:1], o.P, 0.0, 0.9)   # load and warm the library
     t0 = time.perf_counter()
     for s in range(steps):
-        R.step(o, x, m, img, lab, s % 4 + 1, 0.1, 0.9)
+        R.step(o, x, m, img, lab, s % o.P + 1, 0.1, 0.9)
     dt = time.perf_counter() - t0
+    return batch * steps / dt, dt
+
+
+def cpu_baseline(steps, batch):
+    """The oracle (fp64 C, OpenMP), compiled for this host (-O3
+    -march=native), timed on bounded samples: `steps` ResNet-20 worker steps
+    at the headline's batch, and 2 steps each of WRN-16-8 (batch 4) and
+    ResNet-18 at 224x224 (batch 2) -- the oracle's time is linear in the
+    batch, so samples/s of a small batch stands for the workload's."""
+    import tempfile
+    from oracle import build as OB
+    from oracle import lppref as R
+    from oracle import models as OM
+    R.use_library(OB.build_native(tempfile.mkdtemp(prefix="lppref_native_")))
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": round(batch * steps / dt, 2), "unit": "samples/s", "cores": threads, "kind": "oracle",
+    build = "gcc -O3 -march=native -fopenmp"
+    v, dt = _oracle_rate(OM.resnet20_p4(), (3, 32, 32), 10, batch, steps, False, 1)
+    head = {"value": round(v, 2), "unit": "samples/s", "cores": threads, "kind": "oracle", "build": build,
             "sample": "%d ResNet-20 worker steps (fwd + full bwd restricted to the block + update), batch %d, "
                       "fp64, %.1f s" % (steps, batch, dt)}
+    others = {}
+    for name, o, shape, ncls, b in (("wrn16_8_bf16", OM.wrn16_8_p4(), (3, 32, 32), 100, 4),
+                                    ("resnet18_bf16", OM.resnet18_p4(), (3, 224, 224), 1000, 2)):
+        v, dt = _oracle_rate(o, shape, ncls, b, 2, True, 2)
+        others[name] = {"value": round(v, 3), "unit": "samples/s", "cores": threads, "kind": "oracle",
+                        "build": build, "sample": "2 worker steps at batch %d (fp64 on the bf16-rounded images), "
+                                                  "%.1f s" % (b, dt)}
+    return head, others
 
 
 def main():
@@ -677,7 +702,10 @@ def main():
             print("workload %s: %s samples/s" % (name, res["workloads"][name].get("value")), file=sys.stderr,
                   flush=True)
     if not a.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(a.cpu_steps, B)
+        res["cpu_baseline"], others = cpu_baseline(a.cpu_steps, B)
+        for name, cb in others.items():
+            if name in res.get("workloads", {}):
+                res["workloads"][name]["cpu_baseline"] = cb
     print(json.dumps(res), flush=True)
 
 

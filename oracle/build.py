@@ -23,5 +23,17 @@ def build(force: bool = True) -> str:
     return LIB
 
 
+def build_native(out_dir: str) -> str:
+    """A copy of the oracle compiled for the host it runs on (-O3
+    -march=native), for timing it as the CPU baseline; the tests use the
+    portable build above."""
+    os.makedirs(out_dir, exist_ok=True)
+    out = os.path.join(out_dir, "liblppref_native.so")
+    cmd = ["gcc", "-O3", "-march=native", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall", "-Wno-unknown-pragmas",
+           "-o", out, SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    return out
+
+
 if __name__ == "__main__":
     print(build(force="--if-stale" not in sys.argv))

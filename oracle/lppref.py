@@ -33,6 +33,12 @@ class RefLayer(C.Structure):
                 ("k", C.c_int), ("stride", C.c_int), ("pad", C.c_int), ("bias", C.c_int), ("poff", C.c_long)]
 
 
+def use_library(path):
+    """Load the oracle from another build of lppref.c (e.g. build_native)."""
+    global _LIB
+    _LIB = _load(path)
+
+
 def lib():
     global _LIB
     if _LIB is None:
@@ -40,28 +46,32 @@ def lib():
         if not os.path.exists(path):
             from . import build as _b
             _b.build()
-        L = C.CDLL(path)
-        dp = C.POINTER(C.c_double)
-        L.ref_forward_backward.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
-                                           dp, dp, C.POINTER(C.c_int), C.c_double, dp, dp, dp]
-        L.ref_num_params.argtypes = [C.POINTER(RefLayer), C.c_int]
-        L.ref_num_params.restype = C.c_long
-        L.ref_shapes.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.POINTER(C.c_int)]
-        L.ref_block_update.argtypes = [dp, dp, dp, C.c_long, C.c_long, C.c_double, C.c_double, C.c_double]
-        L.ref_average.argtypes = [C.POINTER(dp), C.c_int, C.c_long]
-        L.ref_step.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
-                               dp, dp, dp, C.POINTER(C.c_int), C.c_long, C.c_long, C.c_double, C.c_double,
-                               C.c_double, C.c_double, dp, dp, dp]
-        L.ref_activation_grad.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
-                                          dp, dp, C.POINTER(C.c_int), C.c_double, C.c_int, dp]
-        L.ref_grad_scale.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
-                                     dp, dp, C.POINTER(C.c_int), C.c_double, dp, dp]
-        L.ref_kink_margin.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
-                                      dp, dp, C.c_double, dp]
-        L.ref_activation.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
-                                     dp, dp, C.c_double, C.c_int, dp]
-        _LIB = L
+        _LIB = _load(path)
     return _LIB
+
+
+def _load(path):
+    L = C.CDLL(path)
+    dp = C.POINTER(C.c_double)
+    L.ref_forward_backward.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                       dp, dp, C.POINTER(C.c_int), C.c_double, dp, dp, dp]
+    L.ref_num_params.argtypes = [C.POINTER(RefLayer), C.c_int]
+    L.ref_num_params.restype = C.c_long
+    L.ref_shapes.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.POINTER(C.c_int)]
+    L.ref_block_update.argtypes = [dp, dp, dp, C.c_long, C.c_long, C.c_double, C.c_double, C.c_double]
+    L.ref_average.argtypes = [C.POINTER(dp), C.c_int, C.c_long]
+    L.ref_step.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                           dp, dp, dp, C.POINTER(C.c_int), C.c_long, C.c_long, C.c_double, C.c_double,
+                           C.c_double, C.c_double, dp, dp, dp]
+    L.ref_activation_grad.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                      dp, dp, C.POINTER(C.c_int), C.c_double, C.c_int, dp]
+    L.ref_grad_scale.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                 dp, dp, C.POINTER(C.c_int), C.c_double, dp, dp]
+    L.ref_kink_margin.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                  dp, dp, C.c_double, dp]
+    L.ref_activation.argtypes = [C.POINTER(RefLayer), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                 dp, dp, C.c_double, C.c_int, dp]
+    return L
 
 
 def _dp(a):

@@ -112,6 +112,7 @@ struct Model {
     std::vector<std::vector<int>> consumers;
     std::vector<Group> groups;    // in execution order
     std::vector<char> stored;     // layer output materialised
+    std::vector<char> gstored;    // gradient at the layer output materialised (when the backward reaches it)
     std::vector<int> stats_from;  // BN: conv whose epilogue computes its statistics, or -1
 };
 
@@ -405,9 +406,13 @@ void build_groups(Model& M, bool fused) {
     // a group runs when its last layer's inputs exist: order by output layer
     std::stable_sort(gs.begin(), gs.end(), [](const Group& x, const Group& y) { return x.out < y.out; });
     M.groups = gs;
+    M.gstored.assign(M.layers.size(), 0);
     for (auto& g : M.groups) {
         M.stored[g.out] = 1;
-        if (g.kind == G_HEAD) M.stored[g.a] = 1;   // the pooled features, kept for the weight gradient
+        M.gstored[g.out] = 1;
+        // the pooled features, kept for the weight gradient; their gradient
+        // goes straight to the pool's input
+        if (g.kind == G_HEAD) M.stored[g.a] = 1;
     }
 }
 
@@ -1466,6 +1471,7 @@ static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* 
             if (g.kind == G_BNACT && (layer == g.a || layer == g.add || layer == g.bn2)) G = &g;
         if (grad || !G) return fail(LPP_ESTATE, "this layer's output is fused away (create the context with unfused = 1)");
     }
+    if (grad && !M.gstored[layer]) return fail(LPP_ESTATE, "this layer's gradient is fused away");
     if (grad && (w.last_partition < 0 || !M.plans[w.last_partition].run[layer]))
         return fail(LPP_ESTATE, "the last step's backward pass did not reach this layer");
     rc = sync_all(c);
