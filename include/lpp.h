@@ -323,6 +323,22 @@ int lpp_snapshot_plan_create(const lpp_snap_conv* convs, int n_convs, long d, in
 int lpp_kernel_snapshot(const lpp_snap_plan* plan, const float* x, float* v, void* wbuf, void* stream);
 int lpp_snapshot_plan_destroy(lpp_snap_plan* plan);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * snapshot as lpp_kernel_snapshot, same arguments and results, without a
+ * plan.  Its work table goes into a fixed array in the library's device
+ * memory (one per GPU, 257 entries of 72 bytes, held until the process
+ * ends), so it calls no allocating routine.  At most 128 convs per call
+ * (LPP_EINVAL beyond, and for any list lpp_snapshot_plan_create rejects).
+ * The call copies the table (hipMemcpyAsync on `stream`), launches the
+ * snapshot and waits for the stream before it returns.  Every call on one
+ * GPU shares that GPU's table: calls that overlap on one GPU (from several
+ * host threads) race and must not be made.
+ */
+int lpp_kernel_snapshot_noalloc(const lpp_snap_conv* convs, int n_convs, long d, int dtype, long wbuf_elems,
+                                const float* x, float* v, void* wbuf, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -319,6 +319,14 @@ long snapshot_table(const SnapConvDesc* convs, int n_convs, long d, int dt, Snap
                     int* n_out, double* bytes);
 hipError_t launch_snapshot(int dt, const float* x, float* v, const SnapEntry* tab_dev, int n_ent, long n_tiles,
                            void* wbase, hipStream_t st);
+// The same snapshot with its work table in a fixed device array of
+// kSnapScratchEntries entries (no allocation; lists of up to
+// kSnapNoallocConvs convs).  Waits for the stream before returning.
+// *bad_list = 1 (and nothing launched) for a list the table cannot take.
+constexpr int kSnapNoallocConvs = 128;
+constexpr int kSnapScratchEntries = 2 * kSnapNoallocConvs + 1;
+hipError_t snapshot_noalloc(int dt, const SnapConvDesc* convs, int n_convs, long d, const float* x, float* v,
+                            void* wbase, hipStream_t st, int* bad_list);
 
 // Block update (Alg. 1 updater's last step), e in [lo, hi):
 //   m = mu*m + g + wd*x; x -= lr*m   (m == null: x -= lr*(g + wd*x))

@@ -11,6 +11,7 @@
 // per-channel accumulators (bnacc.h); every other reduction runs in a fixed
 // order.
 #include <algorithm>
+#include <mutex>
 
 #include "act.h"
 #include "bnacc.h"
@@ -1256,6 +1257,63 @@ long snapshot_table(const SnapConvDesc* convs, int n_convs, long d, int dt, Snap
     if (bytes) *bytes = by;
     *n_out = n;
     return tiles;
+}
+
+// The snapshot's work table for callers that cannot allocate device memory:
+// a file-scope array on every device the library runs on (held until the
+// process ends).  Host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device (snap_scratch_ptr);
+// the array's name itself is a host-side stand-in.
+static __device__ __align__(256) SnapEntry scratch[kSnapScratchEntries];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+SnapEntry* g_scratch_ptr[kMaxDevices] = {};
+
+// scratch's address on the current device, looked up once per device
+hipError_t snap_scratch_ptr(SnapEntry** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = (SnapEntry*)p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+}  // namespace
+
+hipError_t snapshot_noalloc(int dt, const SnapConvDesc* convs, int n_convs, long d, const float* x, float* v,
+                            void* wbase, hipStream_t st, int* bad_list) {
+    *bad_list = 0;
+    SnapEntry tab[kSnapScratchEntries];
+    int n_ent = 0;
+    if (n_convs > kSnapNoallocConvs) {
+        *bad_list = 1;
+        return hipSuccess;
+    }
+    const long tiles = snapshot_table(convs, n_convs, d, dt, tab, kSnapScratchEntries, &n_ent, nullptr);
+    if (tiles < 0) {
+        *bad_list = 1;
+        return hipSuccess;
+    }
+    if (n_ent == 0 || tiles == 0) return hipSuccess;
+    SnapEntry* dev_tab = nullptr;
+    hipError_t e = snap_scratch_ptr(&dev_tab);
+    if (e != hipSuccess) return e;
+    e = hipMemcpyAsync(dev_tab, tab, sizeof(SnapEntry) * n_ent, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return e;
+    e = launch_snapshot(dt, x, v, dev_tab, n_ent, tiles, wbase, st);
+    if (e != hipSuccess) return e;
+    // the host table above lives on this stack frame: return only once the
+    // copy (and the kernel after it) has run
+    return hipStreamSynchronize(st);
 }
 
 hipError_t launch_snapshot(int dt, const float* x, float* v, const SnapEntry* tab_dev, int n_ent, long n_tiles,

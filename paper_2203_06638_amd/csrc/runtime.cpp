@@ -1726,6 +1726,21 @@ int lpp_kernel_snapshot(const lpp_snap_plan* plan, const float* x, float* v, voi
     return LPP_OK;
 }
 
+int lpp_kernel_snapshot_noalloc(const lpp_snap_conv* convs, int n_convs, long d, int dtype, long wbuf_elems,
+                                const float* x, float* v, void* wbuf, void* stream) {
+    if (n_convs < 0 || n_convs > lpp::kSnapNoallocConvs)
+        return fail(LPP_EINVAL, "lpp_kernel_snapshot_noalloc takes at most 128 convs");
+    lpp::SnapConvDesc cv[lpp::kSnapNoallocConvs];
+    if (const char* e = snap_convs(convs, n_convs, d, dtype, wbuf_elems, cv)) return fail(LPP_EINVAL, e);
+    if (d > 0 && (!x || !v || !wbuf)) return fail(LPP_EINVAL, "null buffer");
+    if (((uintptr_t)x | (uintptr_t)v | (uintptr_t)wbuf) & 15) return fail(LPP_EINVAL, "buffers must be 16-byte aligned");
+    int bad = 0;
+    hipError_t e = lpp::snapshot_noalloc(dtype, cv, n_convs, d, x, v, wbuf, (hipStream_t)stream, &bad);
+    if (bad) return fail(LPP_EINVAL, "invalid conv list");
+    if (e != hipSuccess) return fail(LPP_EHIP, std::string("snapshot: ") + hipGetErrorString(e));
+    return LPP_OK;
+}
+
 int lpp_snapshot_plan_destroy(lpp_snap_plan* plan) {
     if (!plan) return LPP_OK;
     if (plan->tab && hipFree(plan->tab) != hipSuccess) {

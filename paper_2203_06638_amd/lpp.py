@@ -110,6 +110,8 @@ def lib():
                                           C.POINTER(C.c_void_p)], C.c_int),
             "lpp_kernel_snapshot": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
             "lpp_snapshot_plan_destroy": ([C.c_void_p], C.c_int),
+            "lpp_kernel_snapshot_noalloc": ([C.POINTER(SnapConv), C.c_int, C.c_long, C.c_int, C.c_long, C.c_void_p,
+                                             C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -323,3 +325,10 @@ class SnapshotPlan:
             self.close()
         except Exception:
             pass
+
+
+def kernel_snapshot_noalloc(convs, d, dtype, wbuf_elems, x, v, wbuf, stream=None):
+    """lpp_kernel_snapshot_noalloc on device tensors (see SnapshotPlan.run)."""
+    arr = _snap_convs(convs)
+    _check(lib().lpp_kernel_snapshot_noalloc(arr, len(convs), d, dtype, wbuf_elems, x.data_ptr(), v.data_ptr(),
+                                             wbuf.data_ptr(), _stream_handle(stream)))
