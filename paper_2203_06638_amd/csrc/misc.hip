@@ -1408,7 +1408,7 @@ hipError_t launch_sgd_update(float* x, float* m, const float* g, long lo, long h
 
 // v_k = x_k[e]; vbar = (sum_k v_k) / n; x_k[e] = x_k[e] (re-read) + (vbar - v_k).
 // U quads per thread per pass (1 in use), 512-thread workgroups.  The re-read
-// of x_k is a relaxed agent-scope atomic load per float: it cannot be merged
+// of x_k is a device-scope (sc1) 16-byte buffer load: it cannot be merged
 // with the first read and does not hit the compute unit's own cache, so a
 // block update that another stream's kernel has written back between the two
 // reads is kept (Alg. 1's averager adds vbar - v_k to x_k in place).  The
@@ -1424,6 +1424,12 @@ constexpr long kAvgMaxBlocks = 1L << 20;
 
 __device__ __forceinline__ float reread(const float* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// 16 bytes at base + byte_off (base uniform across the wave) with cache
+// policy sc1: a device-scope load that bypasses the compute unit's cache
+__device__ __forceinline__ f4 reread4(const float* base, unsigned byte_off) {
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, 0x7fffffff, 0x00020000);
+    return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 16));
 }
 
 template <int NR, int U>
@@ -1455,9 +1461,9 @@ __global__ __launch_bounds__(kAvgThreads) void average_k(RepPtrs reps, int n_rep
 #pragma unroll
             for (int k = 0; k < NR; ++k)
                 if (k < n_rep && q < nq) {
-                    float* p = reps.p[k] + 4 * q;
-                    const f4 cur = f4{reread(p), reread(p + 1), reread(p + 2), reread(p + 3)};
-                    __builtin_nontemporal_store(cur + (vbar[u] - v[u][k]), (f4*)p);   // streamed out
+                    const long qb = q - threadIdx.x;        // the workgroup's first quad (uniform)
+                    const f4 cur = reread4(reps.p[k] + 4 * qb, 16u * threadIdx.x);
+                    __builtin_nontemporal_store(cur + (vbar[u] - v[u][k]), (f4*)(reps.p[k] + 4 * q));   // streamed out
                 }
         }
     }
