@@ -73,10 +73,14 @@ struct BfPass {
 // otherwise a step's four 8-channel chunks are decoded one by one (Cs = 8 or
 // 16 spans several taps per step).  KH load steps (1 or 2) form one K-step:
 // one LDS buffer, one barrier.
+// res (forward only): a residual tensor of the output's shape added to the
+// rounded output and rounded again, as a separate residual add of the two
+// stored tensors would; the statistics then describe that sum.
 template <int BM, int BN, bool STATS, bool FASTK, int KH>
 __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src, const bf16* __restrict__ B,
-                                                   const float* __restrict__ bias, bf16* __restrict__ Y, ConvGeom g,
-                                                   BfPass ps, int accumulate, BnSums sums) {
+                                                   const float* __restrict__ bias, bf16* __restrict__ Y,
+                                                   const bf16* __restrict__ res, ConvGeom g, BfPass ps, int accumulate,
+                                                   BnSums sums) {
     constexpr int TM = BM / 32, TN = BN / 32;     // 16x16 blocks per wave; waves 2 x 2
     constexpr int AL = BM / 64, BL = BN / 64;     // 16-byte operand loads per thread per K-step
     constexpr int P = kBfPitch;
@@ -210,12 +214,10 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
     // statistics describe), transpose through LDS, 16-byte channel stores
     const int nvalid = (int)min((long)BM, Mv - m0);
     bf16* Ot = lds;
-    float colsum[TN];
 #pragma unroll
     for (int y = 0; y < TN; ++y) {
         const int col = (wn * TN + y) * 16 + (lane & 15);
         const float bb = (bias && n0 + col < g.Ncols) ? bias[n0 + col] : 0.f;
-        colsum[y] = 0.f;
 #pragma unroll
         for (int x = 0; x < TM; ++x)
 #pragma unroll
@@ -223,7 +225,6 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
                 const int row = (wm * TM + x) * 16 + (lane >> 4) * 4 + i;
                 const bf16 h = to_bf16(acc[x][y][i] + bb);
                 acc[x][y][i] = from_bf16(h);
-                if (STATS && row < nvalid) colsum[y] += acc[x][y][i];
                 Ot[row * OP + col] = h;
             }
     }
@@ -236,8 +237,25 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
         const int ow = (int)(m % ps.Wv);
         const long t = m / ps.Wv;
         const int oh = (int)(t % ps.Hv), img = (int)(t / ps.Hv);
-        bf16* dp = Y + ((long)(img * ps.Hd + oh * ps.os + ps.oa) * ps.Wd + ow * ps.os + ps.ob) * g.Ncols + n0 + ch;
+        const long di = ((long)(img * ps.Hd + oh * ps.os + ps.oa) * ps.Wd + ow * ps.os + ps.ob) * g.Ncols + n0 + ch;
+        bf16* dp = Y + di;
         uint4 v = *(const uint4*)(Ot + row * OP + ch);
+        if (res) {
+            // the residual add on the rounded values; the sum goes back into
+            // the tile for the statistics
+            const uint4 o = *(const uint4*)(res + di);
+            const uint32_t* pv = (const uint32_t*)&v;
+            const uint32_t* po = (const uint32_t*)&o;
+            uint32_t w[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float lo = __uint_as_float(pv[q] << 16) + __uint_as_float(po[q] << 16);
+                const float hi = __uint_as_float(pv[q] & 0xffff0000u) + __uint_as_float(po[q] & 0xffff0000u);
+                w[q] = pack_bf16x2(lo, hi);
+            }
+            v = uint4{w[0], w[1], w[2], w[3]};
+            if (STATS) *(uint4*)(Ot + row * OP + ch) = v;
+        }
         if (accumulate) {
             const uint4 o = *(const uint4*)dp;
             const uint32_t* pv = (const uint32_t*)&v;
@@ -255,9 +273,32 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
     }
     if (STATS) {
         // per output channel of the tile: mean, then the sum of squared
-        // deviations from it, over the tile's valid rows
+        // deviations from it, over the tile's valid rows (of the stored
+        // values: with a residual, the sums written back into the tile)
         __shared__ float red[2][BN];
         __shared__ float tmean[BN];
+        if (res) {
+            __syncthreads();
+#pragma unroll
+            for (int y = 0; y < TN; ++y) {
+                const int col = (wn * TN + y) * 16 + (lane & 15);
+#pragma unroll
+                for (int x = 0; x < TM; ++x)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        acc[x][y][i] = from_bf16(Ot[((wm * TM + x) * 16 + (lane >> 4) * 4 + i) * OP + col]);
+            }
+        }
+        float colsum[TN];
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+            colsum[y] = 0.f;
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if ((wm * TM + x) * 16 + (lane >> 4) * 4 + i < nvalid) colsum[y] += acc[x][y][i];
+        }
 #pragma unroll
         for (int y = 0; y < TN; ++y) {
             float s = colsum[y];
@@ -322,37 +363,40 @@ bool conv_bf16_supported(int mode, const ConvGeom& g) {
 }
 
 template <int BM, int BN>
-static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const ConvGeom& g,
-                                   const BfPass& ps, bool acc, const BnSums* stats, hipStream_t st) {
+static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const bf16* res,
+                                   const ConvGeom& g, const BfPass& ps, bool acc, const BnSums* stats,
+                                   hipStream_t st) {
     const long Mv = (long)g.Nb * ps.Hv * ps.Wv;
     if (Mv == 0) return hipSuccess;
     dim3 grid((unsigned)((Mv + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
     const BnSums sm = stats ? *stats : BnSums{};
     // two load steps per K-step (one barrier per 64 channels) for wide sources
     if (g.Cs >= 128 && g.Cs % 32 == 0) {
-        if (stats) launch((conv_bf16_k<BM, BN, true, true, 2>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, true, 2>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+        if (stats) launch((conv_bf16_k<BM, BN, true, true, 2>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, true, 2>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
     } else if (g.Cs % 32 == 0) {
-        if (stats) launch((conv_bf16_k<BM, BN, true, true, 1>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, true, 1>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+        if (stats) launch((conv_bf16_k<BM, BN, true, true, 1>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, true, 1>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
     } else {
-        if (stats) launch((conv_bf16_k<BM, BN, true, false, 1>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, false, 1>), grid, dim3(256), 0, st, src, B, bias, Y, g, ps, (int)acc, sm);
+        if (stats) launch((conv_bf16_k<BM, BN, true, false, 1>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, false, 1>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
     }
     return hipGetLastError();
 }
 
-static hipError_t run_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const ConvGeom& g,
-                                const BfPass& ps, bool acc, const BnSums* stats, int bm, int bn, hipStream_t st) {
-    if (bm == 128 && bn == 128) return launch_bf16_pass<128, 128>(src, B, bias, Y, g, ps, acc, stats, st);
-    if (bm == 128) return launch_bf16_pass<128, 64>(src, B, bias, Y, g, ps, acc, stats, st);
-    if (bn == 128) return launch_bf16_pass<64, 128>(src, B, bias, Y, g, ps, acc, stats, st);
-    return launch_bf16_pass<64, 64>(src, B, bias, Y, g, ps, acc, stats, st);
+static hipError_t run_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const bf16* res,
+                                const ConvGeom& g, const BfPass& ps, bool acc, const BnSums* stats, int bm, int bn,
+                                hipStream_t st) {
+    if (bm == 128 && bn == 128) return launch_bf16_pass<128, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
+    if (bm == 128) return launch_bf16_pass<128, 64>(src, B, bias, Y, res, g, ps, acc, stats, st);
+    if (bn == 128) return launch_bf16_pass<64, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
+    return launch_bf16_pass<64, 64>(src, B, bias, Y, res, g, ps, acc, stats, st);
 }
 
 hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const float* bias, bf16* Y, const ConvGeom& g,
-                            bool accumulate, const BnSums* stats, hipStream_t st) {
+                            bool accumulate, const BnSums* stats, hipStream_t st, const bf16* res) {
     if (!conv_bf16_supported(mode, g)) return hipErrorInvalidValue;
+    if (res && (mode != CONV_FWD || accumulate)) return hipErrorInvalidValue;
     int bm, bn;
     pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, bm, bn);
     BfPass ps{};
@@ -368,7 +412,7 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
         ps.ss = g.stride;
         ps.offh = ps.offw = -g.pad;
         ps.sgn = 1;
-        return run_bf16_pass(src, B, bias, Y, g, ps, accumulate, stats, bm, bn, st);
+        return run_bf16_pass(src, B, bias, Y, res, g, ps, accumulate, stats, bm, bn, st);
     }
     if (stats) return hipErrorInvalidValue;
     ps.ss = 1;
@@ -378,7 +422,7 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
         ps.Wv = g.Wo;
         ps.os = 1;
         ps.offh = ps.offw = g.pad;
-        return run_bf16_pass(src, B, bias, Y, g, ps, accumulate, nullptr, bm, bn, st);
+        return run_bf16_pass(src, B, bias, Y, nullptr, g, ps, accumulate, nullptr, bm, bn, st);
     }
     // stride 2: one pass per parity class of the dX pixels
     ps.os = 2;
@@ -399,7 +443,7 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
             q.offw = b + g.pad;
             int qbm, qbn;
             pick_bf16((long)g.Nb * q.Hv * q.Wv, g.Ncols, qbm, qbn);
-            const hipError_t e = run_bf16_pass(src, B, nullptr, Y, g, q, accumulate, nullptr, qbm, qbn, st);
+            const hipError_t e = run_bf16_pass(src, B, nullptr, Y, nullptr, g, q, accumulate, nullptr, qbm, qbn, st);
             if (e != hipSuccess) return e;
         }
     return hipSuccess;

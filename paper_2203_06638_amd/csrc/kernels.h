@@ -140,9 +140,12 @@ hipError_t launch_wgrad_reduce_multi(const WgRedTable& t, hipStream_t st);
 // output, float32 accumulation; geometry as for the float32 passes.  The
 // forward epilogue's batch-norm sums describe the stored (rounded) output;
 // partials come per row tile of conv_bf16_tile_rows(g) rows.  Cs and Ncols
-// must be multiples of 8; data gradients of stride 1 or 2.
+// must be multiples of 8; data gradients of stride 1 or 2.  res (forward,
+// not accumulating): a tensor of Y's shape added to the rounded output and
+// rounded again (a fused residual add); the sums then describe Y.
 hipError_t launch_conv_bf16(int mode, const uint16_t* src, const uint16_t* B, const float* bias, uint16_t* Y,
-                            const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st);
+                            const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st,
+                            const uint16_t* res = nullptr);
 int conv_bf16_tile_rows(const ConvGeom& g);
 bool conv_bf16_supported(int mode, const ConvGeom& g);
 // weight gradient from bf16 dY and X into float32 partials part[split][Cout]

@@ -91,8 +91,8 @@ struct Group {
     int a = -1;         // G_CONV: conv; G_BNACT: first BN; G_HEAD: pool; else: the layer
     int stats_bn = -1;  // G_CONV: BN whose batch statistics the conv epilogue computes
     int bn2 = -1;       // G_BNACT: BN of the other branch of the residual add (both normalised)
-    int add = -1;       // G_BNACT: the residual add, if any
-    int res = -1;       // G_BNACT: the residual tensor added unnormalised, if any
+    int add = -1;       // G_BNACT / G_CONV: the residual add, if any
+    int res = -1;       // G_BNACT / G_CONV: the residual tensor added unnormalised, if any
     int relu = -1;      // G_BNACT: the closing ReLU, if any
     int lin = -1;       // G_HEAD: the linear layer
     bool fold = false;  // G_BNACT: BN + ReLU folded into the consuming conv (nothing launched forward)
@@ -403,6 +403,39 @@ void build_groups(Model& M, bool fused) {
             if (x >= 0) taken[x] = 1;
         gs.push_back(g);
     }
+    // bf16: a conv whose only consumer is a residual add of a stored tensor
+    // stores the sum itself (its epilogue adds the other input), and forms
+    // the batch statistics of a BN reading the sum (a pre-activation unit's
+    // end feeding the next unit's first BN)
+    if (fused && M.dt == lpp::DT_BF16) {
+        std::vector<int> group_of(n, -1);
+        for (int i = 0; i < (int)gs.size(); ++i) group_of[gs[i].out] = i;
+        std::vector<char> drop(gs.size(), 0);
+        for (auto& g : gs) {
+            if (g.kind != G_CONV || M.layers[g.a].pw || g.stats_bn >= 0) continue;
+            const int c = sole(g.a);
+            if (c < 0 || op(c) != LPP_ADD || group_of[c] < 0 || gs[group_of[c]].kind != G_ADD || drop[group_of[c]])
+                continue;
+            const lpp_layer& A = M.layers[c].L;
+            if (A.in0 == A.in1) continue;
+            const int other = A.in0 == g.a ? A.in1 : A.in0;
+            if (other < 0 || group_of[other] < 0) continue;       // the residual must be a stored output
+            drop[group_of[c]] = 1;
+            g.add = c;
+            g.res = other;
+            g.out = c;
+            for (int b : M.consumers[c])
+                if (op(b) == LPP_BN && M.layers[b].L.in0 == c && M.stats_from[b] < 0) {
+                    g.stats_bn = b;
+                    M.stats_from[b] = g.a;
+                    break;
+                }
+        }
+        std::vector<Group> kept;
+        for (int i = 0; i < (int)gs.size(); ++i)
+            if (!drop[i]) kept.push_back(gs[i]);
+        gs.swap(kept);
+    }
     // a group runs when its last layer's inputs exist: order by output layer
     std::stable_sort(gs.begin(), gs.end(), [](const Group& x, const Group& y) { return x.out < y.out; });
     M.groups = gs;
@@ -695,7 +728,8 @@ int run_forward(lpp_ctx* c, Worker& w) {
             else if (bf)
                 LAUNCH("conv_fwd", 2.0 * Y.macs, st,
                        lpp::launch_conv_bf16(lpp::CONV_FWD, (const uint16_t*)x0, (const uint16_t*)c->wf(w, Y), bias,
-                                             (uint16_t*)c->act(w, G.a), g, false, sp, st));
+                                             (uint16_t*)c->act(w, G.out), g, false, sp, st,
+                                             G.add >= 0 ? (const uint16_t*)c->act(w, G.res) : nullptr));
             else
                 LAUNCH("conv_fwd", 2.0 * Y.macs, st,
                        lpp::launch_conv_igemm(lpp::CONV_FWD, (const float*)x0, (const float*)c->wf(w, Y), bias,
@@ -905,6 +939,16 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                     LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
                            lpp::launch_conv_igemm(lpp::CONV_DGRAD, (const float*)dy, (const float*)c->wdg(w, Y),
                                                   nullptr, (float*)dx0, g, pl.acc0[G.a] != 0, nullptr, st));
+            }
+            if (G.add >= 0) {
+                // the fused residual add passes the same gradient to its other input
+                const lpp_layer& A = M.layers[G.add].L;
+                const bool want_res = A.in0 == G.res ? pl.din0[G.add] : pl.din1[G.add];
+                const bool acc_res = A.in0 == G.res ? pl.acc0[G.add] : pl.acc1[G.add];
+                const long Mo = (long)N * Y.out.h * Y.out.w;
+                if (want_res)
+                    LAUNCH("add", 2.0 * eb * Mo * Y.out.c, st,
+                           lpp::launch_copy_acc(dt, dy, c->dact(w, G.res), Mo * Y.out.c, acc_res, st));
             }
             break;
         }

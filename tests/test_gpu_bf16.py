@@ -215,12 +215,14 @@ def test_bf16_full_width_small_batch_forward():
 # of every convolution on sampled outputs, and properties of the gradient
 # ---------------------------------------------------------------------------
 
-def _teacher_forced_convs(o, ctx, x, img, rng, samples=96):
+def _teacher_forced_convs(o, ctx, x, img, rng, samples=96, fused=None):
     """For each conv: sampled output entries recomputed in fp64 from the
     GPU's stored input and the bf16-rounded weights; sampled weight-gradient
     entries recomputed from the GPU's stored input and output gradient.
-    Returns the worst normalised errors (forward, weight gradient)."""
+    Returns the worst normalised errors (forward, weight gradient); fused[0]
+    counts the convs checked through their fused residual add."""
     shapes = R.shapes(o)
+    fused = [0] if fused is None else fused
     n = img.shape[0]
     xw = bf(x).astype(np.float64)
     gvec = ctx.get_grad(0).astype(np.float64)
@@ -229,8 +231,23 @@ def _teacher_forced_convs(o, ctx, x, img, rng, samples=96):
         if rec["op"] != OM.CONV:
             continue
         src = img.astype(np.float64) if rec["in0"] < 0 else ctx.get_activation(0, rec["in0"], shapes[rec["in0"]]).astype(np.float64)
-        out = ctx.get_activation(0, li, shapes[li]).astype(np.float64)
-        dout = ctx.get_activation_grad(0, li, shapes[li]).astype(np.float64)
+        resid = None
+        try:
+            out = ctx.get_activation(0, li, shapes[li]).astype(np.float64)
+            dout = ctx.get_activation_grad(0, li, shapes[li]).astype(np.float64)
+        except lpp.LppError as e:
+            # a conv whose epilogue adds the residual (its only consumer, a
+            # residual add): check the stored sum round(round(conv) + res)
+            # against the conv recomputed plus the GPU's stored residual; the
+            # gradient at the conv output is the add's
+            assert e.code == lpp.ESTATE
+            add = next(c for c, r in enumerate(o.layers) if r["in0"] == li or r["in1"] == li)
+            assert o.layers[add]["op"] == OM.ADD
+            other = o.layers[add]["in1"] if o.layers[add]["in0"] == li else o.layers[add]["in0"]
+            out = ctx.get_activation(0, add, shapes[add]).astype(np.float64)
+            resid = ctx.get_activation(0, other, shapes[other]).astype(np.float64)
+            dout = ctx.get_activation_grad(0, add, shapes[add]).astype(np.float64)
+            fused[0] += 1
         k, s, pd, cin, cout = rec["k"], rec["stride"], rec["pad"], rec["cin"], rec["cout"]
         W = xw[rec["poff"]:rec["poff"] + cout * cin * k * k].reshape(cout, cin, k, k)
         xp = np.pad(src, ((0, 0), (0, 0), (pd, pd), (pd, pd)))
@@ -242,8 +259,13 @@ def _teacher_forced_convs(o, ctx, x, img, rng, samples=96):
             scale = float(np.abs(patch * W[co]).sum()) + 1e-30
             # one rounding to bf16 (at most 2^-8 relative: half a unit in the
             # last of 8 significant bits) of an fp32 sum of the exact bf16
-            # products (a few fp32 units of the terms' magnitude sum)
-            worst_f = max(worst_f, abs(out[b, co, i, j] - ref) / (2.0 ** -8 * abs(ref) + 5e-5 * scale))
+            # products (a few fp32 units of the terms' magnitude sum); with a
+            # fused residual, a second rounding of the sum
+            bound = 2.0 ** -8 * abs(ref) + 5e-5 * scale
+            if resid is not None:
+                ref += resid[b, co, i, j]
+                bound += 2.0 ** -8 * abs(ref)
+            worst_f = max(worst_f, abs(out[b, co, i, j] - ref) / bound)
         gW = gvec[rec["poff"]:rec["poff"] + cout * cin * k * k].reshape(cout, cin, k, k)
         for _ in range(samples // 4):
             co, ci, r, q = rng.integers(cout), rng.integers(cin), rng.integers(k), rng.integers(k)
@@ -275,8 +297,12 @@ def test_bf16_full_size_teacher_forced(which):
         loss = ctx.get_loss(0)
         say(which, "loss %.4f (ln C = %.4f)" % (loss, np.log(o.n_classes)))
         assert np.isfinite(loss)
-        wf, ww = _teacher_forced_convs(o, ctx, x, img, np.random.default_rng(5))
-        say(which, "teacher-forced: forward %.3f, weight gradient %.3f (bar 1)" % (wf, ww))
+        fused = [0]
+        wf, ww = _teacher_forced_convs(o, ctx, x, img, np.random.default_rng(5), fused=fused)
+        say(which, "teacher-forced: forward %.3f, weight gradient %.3f (bar 1); %d convs with a fused residual add"
+            % (wf, ww, fused[0]))
+        if which == "wrn16_8":
+            assert fused[0] == 6                 # every unit's last conv adds the shortcut in its epilogue
         assert wf < 1.0 and ww < 1.0
         g = ctx.get_grad(0)
         for part in range(1, 5):
