@@ -76,11 +76,30 @@ struct BfPass {
 // res (forward only): a residual tensor of the output's shape added to the
 // rounded output and rounded again, as a separate residual add of the two
 // stored tensors would; the statistics then describe that sum.
-template <int BM, int BN, bool STATS, bool FASTK, int KH>
-__global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src, const bf16* __restrict__ B,
+// buffer resource over n bytes at p (loads past n return zeros)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t bf_rsrc(const void* p, long n) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, (int)(n < 0x7fffffffL ? n : 0x7fffffffL), 0x00020000);
+}
+// 16 bytes at byte offset voff of r into LDS at dst + 16 * lane (dst uniform)
+__device__ __forceinline__ void bf_dma16(__amdgpu_buffer_rsrc_t r, bf16* dst, unsigned voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, voff, 0, 0, 0);
+}
+
+// DMA (FASTK only): operand tiles go from memory straight into LDS (buffer
+// loads with the LDS bit: no register staging, no LDS store instructions;
+// taps in the zero padding and columns past the output read out of the
+// buffer's range, which yields zeros).  Each wave's load instruction fills
+// 1 KB of LDS in lane order, so a thread loads the 16-byte chunk its lane
+// position holds under the swizzle.  Per K-step: all fragments are read
+// from the current buffer, then the next K-step's loads are issued into the
+// other buffer, then the MFMAs run; the barrier at the step's end waits for
+// the loads.
+template <int BM, int BN, bool STATS, bool FASTK, int KH, bool DMA>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ? 2 : 1, 8))) void conv_bf16_k(const bf16* __restrict__ src, const bf16* __restrict__ B,
                                                    const float* __restrict__ bias, bf16* __restrict__ Y,
                                                    const bf16* __restrict__ res, ConvGeom g, BfPass ps, int accumulate,
                                                    BnSums sums) {
+    static_assert(!DMA || FASTK, "DMA operand loads need 32-channel load steps");
     constexpr int TM = BM / 32, TN = BN / 32;     // 16x16 blocks per wave; waves 2 x 2
     constexpr int AL = BM / 64, BL = BN / 64;     // 16-byte operand loads per thread per K-step
     constexpr int P = kBfPitch;
@@ -183,13 +202,76 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
         for (int y = 0; y < TN; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
 
     const int nk = (nks + KH - 1) / KH;           // K-steps
+    const int a_rd = ((wm * TM) * 16 + (lane & 15)) * P + bf_swz(lane >> 4, lane & 15) * 8;
+    const int b_rd = BM * P + ((wn * TN) * 16 + (lane & 15)) * P + bf_swz(lane >> 4, lane & 15) * 8;
+    if constexpr (DMA) {
+        const __amdgpu_buffer_rsrc_t ars = bf_rsrc(src, (long)g.Nb * g.Hs * g.Ws * g.Cs * 2);
+        const __amdgpu_buffer_rsrc_t brs = bf_rsrc(B, (long)g.Ncols * RS * g.Cs * 2);
+        const int jj = bf_swz(j, rr);             // the source chunk of this thread's LDS position
+        unsigned b_off[BL];
+#pragma unroll
+        for (int u = 0; u < BL; ++u) {
+            const int n = n0 + rr + 64 * u;
+            b_off[u] = n < g.Ncols ? (unsigned)(n * RS * g.Cs + jj * 8) * 2u : 0x80000000u;
+        }
+        // one K-step's loads into LDS buffer buf; (tx, ty, c0) advance
+        auto issue = [&](int buf, int kk) {
+#pragma unroll
+            for (int h = 0; h < KH; ++h) {
+                const bool tok = kk * KH + h < nks;
+                const int r = ps.r0 + ps.step * tx, sc = ps.s0 + ps.step * ty;
+                const int dh = (ps.offh + ps.sgn * r) >> ps.shift, dw = (ps.offw + ps.sgn * sc) >> ps.shift;
+                const int aoff = (dh * g.Ws + dw) * g.Cs + c0 + jj * 8;
+                const unsigned woff = (unsigned)((r * g.S + sc) * g.Cs + c0) * 2u;
+                bf16* As = lds + buf * STAGE + h * HALF + wave * 16 * P;
+#pragma unroll
+                for (int u = 0; u < AL; ++u) {
+                    const int hh = a_h[u] + dh, ww = a_w[u] + dw;
+                    const bool ok = tok && (unsigned)hh < (unsigned)g.Hs && (unsigned)ww < (unsigned)g.Ws;
+                    bf_dma16(ars, As + 64 * u * P, ok ? (unsigned)(a_off[u] + aoff) * 2u : 0x80000000u);
+                }
+#pragma unroll
+                for (int u = 0; u < BL; ++u)
+                    bf_dma16(brs, As + (BM + 64 * u) * P,
+                             tok && b_off[u] < 0x80000000u ? b_off[u] + woff : 0x80000000u);
+                c0 += 32;
+                if (c0 == g.Cs) {
+                    c0 = 0;
+                    if (++ty == ps.ns) {
+                        ty = 0;
+                        ++tx;
+                    }
+                }
+            }
+        };
+        if (nk > 0) issue(0, 0);
+        __syncthreads();
+        for (int kk = 0; kk < nk; ++kk) {
+            const int cur = kk & 1;
+            bf8 a[KH][TM], b[KH][TN];
+#pragma unroll
+            for (int h = 0; h < KH; ++h) {
+                const bf16* base = lds + cur * STAGE + h * HALF;
+#pragma unroll
+                for (int x = 0; x < TM; ++x) a[h][x] = *(const bf8*)(base + a_rd + x * 16 * P);
+#pragma unroll
+                for (int y = 0; y < TN; ++y) b[h][y] = *(const bf8*)(base + b_rd + y * 16 * P);
+            }
+            if (kk + 1 < nk) issue(cur ^ 1, kk + 1);
+#pragma unroll
+            for (int h = 0; h < KH; ++h)
+#pragma unroll
+                for (int x = 0; x < TM; ++x)
+#pragma unroll
+                    for (int y = 0; y < TN; ++y) acc[x][y] = mfma_bf16(a[h][x], b[h][y], acc[x][y]);
+            __syncthreads();
+        }
+    } else {
     if (nk > 0) {
         load_k(0);
         store(0);
     }
     __syncthreads();
-    const int a_rd = ((wm * TM) * 16 + (lane & 15)) * P + bf_swz(lane >> 4, lane & 15) * 8;
-    const int b_rd = BM * P + ((wn * TN) * 16 + (lane & 15)) * P + bf_swz(lane >> 4, lane & 15) * 8;
     for (int kk = 0; kk < nk; ++kk) {
         const int cur = kk & 1;
         if (kk + 1 < nk) load_k(kk + 1);
@@ -208,6 +290,7 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
         }
         if (kk + 1 < nk) store(cur ^ 1);
         __syncthreads();
+    }
     }
 
     // epilogue: bias, rounding to bf16 (the stored values, which the batch
@@ -342,17 +425,25 @@ __global__ __launch_bounds__(256) void conv_bf16_k(const bf16* __restrict__ src,
     }
 }
 
-// Tile shape of a pass: BN = 128 for wide outputs, else 64; BM = 128 unless
-// that leaves fewer than 512 workgroups.
-static void pick_bf16(long Mv, int Ncols, int& bm, int& bn) {
+// Tile shape of a pass: BN = 128 for wide outputs, else 64; BM = 256 (one
+// load step per barrier, two waves per SIMD) when that still gives 512
+// workgroups and the source takes 32-channel load steps, else 128 unless that
+// leaves fewer than 512 workgroups.  (Measured: the 256-row tile gains
+// 10-15% where two of its workgroups fill every compute unit and loses up to
+// 50% where they do not.)
+static void pick_bf16(long Mv, int Ncols, int Cs, int& bm, int& bn) {
     bn = Ncols >= 128 ? 128 : 64;
     const long nt = (Ncols + bn - 1) / bn;
+    if (bn == 128 && Cs % 32 == 0 && ((Mv + 255) / 256) * nt >= 512) {
+        bm = 256;
+        return;
+    }
     bm = ((Mv + 127) / 128) * nt >= 512 ? 128 : 64;
 }
 
 int conv_bf16_tile_rows(const ConvGeom& g) {
     int bm, bn;
-    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, bm, bn);
+    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, g.Cs, bm, bn);
     return bm;
 }
 
@@ -371,15 +462,18 @@ static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* 
     dim3 grid((unsigned)((Mv + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
     const BnSums sm = stats ? *stats : BnSums{};
     // two load steps per K-step (one barrier per 64 channels) for wide sources
-    if (g.Cs >= 128 && g.Cs % 32 == 0) {
-        if (stats) launch((conv_bf16_k<BM, BN, true, true, 2>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, true, 2>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+    if (BM == 256 && g.Cs % 32 == 0) {
+        if (stats) launch((conv_bf16_k<BM, BN, true, true, 1, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, true, 1, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+    } else if (g.Cs >= 128 && g.Cs % 32 == 0) {
+        if (stats) launch((conv_bf16_k<BM, BN, true, true, 2, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, true, 2, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
     } else if (g.Cs % 32 == 0) {
-        if (stats) launch((conv_bf16_k<BM, BN, true, true, 1>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, true, 1>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        if (stats) launch((conv_bf16_k<BM, BN, true, true, 1, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, true, 1, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
     } else {
-        if (stats) launch((conv_bf16_k<BM, BN, true, false, 1>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, false, 1>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        if (stats) launch((conv_bf16_k<BM, BN, true, false, 1, false>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, false, 1, false>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
     }
     return hipGetLastError();
 }
@@ -387,6 +481,7 @@ static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* 
 static hipError_t run_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const bf16* res,
                                 const ConvGeom& g, const BfPass& ps, bool acc, const BnSums* stats, int bm, int bn,
                                 hipStream_t st) {
+    if (bm == 256) return launch_bf16_pass<256, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
     if (bm == 128 && bn == 128) return launch_bf16_pass<128, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
     if (bm == 128) return launch_bf16_pass<128, 64>(src, B, bias, Y, res, g, ps, acc, stats, st);
     if (bn == 128) return launch_bf16_pass<64, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
@@ -398,7 +493,7 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
     if (!conv_bf16_supported(mode, g)) return hipErrorInvalidValue;
     if (res && (mode != CONV_FWD || accumulate)) return hipErrorInvalidValue;
     int bm, bn;
-    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, bm, bn);
+    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, g.Cs, bm, bn);
     BfPass ps{};
     ps.Hd = g.Ho;
     ps.Wd = g.Wo;
@@ -442,7 +537,7 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
             q.offh = a + g.pad;
             q.offw = b + g.pad;
             int qbm, qbn;
-            pick_bf16((long)g.Nb * q.Hv * q.Wv, g.Ncols, qbm, qbn);
+            pick_bf16((long)g.Nb * q.Hv * q.Wv, g.Ncols, g.Cs, qbm, qbn);
             const hipError_t e = run_bf16_pass(src, B, nullptr, Y, nullptr, g, q, accumulate, nullptr, qbm, qbn, st);
             if (e != hipSuccess) return e;
         }
