@@ -36,6 +36,10 @@ namespace lpp {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
+__device__ __forceinline__ f4 relu4(f4 v) {
+    return f4{fmaxf(v[0], 0.f), fmaxf(v[1], 0.f), fmaxf(v[2], 0.f), fmaxf(v[3], 0.f)};
+}
+
 __device__ __forceinline__ f4 mfma16x16x4(float a, float b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
@@ -204,7 +208,7 @@ __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ 
                 if (m >= M) continue;
                 const long o = (long)m * g.Ncols + n;
                 const float v = acc[x][y][i];
-                Y[o] = accumulate ? Y[o] + v : v;
+                Y[o] = accumulate == kStoreAdd ? Y[o] + v : (accumulate == kStoreRelu ? fmaxf(v, 0.f) : v);
             }
     }
     if (STATS) {
@@ -390,7 +394,7 @@ __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ sr
                 if (m >= M) continue;
                 const long o = (long)m * g.Ncols + n;
                 const float v = acc[x][y][i];
-                Y[o] = accumulate ? Y[o] + v : v;
+                Y[o] = accumulate == kStoreAdd ? Y[o] + v : (accumulate == kStoreRelu ? fmaxf(v, 0.f) : v);
             }
     }
     if (STATS) {
@@ -453,7 +457,7 @@ __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ sr
 
 template <int MODE, int BM, int BN, int WM>
 static hipError_t launch_lds(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                             bool acc, const BnSums* stats, hipStream_t st) {
+                             int acc, const BnSums* stats, hipStream_t st) {
     const long M = (long)g.Nb * g.Ho * g.Wo;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
     if (stats)
@@ -679,7 +683,7 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
             if (n < g.Ncols) {
                 const f4 v = *(const f4*)(Ot + p * OP + qd * 4);
                 f4* o = (f4*)(Y + (m0 + pix_base + p) * g.Ncols + n);
-                *o = accumulate ? *o + v : v;
+                *o = accumulate == kStoreAdd ? *o + v : (accumulate == kStoreRelu ? relu4(v) : v);
                 if (MODE == CONV_DGRAD && STATS) {
                     // gm = v where the forward's ReLU passed, xhat of the BN input
                     const f4 x = *(const f4*)(bs.x1 + (m0 + pix_base + p) * g.Ncols + n);
@@ -838,7 +842,7 @@ static bool pick_tile(int mode, const ConvGeom& g, TileCfg& out) {
 
 template <int MODE, int KS, int WM, int TM, int TN>
 static hipError_t launch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              const TileCfg& c, bool acc, const BnSums* stats, const BnFwd* inbn,
+                              const TileCfg& c, int acc, const BnSums* stats, const BnFwd* inbn,
                               const BnBwdSum* bsv, hipStream_t st) {
     constexpr int BN = (4 / WM) * TN * 16;
     dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
@@ -867,7 +871,7 @@ static hipError_t launch_tile(const float* src, const float* B, const float* bia
 
 template <int MODE>
 static hipError_t dispatch_tile(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                                const TileCfg& c, bool acc, const BnSums* stats, const BnFwd* inbn,
+                                const TileCfg& c, int acc, const BnSums* stats, const BnFwd* inbn,
                                 const BnBwdSum* bsv, hipStream_t st) {
 #define TILE(WM_, TM_, TN_)                                                                                        \
     if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) {                                                               \
@@ -1047,7 +1051,7 @@ __global__ __launch_bounds__(256) void conv_dgrad_s2_f32(const float* __restrict
         const int hr = tp / tw, wc = tp - (tp / tw) * tw;
         const f4 v = *(const f4*)(lds + tp * OP + qd * 4);
         f4* o = (f4*)(dX + ((long)(img * g.Ho + 2 * i0 + hr) * g.Wo + wc) * g.Ncols + n);
-        *o = accumulate ? *o + v : v;
+        *o = accumulate == kStoreAdd ? *o + v : (accumulate == kStoreRelu ? relu4(v) : v);
     }
 }
 
@@ -1089,7 +1093,7 @@ static bool pick_s2(const ConvGeom& g, S2Cfg& out) {
 }
 
 template <int KS, int PAD, int WM, int TM, int TN>
-static hipError_t launch_s2(const float* dY, const float* B, float* dX, const ConvGeom& g, const S2Cfg& c, bool acc,
+static hipError_t launch_s2(const float* dY, const float* B, float* dX, const ConvGeom& g, const S2Cfg& c, int acc,
                             hipStream_t st) {
     constexpr int BN = (4 / WM) * TN * 16;
     dim3 grid((unsigned)(g.Nb * c.t.tiles_per_img), (unsigned)((g.Ncols + BN - 1) / BN));
@@ -1098,7 +1102,7 @@ static hipError_t launch_s2(const float* dY, const float* B, float* dX, const Co
     return hipGetLastError();
 }
 
-static hipError_t dispatch_s2(const float* dY, const float* B, float* dX, const ConvGeom& g, const S2Cfg& c, bool acc,
+static hipError_t dispatch_s2(const float* dY, const float* B, float* dX, const ConvGeom& g, const S2Cfg& c, int acc,
                               hipStream_t st) {
 #define S2(WM_, TM_, TN_)                                                                              \
     if (c.wm == WM_ && c.tm == TM_ && c.tn == TN_) {                                                   \
@@ -1112,7 +1116,7 @@ static hipError_t dispatch_s2(const float* dY, const float* B, float* dX, const 
 
 template <int MODE, int WM, int TM, int TN>
 static hipError_t launch_cfg(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                             bool acc, const BnSums* stats, hipStream_t st) {
+                             int acc, const BnSums* stats, hipStream_t st) {
     constexpr int BM = WM * TM * 16, BN = (4 / WM) * TN * 16;
     const long M = (long)g.Nb * g.Ho * g.Wo;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
@@ -1157,7 +1161,7 @@ static ConvCfg pick_cfg(const ConvGeom& g) {
 
 template <int MODE>
 static hipError_t launch_mode(const float* src, const float* B, const float* bias, float* Y, const ConvGeom& g,
-                              bool acc, const BnSums* stats, const BnFwd* inbn, const BnBwdSum* bsv, hipStream_t st) {
+                              int acc, const BnSums* stats, const BnFwd* inbn, const BnBwdSum* bsv, hipStream_t st) {
     TileCfg tc;
     if (pick_tile(MODE, g, tc)) return dispatch_tile<MODE>(src, B, bias, Y, g, tc, acc, stats, inbn, bsv, st);
     if (inbn || bsv) return hipErrorInvalidValue;   // folding and backward sums need the spatial kernel
@@ -1195,7 +1199,7 @@ int conv_tile_rows(const ConvGeom& g) {
 }
 
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st,
+                             const ConvGeom& g, int accumulate, const BnSums* stats, hipStream_t st,
                              const BnFwd* inbn, const BnBwdSum* bsum) {
     if (mode == CONV_FWD) {
         if (bsum) return hipErrorInvalidValue;

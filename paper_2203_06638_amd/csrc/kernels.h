@@ -93,8 +93,12 @@ struct BnBwdSum {
     const float* x1;
     const float* aux;
 };
+// How a pass writes Y: kStoreSet overwrites, kStoreAdd adds to what Y
+// holds, kStoreRelu (forward, without stats) overwrites with max(y, 0) -- a
+// ReLU whose input the conv alone produces, fused into its epilogue.
+constexpr int kStoreSet = 0, kStoreAdd = 1, kStoreRelu = 2;
 hipError_t launch_conv_igemm(int mode, const float* src, const float* B, const float* bias, float* Y,
-                             const ConvGeom& g, bool accumulate, const BnSums* stats, hipStream_t st,
+                             const ConvGeom& g, int store, const BnSums* stats, hipStream_t st,
                              const BnFwd* inbn = nullptr, const BnBwdSum* bsum = nullptr);
 // Tiles of the spatial data-gradient kernel for g, or 0 when it does not take g.
 int conv_dgrad_sum_tiles(const ConvGeom& g);
@@ -251,6 +255,10 @@ hipError_t launch_head_bwd_x(int dt, const float* dz, const float* W, int Nb, in
 // elementwise (n multiple of 4)
 hipError_t launch_relu_fwd(int dt, const void* x, void* y, long n, hipStream_t st);
 hipError_t launch_relu_bwd(int dt, const void* dy, const void* x, void* dx, long n, bool accumulate, hipStream_t st);
+// dy (M x C, C a multiple of 4) := dy where y > 0, else 0, in place, y a
+// ReLU's stored output; pmean[tile][c] = the tile's mean of the masked
+// column c over stats_tiles(M, C) row tiles of stats_rows(M, C) rows.
+hipError_t launch_relu_mask_colsum(int dt, void* dy, const void* y, long M, int C, float* pmean, hipStream_t st);
 hipError_t launch_add_fwd(int dt, const void* a, const void* b, void* y, long n, hipStream_t st);
 hipError_t launch_copy_acc(int dt, const void* src, void* dst, long n, bool accumulate, hipStream_t st);
 // channel concatenation of two NHWC tensors with `rows` pixels (ca, cb
@@ -267,8 +275,19 @@ hipError_t launch_maxpool_bwd(int dt, const void* dy, const uint8_t* arg, void* 
 // pooled features are float32
 hipError_t launch_gap_fwd(int dt, const void* x, float* y, int Nb, int HW, int C, hipStream_t st);
 hipError_t launch_gap_bwd(int dt, const float* dy, void* dx, int Nb, int HW, int C, bool accumulate, hipStream_t st);
+// y = x W^T + b over Nb rows (then max(y, 0) with relu)
 hipError_t launch_linear_fwd(const float* x, const float* W, const float* b, float* y, int Nb, int I, int O,
-                             hipStream_t st);
+                             hipStream_t st, bool relu = false);
+// Weight-gradient partials of y = x W^T + b over M rows in
+// linear_wgrad_splits(M) splits of linear_wgrad_rows(M) rows:
+// part_w[split][O][I] (the weight) and, when part_b is non-null,
+// part_b[split][ceil4(O)] (the bias, zero past O); both reduce with
+// wgrad_reduce_multi (R = S = 1).
+constexpr int kLinWgMaxSplits = 512;
+int linear_wgrad_rows(long M);
+int linear_wgrad_splits(long M);
+hipError_t launch_linear_wgrad_part(const float* dz, const float* x, float* part_w, float* part_b, int M, int I,
+                                    int O, hipStream_t st);
 hipError_t launch_linear_bwd_w(const float* dz, const float* x, float* gW, float* gb, int Nb, int I, int O,
                                hipStream_t st);
 hipError_t launch_linear_bwd_x(const float* dz, const float* W, float* dx, int Nb, int I, int O, bool accumulate,

@@ -661,6 +661,56 @@ __global__ void copy_acc_k(const T* __restrict__ s, T* __restrict__ d, long n4, 
         st4(d, i, acc ? ld4(d, i) + ld4(s, i) : ld4(s, i));
 }
 
+// The gradient at a ReLU's output masked in place into the gradient at its
+// input (where the stored output y is zero: the ReLU clipped), and per row
+// tile of stats_rows(M, C) rows the mean over the tile of each masked
+// column, pmean[tile][c] -- a conv bias gradient's partials, summed by
+// sum_from_tiles.  Tiling as stats_partial_k.
+template <class T>
+__global__ __launch_bounds__(256) void relu_mask_colsum_k(T* __restrict__ dy, const T* __restrict__ y, long M, int C,
+                                                          int R, float* __restrict__ pmean) {
+    __shared__ f4 red[256];
+    const int tid = threadIdx.x;
+    const int C4 = C >> 2;
+    const long r0 = (long)blockIdx.x * R;
+    const long r1 = min(M, r0 + R);
+    const float rows = (float)(r1 - r0);
+    for (int qbase = blockIdx.y * 256; qbase < min(C4, (int)(blockIdx.y + 1) * 256); qbase += 256) {
+        int nq, rl;
+        quad_layout(C4, qbase, nq, rl);
+        const int q = qbase + tid % nq, lr = tid / nq;
+        f4 s = f4{0.f, 0.f, 0.f, 0.f};
+        if (lr < rl)
+            for (long r = r0 + lr; r < r1; r += rl) {
+                f4 g = ld4(dy, r * C4 + q);
+                const f4 v = ld4(y, r * C4 + q);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) g[k] = v[k] > 0.f ? g[k] : 0.f;
+                st4(dy, r * C4 + q, g);
+                s += g;
+            }
+        red[tid] = s;
+        __syncthreads();
+        if (tid < nq) {
+            f4 t = f4{0.f, 0.f, 0.f, 0.f};
+            for (int k = 0; k < rl; ++k) t += red[k * nq + tid];
+            for (int k = 0; k < 4; ++k) pmean[(long)blockIdx.x * C + (qbase + tid) * 4 + k] = t[k] / rows;
+        }
+        __syncthreads();
+    }
+}
+
+hipError_t launch_relu_mask_colsum(int dt, void* dy, const void* y, long M, int C, float* pmean, hipStream_t st) {
+    if (C % 4) return hipErrorInvalidValue;
+    const dim3 grid(stats_tiles(M, C), ((C >> 2) + 255) / 256);
+    const int R = stats_rows(M, C);
+    if (dt == DT_BF16)
+        launch(relu_mask_colsum_k<bf16>, grid, dim3(256), 0, st, (bf16*)dy, (const bf16*)y, M, C, R, pmean);
+    else
+        launch(relu_mask_colsum_k<float>, grid, dim3(256), 0, st, (float*)dy, (const float*)y, M, C, R, pmean);
+    return hipGetLastError();
+}
+
 hipError_t launch_relu_fwd(int dt, const void* x, void* y, long n, hipStream_t st) {
     if (dt == DT_BF16)
         launch(relu_fwd_k<bf16>, dim3(ew_grid(n / 4)), dim3(256), 0, st, (const bf16*)x, (bf16*)y, n / 4);
@@ -879,14 +929,89 @@ hipError_t launch_gap_bwd(int dt, const float* dy, void* dx, int Nb, int HW, int
 // linear head and loss
 // ------------------------------------------------------------------------
 
-__global__ void linear_fwd_k(const float* __restrict__ x, const float* __restrict__ W, const float* __restrict__ b,
-                             float* __restrict__ y, int Nb, int I, int O) {
-    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= Nb * O) return;
-    const int n = idx / O, o = idx - n * O;
-    float s = b ? b[o] : 0.f;
-    for (int i = 0; i < I; ++i) s += W[(long)o * I + i] * x[(long)n * I + i];
-    y[idx] = s;
+// y[m][o] = b[o] + sum_i x[m][i] W[o][i], then max(y, 0) with relu.  16
+// lanes per row (four rows a wave): lane l takes columns 4l + 64j as quads
+// (V4: I a multiple of 4) or l + 16j, for up to 16 outputs per pass over
+// the row; the 16 lane sums of an output meet in a fixed xor-shuffle tree.
+// W stays in the CU cache: every row of the grid reads the same O x I.
+template <bool V4>
+__global__ __launch_bounds__(256) void linear_fwd_k(const float* __restrict__ x, const float* __restrict__ W,
+                                                    const float* __restrict__ b, float* __restrict__ y, int Nb,
+                                                    int I, int O, int relu) {
+    const int l = threadIdx.x & 15;
+    const long m = (long)blockIdx.x * 16 + (threadIdx.x >> 4);
+    const bool live = m < Nb;
+    const float* xr = x + (live ? m : 0) * I;
+    for (int o0 = 0; o0 < O; o0 += 16) {
+        float s[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) s[j] = 0.f;
+        if (V4) {
+            for (int i = 4 * l; i < I; i += 64) {
+                const f4 xv = *(const f4*)(xr + i);
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    if (o0 + j < O) {
+                        const f4 wv = *(const f4*)(W + (long)(o0 + j) * I + i);
+                        s[j] += xv[0] * wv[0] + xv[1] * wv[1] + xv[2] * wv[2] + xv[3] * wv[3];
+                    }
+            }
+        } else {
+            for (int i = l; i < I; i += 16) {
+                const float xv = xr[i];
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    if (o0 + j < O) s[j] += xv * W[(long)(o0 + j) * I + i];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+#pragma unroll
+            for (int h = 8; h > 0; h >>= 1) s[j] += __shfl_xor(s[j], h, 16);
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            if (live && l == j && o0 + j < O) {
+                const float v = s[j] + (b ? b[o0 + j] : 0.f);
+                y[m * O + o0 + j] = relu && v < 0.f ? 0.f : v;
+            }
+    }
+}
+
+// Weight-gradient partials of y = x W^T + b over row splits of `rows` rows:
+// part_w[s][o][i] = sum over the rows m of split s of dz[m][o] x[m][i], and
+// (part_b non-null) part_b[s][o] = sum over the same rows of dz[m][o] for o
+// < O, zero for O <= o < O4 = ceil4(O).  One thread per column: i < I the
+// weights (16 outputs per pass over the rows, dz read at row-uniform
+// addresses), I <= i < I + O4 the bias.  Rows are added in order.
+__global__ __launch_bounds__(256) void linear_wgrad_part_k(const float* __restrict__ dz, const float* __restrict__ x,
+                                                           float* __restrict__ part_w, float* __restrict__ part_b,
+                                                           int M, int I, int O, int rows) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    const int sp = blockIdx.y;
+    const int m0 = sp * rows, m1 = min(M, m0 + rows);
+    const int O4 = (O + 3) & ~3;
+    if (i < I) {
+        for (int o0 = 0; o0 < O; o0 += 16) {
+            float a[16];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) a[j] = 0.f;
+            for (int m = m0; m < m1; ++m) {
+                const float xv = x[(long)m * I + i];
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    if (o0 + j < O) a[j] += dz[(long)m * O + o0 + j] * xv;
+            }
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+                if (o0 + j < O) part_w[((long)sp * O + o0 + j) * I + i] = a[j];
+        }
+    } else if (part_b && i < I + O4) {
+        const int o = i - I;
+        float a = 0.f;
+        if (o < O)
+            for (int m = m0; m < m1; ++m) a += dz[(long)m * O + o];
+        part_b[(long)sp * O4 + o] = a;
+    }
 }
 
 // gW[o][i] = sum_n dz[n][o] x[n][i]; gb[o] = sum_n dz[n][o]
@@ -941,8 +1066,28 @@ __global__ void loss_mean_k(const float* __restrict__ loss_per, int Nb, float* _
 }
 
 hipError_t launch_linear_fwd(const float* x, const float* W, const float* b, float* y, int Nb, int I, int O,
-                             hipStream_t st) {
-    launch(linear_fwd_k, dim3(nblocks((long)Nb * O, 256)), dim3(256), 0, st, x, W, b, y, Nb, I, O);
+                             hipStream_t st, bool relu) {
+    const dim3 grid((unsigned)((Nb + 15) / 16));
+    if (I % 4 == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)W & 15) == 0)
+        launch(linear_fwd_k<true>, grid, dim3(256), 0, st, x, W, b, y, Nb, I, O, (int)relu);
+    else
+        launch(linear_fwd_k<false>, grid, dim3(256), 0, st, x, W, b, y, Nb, I, O, (int)relu);
+    return hipGetLastError();
+}
+int linear_wgrad_rows(long M) {
+    long r = (M + kLinWgMaxSplits - 1) / kLinWgMaxSplits;
+    return (int)(r < 32 ? 32 : r);
+}
+int linear_wgrad_splits(long M) {
+    const long r = linear_wgrad_rows(M);
+    return (int)((M + r - 1) / r);
+}
+hipError_t launch_linear_wgrad_part(const float* dz, const float* x, float* part_w, float* part_b, int M, int I,
+                                    int O, hipStream_t st) {
+    if (M < 1 || I < 1 || O < 1) return hipErrorInvalidValue;
+    const int O4 = (O + 3) & ~3;
+    const dim3 grid((unsigned)((I + (part_b ? O4 : 0) + 255) / 256), (unsigned)linear_wgrad_splits(M));
+    launch(linear_wgrad_part_k, grid, dim3(256), 0, st, dz, x, part_w, part_b, M, I, O, linear_wgrad_rows(M));
     return hipGetLastError();
 }
 hipError_t launch_linear_bwd_w(const float* dz, const float* x, float* gW, float* gb, int Nb, int I, int O,

@@ -93,7 +93,7 @@ struct Group {
     int bn2 = -1;       // G_BNACT: BN of the other branch of the residual add (both normalised)
     int add = -1;       // G_BNACT / G_CONV: the residual add, if any
     int res = -1;       // G_BNACT / G_CONV: the residual tensor added unnormalised, if any
-    int relu = -1;      // G_BNACT: the closing ReLU, if any
+    int relu = -1;      // G_BNACT: the closing ReLU, if any; G_CONV: a ReLU applied by the conv's epilogue
     int lin = -1;       // G_HEAD: the linear layer
     bool fold = false;  // G_BNACT: BN + ReLU folded into the consuming conv (nothing launched forward)
     bool rsum = false;  // G_BNACT (folded): its backward sums come from the consuming conv's data gradient
@@ -113,6 +113,7 @@ struct Model {
     std::vector<Group> groups;    // in execution order
     std::vector<char> stored;     // layer output materialised
     std::vector<char> gstored;    // gradient at the layer output materialised (when the backward reaches it)
+    std::vector<int> gbuf;        // the layer whose gradient buffer holds it
     std::vector<int> stats_from;  // BN: conv whose epilogue computes its statistics, or -1
 };
 
@@ -436,13 +437,40 @@ void build_groups(Model& M, bool fused) {
             if (!drop[i]) kept.push_back(gs[i]);
         gs.swap(kept);
     }
+    // fp32: a conv whose only consumer is a ReLU stores max(y, 0) from its
+    // epilogue (the ReLU's output; the conv's own is never stored); the
+    // backward masks the ReLU's output gradient in place, which then holds
+    // the conv's
+    if (fused && M.dt == lpp::DT_F32) {
+        std::vector<int> group_of(n, -1);
+        for (int i = 0; i < (int)gs.size(); ++i) group_of[gs[i].out] = i;
+        std::vector<char> drop(gs.size(), 0);
+        for (auto& g : gs) {
+            if (g.kind != G_CONV || g.stats_bn >= 0 || g.add >= 0) continue;
+            const int r = sole(g.a);
+            if (r < 0 || op(r) != LPP_RELU || group_of[r] < 0 || gs[group_of[r]].kind != G_RELU) continue;
+            drop[group_of[r]] = 1;
+            g.relu = g.out = r;
+        }
+        std::vector<Group> kept;
+        for (int i = 0; i < (int)gs.size(); ++i)
+            if (!drop[i]) kept.push_back(gs[i]);
+        gs.swap(kept);
+    }
     // a group runs when its last layer's inputs exist: order by output layer
     std::stable_sort(gs.begin(), gs.end(), [](const Group& x, const Group& y) { return x.out < y.out; });
     M.groups = gs;
     M.gstored.assign(M.layers.size(), 0);
+    M.gbuf.resize(M.layers.size());
+    for (int l = 0; l < n; ++l) M.gbuf[l] = l;
     for (auto& g : M.groups) {
         M.stored[g.out] = 1;
         M.gstored[g.out] = 1;
+        if (g.kind == G_CONV && g.relu >= 0) {
+            M.gstored[g.out] = 0;
+            M.gstored[g.a] = 1;
+            M.gbuf[g.a] = g.out;
+        }
         // the pooled features, kept for the weight gradient; their gradient
         // goes straight to the pool's input
         if (g.kind == G_HEAD) M.stored[g.a] = 1;
@@ -723,8 +751,8 @@ int run_forward(lpp_ctx* c, Worker& w) {
             const lpp::BnSums* sp = G.stats_bn >= 0 ? &sums : nullptr;
             if (Y.pw)
                 LAUNCH("conv_fwd", 2.0 * Y.macs, st,
-                       lpp::launch_linear_fwd((const float*)x0, w.v + Y.poff, bias, (float*)c->act(w, G.a), Mrows,
-                                              Y.L.cin, Y.L.cout, st));
+                       lpp::launch_linear_fwd((const float*)x0, w.v + Y.poff, bias, (float*)c->act(w, G.out), Mrows,
+                                              Y.L.cin, Y.L.cout, st, G.relu >= 0));
             else if (bf)
                 LAUNCH("conv_fwd", 2.0 * Y.macs, st,
                        lpp::launch_conv_bf16(lpp::CONV_FWD, (const uint16_t*)x0, (const uint16_t*)c->wf(w, Y), bias,
@@ -733,7 +761,8 @@ int run_forward(lpp_ctx* c, Worker& w) {
             else
                 LAUNCH("conv_fwd", 2.0 * Y.macs, st,
                        lpp::launch_conv_igemm(lpp::CONV_FWD, (const float*)x0, (const float*)c->wf(w, Y), bias,
-                                              (float*)c->act(w, G.a), g, false, sp, st,
+                                              (float*)c->act(w, G.out), g,
+                                              G.relu >= 0 ? lpp::kStoreRelu : lpp::kStoreSet, sp, st,
                                               Y.in_bn >= 0 ? &ib : nullptr));
             if (G.stats_bn >= 0 && c->fixed_order) {
                 const Layer& B = M.layers[G.stats_bn];
@@ -864,12 +893,38 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
         const long Min = (long)N * Y.in0.h * Y.in0.w;
         switch (G.kind) {
         case G_CONV: {
+            // a fused ReLU: its output gradient masked in place into the
+            // conv's (with the bias gradient's column sums on the way)
+            const long Mo = (long)N * Y.out.h * Y.out.w;
+            const bool bias_fused = G.relu >= 0 && !Y.pw && Y.L.bias && pl.wgrad[G.a];
+            if (bias_fused) {
+                LAUNCH("relu", 3.0 * eb * Mo * Y.out.c, st,
+                       lpp::launch_relu_mask_colsum(dt, dy, c->act(w, G.out), Mo, Y.L.cout, w.ps0, st));
+                LAUNCH("bias_grad", 0.0, st,
+                       lpp::launch_sum_from_tiles(w.ps0, lpp::stats_tiles(Mo, Y.L.cout), lpp::stats_rows(Mo, Y.L.cout),
+                                                  Mo, Y.L.cout, w.g + Y.poff + Y.wcount, st));
+            } else if (G.relu >= 0) {
+                LAUNCH("relu", 3.0 * eb * Mo * Y.out.c, st,
+                       lpp::launch_relu_bwd(dt, dy, c->act(w, G.out), dy, Mo * Y.out.c, false, st));
+            }
             if (Y.pw) {
-                if (pl.wgrad[G.a])
+                if (pl.wgrad[G.a]) {
+                    const int S = Y.wg.splits, O = Y.L.cout, I = Y.L.cin, O4 = ceil4(O);
+                    const long pwf = align64((long)S * O * I);
+                    if (red.n + 2 > lpp::kWgRedMaxJobs || woff + align64(Y.wg.part_floats) > c->wpart_floats) {
+                        int rc = flush_reduce();
+                        if (rc) return rc;
+                    }
+                    float* part = w.wpart + woff;
+                    float* partb = Y.L.bias ? part + pwf : nullptr;
+                    if (!lpp::wgred_add(red, part, S, O, I, I, I, 1, 1, w.g + Y.poff) ||
+                        (partb && !lpp::wgred_add(red, partb, S, 1, O4, O, O4, 1, 1, w.g + Y.poff + Y.wcount)))
+                        return fail(LPP_EINVAL, "weight-gradient reduce: unsupported shape");
+                    woff += align64(Y.wg.part_floats);
                     LAUNCH("conv_wgrad", 2.0 * Y.macs, st,
-                           lpp::launch_linear_bwd_w((const float*)dy, (const float*)x0, w.g + Y.poff,
-                                                    Y.L.bias ? w.g + Y.poff + Y.wcount : nullptr, (int)Min, Y.L.cin,
-                                                    Y.L.cout, st));
+                           lpp::launch_linear_wgrad_part((const float*)dy, (const float*)x0, part, partb, (int)Min,
+                                                         I, O, st));
+                }
                 if (dx0)
                     LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
                            lpp::launch_linear_bwd_x((const float*)dy, w.v + Y.poff, (float*)dx0, (int)Min, Y.L.cin,
@@ -905,9 +960,8 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                            lpp::launch_conv_wgrad((const float*)dy, (const float*)x0, part, N, Y.in0.h, Y.in0.w,
                                                   Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
                                                   Y.L.pad, Y.wg, st));
-                if (Y.L.bias) {
+                if (Y.L.bias && !bias_fused) {
                     // column sums of dY, from per-tile means
-                    const long Mo = (long)N * Y.out.h * Y.out.w;
                     const lpp::BnSums tiles{nullptr, w.ps0, w.ps1, nullptr};
                     LAUNCH("bias_grad", eb * Mo * Y.L.cout, st,
                            lpp::launch_stats_partial(dt, dy, Mo, Y.L.cout, tiles, st));
@@ -945,7 +999,6 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                 const lpp_layer& A = M.layers[G.add].L;
                 const bool want_res = A.in0 == G.res ? pl.din0[G.add] : pl.din1[G.add];
                 const bool acc_res = A.in0 == G.res ? pl.acc0[G.add] : pl.acc1[G.add];
-                const long Mo = (long)N * Y.out.h * Y.out.w;
                 if (want_res)
                     LAUNCH("add", 2.0 * eb * Mo * Y.out.c, st,
                            lpp::launch_copy_acc(dt, dy, c->dact(w, G.res), Mo * Y.out.c, acc_res, st));
@@ -1171,6 +1224,14 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
     std::vector<lpp::SnapConvDesc> snaps;
     long wf = 0;
     for (auto& Y : M.layers) {
+        if (Y.L.op == LPP_CONV && Y.pw) {
+            // weight (and bias) gradient partials over row splits
+            const long rows = (long)N * Y.in0.h * Y.in0.w;
+            Y.wg = lpp::WgradPlan{};
+            Y.wg.splits = lpp::linear_wgrad_splits(rows);
+            Y.wg.part_floats = align64((long)Y.wg.splits * Y.L.cout * Y.L.cin) +
+                               (Y.L.bias ? align64((long)Y.wg.splits * ceil4(Y.L.cout)) : 0);
+        }
         if (Y.L.op != LPP_CONV || Y.pw) continue;
         const long nf = (long)Y.L.cout * Y.L.k * Y.L.k * Y.cin_p;
         const long nd = (long)Y.L.cin * Y.L.k * Y.L.k * Y.L.cout;
@@ -1232,6 +1293,10 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
                                        Y.L.stride, Y.L.pad};
                 ps = std::max<long>(ps, (long)lpp::conv_dgrad_sum_tiles(gd) * Y.L.cin);
             }
+            wpart = std::max<long>(wpart, align64(Y.wg.part_floats));
+            wsum += align64(Y.wg.part_floats);
+        }
+        if (Y.L.op == LPP_CONV && Y.pw) {
             wpart = std::max<long>(wpart, align64(Y.wg.part_floats));
             wsum += align64(Y.wg.part_floats);
         }
@@ -1510,10 +1575,10 @@ static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* 
                 G = &g;
                 relu_out = true;
             }
-    if (!M.stored[layer]) {
+    if (!grad && !M.stored[layer]) {
         for (const Group& g : M.groups)
             if (g.kind == G_BNACT && (layer == g.a || layer == g.add || layer == g.bn2)) G = &g;
-        if (grad || !G) return fail(LPP_ESTATE, "this layer's output is fused away (create the context with unfused = 1)");
+        if (!G) return fail(LPP_ESTATE, "this layer's output is fused away (create the context with unfused = 1)");
     }
     if (grad && !M.gstored[layer]) return fail(LPP_ESTATE, "this layer's gradient is fused away");
     if (grad && (w.last_partition < 0 || !M.plans[w.last_partition].run[layer]))
@@ -1523,7 +1588,7 @@ static int copy_layer_nchw(lpp_ctx* c, int worker, int layer, bool grad, float* 
     float* tmp = nullptr;
     if (hipMalloc((void**)&tmp, sizeof(float) * n * (G ? 2 : 1)) != hipSuccess)
         return fail(LPP_ENOMEM, "temporary allocation");
-    const void* src = grad ? c->dact(w, layer) : nullptr;
+    const void* src = grad ? c->dact(w, M.gbuf[layer]) : nullptr;
     hipError_t e = hipSuccess;
     if (G) {
         const int C = Y.out.c;

@@ -93,11 +93,17 @@ def test_conv_passes(case):
     x, img, lab = grid_conv_inputs(o, 11, n)
     loss, logits, _ = R.forward_backward(o, x, img, lab)
     g, sc = R.grad_scale(o, x, img, lab)
-    with lpp.Context(p, K=1, batch=n) as ctx:
+    with lpp.Context(p, K=1, batch=n, unfused=True) as ctx:
         ctx.set_params(x)
         ctx.step(0, *dev(img, lab), 0, 0.0)
         ref0 = R.activation(o, x, img, 0)
         assert np.array_equal(ctx.get_activation(0, 0, ref0.shape[1:]), ref0)   # exact by construction
+    with lpp.Context(p, K=1, batch=n) as ctx:
+        # (the first conv's epilogue applies the ReLU: its output is stored
+        # clipped, still exact)
+        ctx.set_params(x)
+        ctx.step(0, *dev(img, lab), 0, 0.0)
+        assert np.array_equal(ctx.get_activation(0, 1, ref0.shape[1:]), np.maximum(ref0, 0))
         ref2 = R.activation(o, x, img, 2)
         assert T.relerr(ctx.get_activation(0, 2, ref2.shape[1:]), ref2, T.TAU_LOGITS) < T.TOL_LOGITS
         assert T.relerr(ctx.get_logits(0), logits, T.TAU_LOGITS) < T.TOL_LOGITS
@@ -507,19 +513,34 @@ def _teacher_forced_convs_f32(o, ctx, x, img, rng, samples=64):
     recomputed in fp64 from the GPU's stored input and the fp32 weights, and
     sampled weight- and bias-gradient entries from the GPU's stored input and
     output gradient.  Bound: fp32 accumulation, a few units of 2^-24 of the
-    terms' magnitude sum (1e-5 of it, with 1e-6 of the value).  Returns the
-    worst normalised errors (forward, parameter gradient)."""
+    terms' magnitude sum (1e-5 of it, with 1e-6 of the value).  A conv whose
+    ReLU its epilogue applies (its own output never stored) is checked
+    through the ReLU's output against max(0, ref), within the same bound
+    since max(0, .) does not increase distances; its gradient is the
+    ReLU's output gradient masked by the stored output.  Returns the worst
+    normalised errors (forward, parameter gradient) and the number of convs
+    checked through a fused ReLU."""
     shapes = R.shapes(o)
     n = img.shape[0]
     xw = x.astype(np.float64)
     gvec = ctx.get_grad(0).astype(np.float64)
     worst_f = worst_w = 0.0
+    fused = 0
     for li, rec in enumerate(o.layers):
         if rec["op"] != OM.CONV:
             continue
         src = img.astype(np.float64) if rec["in0"] < 0 else \
             ctx.get_activation(0, rec["in0"], shapes[rec["in0"]]).astype(np.float64)
-        out = ctx.get_activation(0, li, shapes[li]).astype(np.float64)
+        relu_out = False
+        try:
+            out = ctx.get_activation(0, li, shapes[li]).astype(np.float64)
+        except lpp.LppError as e:
+            assert e.code == lpp.ESTATE
+            users = [j for j, r in enumerate(o.layers) if r["in0"] == li or r.get("in1") == li]
+            assert len(users) == 1 and o.layers[users[0]]["op"] == OM.RELU, (li, users)
+            out = ctx.get_activation(0, users[0], shapes[li]).astype(np.float64)
+            relu_out = True
+            fused += 1
         dout = ctx.get_activation_grad(0, li, shapes[li]).astype(np.float64)
         k, s, pd, cin, cout = rec["k"], rec["stride"], rec["pad"], rec["cin"], rec["cout"]
         nw = cout * cin * k * k
@@ -532,6 +553,8 @@ def _teacher_forced_convs_f32(o, ctx, x, img, rng, samples=64):
             terms = xp[b, :, i * s:i * s + k, j * s:j * s + k] * W[co]
             ref = float(terms.sum()) + bias[co]
             scale = float(np.abs(terms).sum()) + abs(bias[co]) + 1e-30
+            if relu_out:
+                ref = max(ref, 0.0)
             worst_f = max(worst_f, abs(out[b, co, i, j] - ref) / (1e-6 * abs(ref) + 1e-5 * scale))
         gW = gvec[rec["poff"]:rec["poff"] + nw].reshape(cout, cin, k, k)
         for _ in range(samples // 4):
@@ -544,7 +567,10 @@ def _teacher_forced_convs_f32(o, ctx, x, img, rng, samples=64):
             ref = dout.sum(axis=(0, 2, 3))
             scale = np.abs(dout).sum(axis=(0, 2, 3)) + 1e-30
             worst_w = max(worst_w, float(np.max(np.abs(gb - ref) / (1e-6 * np.abs(ref) + 1e-5 * scale))))
-    return worst_f, worst_w
+        if relu_out:
+            # the gradient at the conv output is zero wherever the ReLU clipped
+            assert not np.any(dout[out <= 0.0]), li
+    return worst_f, worst_w, fused
 
 
 @pytest.mark.parametrize("n_classes", [10, 100])
@@ -567,9 +593,11 @@ def test_full_size_squeezenet(n_classes):
         ti, tl = dev(img, lab)
         ctx.step(0, ti, tl, 0, 0.0)
         assert T.relerr(ctx.get_logits(0), logits, T.TAU_LOGITS) < T.TOL_LOGITS
-        wf, ww = _teacher_forced_convs_f32(o, ctx, x, img, np.random.default_rng(9))
-        say("squeezenet", n_classes, "teacher-forced: forward %.3f, gradient %.3f (bar 1)" % (wf, ww))
+        wf, ww, nf = _teacher_forced_convs_f32(o, ctx, x, img, np.random.default_rng(9))
+        say("squeezenet", n_classes, "teacher-forced: forward %.3f, gradient %.3f (bar 1); %d convs with a fused ReLU"
+            % (wf, ww, nf))
         assert wf < 1.0 and ww < 1.0
+        assert nf == 26      # the stem, 3 per Fire module, the classifier
         g = ctx.get_grad(0)
         for part in range(1, 5):
             ctx.step(part - 1, ti, tl, part, 0.0)
