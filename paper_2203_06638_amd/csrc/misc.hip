@@ -812,47 +812,110 @@ hipError_t launch_concat_bwd(int dt, const void* dy, long rows, int ca, int cb, 
 // ------------------------------------------------------------------------
 
 // arg holds the winning tap r*k + s (first maximum in row-major scan order)
-template <class T>
-__global__ void maxpool_fwd_k(const T* __restrict__ x, T* __restrict__ y, uint8_t* __restrict__ arg,
-                              int Nb, int H, int W, int C, int Ho, int Wo, int k, int st, int pad) {
-    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    const long total = (long)Nb * Ho * Wo * C;
-    if (idx >= total) return;
-    const int c = (int)(idx % C);
-    long t = idx / C;
-    const int q = (int)(t % Wo);
+// VW consecutive channels as floats (16 bytes for VW = 16 / sizeof(T)) and back
+template <int VW>
+__device__ __forceinline__ void ldv(const float* p, float* v) {
+    if constexpr (VW == 4) {
+        const f4 t = *(const f4*)p;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = t[e];
+    } else {
+        v[0] = *p;
+    }
+}
+template <int VW>
+__device__ __forceinline__ void ldv(const bf16* p, float* v) {
+    if constexpr (VW == 8) {
+        const uint4 t = *(const uint4*)p;
+        const uint32_t w[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[2 * e] = __uint_as_float(w[e] << 16);
+            v[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+        }
+    } else {
+        v[0] = from_bf16(*p);
+    }
+}
+template <int VW>
+__device__ __forceinline__ void stv(float* p, const float* v) {
+    if constexpr (VW == 4) st16(p, v);
+    else *p = v[0];
+}
+template <int VW>
+__device__ __forceinline__ void stv(bf16* p, const float* v) {
+    if constexpr (VW == 8) st16(p, v);
+    else *p = to_bf16(v[0]);
+}
+
+// Max pool, one thread per VW consecutive channels of one output pixel
+// (16-byte loads and stores; VW = 1 when C is not a multiple of the vector):
+// the window's largest value, the first in (r, s) order among equals, and
+// its tap r*k + s as a byte per channel.
+template <class T, int VW>
+__global__ __launch_bounds__(256) void maxpool_fwd_k(const T* __restrict__ x, T* __restrict__ y,
+                                                     uint8_t* __restrict__ arg, int Nb, int H, int W, int C, int Ho,
+                                                     int Wo, int k, int st, int pad) {
+    const int CV = C / VW;
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (idx >= Nb * Ho * Wo * CV) return;
+    const int cv = idx % CV;
+    int t = idx / CV;
+    const int q = t % Wo;
     t /= Wo;
-    const int p = (int)(t % Ho);
-    const int n = (int)(t / Ho);
-    float m = -INFINITY;
-    int am = 0;
+    const int p = t % Ho, n = t / Ho;
+    float m[VW];
+    int am[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        m[e] = -INFINITY;
+        am[e] = 0;
+    }
     for (int r = 0; r < k; ++r) {
         const int hi = p * st - pad + r;
         if (hi < 0 || hi >= H) continue;
         for (int s = 0; s < k; ++s) {
             const int wi = q * st - pad + s;
             if (wi < 0 || wi >= W) continue;
-            const float v = ld1(x, (((long)n * H + hi) * W + wi) * C + c);
-            if (v > m) { m = v; am = r * k + s; }
+            float v[VW];
+            ldv<VW>(x + (((long)n * H + hi) * W + wi) * C + cv * VW, v);
+#pragma unroll
+            for (int e = 0; e < VW; ++e)
+                if (v[e] > m[e]) {
+                    m[e] = v[e];
+                    am[e] = r * k + s;
+                }
         }
     }
-    st1(y, idx, m);
-    arg[idx] = (uint8_t)am;
+    stv<VW>(y + (long)idx * VW, m);
+    if constexpr (VW == 8) {
+        *(uint2*)(arg + (long)idx * 8) = uint2{(uint32_t)(am[0] | am[1] << 8 | am[2] << 16 | am[3] << 24),
+                                               (uint32_t)(am[4] | am[5] << 8 | am[6] << 16 | am[7] << 24)};
+    } else if constexpr (VW == 4) {
+        *(uint32_t*)(arg + (long)idx * 4) = (uint32_t)(am[0] | am[1] << 8 | am[2] << 16 | am[3] << 24);
+    } else {
+        arg[idx] = (uint8_t)am[0];
+    }
 }
 
-template <class T>
-__global__ void maxpool_bwd_k(const T* __restrict__ dy, const uint8_t* __restrict__ arg, T* __restrict__ dx,
-                              int Nb, int H, int W, int C, int Ho, int Wo, int k, int st, int pad, int acc) {
-    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    const long total = (long)Nb * H * W * C;
-    if (idx >= total) return;
-    const int c = (int)(idx % C);
-    long t = idx / C;
-    const int w = (int)(t % W);
+// Gradient of the max pool, one thread per VW consecutive channels of one
+// input pixel: the sum, over the windows that contain the pixel (in (p, q)
+// order), of the output gradient of those whose recorded tap is this pixel.
+template <class T, int VW>
+__global__ __launch_bounds__(256) void maxpool_bwd_k(const T* __restrict__ dy, const uint8_t* __restrict__ arg,
+                                                     T* __restrict__ dx, int Nb, int H, int W, int C, int Ho, int Wo,
+                                                     int k, int st, int pad, int acc) {
+    const int CV = C / VW;
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (idx >= Nb * H * W * CV) return;
+    const int cv = idx % CV;
+    int t = idx / CV;
+    const int w = t % W;
     t /= W;
-    const int h = (int)(t % H);
-    const int n = (int)(t / H);
-    float s = 0.f;
+    const int h = t % H, n = t / H;
+    float s[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) s[e] = 0.f;
     // windows p with p*st - pad <= h <= p*st - pad + k - 1
     const int p_lo = max(0, (h + pad - k + st) / st), p_hi = min(Ho - 1, (h + pad) / st);
     const int q_lo = max(0, (w + pad - k + st) / st), q_hi = min(Wo - 1, (w + pad) / st);
@@ -860,10 +923,40 @@ __global__ void maxpool_bwd_k(const T* __restrict__ dy, const uint8_t* __restric
         for (int q = q_lo; q <= q_hi; ++q) {
             const int r = h - (p * st - pad), ss = w - (q * st - pad);
             if (r < 0 || r >= k || ss < 0 || ss >= k) continue;
-            const long o = (((long)n * Ho + p) * Wo + q) * C + c;
-            if (arg[o] == r * k + ss) s += ld1(dy, o);
+            const int tap = r * k + ss;
+            const long o = (((long)n * Ho + p) * Wo + q) * C + cv * VW;
+            uint8_t a[VW];
+            if constexpr (VW == 8) {
+                const uint2 u = *(const uint2*)(arg + o);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    a[e] = (uint8_t)(u.x >> (8 * e));
+                    a[4 + e] = (uint8_t)(u.y >> (8 * e));
+                }
+            } else if constexpr (VW == 4) {
+                const uint32_t u = *(const uint32_t*)(arg + o);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) a[e] = (uint8_t)(u >> (8 * e));
+            } else {
+                a[0] = arg[o];
+            }
+            bool any = false;
+#pragma unroll
+            for (int e = 0; e < VW; ++e) any |= a[e] == tap;
+            if (!any) continue;
+            float g[VW];
+            ldv<VW>(dy + o, g);
+#pragma unroll
+            for (int e = 0; e < VW; ++e)
+                if (a[e] == tap) s[e] += g[e];
         }
-    st1(dx, idx, acc ? ld1(dx, idx) + s : s);
+    if (acc) {
+        float d[VW];
+        ldv<VW>(dx + (long)idx * VW, d);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) s[e] = d[e] + s[e];
+    }
+    stv<VW>(dx + (long)idx * VW, s);
 }
 
 template <class T>
@@ -888,24 +981,44 @@ __global__ void gap_bwd_k(const float* __restrict__ dy, T* __restrict__ dx, int 
 
 hipError_t launch_maxpool_fwd(int dt, const void* x, void* y, uint8_t* arg, int Nb, int H, int W, int C, int Ho,
                               int Wo, int k, int stride, int pad, hipStream_t st) {
-    const dim3 grid(nblocks((long)Nb * Ho * Wo * C, 256));
-    if (dt == DT_BF16)
-        launch(maxpool_fwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)x, (bf16*)y, arg, Nb, H, W, C,
-                           Ho, Wo, k, stride, pad);
-    else
-        launch(maxpool_fwd_k<float>, grid, dim3(256), 0, st, (const float*)x, (float*)y, arg, Nb, H, W, C,
-                           Ho, Wo, k, stride, pad);
+    const long total = (long)Nb * Ho * Wo * C;
+    if (total >= 0x7fffffffL || (long)Nb * H * W * C >= 0x7fffffffL) return hipErrorInvalidValue;
+    if (dt == DT_BF16) {
+        if (C % 8 == 0)
+            launch(maxpool_fwd_k<bf16, 8>, dim3(nblocks(total / 8, 256)), dim3(256), 0, st, (const bf16*)x, (bf16*)y,
+                   arg, Nb, H, W, C, Ho, Wo, k, stride, pad);
+        else
+            launch(maxpool_fwd_k<bf16, 1>, dim3(nblocks(total, 256)), dim3(256), 0, st, (const bf16*)x, (bf16*)y,
+                   arg, Nb, H, W, C, Ho, Wo, k, stride, pad);
+    } else {
+        if (C % 4 == 0)
+            launch(maxpool_fwd_k<float, 4>, dim3(nblocks(total / 4, 256)), dim3(256), 0, st, (const float*)x,
+                   (float*)y, arg, Nb, H, W, C, Ho, Wo, k, stride, pad);
+        else
+            launch(maxpool_fwd_k<float, 1>, dim3(nblocks(total, 256)), dim3(256), 0, st, (const float*)x,
+                   (float*)y, arg, Nb, H, W, C, Ho, Wo, k, stride, pad);
+    }
     return hipGetLastError();
 }
 hipError_t launch_maxpool_bwd(int dt, const void* dy, const uint8_t* arg, void* dx, int Nb, int H, int W, int C,
                               int Ho, int Wo, int k, int stride, int pad, bool accumulate, hipStream_t st) {
-    const dim3 grid(nblocks((long)Nb * H * W * C, 256));
-    if (dt == DT_BF16)
-        launch(maxpool_bwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)dy, arg, (bf16*)dx, Nb, H, W, C,
-                           Ho, Wo, k, stride, pad, (int)accumulate);
-    else
-        launch(maxpool_bwd_k<float>, grid, dim3(256), 0, st, (const float*)dy, arg, (float*)dx, Nb, H, W,
-                           C, Ho, Wo, k, stride, pad, (int)accumulate);
+    const long total = (long)Nb * H * W * C;
+    if (total >= 0x7fffffffL || (long)Nb * Ho * Wo * C >= 0x7fffffffL) return hipErrorInvalidValue;
+    if (dt == DT_BF16) {
+        if (C % 8 == 0)
+            launch(maxpool_bwd_k<bf16, 8>, dim3(nblocks(total / 8, 256)), dim3(256), 0, st, (const bf16*)dy, arg,
+                   (bf16*)dx, Nb, H, W, C, Ho, Wo, k, stride, pad, (int)accumulate);
+        else
+            launch(maxpool_bwd_k<bf16, 1>, dim3(nblocks(total, 256)), dim3(256), 0, st, (const bf16*)dy, arg,
+                   (bf16*)dx, Nb, H, W, C, Ho, Wo, k, stride, pad, (int)accumulate);
+    } else {
+        if (C % 4 == 0)
+            launch(maxpool_bwd_k<float, 4>, dim3(nblocks(total / 4, 256)), dim3(256), 0, st, (const float*)dy, arg,
+                   (float*)dx, Nb, H, W, C, Ho, Wo, k, stride, pad, (int)accumulate);
+        else
+            launch(maxpool_bwd_k<float, 1>, dim3(nblocks(total, 256)), dim3(256), 0, st, (const float*)dy, arg,
+                   (float*)dx, Nb, H, W, C, Ho, Wo, k, stride, pad, (int)accumulate);
+    }
     return hipGetLastError();
 }
 hipError_t launch_gap_fwd(int dt, const void* x, float* y, int Nb, int HW, int C, hipStream_t st) {

@@ -239,7 +239,7 @@ int build_model(const lpp_model_desc* desc, int P, Model& M) {
         Y.dt = (L.op == LPP_GAP || L.op == LPP_LINEAR) ? lpp::DT_F32 : M.dt;
         // tensors whose channels are not a multiple of 4 (a pointwise conv's
         // output) may only feed ReLU, pooling and linear layers
-        const bool any_c = L.op == LPP_LINEAR || L.op == LPP_GAP || L.op == LPP_RELU;
+        const bool any_c = L.op == LPP_LINEAR || L.op == LPP_GAP || L.op == LPP_RELU || L.op == LPP_MAXPOOL;
         if (o.c % 4 && !any_c && !Y.pw)
             return fail(LPP_EUNSUPPORTED, std::string(where) + "channel counts must be multiples of 4");
         if (L.in0 >= 0 && Y.in0.c % 4 && !any_c)

@@ -141,6 +141,38 @@ def test_maxpool_routing_exact_grid():
         check_grads(o, ctx.get_grad(0), g, scale=sc)
 
 
+def test_maxpool_on_channels_not_a_multiple_of_four():
+    """A max pool over 6 channels (the per-element path; every other pool
+    here reads whole 16-byte channel vectors): conv3x3 3->8 + ReLU, a 1x1
+    conv to 6 channels (the per-pixel linear path), max pool 3x3/2 pad 1,
+    global pool, linear.  Every partition against the oracle on a seed whose
+    pool decisions keep a margin."""
+    o = OM.Net("pool6", 3, 12, 12, 5)
+    a = o.relu(o.conv(-1, 3, 8, 3, 1, 1))
+    a = o.gap(o.maxpool(o.conv(a, 8, 6, 1, 1, 0), 3, 2, 1))
+    o.next_unit()
+    o.linear(a, 6, 5)
+    o.set_blocks([1, 2])
+    p = PM.Model("pool6", (3, 12, 12), 5)
+    y = p.relu(p.conv(-1, 8, 3))
+    y = p.gap(p.maxpool(p.conv(y, 6, 1, 1, 0), 3, 2, 1))
+    p.new_unit()
+    p.linear(y, 5)
+    p.assign_blocks([1, 2])
+    band = 1e-5
+
+    def make(seed):
+        return T.init_x(o.specs, seed).astype(np.float64), T.inputs(seed + 3, 6, o.in_shape, 5)[0]
+
+    seed, margin = T.well_posed_seed(o, make, seeds=range(3400, 3600), band=band)
+    say("pool6 seed", seed, "margin %.2e" % margin)
+    x = T.init_x(o.specs, seed)
+    img, lab = T.inputs(seed + 3, 6, o.in_shape, 5)
+    m0 = (np.random.default_rng(seed).standard_normal(o.d) * 1e-2).astype(np.float32)
+    for part in range(0, 3):
+        _partition_step(o, p, x, m0, img, lab, part, band=band)
+
+
 @pytest.mark.parametrize("unfused", [False, True], ids=["fused", "unfused"])
 def test_bn_residual_passes(unfused):
     o, p = T.twin_bn_net(16, 16, 8)
