@@ -84,29 +84,46 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t bf_rsrc(const void* p, long n)
 __device__ __forceinline__ void bf_dma16(__amdgpu_buffer_rsrc_t r, bf16* dst, unsigned voff) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, voff, 0, 0, 0);
 }
+// s_waitcnt immediate that waits for at most n outstanding vector memory
+// operations and leaves the other counters alone
+constexpr int bf_vmcnt(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+// waits until at most `ahead` K-steps of LPS loads each are in flight (ahead < NS - 1)
+template <int LPS, int NS>
+__device__ __forceinline__ void bf_wait_steps(int ahead) {
+    static_assert(NS >= 2 && NS <= 5 && (NS - 2) * LPS < 64, "pipeline depth");
+    if (NS > 4 && ahead >= 3) __builtin_amdgcn_s_waitcnt(bf_vmcnt(3 * LPS));
+    else if (NS > 3 && ahead == 2) __builtin_amdgcn_s_waitcnt(bf_vmcnt(2 * LPS));
+    else if (NS > 2 && ahead == 1) __builtin_amdgcn_s_waitcnt(bf_vmcnt(LPS));
+    else __builtin_amdgcn_s_waitcnt(bf_vmcnt(0));
+}
 
 // DMA (FASTK only): operand tiles go from memory straight into LDS (buffer
 // loads with the LDS bit: no register staging, no LDS store instructions;
 // taps in the zero padding and columns past the output read out of the
 // buffer's range, which yields zeros).  Each wave's load instruction fills
 // 1 KB of LDS in lane order, so a thread loads the 16-byte chunk its lane
-// position holds under the swizzle.  Per K-step: all fragments are read
-// from the current buffer, then the next K-step's loads are issued into the
-// other buffer, then the MFMAs run; the barrier at the step's end waits for
-// the loads.
-template <int BM, int BN, bool STATS, bool FASTK, int KH, bool DMA>
+// position holds under the swizzle.  NS buffers form a pipeline: the loads
+// of K-steps k+1 .. k+NS-2 are in flight while step k's fragments are read
+// and its MFMAs run.  At the top of step k each thread waits (vmcnt) until at
+// most the later steps' loads are outstanding -- its own loads of step k have
+// then landed -- and a plain barrier (no fence, which would wait for every
+// load in flight) makes everyone's landed; step k + NS - 1's loads go into
+// the buffer step k - 1 used, which every wave finished reading before that
+// barrier.
+template <int BM, int BN, bool STATS, bool FASTK, int KH, bool DMA, int NS = 2>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ? 2 : 1, 8))) void conv_bf16_k(const bf16* __restrict__ src, const bf16* __restrict__ B,
                                                    const float* __restrict__ bias, bf16* __restrict__ Y,
                                                    const bf16* __restrict__ res, ConvGeom g, BfPass ps, int accumulate,
                                                    BnSums sums) {
     static_assert(!DMA || FASTK, "DMA operand loads need 32-channel load steps");
+    static_assert(NS == 2 || DMA, "deeper pipelines use DMA operand loads");
     constexpr int TM = BM / 32, TN = BN / 32;     // 16x16 blocks per wave; waves 2 x 2
     constexpr int AL = BM / 64, BL = BN / 64;     // 16-byte operand loads per thread per K-step
     constexpr int P = kBfPitch;
     constexpr int HALF = (BM + BN) * P;           // one load step's A and B tiles
     constexpr int STAGE = KH * HALF;
     constexpr int OP = BN + 8;
-    constexpr int LDSN = BM * OP > 2 * STAGE ? BM * OP : 2 * STAGE;   // the epilogue tile reuses the space
+    constexpr int LDSN = BM * OP > NS * STAGE ? BM * OP : NS * STAGE;   // the epilogue tile reuses the space
     __shared__ __attribute__((aligned(16))) bf16 lds[LDSN];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave & 1, wn = wave >> 1;
@@ -244,10 +261,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
                 }
             }
         };
-        if (nk > 0) issue(0, 0);
-        __syncthreads();
+        constexpr int LPS = KH * (AL + BL);       // loads per K-step per thread
+#pragma unroll
+        for (int kk = 0; kk < NS - 1; ++kk)
+            if (kk < nk) issue(kk, kk);
+        int cur = 0, nxt = NS - 1;                // buffers of step kk and step kk + NS - 1
         for (int kk = 0; kk < nk; ++kk) {
-            const int cur = kk & 1;
+            bf_wait_steps<LPS, NS>(min(NS - 2, nk - 1 - kk));
+            asm volatile("s_barrier" ::: "memory");
             bf8 a[KH][TM], b[KH][TN];
 #pragma unroll
             for (int h = 0; h < KH; ++h) {
@@ -257,15 +278,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
 #pragma unroll
                 for (int y = 0; y < TN; ++y) b[h][y] = *(const bf8*)(base + b_rd + y * 16 * P);
             }
-            if (kk + 1 < nk) issue(cur ^ 1, kk + 1);
+            if (kk + NS - 1 < nk) issue(nxt, kk + NS - 1);
 #pragma unroll
             for (int h = 0; h < KH; ++h)
 #pragma unroll
                 for (int x = 0; x < TM; ++x)
 #pragma unroll
                     for (int y = 0; y < TN; ++y) acc[x][y] = mfma_bf16(a[h][x], b[h][y], acc[x][y]);
-            __syncthreads();
+            cur = cur + 1 == NS ? 0 : cur + 1;
+            nxt = nxt + 1 == NS ? 0 : nxt + 1;
         }
+        __syncthreads();                          // every wave is done with the buffers (the epilogue reuses them)
     } else {
     if (nk > 0) {
         load_k(0);
@@ -461,16 +484,11 @@ static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* 
     if (Mv == 0) return hipSuccess;
     dim3 grid((unsigned)((Mv + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
     const BnSums sm = stats ? *stats : BnSums{};
-    // two load steps per K-step (one barrier per 64 channels) for wide sources
-    if (BM == 256 && g.Cs % 32 == 0) {
-        if (stats) launch((conv_bf16_k<BM, BN, true, true, 1, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, true, 1, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-    } else if (g.Cs >= 128 && g.Cs % 32 == 0) {
-        if (stats) launch((conv_bf16_k<BM, BN, true, true, 2, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, true, 2, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-    } else if (g.Cs % 32 == 0) {
-        if (stats) launch((conv_bf16_k<BM, BN, true, true, 1, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, true, 1, true>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+    // 32-channel load steps straight into LDS, NS of them in flight
+    if (g.Cs % 32 == 0) {
+        constexpr int NSD = BM == 256 ? 3 : 4;
+        if (stats) launch((conv_bf16_k<BM, BN, true, true, 1, true, NSD>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+        else launch((conv_bf16_k<BM, BN, false, true, 1, true, NSD>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
     } else {
         if (stats) launch((conv_bf16_k<BM, BN, true, false, 1, false>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
         else launch((conv_bf16_k<BM, BN, false, false, 1, false>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
