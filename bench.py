@@ -303,8 +303,9 @@ def run_workload(torch, lpp, name, steps, B=128, P=4):
     mean_flops = info.fwd_flops + sum(info.bwd_flops[i] for i in range(1, P + 1)) / P
     conv = {f: round(fams[f][2] / (fams[f][0] / 1e3) / 1e12, 1) for f in ("conv_fwd", "conv_dgrad", "conv_wgrad")
             if fams[f][0] > 0}
-    hbm = {f: round(fams[f][2] / (fams[f][0] / 1e3) / 1e9, 1) for f in ("snapshot", "sgd_update")
-           if fams[f][0] > 0}
+    hbm = {f: round(fams[f][2] / (fams[f][0] / 1e3) / 1e9, 1)
+           for f in ("snapshot", "sgd_update", "bn_act", "bn_bwd", "maxpool", "relu", "add", "concat", "image")
+           if f in fams and fams[f][0] > 0 and fams[f][2] > 0}
     return {"workload": desc, "dtype": "bf16" if dtype == lpp.BF16 else "f32", "value": round(B * steps / dt, 1),
             "unit": "samples/s", "steps": steps, "ms_per_step": round(dt / steps * 1e3, 4),
             "mean_step_gflop": round(mean_flops / 1e9, 2), "model_tflops": round(mean_flops * steps / dt / 1e12, 2),

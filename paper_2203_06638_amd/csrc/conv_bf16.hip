@@ -57,6 +57,16 @@ __device__ __forceinline__ f4 mfma_bf16(bf8 a, bf8 b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Division of pixel indices by a grid dimension d without 64-bit or
+// iterative arithmetic: n / d == umulhi(n, ceil(2^32 / d)) exactly when n * d
+// < 2^32, which the launchers check for every index a kernel divides
+// (largest pixel index times the divisor); magic 0 means d == 1.
+__host__ __device__ inline unsigned bf_magic(unsigned d) {
+    return d <= 1 ? 0u : (unsigned)((0x100000000ull + d - 1) / d);
+}
+__device__ __forceinline__ unsigned bf_div(unsigned n, unsigned magic) { return magic ? __umulhi(n, magic) : n; }
+static inline bool bf_div_exact(long nmax, long d) { return d >= 1 && nmax >= 0 && (nmax + 1) * d <= 0x100000000L; }
+
 // One pass of the implicit GEMM (see the header comment).
 struct BfPass {
     int Hv, Wv;              // output grid of the pass
@@ -65,6 +75,7 @@ struct BfPass {
     int ss;                  // source stride
     int nr, ns, r0, s0, step;// taps r = r0 + step*x (x < nr), s = s0 + step*y (y < ns)
     int offh, offw, sgn, shift;  // dh = (offh + sgn*r) >> shift, dw = (offw + sgn*s) >> shift
+    unsigned mWv, mHv;       // bf_magic(Wv), bf_magic(Hv)
 };
 
 // Output channels in the epilogue: BM x BN tile, bf16, pitch BN + 8.
@@ -140,11 +151,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
     for (int u = 0; u < AL; ++u) {
         const long m = m0 + rr + 64 * u;
         const bool ok = m < Mv;
-        const long mm = ok ? m : 0;
-        const int ow = (int)(mm % ps.Wv);
-        const long t = mm / ps.Wv;
-        const int img = (int)(t / ps.Hv);
-        a_h[u] = (int)(t % ps.Hv) * ps.ss;
+        const unsigned mm = ok ? (unsigned)m : 0u;
+        const unsigned t = bf_div(mm, ps.mWv);
+        const int ow = (int)(mm - t * (unsigned)ps.Wv);
+        const unsigned img = bf_div(t, ps.mHv);
+        a_h[u] = (int)(t - img * (unsigned)ps.Hv) * ps.ss;
         a_w[u] = ow * ps.ss;
         a_off[u] = ((img * g.Hs + a_h[u]) * g.Ws + a_w[u]) * g.Cs;
         if (!ok) a_h[u] = -(1 << 20);             // every tap falls outside
@@ -340,10 +351,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
         const int row = e / CPR, ch = (e - (e / CPR) * CPR) * 8;
         const long m = m0 + row;
         if (m >= Mv || n0 + ch >= g.Ncols) continue;
-        const int ow = (int)(m % ps.Wv);
-        const long t = m / ps.Wv;
-        const int oh = (int)(t % ps.Hv), img = (int)(t / ps.Hv);
-        const long di = ((long)(img * ps.Hd + oh * ps.os + ps.oa) * ps.Wd + ow * ps.os + ps.ob) * g.Ncols + n0 + ch;
+        long di;
+        if (ps.os == 1 && ps.Hd == ps.Hv && ps.Wd == ps.Wv) {
+            di = m * g.Ncols + n0 + ch;           // the pass covers the whole output grid
+        } else {
+            const unsigned t = bf_div((unsigned)m, ps.mWv);
+            const int ow = (int)((unsigned)m - t * (unsigned)ps.Wv);
+            const unsigned img = bf_div(t, ps.mHv);
+            const int oh = (int)(t - img * (unsigned)ps.Hv);
+            di = ((long)((int)img * ps.Hd + oh * ps.os + ps.oa) * ps.Wd + ow * ps.os + ps.ob) * g.Ncols + n0 + ch;
+        }
         bf16* dp = Y + di;
         uint4 v = *(const uint4*)(Ot + row * OP + ch);
         if (res) {
@@ -497,8 +514,16 @@ static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* 
 }
 
 static hipError_t run_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const bf16* res,
-                                const ConvGeom& g, const BfPass& ps, bool acc, const BnSums* stats, int bm, int bn,
+                                const ConvGeom& g, const BfPass& ps0, bool acc, const BnSums* stats, int bm, int bn,
                                 hipStream_t st) {
+    BfPass ps = ps0;
+    const long Mv = (long)g.Nb * ps.Hv * ps.Wv;
+    if (Mv == 0) return hipSuccess;
+    // pixel indices up to Mv + BM (a tile's padding rows) divided by Wv, row indices by Hv
+    if (!bf_div_exact(Mv + 256, ps.Wv) || !bf_div_exact(Mv / (ps.Wv > 0 ? ps.Wv : 1) + 256, ps.Hv))
+        return hipErrorInvalidValue;
+    ps.mWv = bf_magic((unsigned)ps.Wv);
+    ps.mHv = bf_magic((unsigned)ps.Hv);
     if (bm == 256) return launch_bf16_pass<256, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
     if (bm == 128 && bn == 128) return launch_bf16_pass<128, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
     if (bm == 128) return launch_bf16_pass<128, 64>(src, B, bias, Y, res, g, ps, acc, stats, st);
@@ -570,6 +595,7 @@ struct WgB {
     int Nb, Hi, Wi, Cs, Ho, Wo, Cout, S, stride, pad, Ktot;
     long P;        // output pixels N*Ho*Wo
     int pps;       // pixels per split (multiple of 32)
+    unsigned mWo, mHo;   // bf_magic(Wo), bf_magic(Ho)
 };
 
 // part[split][cout][col], col = (r*S + s)*Cs + c, over the split's pixels.
@@ -623,10 +649,11 @@ __global__ __launch_bounds__(256) void wgrad_bf16_k(const bf16* __restrict__ dY,
             const long p = p_lo + (long)ks * 32 + 2 * pq + h;
             pv[h] = p < p_hi;
             const long pp = pv[h] ? p : p_lo;
-            ow[h] = (int)(pp % g.Wo);
-            const long t = pp / g.Wo;
-            oh[h] = (int)(t % g.Ho);
-            img[h] = (int)(t / g.Ho);
+            const unsigned t = bf_div((unsigned)pp, g.mWo);
+            ow[h] = (int)((unsigned)pp - t * (unsigned)g.Wo);
+            const unsigned im = bf_div(t, g.mHo);
+            oh[h] = (int)(t - im * (unsigned)g.Ho);
+            img[h] = (int)im;
 #pragma unroll
             for (int u = 0; u < AE; ++u)
                 ra[u][h] = (pv[h] && a_ok[u]) ? *(const uint4*)(dY + pp * g.Cout + a_c[u]) : uint4{0, 0, 0, 0};
@@ -737,8 +764,10 @@ hipError_t launch_conv_wgrad_bf16(const bf16* dY, const bf16* X, float* part, in
                                   int Ho, int Wo, int Cout, int R, int S, int stride, int pad, const WgradPlan& p,
                                   hipStream_t st) {
     if (Cin_p % 8 || Cout % 8) return hipErrorInvalidValue;
-    const WgB a{Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, S, stride, pad, R * S * Cin_p, (long)Nb * Ho * Wo,
-                p.pix_per_split};
+    const long P = (long)Nb * Ho * Wo;
+    if (!bf_div_exact(P, Wo) || !bf_div_exact(P / Wo, Ho)) return hipErrorInvalidValue;
+    const WgB a{Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, S, stride, pad, R * S * Cin_p, P, p.pix_per_split,
+                bf_magic((unsigned)Wo), bf_magic((unsigned)Ho)};
     if (p.tm == 128 && p.tn == 128) return launch_wg_bf16<128, 128>(dY, X, part, a, p.splits, st);
     if (p.tm == 128) return launch_wg_bf16<128, 64>(dY, X, part, a, p.splits, st);
     if (p.tn == 128) return launch_wg_bf16<64, 128>(dY, X, part, a, p.splits, st);
