@@ -217,7 +217,7 @@ __global__ __launch_bounds__(256) void bn_act_k(const T* __restrict__ x1, BnFwd 
     for (int u = 0; u < E; ++u) {
         const long i = i0 + u * 256;
         if (i >= n4) continue;
-        const int c = (int)(i % C4) * 4;
+        const int c = (int)((unsigned)i % (unsigned)C4) * 4;   // i < 2^31
         f4 o;
 #pragma unroll
         for (int j = 0; j < 4; ++j) o[j] = __builtin_fmaf(xa[u][j], co[c + j], co[C + c + j]);
@@ -473,7 +473,7 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BnBwdArgs a, BnBwdCoef k, 
     for (int u = 0; u < E; ++u) {
         const long i = i0 + u * 256;
         if (i >= n4) continue;
-        const int c = (int)(i % C4) * 4;
+        const int c = (int)((unsigned)i % (unsigned)C4) * 4;   // i < 2^31
         f4 g = gv[u];
         if (MK == 1) {
 #pragma unroll
@@ -758,7 +758,7 @@ __global__ void concat_fwd_k(const T* __restrict__ a, const T* __restrict__ b, T
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
     const int cq = aq + bq;
     if (i >= rows * cq) return;
-    const long r = i / cq;
+    const long r = (unsigned)i / (unsigned)cq;   // i < 2^31
     const int q = (int)(i - r * cq);
     st4(y, i, q < aq ? ld4(a, r * aq + q) : ld4(b, r * bq + (q - aq)));
 }
@@ -770,7 +770,7 @@ __global__ void concat_bwd_k(const T* __restrict__ dy, long rows, int aq, int bq
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
     const int cq = aq + bq;
     if (i >= rows * cq) return;
-    const long r = i / cq;
+    const long r = (unsigned)i / (unsigned)cq;   // i < 2^31
     const int q = (int)(i - r * cq);
     const f4 g = ld4(dy, i);
     if (q < aq) {
@@ -973,8 +973,9 @@ template <class T>
 __global__ void gap_bwd_k(const float* __restrict__ dy, T* __restrict__ dx, int Nb, int HW, int C, int acc) {
     const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= (long)Nb * HW * C) return;
-    const int c = (int)(idx % C);
-    const int n = (int)(idx / ((long)HW * C));
+    const unsigned t = (unsigned)idx / (unsigned)C;   // idx < 2^31
+    const int c = (int)((unsigned)idx - t * (unsigned)C);
+    const int n = (int)(t / (unsigned)HW);
     const float v = dy[n * C + c] / (float)HW;
     st1(dx, idx, acc ? ld1(dx, idx) + v : v);
 }
