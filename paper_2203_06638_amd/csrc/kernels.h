@@ -176,6 +176,9 @@ hipError_t launch_stats_finalize(const float* pmean, const float* pm2, int T, in
                                  const float* gamma, const float* beta, float eps, float* aux, hipStream_t st);
 // out[c] = sum_t rows_t * pmean[t][c]: column sums from tile means
 hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C, float* out, hipStream_t st);
+// the same over C columns of partials stored with row stride ld
+hipError_t launch_sum_from_tiles_ld(const float* pmean, int ld, int T, int R, long M, int C, float* out,
+                                    hipStream_t st);
 // A training-mode batch norm as the per-channel map x*scale + shift.  With
 // acc set, scale and shift come from the batch sums acc [2][kAccSlots][C]
 // over M rows (mean, biased variance, rstd = 1/sqrt(var + eps),
@@ -259,6 +262,11 @@ hipError_t launch_relu_bwd(int dt, const void* dy, const void* x, void* dx, long
 // ReLU's stored output; pmean[tile][c] = the tile's mean of the masked
 // column c over stats_tiles(M, C) row tiles of stats_rows(M, C) rows.
 hipError_t launch_relu_mask_colsum(int dt, void* dy, const void* y, long M, int C, float* pmean, hipStream_t st);
+// Backward of y = concat(a, b) over channels where a and b are stored ReLU
+// outputs: da / db (null: not wanted) := the slices of dy, zero where ya / yb
+// is; pmean (non-null) as launch_relu_mask_colsum's, over C = ca + cb columns.
+hipError_t launch_concat_relu_bwd(int dt, const void* dy, const void* ya, const void* yb, void* da, void* db, long M,
+                                  int ca, int cb, float* pmean, hipStream_t st);
 hipError_t launch_add_fwd(int dt, const void* a, const void* b, void* y, long n, hipStream_t st);
 hipError_t launch_copy_acc(int dt, const void* src, void* dst, long n, bool accumulate, hipStream_t st);
 // channel concatenation of two NHWC tensors with `rows` pixels (ca, cb

@@ -122,19 +122,24 @@ __device__ __forceinline__ double tree_sum256(double v, double* red) {
 }
 
 // out[c] = sum over tiles of n_t * mean_t (the column sum), fixed order
-__global__ __launch_bounds__(256) void sum_from_tiles_k(const float* __restrict__ pmean, int T, int R, long M, int C,
+__global__ __launch_bounds__(256) void sum_from_tiles_k(const float* __restrict__ pmean, int ld, int T, int R, long M,
                                                         float* __restrict__ out) {
     __shared__ double red[256];
     const int c = blockIdx.x;
     double s = 0.0;
     for (int t = threadIdx.x; t < T; t += 256)
-        s += (double)min((long)R, M - (long)t * R) * (double)pmean[(long)t * C + c];
+        s += (double)min((long)R, M - (long)t * R) * (double)pmean[(long)t * ld + c];
     s = tree_sum256(s, red);
     if (threadIdx.x == 0) out[c] = (float)s;
 }
 
 hipError_t launch_sum_from_tiles(const float* pmean, int T, int R, long M, int C, float* out, hipStream_t st) {
-    launch(sum_from_tiles_k, dim3(C), dim3(256), 0, st, pmean, T, R, M, C, out);
+    launch(sum_from_tiles_k, dim3(C), dim3(256), 0, st, pmean, C, T, R, M, out);
+    return hipGetLastError();
+}
+hipError_t launch_sum_from_tiles_ld(const float* pmean, int ld, int T, int R, long M, int C, float* out,
+                                    hipStream_t st) {
+    launch(sum_from_tiles_k, dim3(C), dim3(256), 0, st, pmean, ld, T, R, M, out);
     return hipGetLastError();
 }
 
@@ -708,6 +713,68 @@ hipError_t launch_relu_mask_colsum(int dt, void* dy, const void* y, long M, int 
         launch(relu_mask_colsum_k<bf16>, grid, dim3(256), 0, st, (bf16*)dy, (const bf16*)y, M, C, R, pmean);
     else
         launch(relu_mask_colsum_k<float>, grid, dim3(256), 0, st, (float*)dy, (const float*)y, M, C, R, pmean);
+    return hipGetLastError();
+}
+
+// Backward of a channel concatenation whose two inputs are ReLU outputs
+// (each applied by its producing conv): the slices of dy, masked where the
+// stored ReLU output is zero, into da and db (null: not wanted), and per row
+// tile of stats_rows(M, C) rows the tile means of the masked columns,
+// pmean[tile][c] over the concatenated channels c < C = ca + cb.
+template <class T>
+__global__ __launch_bounds__(256) void concat_relu_bwd_k(const T* __restrict__ dy, const T* __restrict__ ya,
+                                                         const T* __restrict__ yb, T* __restrict__ da,
+                                                         T* __restrict__ db, long M, int ca, int cb, int R,
+                                                         float* __restrict__ pmean) {
+    __shared__ f4 red[256];
+    const int tid = threadIdx.x;
+    const int C = ca + cb, C4 = C >> 2, A4 = ca >> 2, B4 = cb >> 2;
+    const long r0 = (long)blockIdx.x * R;
+    const long r1 = min(M, r0 + R);
+    const float rows = (float)(r1 - r0);
+    for (int qbase = blockIdx.y * 256; qbase < min(C4, (int)(blockIdx.y + 1) * 256); qbase += 256) {
+        int nq, rl;
+        quad_layout(C4, qbase, nq, rl);
+        const int q = qbase + tid % nq, lr = tid / nq;
+        const bool in_a = q < A4;
+        const T* yv = in_a ? ya : yb;
+        T* dv = in_a ? da : db;
+        const int qq = in_a ? q : q - A4, cq = in_a ? A4 : B4;
+        f4 s = f4{0.f, 0.f, 0.f, 0.f};
+        if (lr < rl)
+            for (long r = r0 + lr; r < r1; r += rl) {
+                f4 g = ld4(dy, r * C4 + q);
+                const f4 v = ld4(yv, r * cq + qq);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) g[k] = v[k] > 0.f ? g[k] : 0.f;
+                if (dv) st4(dv, r * cq + qq, g);
+                s += g;
+            }
+        if (pmean) {
+            red[tid] = s;
+            __syncthreads();
+            if (tid < nq) {
+                f4 t = f4{0.f, 0.f, 0.f, 0.f};
+                for (int k = 0; k < rl; ++k) t += red[k * nq + tid];
+                for (int k = 0; k < 4; ++k) pmean[(long)blockIdx.x * C + (qbase + tid) * 4 + k] = t[k] / rows;
+            }
+            __syncthreads();
+        }
+    }
+}
+
+hipError_t launch_concat_relu_bwd(int dt, const void* dy, const void* ya, const void* yb, void* da, void* db, long M,
+                                  int ca, int cb, float* pmean, hipStream_t st) {
+    if ((ca | cb) & 3) return hipErrorInvalidValue;
+    const int C = ca + cb;
+    const dim3 grid(stats_tiles(M, C), ((C >> 2) + 255) / 256);
+    const int R = stats_rows(M, C);
+    if (dt == DT_BF16)
+        launch(concat_relu_bwd_k<bf16>, grid, dim3(256), 0, st, (const bf16*)dy, (const bf16*)ya, (const bf16*)yb,
+               (bf16*)da, (bf16*)db, M, ca, cb, R, pmean);
+    else
+        launch(concat_relu_bwd_k<float>, grid, dim3(256), 0, st, (const float*)dy, (const float*)ya,
+               (const float*)yb, (float*)da, (float*)db, M, ca, cb, R, pmean);
     return hipGetLastError();
 }
 

@@ -97,6 +97,10 @@ struct Group {
     int lin = -1;       // G_HEAD: the linear layer
     bool fold = false;  // G_BNACT: BN + ReLU folded into the consuming conv (nothing launched forward)
     bool rsum = false;  // G_BNACT (folded): its backward sums come from the consuming conv's data gradient
+    bool premask = false;  // G_CONV with a ReLU: the consuming concat's backward masks its output gradient
+                           //   and forms its bias gradient
+    int mconv_a = -1, mconv_b = -1;  // G_CONCAT: the convs whose ReLUs (their outputs are its inputs) its
+                                     //   backward applies
 };
 
 struct Model {
@@ -456,6 +460,27 @@ void build_groups(Model& M, bool fused) {
         for (int i = 0; i < (int)gs.size(); ++i)
             if (!drop[i]) kept.push_back(gs[i]);
         gs.swap(kept);
+    }
+    // fp32: a concat of two such ReLU outputs, each consumed by it alone,
+    // masks both gradient slices in its own backward (one pass instead of a
+    // split pass plus a masking pass per branch)
+    if (fused && M.dt == lpp::DT_F32) {
+        std::vector<int> group_of(n, -1);
+        for (int i = 0; i < (int)gs.size(); ++i) group_of[gs[i].out] = i;
+        for (auto& g : gs) {
+            if (g.kind != G_CONCAT) continue;
+            const int a = M.layers[g.a].L.in0, b = M.layers[g.a].L.in1;
+            if (a < 0 || b < 0 || a == b || group_of[a] < 0 || group_of[b] < 0) continue;
+            Group& A = gs[group_of[a]];
+            Group& B = gs[group_of[b]];
+            auto ok = [&](const Group& c, int out) {
+                return c.kind == G_CONV && c.relu == out && !M.layers[c.a].pw && M.consumers[out].size() == 1;
+            };
+            if (!ok(A, a) || !ok(B, b)) continue;
+            g.mconv_a = A.a;
+            g.mconv_b = B.a;
+            A.premask = B.premask = true;
+        }
     }
     // a group runs when its last layer's inputs exist: order by output layer
     std::stable_sort(gs.begin(), gs.end(), [](const Group& x, const Group& y) { return x.out < y.out; });
@@ -894,16 +919,17 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
         switch (G.kind) {
         case G_CONV: {
             // a fused ReLU: its output gradient masked in place into the
-            // conv's (with the bias gradient's column sums on the way)
+            // conv's, with the bias gradient's column sums on the way (with
+            // premask the consuming concat's backward has done both)
             const long Mo = (long)N * Y.out.h * Y.out.w;
             const bool bias_fused = G.relu >= 0 && !Y.pw && Y.L.bias && pl.wgrad[G.a];
-            if (bias_fused) {
+            if (bias_fused && !G.premask) {
                 LAUNCH("relu", 3.0 * eb * Mo * Y.out.c, st,
                        lpp::launch_relu_mask_colsum(dt, dy, c->act(w, G.out), Mo, Y.L.cout, w.ps0, st));
                 LAUNCH("bias_grad", 0.0, st,
                        lpp::launch_sum_from_tiles(w.ps0, lpp::stats_tiles(Mo, Y.L.cout), lpp::stats_rows(Mo, Y.L.cout),
                                                   Mo, Y.L.cout, w.g + Y.poff + Y.wcount, st));
-            } else if (G.relu >= 0) {
+            } else if (G.relu >= 0 && !G.premask) {
                 LAUNCH("relu", 3.0 * eb * Mo * Y.out.c, st,
                        lpp::launch_relu_bwd(dt, dy, c->act(w, G.out), dy, Mo * Y.out.c, false, st));
             }
@@ -1090,6 +1116,27 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                        lpp::launch_copy_acc(dt, dy, c->dact(w, Y.L.in1), Min * Y.out.c, pl.acc1[G.a] != 0, st));
             break;
         case G_CONCAT:
+            if (G.mconv_a >= 0 && (dx0 || pl.din1[G.a])) {
+                // both inputs are fused ReLU outputs: masked slices, and the
+                // two convs' bias gradients from the masked column sums
+                const Layer& Ca = M.layers[G.mconv_a];
+                const Layer& Cb = M.layers[G.mconv_b];
+                const bool ba = Ca.L.bias && pl.wgrad[G.mconv_a], bb = Cb.L.bias && pl.wgrad[G.mconv_b];
+                const int C = Y.out.c, ca = Y.in0.c, cb = Y.in1.c;
+                if (pl.acc0[G.a] || pl.acc1[G.a]) return fail(LPP_EINVAL, "masked concat backward: accumulating input");
+                LAUNCH("relu", (1.0 + (dx0 ? 2.0 : 0.0) * ca / C + (pl.din1[G.a] ? 2.0 : 0.0) * cb / C) * eb * Min * C, st,
+                       lpp::launch_concat_relu_bwd(dt, dy, c->act(w, Y.L.in0), c->act(w, Y.L.in1), dx0,
+                                                   pl.din1[G.a] ? c->dact(w, Y.L.in1) : nullptr, Min, ca, cb,
+                                                   (ba || bb) ? w.ps0 : nullptr, st));
+                const int T = lpp::stats_tiles(Min, C), R = lpp::stats_rows(Min, C);
+                if (ba)
+                    LAUNCH("bias_grad", 0.0, st,
+                           lpp::launch_sum_from_tiles_ld(w.ps0, C, T, R, Min, ca, w.g + Ca.poff + Ca.wcount, st));
+                if (bb)
+                    LAUNCH("bias_grad", 0.0, st,
+                           lpp::launch_sum_from_tiles_ld(w.ps0 + ca, C, T, R, Min, cb, w.g + Cb.poff + Cb.wcount, st));
+                break;
+            }
             if (dx0 || pl.din1[G.a])
                 LAUNCH("concat", (1.0 + (dx0 ? 1.0 : 0.0) + (pl.din1[G.a] ? 1.0 : 0.0)) * eb * Min * Y.out.c, st,
                        lpp::launch_concat_bwd(dt, dy, Min, Y.in0.c, Y.in1.c, dx0, pl.acc0[G.a] != 0,
@@ -1281,6 +1328,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         const long rin = (long)N * Y.in0.h * Y.in0.w;
         if (Y.L.op == LPP_BN) ps = std::max<long>(ps, (long)lpp::stats_tiles(rin, Y.out.c) * Y.out.c);
         if (Y.L.op == LPP_LINEAR) ps = std::max<long>(ps, (long)N * Y.L.cin);   // the wide head's dfeat
+        if (Y.L.op == LPP_CONCAT) ps = std::max<long>(ps, (long)lpp::stats_tiles(rows_out, Y.out.c) * Y.out.c);
         if (Y.L.op == LPP_CONV && !Y.pw) {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
                             Y.L.pad};
