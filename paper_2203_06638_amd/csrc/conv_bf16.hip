@@ -24,9 +24,10 @@
 // step spans several taps).  Operand tiles go through LDS in rows of 32 bf16
 // (64 bytes) whose four 16-byte chunks are XOR-swizzled by (row / 4) % 4, so
 // both the row-wise stores and the 16-row fragment reads of 16 lanes hit
-// distinct banks.  Tiles are double-buffered and the next step's global loads
-// are in flight during the current step's MFMAs; for Cs >= 128 two load steps
-// share one buffer and one barrier (a 64-wide K-step).
+// distinct banks.  Sources of 32k channels load their tiles straight into
+// LDS through a pipeline of several buffers (see the DMA notes below); the
+// 8/16-channel stem stages them through registers into two buffers, the next
+// step's loads in flight during the current step's MFMAs.
 //
 // Weight gradient: dW[cout][(tap, c)] = sum over output pixels p of
 // dY[p][cout] * X[src(p, tap)][c]: a GEMM whose reduction runs over pixels.
