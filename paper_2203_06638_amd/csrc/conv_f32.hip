@@ -683,13 +683,18 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
             if (n < g.Ncols) {
                 const f4 v = *(const f4*)(Ot + p * OP + qd * 4);
                 f4* o = (f4*)(Y + (m0 + pix_base + p) * g.Ncols + n);
-                *o = accumulate == kStoreAdd ? *o + v : (accumulate == kStoreRelu ? relu4(v) : v);
+                const f4 tot = accumulate == kStoreAdd ? *o + v : (accumulate == kStoreRelu ? relu4(v) : v);
+                *o = tot;
                 if (MODE == CONV_DGRAD && STATS) {
-                    // gm = v where the forward's ReLU passed, xhat of the BN input
-                    const f4 x = *(const f4*)(bs.x1 + (m0 + pix_base + p) * g.Ncols + n);
+                    // gm = the stored gradient where the forward's ReLU passed
+                    // (its output y > 0, or fma(x, scale, shift) > 0), xhat of the BN input
+                    const long e = (m0 + pix_base + p) * g.Ncols + n;
+                    const f4 x = *(const f4*)(bs.x1 + e);
+                    const f4 yv = bs.y ? *(const f4*)(bs.y + e) : f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        const float gm = __builtin_fmaf(x[j], bsc[j], bsh[j]) > 0.f ? v[j] : 0.f;
+                        const bool pass = bs.y ? yv[j] > 0.f : __builtin_fmaf(x[j], bsc[j], bsh[j]) > 0.f;
+                        const float gm = pass ? tot[j] : 0.f;
                         bs0[j] += gm;
                         bs1[j] += gm * ((x[j] - bmu[j]) * brs[j]);
                     }
@@ -850,7 +855,7 @@ static hipError_t launch_tile(const float* src, const float* B, const float* bia
     const BnFwd ib = inbn ? *inbn : BnFwd{};
     const BnBwdSum bsum = bsv ? *bsv : BnBwdSum{};
     // a data gradient's statistics are the sums of a BN backward (bsv)
-    if (MODE == CONV_DGRAD && stats && (!bsv || acc)) return hipErrorInvalidValue;
+    if (MODE == CONV_DGRAD && stats && (!bsv || (acc && !bsv->y))) return hipErrorInvalidValue;
     if (inbn) {
         if (MODE != CONV_FWD || g.Cs > kFoldMaxC) return hipErrorInvalidValue;
         if (stats)

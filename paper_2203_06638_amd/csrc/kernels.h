@@ -88,10 +88,14 @@ constexpr int kFoldMaxC = 512;
 // that BN backward's sums, q = 0: sum gm and q = 1: sum gm*xhat, gm = g
 // where fma(x1, scale, shift) > 0, xhat = (x1 - mean) rstd, from aux =
 // [mean | rstd | scale | shift]: into stats->acc, or as partials p0/p1 per
-// tile, conv_dgrad_sum_tiles(g) tiles (spatial kernel only; not accumulating).
+// tile, conv_dgrad_sum_tiles(g) tiles (spatial kernel only).  With y
+// non-null the ReLU decision is y > 0 instead (y the stored output of a BN +
+// residual add + ReLU group), and the pass may accumulate: the sums then
+// describe the accumulated gradient.
 struct BnBwdSum {
     const float* x1;
     const float* aux;
+    const float* y = nullptr;
 };
 // How a pass writes Y: kStoreSet overwrites, kStoreAdd adds to what Y
 // holds, kStoreRelu (forward, without stats) overwrites with max(y, 0) -- a

@@ -59,6 +59,8 @@ struct Layer {
     bool pw = false;              // conv: 1x1, stride 1, no padding, output channels not a multiple of 4 --
                                   //   run as a linear layer applied to every pixel (fp32)
     int in_bn = -1;               // conv: reads relu(bn(x)) of this BN layer's input x, folded into its loads
+    int gsum_y = -1;              // conv with gsum_bn: the ReLU decision is this layer's stored output > 0 (a BN +
+                                  //   residual add + ReLU group) instead of the folded BN's fma(x, scale, shift) > 0
     int gsum_bn = -1;             // conv: its data gradient (the gradient at that BN + ReLU's output) also
                                   //   forms the sums of this BN's backward
     long wf_off = -1, wd_off = -1;// conv: W_f / W_d in the worker's weight buffer (elements)
@@ -96,7 +98,8 @@ struct Group {
     int relu = -1;      // G_BNACT: the closing ReLU, if any; G_CONV: a ReLU applied by the conv's epilogue
     int lin = -1;       // G_HEAD: the linear layer
     bool fold = false;  // G_BNACT: BN + ReLU folded into the consuming conv (nothing launched forward)
-    bool rsum = false;  // G_BNACT (folded): its backward sums come from the consuming conv's data gradient
+    bool rsum = false;  // G_BNACT: its backward sums come from the data gradient of conv rsum_conv
+    int rsum_conv = -1;
     bool premask = false;  // G_CONV with a ReLU: the consuming concat's backward masks its output gradient
                            //   and forms its bias gradient
     int mconv_a = -1, mconv_b = -1;  // G_CONCAT: the convs whose ReLUs (their outputs are its inputs) its
@@ -529,8 +532,34 @@ void plan_folds(Model& M, int N) {
                           M.groups[gi + 1].a == M.consumers[G.out][0];
         if (next && lpp::conv_dgrad_sum_tiles(gd) > 0) {
             G.rsum = true;
+            G.rsum_conv = M.consumers[G.out][0];
             Y.gsum_bn = G.a;
         }
+    }
+    // BN + residual add of a stored tensor + ReLU (a residual unit's end)
+    // whose output feeds the next unit's first conv and its shortcut: the
+    // conv's data gradient, which runs last among the output's consumers and
+    // adds onto the shortcut's, forms the BN backward's sums with the stored
+    // output's ReLU decisions (when its group runs right after this group's)
+    for (size_t gi = 0; gi + 1 < M.groups.size(); ++gi) {
+        Group& G = M.groups[gi];
+        if (G.kind != G_BNACT || G.fold || G.rsum || G.bn2 >= 0 || G.add < 0 || G.res < 0 || G.relu < 0) continue;
+        const Group& Nx = M.groups[gi + 1];
+        if (Nx.kind != G_CONV || Nx.add >= 0 || Nx.relu >= 0) continue;
+        Layer& Y = M.layers[Nx.a];
+        if (Y.L.op != LPP_CONV || Y.pw || Y.L.in0 != G.out || Y.cin_p != Y.L.cin || Y.in_bn >= 0) continue;
+        // every other consumer of the output runs its backward before this conv's
+        bool later = true;
+        for (int cl : M.consumers[G.out])
+            if (cl != Nx.a && cl <= Nx.out) later = false;
+        if (!later) continue;
+        const lpp::ConvGeom gd{N, Y.out.h, Y.out.w, Y.L.cout, Y.in0.h, Y.in0.w, Y.L.cin, Y.L.k, Y.L.k, Y.L.stride,
+                               Y.L.pad};
+        if (lpp::conv_dgrad_sum_tiles(gd) <= 0) continue;
+        G.rsum = true;
+        G.rsum_conv = Nx.a;
+        Y.gsum_bn = G.a;
+        Y.gsum_y = G.out;
     }
 }
 
@@ -1004,13 +1033,15 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
                            lpp::launch_conv_bf16(lpp::CONV_DGRAD, (const uint16_t*)dy, (const uint16_t*)c->wdg(w, Y),
                                                  nullptr, (uint16_t*)dx0, g, pl.acc0[G.a] != 0, nullptr, st));
                 else if (Y.gsum_bn >= 0) {
-                    // dx0 is the whole gradient at a folded BN + ReLU's output:
-                    // the pass also forms that BN backward's sums
+                    // dx0 is (or completes, adding onto the shortcut's) the
+                    // whole gradient at a BN + ReLU group's output: the pass
+                    // also forms that BN backward's sums
                     const lpp::BnSums out = c->fixed_order ? lpp::BnSums{nullptr, w.ps0, w.ps1, nullptr}
                                                            : lpp::BnSums{c->acc_bwd(w, Y.gsum_bn), nullptr, nullptr,
                                                                          nullptr};
                     const lpp::BnBwdSum bsum{(const float*)c->act(w, M.layers[Y.gsum_bn].L.in0),
-                                             c->aux(w, Y.gsum_bn)};
+                                             c->aux(w, Y.gsum_bn),
+                                             Y.gsum_y >= 0 ? (const float*)c->act(w, Y.gsum_y) : nullptr};
                     LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
                            lpp::launch_conv_igemm(lpp::CONV_DGRAD, (const float*)dy, (const float*)c->wdg(w, Y),
                                                   nullptr, (float*)dx0, g, pl.acc0[G.a] != 0, &out, st, nullptr,
@@ -1034,9 +1065,9 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
         case G_BNACT: {
             const int C = Y.out.c;
             const int b2 = G.bn2;
-            int rsum_tiles = 0;   // partials of the consuming conv's data gradient (folded groups)
+            int rsum_tiles = 0;   // partials of the data gradient that formed the sums
             if (G.rsum) {
-                const Layer& Y2 = M.layers[M.consumers[G.out][0]];
+                const Layer& Y2 = M.layers[G.rsum_conv];
                 rsum_tiles = lpp::conv_dgrad_sum_tiles(lpp::ConvGeom{N, Y2.out.h, Y2.out.w, Y2.L.cout, Y2.in0.h,
                                                                      Y2.in0.w, Y2.L.cin, Y2.L.k, Y2.L.k,
                                                                      Y2.L.stride, Y2.L.pad});
