@@ -33,7 +33,7 @@ KAPPA = 1e-2
 # fp32 accumulation, fp32 master parameters): max relative error 5e-2 per
 # tensor in the max norm, max_e |g_e - r_e| / max_e |r_e| (tau = 1).  Every
 # stored tensor and every conv weight is rounded to 8 significant bits
-# (relative error up to 2^-9), and the error this leaves in a sum is
+# (relative error up to 2^-8), and the error this leaves in a sum is
 # proportional to the magnitudes of its terms, not to the sum: near-zero
 # entries of a tensor carry errors of the size of the tensor's typical
 # entries (measured: ~2e-3 of max|r| per layer), which an elementwise
