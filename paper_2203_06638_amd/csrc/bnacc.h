@@ -13,6 +13,7 @@
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include "act.h"
 #include "kernels.h"
 
 namespace lpp {
@@ -60,6 +61,103 @@ __device__ __forceinline__ void bn_fwd_coeffs(const BnFwd& b, int C, float* sc, 
             sc[c] = b.aux[2 * C + c];
             sh[c] = b.aux[3 * C + c];
         }
+    }
+}
+
+// Per-channel moments of an MFMA output tile, for the batch sums of the
+// producing conv's epilogue.  Each lane of wave (wm, wn) holds acc[x][y][i]:
+// its TM x 4 rows (x, i), of which valid(x, i) lie inside the tensor, in
+// column (wn TN + y) 16 + lane % 16.  A lane takes the count, mean and sum of
+// squared deviations of its valid rows (two passes in registers); the lanes
+// of a column are merged over the four lane groups (xor 16, then 32) and the
+// WM row waves in order by the pairwise rule
+//   n = na + nb,  mean = ma + (mb - ma) nb / n,  M2 = M2a + M2b + (mb - ma)^2 na nb / n,
+// and out(t, n, mean, M2) runs for the tile's columns t < BN.  One barrier;
+// red holds WM x 3 x BN floats of LDS.
+// ALL: every row is valid, so merged counts are equal and known (no
+// divisions); otherwise the weights use the hardware reciprocal (about one
+// ulp, far below the statistics' use).
+template <int TM, int TN, int WM, int BN, bool ALL, class Valid, class Out>
+__device__ __forceinline__ void tile_moments(const f4 (&acc)[TM][TN], int wm, int wn, Valid valid,
+                                             float (&red)[WM][3][BN], Out out) {
+    const int lane = threadIdx.x & 63;
+    float cl = 0.f;
+#pragma unroll
+    for (int x = 0; x < TM; ++x)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cl += (ALL || valid(x, i)) ? 1.f : 0.f;
+#pragma unroll
+    for (int y = 0; y < TN; ++y) {
+        float cnt = cl, mu = 0.f, m2 = 0.f;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (ALL || valid(x, i)) mu += acc[x][y][i];
+        if (ALL) mu *= 1.f / (4 * TM);
+        else mu = cnt > 0.f ? mu * __builtin_amdgcn_rcpf(cnt) : 0.f;
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float dv = acc[x][y][i] - mu;
+                if (ALL || valid(x, i)) m2 += dv * dv;
+            }
+#pragma unroll
+        for (int o = 16; o <= 32; o <<= 1) {
+            const float co = __shfl_xor(cnt, o), mo = __shfl_xor(mu, o), qo = __shfl_xor(m2, o);
+            const float n = cnt + co, d = mo - mu;
+            if (ALL) {
+                // equal counts: mean (a + b) / 2, M2 += d^2 n / 4
+                m2 = (m2 + qo) + d * d * (0.25f * n);
+                mu = 0.5f * (mu + mo);
+            } else if (n > 0.f) {
+                const float r = __builtin_amdgcn_rcpf(n);
+                mu += d * (co * r);
+                m2 += qo + d * d * (cnt * co * r);
+            }
+            cnt = n;
+        }
+        if (lane < 16) {
+            const int col = (wn * TN + y) * 16 + lane;
+            red[wm][0][col] = cnt;
+            red[wm][1][col] = mu;
+            red[wm][2][col] = m2;
+        }
+    }
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < BN) {
+        float cnt = red[0][0][t], mu = red[0][1][t], m2 = red[0][2][t];
+#pragma unroll
+        for (int w = 1; w < WM; ++w) {
+            const float cb = red[w][0][t], n = cnt + cb, d = red[w][1][t] - mu;
+            if (ALL) {
+                // counts w k and k: weights 1 / (w + 1) and w k / (w + 1)
+                mu += d * (1.f / (w + 1));
+                m2 += red[w][2][t] + d * d * (cb * ((float)w / (w + 1)));
+            } else if (n > 0.f) {
+                const float r = __builtin_amdgcn_rcpf(n);
+                mu += d * (cb * r);
+                m2 += red[w][2][t] + d * d * (cnt * cb * r);
+            }
+            cnt = n;
+        }
+        out(t, cnt, mu, m2);
+    }
+}
+
+// A tile's moments into the batch sums: sum x = n mean and sum x^2 = M2 +
+// n mean^2 added to the fp64 accumulators, or the tile's mean and M2 as the
+// fixed-order partials of tile `tile`
+__device__ __forceinline__ void tile_moments_store(const BnSums& sums, int tile, int C, int c, float n, float mu,
+                                                   float m2) {
+    if (sums.acc) {
+        acc_add(sums.acc, 0, tile, C, c, (double)mu * n);
+        acc_add(sums.acc, 1, tile, C, c, (double)m2 + (double)n * mu * mu);
+    } else {
+        sums.p0[(long)tile * C + c] = mu;
+        sums.p1[(long)tile * C + c] = m2;
     }
 }
 

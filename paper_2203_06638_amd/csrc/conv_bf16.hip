@@ -396,11 +396,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
         *(uint4*)dp = v;
     }
     if (STATS) {
-        // per output channel of the tile: mean, then the sum of squared
-        // deviations from it, over the tile's valid rows (of the stored
-        // values: with a residual, the sums written back into the tile)
-        __shared__ float red[2][BN];
-        __shared__ float tmean[BN];
+        // per output channel of the tile: count, mean and sum of squared
+        // deviations of the stored values (with a residual, the sums written
+        // back into the tile)
+        __shared__ float red[2][3][BN];
         if (res) {
             __syncthreads();
 #pragma unroll
@@ -413,56 +412,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
                         acc[x][y][i] = from_bf16(Ot[((wm * TM + x) * 16 + (lane >> 4) * 4 + i) * OP + col]);
             }
         }
-        float colsum[TN];
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            colsum[y] = 0.f;
-#pragma unroll
-            for (int x = 0; x < TM; ++x)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if ((wm * TM + x) * 16 + (lane >> 4) * 4 + i < nvalid) colsum[y] += acc[x][y][i];
-        }
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            float s = colsum[y];
-            s += __shfl_xor(s, 16);
-            s += __shfl_xor(s, 32);
-            if (lane < 16) red[wm][(wn * TN + y) * 16 + lane] = s;
-        }
-        __syncthreads();
-        if (tid < BN) tmean[tid] = (red[0][tid] + red[1][tid]) / (float)nvalid;
-        __syncthreads();
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            const int col = (wn * TN + y) * 16 + (lane & 15);
-            const float mu = tmean[col];
-            float q = 0.f;
-#pragma unroll
-            for (int x = 0; x < TM; ++x)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int row = (wm * TM + x) * 16 + (lane >> 4) * 4 + i;
-                    const float dv = acc[x][y][i] - mu;
-                    if (row < nvalid) q += dv * dv;
-                }
-            q += __shfl_xor(q, 16);
-            q += __shfl_xor(q, 32);
-            if (lane < 16) red[wm][col - (lane & 15) + lane] = q;
-        }
-        __syncthreads();
-        if (tid < BN && n0 + tid < g.Ncols) {
-            const int n = n0 + tid;
-            const float m2 = red[0][tid] + red[1][tid];
-            if (sums.acc) {
-                const double mu = tmean[tid], nr = (double)nvalid;
-                acc_add(sums.acc, 0, (int)blockIdx.x, g.Ncols, n, mu * nr);
-                acc_add(sums.acc, 1, (int)blockIdx.x, g.Ncols, n, (double)m2 + nr * mu * mu);
-            } else {
-                sums.p0[(long)blockIdx.x * g.Ncols + n] = tmean[tid];
-                sums.p1[(long)blockIdx.x * g.Ncols + n] = m2;
-            }
-        }
+        const auto valid = [&](int x, int i) { return (wm * TM + x) * 16 + (lane >> 4) * 4 + i < nvalid; };
+        const auto store = [&](int t, float n, float mu, float m2) {
+            if (n0 + t < g.Ncols) tile_moments_store(sums, (int)blockIdx.x, g.Ncols, n0 + t, n, mu, m2);
+        };
+        if (nvalid == BM) tile_moments<TM, TN, 2, BN, true>(acc, wm, wn, valid, red, store);
+        else tile_moments<TM, TN, 2, BN, false>(acc, wm, wn, valid, red, store);
     }
 }
 

@@ -212,64 +212,14 @@ __global__ __launch_bounds__(256) void conv_igemm_f32(const float* __restrict__ 
             }
     }
     if (STATS) {
-        // two passes over the tile held in registers: the mean, then the sum
-        // of squared deviations from it; lanes of a wave are combined with
-        // xor shuffles over the row-group bits, waves through LDS, all in a
-        // fixed order
-        __shared__ float red[WM][BN];
-        __shared__ float tile_mean[BN];
-        const int rows = min(BM, M - (int)blockIdx.x * BM);
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            float sacc = 0.f;
-#pragma unroll
-            for (int x = 0; x < TM; ++x)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (m_base + x * 16 + gi * 4 + i < M) sacc += acc[x][y][i];
-            sacc += __shfl_xor(sacc, 16);
-            sacc += __shfl_xor(sacc, 32);
-            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = sacc;
-        }
-        __syncthreads();
-        if (threadIdx.x < BN) {
-            float t = 0.f;
-            for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
-            tile_mean[threadIdx.x] = t / (float)rows;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            const float mu = tile_mean[wn * TN * 16 + y * 16 + li];
-            float q = 0.f;
-#pragma unroll
-            for (int x = 0; x < TM; ++x)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (m_base + x * 16 + gi * 4 + i < M) {
-                        const float dv = acc[x][y][i] - mu;
-                        q += dv * dv;
-                    }
-            q += __shfl_xor(q, 16);
-            q += __shfl_xor(q, 32);
-            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = q;
-        }
-        __syncthreads();
-        if (threadIdx.x < BN) {
-            const int n = blockIdx.y * BN + threadIdx.x;
-            if (n < g.Ncols) {
-                float t = 0.f;
-                for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
-                if (sums.acc) {
-                    const double mu = tile_mean[threadIdx.x], nr = (double)rows;
-                    acc_add(sums.acc, 0, (int)blockIdx.x, g.Ncols, n, mu * nr);
-                    acc_add(sums.acc, 1, (int)blockIdx.x, g.Ncols, n, (double)t + nr * mu * mu);
-                } else {
-                    sums.p0[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
-                    sums.p1[(long)blockIdx.x * g.Ncols + n] = t;
-                }
-            }
-        }
+        __shared__ float red[WM][3][BN];
+        const auto valid = [&](int x, int i) { return m_base + x * 16 + gi * 4 + i < M; };
+        const auto store = [&](int t, float n, float mu, float m2) {
+            if (blockIdx.y * BN + t < g.Ncols)
+                tile_moments_store(sums, (int)blockIdx.x, g.Ncols, blockIdx.y * BN + t, n, mu, m2);
+        };
+        if ((int)blockIdx.x * BM + BM <= M) tile_moments<TM, TN, WM, BN, true>(acc, wm, wn, valid, red, store);
+        else tile_moments<TM, TN, WM, BN, false>(acc, wm, wn, valid, red, store);
     }
 }
 
@@ -398,60 +348,13 @@ __global__ __launch_bounds__(256) void conv_lds_f32(const float* __restrict__ sr
             }
     }
     if (STATS) {
-        __shared__ float red[WM][BN];
-        __shared__ float tile_mean[BN];
-        const int rows = min(BM, M - m0);
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            float sacc = 0.f;
-#pragma unroll
-            for (int x = 0; x < TM; ++x)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (m_base + x * 16 + gi * 4 + i < M) sacc += acc[x][y][i];
-            sacc += __shfl_xor(sacc, 16);
-            sacc += __shfl_xor(sacc, 32);
-            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = sacc;
-        }
-        __syncthreads();
-        if (threadIdx.x < BN) {
-            float t = 0.f;
-            for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
-            tile_mean[threadIdx.x] = t / (float)rows;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            const float mu = tile_mean[wn * TN * 16 + y * 16 + li];
-            float q = 0.f;
-#pragma unroll
-            for (int x = 0; x < TM; ++x)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (m_base + x * 16 + gi * 4 + i < M) {
-                        const float dv = acc[x][y][i] - mu;
-                        q += dv * dv;
-                    }
-            q += __shfl_xor(q, 16);
-            q += __shfl_xor(q, 32);
-            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = q;
-        }
-        __syncthreads();
-        if (threadIdx.x < BN) {
-            const int n = n0 + threadIdx.x;
-            if (n < g.Ncols) {
-                float t = 0.f;
-                for (int w = 0; w < WM; ++w) t += red[w][threadIdx.x];
-                if (sums.acc) {
-                    const double mu = tile_mean[threadIdx.x], nr = (double)rows;
-                    acc_add(sums.acc, 0, (int)blockIdx.x, g.Ncols, n, mu * nr);
-                    acc_add(sums.acc, 1, (int)blockIdx.x, g.Ncols, n, (double)t + nr * mu * mu);
-                } else {
-                    sums.p0[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
-                    sums.p1[(long)blockIdx.x * g.Ncols + n] = t;
-                }
-            }
-        }
+        __shared__ float red[WM][3][BN];
+        const auto valid = [&](int x, int i) { return m_base + x * 16 + gi * 4 + i < M; };
+        const auto store = [&](int t, float n, float mu, float m2) {
+            if (n0 + t < g.Ncols) tile_moments_store(sums, (int)blockIdx.x, g.Ncols, n0 + t, n, mu, m2);
+        };
+        if (m0 + BM <= M) tile_moments<TM, TN, WM, BN, true>(acc, wm, wn, valid, red, store);
+        else tile_moments<TM, TN, WM, BN, false>(acc, wm, wn, valid, red, store);
     }
 }
 
@@ -744,58 +647,14 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
             }
         }
     }
-    if (MODE == CONV_FWD && STATS) {
-        __shared__ float red[WM][BN];
-        __shared__ float tile_mean[BN];
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            float sacc = 0.f;
-#pragma unroll
-            for (int x = 0; x < TM; ++x)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) sacc += acc[x][y][i];
-            sacc += __shfl_xor(sacc, 16);
-            sacc += __shfl_xor(sacc, 32);
-            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = sacc;
-        }
-        __syncthreads();
-        if (threadIdx.x < BN) {
-            float tt = 0.f;
-            for (int w = 0; w < WM; ++w) tt += red[w][threadIdx.x];
-            tile_mean[threadIdx.x] = tt / (float)npix;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-            const float mu = tile_mean[wn * TN * 16 + y * 16 + li];
-            float qs = 0.f;
-#pragma unroll
-            for (int x = 0; x < TM; ++x)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float dv = acc[x][y][i] - mu;
-                    qs += dv * dv;
-                }
-            qs += __shfl_xor(qs, 16);
-            qs += __shfl_xor(qs, 32);
-            if (gi == 0) red[wm][wn * TN * 16 + y * 16 + li] = qs;
-        }
-        __syncthreads();
-        if (threadIdx.x < BN) {
-            const int n = n0 + threadIdx.x;
-            if (n < g.Ncols) {
-                float tt = 0.f;
-                for (int w = 0; w < WM; ++w) tt += red[w][threadIdx.x];
-                if (sums.acc) {
-                    const double mu = tile_mean[threadIdx.x], nr = (double)npix;
-                    acc_add(sums.acc, 0, (int)blockIdx.x, g.Ncols, n, mu * nr);
-                    acc_add(sums.acc, 1, (int)blockIdx.x, g.Ncols, n, (double)tt + nr * mu * mu);
-                } else {
-                    sums.p0[(long)blockIdx.x * g.Ncols + n] = tile_mean[threadIdx.x];
-                    sums.p1[(long)blockIdx.x * g.Ncols + n] = tt;
-                }
-            }
-        }
+    if constexpr (MODE == CONV_FWD && STATS) {
+        // (every pixel of a tile lies inside the tensor)
+        __shared__ float red[WM][3][BN];
+        tile_moments<TM, TN, WM, BN, true>(
+            acc, wm, wn, [](int, int) { return true; }, red,
+            [&](int t, float n, float mu, float m2) {
+                if (n0 + t < g.Ncols) tile_moments_store(sums, (int)blockIdx.x, g.Ncols, n0 + t, n, mu, m2);
+            });
     }
 }
 
