@@ -619,7 +619,6 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
             }
         }
         __shared__ f4 bred[4][2][QPP];
-        __syncthreads();
         if (lane < QPP) {
             bred[wave][0][lane] = bs0;
             bred[wave][1][lane] = bs1;
