@@ -422,31 +422,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
 }
 
 // Tile shape of a pass: BN = 128 for wide outputs, else 64; BM = 256 (one
-// load step per barrier, two waves per SIMD) when that still gives 512
-// workgroups (1024 for BN = 64) and the source takes 32-channel load steps,
-// else 128 unless that leaves fewer than 512 workgroups.  (Measured: the 256-row tile gains
+// load step per barrier, two waves per SIMD) when that still gives `fill`
+// workgroups and the source takes 32-channel load steps, else 128 when that
+// does, else 64.  Measured with one stream (fill 512): the 256-row tile gains
 // 10-15% where two of its workgroups fill every compute unit and loses up to
-// 50% where they do not.)
-static void pick_bf16(long Mv, int Ncols, int Cs, int& bm, int& bn) {
+// 50% where they do not.  With four worker streams at once (fill 128) the
+// larger tiles win although each pass alone is slower: WRN-16-8 +11%,
+// ResNet-18 +5%, ResNet-50 +2% against fill 512 (64 and 96 are no better).
+static void pick_bf16(long Mv, int Ncols, int Cs, int fill, int& bm, int& bn) {
     bn = Ncols >= 128 ? 128 : 64;
     const long nt = (Ncols + bn - 1) / bn;
-    if (bn == 128 && Cs % 32 == 0 && ((Mv + 255) / 256) * nt >= 512) {
+    if (Cs % 32 == 0 && ((Mv + 255) / 256) * nt >= fill) {
         bm = 256;
         return;
     }
-    // 64-wide outputs of large grids (ResNet-18's first stage): 256 x 64
-    // tiles, a step of 16 MFMAs per wave (measured +1.1% on ResNet-18 with
-    // four streams, though a single pass alone is no faster)
-    if (bn == 64 && Cs % 32 == 0 && ((Mv + 255) / 256) * nt >= 1024) {
-        bm = 256;
-        return;
-    }
-    bm = ((Mv + 127) / 128) * nt >= 512 ? 128 : 64;
+    bm = ((Mv + 127) / 128) * nt >= fill ? 128 : 64;
 }
 
 int conv_bf16_tile_rows(const ConvGeom& g) {
     int bm, bn;
-    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, g.Cs, bm, bn);
+    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, g.Cs, g.fill, bm, bn);
     return bm;
 }
 
@@ -505,7 +500,7 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
     if (!conv_bf16_supported(mode, g)) return hipErrorInvalidValue;
     if (res && (mode != CONV_FWD || accumulate)) return hipErrorInvalidValue;
     int bm, bn;
-    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, g.Cs, bm, bn);
+    pick_bf16((long)g.Nb * g.Ho * g.Wo, g.Ncols, g.Cs, g.fill, bm, bn);
     BfPass ps{};
     ps.Hd = g.Ho;
     ps.Wd = g.Wo;
@@ -549,7 +544,7 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
             q.offh = a + g.pad;
             q.offw = b + g.pad;
             int qbm, qbn;
-            pick_bf16((long)g.Nb * q.Hv * q.Wv, g.Ncols, g.Cs, qbm, qbn);
+            pick_bf16((long)g.Nb * q.Hv * q.Wv, g.Ncols, g.Cs, g.fill, qbm, qbn);
             const hipError_t e = run_bf16_pass(src, B, nullptr, Y, nullptr, g, q, accumulate, nullptr, qbm, qbn, st);
             if (e != hipSuccess) return e;
         }

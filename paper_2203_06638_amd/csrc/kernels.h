@@ -21,6 +21,10 @@ struct ConvGeom {
     int Nb, Hs, Ws, Cs;   // source activation (NHWC)
     int Ho, Wo, Ncols;    // output grid and channels (NHWC)
     int R, S, stride, pad;
+    // bf16 passes: the workgroups a pass aims for (the larger tiles are taken
+    // while they still give this many); with several worker streams running
+    // at once each pass needs only its share of the chip
+    int fill = 512;
 };
 
 enum ConvMode { CONV_FWD = 0, CONV_DGRAD = 1 };

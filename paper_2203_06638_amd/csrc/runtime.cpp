@@ -122,6 +122,9 @@ struct Model {
     std::vector<char> gstored;    // gradient at the layer output materialised (when the backward reaches it)
     std::vector<int> gbuf;        // the layer whose gradient buffer holds it
     std::vector<int> stats_from;  // BN: conv whose epilogue computes its statistics, or -1
+    // workgroups a bf16 conv pass aims for: the chip's share of one of the
+    // K * P worker streams that run at once, at least a quarter of 512
+    int conv_fill = 512;
 };
 
 int ceil4(int c) { return (c + 3) / 4 * 4; }
@@ -790,6 +793,7 @@ int run_forward(lpp_ctx* c, Worker& w) {
         switch (G.kind) {
         case G_CONV: {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride, Y.L.pad};
+            g.fill = M.conv_fill;
             const float* bias = Y.L.bias ? w.v + Y.poff + Y.wcount : nullptr;
             // a folded BN + ReLU: read the BN's input, normalised while staged
             lpp::BnFwd ib{};
@@ -1028,6 +1032,7 @@ int run_backward(lpp_ctx* c, Worker& w, int partition) {
             if (dx0) {
                 lpp::ConvGeom g{N, Y.out.h, Y.out.w, Y.L.cout, Y.in0.h, Y.in0.w, Y.L.cin, Y.L.k, Y.L.k, Y.L.stride,
                                 Y.L.pad};
+                g.fill = M.conv_fill;
                 if (bf)
                     LAUNCH("conv_dgrad", 2.0 * Y.macs, st,
                            lpp::launch_conv_bf16(lpp::CONV_DGRAD, (const uint16_t*)dy, (const uint16_t*)c->wdg(w, Y),
@@ -1287,6 +1292,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
     if (rc) return rc;
     c->K = K;
     c->P = P;
+    c->M.conv_fill = std::max(128, 512 / (K * std::max(P, 1)));
     c->mode = opt ? opt->mode : LPP_SEQUENTIAL;
     c->fixed_order = c->mode == LPP_SEQUENTIAL;
     if (c->mode != LPP_SEQUENTIAL && c->mode != LPP_ASYNC) return fail(LPP_EINVAL, "unknown mode");
@@ -1363,6 +1369,7 @@ int lpp_init(const lpp_model_desc* desc, int K, int P, const lpp_options* opt, l
         if (Y.L.op == LPP_CONV && !Y.pw) {
             lpp::ConvGeom g{N, Y.in0.h, Y.in0.w, Y.cin_p, Y.out.h, Y.out.w, Y.L.cout, Y.L.k, Y.L.k, Y.L.stride,
                             Y.L.pad};
+            g.fill = M.conv_fill;
             const int tr = M.dt == lpp::DT_BF16 ? lpp::conv_bf16_tile_rows(g) : lpp::conv_tile_rows(g);
             const long tiles = (rows_out + tr - 1) / tr;
             ps = std::max<long>(ps, tiles * Y.L.cout);
