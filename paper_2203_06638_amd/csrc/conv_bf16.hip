@@ -38,6 +38,7 @@
 // a fixed order; nothing here uses atomics except the batch-norm sums of the
 // forward epilogue in async mode (bnacc.h).
 #include <algorithm>
+#include <type_traits>
 
 #include "act.h"
 #include "bnacc.h"
@@ -695,54 +696,64 @@ __global__ __launch_bounds__(256) void wgrad_bf16_k(const bf16* __restrict__ dY,
         }
 }
 
-// Weight gradient on 128 x 128 tiles with both operands loaded straight into
-// LDS as they lie in memory (pixel-major: a K-step is 32 pixel rows of 128
-// output channels for A = dY, of 128 columns (tap, channel) for B = X at that
-// tap) and read as MFMA fragments by the LDS transpose read: within each
-// 16-lane group, lane j receives element j % 4 of the 8-byte reads of lanes
-// j / 4 + 4k (k = 0..3).  So when lane s reads the four channels c0 + 4 (s %
-// 4) .. + 3 of pixel row p0 + s / 4, lane j receives channel c0 + j at pixels
-// p0 .. p0 + 3: half of a fragment (8 consecutive pixels of one row of A or
-// B), the other half from rows p0 + 4 .. p0 + 7.  The 16-byte chunks of a row
-// are XOR-swizzled in pairs by wg_swz(row), so the 8 rows that a half-wave's
-// reads touch hit 8 different chunk pairs (all 64 banks).  The operand loads
-// run through the same NS-buffer pipeline as the forward kernel's.
-__device__ __forceinline__ int wg_swz(int row) { return (row & 3) | (((row >> 3) & 1) << 2); }
-// physical chunk (0..15) of logical chunk c in pixel row `row`, and back
-__device__ __forceinline__ int wg_chunk(int c, int row) { return (((c >> 1) ^ wg_swz(row)) << 1) | (c & 1); }
+// Weight gradient on BM x 128 tiles (BM = 128 or 64 output channels) with
+// both operands loaded straight into LDS as they lie in memory (pixel-major:
+// a K-step is 32 pixel rows of BM output channels for A = dY and of 128
+// columns (tap, channel) for B = X at that tap) and read as MFMA fragments by
+// the LDS transpose read: within each 16-lane group, lane j receives element
+// j % 4 of the 8-byte reads of lanes j / 4 + 4k (k = 0..3).  So when lane s
+// reads the four channels c0 + 4 (s % 4) .. + 3 of pixel row p0 + s / 4, lane
+// j receives channel c0 + j at pixels p0 .. p0 + 3: half of a fragment (8
+// consecutive pixels of one row of A or B), the other half from rows p0 + 4
+// .. p0 + 7.  The 16-byte chunks of a row are XOR-swizzled in pairs by row,
+// so that the 8 rows a half-wave's reads touch (p0 .. p0 + 3 and p0 + 8 ..
+// p0 + 11) hit all 64 banks once: with 16 chunks a row the pair index is
+// XORed with row bits 0, 1 and 3; with 8 (128-byte rows, two rows a bank
+// cycle) with bits 1 and 3.  The operand loads run through the same NS-buffer
+// pipeline as the forward kernel's.
+template <int W>   // chunks (8 channels) per pixel row
+__device__ __forceinline__ int wg_chunk(int c, int row) {
+    const int f = W == 16 ? ((row & 3) | (((row >> 3) & 1) << 2)) : (((row >> 1) & 1) | (((row >> 3) & 1) << 1));
+    return (((c >> 1) ^ f) << 1) | (c & 1);
+}
 
 typedef short s4v __attribute__((ext_vector_type(4)));
 typedef short s8v __attribute__((ext_vector_type(8)));
 
-template <int NS>
+template <int BM, int NS>
 __global__ __launch_bounds__(256) void wgrad_tr_bf16_k(const bf16* __restrict__ dY, const bf16* __restrict__ X,
                                                        float* __restrict__ part, WgB g) {
-    constexpr int TM = 4, TN = 4;                 // 16x16 blocks per wave; waves 2 x 2
-    constexpr int RW = 128;                       // bf16 per pixel row of one operand
-    constexpr int STEP = 2 * 32 * RW;             // one K-step: A rows, then B rows
+    static_assert(BM == 128 || BM == 64, "output-channel tile");
+    constexpr int TM = BM / 32, TN = 4;           // 16x16 blocks per wave; waves 2 x 2
+    constexpr int WA = BM / 8, WB = 16;           // chunks per pixel row of A, of B
+    constexpr int UA = BM / 64;                   // A loads per thread per K-step
+    constexpr int SA = 32 * BM, STEP = SA + 32 * 128;
     __shared__ __attribute__((aligned(16))) bf16 lds[NS * STEP];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave & 1, wn = wave >> 1;
     const int n0 = blockIdx.x * 128;              // first column
-    const int m0 = blockIdx.y * 128;              // first output channel
+    const int m0 = blockIdx.y * BM;               // first output channel
     const long p_lo = (long)blockIdx.z * g.pps;
     const long p_hi = min(g.P, p_lo + g.pps);
     const int nk = (int)((p_hi - p_lo + 31) / 32);
     const __amdgpu_buffer_rsrc_t ars = bf_rsrc(dY, g.P * g.Cout * 2);
     const __amdgpu_buffer_rsrc_t brs = bf_rsrc(X, (long)g.Nb * g.Hi * g.Wi * g.Cs * 2);
 
-    // this thread's two load slots per operand: LDS row (wave * 2 + u) * 4 +
-    // lane / 16 of the K-step, physical chunk lane % 16, whose logical chunk
-    // (8 channels) is what it loads
-    int rowu[2], a_off[2], b_r[2], b_s[2], b_c[2];
+    // load slots: wave-instruction u fills 1 KB of LDS, 64 / W rows of W
+    // chunks; lane % W is the physical chunk, whose logical chunk (8
+    // channels) is what the lane loads
+    int arow[UA], a_off[UA], brow[2], b_r[2], b_s[2], b_c[2];
     bool b_ok[2];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        rowu[u] = (wave * 2 + u) * 4 + (lane >> 4);
-        const int c = wg_chunk(lane & 15, rowu[u]);
-        const int m = m0 + c * 8;
+    for (int u = 0; u < UA; ++u) {
+        arow[u] = (wave * UA + u) * (64 / WA) + lane / WA;
+        const int m = m0 + wg_chunk<WA>(lane % WA, arow[u]) * 8;
         a_off[u] = m < g.Cout ? m : -1;
-        const int col = n0 + c * 8;
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        brow[u] = (wave * 2 + u) * 4 + (lane >> 4);
+        const int col = n0 + wg_chunk<WB>(lane & 15, brow[u]) * 8;
         b_ok[u] = col < g.Ktot;
         const int tap = b_ok[u] ? col / g.Cs : 0;
         b_c[u] = col - tap * g.Cs;
@@ -751,38 +762,43 @@ __global__ __launch_bounds__(256) void wgrad_tr_bf16_k(const bf16* __restrict__ 
     }
     auto issue = [&](int buf, int kk) {
         bf16* As = lds + buf * STEP;
-        bf16* Bs = As + 32 * RW;
+        bf16* Bs = As + SA;
+        const long pk = p_lo + (long)kk * 32;
+#pragma unroll
+        for (int u = 0; u < UA; ++u) {
+            const long p = pk + arow[u];
+            const bool ok = p < p_hi && a_off[u] >= 0;
+            bf_dma16(ars, As + (wave * UA + u) * 512, ok ? (unsigned)(p * g.Cout + a_off[u]) * 2u : 0x80000000u);
+        }
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            const long p = p_lo + (long)kk * 32 + rowu[u];
+            const long p = pk + brow[u];
             const bool pv = p < p_hi;
             const unsigned pp = pv ? (unsigned)p : 0u;
-            bf_dma16(ars, As + (wave * 2 + u) * 4 * RW,
-                     pv && a_off[u] >= 0 ? (unsigned)((long)pp * g.Cout + a_off[u]) * 2u : 0x80000000u);
             const unsigned t = bf_div(pp, g.mWo);
             const int ow = (int)(pp - t * (unsigned)g.Wo);
             const unsigned img = bf_div(t, g.mHo);
             const int oh = (int)(t - img * (unsigned)g.Ho);
             const int hh = oh * g.stride - g.pad + b_r[u], ww = ow * g.stride - g.pad + b_s[u];
             const bool ok = pv && b_ok[u] && (unsigned)hh < (unsigned)g.Hi && (unsigned)ww < (unsigned)g.Wi;
-            bf_dma16(brs, Bs + (wave * 2 + u) * 4 * RW,
+            bf_dma16(brs, Bs + (wave * 2 + u) * 512,
                      ok ? (unsigned)((((long)img * g.Hi + hh) * g.Wi + ww) * g.Cs + b_c[u]) * 2u : 0x80000000u);
         }
     };
-    // fragment half h of the 16-row block at channel (or column) c16 of a
-    // K-step's operand: this lane's read address
+    // the 16-row block at channel (or column) c16 of an operand with W chunks
+    // a row: this lane's two transposed reads
     const int fs = lane & 15, fg = lane >> 4;
-    auto frag_addr = [&](const bf16* base, int c16, int h) {
-        const int row = 8 * fg + 4 * h + (fs >> 2);
-        const int ch = c16 + 4 * (fs & 3);
-        return base + row * RW + wg_chunk(ch >> 3, row) * 8 + (ch & 7);
-    };
-    auto frag = [&](const bf16* base, int c16) {
-        const s4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s4v*)frag_addr(base, c16, 0));
-        const s4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s4v*)frag_addr(base, c16, 1));
-        const s8v v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    auto frag = [&](const bf16* base, int c16, auto w) {
+        constexpr int W = decltype(w)::value;
+        s4v h[2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int row = 8 * fg + 4 * k + (fs >> 2);
+            const int ch = c16 + 4 * (fs & 3);
+            h[k] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4v*)(
+                base + row * (8 * W) + wg_chunk<W>(ch >> 3, row) * 8 + (ch & 7)));
+        }
+        const s8v v = __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7);
         return __builtin_bit_cast(bf8, v);
     };
 
@@ -791,7 +807,7 @@ __global__ __launch_bounds__(256) void wgrad_tr_bf16_k(const bf16* __restrict__ 
     for (int x = 0; x < TM; ++x)
 #pragma unroll
         for (int y = 0; y < TN; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
-    constexpr int LPS = 4;                        // loads per K-step per thread
+    constexpr int LPS = UA + 2;                   // loads per K-step per thread
 #pragma unroll
     for (int kk = 0; kk < NS - 1; ++kk)
         if (kk < nk) issue(kk, kk);
@@ -800,12 +816,12 @@ __global__ __launch_bounds__(256) void wgrad_tr_bf16_k(const bf16* __restrict__ 
         bf_wait_steps<LPS, NS>(min(NS - 2, nk - 1 - kk));
         asm volatile("s_barrier" ::: "memory");
         const bf16* As = lds + cur * STEP;
-        const bf16* Bs = As + 32 * RW;
+        const bf16* Bs = As + SA;
         bf8 a[TM], b[TN];
 #pragma unroll
-        for (int x = 0; x < TM; ++x) a[x] = frag(As, (wm * TM + x) * 16);
+        for (int x = 0; x < TM; ++x) a[x] = frag(As, (wm * TM + x) * 16, std::integral_constant<int, WA>{});
 #pragma unroll
-        for (int y = 0; y < TN; ++y) b[y] = frag(Bs, (wn * TN + y) * 16);
+        for (int y = 0; y < TN; ++y) b[y] = frag(Bs, (wn * TN + y) * 16, std::integral_constant<int, WB>{});
         if (kk + NS - 1 < nk) issue(nxt, kk + NS - 1);
 #pragma unroll
         for (int x = 0; x < TM; ++x)
@@ -865,15 +881,15 @@ hipError_t launch_conv_wgrad_bf16(const bf16* dY, const bf16* X, float* part, in
     if (!bf_div_exact(P, Wo) || !bf_div_exact(P / Wo, Ho)) return hipErrorInvalidValue;
     const WgB a{Nb, Hi, Wi, Cin_p, Ho, Wo, Cout, S, stride, pad, R * S * Cin_p, P, p.pix_per_split,
                 bf_magic((unsigned)Wo), bf_magic((unsigned)Ho)};
-    if (p.tm == 128 && p.tn == 128) {
-        // both operands' byte offsets must fit the 32-bit buffer offsets
-        if (P * Cout * 2 < 0x7fffffffL && (long)Nb * Hi * Wi * Cin_p * 2 < 0x7fffffffL) {
-            dim3 grid((unsigned)((a.Ktot + 127) / 128), (unsigned)((Cout + 127) / 128), (unsigned)p.splits);
-            launch((wgrad_tr_bf16_k<4>), grid, dim3(256), 0, st, dY, X, part, a);
-            return hipGetLastError();
-        }
-        return launch_wg_bf16<128, 128>(dY, X, part, a, p.splits, st);
+    // 128-column tiles: operands through LDS as they lie, when both
+    // tensors' byte offsets fit the 32-bit buffer offsets
+    if (p.tn == 128 && P * Cout * 2 < 0x7fffffffL && (long)Nb * Hi * Wi * Cin_p * 2 < 0x7fffffffL) {
+        dim3 grid((unsigned)((a.Ktot + 127) / 128), (unsigned)((Cout + p.tm - 1) / p.tm), (unsigned)p.splits);
+        if (p.tm == 128) launch((wgrad_tr_bf16_k<128, 4>), grid, dim3(256), 0, st, dY, X, part, a);
+        else launch((wgrad_tr_bf16_k<64, 4>), grid, dim3(256), 0, st, dY, X, part, a);
+        return hipGetLastError();
     }
+    if (p.tm == 128 && p.tn == 128) return launch_wg_bf16<128, 128>(dY, X, part, a, p.splits, st);
     if (p.tm == 128) return launch_wg_bf16<128, 64>(dY, X, part, a, p.splits, st);
     if (p.tn == 128) return launch_wg_bf16<64, 128>(dY, X, part, a, p.splits, st);
     return launch_wg_bf16<64, 64>(dY, X, part, a, p.splits, st);
