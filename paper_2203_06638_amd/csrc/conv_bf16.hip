@@ -80,6 +80,10 @@ struct BfPass {
     unsigned mWv, mHv;       // bf_magic(Wv), bf_magic(Hv)
 };
 
+// Up to four passes of one launch (the parity classes of a stride-2 data
+// gradient), pass blockIdx.z; a pass's workgroups beyond its grid exit.
+struct BfPasses { BfPass p[4]; };
+
 // Output channels in the epilogue: BM x BN tile, bf16, pitch BN + 8.
 // FASTK (Cs % 32 == 0): a load step is 32 channels of one tap, and the tap and
 // channel counters advance incrementally (no divisions in the loop);
@@ -126,7 +130,7 @@ __device__ __forceinline__ void bf_wait_steps(int ahead) {
 template <int BM, int BN, bool STATS, bool FASTK, int KH, bool DMA, int NS = 2>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ? 2 : 1, 8))) void conv_bf16_k(const bf16* __restrict__ src, const bf16* __restrict__ B,
                                                    const float* __restrict__ bias, bf16* __restrict__ Y,
-                                                   const bf16* __restrict__ res, ConvGeom g, BfPass ps, int accumulate,
+                                                   const bf16* __restrict__ res, ConvGeom g, BfPasses pp, int accumulate,
                                                    BnSums sums) {
     static_assert(!DMA || FASTK, "DMA operand loads need 32-channel load steps");
     static_assert(NS == 2 || DMA, "deeper pipelines use DMA operand loads");
@@ -138,10 +142,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
     constexpr int OP = BN + 8;
     constexpr int LDSN = BM * OP > NS * STAGE ? BM * OP : NS * STAGE;   // the epilogue tile reuses the space
     __shared__ __attribute__((aligned(16))) bf16 lds[LDSN];
+    const BfPass ps = blockIdx.z == 0 ? pp.p[0] : (blockIdx.z == 1 ? pp.p[1] : (blockIdx.z == 2 ? pp.p[2] : pp.p[3]));
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave & 1, wn = wave >> 1;
     const long Mv = (long)g.Nb * ps.Hv * ps.Wv;
     const long m0 = (long)blockIdx.x * BM;
+    if (m0 >= Mv) return;                         // (the whole workgroup)
     const int n0 = blockIdx.y * BN;
     const int j = tid & 3, rr = tid >> 2;
     const int RS = g.R * g.S;
@@ -454,11 +460,12 @@ bool conv_bf16_supported(int mode, const ConvGeom& g) {
 
 template <int BM, int BN>
 static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const bf16* res,
-                                   const ConvGeom& g, const BfPass& ps, bool acc, const BnSums* stats,
+                                   const ConvGeom& g, const BfPasses& ps, int np, bool acc, const BnSums* stats,
                                    hipStream_t st) {
-    const long Mv = (long)g.Nb * ps.Hv * ps.Wv;
-    if (Mv == 0) return hipSuccess;
-    dim3 grid((unsigned)((Mv + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN));
+    long Mmax = 0;
+    for (int i = 0; i < np; ++i) Mmax = std::max(Mmax, (long)g.Nb * ps.p[i].Hv * ps.p[i].Wv);
+    if (Mmax == 0) return hipSuccess;
+    dim3 grid((unsigned)((Mmax + BM - 1) / BM), (unsigned)((g.Ncols + BN - 1) / BN), (unsigned)np);
     const BnSums sm = stats ? *stats : BnSums{};
     // 32-channel load steps straight into LDS, NS of them in flight; 64 x 128
     // tiles (a step of 8 MFMAs per wave) take two load steps per buffer and
@@ -477,23 +484,27 @@ static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* 
     return hipGetLastError();
 }
 
+// np passes (1, or the four parity classes of a stride-2 data gradient) in
+// one launch with tiles of bm x bn
 static hipError_t run_bf16_pass(const bf16* src, const bf16* B, const float* bias, bf16* Y, const bf16* res,
-                                const ConvGeom& g, const BfPass& ps0, bool acc, const BnSums* stats, int bm, int bn,
-                                hipStream_t st) {
-    BfPass ps = ps0;
-    const long Mv = (long)g.Nb * ps.Hv * ps.Wv;
-    if (Mv == 0) return hipSuccess;
-    // pixel indices up to Mv + BM (a tile's padding rows) divided by Wv, row indices by Hv
-    if (!bf_div_exact(Mv + 256, ps.Wv) || !bf_div_exact(Mv / (ps.Wv > 0 ? ps.Wv : 1) + 256, ps.Hv))
-        return hipErrorInvalidValue;
-    ps.mWv = bf_magic((unsigned)ps.Wv);
-    ps.mHv = bf_magic((unsigned)ps.Hv);
-    if (bm == 256 && bn == 64) return launch_bf16_pass<256, 64>(src, B, bias, Y, res, g, ps, acc, stats, st);
-    if (bm == 256) return launch_bf16_pass<256, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
-    if (bm == 128 && bn == 128) return launch_bf16_pass<128, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
-    if (bm == 128) return launch_bf16_pass<128, 64>(src, B, bias, Y, res, g, ps, acc, stats, st);
-    if (bn == 128) return launch_bf16_pass<64, 128>(src, B, bias, Y, res, g, ps, acc, stats, st);
-    return launch_bf16_pass<64, 64>(src, B, bias, Y, res, g, ps, acc, stats, st);
+                                const ConvGeom& g, const BfPasses& ps0, int np, bool acc, const BnSums* stats, int bm,
+                                int bn, hipStream_t st) {
+    BfPasses ps = ps0;
+    for (int i = 0; i < np; ++i) {
+        BfPass& q = ps.p[i];
+        const long Mv = (long)g.Nb * q.Hv * q.Wv;
+        if (Mv == 0) continue;                    // (its workgroups exit at once)
+        // pixel indices up to Mv + BM (a tile's padding rows) divided by Wv, row indices by Hv
+        if (!bf_div_exact(Mv + 256, q.Wv) || !bf_div_exact(Mv / q.Wv + 256, q.Hv)) return hipErrorInvalidValue;
+        q.mWv = bf_magic((unsigned)q.Wv);
+        q.mHv = bf_magic((unsigned)q.Hv);
+    }
+    if (bm == 256 && bn == 64) return launch_bf16_pass<256, 64>(src, B, bias, Y, res, g, ps, np, acc, stats, st);
+    if (bm == 256) return launch_bf16_pass<256, 128>(src, B, bias, Y, res, g, ps, np, acc, stats, st);
+    if (bm == 128 && bn == 128) return launch_bf16_pass<128, 128>(src, B, bias, Y, res, g, ps, np, acc, stats, st);
+    if (bm == 128) return launch_bf16_pass<128, 64>(src, B, bias, Y, res, g, ps, np, acc, stats, st);
+    if (bn == 128) return launch_bf16_pass<64, 128>(src, B, bias, Y, res, g, ps, np, acc, stats, st);
+    return launch_bf16_pass<64, 64>(src, B, bias, Y, res, g, ps, np, acc, stats, st);
 }
 
 hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const float* bias, bf16* Y, const ConvGeom& g,
@@ -515,7 +526,7 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
         ps.ss = g.stride;
         ps.offh = ps.offw = -g.pad;
         ps.sgn = 1;
-        return run_bf16_pass(src, B, bias, Y, res, g, ps, accumulate, stats, bm, bn, st);
+        return run_bf16_pass(src, B, bias, Y, res, g, BfPasses{{ps}}, 1, accumulate, stats, bm, bn, st);
     }
     if (stats) return hipErrorInvalidValue;
     ps.ss = 1;
@@ -525,15 +536,19 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
         ps.Wv = g.Wo;
         ps.os = 1;
         ps.offh = ps.offw = g.pad;
-        return run_bf16_pass(src, B, bias, Y, nullptr, g, ps, accumulate, nullptr, bm, bn, st);
+        return run_bf16_pass(src, B, bias, Y, nullptr, g, BfPasses{{ps}}, 1, accumulate, nullptr, bm, bn, st);
     }
-    // stride 2: one pass per parity class of the dX pixels
+    // stride 2: one pass per parity class of the dX pixels, all four in one
+    // launch, with the tile shape of the largest class
     ps.os = 2;
     ps.step = 2;
     ps.shift = 1;
+    BfPasses qs{};
+    long Mmax = 0;
     for (int a = 0; a < 2; ++a)
         for (int b = 0; b < 2; ++b) {
-            BfPass q = ps;
+            BfPass& q = qs.p[2 * a + b];
+            q = ps;
             q.oa = a;
             q.ob = b;
             q.Hv = (g.Ho - a + 1) / 2;
@@ -544,12 +559,11 @@ hipError_t launch_conv_bf16(int mode, const bf16* src, const bf16* B, const floa
             q.ns = q.s0 < g.S ? (g.S - q.s0 + 1) / 2 : 0;
             q.offh = a + g.pad;
             q.offw = b + g.pad;
-            int qbm, qbn;
-            pick_bf16((long)g.Nb * q.Hv * q.Wv, g.Ncols, g.Cs, g.fill, qbm, qbn);
-            const hipError_t e = run_bf16_pass(src, B, nullptr, Y, nullptr, g, q, accumulate, nullptr, qbm, qbn, st);
-            if (e != hipSuccess) return e;
+            Mmax = std::max(Mmax, (long)g.Nb * q.Hv * q.Wv);
         }
-    return hipSuccess;
+    int qbm, qbn;
+    pick_bf16(Mmax, g.Ncols, g.Cs, g.fill, qbm, qbn);
+    return run_bf16_pass(src, B, nullptr, Y, nullptr, g, qs, 4, accumulate, nullptr, qbm, qbn, st);
 }
 
 // ------------------------------------------------------------------------
