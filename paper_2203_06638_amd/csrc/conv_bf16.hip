@@ -141,7 +141,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
     constexpr int STAGE = KH * HALF;
     constexpr int OP = BN + 8;
     constexpr int LDSN = BM * OP > NS * STAGE ? BM * OP : NS * STAGE;   // the epilogue tile reuses the space
-    __shared__ __attribute__((aligned(16))) bf16 lds[LDSN];
+    // the statistics' merge area (2 x 3 x BN floats) follows, in the same
+    // array: a kernel with one LDS object keeps the DMA loads' partial vmcnt
+    // waits (with a second object the compiler adds a full wait before every
+    // step's fragment reads)
+    constexpr int REDN = STATS ? 2 * 3 * BN * 2 : 0;
+    __shared__ __attribute__((aligned(16))) bf16 lds[LDSN + REDN];
     const BfPass ps = blockIdx.z == 0 ? pp.p[0] : (blockIdx.z == 1 ? pp.p[1] : (blockIdx.z == 2 ? pp.p[2] : pp.p[3]));
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave & 1, wn = wave >> 1;
@@ -406,7 +411,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(BM == 256 ?
         // per output channel of the tile: count, mean and sum of squared
         // deviations of the stored values (with a residual, the sums written
         // back into the tile)
-        __shared__ float red[2][3][BN];
+        float(&red)[2][3][BN] = *reinterpret_cast<float(*)[2][3][BN]>(lds + LDSN);
         if (res) {
             __syncthreads();
 #pragma unroll
