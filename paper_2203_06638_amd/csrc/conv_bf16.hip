@@ -739,6 +739,37 @@ __device__ __forceinline__ int wg_chunk(int c, int row) {
 typedef short s4v __attribute__((ext_vector_type(4)));
 typedef short s8v __attribute__((ext_vector_type(8)));
 
+// ds_read_b64_tr_b16 at LDS location p.  Written out because with the
+// builtin the compiler drains every DMA load in flight before each read (it
+// cannot tell the read from the loads' LDS destinations), which would empty
+// the pipeline at every step; the pipeline's own vmcnt waits and barrier
+// already order them.  The compiler does not count these reads, so the
+// caller waits for them itself (lgkm_wait) before using the results.
+__device__ __forceinline__ s4v lds_read_tr16(const bf16* p) {
+    const unsigned a = (unsigned)(uintptr_t)(const __attribute__((address_space(3))) bf16*)p;
+    s4v r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(a) : "memory");
+    return r;
+}
+// waits until this wave's LDS reads have returned; the read values are tied
+// to the wait, so that no use of them (a register copy included) moves above
+template <int N>
+__device__ __forceinline__ void lgkm_wait(s4v (&h)[N]) {
+    static_assert(N == 12 || N == 16, "fragment halves per step");
+    if constexpr (N == 16)
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(h[0]), "+v"(h[1]), "+v"(h[2]), "+v"(h[3]), "+v"(h[4]), "+v"(h[5]), "+v"(h[6]), "+v"(h[7]),
+                       "+v"(h[8]), "+v"(h[9]), "+v"(h[10]), "+v"(h[11]), "+v"(h[12]), "+v"(h[13]), "+v"(h[14]),
+                       "+v"(h[15]));
+    else
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(h[0]), "+v"(h[1]), "+v"(h[2]), "+v"(h[3]), "+v"(h[4]), "+v"(h[5]), "+v"(h[6]), "+v"(h[7]),
+                       "+v"(h[8]), "+v"(h[9]), "+v"(h[10]), "+v"(h[11]));
+}
+__device__ __forceinline__ bf8 tr_frag(s4v lo, s4v hi) {
+    return __builtin_bit_cast(bf8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
 template <int BM, int NS>
 __global__ __launch_bounds__(256) void wgrad_tr_bf16_k(const bf16* __restrict__ dY, const bf16* __restrict__ X,
                                                        float* __restrict__ part, WgB g) {
@@ -805,20 +836,16 @@ __global__ __launch_bounds__(256) void wgrad_tr_bf16_k(const bf16* __restrict__ 
         }
     };
     // the 16-row block at channel (or column) c16 of an operand with W chunks
-    // a row: this lane's two transposed reads
+    // a row: this lane's two transposed reads, into h[0] and h[1]
     const int fs = lane & 15, fg = lane >> 4;
-    auto frag = [&](const bf16* base, int c16, auto w) {
+    auto frag = [&](s4v* h, const bf16* base, int c16, auto w) {
         constexpr int W = decltype(w)::value;
-        s4v h[2];
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
             const int row = 8 * fg + 4 * k + (fs >> 2);
             const int ch = c16 + 4 * (fs & 3);
-            h[k] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4v*)(
-                base + row * (8 * W) + wg_chunk<W>(ch >> 3, row) * 8 + (ch & 7)));
+            h[k] = lds_read_tr16(base + row * (8 * W) + wg_chunk<W>(ch >> 3, row) * 8 + (ch & 7));
         }
-        const s8v v = __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7);
-        return __builtin_bit_cast(bf8, v);
     };
 
     f4 acc[TM][TN];
@@ -836,16 +863,20 @@ __global__ __launch_bounds__(256) void wgrad_tr_bf16_k(const bf16* __restrict__ 
         asm volatile("s_barrier" ::: "memory");
         const bf16* As = lds + cur * STEP;
         const bf16* Bs = As + SA;
-        bf8 a[TM], b[TN];
+        s4v h[2 * (TM + TN)];                     // A fragments' halves, then B's
 #pragma unroll
-        for (int x = 0; x < TM; ++x) a[x] = frag(As, (wm * TM + x) * 16, std::integral_constant<int, WA>{});
+        for (int x = 0; x < TM; ++x) frag(h + 2 * x, As, (wm * TM + x) * 16, std::integral_constant<int, WA>{});
 #pragma unroll
-        for (int y = 0; y < TN; ++y) b[y] = frag(Bs, (wn * TN + y) * 16, std::integral_constant<int, WB>{});
+        for (int y = 0; y < TN; ++y)
+            frag(h + 2 * (TM + y), Bs, (wn * TN + y) * 16, std::integral_constant<int, WB>{});
         if (kk + NS - 1 < nk) issue(nxt, kk + NS - 1);
+        lgkm_wait(h);
 #pragma unroll
         for (int x = 0; x < TM; ++x)
 #pragma unroll
-            for (int y = 0; y < TN; ++y) acc[x][y] = mfma_bf16(a[x], b[y], acc[x][y]);
+            for (int y = 0; y < TN; ++y)
+                acc[x][y] = mfma_bf16(tr_frag(h[2 * x], h[2 * x + 1]), tr_frag(h[2 * (TM + y)], h[2 * (TM + y) + 1]),
+                                      acc[x][y]);
         cur = cur + 1 == NS ? 0 : cur + 1;
         nxt = nxt + 1 == NS ? 0 : nxt + 1;
     }
