@@ -475,10 +475,14 @@ static hipError_t launch_bf16_pass(const bf16* src, const bf16* B, const float* 
     // 32-channel load steps straight into LDS, NS of them in flight; 64 x 128
     // tiles (a step of 8 MFMAs per wave) take two load steps per buffer and
     // barrier (measured 7-23% faster on 256- and 512-channel sources)
-    if (BM == 64 && BN == 128 && g.Cs % 64 == 0) {
-        if (stats) launch((conv_bf16_k<BM, BN, true, true, 2, true, 3>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-        else launch((conv_bf16_k<BM, BN, false, true, 2, true, 3>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
-    } else if (g.Cs % 32 == 0) {
+    if constexpr (BM == 64 && BN == 128) {
+        if (g.Cs % 64 == 0) {
+            if (stats) launch((conv_bf16_k<BM, BN, true, true, 2, true, 3>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+            else launch((conv_bf16_k<BM, BN, false, true, 2, true, 3>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
+            return hipGetLastError();
+        }
+    }
+    if (g.Cs % 32 == 0) {
         constexpr int NSD = BM == 256 ? 3 : 4;
         if (stats) launch((conv_bf16_k<BM, BN, true, true, 1, true, NSD>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
         else launch((conv_bf16_k<BM, BN, false, true, 1, true, NSD>), grid, dim3(256), 0, st, src, B, bias, Y, res, g, ps, (int)acc, sm);
