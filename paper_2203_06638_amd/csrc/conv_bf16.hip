@@ -744,10 +744,9 @@ typedef short s4v __attribute__((ext_vector_type(4)));
 typedef short s8v __attribute__((ext_vector_type(8)));
 
 // ds_read_b64_tr_b16 at LDS location p.  Written out because with the
-// builtin the compiler drains every DMA load in flight before each read (it
-// cannot tell the read from the loads' LDS destinations), which would empty
-// the pipeline at every step; the pipeline's own vmcnt waits and barrier
-// already order them.  The compiler does not count these reads, so the
+// builtin the compiler waits for every DMA load in flight before the reads,
+// which would empty the pipeline at every step; the pipeline's own vmcnt
+// waits and barrier already order them.  The compiler does not count these reads, so the
 // caller waits for them itself (lgkm_wait) before using the results.
 __device__ __forceinline__ s4v lds_read_tr16(const bf16* p) {
     const unsigned a = (unsigned)(uintptr_t)(const __attribute__((address_space(3))) bf16*)p;
