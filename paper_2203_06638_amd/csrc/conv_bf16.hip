@@ -736,7 +736,7 @@ __global__ __launch_bounds__(256) void wgrad_bf16_k(const bf16* __restrict__ dY,
 // pipeline as the forward kernel's.
 template <int W>   // chunks (8 channels) per pixel row
 __device__ __forceinline__ int wg_chunk(int c, int row) {
-    const int f = W == 16 ? ((row & 3) | (((row >> 3) & 1) << 2)) : (((row >> 1) & 1) | (((row >> 3) & 1) << 1));
+    const int f = W >= 16 ? ((row & 3) | (((row >> 3) & 1) << 2)) : (((row >> 1) & 1) | (((row >> 3) & 1) << 1));
     return (((c >> 1) ^ f) << 1) | (c & 1);
 }
 
@@ -758,8 +758,14 @@ __device__ __forceinline__ s4v lds_read_tr16(const bf16* p) {
 // to the wait, so that no use of them (a register copy included) moves above
 template <int N>
 __device__ __forceinline__ void lgkm_wait(s4v (&h)[N]) {
-    static_assert(N == 12 || N == 16, "fragment halves per step");
-    if constexpr (N == 16)
+    static_assert(N == 12 || N == 16 || N == 24, "fragment halves per step");
+    if constexpr (N == 24)
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(h[0]), "+v"(h[1]), "+v"(h[2]), "+v"(h[3]), "+v"(h[4]), "+v"(h[5]), "+v"(h[6]), "+v"(h[7]),
+                       "+v"(h[8]), "+v"(h[9]), "+v"(h[10]), "+v"(h[11]), "+v"(h[12]), "+v"(h[13]), "+v"(h[14]),
+                       "+v"(h[15]), "+v"(h[16]), "+v"(h[17]), "+v"(h[18]), "+v"(h[19]), "+v"(h[20]), "+v"(h[21]),
+                       "+v"(h[22]), "+v"(h[23]));
+    else if constexpr (N == 16)
         asm volatile("s_waitcnt lgkmcnt(0)"
                      : "+v"(h[0]), "+v"(h[1]), "+v"(h[2]), "+v"(h[3]), "+v"(h[4]), "+v"(h[5]), "+v"(h[6]), "+v"(h[7]),
                        "+v"(h[8]), "+v"(h[9]), "+v"(h[10]), "+v"(h[11]), "+v"(h[12]), "+v"(h[13]), "+v"(h[14]),
@@ -776,7 +782,7 @@ __device__ __forceinline__ bf8 tr_frag(s4v lo, s4v hi) {
 template <int BM, int NS>
 __global__ __launch_bounds__(256) void wgrad_tr_bf16_k(const bf16* __restrict__ dY, const bf16* __restrict__ X,
                                                        float* __restrict__ part, WgB g) {
-    static_assert(BM == 128 || BM == 64, "output-channel tile");
+    static_assert(BM == 256 || BM == 128 || BM == 64, "output-channel tile");
     constexpr int TM = BM / 32, TN = 4;           // 16x16 blocks per wave; waves 2 x 2
     constexpr int WA = BM / 8, WB = 16;           // chunks per pixel row of A, of B
     constexpr int UA = BM / 64;                   // A loads per thread per K-step
@@ -897,15 +903,19 @@ __global__ __launch_bounds__(256) void wgrad_tr_bf16_k(const bf16* __restrict__ 
         }
 }
 
-// Tiles of 128 (64 when narrower) output channels x 128 columns; about 512
-// workgroups per pass, each over at least 512 pixels.
+// Tiles of 128 (64 when narrower) output channels x 128 columns and pixel
+// splits for about 512 workgroups per pass, each over at least 512 pixels;
+// then 256-channel tiles over the same splits where those still give 256
+// workgroups (fewer, larger workgroups: half the column operand's loads per
+// MFMA, and room for the other worker streams' kernels).
 WgradPlan wgrad_plan_bf16(int Nb, int Ho, int Wo, int Cin_p, int Cout, int R, int S) {
     WgradPlan p{};
     const long M = (long)Nb * Ho * Wo;
     const int Ktot = R * S * Cin_p;
     p.tm = Cout >= 128 ? 128 : 64;
     p.tn = Ktot >= 128 ? 128 : 64;
-    const long tiles = (long)((Cout + p.tm - 1) / p.tm) * ((Ktot + p.tn - 1) / p.tn);
+    const long ktiles = (Ktot + p.tn - 1) / p.tn;
+    const long tiles = (long)((Cout + p.tm - 1) / p.tm) * ktiles;
     long splits = (512 + tiles - 1) / tiles;
     const long max_splits = (M + 511) / 512;
     if (splits > max_splits) splits = max_splits;
@@ -915,6 +925,7 @@ WgradPlan wgrad_plan_bf16(int Nb, int Ho, int Wo, int Cin_p, int Cout, int R, in
     p.pix_per_split = (int)pps;
     p.splits = (int)((M + pps - 1) / pps);
     p.part_floats = (long)p.splits * Cout * Ktot;
+    if (p.tn == 128 && Cout >= 256 && ((Cout + 255) / 256) * ktiles * p.splits >= 256) p.tm = 256;
     return p;
 }
 
@@ -938,12 +949,15 @@ hipError_t launch_conv_wgrad_bf16(const bf16* dY, const bf16* X, float* part, in
     // tensors' byte offsets fit the 32-bit buffer offsets
     if (p.tn == 128 && P * Cout * 2 < 0x7fffffffL && (long)Nb * Hi * Wi * Cin_p * 2 < 0x7fffffffL) {
         dim3 grid((unsigned)((a.Ktot + 127) / 128), (unsigned)((Cout + p.tm - 1) / p.tm), (unsigned)p.splits);
-        if (p.tm == 128) launch((wgrad_tr_bf16_k<128, 4>), grid, dim3(256), 0, st, dY, X, part, a);
+        if (p.tm == 256) launch((wgrad_tr_bf16_k<256, 3>), grid, dim3(256), 0, st, dY, X, part, a);
+        else if (p.tm == 128) launch((wgrad_tr_bf16_k<128, 4>), grid, dim3(256), 0, st, dY, X, part, a);
         else launch((wgrad_tr_bf16_k<64, 4>), grid, dim3(256), 0, st, dY, X, part, a);
         return hipGetLastError();
     }
-    if (p.tm == 128 && p.tn == 128) return launch_wg_bf16<128, 128>(dY, X, part, a, p.splits, st);
-    if (p.tm == 128) return launch_wg_bf16<128, 64>(dY, X, part, a, p.splits, st);
+    // (the register-staged kernels take 128- or 64-row tiles; the partial
+    // sums' layout does not depend on the tile)
+    if (p.tm >= 128 && p.tn == 128) return launch_wg_bf16<128, 128>(dY, X, part, a, p.splits, st);
+    if (p.tm >= 128) return launch_wg_bf16<128, 64>(dY, X, part, a, p.splits, st);
     if (p.tn == 128) return launch_wg_bf16<64, 128>(dY, X, part, a, p.splits, st);
     return launch_wg_bf16<64, 64>(dY, X, part, a, p.splits, st);
 }
