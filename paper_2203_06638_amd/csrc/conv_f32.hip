@@ -392,6 +392,13 @@ struct TileGeom { int OH, IH, IW, pad_eff, tiles_per_img; unsigned IW_inv; };
 // Variants with at most two row blocks per wave and no epilogue statistics
 // or folded input fit 128 registers without spilling: they are held to that,
 // for four waves per SIMD instead of three.
+// 16 bytes of device memory at p, through a global-address-space pointer (a
+// pointer chosen at run time between buffers would otherwise be a flat
+// address, whose loads also count with the LDS accesses)
+__device__ __forceinline__ f4 ld_global4(const float* p) {
+    return *(const __attribute__((address_space(1))) f4*)p;
+}
+
 template <int MODE, int KS, int WM, int TM, int TN, bool STATS, bool INBN>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu((TM <= 2 && !INBN && !STATS) ? 4 : 1, 8)))
 void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
@@ -453,6 +460,8 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
     const int q = tid & 3;
     const int nx = t.IH * t.IW * 4, ntot = nx + BN * RS * 4;
     const int ngroups = g.Cs >> 4;
+    // decode: the element's source quad sp (nullptr: none -- zero padding, a
+    // column past the output) and its LDS offset d (-1: past the tiles)
     auto decode = [&](int e, const float*& sp, int& d) {
         sp = nullptr;
         d = -1;
@@ -518,14 +527,24 @@ void conv_tile_f32(const float* __restrict__ src, const float* __restrict__ B,
         for (int cgp = 0; cgp < ngroups; ++cgp) {
             const int c0 = cgp * 16;
             for (int base = tid; base < ntot; base += NU * 256) {
+                // all of the batch's loads first (elements without a source
+                // load the source's first quad, a valid address, and are
+                // zeroed afterwards): with a conditional load and the fold
+                // right behind each, they would go out one at a time
                 f4 v[NU];
                 int d[NU];
+                bool z[NU];
 #pragma unroll
                 for (int u = 0; u < NU; ++u) {
                     const float* sp;
                     decode(base + u * 256, sp, d[u]);
-                    v[u] = sp ? *(const f4*)(sp + c0) : f4{0.f, 0.f, 0.f, 0.f};
-                    if (INBN && sp && base + u * 256 < nx) v[u] = fold(v[u], c0 + q * 4);
+                    z[u] = !sp;
+                    v[u] = ld_global4((sp ? sp : src + q * 4) + c0);
+                }
+#pragma unroll
+                for (int u = 0; u < NU; ++u) {
+                    if (z[u]) v[u] = f4{0.f, 0.f, 0.f, 0.f};
+                    else if (INBN && base + u * 256 < nx) v[u] = fold(v[u], c0 + q * 4);
                 }
 #pragma unroll
                 for (int u = 0; u < NU; ++u)
@@ -1252,17 +1271,34 @@ void conv_wgrad_tile_f32(const float* __restrict__ dY, const float* __restrict__
     float* Xs = lds;                         // [npix][LDW] input rows of the tile
     float* Ds = lds + npix * LDW;            // [TP][LDW] dY of the tile, 16 channels
 
-    // stage X rows and the dY tile: element e = tid + 256 u has quad tid & 3
+    // stage X rows and the dY tile: element e = tid + 256 u has quad tid & 3.
+    // All of a batch's loads are issued before any value is used: elements
+    // without a source (zero padding, past the tiles) load X's first quad of
+    // the channel block, a valid address, and are zeroed afterwards (with
+    // conditional loads and the fold right behind each, the loads would go
+    // out one round trip at a time).
     {
         const int q = tid & 3;
         const int nx = npix * 4, ntot = nx + TP * 4;
+        // the fold's scale and shift of this thread's channel quad (the same
+        // for all its elements)
+        float fsc[4] = {1.f, 1.f, 1.f, 1.f}, fsh[4] = {0.f, 0.f, 0.f, 0.f};
+        if (in_ss) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                fsc[k] = in_ss[c0 + q * 4 + k];
+                fsh[k] = in_ss[a.Cin_p + c0 + q * 4 + k];
+            }
+        }
         for (int base = tid; base < ntot; base += NU * 256) {
             f4 v[NU];
             int d[NU];
+            bool z[NU];
 #pragma unroll
             for (int u = 0; u < NU; ++u) {
                 const int e = base + u * 256;
-                const float* sp = nullptr;
+                const float* sp = X + c0 + q * 4;
+                z[u] = true;
                 d[u] = -1;
                 if (e < nx) {
                     const int pix = e >> 2;
@@ -1272,21 +1308,26 @@ void conv_wgrad_tile_f32(const float* __restrict__ dY, const float* __restrict__
                     const int iw = rem - ih * t.IW;
                     const int h = K1 ? (oh0 + ih) * ST : oh0 * ST - a.pad + ih;
                     const int w = K1 ? iw * ST : iw - a.pad;
-                    if (h >= 0 && h < a.Hi && w >= 0 && w < a.Wi)
+                    if (h >= 0 && h < a.Hi && w >= 0 && w < a.Wi) {
                         sp = X + ((long)((img0 + il) * a.Hi + h) * a.Wi + w) * a.Cin_p + c0 + q * 4;
+                        z[u] = false;
+                    }
                     d[u] = pix * LDW + q * 4;
                 } else if (e < ntot) {
                     const int p = (e - nx) >> 2;
                     sp = dY + (m0 + p) * a.Cout + co0 + q * 4;
+                    z[u] = false;
                     d[u] = (npix + p) * LDW + q * 4;
                 }
-                v[u] = sp ? *(const f4*)sp : f4{0.f, 0.f, 0.f, 0.f};
-                // X read through a folded BN + ReLU (padding stays zero)
-                if (in_ss && sp && e < nx) {
-                    const int c = c0 + q * 4;
+                v[u] = ld_global4(sp);
+            }
 #pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        v[u][k] = fmaxf(__builtin_fmaf(v[u][k], in_ss[c + k], in_ss[a.Cin_p + c + k]), 0.f);
+            for (int u = 0; u < NU; ++u) {
+                if (z[u]) v[u] = f4{0.f, 0.f, 0.f, 0.f};
+                // X read through a folded BN + ReLU (padding stays zero)
+                else if (in_ss && base + u * 256 < nx) {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) v[u][k] = fmaxf(__builtin_fmaf(v[u][k], fsc[k], fsh[k]), 0.f);
                 }
             }
 #pragma unroll
