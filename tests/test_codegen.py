@@ -10,6 +10,11 @@ avoid both; these tests compile the source to assembly and check that the main
 loops carry no such wait, and that the transpose reads issued as inline asm
 (which the compiler does not count) leave their destination registers alone
 until the kernel's own lgkmcnt wait.
+
+The fp32 weight-gradient tile kernel stages its tiles in batches of eight
+loads per thread; with a conditional load and the BN fold right behind each,
+the compiler sent them out one round trip at a time.  The kernel issues a
+batch's loads first; a test checks that every instance still does.
 """
 import os
 import re
@@ -23,14 +28,18 @@ from paper_2203_06638_amd import build as B
 pytestmark = pytest.mark.skipif(shutil.which("hipcc") is None, reason="needs hipcc")
 
 
-@pytest.fixture(scope="module")
-def asm(tmp_path_factory):
-    out = str(tmp_path_factory.mktemp("asm") / "conv_bf16.s")
-    src = os.path.join(B.CSRC, "conv_bf16.hip")
+def compile_asm(tmp_path_factory, name):
+    out = str(tmp_path_factory.mktemp("asm") / (name + ".s"))
+    src = os.path.join(B.CSRC, name + ".hip")
     r = subprocess.run(["hipcc"] + B.COMMON + ["--cuda-device-only", "-S", src, "-o", out],
                        capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     return open(out).read()
+
+
+@pytest.fixture(scope="module")
+def asm(tmp_path_factory):
+    return compile_asm(tmp_path_factory, "conv_bf16")
 
 
 def functions(s, prefix):
@@ -110,3 +119,17 @@ def test_wgrad_transpose_reads(asm):
                 continue
             assert not (regs(l.split(" ", 1)[1]) & inflight), (name, l)
         assert waited, name
+
+
+def test_fp32_wgrad_staging_loads_in_flight(tmp_path_factory):
+    fns = functions(compile_asm(tmp_path_factory, "conv_f32"), "_ZN3lpp19conv_wgrad_tile_f32")
+    assert len(fns) >= 12
+    for name, body in fns.items():
+        # loads (G) and full vmcnt waits (V) in program order
+        seq = "".join("G" if l.startswith(("global_load", "flat_load", "buffer_load")) else "V" for l in body
+                      if l.startswith(("global_load", "flat_load", "buffer_load"))
+                      or (l.startswith("s_waitcnt") and "vmcnt(0)" in l))
+        # the first staging batch: eight loads before the first full wait,
+        # and nowhere a run of single loads each followed by one
+        assert seq.find("V") >= 8, (name, seq[:40])
+        assert not re.search(r"(?:G{1,3}V){4,}", seq), (name, seq[:80])
